@@ -1,0 +1,111 @@
+"""Pins of the oracle's expert-cache policy: a hand-worked trace, invariants
+and a lower bound from an exhaustive search of eviction choices."""
+import functools
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle.stmoe_oracle import CacheSim
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def test_hand_worked_trace():
+    with open(os.path.join(GOLD, "cache_trace.json")) as f:
+        g = json.load(f)
+    c = CacheSim(g["L"], g["E"], g["C"], g["warm"])
+    for st in g["steps"]:
+        if st["op"] == "A":
+            _, demand, overflow = c.acquire(0, st["set"], st["stamp"])
+            assert [list(d) for d in demand] == st["demand"]
+            assert overflow == st["overflow"]
+        else:
+            copies = c.prefetch(0, st["set"], st["stamp"])
+            assert [list(d) for d in copies] == st["copies"]
+    assert c.slot == g["final_slots"]
+    n = c.n
+    got = dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
+               useful=n.useful, wasted=n.wasted)
+    assert got == g["counts"]
+
+
+def _random_sets(rng, n, E, K):
+    return [sorted(rng.choice(E, size=K, replace=False).tolist()) for _ in range(n)]
+
+
+@pytest.mark.parametrize("E,C,K", [(8, 3, 2), (16, 4, 5), (6, 6, 2)])
+def test_invariants(E, C, K):
+    rng = np.random.default_rng(E + C)
+    L = 3
+    warm = [list(range(C)) for _ in range(L)]
+    c = CacheSim(L, E, C, warm)
+    tot = 0
+    stamp = 0
+    for t in range(50):
+        for l in range(L):
+            stamp += 1
+            U = _random_sets(rng, 1, E, K)[0]
+            tot += len(U)
+            c.acquire(l, U, stamp)
+            c.prefetch((l + 1) % L, _random_sets(rng, 1, E, min(E, K + 1))[0], stamp)
+            for ll in range(L):
+                s = [v for v in c.slot[ll] if v >= 0]
+                assert len(s) == len(set(s))
+    assert c.n.hits + c.n.demand + c.n.overflow == tot
+    outstanding = sum(len(p) for p in c.pending)
+    assert c.n.useful + c.n.wasted + outstanding == c.n.prefetch
+    if C >= E:
+        assert c.n.demand == 0 and c.n.overflow == 0
+
+
+def test_capacity_covers_all_experts_no_misses():
+    E, C = 5, 5
+    c = CacheSim(1, E, C, [list(range(E))])
+    want = 0
+    for s in range(1, 30):
+        U = {s % E, (s * 3 + 1) % E}
+        want += len(U)
+        c.acquire(0, sorted(U), s)
+    assert c.n.demand == 0 and c.n.hits == want
+
+
+def _optimal_misses(seq, C, warm):
+    """Fewest slot loads over all eviction choices (exhaustive; tiny inputs)."""
+    @functools.lru_cache(maxsize=None)
+    def go(i, resident):
+        if i == len(seq):
+            return 0
+        need = [f for f in seq[i] if f not in resident]
+        best = None
+        keep = frozenset(seq[i])
+        evictable = [v for v in resident if v not in keep]
+        free = C - len(resident)
+        if len(need) > free + len(evictable):
+            # more misses than slots: the extra stream without admission
+            n_admit = free + len(evictable)
+        else:
+            n_admit = len(need)
+        for adm in itertools.combinations(need, n_admit):
+            n_ev = max(0, len(adm) - free)
+            for ev in itertools.combinations(evictable, n_ev):
+                nr = frozenset((set(resident) - set(ev)) | set(adm))
+                v = go(i + 1, nr)
+                if best is None or v < best:
+                    best = v
+        return len(need) + best
+    return go(0, frozenset(warm))
+
+
+def test_on_demand_policy_is_not_better_than_optimum():
+    rng = np.random.default_rng(9)
+    for trial in range(12):
+        E, C, K = 5, 2, 2
+        seq = _random_sets(rng, 7, E, K)
+        c = CacheSim(1, E, C, [[0, 1]])
+        for i, U in enumerate(seq):
+            c.acquire(0, U, i + 1)
+        opt = _optimal_misses([tuple(s) for s in seq], C, (0, 1))
+        assert c.n.demand + c.n.overflow >= opt

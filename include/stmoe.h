@@ -1,0 +1,296 @@
+/*
+ * stmoe.h -- C ABI of the MI355X (gfx950) decode-step MoE layer with
+ * spatio-temporal expert prefetching (ST-MoE).
+ *
+ * The calls follow the paper's problem statement:
+ *   gating                      Section 2 (z_j = w_j^T x, softmax, top-K, weighted sum)
+ *   profile / predict / update  Section 4.2, Algorithms 1-3 and Eq. 1
+ *   prefetch, verify, missed    Section 4.1 and Section 4.3.4 (pipelined workflow)
+ *   loading
+ *   expert computation          Section 2 (experts are feed-forward networks; SwiGLU form)
+ *
+ * Conventions
+ *   - Every int-returning call returns STMOE_OK (0) or a negative status code;
+ *     stmoe_last_error() then returns a thread-local message.  No C++
+ *     exception crosses this boundary.
+ *   - Arguments are validated before any device work; an invalid call does
+ *     nothing on the device.
+ *   - "device" pointers are HIP device allocations of the current device;
+ *     "host" pointers are ordinary (or pinned, where stated) host memory.
+ *   - The caller owns every buffer it passes and every stream.  The library
+ *     owns only the opaque handles it creates (and the device tables behind
+ *     them) and frees them in the matching destroy call.
+ *   - `stream` arguments are hipStream_t values passed as void* (NULL is the
+ *     default stream).  Calls are asynchronous on that stream unless marked
+ *     [sync].
+ *   - Limits: 1 <= E <= 256 (8-bit expert indices in the tables),
+ *     1 <= K <= min(E, 16), 1 <= B <= 16, H and I multiples of 8, H <= 16384.
+ *   - Data types: STMOE_BF16 (weights and activations bfloat16, fp32
+ *     accumulation) or STMOE_F32.  Outputs of the FFN are fp32.
+ */
+#ifndef STMOE_H
+#define STMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    STMOE_OK = 0,
+    STMOE_EINVAL = -1,     /* invalid argument */
+    STMOE_EHIP = -2,       /* a HIP runtime call failed */
+    STMOE_ENOMEM = -3,     /* allocation failed or workspace too small */
+    STMOE_ECAPACITY = -4,  /* cache arena too small for the requested slots */
+    STMOE_ESTATE = -5      /* call out of order (e.g. predict before profile) */
+};
+
+typedef enum { STMOE_F32 = 0, STMOE_BF16 = 1 } stmoe_dtype;
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* stmoe_last_error(void);
+/* ABI version of this header: 1. */
+int stmoe_abi_version(void);
+
+/* ------------------------------------------------------------------------
+ * Gating (Section 2): z[b][e] = sum_h x[b][h] * w_gate[e][h] (fp32
+ * accumulation), s = softmax(z[b]), top-K experts by logit (descending,
+ * equal logits -> lower index), weight = s of the selected expert (the
+ * paper weights expert outputs by their gating probabilities), or, with
+ * renorm = 1, that probability divided by the sum over the K selected.
+ *
+ *   x        device [B][H] row-major, dtype
+ *   w_gate   device [E][H] row-major, dtype
+ *   topk_idx device out [B][K] int32, in descending-logit order
+ *   topk_w   device out [B][K] fp32
+ *   logits   device out [B][E] fp32, or NULL
+ *   ws       device workspace of moe_route_workspace_bytes(B, E) bytes that
+ *            the caller zero-fills once before its first use; every call
+ *            leaves it zero-filled again at kernel exit (a completion ticket)
+ *   Calls sharing one workspace must be ordered on one stream.
+ * ---------------------------------------------------------------------- */
+size_t moe_route_workspace_bytes(int B, int E);
+int moe_route_topk(const void* x, const void* w_gate, int B, int H, int E, int K,
+                   int dtype, int renorm, int32_t* topk_idx, float* topk_w, float* logits,
+                   void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Spatio-temporal predictor (Section 4.2).
+ *
+ * Device state per predictor: for every adjacent layer pair i (0..L-2) a
+ * Cross-layer Correlation Table CCT_i[E][K] of (expert index, 2-bit
+ * confidence) slots; for every layer l and batch row b a History Table entry
+ * HT[l][b][K] holding the previous token's selection (kept sorted ascending;
+ * its confidence is fixed at 2, "10").  Batch rows share the CCTs.
+ * ---------------------------------------------------------------------- */
+typedef struct stmoe_predictor stmoe_predictor;
+
+/* Prediction sources, for the ablation of Section 5 (temporal / spatial). */
+enum { STMOE_USE_CCT = 1, STMOE_USE_HT = 2, STMOE_USE_BOTH = 3 };
+
+/* Allocate the device tables of a predictor (zeroed).  [sync] */
+int stmoe_create(int L, int E, int K, int B, stmoe_predictor** out);
+int stmoe_destroy(stmoe_predictor* p);
+
+/* Algorithm 1 and the HT initialisation (Section 4.1).  [sync]
+ *   sel  host [P][B][L][K] int32: the profiling tokens' selections (distinct
+ *        within each [K] row, each < E).
+ * For each pair i, Co_i[e][f] counts tokens and rows that selected e at
+ * layer i and f at layer i+1; CCT_i[e] takes the K largest counts (equal
+ * counts -> lower index) with confidence 2; HT[l][b] <- sel[P-1][b][l].
+ * Resets the hit statistics. */
+int stmoe_profile(stmoe_predictor* p, const int32_t* sel, int P);
+
+/* Verify + table update at `layer` (Algorithm 3; Section 4.3.4).
+ *   sel_prev device [B][K] int32: selection at layer-1 (ignored at layer 0)
+ *   sel_cur  device [B][K] int32: selection at layer
+ * For b = 0..B-1 in order, every CCT_{layer-1} entry e in sel_prev[b] is
+ * updated against F = sel_cur[b]: a slot whose expert is in F gains 1
+ * (saturating at 3); otherwise it loses 1 while above 0, and at 0 it is
+ * replaced by the next expert (ascending) of F that the entry did not hold
+ * before this update, with confidence 2.  Then HT[layer][b] <- sel_cur[b].
+ * If `online` is 0 the CCT is left unchanged (HT is still overwritten).
+ * Also counts |sel_cur[b] intersect P_layer[b]| against the last prediction
+ * made for this layer, into the statistics. */
+int stmoe_update(stmoe_predictor* p, int layer, const int32_t* sel_prev,
+                 const int32_t* sel_cur, int online, void* stream);
+
+/* Expert prediction for layer+1 (Algorithm 2 with Eq. 1).
+ *   layer    0..L-2 predicts layer+1 from sel_cur; -1 predicts layer 0 from
+ *            HT[0] alone (sel_cur ignored).
+ *   sel_cur  device [B][K] int32
+ *   use      STMOE_USE_* bit set
+ *   score    device out [B][E] uint8 or NULL:
+ *            score[b][f] = sum_{e in sel_cur[b]} conf of f in CCT_layer[e]
+ *                          + 2 * [f in HT[layer+1][b]]
+ *   mask     device out [E] uint8 or NULL: 1 where any row scores >= 2
+ *   ranked   device out [E] int32 or NULL: experts with mask = 1 ordered by
+ *            (max over rows of score desc, index asc), then -1 padding
+ *   n_ranked device out [1] int32 or NULL: number of such experts */
+int stmoe_predict(stmoe_predictor* p, int layer, const int32_t* sel_cur, int use,
+                  uint8_t* score, uint8_t* mask, int32_t* ranked, int32_t* n_ranked,
+                  void* stream);
+
+/* Copy the tables to host memory (any pointer may be NULL).  [sync]
+ *   co [L-1][E][E] int32, cct_idx / cct_conf [L-1][E][K] uint8,
+ *   ht [L][B][K] uint8 */
+int stmoe_export(stmoe_predictor* p, int32_t* co, uint8_t* cct_idx, uint8_t* cct_conf,
+                 uint8_t* ht);
+/* Replace the CCT and HT with host copies (same layouts).  [sync] */
+int stmoe_import(stmoe_predictor* p, const uint8_t* cct_idx, const uint8_t* cct_conf,
+                 const uint8_t* ht);
+
+/* Hit statistics per layer since stmoe_profile, host out [L][3] int64:
+ * (sum |A intersect P|, sum |A|, sum |P|) over batch rows.  [sync] */
+int stmoe_stats(stmoe_predictor* p, int64_t* out);
+
+/* ------------------------------------------------------------------------
+ * Expert packing.  A packed expert ("blob") is one contiguous buffer:
+ * W_gate [I][H], then W_up [I][H], then W_down [H][I], each row-major in
+ * the storage dtype; 3*H*I elements.  One blob moves with one copy.
+ * ---------------------------------------------------------------------- */
+size_t moe_blob_bytes(int H, int I, int dtype);
+/* [sync, host] blob_out: host, moe_blob_bytes(H, I, dtype) bytes. */
+int moe_pack_expert(const void* w_gate, const void* w_up, const void* w_down, int H, int I,
+                    int dtype, void* blob_out);
+
+/* ------------------------------------------------------------------------
+ * Expert FFN (Section 2): for every batch row b
+ *   y[b] = sum_k topk_w[b][k] * W_down e (silu(W_gate e x[b]) * (W_up e x[b]))
+ *        + sum_s  W_down s (silu(W_gate s x[b]) * (W_up s x[b]))   (shared, weight 1)
+ * with e = topk_idx[b][k] and silu(g) = g / (1 + exp(-g)).
+ * Each distinct selected expert's weights are read once per call.  The sum
+ * over experts runs in ascending expert index (shared experts last), so the
+ * result does not depend on where the blobs live.
+ *
+ *   x            device [B][H] dtype
+ *   topk_idx     device [B][K] int32 (< E), topk_w device [B][K] fp32
+ *   expert_ptrs  device array [E] of device blob pointers; only selected
+ *                experts' entries are read
+ *   shared_ptrs  device array [n_shared] of device blob pointers, or NULL
+ *   y            device out [B][H] fp32 (overwritten)
+ *   ws           device workspace, moe_expert_ffn_workspace_bytes(...) bytes
+ *   B < 8 runs the GEMV kernels; B >= 8 the MFMA grouped-GEMM kernels.
+ * ---------------------------------------------------------------------- */
+size_t moe_expert_ffn_workspace_bytes(int B, int K, int E, int I, int n_shared);
+int moe_expert_ffn(const void* x, const int32_t* topk_idx, const float* topk_w, int B, int K,
+                   int H, int I, int E, int dtype, const void* const* expert_ptrs,
+                   const void* const* shared_ptrs, int n_shared, float* y, void* ws,
+                   size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Expert cache policy (host only, no HIP calls): per-layer partition of C
+ * slots, least recently used with protection of the current set.
+ *   prefetch(layer, ranked, n, stamp): for each of the first min(n, C)
+ *     ranked experts not resident, evict the slot whose expert is not among
+ *     them with the smallest (last use, slot); stop when none is left.
+ *   acquire(layer, needed, n, stamp): for each needed expert (ascending) not
+ *     resident, evict the slot whose expert is not needed with the smallest
+ *     (last use, slot); with no such slot the expert is "overflow" (served
+ *     from staging, not admitted).  Then needed resident experts get
+ *     last use = stamp.
+ * Decisions are returned as (expert, slot) pairs; overflow experts as slot -1.
+ * ---------------------------------------------------------------------- */
+typedef struct stmoe_policy stmoe_policy;
+typedef struct {
+    int64_t hits, demand, overflow, prefetch, useful, wasted;
+} stmoe_cache_stats;
+
+int stmoe_policy_create(int L, int E, int C, const int32_t* warm /* host [L][C], -1 = empty */,
+                        stmoe_policy** out);
+int stmoe_policy_destroy(stmoe_policy* p);
+/* returns the number of copies (>= 0); pairs host out [2*C] (expert, slot) */
+int stmoe_policy_prefetch(stmoe_policy* p, int layer, const int32_t* ranked, int n,
+                          int64_t stamp, int32_t* pairs);
+/* returns the number of entries written to pairs (host out [2*n]):
+ * (expert, slot) for each needed expert that was not resident, slot -1 for
+ * overflow; *n_hits receives the number of resident experts. */
+int stmoe_policy_acquire(stmoe_policy* p, int layer, const int32_t* needed, int n,
+                         int64_t stamp, int32_t* pairs, int32_t* n_hits);
+/* slot_expert host out [L][C] (-1 = empty) */
+int stmoe_policy_slots(const stmoe_policy* p, int32_t* slot_expert);
+int stmoe_policy_stats(const stmoe_policy* p, stmoe_cache_stats* out);
+
+/* ------------------------------------------------------------------------
+ * HBM expert cache (Section 4.1 prefetch staging; Section 4.3.4 missed
+ * loading).  Routed experts of layer l live either in one of the layer's C
+ * HBM slots or only in the pinned host pool; copies are one hipMemcpyAsync
+ * per blob.  Prefetches run on `side`, demand copies on `demand`; slot
+ * reuse is ordered by events (a slot is overwritten only after its last
+ * reader and its previous copy have completed).
+ *
+ *   arena       device, at least expert_cache_arena_bytes(L, C, blob, n_stage)
+ *   host_blobs  host array [L*E] of pinned host blob pointers
+ *   n_stage     staging slots for overflow experts (>= 1 when a layer can
+ *               select more distinct experts than C)
+ * ---------------------------------------------------------------------- */
+typedef struct expert_cache expert_cache;
+
+size_t expert_cache_arena_bytes(int L, int C, size_t blob_bytes, int n_stage);
+int expert_cache_create(int L, int E, int C, size_t blob_bytes, int n_stage, void* arena,
+                        size_t arena_bytes, const void* const* host_blobs, void* demand_stream,
+                        void* side_stream, expert_cache** out);
+int expert_cache_destroy(expert_cache* c);
+/* Load the initial residency warm [L][C] (host, -1 = empty).  [sync] */
+int expert_cache_warm(expert_cache* c, const int32_t* warm);
+/* Issue prefetch copies on the side stream; returns the number of copies. */
+int expert_cache_prefetch(expert_cache* c, int layer, const int32_t* ranked, int n,
+                          int64_t stamp);
+/* Make `needed` (host, n distinct experts) resident for a kernel on
+ * `compute`: demand copies on the demand stream, `compute` waits for every
+ * copy it needs; dev_table_out (host [E]) receives the device blob pointer
+ * of each needed expert (other entries untouched). */
+int expert_cache_acquire(expert_cache* c, int layer, const int32_t* needed, int n,
+                         int64_t stamp, const void** dev_table_out, void* compute);
+/* Mark the slots handed out by the last acquire of `layer` as read by work
+ * enqueued so far on `compute`. */
+int expert_cache_release(expert_cache* c, int layer, void* compute);
+int expert_cache_stats(const expert_cache* c, stmoe_cache_stats* out);
+
+/* ------------------------------------------------------------------------
+ * One decode-step MoE layer (Section 4.3.4): route, verify/update, predict
+ * the next layer, fetch missed experts, expert FFN, prefetch the next
+ * layer's predicted experts.
+ * ---------------------------------------------------------------------- */
+enum { MOE_MODE_ON_DEMAND = 0, MOE_MODE_STMOE = 1, MOE_MODE_HT_ONLY = 2, MOE_MODE_CCT_ONLY = 3 };
+
+typedef struct {
+    int L, E, K, B, H, I, n_shared, dtype, renorm;
+    const void* const* router_w;   /* host [L] device pointers to W_g [E][H] */
+    const void* const* shared_w;   /* host [L*n_shared] device blob pointers, or NULL */
+    const void* const* resident_w; /* host [L*E] device blob pointers when every routed
+                                      expert is in HBM (cache must then be NULL) */
+} moe_model_desc;
+
+typedef struct moe_ctx moe_ctx;
+
+/* cache may be NULL only when desc->resident_w is given. */
+int moe_ctx_create(const moe_model_desc* desc, stmoe_predictor* pred, expert_cache* cache,
+                   void* compute_stream, moe_ctx** out);
+int moe_ctx_destroy(moe_ctx* ctx);
+/* One MoE layer for decode token `token`:
+ *   x device [B][H] dtype; y device out [B][H] fp32.
+ * With a cache, this call waits once on the host for the layer's routing
+ * record (selected and predicted experts).  Without one it never waits.
+ * Layer-0 predictions come from HT[0]; the prefetch for layer 0 of the next
+ * token is issued at layer L-1. */
+int moe_decode_layer(moe_ctx* ctx, int token, int layer, const void* x, float* y, int mode);
+/* All L layers of one token: xs device [L][B][H], ys device out [L][B][H]. */
+int moe_decode_token(moe_ctx* ctx, int token, const void* xs, float* ys, int mode);
+/* Last routing of each layer: host out idx [L][B][K] int32, w [L][B][K] fp32.  [sync] */
+int moe_ctx_last_routing(moe_ctx* ctx, int32_t* idx, float* w);
+/* Event timing of the expert-FFN kernels: enable = 1 starts recording
+ * (resets totals), 0 stops.  moe_ctx_timing syncs and returns the summed
+ * milliseconds of the gate/up kernel and of the down kernel (events recorded
+ * on the compute stream before, between and after them), the number of FFN
+ * calls and the summed number of distinct routed experts over those calls. */
+int moe_ctx_set_timing(moe_ctx* ctx, int enable);
+int moe_ctx_timing(moe_ctx* ctx, double* up_ms, double* down_ms, int64_t* n_calls,
+                   int64_t* n_experts);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* STMOE_H */

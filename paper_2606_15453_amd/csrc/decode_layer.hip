@@ -1,0 +1,347 @@
+// One decode-step MoE layer (Section 4.3.4, pipelined workflow):
+//   route (R) -> verify + table update (V) -> predict the next layer (P)
+//   -> missed loading of experts the prediction did not stage (ML)
+//   -> expert computation (Com.) -> prefetch of the next layer's predicted
+//   experts (EP), overlapping the computation.
+//
+// Without a cache (every routed expert resident in HBM) the layer is a fixed
+// sequence of kernels on the compute stream and never waits on the host.
+// With a cache, the host reads one small routing record per layer (the
+// selection and the ranked prediction) because hipMemcpyAsync needs
+// host-known source addresses; that is the layer's only host wait.
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+namespace stmoe {
+int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, int H, int I, int E,
+               int dtype, const void* const* eptr, const void* const* sptr, int n_shared,
+               float* y, void* ws, hipStream_t s, unsigned long long* n_experts, hipEvent_t ev_mid);
+
+namespace {
+
+struct PtrTable {
+    const void* p[kMaxE];
+};
+
+// Write one layer's expert pointer table; the pointers travel as kernel
+// arguments, so the host may reuse its copy as soon as the launch returns.
+__global__ void set_table_kernel(PtrTable t, const void** dst, int E) {
+    for (int e = threadIdx.x; e < E; e += blockDim.x) dst[e] = t.p[e];
+}
+
+}  // namespace
+}  // namespace stmoe
+
+using namespace stmoe;
+
+struct moe_ctx {
+    int L, E, K, B, H, I, n_shared, dtype, renorm;
+    size_t esz;
+    std::vector<const void*> router;       // [L]
+    stmoe_predictor* pred = nullptr;
+    expert_cache* cache = nullptr;
+    hipStream_t s = nullptr;
+    int32_t* idx = nullptr;                // [L][B][K] device
+    float* w = nullptr;                    // [L][B][K] device
+    int32_t* ranked = nullptr;             // [E + 1] device: ranked list, then its length
+    void* route_ws = nullptr;
+    size_t route_ws_bytes = 0;
+    void* ffn_ws = nullptr;
+    size_t ffn_ws_bytes = 0;
+    const void** tables = nullptr;         // [L][E] device blob pointers
+    const void** shared = nullptr;         // [L][n_shared] device blob pointers
+    int32_t* rec = nullptr;                // pinned host: idx [B][K], ranked [E], n_ranked
+    hipEvent_t rec_ev = nullptr;
+    std::vector<const void*> host_table;   // [E] scratch for the cache's answers
+    bool started = false;
+    int last_token = -1, last_layer = -1;
+    // FFN timing
+    bool timing = false;
+    std::vector<hipEvent_t> ev_pool;
+    size_t ev_used = 0;
+    unsigned long long* n_experts = nullptr;   // device counter
+    int64_t n_calls = 0;
+};
+
+namespace {
+
+void free_ctx(moe_ctx* c) {
+    if (!c) return;
+    if (c->s) (void)hipStreamSynchronize(c->s);
+    (void)hipFree(c->idx);
+    (void)hipFree(c->w);
+    (void)hipFree(c->ranked);
+    (void)hipFree(c->route_ws);
+    (void)hipFree(c->ffn_ws);
+    (void)hipFree(c->tables);
+    (void)hipFree(c->shared);
+    (void)hipFree(c->n_experts);
+    if (c->rec) (void)hipHostFree(c->rec);
+    if (c->rec_ev) (void)hipEventDestroy(c->rec_ev);
+    for (auto e : c->ev_pool) (void)hipEventDestroy(e);
+    delete c;
+}
+
+int use_bits(int mode) {
+    switch (mode) {
+        case MOE_MODE_STMOE: return STMOE_USE_BOTH;
+        case MOE_MODE_HT_ONLY: return STMOE_USE_HT;
+        case MOE_MODE_CCT_ONLY: return STMOE_USE_CCT;
+        default: return 0;
+    }
+}
+
+int set_table(moe_ctx* c, int layer, const std::vector<const void*>& tab) {
+    PtrTable t;
+    for (int e = 0; e < c->E; ++e) t.p[e] = tab[e];
+    hipLaunchKernelGGL(set_table_kernel, dim3(1), dim3(256), 0, c->s, t, c->tables + size_t(layer) * c->E,
+                       c->E);
+    STMOE_LAUNCHED();
+    return STMOE_OK;
+}
+
+// Copy the ranked prediction to the host and prefetch it.
+int prefetch_from_record(moe_ctx* c, int target, int64_t stamp) {
+    const int32_t* ranked = c->rec + c->B * c->K;
+    const int n = ranked[c->E];
+    if (n <= 0) return STMOE_OK;
+    const int rc = expert_cache_prefetch(c->cache, target, ranked, n, stamp);
+    return rc < 0 ? rc : STMOE_OK;
+}
+
+int fetch_record(moe_ctx* c, const int32_t* idx_dev, bool with_ranked) {
+    STMOE_HIP(hipMemcpyAsync(c->rec, idx_dev, size_t(c->B) * c->K * sizeof(int32_t),
+                             hipMemcpyDeviceToHost, c->s));
+    if (with_ranked)
+        STMOE_HIP(hipMemcpyAsync(c->rec + c->B * c->K, c->ranked, size_t(c->E + 1) * sizeof(int32_t),
+                                 hipMemcpyDeviceToHost, c->s));
+    STMOE_HIP(hipEventRecord(c->rec_ev, c->s));
+    STMOE_HIP(hipEventSynchronize(c->rec_ev));
+    return STMOE_OK;
+}
+
+hipEvent_t next_event(moe_ctx* c) {
+    if (c->ev_used == c->ev_pool.size()) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        c->ev_pool.push_back(e);
+    }
+    return c->ev_pool[c->ev_used++];
+}
+
+}  // namespace
+
+extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, expert_cache* cache,
+                              void* compute_stream, moe_ctx** out) {
+    clear_error();
+    STMOE_CHECK(d && out && d->router_w, "null pointer");
+    STMOE_CHECK(d->L >= 1 && d->E >= 1 && d->E <= kMaxE, "bad L/E");
+    STMOE_CHECK(d->K >= 1 && d->K <= d->E && d->K <= kMaxK, "bad K");
+    STMOE_CHECK(d->B >= 1 && d->B <= kMaxB, "bad B");
+    STMOE_CHECK(d->H >= 8 && d->H % 8 == 0 && d->H <= kMaxH, "bad H");
+    STMOE_CHECK(d->I >= 8 && d->I % 8 == 0, "bad I");
+    STMOE_CHECK(d->n_shared >= 0 && d->n_shared <= 8, "bad n_shared");
+    STMOE_CHECK(d->n_shared == 0 || d->shared_w, "shared_w is required when n_shared > 0");
+    STMOE_CHECK(d->dtype == STMOE_BF16 || d->dtype == STMOE_F32, "bad dtype");
+    STMOE_CHECK((cache == nullptr) != (d->resident_w == nullptr),
+                "give exactly one of a cache or resident expert pointers");
+    for (int l = 0; l < d->L; ++l) STMOE_CHECK(d->router_w[l], "null router pointer");
+    auto* c = new moe_ctx();
+    c->L = d->L; c->E = d->E; c->K = d->K; c->B = d->B; c->H = d->H; c->I = d->I;
+    c->n_shared = d->n_shared; c->dtype = d->dtype; c->renorm = d->renorm;
+    c->esz = d->dtype == STMOE_BF16 ? 2 : 4;
+    c->router.assign(d->router_w, d->router_w + d->L);
+    c->pred = pred;
+    c->cache = cache;
+    c->s = as_stream(compute_stream);
+    c->host_table.assign(c->E, nullptr);
+    const size_t LBK = size_t(c->L) * c->B * c->K;
+    c->route_ws_bytes = moe_route_workspace_bytes(c->B, c->E);
+    c->ffn_ws_bytes = moe_expert_ffn_workspace_bytes(c->B, c->K, c->E, c->I, c->n_shared);
+    hipError_t e = hipSuccess;
+    if (e == hipSuccess) e = hipMalloc(&c->idx, LBK * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMalloc(&c->w, LBK * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(&c->ranked, size_t(c->E + 1) * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMalloc(&c->route_ws, c->route_ws_bytes);
+    if (e == hipSuccess) e = hipMalloc(&c->ffn_ws, c->ffn_ws_bytes);
+    if (e == hipSuccess) e = hipMalloc(&c->tables, size_t(c->L) * c->E * sizeof(void*));
+    if (e == hipSuccess && c->n_shared)
+        e = hipMalloc(&c->shared, size_t(c->L) * c->n_shared * sizeof(void*));
+    if (e == hipSuccess) e = hipMalloc(&c->n_experts, sizeof(unsigned long long));
+    if (e == hipSuccess) e = hipHostMalloc(&c->rec, size_t(c->B * c->K + c->E + 1) * sizeof(int32_t));
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->rec_ev, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipMemset(c->route_ws, 0, c->route_ws_bytes);
+    if (e == hipSuccess) e = hipMemset(c->idx, 0, LBK * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(c->w, 0, LBK * sizeof(float));
+    if (e == hipSuccess) e = hipMemset(c->tables, 0, size_t(c->L) * c->E * sizeof(void*));
+    if (e == hipSuccess) e = hipMemset(c->n_experts, 0, sizeof(unsigned long long));
+    if (e == hipSuccess && d->resident_w)
+        e = hipMemcpy(c->tables, d->resident_w, size_t(c->L) * c->E * sizeof(void*), hipMemcpyHostToDevice);
+    if (e == hipSuccess && c->n_shared)
+        e = hipMemcpy(c->shared, d->shared_w, size_t(c->L) * c->n_shared * sizeof(void*),
+                      hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        set_error(std::string("moe_ctx_create: ") + hipGetErrorString(e));
+        free_ctx(c);
+        return e == hipErrorOutOfMemory ? STMOE_ENOMEM : STMOE_EHIP;
+    }
+    *out = c;
+    return STMOE_OK;
+}
+
+extern "C" int moe_ctx_destroy(moe_ctx* c) {
+    free_ctx(c);
+    return STMOE_OK;
+}
+
+extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int mode) {
+    clear_error();
+    STMOE_CHECK(c && x && y, "null pointer");
+    STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
+    STMOE_CHECK(token >= 0, "token must be >= 0");
+    STMOE_CHECK(mode >= MOE_MODE_ON_DEMAND && mode <= MOE_MODE_CCT_ONLY, "bad mode");
+    const int use = use_bits(mode);
+    STMOE_CHECK(use == 0 || c->pred, "prediction modes need a predictor");
+    const int L = c->L, B = c->B, K = c->K, E = c->E;
+    const int64_t stamp = int64_t(token) * L + layer + 1;
+    int32_t* idx_l = c->idx + size_t(layer) * B * K;
+    float* w_l = c->w + size_t(layer) * B * K;
+
+    // first call: layer 0's prediction comes from the profiled HT[0]
+    if (!c->started) {
+        c->started = true;
+        if (use) {
+            if (int rc = stmoe_predict(c->pred, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr,
+                                       c->ranked, c->ranked + E, c->s))
+                return rc;
+            if (c->cache) {
+                if (int rc = fetch_record(c, idx_l, true)) return rc;
+                if (int rc = prefetch_from_record(c, 0, stamp - 1)) return rc;
+            }
+        }
+    }
+
+    // R: gating
+    if (int rc = moe_route_topk(x, c->router[layer], B, c->H, E, K, c->dtype, c->renorm, idx_l, w_l,
+                                nullptr, c->route_ws, c->route_ws_bytes, c->s))
+        return rc;
+    // V + P: verify/update against the previous layer, predict the next one
+    if (use) {
+        const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
+        if (int rc = stmoe_update(c->pred, layer, prev, idx_l, 1, c->s)) return rc;
+        if (layer + 1 < L) {
+            if (int rc = stmoe_predict(c->pred, layer, idx_l, use, nullptr, nullptr, c->ranked,
+                                       c->ranked + E, c->s))
+                return rc;
+        } else {
+            if (int rc = stmoe_predict(c->pred, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr,
+                                       c->ranked, c->ranked + E, c->s))
+                return rc;
+        }
+    }
+    // ML: make the selection resident
+    if (c->cache) {
+        if (int rc = fetch_record(c, idx_l, use != 0)) return rc;
+        int needed[kMaxE];
+        int n = 0;
+        {
+            std::vector<char> seen(E, 0);
+            for (int i = 0; i < B * K; ++i) {
+                const int e = c->rec[i];
+                if (e < 0 || e >= E) {
+                    set_error("moe_decode_layer: routing produced an invalid expert index");
+                    return STMOE_ESTATE;
+                }
+                if (!seen[e]) { seen[e] = 1; needed[n++] = e; }
+            }
+            std::sort(needed, needed + n);
+        }
+        const int rc = expert_cache_acquire(c->cache, layer, needed, n, stamp, c->host_table.data(), c->s);
+        if (rc < 0) return rc;
+        if (int rc2 = set_table(c, layer, c->host_table)) return rc2;
+    }
+    // Com.: expert FFN (timed with events before, between and after its two kernels)
+    hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
+    if (c->timing) {
+        e0 = next_event(c);
+        e1 = next_event(c);
+        e2 = next_event(c);
+        if (!e0 || !e1 || !e2) { set_error("moe_decode_layer: hipEventCreate failed"); return STMOE_EHIP; }
+        STMOE_HIP(hipEventRecord(e0, c->s));
+    }
+    if (int rc = ffn_launch(x, idx_l, w_l, B, K, c->H, c->I, E, c->dtype, c->tables + size_t(layer) * E,
+                            c->n_shared ? c->shared + size_t(layer) * c->n_shared : nullptr, c->n_shared,
+                            y, c->ffn_ws, c->s, c->timing ? c->n_experts : nullptr, e1))
+        return rc;
+    if (c->timing) {
+        STMOE_HIP(hipEventRecord(e2, c->s));
+        ++c->n_calls;
+    }
+    // EP: prefetch the next layer's predicted experts, overlapping the FFN
+    if (c->cache) {
+        if (int rc = expert_cache_release(c->cache, layer, c->s)) return rc;
+        if (use) {
+            if (int rc = prefetch_from_record(c, (layer + 1) % L, stamp)) return rc;
+        }
+    }
+    c->last_token = token;
+    c->last_layer = layer;
+    return STMOE_OK;
+}
+
+extern "C" int moe_decode_token(moe_ctx* c, int token, const void* xs, float* ys, int mode) {
+    clear_error();
+    STMOE_CHECK(c && xs && ys, "null pointer");
+    for (int l = 0; l < c->L; ++l) {
+        const char* x = reinterpret_cast<const char*>(xs) + size_t(l) * c->B * c->H * c->esz;
+        if (int rc = moe_decode_layer(c, token, l, x, ys + size_t(l) * c->B * c->H, mode)) return rc;
+    }
+    return STMOE_OK;
+}
+
+extern "C" int moe_ctx_last_routing(moe_ctx* c, int32_t* idx, float* w) {
+    clear_error();
+    STMOE_CHECK(c, "null ctx");
+    STMOE_HIP(hipStreamSynchronize(c->s));
+    const size_t n = size_t(c->L) * c->B * c->K;
+    if (idx) STMOE_HIP(hipMemcpy(idx, c->idx, n * sizeof(int32_t), hipMemcpyDeviceToHost));
+    if (w) STMOE_HIP(hipMemcpy(w, c->w, n * sizeof(float), hipMemcpyDeviceToHost));
+    return STMOE_OK;
+}
+
+extern "C" int moe_ctx_set_timing(moe_ctx* c, int enable) {
+    clear_error();
+    STMOE_CHECK(c, "null ctx");
+    STMOE_HIP(hipStreamSynchronize(c->s));
+    c->timing = enable != 0;
+    c->ev_used = 0;
+    c->n_calls = 0;
+    STMOE_HIP(hipMemset(c->n_experts, 0, sizeof(unsigned long long)));
+    return STMOE_OK;
+}
+
+extern "C" int moe_ctx_timing(moe_ctx* c, double* up_ms, double* down_ms, int64_t* n_calls,
+                              int64_t* n_experts) {
+    clear_error();
+    STMOE_CHECK(c, "null ctx");
+    STMOE_HIP(hipStreamSynchronize(c->s));
+    double a = 0.0, b = 0.0;
+    for (size_t i = 0; i + 2 < c->ev_used; i += 3) {
+        float t0 = 0.f, t1 = 0.f;
+        STMOE_HIP(hipEventElapsedTime(&t0, c->ev_pool[i], c->ev_pool[i + 1]));
+        STMOE_HIP(hipEventElapsedTime(&t1, c->ev_pool[i + 1], c->ev_pool[i + 2]));
+        a += t0;
+        b += t1;
+    }
+    unsigned long long ne = 0;
+    STMOE_HIP(hipMemcpy(&ne, c->n_experts, sizeof(ne), hipMemcpyDeviceToHost));
+    if (up_ms) *up_ms = a;
+    if (down_ms) *down_ms = b;
+    if (n_calls) *n_calls = c->n_calls;
+    if (n_experts) *n_experts = int64_t(ne);
+    return STMOE_OK;
+}

@@ -1,0 +1,401 @@
+// HBM expert cache: the staging buffer that predicted experts are prefetched
+// into (Section 4.1; Section 4.3.4, "EP" and "ML" stages of the pipelined
+// workflow).  On the GPU the slow link is PCIe from pinned host memory and
+// the fast memory is HBM; one hipMemcpyAsync moves one packed expert.
+//
+// stmoe_policy is the pure decision logic (no HIP calls): per-layer slot
+// partitions, least recently used with protection of the current ranked or
+// selected set, residency counted from copy issue so decisions never depend
+// on timing.  expert_cache wraps it with slots in an HBM arena, a demand and
+// a side stream, and two events per slot (last copy into it, last reader of
+// it) that order every reuse.
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+struct stmoe_policy {
+    int L, E, C;
+    std::vector<int> slot;          // [L*C] expert in slot or -1
+    std::vector<int64_t> last;      // [L*C] last use stamp
+    std::vector<int> where;         // [L*E] slot of expert or -1
+    std::vector<char> pending;      // [L*E] prefetched, not yet verified
+    stmoe_cache_stats st{};
+
+    int victim(int l, const std::vector<char>& keep) const {
+        int best = -1;
+        for (int c = 0; c < C; ++c) {
+            const int e = slot[l * C + c];
+            if (e >= 0 && keep[e]) continue;
+            if (best < 0 || last[l * C + c] < last[l * C + best]) best = c;
+        }
+        return best;
+    }
+    void place(int l, int c, int e) {
+        const int old = slot[l * C + c];
+        if (old >= 0) where[l * E + old] = -1;
+        slot[l * C + c] = e;
+        where[l * E + e] = c;
+    }
+};
+
+namespace stmoe {
+namespace {
+
+int check_list(const int32_t* v, int n, int E, bool distinct) {
+    STMOE_CHECK(n >= 0 && n <= E, "list length must be in [0, E]");
+    STMOE_CHECK(n == 0 || v, "null list");
+    std::vector<char> seen(E, 0);
+    for (int i = 0; i < n; ++i) {
+        STMOE_CHECK(v[i] >= 0 && v[i] < E, "expert index out of range");
+        if (distinct) STMOE_CHECK(!seen[v[i]], "repeated expert in list");
+        seen[v[i]] = 1;
+    }
+    return STMOE_OK;
+}
+
+int policy_prefetch(stmoe_policy* p, int l, const int32_t* ranked, int n, int64_t stamp,
+                    int32_t* pairs) {
+    const int m = std::min(n, p->C);
+    std::vector<char> keep(p->E, 0);
+    for (int i = 0; i < m; ++i) keep[ranked[i]] = 1;
+    int copies = 0;
+    for (int i = 0; i < m; ++i) {
+        const int f = ranked[i];
+        if (p->where[l * p->E + f] >= 0) continue;
+        const int c = p->victim(l, keep);
+        if (c < 0) break;
+        p->place(l, c, f);
+        p->last[l * p->C + c] = stamp;
+        p->pending[l * p->E + f] = 1;
+        if (pairs) {
+            pairs[2 * copies] = f;
+            pairs[2 * copies + 1] = c;
+        }
+        ++copies;
+    }
+    p->st.prefetch += copies;
+    return copies;
+}
+
+int policy_acquire(stmoe_policy* p, int l, const int32_t* needed, int n, int64_t stamp,
+                   int32_t* pairs, int32_t* n_hits) {
+    std::vector<int> U(needed, needed + n);
+    std::sort(U.begin(), U.end());
+    std::vector<char> keep(p->E, 0);
+    for (int f : U) keep[f] = 1;
+    int out = 0, hits = 0;
+    std::vector<int> used;
+    for (int f : U) {
+        int c = p->where[l * p->E + f];
+        if (c >= 0) {
+            ++hits;
+            used.push_back(c);
+            continue;
+        }
+        c = p->victim(l, keep);
+        if (c < 0) {
+            if (pairs) { pairs[2 * out] = f; pairs[2 * out + 1] = -1; }
+            ++out;
+            ++p->st.overflow;
+            continue;
+        }
+        p->place(l, c, f);
+        used.push_back(c);
+        if (pairs) { pairs[2 * out] = f; pairs[2 * out + 1] = c; }
+        ++out;
+        ++p->st.demand;
+    }
+    for (int c : used) p->last[l * p->C + c] = stamp;
+    for (int e = 0; e < p->E; ++e) {
+        if (!p->pending[l * p->E + e]) continue;
+        if (keep[e]) ++p->st.useful; else ++p->st.wasted;
+        p->pending[l * p->E + e] = 0;
+    }
+    p->st.hits += hits;
+    if (n_hits) *n_hits = hits;
+    return out;
+}
+
+}  // namespace
+}  // namespace stmoe
+
+using namespace stmoe;
+
+extern "C" int stmoe_policy_create(int L, int E, int C, const int32_t* warm, stmoe_policy** out) {
+    clear_error();
+    STMOE_CHECK(out, "null output");
+    STMOE_CHECK(L >= 1 && E >= 1 && E <= kMaxE && C >= 1 && C <= kMaxE, "bad L/E/C");
+    auto* p = new stmoe_policy();
+    p->L = L; p->E = E; p->C = C;
+    p->slot.assign(size_t(L) * C, -1);
+    p->last.assign(size_t(L) * C, 0);
+    p->where.assign(size_t(L) * E, -1);
+    p->pending.assign(size_t(L) * E, 0);
+    if (warm) {
+        for (int l = 0; l < L; ++l)
+            for (int c = 0; c < C; ++c) {
+                const int e = warm[l * C + c];
+                if (e < 0) continue;
+                if (e >= E || p->where[l * E + e] >= 0) {
+                    delete p;
+                    set_error("stmoe_policy_create: warm set has an invalid or repeated expert");
+                    return STMOE_EINVAL;
+                }
+                p->place(l, c, e);
+            }
+    }
+    *out = p;
+    return STMOE_OK;
+}
+
+extern "C" int stmoe_policy_destroy(stmoe_policy* p) {
+    delete p;
+    return STMOE_OK;
+}
+
+extern "C" int stmoe_policy_prefetch(stmoe_policy* p, int layer, const int32_t* ranked, int n,
+                                     int64_t stamp, int32_t* pairs) {
+    clear_error();
+    STMOE_CHECK(p, "null policy");
+    STMOE_CHECK(layer >= 0 && layer < p->L, "layer out of range");
+    if (int rc = check_list(ranked, n, p->E, true)) return rc;
+    return policy_prefetch(p, layer, ranked, n, stamp, pairs);
+}
+
+extern "C" int stmoe_policy_acquire(stmoe_policy* p, int layer, const int32_t* needed, int n,
+                                    int64_t stamp, int32_t* pairs, int32_t* n_hits) {
+    clear_error();
+    STMOE_CHECK(p, "null policy");
+    STMOE_CHECK(layer >= 0 && layer < p->L, "layer out of range");
+    if (int rc = check_list(needed, n, p->E, true)) return rc;
+    return policy_acquire(p, layer, needed, n, stamp, pairs, n_hits);
+}
+
+extern "C" int stmoe_policy_slots(const stmoe_policy* p, int32_t* slot_expert) {
+    clear_error();
+    STMOE_CHECK(p && slot_expert, "null pointer");
+    std::copy(p->slot.begin(), p->slot.end(), slot_expert);
+    return STMOE_OK;
+}
+
+extern "C" int stmoe_policy_stats(const stmoe_policy* p, stmoe_cache_stats* out) {
+    clear_error();
+    STMOE_CHECK(p && out, "null pointer");
+    *out = p->st;
+    return STMOE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// device-backed cache
+// ---------------------------------------------------------------------------
+
+struct expert_cache {
+    stmoe_policy* pol = nullptr;
+    int L = 0, E = 0, C = 0, n_stage = 0;
+    size_t blob = 0;
+    char* arena = nullptr;
+    std::vector<const void*> host;       // [L*E]
+    hipStream_t demand = nullptr, side = nullptr;
+    std::vector<hipEvent_t> loaded, released;   // [L*C + n_stage]
+    std::vector<char> loaded_set, released_set;
+    int stage_next = 0;
+    std::vector<std::vector<int>> held;  // per layer: slots (global ids) read by the last acquire
+
+    char* slot_ptr(int gid) const { return arena + size_t(gid) * blob; }
+};
+
+namespace stmoe {
+namespace {
+
+// Order a copy into slot `gid` on stream `s` after its previous copy and
+// its last reader, then issue it and record the slot's loaded event.
+int copy_into(expert_cache* c, int gid, const void* src, hipStream_t s) {
+    if (c->loaded_set[gid]) STMOE_HIP(hipStreamWaitEvent(s, c->loaded[gid], 0));
+    if (c->released_set[gid]) STMOE_HIP(hipStreamWaitEvent(s, c->released[gid], 0));
+    STMOE_HIP(hipMemcpyAsync(c->slot_ptr(gid), src, c->blob, hipMemcpyHostToDevice, s));
+    STMOE_HIP(hipEventRecord(c->loaded[gid], s));
+    c->loaded_set[gid] = 1;
+    return STMOE_OK;
+}
+
+}  // namespace
+}  // namespace stmoe
+
+extern "C" size_t expert_cache_arena_bytes(int L, int C, size_t blob_bytes, int n_stage) {
+    if (L < 1 || C < 1 || n_stage < 0) return 0;
+    return (size_t(L) * C + n_stage) * blob_bytes;
+}
+
+extern "C" int expert_cache_create(int L, int E, int C, size_t blob_bytes, int n_stage, void* arena,
+                                   size_t arena_bytes, const void* const* host_blobs,
+                                   void* demand_stream, void* side_stream, expert_cache** out) {
+    clear_error();
+    STMOE_CHECK(out && arena && host_blobs, "null pointer");
+    STMOE_CHECK(L >= 1 && E >= 1 && E <= kMaxE && C >= 1 && C <= E, "bad L/E/C");
+    STMOE_CHECK(n_stage >= 0 && n_stage <= kMaxE, "n_stage must be in [0, 256]");
+    STMOE_CHECK(blob_bytes > 0 && blob_bytes % 16 == 0, "blob_bytes must be a positive multiple of 16");
+    STMOE_CHECK((reinterpret_cast<uintptr_t>(arena) & 255) == 0, "arena must be 256-byte aligned");
+    if (arena_bytes < expert_cache_arena_bytes(L, C, blob_bytes, n_stage)) {
+        set_error("expert_cache_create: arena smaller than (L*C + n_stage) * blob_bytes");
+        return STMOE_ECAPACITY;
+    }
+    for (size_t i = 0; i < size_t(L) * E; ++i) STMOE_CHECK(host_blobs[i], "null host blob pointer");
+    auto* c = new expert_cache();
+    if (int rc = stmoe_policy_create(L, E, C, nullptr, &c->pol)) {
+        delete c;
+        return rc;
+    }
+    c->L = L; c->E = E; c->C = C; c->n_stage = n_stage;
+    c->blob = blob_bytes;
+    c->arena = reinterpret_cast<char*>(arena);
+    c->host.assign(host_blobs, host_blobs + size_t(L) * E);
+    c->demand = as_stream(demand_stream);
+    c->side = as_stream(side_stream);
+    const size_t n = size_t(L) * C + n_stage;
+    c->loaded.assign(n, nullptr);
+    c->released.assign(n, nullptr);
+    c->loaded_set.assign(n, 0);
+    c->released_set.assign(n, 0);
+    c->held.assign(L, {});
+    for (size_t i = 0; i < n; ++i) {
+        if (hipEventCreateWithFlags(&c->loaded[i], hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&c->released[i], hipEventDisableTiming) != hipSuccess) {
+            expert_cache_destroy(c);
+            set_error("expert_cache_create: hipEventCreateWithFlags failed");
+            return STMOE_EHIP;
+        }
+    }
+    *out = c;
+    return STMOE_OK;
+}
+
+extern "C" int expert_cache_destroy(expert_cache* c) {
+    if (!c) return STMOE_OK;
+    if (c->demand) (void)hipStreamSynchronize(c->demand);
+    if (c->side) (void)hipStreamSynchronize(c->side);
+    for (auto e : c->loaded)
+        if (e) (void)hipEventDestroy(e);
+    for (auto e : c->released)
+        if (e) (void)hipEventDestroy(e);
+    stmoe_policy_destroy(c->pol);
+    delete c;
+    return STMOE_OK;
+}
+
+extern "C" int expert_cache_warm(expert_cache* c, const int32_t* warm) {
+    clear_error();
+    STMOE_CHECK(c && warm, "null pointer");
+    stmoe_policy* np = nullptr;
+    if (int rc = stmoe_policy_create(c->L, c->E, c->C, warm, &np)) return rc;
+    STMOE_HIP(hipStreamSynchronize(c->demand));
+    STMOE_HIP(hipStreamSynchronize(c->side));
+    stmoe_policy_destroy(c->pol);
+    c->pol = np;
+    for (int l = 0; l < c->L; ++l)
+        for (int s = 0; s < c->C; ++s) {
+            const int e = warm[l * c->C + s];
+            if (e < 0) continue;
+            STMOE_HIP(hipMemcpyAsync(c->slot_ptr(l * c->C + s), c->host[size_t(l) * c->E + e], c->blob,
+                                     hipMemcpyHostToDevice, c->demand));
+        }
+    STMOE_HIP(hipStreamSynchronize(c->demand));
+    std::fill(c->loaded_set.begin(), c->loaded_set.end(), 0);
+    std::fill(c->released_set.begin(), c->released_set.end(), 0);
+    for (auto& h : c->held) h.clear();
+    return STMOE_OK;
+}
+
+extern "C" int expert_cache_prefetch(expert_cache* c, int layer, const int32_t* ranked, int n,
+                                     int64_t stamp) {
+    clear_error();
+    STMOE_CHECK(c, "null cache");
+    STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
+    if (int rc = check_list(ranked, n, c->E, true)) return rc;
+    int32_t pairs[2 * kMaxE];
+    const int m = policy_prefetch(c->pol, layer, ranked, n, stamp, pairs);
+    for (int i = 0; i < m; ++i) {
+        const int e = pairs[2 * i], s = pairs[2 * i + 1];
+        if (int rc = copy_into(c, layer * c->C + s, c->host[size_t(layer) * c->E + e], c->side)) return rc;
+    }
+    return m;
+}
+
+extern "C" int expert_cache_acquire(expert_cache* c, int layer, const int32_t* needed, int n,
+                                    int64_t stamp, const void** dev_table_out, void* compute) {
+    clear_error();
+    STMOE_CHECK(c && dev_table_out, "null pointer");
+    STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
+    if (int rc = check_list(needed, n, c->E, true)) return rc;
+    hipStream_t cs = as_stream(compute);
+    int32_t pairs[2 * kMaxE];
+    int32_t n_hits = 0;
+    // overflow must fit the staging ring: count before committing
+    {
+        int missing = 0;
+        for (int i = 0; i < n; ++i) missing += c->pol->where[layer * c->E + needed[i]] < 0;
+        int evictable = 0;
+        std::vector<char> keep(c->E, 0);
+        for (int i = 0; i < n; ++i) keep[needed[i]] = 1;
+        for (int s = 0; s < c->C; ++s) {
+            const int e = c->pol->slot[layer * c->C + s];
+            evictable += (e < 0 || !keep[e]);
+        }
+        const int overflow = missing > evictable ? missing - evictable : 0;
+        if (overflow > c->n_stage) {
+            set_error("expert_cache_acquire: more overflow experts than staging slots");
+            return STMOE_ECAPACITY;
+        }
+    }
+    const int m = policy_acquire(c->pol, layer, needed, n, stamp, pairs, &n_hits);
+    auto& held = c->held[layer];
+    held.clear();
+    // demand copies and overflow staging
+    std::vector<int> gid_of(c->E, -1);
+    for (int i = 0; i < m; ++i) {
+        const int e = pairs[2 * i], s = pairs[2 * i + 1];
+        int gid;
+        if (s >= 0) {
+            gid = layer * c->C + s;
+        } else {
+            gid = c->L * c->C + c->stage_next;
+            c->stage_next = (c->stage_next + 1) % c->n_stage;
+        }
+        if (int rc = copy_into(c, gid, c->host[size_t(layer) * c->E + e], c->demand)) return rc;
+        gid_of[e] = gid;
+    }
+    // every needed expert: the compute stream waits for its slot's last copy
+    for (int i = 0; i < n; ++i) {
+        const int e = needed[i];
+        const int s = c->pol->where[layer * c->E + e];
+        const int gid = s >= 0 ? layer * c->C + s : gid_of[e];
+        if (gid < 0) {
+            set_error("expert_cache_acquire: internal error, expert without a slot");
+            return STMOE_ESTATE;
+        }
+        dev_table_out[e] = c->slot_ptr(gid);
+        if (c->loaded_set[gid]) STMOE_HIP(hipStreamWaitEvent(cs, c->loaded[gid], 0));
+        held.push_back(gid);
+    }
+    return n_hits;
+}
+
+extern "C" int expert_cache_release(expert_cache* c, int layer, void* compute) {
+    clear_error();
+    STMOE_CHECK(c, "null cache");
+    STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
+    for (int gid : c->held[layer]) {
+        STMOE_HIP(hipEventRecord(c->released[gid], as_stream(compute)));
+        c->released_set[gid] = 1;
+    }
+    c->held[layer].clear();
+    return STMOE_OK;
+}
+
+extern "C" int expert_cache_stats(const expert_cache* c, stmoe_cache_stats* out) {
+    clear_error();
+    STMOE_CHECK(c && out, "null pointer");
+    *out = c->pol->st;
+    return STMOE_OK;
+}

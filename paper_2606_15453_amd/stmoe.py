@@ -1,0 +1,379 @@
+"""Python binding of libstmoe.so (ctypes).
+
+Argument marshalling only: torch tensors become raw device/host pointers,
+torch streams become hipStream_t handles, and every call goes straight to
+the C ABI declared in include/stmoe.h.  Nothing here computes any step of
+the decode-step MoE layer.  Importing this module loads the library and
+raises if it has not been built (see paper_2606_15453_amd.build).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libstmoe.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_15453_amd.build`")
+
+# torch must load its HIP runtime first: the library then binds to that same
+# runtime (matching SONAME) instead of mapping a second one into the process.
+import torch  # noqa: E402,F401
+
+_lib = C.CDLL(LIB_PATH)
+
+
+def _hip_runtimes():
+    paths = set()
+    with open("/proc/self/maps") as f:
+        for line in f:
+            if "libamdhip64" in line:
+                paths.add(line.split()[-1])
+    return sorted(paths)
+
+
+if len(_hip_runtimes()) > 1:
+    raise ImportError(f"more than one HIP runtime mapped: {_hip_runtimes()}")
+
+OK, EINVAL, EHIP, ENOMEM, ECAPACITY, ESTATE = 0, -1, -2, -3, -4, -5
+F32, BF16 = 0, 1
+USE_CCT, USE_HT, USE_BOTH = 1, 2, 3
+MODE_ON_DEMAND, MODE_STMOE, MODE_HT_ONLY, MODE_CCT_ONLY = 0, 1, 2, 3
+
+vp, i32, i64, sz = C.c_void_p, C.c_int, C.c_int64, C.c_size_t
+P = C.POINTER
+
+
+class CacheStats(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in ("hits", "demand", "overflow", "prefetch", "useful", "wasted")]
+
+    def as_dict(self):
+        return {n: int(getattr(self, n)) for n, _ in self._fields_}
+
+
+class ModelDesc(C.Structure):
+    _fields_ = [("L", i32), ("E", i32), ("K", i32), ("B", i32), ("H", i32), ("I", i32),
+                ("n_shared", i32), ("dtype", i32), ("renorm", i32),
+                ("router_w", P(vp)), ("shared_w", P(vp)), ("resident_w", P(vp))]
+
+
+_SIGS = {
+    "stmoe_last_error": (C.c_char_p, []),
+    "stmoe_abi_version": (i32, []),
+    "moe_route_workspace_bytes": (sz, [i32, i32]),
+    "moe_route_topk": (i32, [vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]),
+    "stmoe_create": (i32, [i32, i32, i32, i32, P(vp)]),
+    "stmoe_destroy": (i32, [vp]),
+    "stmoe_profile": (i32, [vp, vp, i32]),
+    "stmoe_update": (i32, [vp, i32, vp, vp, i32, vp]),
+    "stmoe_predict": (i32, [vp, i32, vp, i32, vp, vp, vp, vp, vp]),
+    "stmoe_export": (i32, [vp, vp, vp, vp, vp]),
+    "stmoe_import": (i32, [vp, vp, vp, vp]),
+    "stmoe_stats": (i32, [vp, vp]),
+    "moe_blob_bytes": (sz, [i32, i32, i32]),
+    "moe_pack_expert": (i32, [vp, vp, vp, i32, i32, i32, vp]),
+    "moe_expert_ffn_workspace_bytes": (sz, [i32, i32, i32, i32, i32]),
+    "moe_expert_ffn": (i32, [vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp, sz, vp]),
+    "stmoe_policy_create": (i32, [i32, i32, i32, vp, P(vp)]),
+    "stmoe_policy_destroy": (i32, [vp]),
+    "stmoe_policy_prefetch": (i32, [vp, i32, vp, i32, i64, vp]),
+    "stmoe_policy_acquire": (i32, [vp, i32, vp, i32, i64, vp, vp]),
+    "stmoe_policy_slots": (i32, [vp, vp]),
+    "stmoe_policy_stats": (i32, [vp, P(CacheStats)]),
+    "expert_cache_arena_bytes": (sz, [i32, i32, sz, i32]),
+    "expert_cache_create": (i32, [i32, i32, i32, sz, i32, vp, sz, P(vp), vp, vp, P(vp)]),
+    "expert_cache_destroy": (i32, [vp]),
+    "expert_cache_warm": (i32, [vp, vp]),
+    "expert_cache_prefetch": (i32, [vp, i32, vp, i32, i64]),
+    "expert_cache_acquire": (i32, [vp, i32, vp, i32, i64, P(vp), vp]),
+    "expert_cache_release": (i32, [vp, i32, vp]),
+    "expert_cache_stats": (i32, [vp, P(CacheStats)]),
+    "moe_ctx_create": (i32, [P(ModelDesc), vp, vp, vp, P(vp)]),
+    "moe_ctx_destroy": (i32, [vp]),
+    "moe_decode_layer": (i32, [vp, i32, i32, vp, vp, i32]),
+    "moe_decode_token": (i32, [vp, i32, vp, vp, i32]),
+    "moe_ctx_last_routing": (i32, [vp, vp, vp]),
+    "moe_ctx_set_timing": (i32, [vp, i32]),
+    "moe_ctx_timing": (i32, [vp, P(C.c_double), P(C.c_double), P(i64), P(i64)]),
+}
+
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+EXPORTED = tuple(_SIGS)
+
+
+class StmoeError(RuntimeError):
+    def __init__(self, fn, rc):
+        msg = _lib.stmoe_last_error().decode()
+        super().__init__(f"{fn} failed with status {rc}: {msg}")
+        self.rc = rc
+
+
+def _call(name, *args):
+    rc = getattr(_lib, name)(*args)
+    if rc < 0:
+        raise StmoeError(name, rc)
+    return rc
+
+
+def _p(t):
+    """Raw pointer of a torch tensor / numpy array / int / None."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _s(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _i32(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def abi_version() -> int:
+    return _lib.stmoe_abi_version()
+
+
+# ---------------------------------------------------------------- gating
+def route_workspace_bytes(B, E):
+    return _lib.moe_route_workspace_bytes(B, E)
+
+
+def route_topk(x, w_gate, K, idx, w, ws, renorm=False, logits=None, stream=None, dtype=None):
+    B, H = x.shape
+    E = w_gate.shape[0]
+    dt = dtype if dtype is not None else (BF16 if x.element_size() == 2 else F32)
+    _call("moe_route_topk", _p(x), _p(w_gate), B, H, E, K, dt, int(renorm), _p(idx), _p(w),
+          _p(logits), _p(ws), ws.numel() * ws.element_size(), _s(stream))
+
+
+# ------------------------------------------------------------- predictor
+class Predictor:
+    def __init__(self, L, E, K, B):
+        self.L, self.E, self.K, self.B = L, E, K, B
+        h = vp()
+        _call("stmoe_create", L, E, K, B, C.byref(h))
+        self.h = h
+
+    def close(self):
+        if self.h:
+            _lib.stmoe_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def profile(self, sel):
+        sel = _i32(sel)
+        _call("stmoe_profile", self.h, sel.ctypes.data, sel.shape[0])
+
+    def update(self, layer, sel_prev, sel_cur, online=True, stream=None):
+        _call("stmoe_update", self.h, layer, _p(sel_prev), _p(sel_cur), int(online), _s(stream))
+
+    def predict(self, layer, sel_cur, use=USE_BOTH, score=None, mask=None, ranked=None,
+                n_ranked=None, stream=None):
+        _call("stmoe_predict", self.h, layer, _p(sel_cur), use, _p(score), _p(mask), _p(ranked),
+              _p(n_ranked), _s(stream))
+
+    def export(self):
+        L, E, K, B = self.L, self.E, self.K, self.B
+        pr = max(L - 1, 0)
+        co = np.zeros((pr, E, E), np.int32)
+        ci = np.zeros((pr, E, K), np.uint8)
+        cc = np.zeros((pr, E, K), np.uint8)
+        ht = np.zeros((L, B, K), np.uint8)
+        _call("stmoe_export", self.h, co.ctypes.data, ci.ctypes.data, cc.ctypes.data, ht.ctypes.data)
+        return co, ci, cc, ht
+
+    def import_tables(self, cct_idx, cct_conf, ht):
+        ci = np.ascontiguousarray(cct_idx, np.uint8)
+        cc = np.ascontiguousarray(cct_conf, np.uint8)
+        h = np.ascontiguousarray(ht, np.uint8)
+        _call("stmoe_import", self.h, ci.ctypes.data, cc.ctypes.data, h.ctypes.data)
+
+    def stats(self):
+        out = np.zeros((self.L, 3), np.int64)
+        _call("stmoe_stats", self.h, out.ctypes.data)
+        return out
+
+
+# ------------------------------------------------------------- packing
+def blob_bytes(H, I, dtype):
+    return _lib.moe_blob_bytes(H, I, dtype)
+
+
+def pack_expert(w_gate, w_up, w_down, dtype, out):
+    I, H = w_gate.shape
+    _call("moe_pack_expert", _p(w_gate), _p(w_up), _p(w_down), H, I, dtype, _p(out))
+
+
+# ------------------------------------------------------------- FFN
+def ffn_workspace_bytes(B, K, E, I, n_shared=0):
+    return _lib.moe_expert_ffn_workspace_bytes(B, K, E, I, n_shared)
+
+
+def expert_ffn(x, idx, w, H, I, E, dtype, expert_ptrs, y, ws, shared_ptrs=None, n_shared=0,
+               stream=None):
+    B, K = idx.shape
+    _call("moe_expert_ffn", _p(x), _p(idx), _p(w), B, K, H, I, E, dtype, _p(expert_ptrs),
+          _p(shared_ptrs), n_shared, _p(y), _p(ws), ws.numel() * ws.element_size(), _s(stream))
+
+
+# ------------------------------------------------------------- cache policy
+class Policy:
+    def __init__(self, L, E, C_, warm=None):
+        self.L, self.E, self.C = L, E, C_
+        h = vp()
+        wa = None if warm is None else _i32(warm)
+        _call("stmoe_policy_create", L, E, C_, None if wa is None else wa.ctypes.data, C.byref(h))
+        self.h = h
+
+    def __del__(self):
+        if getattr(self, "h", None):
+            _lib.stmoe_policy_destroy(self.h)
+            self.h = None
+
+    def prefetch(self, layer, ranked, stamp):
+        r = _i32(ranked)
+        pairs = np.zeros(2 * self.C + 2, np.int32)
+        n = _call("stmoe_policy_prefetch", self.h, layer, r.ctypes.data, len(r), stamp, pairs.ctypes.data)
+        return [tuple(pairs[2 * i:2 * i + 2].tolist()) for i in range(n)]
+
+    def acquire(self, layer, needed, stamp):
+        r = _i32(needed)
+        pairs = np.zeros(2 * max(len(r), 1), np.int32)
+        nh = C.c_int32()
+        n = _call("stmoe_policy_acquire", self.h, layer, r.ctypes.data, len(r), stamp, pairs.ctypes.data,
+                  C.byref(nh))
+        return [tuple(pairs[2 * i:2 * i + 2].tolist()) for i in range(n)], nh.value
+
+    def slots(self):
+        out = np.zeros((self.L, self.C), np.int32)
+        _call("stmoe_policy_slots", self.h, out.ctypes.data)
+        return out
+
+    def stats(self):
+        st = CacheStats()
+        _call("stmoe_policy_stats", self.h, C.byref(st))
+        return st.as_dict()
+
+
+# ------------------------------------------------------------- HBM cache
+def cache_arena_bytes(L, C_, blob, n_stage):
+    return _lib.expert_cache_arena_bytes(L, C_, blob, n_stage)
+
+
+class ExpertCache:
+    def __init__(self, L, E, C_, blob, n_stage, arena, host_ptrs, demand_stream, side_stream):
+        self.L, self.E, self.C = L, E, C_
+        self._host = (vp * (L * E))(*[int(p) for p in host_ptrs])
+        h = vp()
+        _call("expert_cache_create", L, E, C_, blob, n_stage, _p(arena), arena.numel() * arena.element_size(),
+              self._host, _s(demand_stream), _s(side_stream), C.byref(h))
+        self.h = h
+        self._arena = arena
+
+    def close(self):
+        if self.h:
+            _lib.expert_cache_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def warm(self, warm):
+        w = _i32(warm)
+        _call("expert_cache_warm", self.h, w.ctypes.data)
+
+    def prefetch(self, layer, ranked, stamp):
+        r = _i32(ranked)
+        return _call("expert_cache_prefetch", self.h, layer, r.ctypes.data, len(r), stamp)
+
+    def acquire(self, layer, needed, stamp, compute_stream=None):
+        r = _i32(needed)
+        tab = (vp * self.E)()
+        hits = _call("expert_cache_acquire", self.h, layer, r.ctypes.data, len(r), stamp, tab,
+                     _s(compute_stream))
+        return hits, [tab[e] for e in range(self.E)]
+
+    def release(self, layer, compute_stream=None):
+        _call("expert_cache_release", self.h, layer, _s(compute_stream))
+
+    def stats(self):
+        st = CacheStats()
+        _call("expert_cache_stats", self.h, C.byref(st))
+        return st.as_dict()
+
+
+# ------------------------------------------------------------- decode layer
+class DecodeContext:
+    """moe_ctx: one MoE decode stack on one stream (router, predictor, cache/FFN)."""
+
+    def __init__(self, L, E, K, B, H, I, dtype, router_ptrs, predictor=None, cache=None,
+                 resident_ptrs=None, shared_ptrs=None, n_shared=0, renorm=False, stream=None):
+        self.L, self.E, self.K, self.B = L, E, K, B
+        self._router = (vp * L)(*[int(p) for p in router_ptrs])
+        self._resident = None if resident_ptrs is None else (vp * (L * E))(*[int(p) for p in resident_ptrs])
+        self._shared = None if not n_shared else (vp * (L * n_shared))(*[int(p) for p in shared_ptrs])
+        d = ModelDesc(L, E, K, B, H, I, n_shared, dtype, int(renorm), self._router,
+                      self._shared, self._resident)
+        h = vp()
+        _call("moe_ctx_create", C.byref(d), predictor.h if predictor else None,
+              cache.h if cache else None, _s(stream), C.byref(h))
+        self.h = h
+        self._keep = (predictor, cache)
+
+    def close(self):
+        if self.h:
+            _lib.moe_ctx_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def layer(self, token, layer, x, y, mode=MODE_STMOE):
+        _call("moe_decode_layer", self.h, token, layer, _p(x), _p(y), mode)
+
+    def token(self, token, xs, ys, mode=MODE_STMOE):
+        _call("moe_decode_token", self.h, token, _p(xs), _p(ys), mode)
+
+    def last_routing(self):
+        idx = np.zeros((self.L, self.B, self.K), np.int32)
+        w = np.zeros((self.L, self.B, self.K), np.float32)
+        _call("moe_ctx_last_routing", self.h, idx.ctypes.data, w.ctypes.data)
+        return idx, w
+
+    def set_timing(self, on):
+        _call("moe_ctx_set_timing", self.h, int(on))
+
+    def timing(self):
+        """(gate/up kernel ms, down kernel ms, FFN calls, distinct routed experts) since set_timing(1)."""
+        up, down = C.c_double(), C.c_double()
+        nc, ne = i64(), i64()
+        _call("moe_ctx_timing", self.h, C.byref(up), C.byref(down), C.byref(nc), C.byref(ne))
+        return up.value, down.value, nc.value, ne.value

@@ -1,0 +1,106 @@
+"""The C-ABI library: it loads, exports every declared symbol, rejects invalid
+arguments before any device work, and its host-only cache policy makes the
+same decisions as the oracle's CacheSim."""
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle.stmoe_oracle import CacheSim
+
+S = pytest.importorskip("paper_2606_15453_amd.stmoe")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "stmoe.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", txt)) - {"sizeof"})
+
+
+def test_every_declared_symbol_is_exported_and_bound():
+    names = _declared()
+    assert "moe_route_topk" in names and "moe_decode_layer" in names
+    for n in names:
+        assert hasattr(S._lib, n), n
+    assert sorted(S.EXPORTED) == names
+
+
+def test_invalid_arguments_rejected_without_device_work():
+    # K > E, E > 256, H not a multiple of 8, null pointers
+    for args in [(16, 4096, 4, 8), (1, 4096, 300, 8), (1, 100, 8, 2), (0, 4096, 8, 2)]:
+        B, H, E, K = args
+        rc = S._lib.moe_route_topk(16, 16, B, H, E, K, S.BF16, 0, 16, 16, None, 16, 1 << 20, None)
+        assert rc == S.EINVAL
+    rc = S._lib.moe_route_topk(None, 16, 1, 64, 8, 2, S.BF16, 0, 16, 16, None, 16, 1 << 20, None)
+    assert rc == S.EINVAL
+    assert "null" in S._lib.stmoe_last_error().decode()
+    # workspace too small
+    rc = S._lib.moe_route_topk(16, 16, 1, 64, 8, 2, S.BF16, 0, 16, 16, None, 16, 4, None)
+    assert rc == S.EINVAL and "workspace" in S._lib.stmoe_last_error().decode()
+    rc = S._lib.moe_expert_ffn(16, 16, 16, 1, 2, 100, 64, 8, S.BF16, 16, None, 0, 16, 16, 1 << 20, None)
+    assert rc == S.EINVAL
+    rc = S._lib.moe_expert_ffn(16, 16, 16, 1, 2, 64, 64, 8, S.BF16, 16, None, 2, 16, 16, 1 << 20, None)
+    assert rc == S.EINVAL      # shared experts without pointers
+    assert S._lib.stmoe_predict(None, 0, None, 3, None, None, None, None, None) == S.EINVAL
+    assert S.blob_bytes(4096, 14336, S.BF16) == 3 * 4096 * 14336 * 2
+
+
+def test_pack_expert_is_concatenation():
+    rng = np.random.default_rng(0)
+    H, I = 16, 8
+    g, u, d = (rng.integers(0, 65535, size=s, dtype=np.uint16) for s in ((I, H), (I, H), (H, I)))
+    out = np.zeros(3 * H * I, np.uint16)
+    S.pack_expert(g, u, d, S.BF16, out)
+    assert np.array_equal(out, np.concatenate([g.ravel(), u.ravel(), d.ravel()]))
+
+
+def test_policy_hand_trace():
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "cache_trace.json")))
+    p = S.Policy(g["L"], g["E"], g["C"], g["warm"])
+    for st in g["steps"]:
+        if st["op"] == "A":
+            pairs, _ = p.acquire(0, st["set"], st["stamp"])
+            assert [list(x) for x in pairs if x[1] >= 0] == st["demand"]
+            assert [x[0] for x in pairs if x[1] < 0] == st["overflow"]
+        else:
+            assert [list(x) for x in p.prefetch(0, st["set"], st["stamp"])] == st["copies"]
+    assert p.slots().tolist() == g["final_slots"]
+    assert p.stats() == g["counts"]
+
+
+@pytest.mark.parametrize("E,C,K,L", [(8, 3, 2, 4), (128, 32, 8, 3), (64, 24, 6, 2), (16, 16, 4, 2)])
+def test_policy_matches_oracle_on_random_traces(E, C, K, L):
+    rng = np.random.default_rng(E * 100 + C)
+    warm = [sorted(rng.choice(E, size=C, replace=False).tolist()) for _ in range(L)]
+    ref = CacheSim(L, E, C, warm)
+    p = S.Policy(L, E, C, warm)
+    for t in range(60):
+        for l in range(L):
+            stamp = t * L + l + 1
+            B = int(rng.integers(1, 4))
+            U = sorted(set(rng.choice(E, size=min(E, K * B), replace=False).tolist()))
+            _, demand, overflow = ref.acquire(l, U, stamp)
+            pairs, _ = p.acquire(l, U, stamp)
+            assert [x for x in pairs if x[1] >= 0] == [tuple(d) for d in demand]
+            assert [x[0] for x in pairs if x[1] < 0] == overflow
+            n = int(rng.integers(0, min(E, 2 * K + 3)))
+            ranked = rng.permutation(E)[:n].tolist()
+            nl = (l + 1) % L
+            assert p.prefetch(nl, ranked, stamp) == [tuple(c) for c in ref.prefetch(nl, ranked, stamp)]
+    assert p.slots().tolist() == ref.slot
+    n = ref.n
+    assert p.stats() == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
+                             useful=n.useful, wasted=n.wasted)
+
+
+def test_policy_rejects_bad_lists():
+    p = S.Policy(2, 8, 3)
+    with pytest.raises(S.StmoeError):
+        p.acquire(0, [1, 1], 1)
+    with pytest.raises(S.StmoeError):
+        p.prefetch(0, [9], 1)
+    with pytest.raises(S.StmoeError):
+        p.acquire(5, [1], 1)

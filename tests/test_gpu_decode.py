@@ -1,0 +1,141 @@
+"""End-to-end parity of moe_decode_layer / moe_decode_token against the
+oracle's decode loop (Section 4.3.4): routing, predictor statistics, cache
+decisions and FFN outputs; prediction never changes the numbers."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+class Stack:
+    """Device copies of one synthetic MoE stack."""
+
+    def __init__(self, cfg):
+        import torch
+        from gpuhelp import DEV, blob_dev, to_dev
+        from paper_2606_15453_amd import workload as W
+        self.cfg = cfg
+        self.sel = W.planted_trace(cfg)
+        self.wg = [W.router_rows(cfg, l) for l in range(cfg.L)]
+        self.wg_dev = [to_dev(g) for g in self.wg]
+        self.blobs = [[blob_dev(cfg, l, e) for e in range(cfg.E)] for l in range(cfg.L)]
+        self.shared = [[blob_dev(cfg, l, s, shared=True) for s in range(cfg.n_shared)]
+                       for l in range(cfg.L)]
+        xs = [[W.to_storage(cfg, W.hidden_f64(cfg, self.sel, cfg.P + t, l)) for l in range(cfg.L)]
+              for t in range(cfg.T)]
+        self.x_store = xs
+        self.x_dev = [to_dev(np.stack(xs[t])) for t in range(cfg.T)]      # [L][B][H] per token
+        self.prof = W.profiling_selections(cfg, self.sel)
+        self.warm = W.warm_sets(cfg, self.prof)
+
+    def shared_ptrs(self):
+        return [s.data_ptr() for l in range(self.cfg.L) for s in self.shared[l]]
+
+
+def _oracle(st, mode, C=None, ffn_tokens=0):
+    from gpuhelp import expert_f64
+    from oracle.stmoe_oracle import decode_reference, decode_storage, moe_ffn
+    cfg = st.cfg
+
+    def ffn_of(l):
+        sh = [expert_f64(cfg, l, s, shared=True) for s in range(cfg.n_shared)]
+        return lambda x, idx, w: moe_ffn(x, idx, w, lambda e: expert_f64(cfg, l, e), shared=sh)
+
+    return decode_reference(cfg.L, cfg.E, cfg.K, cfg.B, lambda t, l: decode_storage(st.x_store[t][l]),
+                            lambda l: decode_storage(st.wg[l]), st.prof, cfg.T, C=C,
+                            warm=None if C is None else st.warm, mode=mode, ffn_of=ffn_of,
+                            ffn_tokens=ffn_tokens)
+
+
+def _run_gpu(st, mode, capped):
+    import torch
+    from gpuhelp import DEV, storage_dtype
+    from paper_2606_15453_amd import stmoe as S
+    cfg = st.cfg
+    pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+    pred.profile(st.prof)
+    stream = torch.cuda.current_stream()
+    cache = None
+    keep = []
+    if capped:
+        host = []
+        for l in range(cfg.L):
+            for e in range(cfg.E):
+                h = st.blobs[l][e].cpu().pin_memory()
+                keep.append(h)
+                host.append(h.data_ptr())
+        n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
+        arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage),
+                            dtype=torch.uint8, device=DEV)
+        demand, side = torch.cuda.Stream(), torch.cuda.Stream()
+        keep += [arena, demand, side]
+        cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, cfg.blob_bytes, n_stage, arena, host, demand, side)
+        cache.warm(st.warm)
+        ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
+                              [g.data_ptr() for g in st.wg_dev], predictor=pred, cache=cache,
+                              shared_ptrs=st.shared_ptrs(), n_shared=cfg.n_shared, stream=stream)
+    else:
+        resident = [st.blobs[l][e].data_ptr() for l in range(cfg.L) for e in range(cfg.E)]
+        ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
+                              [g.data_ptr() for g in st.wg_dev], predictor=pred,
+                              resident_ptrs=resident, shared_ptrs=st.shared_ptrs(),
+                              n_shared=cfg.n_shared, stream=stream)
+    idx_hist, ys = [], []
+    for t in range(cfg.T):
+        y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device=DEV)
+        ctx.token(t, st.x_dev[t], y, mode=mode)
+        idx, _ = ctx.last_routing()
+        idx_hist.append(idx)
+        ys.append(y.cpu().numpy())
+    stats = pred.stats()
+    cst = cache.stats() if cache else None
+    ctx.close()
+    if cache:
+        cache.close()
+    pred.close()
+    return idx_hist, ys, stats, cst
+
+
+CFGS = [("tiny", dict(T=12)), ("qwen30b", dict(L=4, T=6, P=3, C=10)),
+        ("dsv2lite", dict(L=3, T=5, P=2, C=12)), ("qwen30b-b8", dict(L=3, T=4, P=2, C=40))]
+
+
+@pytest.mark.parametrize("name,over", CFGS)
+def test_decode_resident_matches_oracle(name, over):
+    from gpuhelp import rel_l2
+    from oracle.stmoe_oracle import MODE_STMOE
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    ref = _oracle(st, MODE_STMOE, ffn_tokens=cfg.T)
+    assert ref["tie_boundary"] == 0
+    idx_hist, ys, stats, _ = _run_gpu(st, 1, capped=False)
+    for t in range(cfg.T):
+        for l in range(cfg.L):
+            r = ref["idx"][t * cfg.L + l]
+            for b in range(cfg.B):
+                assert sorted(idx_hist[t][l][b].tolist()) == sorted(r[b].tolist())
+            err = rel_l2(ys[t][l], ref["y"][(t, l)])
+            assert err <= 1e-2, (t, l, err)
+    # hit statistics per layer: (hits, |A|, |P|)
+    assert np.array_equal(stats[:, 0], ref["hits"].sum(axis=0))
+    assert np.array_equal(stats[:, 2], ref["npred"].sum(axis=0))
+
+
+@pytest.mark.parametrize("name,over", CFGS)
+@pytest.mark.parametrize("mode", [0, 1, 2, 3])
+def test_decode_capped_counts_and_invariance(name, over, mode):
+    """At the capped budget the cache makes the oracle's decisions, and the
+    outputs are bit-identical to the all-resident run whatever the mode."""
+    from oracle.stmoe_oracle import decode_reference
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    idx_hist, ys, stats, cst = _run_gpu(st, mode, capped=True)
+    for t in range(cfg.T):
+        assert np.array_equal(ys[t], ys_res[t])
+    ref = _oracle(st, mode, C=cfg.C)
+    n = ref["cache"].n
+    assert cst == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
+                       useful=n.useful, wasted=n.wasted)

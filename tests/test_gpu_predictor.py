@@ -1,0 +1,133 @@
+"""GPU parity of the predictor kernels (Algorithms 1-3, Eq. 1): tables,
+scores, masks, ranked lists and hit statistics, bit-exact against the oracle
+on the same seeded index streams."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _run(L, E, K, B, prof, stream_sel, use=3, online=True):
+    """Drive GPU and oracle predictors with the same selections; compare every step."""
+    import torch
+    from gpuhelp import DEV, i32
+    from oracle.stmoe_oracle import STPredictor
+    from paper_2606_15453_amd import stmoe as S
+    ref = STPredictor(L, E, K, B)
+    ref.profile(prof)
+    gp = S.Predictor(L, E, K, B)
+    gp.profile(prof)
+    co, ci, cc, ht = gp.export()
+    rco, rci, rcc, rht = ref.tables()
+    assert np.array_equal(co, rco) and np.array_equal(ci, rci) and np.array_equal(cc, rcc)
+    assert np.array_equal(ht, rht)
+    score = torch.zeros((B, E), dtype=torch.uint8, device=DEV)
+    mask = torch.zeros(E, dtype=torch.uint8, device=DEV)
+    ranked = torch.zeros(E, dtype=torch.int32, device=DEV)
+    nr = torch.zeros(1, dtype=torch.int32, device=DEV)
+    use_cct, use_ht = bool(use & 1), bool(use & 2)
+
+    def check_pred(sc_ref):
+        torch.cuda.synchronize()
+        assert np.array_equal(score.cpu().numpy(), sc_ref)
+        assert np.array_equal(mask.cpu().numpy(), (sc_ref.max(axis=0) >= 2).astype(np.uint8))
+        rr = STPredictor.ranked_union(sc_ref)
+        assert int(nr.item()) == len(rr)
+        r = ranked.cpu().numpy()
+        assert r[:len(rr)].tolist() == rr and np.all(r[len(rr):] == -1)
+
+    gp.predict(-1, None, use=use & 2, score=score, mask=mask, ranked=ranked, n_ranked=nr)
+    sc = ref.predict(-1, None, use_cct=False, use_ht=use_ht)
+    check_pred(sc)
+    hits = np.zeros((L, 3), np.int64)
+    pend = {0: sc}
+    for t in range(stream_sel.shape[0]):
+        prev_ref = prev_dev = None
+        for l in range(L):
+            cur = [sorted(int(v) for v in stream_sel[t, b, l]) for b in range(B)]
+            cur_dev = i32(stream_sel[t, :, l, :])
+            ps = STPredictor.prefetch_sets(pend[l])
+            hits[l, 0] += sum(len(set(cur[b]) & set(ps[b])) for b in range(B))
+            hits[l, 1] += B * K
+            hits[l, 2] += sum(len(p) for p in ps)
+            gp.update(l, prev_dev, cur_dev, online=online)
+            ref.update(l, prev_ref, cur, online=online)
+            if l + 1 < L:
+                gp.predict(l, cur_dev, use=use, score=score, mask=mask, ranked=ranked, n_ranked=nr)
+                sc = ref.predict(l, cur, use_cct=use_cct, use_ht=use_ht)
+                pend[l + 1] = sc
+            else:
+                gp.predict(-1, None, use=use & 2, score=score, mask=mask, ranked=ranked, n_ranked=nr)
+                sc = ref.predict(-1, None, use_cct=False, use_ht=use_ht)
+                pend[0] = sc
+            check_pred(sc)
+            prev_ref, prev_dev = cur, cur_dev
+        _, ci, cc, ht = gp.export()
+        _, rci, rcc, rht = ref.tables()
+        assert np.array_equal(ci, rci), f"CCT indices differ after token {t}"
+        assert np.array_equal(cc, rcc), f"CCT confidences differ after token {t}"
+        assert np.array_equal(ht, rht)
+    assert np.array_equal(gp.stats(), hits)
+    gp.close()
+
+
+def test_worked_example_on_gpu():
+    g = json.load(open(os.path.join(GOLD, "predictor_worked_example.json")))
+    prof = np.array([[[tok[0], tok[1]]] for tok in g["profiling"]], np.int32)
+    dec = np.array([[[s["A0"], s["A1"]]] for s in g["decode"]], np.int32)
+    _run(g["L"], g["E"], g["K"], g["B"], prof, dec)
+
+
+@pytest.mark.parametrize("name,L,T,B", [("tiny", 4, 24, 1), ("qwen30b", 5, 12, 1),
+                                        ("qwen30b-b8", 3, 8, 8), ("dsv2lite", 4, 10, 4),
+                                        ("qwen235b", 3, 4, 16)])
+def test_planted_trace_parity(name, L, T, B):
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(L=L, T=T, P=max(2, T // 4), B=B)
+    sel = W.planted_trace(cfg)
+    _run(cfg.L, cfg.E, cfg.K, cfg.B, sel[:cfg.P], sel[cfg.P:])
+
+
+@pytest.mark.parametrize("use", [1, 2])
+def test_ablation_sources(use):
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen30b"].scaled(L=4, T=8, P=3, B=2)
+    sel = W.planted_trace(cfg)
+    _run(cfg.L, cfg.E, cfg.K, cfg.B, sel[:cfg.P], sel[cfg.P:], use=use)
+
+
+def test_online_update_off_keeps_cct():
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["tiny"].scaled(T=10, P=4)
+    sel = W.planted_trace(cfg)
+    _run(cfg.L, cfg.E, cfg.K, cfg.B, sel[:cfg.P], sel[cfg.P:], online=False)
+
+
+def test_random_uniform_stream_max_sizes():
+    """E = 256, K = 16, B = 16: the widest tables and the most slots per row."""
+    rng = np.random.default_rng(4)
+    L, E, K, B = 3, 256, 16, 16
+    sel = np.stack([np.stack([np.stack([rng.choice(E, K, replace=False) for _ in range(L)])
+                              for _ in range(B)]) for _ in range(6)]).astype(np.int32)
+    _run(L, E, K, B, sel[:2], sel[2:])
+
+
+def test_import_export_roundtrip():
+    from paper_2606_15453_amd import stmoe as S
+    rng = np.random.default_rng(1)
+    L, E, K, B = 3, 16, 4, 2
+    p = S.Predictor(L, E, K, B)
+    ci = np.stack([np.stack([rng.choice(E, K, replace=False) for _ in range(E)]) for _ in range(L - 1)])
+    cc = rng.integers(0, 4, size=(L - 1, E, K))
+    ht = np.sort(np.stack([np.stack([rng.choice(E, K, replace=False) for _ in range(B)])
+                           for _ in range(L)]), axis=2)
+    p.import_tables(ci, cc, ht)
+    _, ci2, cc2, ht2 = p.export()
+    assert np.array_equal(ci2, ci) and np.array_equal(cc2, cc) and np.array_equal(ht2, ht)
+    with pytest.raises(S.StmoeError):
+        p.import_tables(ci, np.full_like(cc, 4), ht)

@@ -1,0 +1,340 @@
+"""Decode-step MoE benchmark on one MI355X.
+
+One step = one decode token through every MoE layer of the stack: router GEMV
++ softmax top-k, predictor verify/update and next-layer prediction, expert
+residency, and the bf16 SwiGLU expert FFN.  Inputs (router rows, expert
+weights, every token's hidden states) are resident in HBM before timing.
+
+Default workload: the Mixtral-8x7B-shaped stack (32 layers, hidden 4096,
+intermediate 14336, 8 experts top-2, bf16, batch 1), seeded synthetic data.
+
+Besides the timed HBM-resident run the JSON line carries:
+  roofline      the gate/up FFN kernel's algorithmic bytes per launch over its
+                event-timed average duration, against 8 TB/s
+  offload       the same stack with the HBM cache capped (3 experts per layer
+                for Mixtral shapes) and the other experts in pinned host
+                memory: decode tokens/s on demand and with prediction-driven
+                prefetch, stall per token, predictor hit rates, cache counts
+  cpu_baseline  the CPU oracle timed on a bounded sample of the same workload
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config mixtral]
+                       [--offload-tokens N] [--cpu-tokens S]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="mixtral")
+    ap.add_argument("--offload-tokens", type=int, default=16,
+                    help="decode tokens per capped-cache mode (0 skips the offload runs)")
+    ap.add_argument("--pinned-gb", type=float, default=56.0,
+                    help="pinned host pool budget; larger stacks alias experts onto it")
+    ap.add_argument("--cpu-tokens", type=int, default=2,
+                    help="decode tokens of the CPU oracle sample (0 skips it)")
+    return ap.parse_args()
+
+
+class Workload:
+    """Seeded synthetic inputs of one config, placed in HBM."""
+
+    def __init__(self, cfg):
+        import torch
+        from paper_2606_15453_amd import stmoe as S
+        from paper_2606_15453_amd import workload as W
+        self.cfg = cfg
+        dev = "cuda:0"
+        self.dt = S.BF16 if cfg.dtype == "bf16" else S.F32
+        tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+        t0 = time.time()
+        self.sel = W.planted_trace(cfg)
+        self.prof = W.profiling_selections(cfg, self.sel)
+        self.warm = W.warm_sets(cfg, self.prof)
+        log(f"planted trace {self.sel.shape} in {time.time() - t0:.1f}s")
+        t0 = time.time()
+        self.wg_f64 = [W.router_rows_f64(cfg, l) for l in range(cfg.L)]
+        self.wg = [self._dev(W.to_storage(cfg, g)) for g in self.wg_f64]
+        xs = np.stack([np.stack([W.to_storage(cfg, W.hidden_f64(cfg, self.sel, cfg.P + t, l, self.wg_f64[l]))
+                                 for l in range(cfg.L)]) for t in range(cfg.T)])
+        self.x_store = xs
+        self.x = self._dev(xs)                              # [T][L][B][H]
+        log(f"router rows + hidden states in {time.time() - t0:.1f}s")
+        t0 = time.time()
+        self.blobs = torch.empty((cfg.L * cfg.E, cfg.blob_elems), dtype=tdt, device=dev)
+        for l in range(cfg.L):
+            for e in range(cfg.E):
+                W.expert_blob_torch(cfg, l, e, self.blobs[l * cfg.E + e])
+        self.shared = None
+        if cfg.n_shared:
+            self.shared = torch.empty((cfg.L * cfg.n_shared, cfg.blob_elems), dtype=tdt, device=dev)
+            for l in range(cfg.L):
+                for s in range(cfg.n_shared):
+                    W.expert_blob_torch(cfg, l, s, self.shared[l * cfg.n_shared + s], shared=True)
+        torch.cuda.synchronize()
+        gb = self.blobs.numel() * self.blobs.element_size() / 1e9
+        log(f"{cfg.L * cfg.E} expert blobs ({gb:.1f} GB) generated in HBM in {time.time() - t0:.1f}s")
+
+    @staticmethod
+    def _dev(a):
+        import torch
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to("cuda:0").view(torch.bfloat16)
+        return torch.from_numpy(a).to("cuda:0")
+
+    def blob_ptr(self, l, e):
+        return self.blobs[l * self.cfg.E + e].data_ptr()
+
+    def shared_ptrs(self):
+        if self.shared is None:
+            return None
+        return [self.shared[i].data_ptr() for i in range(self.shared.shape[0])]
+
+
+def make_ctx(wl, pred, cache=None):
+    from paper_2606_15453_amd import stmoe as S
+    cfg = wl.cfg
+    resident = None if cache else [wl.blob_ptr(l, e) for l in range(cfg.L) for e in range(cfg.E)]
+    return S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, wl.dt, [g.data_ptr() for g in wl.wg],
+                           predictor=pred, cache=cache, resident_ptrs=resident,
+                           shared_ptrs=wl.shared_ptrs(), n_shared=cfg.n_shared)
+
+
+def run_tokens(ctx, wl, first, n, y, mode):
+    T = wl.cfg.T
+    for i in range(n):
+        t = first + i
+        ctx.token(t, wl.x[t % T], y, mode=mode)
+
+
+def hbm_resident(wl, steps, warmup):
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    cfg = wl.cfg
+    pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+    pred.profile(wl.prof)
+    ctx = make_ctx(wl, pred)
+    y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
+    run_tokens(ctx, wl, 0, warmup, y, S.MODE_STMOE)
+    torch.cuda.synchronize()
+    ctx.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run_tokens(ctx, wl, warmup, steps, y, S.MODE_STMOE)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    up_ms, down_ms, n_calls, n_exp = ctx.timing()
+    stats = pred.stats()
+    ctx.close()
+    pred.close()
+    return dict(seconds=dt, up_ms=up_ms, down_ms=down_ms, n_calls=n_calls, n_experts=n_exp, stats=stats)
+
+
+def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
+    """Capped HBM cache over a pinned host pool: on-demand vs ST-MoE prefetch.
+
+    The pool holds M = min(L*E, pinned budget / blob) distinct blobs; expert
+    (l, e) is copied from pool slot (l*E + e) mod M.  Every copy still moves a
+    whole blob over PCIe, so the timing is that of distinct experts."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    cfg = wl.cfg
+    blob = cfg.blob_bytes
+    n_all = cfg.L * cfg.E
+    M = min(n_all, int(pinned_gb * 1e9) // blob)
+    t0 = time.time()
+    pool = S.PinnedHost(M * blob)
+    host = pool.tensor()
+    for i in range(M):
+        host[i * blob:(i + 1) * blob].copy_(wl.blobs[i].view(torch.uint8))
+    log(f"pinned host pool {pool.nbytes / 1e9:.1f} GB ({M} of {n_all} blobs) filled in {time.time() - t0:.1f}s")
+    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
+    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, blob, n_stage), dtype=torch.uint8, device="cuda:0")
+    demand, side = torch.cuda.Stream(), torch.cuda.Stream()
+    ptrs = [pool.ptr + (i % M) * blob for i in range(n_all)]
+    y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
+    out = {}
+    for name, mode in (("on_demand", S.MODE_ON_DEMAND), ("st_moe", S.MODE_STMOE)):
+        cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, blob, n_stage, arena, ptrs, demand, side)
+        cache.warm(wl.warm)
+        pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+        pred.profile(wl.prof)
+        ctx = make_ctx(wl, pred, cache)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run_tokens(ctx, wl, 0, n_tokens, y, mode)
+        torch.cuda.synchronize()
+        demand.synchronize()
+        side.synchronize()
+        dt = time.perf_counter() - t0
+        cst = cache.stats()
+        st = pred.stats()
+        copies = cst["demand"] + cst["overflow"] + cst["prefetch"]
+        rec = dict(tokens=n_tokens, seconds=round(dt, 4),
+                   tokens_per_s=round(cfg.B * n_tokens / dt, 3),
+                   ms_per_token=round(1e3 * dt / n_tokens, 3),
+                   stall_ms_per_token=round(1e3 * dt / n_tokens - resident_ms_per_token, 3),
+                   h2d_copies=copies, h2d_gbps=round(copies * blob / dt / 1e9, 2), cache=cst)
+        if mode != S.MODE_ON_DEMAND:
+            rec["recall_layers_ge1"] = round(float(st[1:, 0].sum() / max(st[1:, 1].sum(), 1)), 4)
+            rec["recall_layer0"] = round(float(st[0, 0] / max(st[0, 1], 1)), 4)
+            rec["precision"] = round(float(st[:, 0].sum() / max(st[:, 2].sum(), 1)), 4)
+            rec["mean_predicted_per_row"] = round(float(st[:, 2].sum() / max(st[:, 1].sum() / cfg.K, 1)), 3)
+        out[name] = rec
+        log(f"offload {name}: {rec['tokens_per_s']} tok/s, {rec['ms_per_token']} ms/token, cache {cst}")
+        ctx.close()
+        pred.close()
+        cache.close()
+    od, st = out["on_demand"]["stall_ms_per_token"], out["st_moe"]["stall_ms_per_token"]
+    out["stall_reduction"] = round(1.0 - st / od, 4) if od > 0 else None
+    out["cache_slots_per_layer"] = cfg.C
+    out["host_pool"] = {"distinct_blobs": M, "experts": n_all, "slot_of_expert": "(l*E + e) mod distinct_blobs"}
+    out["h2d_link"] = "PCIe, pinned host memory, hipMemcpyAsync on demand/side streams"
+    del arena
+    pool.close()
+    return out
+
+
+def cpu_baseline(wl, n_tokens):
+    """The CPU oracle on the first n_tokens decode tokens of the same workload.
+
+    Timed: routing, predictor update/predict, cache policy and the fp64 FFN of
+    every layer.  Not timed: preparing each layer's fp64 expert matrices (the
+    generator's GPU backend, copied to the host)."""
+    import torch
+    from oracle.stmoe_oracle import STPredictor, CacheSim, decode_storage, moe_ffn, route
+    cfg = wl.cfg
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    pred = STPredictor(cfg.L, cfg.E, cfg.K, cfg.B)
+    pred.profile(wl.prof)
+    cache = CacheSim(cfg.L, cfg.E, cfg.C, wl.warm)
+    P_cur = pred.predict(-1, None)
+    timed = 0.0
+    n, Hh, Ii = cfg.H * cfg.I, cfg.H, cfg.I
+
+    def mats(blob):
+        b = blob.to(torch.float64).cpu().numpy()
+        return b[:n].reshape(Ii, Hh), b[n:2 * n].reshape(Ii, Hh), b[2 * n:].reshape(Hh, Ii)
+
+    for t in range(n_tokens):
+        prev = None
+        for l in range(cfg.L):
+            x = decode_storage(wl.x_store[t][l])
+            t0 = time.perf_counter()
+            r = route(x, wl.wg_f64[l], cfg.K)
+            cur = [sorted(int(v) for v in r["idx"][b]) for b in range(cfg.B)]
+            pred.update(l, prev, cur)
+            P_next = pred.predict(l, cur) if l + 1 < cfg.L else pred.predict(-1, None)
+            U = sorted(set(v for s in cur for v in s))
+            cache.acquire(l, U, t * cfg.L + l + 1)
+            timed += time.perf_counter() - t0
+            experts = {e: mats(wl.blobs[l * cfg.E + e]) for e in U}
+            shared = [mats(wl.shared[l * cfg.n_shared + s]) for s in range(cfg.n_shared)]
+            t0 = time.perf_counter()
+            moe_ffn(x, r["idx"], r["w"], lambda e: experts[e], shared=shared)
+            cache.prefetch((l + 1) % cfg.L, STPredictor.ranked_union(P_next), t * cfg.L + l + 1)
+            timed += time.perf_counter() - t0
+            prev, P_cur = cur, P_next
+            del experts
+    return dict(value=round(cfg.B * n_tokens / timed, 4), unit="tokens/s", cores=int(cores),
+                kind="oracle", seconds=round(timed, 3),
+                sample=f"first {n_tokens} decode token(s) x {cfg.L} layers x batch {cfg.B} of the same "
+                       f"workload: fp64 routing, predictor, cache policy and SwiGLU FFN (expert matrix "
+                       f"preparation not timed)")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (this build has no "
+              f"multi-GPU path)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_15453_amd import workload as W
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    cfg = W.CONFIGS[args.config]
+    log(f"workload {cfg.name}")
+    wl = Workload(cfg)
+    r = hbm_resident(wl, args.steps, args.warmup)
+    ms_per_step = 1e3 * r["seconds"] / args.steps
+    value = cfg.B * args.steps / r["seconds"]
+    log(f"HBM-resident: {value:.2f} tok/s, {ms_per_step:.3f} ms/token")
+    esz = cfg.wbytes
+    up_bytes = r["n_experts"] * 2 * cfg.H * cfg.I * esz + r["n_calls"] * cfg.n_shared * 2 * cfg.H * cfg.I * esz
+    dn_bytes = r["n_experts"] * cfg.H * cfg.I * esz + r["n_calls"] * cfg.n_shared * cfg.H * cfg.I * esz
+    up_gbps = up_bytes / (r["up_ms"] * 1e-3) / 1e9
+    dn_gbps = dn_bytes / (r["down_ms"] * 1e-3) / 1e9
+    ffn_gbps = (up_bytes + dn_bytes) / ((r["up_ms"] + r["down_ms"]) * 1e-3) / 1e9
+    stats = r["stats"]
+    out = {
+        "metric": "MoE decode tokens/s; expert-weight HBM GB/s vs peak; prefetch hit rate",
+        "value": round(value, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "accum_dtype": "f32",
+        "data": "synthetic (seeded planted-Markov routing, N(0, 0.02) expert weights)",
+        "config": {"workload": cfg.name, "layers": cfg.L, "hidden": cfg.H, "intermediate": cfg.I,
+                   "experts": cfg.E, "shared_experts": cfg.n_shared, "top_k": cfg.K, "global_batch": cfg.B,
+                   "mode": "all experts HBM-resident, ST-MoE predictor on", "parallelism": "none (1 GPU)"},
+        "roofline": {
+            "bound": "hbm", "kernel": "ffn_gate_up",
+            "achieved": round(up_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(up_gbps / PEAK_HBM_GBPS, 4), "traffic": None,
+            "bytes_per_launch": int(up_bytes / max(r["n_calls"], 1)),
+            "avg_launch_us": round(1e3 * r["up_ms"] / max(r["n_calls"], 1), 3),
+            "launches": r["n_calls"],
+        },
+        "ffn_down": {"achieved_gbps": round(dn_gbps, 1), "frac": round(dn_gbps / PEAK_HBM_GBPS, 4),
+                     "avg_launch_us": round(1e3 * r["down_ms"] / max(r["n_calls"], 1), 3)},
+        "ffn_hbm_gbps": round(ffn_gbps, 1),
+        "step_hbm_gbps": round((up_bytes + dn_bytes) / r["seconds"] / 1e9, 1),
+        "prediction": {
+            "recall_layers_ge1": round(float(stats[1:, 0].sum() / max(stats[1:, 1].sum(), 1)), 4),
+            "recall_layer0": round(float(stats[0, 0] / max(stats[0, 1], 1)), 4),
+            "precision": round(float(stats[:, 0].sum() / max(stats[:, 2].sum(), 1)), 4),
+        },
+    }
+    if args.offload_tokens > 0:
+        out["offload"] = offload(wl, args.offload_tokens, ms_per_step, args.pinned_gb)
+    if args.cpu_tokens > 0:
+        t0 = time.time()
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
+        log(f"cpu baseline {out['cpu_baseline']['value']} tok/s in {time.time() - t0:.1f}s wall")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

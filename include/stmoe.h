@@ -54,6 +54,12 @@ const char* stmoe_last_error(void);
 /* ABI version of this header: 1. */
 int stmoe_abi_version(void);
 
+/* Pinned host memory for the expert pool (exact size, hipHostMalloc; not
+ * rounded up the way caching allocators do).  The caller owns the block
+ * and releases it with stmoe_host_free.  [sync] */
+int stmoe_host_alloc(size_t bytes, void** out);
+int stmoe_host_free(void* p);
+
 /* ------------------------------------------------------------------------
  * Gating (Section 2): z[b][e] = sum_h x[b][h] * w_gate[e][h] (fp32
  * accumulation), s = softmax(z[b]), top-K experts by logit (descending,

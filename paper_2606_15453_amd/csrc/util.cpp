@@ -18,6 +18,24 @@ extern "C" const char* stmoe_last_error(void) { return g_last_error.c_str(); }
 
 extern "C" int stmoe_abi_version(void) { return 1; }
 
+extern "C" int stmoe_host_alloc(size_t bytes, void** out) {
+    clear_error();
+    STMOE_CHECK(out && bytes > 0, "null output or zero size");
+    *out = nullptr;
+    const hipError_t e = hipHostMalloc(out, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        set_error(std::string("stmoe_host_alloc: ") + hipGetErrorString(e));
+        return e == hipErrorOutOfMemory ? STMOE_ENOMEM : STMOE_EHIP;
+    }
+    return STMOE_OK;
+}
+
+extern "C" int stmoe_host_free(void* p) {
+    clear_error();
+    if (p) STMOE_HIP(hipHostFree(p));
+    return STMOE_OK;
+}
+
 extern "C" size_t moe_blob_bytes(int H, int I, int dtype) {
     if (H < 1 || I < 1 || (dtype != STMOE_BF16 && dtype != STMOE_F32)) return 0;
     return size_t(3) * H * I * (dtype == STMOE_BF16 ? 2 : 4);

@@ -63,6 +63,8 @@ class ModelDesc(C.Structure):
 _SIGS = {
     "stmoe_last_error": (C.c_char_p, []),
     "stmoe_abi_version": (i32, []),
+    "stmoe_host_alloc": (i32, [sz, P(vp)]),
+    "stmoe_host_free": (i32, [vp]),
     "moe_route_workspace_bytes": (sz, [i32, i32]),
     "moe_route_topk": (i32, [vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]),
     "stmoe_create": (i32, [i32, i32, i32, i32, P(vp)]),
@@ -148,6 +150,32 @@ def _i32(a):
 
 def abi_version() -> int:
     return _lib.stmoe_abi_version()
+
+
+class PinnedHost:
+    """A pinned host block of exactly `nbytes` (stmoe_host_alloc), viewable as a
+    CPU uint8 tensor; freed on close()."""
+
+    def __init__(self, nbytes):
+        p = vp()
+        _call("stmoe_host_alloc", nbytes, C.byref(p))
+        self.ptr, self.nbytes = p.value, nbytes
+
+    def tensor(self, offset=0, nbytes=None):
+        n = self.nbytes - offset if nbytes is None else nbytes
+        buf = (C.c_uint8 * n).from_address(self.ptr + offset)
+        return torch.frombuffer(buf, dtype=torch.uint8)
+
+    def close(self):
+        if self.ptr:
+            _lib.stmoe_host_free(self.ptr)
+            self.ptr = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 # ---------------------------------------------------------------- gating

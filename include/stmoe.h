@@ -177,10 +177,15 @@ int moe_pack_expert(const void* w_gate, const void* w_up, const void* w_down, in
  *                experts' entries are read
  *   shared_ptrs  device array [n_shared] of device blob pointers, or NULL
  *   y            device out [B][H] fp32 (overwritten)
- *   ws           device workspace, moe_expert_ffn_workspace_bytes(...) bytes
- *   B < 8 runs the GEMV kernels; B >= 8 the MFMA grouped-GEMM kernels.
+ *   ws           device workspace of moe_expert_ffn_workspace_bytes(...) bytes,
+ *                256-byte aligned, zero-filled by the caller once before its
+ *                first use (it holds completion tickets that every call leaves
+ *                at zero); calls sharing a workspace must be ordered on one stream
+ *   B < 8 runs the GEMV kernels; B >= 8 with bf16 and H, I multiples of 64
+ *   runs the MFMA grouped-GEMM kernels (the SwiGLU activation then passes
+ *   through bf16); other shapes fall back to the GEMV kernels.
  * ---------------------------------------------------------------------- */
-size_t moe_expert_ffn_workspace_bytes(int B, int K, int E, int I, int n_shared);
+size_t moe_expert_ffn_workspace_bytes(int B, int K, int E, int H, int I, int n_shared, int dtype);
 int moe_expert_ffn(const void* x, const int32_t* topk_idx, const float* topk_w, int B, int K,
                    int H, int I, int E, int dtype, const void* const* expert_ptrs,
                    const void* const* shared_ptrs, int n_shared, float* y, void* ws,

@@ -160,7 +160,7 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     c->host_table.assign(c->E, nullptr);
     const size_t LBK = size_t(c->L) * c->B * c->K;
     c->route_ws_bytes = moe_route_workspace_bytes(c->B, c->E);
-    c->ffn_ws_bytes = moe_expert_ffn_workspace_bytes(c->B, c->K, c->E, c->I, c->n_shared);
+    c->ffn_ws_bytes = moe_expert_ffn_workspace_bytes(c->B, c->K, c->E, c->H, c->I, c->n_shared, c->dtype);
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMalloc(&c->idx, LBK * sizeof(int32_t));
     if (e == hipSuccess) e = hipMalloc(&c->w, LBK * sizeof(float));
@@ -174,6 +174,7 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     if (e == hipSuccess) e = hipHostMalloc(&c->rec, size_t(c->B * c->K + c->E + 1) * sizeof(int32_t));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->rec_ev, hipEventDisableTiming);
     if (e == hipSuccess) e = hipMemset(c->route_ws, 0, c->route_ws_bytes);
+    if (e == hipSuccess) e = hipMemset(c->ffn_ws, 0, c->ffn_ws_bytes);
     if (e == hipSuccess) e = hipMemset(c->idx, 0, LBK * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(c->w, 0, LBK * sizeof(float));
     if (e == hipSuccess) e = hipMemset(c->tables, 0, size_t(c->L) * c->E * sizeof(void*));

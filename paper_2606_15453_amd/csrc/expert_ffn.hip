@@ -2,25 +2,32 @@
 //   y[b] = sum over selected experts e of w[b][e] * W_down_e (silu(W_gate_e x_b) * (W_up_e x_b))
 //        + the same with weight 1 for shared experts.
 //
-// Decode is bandwidth-bound: every selected expert's weights are streamed
-// from HBM once per call, at about 2 flops per weight byte per token.  Two
-// kernels, both reading 16-byte weight chunks with non-temporal loads:
+// Decode is bandwidth-bound (about 2 flops per weight byte per token), so
+// every kernel here streams each selected expert's weights from HBM exactly
+// once, as 16-byte non-temporal loads, and is priced against 8 TB/s.
 //
-//   ffn_gate_up  one workgroup = (expert slot, 8*R rows of W_gate and W_up).
-//                A group of G lanes owns R rows; each lane strides over the
-//                row's 16-byte chunks, dots them with the tokens' activations
-//                (cache-resident), and the G-lane segment sums give g and u.
-//                a = w_b * silu(g) * u goes to the workspace [slot][b][I].
-//   ffn_down     one workgroup = a block of output rows h.  For each slot in
-//                ascending expert order (shared experts last) it streams row h
-//                of W_down and dots it with a[slot][b][*]; partial sums stay in
-//                registers across slots, so y is written once, with a fixed
-//                summation order (the result does not depend on where the
-//                blobs live).
+// Two phases, two launches:
+//   gate/up  one workgroup = (expert slot, block of rows of W_gate and W_up):
+//            a[slot][b][i] = w_b * silu(W_gate[i] . x_b) * (W_up[i] . x_b)
+//   down     one workgroup = (block of output rows h, group of expert slots):
+//            sum over the group's slots (ascending expert index, shared
+//            experts last) of W_down_slot[h] . a[slot][b].  With more than one
+//            group the groups' partial sums go to the workspace and the last
+//            workgroup of each row block (a completion ticket) adds them in
+//            group order, so the summation order depends only on the routing.
 //
-// Both kernels rebuild the slot plan (distinct selected experts ascending,
-// their token masks and weights) from topk_idx/topk_w in LDS; no host
-// round trip and no separate planning launch.
+// Batch < 8: GEMV kernels.  A group of G lanes (64, 32 or 16, by row length)
+// owns R rows and strides over their 16-byte chunks; the activations come
+// from L1/L2; DPP / shuffle segment sums reduce.  For long down rows the
+// whole workgroup strides one row block (split-K over its four waves).
+// Batch >= 8: MFMA kernels (v_mfma_f32_16x16x32_bf16).  The tokens form the
+// 16-row A operand (padded with zeros), 16 weight rows the B operand; each
+// lane loads 32 contiguous bytes of one row per 64-element step, so a wave
+// reads 16 rows x 128 B per step.  The SwiGLU activation goes through bf16.
+//
+// Every kernel rebuilds the slot plan (distinct selected experts ascending,
+// token masks) from topk_idx/topk_w in LDS: no host round trip, no planning
+// launch.
 #include "common.h"
 
 namespace stmoe {
@@ -30,27 +37,34 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxShared = 8;
 constexpr int kMaxSlots = kMaxE + kMaxShared;
+constexpr int kDownWgTarget = 1024;   // workgroups the down phase aims for
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct FfnArgs {
-    const void* x;               // [B][H]
-    const int32_t* idx;          // [B][K]
-    const float* w;              // [B][K]
-    const void* const* eptr;     // [E] device blob pointers
-    const void* const* sptr;     // [n_shared] or null
+    const void* x;                   // [B][H]
+    const int32_t* idx;              // [B][K]
+    const float* w;                  // [B][K]
+    const void* const* eptr;         // [E] device blob pointers
+    const void* const* sptr;         // [n_shared] or null
     int B, K, H, I, E, n_shared;
-    float* act;                  // [slots][B][I]
-    float* y;                    // [B][H]
+    void* act;                       // [slots][B][I]: fp32 (GEMV) or bf16 (MFMA)
+    float* part;                     // [ng][B][H] partial sums (ng > 1)
+    unsigned* tick;                  // [row blocks] completion tickets, zero between launches
+    float* y;                        // [B][H]
     unsigned long long* n_experts;   // optional: += distinct routed experts (block 0)
+    int ng, spg;                     // expert-slot groups of the down phase, slots per group
 };
 
 struct Plan {
     int32_t idx[kMaxB * kMaxK];
     float w[kMaxB * kMaxK];
     unsigned sel[kMaxE / 32];
-    int expert[kMaxSlots];       // routed slots: expert index; shared slots: -1 - s
-    unsigned tok[kMaxSlots];     // token bit mask per slot
-    float wt[kMaxSlots][kMaxB];  // gate weight per slot and token (valid where tok is set)
+    int expert[kMaxSlots];           // routed slots: expert index; shared slots: -1 - s
+    unsigned tok[kMaxSlots];         // token bit mask per slot
     int n_routed, n_slots;
+    bool last;                       // this workgroup took the last ticket
 };
 
 // Build the slot plan in LDS (all threads participate; ends with a barrier).
@@ -78,19 +92,26 @@ __device__ void build_plan(const FfnArgs& a, Plan& p) {
         int rank = __popc(p.sel[e >> 5] & ((1u << (e & 31)) - 1u));
         for (int q = 0; q < (e >> 5); ++q) rank += __popc(p.sel[q]);
         atomicOr(&p.tok[rank], 1u << b);
-        p.wt[rank][b] = p.w[t];
         p.expert[rank] = e;
     }
     for (int s = tid; s < a.n_shared; s += kThreads) {
         p.expert[total + s] = -1 - s;
         p.tok[total + s] = (1u << a.B) - 1u;
-        for (int b = 0; b < a.B; ++b) p.wt[total + s][b] = 1.f;
     }
     if (tid == 0) {
         p.n_routed = total;
         p.n_slots = total + a.n_shared;
     }
     __syncthreads();
+}
+
+// Gate weight of token b for slot j (1 for shared experts, 0 if not routed).
+__device__ __forceinline__ float slot_weight(const FfnArgs& a, const Plan& p, int j, int b) {
+    const int e = p.expert[j];
+    if (e < 0) return 1.f;
+    for (int k = 0; k < a.K; ++k)
+        if (p.idx[b * a.K + k] == e) return p.w[b * a.K + k];
+    return 0.f;
 }
 
 __device__ __forceinline__ const char* slot_blob(const FfnArgs& a, const Plan& p, int j) {
@@ -111,6 +132,13 @@ struct Chunk {
             v[2] = __uint_as_float(q.z); v[3] = __uint_as_float(q.w);
         }
     }
+    __device__ __forceinline__ void load_f32(const float* p) {
+#pragma unroll
+        for (int q = 0; q < N / 4; ++q) {
+            const float4 f = reinterpret_cast<const float4*>(p)[q];
+            v[4 * q + 0] = f.x; v[4 * q + 1] = f.y; v[4 * q + 2] = f.z; v[4 * q + 3] = f.w;
+        }
+    }
 };
 
 template <bool BF>
@@ -127,22 +155,73 @@ __device__ __forceinline__ uint4 ld_stream(const char* p) {
 __device__ __forceinline__ uint4 ld_cached(const char* p) {
     return *reinterpret_cast<const uint4*>(p);
 }
+__device__ __forceinline__ bf16x8 ld_bf8_stream(const char* p) {
+    return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+}
+__device__ __forceinline__ bf16x8 ld_bf8(const char* p) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
+}
 
 // Sum over a segment of G consecutive lanes (G = 16, 32 or 64); every lane
 // of the segment returns the segment's sum.
 template <int G>
 __device__ __forceinline__ float seg_sum(float v) {
-    if (G == 64) return wave_sum(v);
+    if constexpr (G == 64) {
+        return wave_sum(v);
+    } else {
 #pragma unroll
-    for (int o = G / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+        for (int o = G / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+        return v;
+    }
 }
 
 __device__ __forceinline__ float silu(float g) { return g / (1.f + expf(-g)); }
 
-// ----------------------------------------------------------------------------
-// gate/up: rows of W_gate and W_up of one slot -> a = w * silu(g) * u
-// ----------------------------------------------------------------------------
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return uint16_t((u + (((u >> 16) & 1u) + 0x7fffu)) >> 16);
+}
+
+// Down-phase epilogue.  One slot group: store y.  Several: store this
+// group's partial sums, take the row block's ticket; the workgroup that takes
+// the last ticket adds the partials in group order and resets the ticket.
+struct DownEpilogue {
+    const FfnArgs& a;
+    Plan& p;
+    int rb, grp, h_base, rows;
+
+    __device__ __forceinline__ void put(int b, int h, float v) const {
+        if (a.ng == 1)
+            a.y[size_t(b) * a.H + h] = v;
+        else
+            a.part[(size_t(grp) * a.B + b) * a.H + h] = v;
+    }
+    __device__ __forceinline__ void finish() const {
+        if (a.ng == 1) return;
+        __threadfence();
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const unsigned t = atomicAdd(&a.tick[rb], 1u);
+            p.last = (t == unsigned(a.ng) - 1);
+        }
+        __syncthreads();
+        if (!p.last) return;
+        __threadfence();
+        for (int q = threadIdx.x; q < rows * a.B; q += kThreads) {
+            const int b = q / rows, h = h_base + q % rows;
+            if (h >= a.H) continue;
+            float s = 0.f;
+            for (int g = 0; g < a.ng; ++g) s += a.part[(size_t(g) * a.B + b) * a.H + h];
+            a.y[size_t(b) * a.H + h] = s;
+        }
+        if (threadIdx.x == 0) atomicExch(&a.tick[rb], 0u);
+    }
+};
+
+// ============================================================================
+// GEMV path (batch < 8)
+// ============================================================================
+
 template <bool BF, int G, int R, int NB>
 __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_per_slot) {
     __shared__ Plan p;
@@ -169,13 +248,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
 #pragma unroll
         for (int b = 0; b < NB; ++b) accg[r][b] = accu[r][b] = 0.f;
 
-    for (int c = g; c < cpr; c += G) {
-        uint4 qg[R], qu[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            qg[r] = ld_stream(wg + r * rowb + size_t(c) * 16);
-            qu[r] = ld_stream(wu + r * rowb + size_t(c) * 16);
-        }
+    auto compute = [&](int c, const uint4 (&qg)[R], const uint4 (&qu)[R]) {
         Chunk<BF> cg[R], cu[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) { cg[r].unpack(qg[r]); cu[r].unpack(qu[r]); }
@@ -190,38 +263,61 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
                 accu[r][b] = dotc<BF>(cu[r], cx, accu[r][b]);
             }
         }
+    };
+    int c = g;
+    for (; c + G < cpr; c += 2 * G) {          // two chunks in flight per row
+        uint4 ga[R], ua[R], gb[R], ub[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            ga[r] = ld_stream(wg + r * rowb + size_t(c) * 16);
+            ua[r] = ld_stream(wu + r * rowb + size_t(c) * 16);
+            gb[r] = ld_stream(wg + r * rowb + size_t(c + G) * 16);
+            ub[r] = ld_stream(wu + r * rowb + size_t(c + G) * 16);
+        }
+        compute(c, ga, ua);
+        compute(c + G, gb, ub);
     }
+    if (c < cpr) {
+        uint4 ga[R], ua[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            ga[r] = ld_stream(wg + r * rowb + size_t(c) * 16);
+            ua[r] = ld_stream(wu + r * rowb + size_t(c) * 16);
+        }
+        compute(c, ga, ua);
+    }
+    float* act = reinterpret_cast<float*>(a.act);
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
         if (!((tm >> b) & 1u)) continue;
-        const float wb = p.wt[j][b];
+        const float wb = slot_weight(a, p, j, b);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const float gs = seg_sum<G>(accg[r][b]);
             const float us = seg_sum<G>(accu[r][b]);
-            if (g == 0) a.act[(size_t(j) * a.B + b) * a.I + i0 + r] = wb * silu(gs) * us;
+            if (g == 0) act[(size_t(j) * a.B + b) * a.I + i0 + r] = wb * silu(gs) * us;
         }
     }
 }
 
-// ----------------------------------------------------------------------------
-// down: y[b][h] = sum over slots j (ascending) of W_down_j[h] . a[j][b]
-// ----------------------------------------------------------------------------
+// Down, rows owned by lane groups (rows of at most 512 chunks).
 template <bool BF, int G, int R, int NB>
-__global__ __launch_bounds__(kThreads) void ffn_down(FfnArgs a) {
+__global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
     __shared__ Plan p;
     build_plan(a, p);
+    const int rb = blockIdx.x / a.ng, grp = blockIdx.x % a.ng;
     const int rows_per_block = kWaves * (64 / G) * R;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int grp = lane / G, g = lane % G;
-    const int h0 = blockIdx.x * rows_per_block + (wave * (64 / G) + grp) * R;
+    const int lg = lane / G, g = lane % G;
+    const int h0 = rb * rows_per_block + (wave * (64 / G) + lg) * R;
     if (blockIdx.x == 0 && threadIdx.x == 0 && a.n_experts)
         atomicAdd(a.n_experts, (unsigned long long)p.n_routed);
-    if (h0 >= a.H) return;   // H is a multiple of R
+    const bool live = h0 < a.H;   // H is a multiple of R
     constexpr int esz = BF ? 2 : 4;
     constexpr int N = Chunk<BF>::N;
     const size_t rowb = size_t(a.I) * esz;
     const int cpr = int(rowb / 16);
+    const int j0 = grp * a.spg, j1 = min(p.n_slots, j0 + a.spg);
 
     float acc[R][NB];
 #pragma unroll
@@ -229,43 +325,262 @@ __global__ __launch_bounds__(kThreads) void ffn_down(FfnArgs a) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
 
-    for (int j = 0; j < p.n_slots; ++j) {
+    for (int j = j0; live && j < j1; ++j) {
         const unsigned tm = p.tok[j];
         const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb;
-        const float* act = a.act + size_t(j) * a.B * a.I;
-        for (int c = g; c < cpr; c += G) {
-            uint4 q[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) q[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
+        const float* act = reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I;
+        auto compute = [&](int c, const uint4 (&q)[R]) {
             Chunk<BF> cw[R];
 #pragma unroll
             for (int r = 0; r < R; ++r) cw[r].unpack(q[r]);
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 if (!((tm >> b) & 1u)) continue;
-                const float4* ap = reinterpret_cast<const float4*>(act + size_t(b) * a.I + c * N);
                 Chunk<BF> cx;
-#pragma unroll
-                for (int q4 = 0; q4 < N / 4; ++q4) {
-                    const float4 f = ap[q4];
-                    cx.v[q4 * 4 + 0] = f.x; cx.v[q4 * 4 + 1] = f.y;
-                    cx.v[q4 * 4 + 2] = f.z; cx.v[q4 * 4 + 3] = f.w;
-                }
+                cx.load_f32(act + size_t(b) * a.I + c * N);
 #pragma unroll
                 for (int r = 0; r < R; ++r) acc[r][b] = dotc<BF>(cw[r], cx, acc[r][b]);
             }
+        };
+        int c = g;
+        for (; c + G < cpr; c += 2 * G) {
+            uint4 qa[R], qb[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                qa[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
+                qb[r] = ld_stream(wd + r * rowb + size_t(c + G) * 16);
+            }
+            compute(c, qa);
+            compute(c + G, qb);
+        }
+        if (c < cpr) {
+            uint4 qa[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) qa[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
+            compute(c, qa);
         }
     }
+    DownEpilogue ep{a, p, rb, grp, rb * rows_per_block, rows_per_block};
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
         if (b >= a.B) break;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const float s = seg_sum<G>(acc[r][b]);
-            if (g == 0) a.y[size_t(b) * a.H + h0 + r] = s;
+            if (live && g == 0) ep.put(b, h0 + r, s);
+        }
+    }
+    ep.finish();
+}
+
+// Down, long rows: the whole workgroup strides one block of R rows (split-K
+// over the four waves), then combines the waves' sums through LDS.
+template <bool BF, int R, int NB>
+__global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
+    __shared__ Plan p;
+    __shared__ float red[kWaves][R][NB];
+    build_plan(a, p);
+    const int rb = blockIdx.x / a.ng, grp = blockIdx.x % a.ng;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int h0 = rb * R;   // H is a multiple of R
+    if (blockIdx.x == 0 && tid == 0 && a.n_experts)
+        atomicAdd(a.n_experts, (unsigned long long)p.n_routed);
+    constexpr int esz = BF ? 2 : 4;
+    constexpr int N = Chunk<BF>::N;
+    const size_t rowb = size_t(a.I) * esz;
+    const int cpr = int(rowb / 16);
+    const int j0 = grp * a.spg, j1 = min(p.n_slots, j0 + a.spg);
+
+    float acc[R][NB];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
+
+    for (int j = j0; j < j1; ++j) {
+        const unsigned tm = p.tok[j];
+        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb;
+        const float* act = reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I;
+        auto compute = [&](int c, const uint4 (&q)[R]) {
+            Chunk<BF> cw[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) cw[r].unpack(q[r]);
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                if (!((tm >> b) & 1u)) continue;
+                Chunk<BF> cx;
+                cx.load_f32(act + size_t(b) * a.I + c * N);
+#pragma unroll
+                for (int r = 0; r < R; ++r) acc[r][b] = dotc<BF>(cw[r], cx, acc[r][b]);
+            }
+        };
+        int c = tid;
+        for (; c + kThreads < cpr; c += 2 * kThreads) {
+            uint4 qa[R], qb[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                qa[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
+                qb[r] = ld_stream(wd + r * rowb + size_t(c + kThreads) * 16);
+            }
+            compute(c, qa);
+            compute(c + kThreads, qb);
+        }
+        if (c < cpr) {
+            uint4 qa[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) qa[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
+            compute(c, qa);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const float s = wave_sum(acc[r][b]);
+            if (lane == 0) red[wave][r][b] = s;
+        }
+    __syncthreads();
+    DownEpilogue ep{a, p, rb, grp, h0, R};
+    if (tid < R * NB) {
+        const int r = tid / NB, b = tid % NB;
+        if (b < a.B) {
+            float s = 0.f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) s += red[w][r][b];
+            ep.put(b, h0 + r, s);
+        }
+    }
+    ep.finish();
+}
+
+// ============================================================================
+// MFMA path (batch >= 8, bf16, H and I multiples of 64)
+// ============================================================================
+
+// gate/up: each wave computes NT tiles of 16 rows x 16 tokens for W_gate and
+// W_up over the whole hidden dimension, then writes the bf16 activation
+// (zero for tokens not routed to the slot).
+template <int NT>
+__global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int blocks_per_slot) {
+    __shared__ Plan p;
+    build_plan(a, p);
+    const int j = blockIdx.x / blocks_per_slot;
+    if (j >= p.n_slots) return;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n = lane & 15, q = lane >> 4;
+    const int i0 = (blockIdx.x % blocks_per_slot) * (kWaves * NT * 16) + wave * NT * 16;
+    if (i0 >= a.I) return;   // I is a multiple of 16
+    const unsigned tm = p.tok[j];
+    const size_t rowb = size_t(a.H) * 2;
+    const char* blob = slot_blob(a, p, j);
+    const bool xrow = n < a.B;     // A operand row n = token n
+    const char* xs = reinterpret_cast<const char*>(a.x) + size_t(xrow ? n : 0) * rowb + q * 32;
+    const char* wg[NT];
+    const char* wu[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        wg[t] = blob + size_t(i0 + t * 16 + n) * rowb + q * 32;
+        wu[t] = blob + size_t(a.I + i0 + t * 16 + n) * rowb + q * 32;
+    }
+    f32x4 dg[NT], du[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) dg[t] = du[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    for (int h = 0; h < a.H; h += 64) {
+        const size_t off = size_t(h) * 2;
+        bf16x8 ga[NT], gb[NT], ua[NT], ub[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            ga[t] = ld_bf8_stream(wg[t] + off);
+            gb[t] = ld_bf8_stream(wg[t] + off + 16);
+            ua[t] = ld_bf8_stream(wu[t] + off);
+            ub[t] = ld_bf8_stream(wu[t] + off + 16);
+        }
+        const bf16x8 xa = xrow ? ld_bf8(xs + off) : zero;
+        const bf16x8 xb = xrow ? ld_bf8(xs + off + 16) : zero;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            dg[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, ga[t], dg[t], 0, 0, 0);
+            dg[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, gb[t], dg[t], 0, 0, 0);
+            du[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, ua[t], du[t], 0, 0, 0);
+            du[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, ub[t], du[t], 0, 0, 0);
+        }
+    }
+    // D layout: lane holds rows m = 4q + r (tokens) of column n (weight row)
+    uint16_t* act = reinterpret_cast<uint16_t*>(a.act) + size_t(j) * a.B * a.I;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int b = 4 * q + r;
+        if (b >= a.B) continue;
+        const bool routed = (tm >> b) & 1u;
+        const float wb = routed ? slot_weight(a, p, j, b) : 0.f;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const float v = routed ? wb * silu(dg[t][r]) * du[t][r] : 0.f;
+            act[size_t(b) * a.I + i0 + t * 16 + n] = f32_to_bf16_rne(v);
         }
     }
 }
+
+// down: each wave computes NT tiles of 16 output rows x 16 tokens, summing
+// the slots of its group (A operand = the slot's bf16 activations).
+template <int NT>
+__global__ __launch_bounds__(kThreads) void ffn_down_mfma(FfnArgs a) {
+    __shared__ Plan p;
+    build_plan(a, p);
+    const int rb = blockIdx.x / a.ng, grp = blockIdx.x % a.ng;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n = lane & 15, q = lane >> 4;
+    const int rows_per_block = kWaves * NT * 16;
+    const int h0 = rb * rows_per_block + wave * NT * 16;
+    if (blockIdx.x == 0 && threadIdx.x == 0 && a.n_experts)
+        atomicAdd(a.n_experts, (unsigned long long)p.n_routed);
+    const bool live = h0 < a.H;   // H is a multiple of 16
+    const size_t rowb = size_t(a.I) * 2;
+    const bool arow = n < a.B;
+    const int j0 = grp * a.spg, j1 = min(p.n_slots, j0 + a.spg);
+    f32x4 d[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) d[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    for (int j = j0; live && j < j1; ++j) {
+        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * 2 + q * 32;
+        const char* wr[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) wr[t] = wd + size_t(h0 + t * 16 + n) * rowb;
+        const char* ar = reinterpret_cast<const char*>(a.act) +
+                         (size_t(j) * a.B + (arow ? n : 0)) * rowb + q * 32;
+        for (int k = 0; k < a.I; k += 64) {
+            const size_t off = size_t(k) * 2;
+            bf16x8 wa[NT], wb[NT];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                wa[t] = ld_bf8_stream(wr[t] + off);
+                wb[t] = ld_bf8_stream(wr[t] + off + 16);
+            }
+            const bf16x8 aa = arow ? ld_bf8(ar + off) : zero;
+            const bf16x8 ab = arow ? ld_bf8(ar + off + 16) : zero;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                d[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aa, wa[t], d[t], 0, 0, 0);
+                d[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ab, wb[t], d[t], 0, 0, 0);
+            }
+        }
+    }
+    DownEpilogue ep{a, p, rb, grp, rb * rows_per_block, rows_per_block};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int b = 4 * q + r;
+        if (!live || b >= a.B) continue;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) ep.put(b, h0 + t * 16 + n, d[t][r]);
+    }
+    ep.finish();
+}
+
+// ============================================================================
+// host side
+// ============================================================================
 
 // lanes per row: the widest of 64/32/16 that divides the row's chunk count
 int pick_group(int chunks) {
@@ -275,66 +590,133 @@ int pick_group(int chunks) {
     return 64;
 }
 
+struct Shape {
+    bool mfma;          // MFMA path
+    int slots;          // slot capacity
+    int gu_G;           // GEMV gate/up lanes per row
+    int dn_kind;        // 0: rows (lane groups), 1: whole-workgroup rows, 2: MFMA
+    int dn_G;           // lanes per row for kind 0
+    int dn_rows;        // rows per down workgroup
+    int n_rb;           // down row blocks
+    int ng, spg;        // slot groups
+};
+
+constexpr int kGemvR = 2;     // rows per lane group (GEMV)
+constexpr int kDownWgR = 4;   // rows per workgroup (whole-workgroup down)
+
+Shape plan_shape(int B, int K, int H, int I, int E, int n_shared, int dtype) {
+    Shape s{};
+    const int esz = dtype == STMOE_BF16 ? 2 : 4;
+    s.slots = (B * K < E ? B * K : E) + n_shared;
+    s.mfma = dtype == STMOE_BF16 && B >= 8 && H % 64 == 0 && I % 64 == 0;
+    s.gu_G = pick_group(H * esz / 16);
+    const int cpr_i = I * esz / 16;
+    if (s.mfma) {
+        s.dn_kind = 2;
+        s.dn_rows = kWaves * 16;
+    } else if (cpr_i >= 512 && H % kDownWgR == 0) {
+        s.dn_kind = 1;
+        s.dn_rows = kDownWgR;
+    } else {
+        s.dn_kind = 0;
+        s.dn_G = pick_group(cpr_i);
+        s.dn_rows = kWaves * (64 / s.dn_G) * kGemvR;
+    }
+    s.n_rb = (H + s.dn_rows - 1) / s.dn_rows;
+    int ng = (kDownWgTarget + s.n_rb - 1) / s.n_rb;
+    if (ng > s.slots) ng = s.slots;
+    if (ng < 1) ng = 1;
+    s.spg = (s.slots + ng - 1) / ng;
+    s.ng = (s.slots + s.spg - 1) / s.spg;
+    return s;
+}
+
+struct WsLayout {
+    size_t act, part, tick, total;
+};
+
+WsLayout ws_layout(int B, int H, int I, const Shape& s) {
+    auto up = [](size_t v) { return (v + 255) / 256 * 256; };
+    WsLayout w{};
+    w.act = 0;
+    w.part = up(size_t(s.slots) * B * I * sizeof(float));
+    w.tick = w.part + (s.ng > 1 ? up(size_t(s.ng) * B * H * sizeof(float)) : 0);
+    w.total = w.tick + up(size_t(s.n_rb) * sizeof(unsigned));
+    return w;
+}
+
 template <bool BF, int G, int NB>
-int launch_g(const FfnArgs& a, int slots, hipStream_t s, int G_down, hipEvent_t ev_mid) {
-    constexpr int R = 2;
-    const int rows_up = kWaves * (64 / G) * R;
-    const int bps = (a.I + rows_up - 1) / rows_up;
-    hipLaunchKernelGGL((ffn_gate_up<BF, G, R, NB>), dim3(unsigned(bps * slots)), dim3(kThreads), 0, s,
-                       a, bps);
+int launch_gate_up(const FfnArgs& a, const Shape& s, hipStream_t st) {
+    const int rows = kWaves * (64 / G) * kGemvR;
+    const int bps = (a.I + rows - 1) / rows;
+    hipLaunchKernelGGL((ffn_gate_up<BF, G, kGemvR, NB>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0,
+                       st, a, bps);
     STMOE_LAUNCHED();
-    if (ev_mid) STMOE_HIP(hipEventRecord(ev_mid, s));
-    // the down kernel's row length is I (its own lane grouping)
-    switch (G_down) {
-        case 16: {
-            const int rows = kWaves * 4 * R;
-            hipLaunchKernelGGL((ffn_down<BF, 16, R, NB>), dim3(unsigned((a.H + rows - 1) / rows)),
-                               dim3(kThreads), 0, s, a);
-            break;
-        }
-        case 32: {
-            const int rows = kWaves * 2 * R;
-            hipLaunchKernelGGL((ffn_down<BF, 32, R, NB>), dim3(unsigned((a.H + rows - 1) / rows)),
-                               dim3(kThreads), 0, s, a);
-            break;
-        }
-        default: {
-            const int rows = kWaves * 1 * R;
-            hipLaunchKernelGGL((ffn_down<BF, 64, R, NB>), dim3(unsigned((a.H + rows - 1) / rows)),
-                               dim3(kThreads), 0, s, a);
-        }
+    return STMOE_OK;
+}
+
+template <bool BF, int NB>
+int launch_down(const FfnArgs& a, const Shape& s, hipStream_t st) {
+    const dim3 grid(unsigned(s.n_rb * s.ng));
+    if (s.dn_kind == 1) {
+        hipLaunchKernelGGL((ffn_down_wg<BF, kDownWgR, NB>), grid, dim3(kThreads), 0, st, a);
+    } else if (s.dn_G == 16) {
+        hipLaunchKernelGGL((ffn_down_rows<BF, 16, kGemvR, NB>), grid, dim3(kThreads), 0, st, a);
+    } else if (s.dn_G == 32) {
+        hipLaunchKernelGGL((ffn_down_rows<BF, 32, kGemvR, NB>), grid, dim3(kThreads), 0, st, a);
+    } else {
+        hipLaunchKernelGGL((ffn_down_rows<BF, 64, kGemvR, NB>), grid, dim3(kThreads), 0, st, a);
     }
     STMOE_LAUNCHED();
     return STMOE_OK;
 }
 
 template <bool BF, int NB>
-int launch_nb(const FfnArgs& a, int slots, hipStream_t s, hipEvent_t ev_mid) {
-    constexpr int esz = BF ? 2 : 4;
-    const int gu = pick_group(a.H * esz / 16);
-    const int gd = pick_group(a.I * esz / 16);
-    switch (gu) {
-        case 16: return launch_g<BF, 16, NB>(a, slots, s, gd, ev_mid);
-        case 32: return launch_g<BF, 32, NB>(a, slots, s, gd, ev_mid);
-        default: return launch_g<BF, 64, NB>(a, slots, s, gd, ev_mid);
-    }
+int launch_gemv(const FfnArgs& a, const Shape& s, hipStream_t st, hipEvent_t ev_mid) {
+    int rc;
+    if (s.gu_G == 16) rc = launch_gate_up<BF, 16, NB>(a, s, st);
+    else if (s.gu_G == 32) rc = launch_gate_up<BF, 32, NB>(a, s, st);
+    else rc = launch_gate_up<BF, 64, NB>(a, s, st);
+    if (rc) return rc;
+    if (ev_mid) STMOE_HIP(hipEventRecord(ev_mid, st));
+    return launch_down<BF, NB>(a, s, st);
 }
 
 template <bool BF>
-int launch_gemv(const FfnArgs& a, int slots, hipStream_t s, hipEvent_t ev_mid) {
-    if (a.B <= 1) return launch_nb<BF, 1>(a, slots, s, ev_mid);
-    if (a.B <= 2) return launch_nb<BF, 2>(a, slots, s, ev_mid);
-    if (a.B <= 4) return launch_nb<BF, 4>(a, slots, s, ev_mid);
-    if (a.B <= 8) return launch_nb<BF, 8>(a, slots, s, ev_mid);
-    return launch_nb<BF, 16>(a, slots, s, ev_mid);
+int launch_gemv_b(const FfnArgs& a, const Shape& s, hipStream_t st, hipEvent_t ev_mid) {
+    if (a.B <= 1) return launch_gemv<BF, 1>(a, s, st, ev_mid);
+    if (a.B <= 2) return launch_gemv<BF, 2>(a, s, st, ev_mid);
+    if (a.B <= 4) return launch_gemv<BF, 4>(a, s, st, ev_mid);
+    if (a.B <= 8) return launch_gemv<BF, 8>(a, s, st, ev_mid);
+    return launch_gemv<BF, 16>(a, s, st, ev_mid);
+}
+
+int launch_mfma(const FfnArgs& a, const Shape& s, hipStream_t st, hipEvent_t ev_mid) {
+    constexpr int NT = 1;
+    const int rows = kWaves * NT * 16;
+    const int bps = (a.I + rows - 1) / rows;
+    hipLaunchKernelGGL((ffn_gate_up_mfma<NT>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
+    STMOE_LAUNCHED();
+    if (ev_mid) STMOE_HIP(hipEventRecord(ev_mid, st));
+    hipLaunchKernelGGL((ffn_down_mfma<NT>), dim3(unsigned(s.n_rb * s.ng)), dim3(kThreads), 0, st, a);
+    STMOE_LAUNCHED();
+    return STMOE_OK;
 }
 
 }  // namespace
 
+size_t ffn_workspace_bytes(int B, int K, int E, int H, int I, int n_shared, int dtype) {
+    const Shape s = plan_shape(B, K, H, I, E, n_shared, dtype);
+    return ws_layout(B, H, I, s).total;
+}
+
 // Internal entry used by the decode-layer orchestration (no argument checks).
 int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, int H, int I, int E,
                int dtype, const void* const* eptr, const void* const* sptr, int n_shared,
-               float* y, void* ws, hipStream_t s, unsigned long long* n_experts, hipEvent_t ev_mid) {
+               float* y, void* ws, hipStream_t st, unsigned long long* n_experts, hipEvent_t ev_mid) {
+    const Shape s = plan_shape(B, K, H, I, E, n_shared, dtype);
+    const WsLayout L = ws_layout(B, H, I, s);
+    char* base = reinterpret_cast<char*>(ws);
     FfnArgs a;
     a.x = x;
     a.idx = idx;
@@ -347,22 +729,27 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
     a.I = I;
     a.E = E;
     a.n_shared = n_shared;
-    a.act = reinterpret_cast<float*>(ws);
+    a.act = base + L.act;
+    a.part = reinterpret_cast<float*>(base + L.part);
+    a.tick = reinterpret_cast<unsigned*>(base + L.tick);
     a.y = y;
     a.n_experts = n_experts;
-    const int slots = (B * K < E ? B * K : E) + n_shared;
-    return dtype == STMOE_BF16 ? launch_gemv<true>(a, slots, s, ev_mid)
-                                : launch_gemv<false>(a, slots, s, ev_mid);
+    a.ng = s.ng;
+    a.spg = s.spg;
+    if (s.mfma) return launch_mfma(a, s, st, ev_mid);
+    return dtype == STMOE_BF16 ? launch_gemv_b<true>(a, s, st, ev_mid)
+                               : launch_gemv_b<false>(a, s, st, ev_mid);
 }
 
 }  // namespace stmoe
 
 using namespace stmoe;
 
-extern "C" size_t moe_expert_ffn_workspace_bytes(int B, int K, int E, int I, int n_shared) {
-    if (B < 1 || K < 1 || E < 1 || I < 1 || n_shared < 0) return 0;
-    const size_t slots = size_t(B * K < E ? B * K : E) + n_shared;
-    return slots * B * I * sizeof(float);
+extern "C" size_t moe_expert_ffn_workspace_bytes(int B, int K, int E, int H, int I, int n_shared,
+                                                 int dtype) {
+    if (B < 1 || K < 1 || E < 1 || H < 1 || I < 1 || n_shared < 0) return 0;
+    if (dtype != STMOE_BF16 && dtype != STMOE_F32) return 0;
+    return ffn_workspace_bytes(B, K, E, H, I, n_shared, dtype);
 }
 
 extern "C" int moe_expert_ffn(const void* x, const int32_t* topk_idx, const float* topk_w, int B,
@@ -379,8 +766,10 @@ extern "C" int moe_expert_ffn(const void* x, const int32_t* topk_idx, const floa
     STMOE_CHECK(n_shared >= 0 && n_shared <= kMaxShared, "n_shared must be in [0, 8]");
     STMOE_CHECK(n_shared == 0 || shared_ptrs, "shared_ptrs is required when n_shared > 0");
     STMOE_CHECK(dtype == STMOE_BF16 || dtype == STMOE_F32, "dtype must be STMOE_BF16 or STMOE_F32");
-    STMOE_CHECK(ws_bytes >= moe_expert_ffn_workspace_bytes(B, K, E, I, n_shared), "workspace too small");
-    STMOE_CHECK((reinterpret_cast<uintptr_t>(x) & 15) == 0, "x must be 16-byte aligned");
+    STMOE_CHECK(ws_bytes >= moe_expert_ffn_workspace_bytes(B, K, E, H, I, n_shared, dtype),
+                "workspace too small");
+    STMOE_CHECK((reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(ws) & 255) == 0,
+                "x must be 16-byte and ws 256-byte aligned");
     return ffn_launch(x, topk_idx, topk_w, B, K, H, I, E, dtype, expert_ptrs, shared_ptrs, n_shared, y,
                       ws, as_stream(stream), nullptr, nullptr);
 }

@@ -77,7 +77,7 @@ _SIGS = {
     "stmoe_stats": (i32, [vp, vp]),
     "moe_blob_bytes": (sz, [i32, i32, i32]),
     "moe_pack_expert": (i32, [vp, vp, vp, i32, i32, i32, vp]),
-    "moe_expert_ffn_workspace_bytes": (sz, [i32, i32, i32, i32, i32]),
+    "moe_expert_ffn_workspace_bytes": (sz, [i32, i32, i32, i32, i32, i32, i32]),
     "moe_expert_ffn": (i32, [vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp, sz, vp]),
     "stmoe_policy_create": (i32, [i32, i32, i32, vp, P(vp)]),
     "stmoe_policy_destroy": (i32, [vp]),
@@ -255,8 +255,9 @@ def pack_expert(w_gate, w_up, w_down, dtype, out):
 
 
 # ------------------------------------------------------------- FFN
-def ffn_workspace_bytes(B, K, E, I, n_shared=0):
-    return _lib.moe_expert_ffn_workspace_bytes(B, K, E, I, n_shared)
+def ffn_workspace_bytes(B, K, E, H, I, n_shared=0, dtype=BF16):
+    """Workspace bytes for expert_ffn; allocate zero-filled (torch.zeros), 256-byte aligned."""
+    return _lib.moe_expert_ffn_workspace_bytes(B, K, E, H, I, n_shared, dtype)
 
 
 def expert_ffn(x, idx, w, H, I, E, dtype, expert_ptrs, y, ws, shared_ptrs=None, n_shared=0,

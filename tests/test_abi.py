@@ -40,9 +40,9 @@ def test_invalid_arguments_rejected_without_device_work():
     # workspace too small
     rc = S._lib.moe_route_topk(16, 16, 1, 64, 8, 2, S.BF16, 0, 16, 16, None, 16, 4, None)
     assert rc == S.EINVAL and "workspace" in S._lib.stmoe_last_error().decode()
-    rc = S._lib.moe_expert_ffn(16, 16, 16, 1, 2, 100, 64, 8, S.BF16, 16, None, 0, 16, 16, 1 << 20, None)
+    rc = S._lib.moe_expert_ffn(16, 16, 16, 1, 2, 100, 64, 8, S.BF16, 16, None, 0, 16, 256, 1 << 20, None)
     assert rc == S.EINVAL
-    rc = S._lib.moe_expert_ffn(16, 16, 16, 1, 2, 64, 64, 8, S.BF16, 16, None, 2, 16, 16, 1 << 20, None)
+    rc = S._lib.moe_expert_ffn(16, 16, 16, 1, 2, 64, 64, 8, S.BF16, 16, None, 2, 16, 256, 1 << 20, None)
     assert rc == S.EINVAL      # shared experts without pointers
     assert S._lib.stmoe_predict(None, 0, None, 3, None, None, None, None, None) == S.EINVAL
     assert S.blob_bytes(4096, 14336, S.BF16) == 3 * 4096 * 14336 * 2

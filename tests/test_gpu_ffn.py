@@ -19,7 +19,8 @@ def _run_ffn(cfg, layer, idx, w, x_store, n_shared=0):
     ptrs = [blobs[e].data_ptr() if e in blobs else 0 for e in range(cfg.E)]
     shared = [blob_dev(cfg, layer, s, shared=True) for s in range(n_shared)]
     y = torch.full((B, cfg.H), float("nan"), dtype=torch.float32, device=DEV)
-    ws = torch.empty(S.ffn_workspace_bytes(B, K, cfg.E, cfg.I, n_shared), dtype=torch.uint8, device=DEV)
+    ws = torch.zeros(S.ffn_workspace_bytes(B, K, cfg.E, cfg.H, cfg.I, n_shared, storage_dtype(cfg)),
+                     dtype=torch.uint8, device=DEV)
     S.expert_ffn(to_dev(x_store), i32(idx), torch.from_numpy(w.astype(np.float32)).to(DEV), cfg.H,
                  cfg.I, cfg.E, storage_dtype(cfg), ptr_array(ptrs), y, ws,
                  shared_ptrs=ptr_array([s.data_ptr() for s in shared]) if n_shared else None,
@@ -41,7 +42,8 @@ def _inputs(cfg, B, K, seed, distinct_rows=True):
 
 
 @pytest.mark.parametrize("name,B", [("tiny", 1), ("qwen30b", 1), ("qwen30b", 3), ("qwen30b-b8", 8),
-                                    ("dsv2lite", 4), ("qwen235b", 16), ("qwen235b", 2)])
+                                    ("qwen30b-b8", 12), ("dsv2lite", 4), ("dsv2lite", 9),
+                                    ("qwen235b", 16), ("qwen235b", 9), ("qwen235b", 2), ("mixtral", 8)])
 def test_ffn_parity(name, B):
     from paper_2606_15453_amd import workload as W
     cfg = W.CONFIGS[name].scaled(B=B)
@@ -72,6 +74,38 @@ def test_ffn_shared_tokens_overlap():
     x = W.to_storage(cfg, np.random.default_rng(3).normal(0, 1, (6, cfg.H)))
     got, ref, err = _run_ffn(cfg, 0, idx, w, x)
     assert err <= TOL
+
+
+@pytest.mark.parametrize("B", [8, 11])
+def test_ffn_batch8_fallback_shapes(B):
+    """Batch >= 8 with H, I not multiples of 64 runs the GEMV kernels."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen30b"].scaled(H=264, I=40, E=12, K=3, B=B)
+    idx, w, x = _inputs(cfg, B, 3, seed=B)
+    got, ref, err = _run_ffn(cfg, 0, idx, w, x)
+    assert err <= TOL
+
+
+def test_ffn_repeated_calls_reuse_workspace():
+    """Completion tickets in the workspace are reset by every call."""
+    import torch
+    from gpuhelp import DEV, blob_dev, expert_f64, i32, ptr_array, rel_l2, storage_dtype, to_dev
+    from oracle.stmoe_oracle import decode_storage, moe_ffn
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    for name, B in (("qwen30b", 1), ("qwen235b", 16)):
+        cfg = W.CONFIGS[name].scaled(B=B, E=24)
+        blobs = [blob_dev(cfg, 0, e) for e in range(cfg.E)]
+        ptrs = ptr_array([b.data_ptr() for b in blobs])
+        ws = torch.zeros(S.ffn_workspace_bytes(B, cfg.K, cfg.E, cfg.H, cfg.I, 0, storage_dtype(cfg)),
+                         dtype=torch.uint8, device=DEV)
+        y = torch.empty((B, cfg.H), dtype=torch.float32, device=DEV)
+        for rep in range(3):
+            idx, w, x = _inputs(cfg, B, cfg.K, seed=100 + rep)
+            S.expert_ffn(to_dev(x), i32(idx), torch.from_numpy(w).to(DEV), cfg.H, cfg.I, cfg.E,
+                         storage_dtype(cfg), ptrs, y, ws)
+            ref = moe_ffn(decode_storage(x), idx, w, lambda e: expert_f64(cfg, 0, e))
+            assert rel_l2(y.cpu().numpy(), ref) <= TOL
 
 
 def test_ffn_zero_input_and_linearity():

@@ -52,7 +52,148 @@ def parse():
                     help="pinned host pool budget; larger stacks alias experts onto it")
     ap.add_argument("--cpu-tokens", type=int, default=2,
                     help="decode tokens of the CPU oracle sample (0 skips it)")
+    ap.add_argument("--counters", action="store_true",
+                    help="run the fixed workload profiled by the rocprofv3 --pmc passes and exit")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the markdown counter summary of two rocprofv3 --pmc runs and exit")
     return ap.parse_args()
+
+
+COUNTERS_MD = os.path.join(ROOT, "profiles", "ffn_gate_up_mixtral8x7b_b1_counters.md")
+FFN_SOURCE = os.path.join(ROOT, "paper_2606_15453_amd", "csrc", "expert_ffn.hip")
+CALIB_BYTES = 1 << 30
+COUNTER_TOKENS = 20
+
+
+def ffn_source_sha():
+    import hashlib
+    with open(FFN_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def committed_traffic():
+    """HBM bytes per ffn_gate_up launch from the committed counter summary, if
+    it was taken on the current kernel source; else None."""
+    try:
+        lines = open(COUNTERS_MD).read().splitlines()
+    except OSError:
+        return None
+    kv = dict(l.split(": ", 1) for l in lines if l.startswith(("traffic_bytes_per_launch: ", "expert_ffn_source_sha: ")))
+    if kv.get("expert_ffn_source_sha") != ffn_source_sha():
+        return None
+    return int(kv["traffic_bytes_per_launch"])
+
+
+def counter_means(path, counter):
+    """Mean counter value per kernel name from a rocprofv3 counter_collection.csv."""
+    import csv
+    acc = {}
+    for r in csv.DictReader(open(path)):
+        if r.get("Counter_Name") != counter:
+            continue
+        name = r["Kernel_Name"]
+        v = float(r["Counter_Value"])
+        s, n = acc.get(name, (0.0, 0))
+        acc[name] = (s + v, n + 1)
+    return {k: (s / n, n) for k, (s, n) in acc.items()}
+
+
+def summarize_counters(fetch_csv, write_csv):
+    f = counter_means(fetch_csv, "FETCH_SIZE")
+    w = counter_means(write_csv, "WRITE_SIZE")
+
+    def pick(d, key):
+        m = [(k, v) for k, v in d.items() if key in k]
+        if not m:
+            raise SystemExit(f"no {key} dispatches in the counter file")
+        return m[0][1]
+
+    cf, _ = pick(f, "calib_copy_kernel")
+    cw, _ = pick(w, "calib_copy_kernel")
+    gf, n_g = pick(f, "ffn_gate_up")
+    gw, _ = pick(w, "ffn_gate_up")
+    df, _ = pick(f, "ffn_down")
+    dw, _ = pick(w, "ffn_down")
+    kf = CALIB_BYTES / (cf * 1024.0)
+    kw = CALIB_BYTES / (cw * 1024.0)
+    up_bytes = gf * 1024 * kf + gw * 1024 * kw
+    dn_bytes = df * 1024 * kf + dw * 1024 * kw
+    alg_up = 2 * 2 * 4096 * 14336 * 2
+    alg_dn = 2 * 4096 * 14336 * 2
+    cmd_f = ("rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/pmc_fetch -o fetch --output-format csv "
+             "-- python -u $R/bench.py --counters")
+    cmd_w = cmd_f.replace("FETCH_SIZE", "WRITE_SIZE").replace("pmc_fetch", "pmc_write").replace("-o fetch", "-o write")
+    out = [
+        "# HBM traffic counters: ffn_gate_up / ffn_down, Mixtral-8x7B shapes, batch 1",
+        "",
+        "Commands (run from `/tmp` with `TMPDIR=/tmp`, repository at `$R`), one counter per run:",
+        "",
+        "```", cmd_f, cmd_w, "```",
+        "",
+        f"The profiled workload runs {COUNTER_TOKENS} decode tokens of the HBM-resident stack (2 experts",
+        f"per layer) and then {CALIB_BYTES >> 30} GiB copies with `stmoe_calib_copy` (reads and writes exactly",
+        f"{CALIB_BYTES} bytes each).  Counters are in KiB per dispatch.",
+        "",
+        "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB |",
+        "|---|---|---|---|",
+        f"| `calib_copy_kernel` (1 GiB) | - | {cf:.0f} | {cw:.0f} |",
+        f"| `ffn_gate_up` | {n_g} | {gf:.0f} | {gw:.0f} |",
+        f"| `ffn_down` | - | {df:.0f} | {dw:.0f} |",
+        "",
+        f"Scale factors from the copy kernel: fetch {kf:.4f} bytes per counted byte, write {kw:.4f}.",
+        "",
+        f"ffn_gate_up: measured {up_bytes / 1e6:.1f} MB per launch against {alg_up / 1e6:.1f} MB algorithmic "
+        f"({up_bytes / alg_up:.4f}x).",
+        f"ffn_down: measured {dn_bytes / 1e6:.1f} MB per launch against {alg_dn / 1e6:.1f} MB algorithmic "
+        f"({dn_bytes / alg_dn:.4f}x).",
+        "",
+        f"traffic_bytes_per_launch: {int(round(up_bytes))}",
+        f"expert_ffn_source_sha: {ffn_source_sha()}",
+    ]
+    print("\n".join(out))
+
+
+def counters_workload():
+    """Fixed workload for the rocprofv3 --pmc passes: decode tokens of the
+    resident Mixtral-shaped stack, then calibration copies of known size."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["mixtral"]
+    wl = Workload(cfg)
+    pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+    pred.profile(wl.prof)
+    ctx = make_ctx(wl, pred)
+    y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
+    run_tokens(ctx, wl, 0, COUNTER_TOKENS, y, S.MODE_STMOE)
+    torch.cuda.synchronize()
+    src = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        S.calib_copy(src, dst, CALIB_BYTES)
+    torch.cuda.synchronize()
+    ctx.close()
+    pred.close()
+    log("counters workload done")
+
+
+def achievable_read_gbps(nbytes=4 << 30, reps=10):
+    """Streaming-read bandwidth of stmoe_calib_read (the FFN's load pattern), event-timed."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    src.zero_()
+    out = torch.empty(S.calib_read_out_words(nbytes), dtype=torch.int32, device="cuda:0")
+    S.calib_read(src, nbytes, out)
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record()
+    for _ in range(reps):
+        S.calib_read(src, nbytes, out)
+    s1.record()
+    torch.cuda.synchronize()
+    ms = s0.elapsed_time(s1)
+    del src
+    return nbytes * reps / (ms * 1e-3) / 1e9
 
 
 class Workload:
@@ -174,12 +315,19 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
     ptrs = [pool.ptr + (i % M) * blob for i in range(n_all)]
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
     out = {}
-    for name, mode in (("on_demand", S.MODE_ON_DEMAND), ("st_moe", S.MODE_STMOE)):
+    # (name, mode, min prediction score to prefetch, max prefetches per layer)
+    variants = [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C),
+                ("st_moe", S.MODE_STMOE, 2, cfg.C),
+                ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K),
+                ("ht_only", S.MODE_HT_ONLY, 2, cfg.C),
+                ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C)]
+    for name, mode, min_score, max_pf in variants:
         cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, blob, n_stage, arena, ptrs, demand, side)
         cache.warm(wl.warm)
         pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
         pred.profile(wl.prof)
         ctx = make_ctx(wl, pred, cache)
+        ctx.set_prefetch(min_score, max_pf)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         run_tokens(ctx, wl, 0, n_tokens, y, mode)
@@ -190,7 +338,8 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
         cst = cache.stats()
         st = pred.stats()
         copies = cst["demand"] + cst["overflow"] + cst["prefetch"]
-        rec = dict(tokens=n_tokens, seconds=round(dt, 4),
+        rec = dict(tokens=n_tokens, seconds=round(dt, 4), prefetch_min_score=min_score,
+                   prefetch_max_per_layer=max_pf,
                    tokens_per_s=round(cfg.B * n_tokens / dt, 3),
                    ms_per_token=round(1e3 * dt / n_tokens, 3),
                    stall_ms_per_token=round(1e3 * dt / n_tokens - resident_ms_per_token, 3),
@@ -205,8 +354,9 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
         ctx.close()
         pred.close()
         cache.close()
-    od, st = out["on_demand"]["stall_ms_per_token"], out["st_moe"]["stall_ms_per_token"]
-    out["stall_reduction"] = round(1.0 - st / od, 4) if od > 0 else None
+    od = out["on_demand"]["stall_ms_per_token"]
+    out["stall_reduction"] = {name: (round(1.0 - out[name]["stall_ms_per_token"] / od, 4) if od > 0 else None)
+                              for name, *_ in variants if name != "on_demand"}
     out["cache_slots_per_layer"] = cfg.C
     out["host_pool"] = {"distinct_blobs": M, "experts": n_all, "slot_of_expert": "(l*E + e) mod distinct_blobs"}
     out["h2d_link"] = "PCIe, pinned host memory, hipMemcpyAsync on demand/side streams"
@@ -269,6 +419,9 @@ def cpu_baseline(wl, n_tokens):
 
 def main():
     args = parse()
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (this build has no "
               f"multi-GPU path)", file=sys.stderr)
@@ -278,6 +431,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.counters:
+        counters_workload()
+        return
     cfg = W.CONFIGS[args.config]
     log(f"workload {cfg.name}")
     wl = Workload(cfg)
@@ -312,7 +468,8 @@ def main():
         "roofline": {
             "bound": "hbm", "kernel": "ffn_gate_up",
             "achieved": round(up_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-            "frac": round(up_gbps / PEAK_HBM_GBPS, 4), "traffic": None,
+            "frac": round(up_gbps / PEAK_HBM_GBPS, 4),
+            "traffic": committed_traffic() if cfg.name == W.CONFIGS["mixtral"].name else None,
             "bytes_per_launch": int(up_bytes / max(r["n_calls"], 1)),
             "avg_launch_us": round(1e3 * r["up_ms"] / max(r["n_calls"], 1), 3),
             "launches": r["n_calls"],
@@ -327,6 +484,10 @@ def main():
             "precision": round(float(stats[:, 0].sum() / max(stats[:, 2].sum(), 1)), 4),
         },
     }
+    read_gbps = achievable_read_gbps()
+    out["achievable_read_gbps"] = round(read_gbps, 1)
+    out["roofline"]["frac_of_achievable_read"] = round(up_gbps / read_gbps, 4)
+    log(f"streaming-read probe: {read_gbps:.0f} GB/s")
     if args.offload_tokens > 0:
         out["offload"] = offload(wl, args.offload_tokens, ms_per_step, args.pinned_gb)
     if args.cpu_tokens > 0:

@@ -132,12 +132,13 @@ int stmoe_update(stmoe_predictor* p, int layer, const int32_t* sel_prev,
  *            score[b][f] = sum_{e in sel_cur[b]} conf of f in CCT_layer[e]
  *                          + 2 * [f in HT[layer+1][b]]
  *   mask     device out [E] uint8 or NULL: 1 where any row scores >= 2
+ *   max_score device out [E] uint8 or NULL: max over rows of score[b][f]
  *   ranked   device out [E] int32 or NULL: experts with mask = 1 ordered by
  *            (max over rows of score desc, index asc), then -1 padding
  *   n_ranked device out [1] int32 or NULL: number of such experts */
 int stmoe_predict(stmoe_predictor* p, int layer, const int32_t* sel_cur, int use,
-                  uint8_t* score, uint8_t* mask, int32_t* ranked, int32_t* n_ranked,
-                  void* stream);
+                  uint8_t* score, uint8_t* mask, uint8_t* max_score, int32_t* ranked,
+                  int32_t* n_ranked, void* stream);
 
 /* Copy the tables to host memory (any pointer may be NULL).  [sync]
  *   co [L-1][E][E] int32, cct_idx / cct_conf [L-1][E][K] uint8,
@@ -288,6 +289,12 @@ int moe_ctx_destroy(moe_ctx* ctx);
  * Layer-0 predictions come from HT[0]; the prefetch for layer 0 of the next
  * token is issued at layer L-1. */
 int moe_decode_layer(moe_ctx* ctx, int token, int layer, const void* x, float* y, int mode);
+/* Prefetch admission (cache only).  A predicted expert is prefetched only if
+ * its prediction score (max over rows, Eq. 1) is at least min_score, and at
+ * most max_per_layer experts are prefetched per layer (the ranked order
+ * decides which).  Defaults: min_score = 2 (the paper's threshold) and
+ * max_per_layer = the cache's slots per layer. */
+int moe_ctx_set_prefetch(moe_ctx* ctx, int min_score, int max_per_layer);
 /* All L layers of one token: xs device [L][B][H], ys device out [L][B][H]. */
 int moe_decode_token(moe_ctx* ctx, int token, const void* xs, float* ys, int mode);
 /* Last routing of each layer: host out idx [L][B][K] int32, w [L][B][K] fp32.  [sync] */
@@ -300,6 +307,19 @@ int moe_ctx_last_routing(moe_ctx* ctx, int32_t* idx, float* w);
 int moe_ctx_set_timing(moe_ctx* ctx, int enable);
 int moe_ctx_timing(moe_ctx* ctx, double* up_ms, double* down_ms, int64_t* n_calls,
                    int64_t* n_experts);
+
+/* ------------------------------------------------------------------------
+ * Measurement kernels of known traffic (not part of the decode path).
+ *   stmoe_calib_copy: dst[i] = src[i] over `bytes` (multiple of 16, 16-byte
+ *     aligned): reads and writes exactly `bytes`; used to turn the
+ *     FETCH_SIZE / WRITE_SIZE hardware counters into bytes.
+ *   stmoe_calib_read: streams `bytes` with the expert FFN's non-temporal
+ *     16-byte loads; out (device, stmoe_calib_read_out_words(bytes) words)
+ *     receives one checksum word per workgroup.
+ * ---------------------------------------------------------------------- */
+int stmoe_calib_copy(const void* src, void* dst, size_t bytes, void* stream);
+size_t stmoe_calib_read_out_words(size_t bytes);
+int stmoe_calib_read(const void* src, size_t bytes, unsigned* out, void* stream);
 
 #ifdef __cplusplus
 }

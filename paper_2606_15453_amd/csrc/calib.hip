@@ -1,0 +1,75 @@
+// Measurement kernels of known traffic, for pricing the hot-path kernels:
+//   stmoe_calib_copy   reads n bytes and writes n bytes (16-byte vector copy);
+//                      its FETCH_SIZE / WRITE_SIZE counter readings give the
+//                      factor that turns those counters into bytes.
+//   stmoe_calib_read   reads n bytes with the same non-temporal 16-byte loads
+//                      as the expert FFN and writes one word per workgroup:
+//                      the achievable streaming-read bandwidth of the chip.
+#include "common.h"
+
+namespace stmoe {
+namespace {
+
+constexpr int kThreads = 256;
+
+__global__ __launch_bounds__(kThreads) void calib_copy_kernel(const uint4* src, uint4* dst, size_t n) {
+    const size_t stride = size_t(gridDim.x) * kThreads;
+    for (size_t i = size_t(blockIdx.x) * kThreads + threadIdx.x; i < n; i += stride) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(kThreads) void calib_read_kernel(const char* src, size_t n, unsigned* out) {
+    const size_t stride = size_t(gridDim.x) * kThreads;
+    unsigned acc = 0;
+    size_t i = size_t(blockIdx.x) * kThreads + threadIdx.x;
+    for (; i + stride < n; i += 2 * stride) {
+        const u32x4 a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + i);
+        const u32x4 b = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + i + stride);
+        acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w;
+    }
+    if (i < n) {
+        const u32x4 a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + i);
+        acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    }
+    // keep the loads live: one word per workgroup
+    for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o, 64);
+    __shared__ unsigned w[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) w[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) out[blockIdx.x] = w[0] ^ w[1] ^ w[2] ^ w[3];
+}
+
+unsigned grid_for(size_t n16) {
+    size_t g = (n16 + kThreads - 1) / kThreads;
+    if (g > 8192) g = 8192;
+    return unsigned(g < 1 ? 1 : g);
+}
+
+}  // namespace
+}  // namespace stmoe
+
+using namespace stmoe;
+
+extern "C" int stmoe_calib_copy(const void* src, void* dst, size_t bytes, void* stream) {
+    clear_error();
+    STMOE_CHECK(src && dst && bytes > 0 && bytes % 16 == 0, "null pointer or size not a multiple of 16");
+    STMOE_CHECK((reinterpret_cast<uintptr_t>(src) & 15) == 0 && (reinterpret_cast<uintptr_t>(dst) & 15) == 0,
+                "pointers must be 16-byte aligned");
+    const size_t n = bytes / 16;
+    hipLaunchKernelGGL(calib_copy_kernel, dim3(grid_for(n)), dim3(kThreads), 0, as_stream(stream),
+                       reinterpret_cast<const uint4*>(src), reinterpret_cast<uint4*>(dst), n);
+    STMOE_LAUNCHED();
+    return STMOE_OK;
+}
+
+extern "C" size_t stmoe_calib_read_out_words(size_t bytes) { return grid_for(bytes / 16); }
+
+extern "C" int stmoe_calib_read(const void* src, size_t bytes, unsigned* out, void* stream) {
+    clear_error();
+    STMOE_CHECK(src && out && bytes > 0 && bytes % 16 == 0, "null pointer or size not a multiple of 16");
+    STMOE_CHECK((reinterpret_cast<uintptr_t>(src) & 15) == 0, "src must be 16-byte aligned");
+    const size_t n = bytes / 16;
+    hipLaunchKernelGGL(calib_read_kernel, dim3(grid_for(n)), dim3(kThreads), 0, as_stream(stream),
+                       reinterpret_cast<const char*>(src), n, out);
+    STMOE_LAUNCHED();
+    return STMOE_OK;
+}

@@ -19,6 +19,10 @@ namespace stmoe {
 int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, int H, int I, int E,
                int dtype, const void* const* eptr, const void* const* sptr, int n_shared,
                float* y, void* ws, hipStream_t s, unsigned long long* n_experts, hipEvent_t ev_mid);
+int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int renorm, int32_t* idx,
+                        float* w, void* route_ws, stmoe_predictor* p, int layer, const int32_t* sel_prev,
+                        int use, int online, int32_t* ranked, int32_t* n_ranked, uint8_t* max_score,
+                        hipStream_t s);
 
 namespace {
 
@@ -46,14 +50,15 @@ struct moe_ctx {
     hipStream_t s = nullptr;
     int32_t* idx = nullptr;                // [L][B][K] device
     float* w = nullptr;                    // [L][B][K] device
-    int32_t* ranked = nullptr;             // [E + 1] device: ranked list, then its length
+    int32_t* ranked = nullptr;             // device: ranked [E], n_ranked [1], max scores [E] (uint8)
     void* route_ws = nullptr;
     size_t route_ws_bytes = 0;
     void* ffn_ws = nullptr;
     size_t ffn_ws_bytes = 0;
     const void** tables = nullptr;         // [L][E] device blob pointers
     const void** shared = nullptr;         // [L][n_shared] device blob pointers
-    int32_t* rec = nullptr;                // pinned host: idx [B][K], ranked [E], n_ranked
+    int32_t* rec = nullptr;                // pinned host: idx [B][K], ranked [E], n_ranked, max scores [E] (uint8)
+    int pf_min_score = 2, pf_max = 1 << 30;
     hipEvent_t rec_ev = nullptr;
     std::vector<const void*> host_table;   // [E] scratch for the cache's answers
     bool started = false;
@@ -67,6 +72,10 @@ struct moe_ctx {
 };
 
 namespace {
+
+// device/host record of one prediction: ranked [E] int32, n_ranked int32, max scores [E] uint8
+size_t ranked_bytes(int E) { return size_t(E + 1) * sizeof(int32_t) + size_t(E); }
+uint8_t* max_scores(int32_t* ranked, int E) { return reinterpret_cast<uint8_t*>(ranked + E + 1); }
 
 void free_ctx(moe_ctx* c) {
     if (!c) return;
@@ -103,10 +112,14 @@ int set_table(moe_ctx* c, int layer, const std::vector<const void*>& tab) {
     return STMOE_OK;
 }
 
-// Copy the ranked prediction to the host and prefetch it.
+// Prefetch the ranked prediction held in the host record, subject to the
+// admission knobs (minimum score, maximum per layer).
 int prefetch_from_record(moe_ctx* c, int target, int64_t stamp) {
-    const int32_t* ranked = c->rec + c->B * c->K;
-    const int n = ranked[c->E];
+    int32_t* ranked = c->rec + c->B * c->K;
+    const uint8_t* ms = max_scores(ranked, c->E);
+    int n = 0;
+    const int total = ranked[c->E];
+    while (n < total && n < c->pf_max && ms[ranked[n]] >= c->pf_min_score) ++n;
     if (n <= 0) return STMOE_OK;
     const int rc = expert_cache_prefetch(c->cache, target, ranked, n, stamp);
     return rc < 0 ? rc : STMOE_OK;
@@ -116,8 +129,8 @@ int fetch_record(moe_ctx* c, const int32_t* idx_dev, bool with_ranked) {
     STMOE_HIP(hipMemcpyAsync(c->rec, idx_dev, size_t(c->B) * c->K * sizeof(int32_t),
                              hipMemcpyDeviceToHost, c->s));
     if (with_ranked)
-        STMOE_HIP(hipMemcpyAsync(c->rec + c->B * c->K, c->ranked, size_t(c->E + 1) * sizeof(int32_t),
-                                 hipMemcpyDeviceToHost, c->s));
+        STMOE_HIP(hipMemcpyAsync(c->rec + c->B * c->K, c->ranked, ranked_bytes(c->E), hipMemcpyDeviceToHost,
+                                 c->s));
     STMOE_HIP(hipEventRecord(c->rec_ev, c->s));
     STMOE_HIP(hipEventSynchronize(c->rec_ev));
     return STMOE_OK;
@@ -164,14 +177,14 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMalloc(&c->idx, LBK * sizeof(int32_t));
     if (e == hipSuccess) e = hipMalloc(&c->w, LBK * sizeof(float));
-    if (e == hipSuccess) e = hipMalloc(&c->ranked, size_t(c->E + 1) * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMalloc(&c->ranked, ranked_bytes(c->E));
     if (e == hipSuccess) e = hipMalloc(&c->route_ws, c->route_ws_bytes);
     if (e == hipSuccess) e = hipMalloc(&c->ffn_ws, c->ffn_ws_bytes);
     if (e == hipSuccess) e = hipMalloc(&c->tables, size_t(c->L) * c->E * sizeof(void*));
     if (e == hipSuccess && c->n_shared)
         e = hipMalloc(&c->shared, size_t(c->L) * c->n_shared * sizeof(void*));
     if (e == hipSuccess) e = hipMalloc(&c->n_experts, sizeof(unsigned long long));
-    if (e == hipSuccess) e = hipHostMalloc(&c->rec, size_t(c->B * c->K + c->E + 1) * sizeof(int32_t));
+    if (e == hipSuccess) e = hipHostMalloc(&c->rec, size_t(c->B * c->K) * sizeof(int32_t) + ranked_bytes(c->E));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->rec_ev, hipEventDisableTiming);
     if (e == hipSuccess) e = hipMemset(c->route_ws, 0, c->route_ws_bytes);
     if (e == hipSuccess) e = hipMemset(c->ffn_ws, 0, c->ffn_ws_bytes);
@@ -217,7 +230,7 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
         c->started = true;
         if (use) {
             if (int rc = stmoe_predict(c->pred, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr,
-                                       c->ranked, c->ranked + E, c->s))
+                                       max_scores(c->ranked, E), c->ranked, c->ranked + E, c->s))
                 return rc;
             if (c->cache) {
                 if (int rc = fetch_record(c, idx_l, true)) return rc;
@@ -226,23 +239,18 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
         }
     }
 
-    // R: gating
-    if (int rc = moe_route_topk(x, c->router[layer], B, c->H, E, K, c->dtype, c->renorm, idx_l, w_l,
-                                nullptr, c->route_ws, c->route_ws_bytes, c->s))
-        return rc;
-    // V + P: verify/update against the previous layer, predict the next one
+    // R + V + P: gating, verify/update against the previous layer and the
+    // next layer's prediction, fused into one launch
     if (use) {
         const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
-        if (int rc = stmoe_update(c->pred, layer, prev, idx_l, 1, c->s)) return rc;
-        if (layer + 1 < L) {
-            if (int rc = stmoe_predict(c->pred, layer, idx_l, use, nullptr, nullptr, c->ranked,
-                                       c->ranked + E, c->s))
-                return rc;
-        } else {
-            if (int rc = stmoe_predict(c->pred, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr,
-                                       c->ranked, c->ranked + E, c->s))
-                return rc;
-        }
+        if (int rc = fused_route_predict(x, c->router[layer], c->H, c->dtype, c->renorm, idx_l, w_l,
+                                         c->route_ws, c->pred, layer, prev, use, 1, c->ranked,
+                                         c->ranked + E, max_scores(c->ranked, E), c->s))
+            return rc;
+    } else {
+        if (int rc = moe_route_topk(x, c->router[layer], B, c->H, E, K, c->dtype, c->renorm, idx_l, w_l,
+                                    nullptr, c->route_ws, c->route_ws_bytes, c->s))
+            return rc;
     }
     // ML: make the selection resident
     if (c->cache) {
@@ -291,6 +299,15 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
     }
     c->last_token = token;
     c->last_layer = layer;
+    return STMOE_OK;
+}
+
+extern "C" int moe_ctx_set_prefetch(moe_ctx* c, int min_score, int max_per_layer) {
+    clear_error();
+    STMOE_CHECK(c, "null ctx");
+    STMOE_CHECK(min_score >= 0 && max_per_layer >= 0, "knobs must be >= 0");
+    c->pf_min_score = min_score;
+    c->pf_max = max_per_layer;
     return STMOE_OK;
 }
 

@@ -9,27 +9,14 @@
 // which is exact and order-free.
 #include <vector>
 
-#include "common.h"
+#include "gating_dev.h"
+#include "predictor_dev.h"
 
-struct stmoe_predictor {
-    int L, E, K, B;
-    int32_t* co;                 // [L-1][E][E] profiling co-activation counts
-    uint8_t* cct_idx;            // [L-1][E][K]
-    uint8_t* cct_conf;           // [L-1][E][K]
-    uint8_t* ht;                 // [L][B][K], each row sorted ascending
-    uint8_t* pend;               // [L][B][E] last prediction scores made for each layer
-    unsigned long long* stats;   // [L][3]: hits, |A|, |P|
-    bool profiled;
-};
 
 namespace stmoe {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kConfInit = 2;   // "10", preferred
-constexpr int kConfMax = 3;    // "11", strongly preferred
-constexpr int kThreshold = 2;  // prefetch when the score reaches "10"
-constexpr int kHtScore = 2;    // HT confidences stay at "10"
+using namespace pred;
 
 // ---------------------------------------------------------------- profiling
 // Algorithm 1, counting: one workgroup per (profiling token, layer pair).
@@ -80,153 +67,35 @@ __global__ __launch_bounds__(kThreads) void ht_init_kernel(const int32_t* sel_la
     sorted_row(sel_last + (size_t(b) * L + l) * K, K, ht + (size_t(l) * B + b) * K);
 }
 
-// ------------------------------------------------------------------- update
-// Algorithm 3 on CCT_{layer-1} for the rows selected at layer-1, then the HT
-// overwrite and the hit count against the prediction made for this layer.
-struct UpdateArgs {
-    const int32_t* sel_prev;   // [B][K] or null at layer 0
-    const int32_t* sel_cur;    // [B][K]
-    uint8_t* cidx;             // CCT_{layer-1} [E][K] or null
-    uint8_t* cconf;
-    uint8_t* ht;               // HT[layer] [B][K]
-    const uint8_t* pend;       // [B][E] prediction for this layer
-    unsigned long long* stats; // [3]
-    int B, E, K, online;
-};
-
+// ------------------------------------------------------ update and predict
 __global__ __launch_bounds__(kThreads) void update_kernel(UpdateArgs a) {
-    __shared__ int32_t F[kMaxK];          // actual set, ascending
-    __shared__ uint8_t snap[kMaxK * kMaxK];  // entries before this row's update
-    __shared__ uint8_t repl[kMaxK * kMaxK];  // slot is replaced
-    __shared__ unsigned hits, npred;
-    const int tid = threadIdx.x, K = a.K, KK = a.K * a.K;
-    if (tid == 0) { hits = 0; npred = 0; }
-    for (int b = 0; b < a.B; ++b) {
-        const int32_t* cur = a.sel_cur + b * K;
-        if (tid < K) {
-            const int v = cur[tid];
-            int rank = 0;
-            for (int j = 0; j < K; ++j) rank += cur[j] < v;
-            F[rank] = v;
-        }
-        int e = 0, s = 0, conf = 0;
-        bool hit = false;
-        const bool upd = a.cidx != nullptr && a.online && tid < KK;
-        bool upd_ok = upd;
-        if (upd) {
-            e = a.sel_prev[b * K + tid / K];
-            s = tid % K;
-            upd_ok = e >= 0 && e < a.E;      // out-of-range selections are ignored
-            snap[tid] = upd_ok ? a.cidx[e * K + s] : 0xff;
-            conf = upd_ok ? a.cconf[e * K + s] : 1;
-        }
-        __syncthreads();
-        if (upd) {
-            const int f = snap[tid];
-            for (int j = 0; j < K; ++j) hit |= (F[j] == f);
-            repl[tid] = upd_ok && (!hit && conf == 0);
-        }
-        __syncthreads();
-        if (upd_ok) {
-            if (hit) {
-                conf = min(conf + 1, kConfMax);
-            } else if (conf > 0) {
-                conf -= 1;
-            } else {
-                // the rank-th expert of F (ascending) absent from the entry's snapshot
-                const int base = tid - s;
-                int rank = 0;
-                for (int q = 0; q < s; ++q) rank += repl[base + q];
-                int pick = -1;
-                for (int j = 0; j < K && pick < 0; ++j) {
-                    bool held = false;
-                    for (int q = 0; q < K; ++q) held |= (snap[base + q] == F[j]);
-                    if (!held) {
-                        if (rank == 0) pick = F[j];
-                        --rank;
-                    }
-                }
-                if (pick >= 0) a.cidx[e * K + s] = uint8_t(pick);
-                conf = kConfInit;
-            }
-            a.cconf[e * K + s] = uint8_t(conf);
-        }
-        // verification against the prediction made for this layer
-        if (tid < K && cur[tid] >= 0 && cur[tid] < a.E && a.pend[b * a.E + cur[tid]] >= kThreshold)
-            atomicAdd(&hits, 1u);
-        for (int f = tid; f < a.E; f += kThreads)
-            if (a.pend[b * a.E + f] >= kThreshold) atomicAdd(&npred, 1u);
-        if (tid < K) a.ht[b * K + tid] = uint8_t(F[tid]);
-        // next row may update the same entries: make this row's writes visible
-        __threadfence_block();
-        __syncthreads();
-    }
-    if (tid == 0) {
-        atomicAdd(&a.stats[0], (unsigned long long)hits);
-        atomicAdd(&a.stats[1], (unsigned long long)(a.B * K));
-        atomicAdd(&a.stats[2], (unsigned long long)npred);
-    }
+    __shared__ UpdateShared sh;
+    update_body(a, sh);
 }
 
-// ------------------------------------------------------------------ predict
-// Algorithm 2 with Eq. 1: score_b[f] = sum_{e in A[b]} conf of f in CCT[e]
-// + 2 [f in HT_next[b]]; PrefetchSet = {f : score >= 2}.
-struct PredictArgs {
-    const int32_t* sel_cur;    // [B][K] (unused when cidx is null)
-    const uint8_t* cidx;       // CCT_layer [E][K] or null (layer -1 or HT-only)
-    const uint8_t* cconf;
-    const uint8_t* ht_next;    // HT[layer+1] [B][K] or null (CCT-only)
-    uint8_t* pend;             // [B][E] kept for the next update's hit count
-    uint8_t* score;            // [B][E] or null
-    uint8_t* mask;             // [E] or null
-    int32_t* ranked;           // [E] or null
-    int32_t* n_ranked;         // [1] or null
-    int B, E, K;
-};
-
 __global__ __launch_bounds__(kThreads) void predict_kernel(PredictArgs a) {
-    __shared__ int sc[kMaxB * kMaxE];
-    __shared__ int mx[kMaxE];
-    const int tid = threadIdx.x, K = a.K, E = a.E;
-    for (int i = tid; i < a.B * E; i += kThreads) sc[i] = 0;
+    __shared__ PredictShared sh;
+    predict_body(a, sh);
+}
+
+// One decode layer's router, verify/update and next-layer prediction in one
+// launch: the router's last workgroup keeps the selection in LDS and runs
+// the update and the prediction on it.
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void route_update_predict_kernel(gating::RouteArgs r, UpdateArgs u,
+                                                                        PredictArgs p) {
+    __shared__ float part[kMaxB][kThreads / 64];
+    __shared__ bool last;
+    __shared__ int32_t sel[kMaxB * kMaxK];
+    __shared__ UpdateShared ush;
+    __shared__ PredictShared psh;
+    if (!gating::logits_and_ticket<BF16>(r, part, last)) return;
+    gating::softmax_topk_tail(r, sel);
+    u.sel_cur = sel;
+    update_body(u, ush);
     __syncthreads();
-    for (int b = 0; b < a.B; ++b) {
-        if (a.cidx && tid < K * K) {
-            const int e = a.sel_cur[b * K + tid / K], s = tid % K;
-            if (e >= 0 && e < E) atomicAdd(&sc[b * E + a.cidx[e * K + s]], int(a.cconf[e * K + s]));
-        }
-        if (a.ht_next && tid < K) atomicAdd(&sc[b * E + a.ht_next[b * K + tid]], kHtScore);
-    }
-    __syncthreads();
-    for (int i = tid; i < a.B * E; i += kThreads) {
-        a.pend[i] = uint8_t(sc[i]);
-        if (a.score) a.score[i] = uint8_t(sc[i]);
-    }
-    for (int f = tid; f < E; f += kThreads) {
-        int m = 0;
-        for (int b = 0; b < a.B; ++b) m = max(m, sc[b * E + f]);
-        mx[f] = m;
-        if (a.mask) a.mask[f] = m >= kThreshold;
-    }
-    __syncthreads();
-    if (a.ranked || a.n_ranked) {
-        int count = 0;
-        for (int f = tid; f < E; f += kThreads) {
-            if (a.ranked) a.ranked[f] = -1;
-        }
-        __syncthreads();
-        for (int f = tid; f < E; f += kThreads) {
-            if (mx[f] < kThreshold) continue;
-            int rank = 0;
-            for (int g = 0; g < E; ++g)
-                rank += mx[g] >= kThreshold && (mx[g] > mx[f] || (mx[g] == mx[f] && g < f));
-            if (a.ranked) a.ranked[rank] = f;
-        }
-        if (a.n_ranked && tid == 0) {
-            for (int g = 0; g < E; ++g) count += mx[g] >= kThreshold;
-            *a.n_ranked = count;
-        }
-    }
+    if (p.cidx) p.sel_cur = sel;
+    predict_body(p, psh);
 }
 
 int check_sel_host(const int32_t* sel, size_t rows, int E, int K) {
@@ -340,26 +209,15 @@ extern "C" int stmoe_update(stmoe_predictor* p, int layer, const int32_t* sel_pr
         set_error("stmoe_update: predictor has not been profiled");
         return STMOE_ESTATE;
     }
-    UpdateArgs a;
-    a.sel_prev = sel_prev;
-    a.sel_cur = sel_cur;
-    a.cidx = layer >= 1 ? p->cct_idx + size_t(layer - 1) * p->E * p->K : nullptr;
-    a.cconf = layer >= 1 ? p->cct_conf + size_t(layer - 1) * p->E * p->K : nullptr;
-    a.ht = p->ht + size_t(layer) * p->B * p->K;
-    a.pend = p->pend + size_t(layer) * p->B * p->E;
-    a.stats = p->stats + size_t(layer) * 3;
-    a.B = p->B;
-    a.E = p->E;
-    a.K = p->K;
-    a.online = online ? 1 : 0;
+    const UpdateArgs a = update_args(p, layer, sel_prev, sel_cur, online);
     hipLaunchKernelGGL(update_kernel, dim3(1), dim3(kThreads), 0, as_stream(stream), a);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }
 
 extern "C" int stmoe_predict(stmoe_predictor* p, int layer, const int32_t* sel_cur, int use,
-                             uint8_t* score, uint8_t* mask, int32_t* ranked, int32_t* n_ranked,
-                             void* stream) {
+                             uint8_t* score, uint8_t* mask, uint8_t* max_score, int32_t* ranked,
+                             int32_t* n_ranked, void* stream) {
     clear_error();
     STMOE_CHECK(p, "null predictor");
     STMOE_CHECK(layer >= -1 && layer < p->L - 1, "layer must be in [-1, L-2]");
@@ -370,24 +228,53 @@ extern "C" int stmoe_predict(stmoe_predictor* p, int layer, const int32_t* sel_c
         set_error("stmoe_predict: predictor has not been profiled");
         return STMOE_ESTATE;
     }
-    const int tgt = layer + 1;
-    PredictArgs a;
-    a.sel_cur = sel_cur;
-    a.cidx = cct ? p->cct_idx + size_t(layer) * p->E * p->K : nullptr;
-    a.cconf = cct ? p->cct_conf + size_t(layer) * p->E * p->K : nullptr;
-    a.ht_next = (use & STMOE_USE_HT) ? p->ht + size_t(tgt) * p->B * p->K : nullptr;
-    a.pend = p->pend + size_t(tgt) * p->B * p->E;
-    a.score = score;
-    a.mask = mask;
-    a.ranked = ranked;
-    a.n_ranked = n_ranked;
-    a.B = p->B;
-    a.E = p->E;
-    a.K = p->K;
+    const PredictArgs a = predict_args(p, layer, sel_cur, use, score, mask, max_score, ranked, n_ranked);
     hipLaunchKernelGGL(predict_kernel, dim3(1), dim3(kThreads), 0, as_stream(stream), a);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }
+
+namespace stmoe {
+// Internal: router + verify/update at `layer` + prediction of the next layer
+// (layer 0 of the next token after the last layer) in one launch.  The
+// caller has validated the shapes; the routing workspace follows
+// moe_route_workspace_bytes.
+int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int renorm, int32_t* idx,
+                        float* w, void* route_ws, stmoe_predictor* p, int layer, const int32_t* sel_prev,
+                        int use, int online, int32_t* ranked, int32_t* n_ranked, uint8_t* max_score,
+                        hipStream_t s) {
+    if (!p->profiled) {
+        set_error("moe_decode_layer: predictor has not been profiled");
+        return STMOE_ESTATE;
+    }
+    gating::RouteArgs r;
+    r.x = x;
+    r.wg = w_gate;
+    r.B = p->B;
+    r.H = H;
+    r.E = p->E;
+    r.K = p->K;
+    r.renorm = renorm ? 1 : 0;
+    r.bf16 = dtype == STMOE_BF16;
+    r.idx = idx;
+    r.w = w;
+    r.logits = nullptr;
+    r.zbuf = reinterpret_cast<float*>(route_ws);
+    r.ticket = reinterpret_cast<unsigned*>(reinterpret_cast<char*>(route_ws) +
+                                           (size_t(p->B) * p->E * sizeof(float) + 255) / 256 * 256);
+    const UpdateArgs u = update_args(p, layer, sel_prev, idx, online);
+    const PredictArgs q = layer + 1 < p->L
+                              ? predict_args(p, layer, idx, use, nullptr, nullptr, max_score, ranked, n_ranked)
+                              : predict_args(p, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr, max_score,
+                                             ranked, n_ranked);
+    if (r.bf16)
+        hipLaunchKernelGGL(route_update_predict_kernel<true>, dim3(p->E), dim3(kThreads), 0, s, r, u, q);
+    else
+        hipLaunchKernelGGL(route_update_predict_kernel<false>, dim3(p->E), dim3(kThreads), 0, s, r, u, q);
+    STMOE_LAUNCHED();
+    return STMOE_OK;
+}
+}  // namespace stmoe
 
 extern "C" int stmoe_export(stmoe_predictor* p, int32_t* co, uint8_t* cct_idx, uint8_t* cct_conf,
                             uint8_t* ht) {

@@ -71,7 +71,7 @@ _SIGS = {
     "stmoe_destroy": (i32, [vp]),
     "stmoe_profile": (i32, [vp, vp, i32]),
     "stmoe_update": (i32, [vp, i32, vp, vp, i32, vp]),
-    "stmoe_predict": (i32, [vp, i32, vp, i32, vp, vp, vp, vp, vp]),
+    "stmoe_predict": (i32, [vp, i32, vp, i32, vp, vp, vp, vp, vp, vp]),
     "stmoe_export": (i32, [vp, vp, vp, vp, vp]),
     "stmoe_import": (i32, [vp, vp, vp, vp]),
     "stmoe_stats": (i32, [vp, vp]),
@@ -97,9 +97,13 @@ _SIGS = {
     "moe_ctx_destroy": (i32, [vp]),
     "moe_decode_layer": (i32, [vp, i32, i32, vp, vp, i32]),
     "moe_decode_token": (i32, [vp, i32, vp, vp, i32]),
+    "moe_ctx_set_prefetch": (i32, [vp, i32, i32]),
     "moe_ctx_last_routing": (i32, [vp, vp, vp]),
     "moe_ctx_set_timing": (i32, [vp, i32]),
     "moe_ctx_timing": (i32, [vp, P(C.c_double), P(C.c_double), P(i64), P(i64)]),
+    "stmoe_calib_copy": (i32, [vp, vp, sz, vp]),
+    "stmoe_calib_read_out_words": (sz, [sz]),
+    "stmoe_calib_read": (i32, [vp, sz, vp, vp]),
 }
 
 for _name, (_res, _args) in _SIGS.items():
@@ -218,9 +222,9 @@ class Predictor:
         _call("stmoe_update", self.h, layer, _p(sel_prev), _p(sel_cur), int(online), _s(stream))
 
     def predict(self, layer, sel_cur, use=USE_BOTH, score=None, mask=None, ranked=None,
-                n_ranked=None, stream=None):
-        _call("stmoe_predict", self.h, layer, _p(sel_cur), use, _p(score), _p(mask), _p(ranked),
-              _p(n_ranked), _s(stream))
+                n_ranked=None, max_score=None, stream=None):
+        _call("stmoe_predict", self.h, layer, _p(sel_cur), use, _p(score), _p(mask), _p(max_score),
+              _p(ranked), _p(n_ranked), _s(stream))
 
     def export(self):
         L, E, K, B = self.L, self.E, self.K, self.B
@@ -388,6 +392,9 @@ class DecodeContext:
     def layer(self, token, layer, x, y, mode=MODE_STMOE):
         _call("moe_decode_layer", self.h, token, layer, _p(x), _p(y), mode)
 
+    def set_prefetch(self, min_score=2, max_per_layer=1 << 30):
+        _call("moe_ctx_set_prefetch", self.h, min_score, max_per_layer)
+
     def token(self, token, xs, ys, mode=MODE_STMOE):
         _call("moe_decode_token", self.h, token, _p(xs), _p(ys), mode)
 
@@ -406,3 +413,16 @@ class DecodeContext:
         nc, ne = i64(), i64()
         _call("moe_ctx_timing", self.h, C.byref(up), C.byref(down), C.byref(nc), C.byref(ne))
         return up.value, down.value, nc.value, ne.value
+
+
+# ------------------------------------------------------------- measurement
+def calib_copy(src, dst, nbytes, stream=None):
+    _call("stmoe_calib_copy", _p(src), _p(dst), nbytes, _s(stream))
+
+
+def calib_read(src, nbytes, out, stream=None):
+    _call("stmoe_calib_read", _p(src), nbytes, _p(out), _s(stream))
+
+
+def calib_read_out_words(nbytes):
+    return _lib.stmoe_calib_read_out_words(nbytes)

@@ -44,7 +44,7 @@ def test_invalid_arguments_rejected_without_device_work():
     assert rc == S.EINVAL
     rc = S._lib.moe_expert_ffn(16, 16, 16, 1, 2, 64, 64, 8, S.BF16, 16, None, 2, 16, 256, 1 << 20, None)
     assert rc == S.EINVAL      # shared experts without pointers
-    assert S._lib.stmoe_predict(None, 0, None, 3, None, None, None, None, None) == S.EINVAL
+    assert S._lib.stmoe_predict(None, 0, None, 3, None, None, None, None, None, None) == S.EINVAL
     assert S.blob_bytes(4096, 14336, S.BF16) == 3 * 4096 * 14336 * 2
 
 

@@ -30,18 +30,21 @@ def _run(L, E, K, B, prof, stream_sel, use=3, online=True):
     mask = torch.zeros(E, dtype=torch.uint8, device=DEV)
     ranked = torch.zeros(E, dtype=torch.int32, device=DEV)
     nr = torch.zeros(1, dtype=torch.int32, device=DEV)
+    mx = torch.zeros(E, dtype=torch.uint8, device=DEV)
     use_cct, use_ht = bool(use & 1), bool(use & 2)
 
     def check_pred(sc_ref):
         torch.cuda.synchronize()
         assert np.array_equal(score.cpu().numpy(), sc_ref)
         assert np.array_equal(mask.cpu().numpy(), (sc_ref.max(axis=0) >= 2).astype(np.uint8))
+        assert np.array_equal(mx.cpu().numpy(), sc_ref.max(axis=0).astype(np.uint8))
         rr = STPredictor.ranked_union(sc_ref)
         assert int(nr.item()) == len(rr)
         r = ranked.cpu().numpy()
         assert r[:len(rr)].tolist() == rr and np.all(r[len(rr):] == -1)
 
-    gp.predict(-1, None, use=use & 2, score=score, mask=mask, ranked=ranked, n_ranked=nr)
+    gp.predict(-1, None, use=use & 2, score=score, mask=mask, ranked=ranked, n_ranked=nr,
+               max_score=mx)
     sc = ref.predict(-1, None, use_cct=False, use_ht=use_ht)
     check_pred(sc)
     hits = np.zeros((L, 3), np.int64)
@@ -58,11 +61,13 @@ def _run(L, E, K, B, prof, stream_sel, use=3, online=True):
             gp.update(l, prev_dev, cur_dev, online=online)
             ref.update(l, prev_ref, cur, online=online)
             if l + 1 < L:
-                gp.predict(l, cur_dev, use=use, score=score, mask=mask, ranked=ranked, n_ranked=nr)
+                gp.predict(l, cur_dev, use=use, score=score, mask=mask, ranked=ranked, n_ranked=nr,
+                           max_score=mx)
                 sc = ref.predict(l, cur, use_cct=use_cct, use_ht=use_ht)
                 pend[l + 1] = sc
             else:
-                gp.predict(-1, None, use=use & 2, score=score, mask=mask, ranked=ranked, n_ranked=nr)
+                gp.predict(-1, None, use=use & 2, score=score, mask=mask, ranked=ranked, n_ranked=nr,
+                           max_score=mx)
                 sc = ref.predict(-1, None, use_cct=False, use_ht=use_ht)
                 pend[0] = sc
             check_pred(sc)

@@ -179,9 +179,9 @@ int moe_pack_expert(const void* w_gate, const void* w_up, const void* w_down, in
  *   shared_ptrs  device array [n_shared] of device blob pointers, or NULL
  *   y            device out [B][H] fp32 (overwritten)
  *   ws           device workspace of moe_expert_ffn_workspace_bytes(...) bytes,
- *                256-byte aligned, zero-filled by the caller once before its
- *                first use (it holds completion tickets that every call leaves
- *                at zero); calls sharing a workspace must be ordered on one stream
+ *                256-byte aligned (activations and partial sums; no initial
+ *                contents required); calls sharing it must be ordered on one
+ *                stream
  *   B < 8 runs the GEMV kernels; B >= 8 with bf16 and H, I multiples of 64
  *   runs the MFMA grouped-GEMM kernels (the SwiGLU activation then passes
  *   through bf16); other shapes fall back to the GEMV kernels.

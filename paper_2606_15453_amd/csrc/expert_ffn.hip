@@ -9,12 +9,15 @@
 // Two phases, two launches:
 //   gate/up  one workgroup = (expert slot, block of rows of W_gate and W_up):
 //            a[slot][b][i] = w_b * silu(W_gate[i] . x_b) * (W_up[i] . x_b)
-//   down     one workgroup = (block of output rows h, group of expert slots):
-//            sum over the group's slots (ascending expert index, shared
-//            experts last) of W_down_slot[h] . a[slot][b].  With more than one
-//            group the groups' partial sums go to the workspace and the last
-//            workgroup of each row block (a completion ticket) adds them in
-//            group order, so the summation order depends only on the routing.
+//   down     sum over slots (ascending expert index, shared experts last)
+//            of W_down_slot[h] . a[slot][b].  The GEMV kernels give each
+//            workgroup a block of output rows and split the slots (or the row
+//            length) over its four waves, combining them through LDS; the MFMA
+//            kernel splits slots over workgroups into partial sums that a
+//            third small kernel adds in group order.  No workgroup waits on
+//            another (device-scope fences between workgroups would write back
+//            the L2 of every XCD), and the summation order depends only on the
+//            routing, never on where the blobs live.
 //
 // Batch < 8: GEMV kernels.  A group of G lanes (64, 32 or 16, by row length)
 // owns R rows and strides over their 16-byte chunks; the activations come
@@ -50,8 +53,7 @@ struct FfnArgs {
     const void* const* sptr;         // [n_shared] or null
     int B, K, H, I, E, n_shared;
     void* act;                       // [slots][B][I]: fp32 (GEMV) or bf16 (MFMA)
-    float* part;                     // [ng][B][H] partial sums (ng > 1)
-    unsigned* tick;                  // [row blocks] completion tickets, zero between launches
+    float* part;                     // [ng][B][H] partial sums of the MFMA down phase (ng > 1)
     float* y;                        // [B][H]
     unsigned long long* n_experts;   // optional: += distinct routed experts (block 0)
     int ng, spg;                     // expert-slot groups of the down phase, slots per group
@@ -64,7 +66,6 @@ struct Plan {
     int expert[kMaxSlots];           // routed slots: expert index; shared slots: -1 - s
     unsigned tok[kMaxSlots];         // token bit mask per slot
     int n_routed, n_slots;
-    bool last;                       // this workgroup took the last ticket
 };
 
 // Build the slot plan in LDS (all threads participate; ends with a barrier).
@@ -182,42 +183,6 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     return uint16_t((u + (((u >> 16) & 1u) + 0x7fffu)) >> 16);
 }
 
-// Down-phase epilogue.  One slot group: store y.  Several: store this
-// group's partial sums, take the row block's ticket; the workgroup that takes
-// the last ticket adds the partials in group order and resets the ticket.
-struct DownEpilogue {
-    const FfnArgs& a;
-    Plan& p;
-    int rb, grp, h_base, rows;
-
-    __device__ __forceinline__ void put(int b, int h, float v) const {
-        if (a.ng == 1)
-            a.y[size_t(b) * a.H + h] = v;
-        else
-            a.part[(size_t(grp) * a.B + b) * a.H + h] = v;
-    }
-    __device__ __forceinline__ void finish() const {
-        if (a.ng == 1) return;
-        __threadfence();
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            const unsigned t = atomicAdd(&a.tick[rb], 1u);
-            p.last = (t == unsigned(a.ng) - 1);
-        }
-        __syncthreads();
-        if (!p.last) return;
-        __threadfence();
-        for (int q = threadIdx.x; q < rows * a.B; q += kThreads) {
-            const int b = q / rows, h = h_base + q % rows;
-            if (h >= a.H) continue;
-            float s = 0.f;
-            for (int g = 0; g < a.ng; ++g) s += a.part[(size_t(g) * a.B + b) * a.H + h];
-            a.y[size_t(b) * a.H + h] = s;
-        }
-        if (threadIdx.x == 0) atomicExch(&a.tick[rb], 0u);
-    }
-};
-
 // ============================================================================
 // GEMV path (batch < 8)
 // ============================================================================
@@ -300,16 +265,107 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
     }
 }
 
-// Down, rows owned by lane groups (rows of at most 512 chunks).
+// gate/up, whole workgroup per block of R rows: the 256 lanes stride the
+// rows' chunks together (every lane issues all its loads of an iteration at
+// once), then the four waves' sums combine through LDS.
+template <bool BF, int R, int NB>
+__global__ __launch_bounds__(kThreads) void ffn_gate_up_wg(FfnArgs a, int blocks_per_slot) {
+    __shared__ Plan p;
+    __shared__ float red[kWaves][2][R][NB];
+    build_plan(a, p);
+    const int j = blockIdx.x / blocks_per_slot;
+    if (j >= p.n_slots) return;
+    const int i0 = (blockIdx.x % blocks_per_slot) * R;
+    if (i0 >= a.I) return;   // I is a multiple of R
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const unsigned tm = p.tok[j];
+    constexpr int esz = BF ? 2 : 4;
+    const size_t rowb = size_t(a.H) * esz;
+    const char* blob = slot_blob(a, p, j);
+    const char* wg = blob + size_t(i0) * rowb;
+    const char* wu = blob + size_t(a.I) * rowb + size_t(i0) * rowb;
+    const char* xs = reinterpret_cast<const char*>(a.x);
+    const int cpr = int(rowb / 16);
+
+    float accg[R][NB], accu[R][NB];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) accg[r][b] = accu[r][b] = 0.f;
+
+    auto compute = [&](int c, const uint4 (&qg)[R], const uint4 (&qu)[R]) {
+        Chunk<BF> cg[R], cu[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) { cg[r].unpack(qg[r]); cu[r].unpack(qu[r]); }
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            if (!((tm >> b) & 1u)) continue;
+            Chunk<BF> cx;
+            cx.unpack(ld_cached(xs + b * rowb + size_t(c) * 16));
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                accg[r][b] = dotc<BF>(cg[r], cx, accg[r][b]);
+                accu[r][b] = dotc<BF>(cu[r], cx, accu[r][b]);
+            }
+        }
+    };
+    int c = tid;
+    for (; c + kThreads < cpr; c += 2 * kThreads) {
+        uint4 ga[R], ua[R], gb[R], ub[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            ga[r] = ld_stream(wg + r * rowb + size_t(c) * 16);
+            ua[r] = ld_stream(wu + r * rowb + size_t(c) * 16);
+            gb[r] = ld_stream(wg + r * rowb + size_t(c + kThreads) * 16);
+            ub[r] = ld_stream(wu + r * rowb + size_t(c + kThreads) * 16);
+        }
+        compute(c, ga, ua);
+        compute(c + kThreads, gb, ub);
+    }
+    if (c < cpr) {
+        uint4 ga[R], ua[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            ga[r] = ld_stream(wg + r * rowb + size_t(c) * 16);
+            ua[r] = ld_stream(wu + r * rowb + size_t(c) * 16);
+        }
+        compute(c, ga, ua);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            if (!((tm >> b) & 1u)) continue;
+            const float gs = wave_sum(accg[r][b]);
+            const float us = wave_sum(accu[r][b]);
+            if (lane == 0) { red[wave][0][r][b] = gs; red[wave][1][r][b] = us; }
+        }
+    __syncthreads();
+    if (tid < R * NB) {
+        const int r = tid / NB, b = tid % NB;
+        if ((tm >> b) & 1u) {
+            float gs = 0.f, us = 0.f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) { gs += red[w][0][r][b]; us += red[w][1][r][b]; }
+            float* act = reinterpret_cast<float*>(a.act);
+            act[(size_t(j) * a.B + b) * a.I + i0 + r] = slot_weight(a, p, j, b) * silu(gs) * us;
+        }
+    }
+}
+
+// Down, rows owned by lane groups (rows of at most 512 chunks): every wave
+// covers the workgroup's rows; the four waves split the slots (wave w takes
+// slots w, w+4, ...) and their sums are added in wave order through LDS.
 template <bool BF, int G, int R, int NB>
 __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
+    constexpr int kRows = (64 / G) * R;
     __shared__ Plan p;
+    __shared__ float red[kWaves][kRows][NB];
     build_plan(a, p);
-    const int rb = blockIdx.x / a.ng, grp = blockIdx.x % a.ng;
-    const int rows_per_block = kWaves * (64 / G) * R;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lg = lane / G, g = lane % G;
-    const int h0 = rb * rows_per_block + (wave * (64 / G) + lg) * R;
+    const int hb = blockIdx.x * kRows;
+    const int h0 = hb + lg * R;
     if (blockIdx.x == 0 && threadIdx.x == 0 && a.n_experts)
         atomicAdd(a.n_experts, (unsigned long long)p.n_routed);
     const bool live = h0 < a.H;   // H is a multiple of R
@@ -317,7 +373,6 @@ __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
     constexpr int N = Chunk<BF>::N;
     const size_t rowb = size_t(a.I) * esz;
     const int cpr = int(rowb / 16);
-    const int j0 = grp * a.spg, j1 = min(p.n_slots, j0 + a.spg);
 
     float acc[R][NB];
 #pragma unroll
@@ -325,7 +380,7 @@ __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
 
-    for (int j = j0; live && j < j1; ++j) {
+    for (int j = wave; live && j < p.n_slots; j += kWaves) {
         const unsigned tm = p.tok[j];
         const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb;
         const float* act = reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I;
@@ -360,36 +415,41 @@ __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
             compute(c, qa);
         }
     }
-    DownEpilogue ep{a, p, rb, grp, rb * rows_per_block, rows_per_block};
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-        if (b >= a.B) break;
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const float s = seg_sum<G>(acc[r][b]);
-            if (live && g == 0) ep.put(b, h0 + r, s);
+            if (g == 0) red[wave][lg * R + r][b] = s;
+        }
+    __syncthreads();
+    for (int t = threadIdx.x; t < kRows * NB; t += kThreads) {
+        const int q = t / NB, b = t % NB, h = hb + q;
+        if (b < a.B && h < a.H) {
+            float s = 0.f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) s += red[w][q][b];
+            a.y[size_t(b) * a.H + h] = s;
         }
     }
-    ep.finish();
 }
 
 // Down, long rows: the whole workgroup strides one block of R rows (split-K
-// over the four waves), then combines the waves' sums through LDS.
+// over the four waves) for every slot, then combines the waves' sums
+// through LDS.
 template <bool BF, int R, int NB>
 __global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
     __shared__ Plan p;
     __shared__ float red[kWaves][R][NB];
     build_plan(a, p);
-    const int rb = blockIdx.x / a.ng, grp = blockIdx.x % a.ng;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int h0 = rb * R;   // H is a multiple of R
+    const int h0 = blockIdx.x * R;   // H is a multiple of R
     if (blockIdx.x == 0 && tid == 0 && a.n_experts)
         atomicAdd(a.n_experts, (unsigned long long)p.n_routed);
     constexpr int esz = BF ? 2 : 4;
     constexpr int N = Chunk<BF>::N;
     const size_t rowb = size_t(a.I) * esz;
     const int cpr = int(rowb / 16);
-    const int j0 = grp * a.spg, j1 = min(p.n_slots, j0 + a.spg);
 
     float acc[R][NB];
 #pragma unroll
@@ -397,7 +457,7 @@ __global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
 
-    for (int j = j0; j < j1; ++j) {
+    for (int j = 0; j < p.n_slots; ++j) {
         const unsigned tm = p.tok[j];
         const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb;
         const float* act = reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I;
@@ -440,17 +500,15 @@ __global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
             if (lane == 0) red[wave][r][b] = s;
         }
     __syncthreads();
-    DownEpilogue ep{a, p, rb, grp, h0, R};
     if (tid < R * NB) {
         const int r = tid / NB, b = tid % NB;
         if (b < a.B) {
             float s = 0.f;
 #pragma unroll
             for (int w = 0; w < kWaves; ++w) s += red[w][r][b];
-            ep.put(b, h0 + r, s);
+            a.y[size_t(b) * a.H + h0 + r] = s;
         }
     }
-    ep.finish();
 }
 
 // ============================================================================
@@ -486,25 +544,51 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int bloc
 #pragma unroll
     for (int t = 0; t < NT; ++t) dg[t] = du[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
-    for (int h = 0; h < a.H; h += 64) {
-        const size_t off = size_t(h) * 2;
-        bf16x8 ga[NT], gb[NT], ua[NT], ub[NT];
+    // two 64-element steps in flight: all loads of both steps issue before
+    // the first MFMA waits on them (H is a multiple of 64; an odd last step
+    // runs alone)
+    auto step = [&](const bf16x8 (&g0)[NT], const bf16x8 (&g1)[NT], const bf16x8 (&u0)[NT],
+                    const bf16x8 (&u1)[NT], const bf16x8& x0, const bf16x8& x1) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            ga[t] = ld_bf8_stream(wg[t] + off);
-            gb[t] = ld_bf8_stream(wg[t] + off + 16);
-            ua[t] = ld_bf8_stream(wu[t] + off);
-            ub[t] = ld_bf8_stream(wu[t] + off + 16);
+            dg[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, g0[t], dg[t], 0, 0, 0);
+            dg[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, g1[t], dg[t], 0, 0, 0);
+            du[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0, u0[t], du[t], 0, 0, 0);
+            du[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1, u1[t], du[t], 0, 0, 0);
         }
-        const bf16x8 xa = xrow ? ld_bf8(xs + off) : zero;
-        const bf16x8 xb = xrow ? ld_bf8(xs + off + 16) : zero;
+    };
+    int h = 0;
+    for (; h + 64 < a.H; h += 128) {
+        const size_t o0 = size_t(h) * 2, o1 = o0 + 128;
+        bf16x8 ga0[NT], gb0[NT], ua0[NT], ub0[NT], ga1[NT], gb1[NT], ua1[NT], ub1[NT];
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            dg[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, ga[t], dg[t], 0, 0, 0);
-            dg[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, gb[t], dg[t], 0, 0, 0);
-            du[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, ua[t], du[t], 0, 0, 0);
-            du[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb, ub[t], du[t], 0, 0, 0);
+            ga0[t] = ld_bf8_stream(wg[t] + o0);
+            gb0[t] = ld_bf8_stream(wg[t] + o0 + 16);
+            ua0[t] = ld_bf8_stream(wu[t] + o0);
+            ub0[t] = ld_bf8_stream(wu[t] + o0 + 16);
+            ga1[t] = ld_bf8_stream(wg[t] + o1);
+            gb1[t] = ld_bf8_stream(wg[t] + o1 + 16);
+            ua1[t] = ld_bf8_stream(wu[t] + o1);
+            ub1[t] = ld_bf8_stream(wu[t] + o1 + 16);
         }
+        const bf16x8 xa0 = xrow ? ld_bf8(xs + o0) : zero, xb0 = xrow ? ld_bf8(xs + o0 + 16) : zero;
+        const bf16x8 xa1 = xrow ? ld_bf8(xs + o1) : zero, xb1 = xrow ? ld_bf8(xs + o1 + 16) : zero;
+        step(ga0, gb0, ua0, ub0, xa0, xb0);
+        step(ga1, gb1, ua1, ub1, xa1, xb1);
+    }
+    if (h < a.H) {
+        const size_t o0 = size_t(h) * 2;
+        bf16x8 ga0[NT], gb0[NT], ua0[NT], ub0[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            ga0[t] = ld_bf8_stream(wg[t] + o0);
+            gb0[t] = ld_bf8_stream(wg[t] + o0 + 16);
+            ua0[t] = ld_bf8_stream(wu[t] + o0);
+            ub0[t] = ld_bf8_stream(wu[t] + o0 + 16);
+        }
+        const bf16x8 xa0 = xrow ? ld_bf8(xs + o0) : zero, xb0 = xrow ? ld_bf8(xs + o0 + 16) : zero;
+        step(ga0, gb0, ua0, ub0, xa0, xb0);
     }
     // D layout: lane holds rows m = 4q + r (tokens) of column n (weight row)
     uint16_t* act = reinterpret_cast<uint16_t*>(a.act) + size_t(j) * a.B * a.I;
@@ -550,32 +634,58 @@ __global__ __launch_bounds__(kThreads) void ffn_down_mfma(FfnArgs a) {
         for (int t = 0; t < NT; ++t) wr[t] = wd + size_t(h0 + t * 16 + n) * rowb;
         const char* ar = reinterpret_cast<const char*>(a.act) +
                          (size_t(j) * a.B + (arow ? n : 0)) * rowb + q * 32;
-        for (int k = 0; k < a.I; k += 64) {
-            const size_t off = size_t(k) * 2;
-            bf16x8 wa[NT], wb[NT];
+        auto step = [&](const bf16x8 (&w0)[NT], const bf16x8 (&w1)[NT], const bf16x8& a0, const bf16x8& a1) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                wa[t] = ld_bf8_stream(wr[t] + off);
-                wb[t] = ld_bf8_stream(wr[t] + off + 16);
+                d[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, w0[t], d[t], 0, 0, 0);
+                d[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, w1[t], d[t], 0, 0, 0);
             }
-            const bf16x8 aa = arow ? ld_bf8(ar + off) : zero;
-            const bf16x8 ab = arow ? ld_bf8(ar + off + 16) : zero;
+        };
+        int k = 0;
+        for (; k + 64 < a.I; k += 128) {
+            const size_t o0 = size_t(k) * 2, o1 = o0 + 128;
+            bf16x8 wa0[NT], wb0[NT], wa1[NT], wb1[NT];
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                d[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aa, wa[t], d[t], 0, 0, 0);
-                d[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ab, wb[t], d[t], 0, 0, 0);
+                wa0[t] = ld_bf8_stream(wr[t] + o0);
+                wb0[t] = ld_bf8_stream(wr[t] + o0 + 16);
+                wa1[t] = ld_bf8_stream(wr[t] + o1);
+                wb1[t] = ld_bf8_stream(wr[t] + o1 + 16);
             }
+            const bf16x8 aa0 = arow ? ld_bf8(ar + o0) : zero, ab0 = arow ? ld_bf8(ar + o0 + 16) : zero;
+            const bf16x8 aa1 = arow ? ld_bf8(ar + o1) : zero, ab1 = arow ? ld_bf8(ar + o1 + 16) : zero;
+            step(wa0, wb0, aa0, ab0);
+            step(wa1, wb1, aa1, ab1);
+        }
+        if (k < a.I) {
+            const size_t o0 = size_t(k) * 2;
+            bf16x8 wa0[NT], wb0[NT];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                wa0[t] = ld_bf8_stream(wr[t] + o0);
+                wb0[t] = ld_bf8_stream(wr[t] + o0 + 16);
+            }
+            const bf16x8 aa0 = arow ? ld_bf8(ar + o0) : zero, ab0 = arow ? ld_bf8(ar + o0 + 16) : zero;
+            step(wa0, wb0, aa0, ab0);
         }
     }
-    DownEpilogue ep{a, p, rb, grp, rb * rows_per_block, rows_per_block};
+    float* out = a.ng == 1 ? a.y : a.part + size_t(grp) * a.B * a.H;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int b = 4 * q + r;
         if (!live || b >= a.B) continue;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) ep.put(b, h0 + t * 16 + n, d[t][r]);
+        for (int t = 0; t < NT; ++t) out[size_t(b) * a.H + h0 + t * 16 + n] = d[t][r];
     }
-    ep.finish();
+}
+
+// y = sum over slot groups of the MFMA down phase's partial sums, in group order.
+__global__ __launch_bounds__(kThreads) void ffn_reduce(const float* part, int ng, int n, float* y) {
+    const int i = blockIdx.x * kThreads + threadIdx.x;
+    if (i >= n) return;
+    float s = 0.f;
+    for (int g = 0; g < ng; ++g) s += part[size_t(g) * n + i];
+    y[i] = s;
 }
 
 // ============================================================================
@@ -594,15 +704,20 @@ struct Shape {
     bool mfma;          // MFMA path
     int slots;          // slot capacity
     int gu_G;           // GEMV gate/up lanes per row
-    int dn_kind;        // 0: rows (lane groups), 1: whole-workgroup rows, 2: MFMA
+    int dn_kind;        // 0: rows (lane groups, slots split over waves), 1: whole-workgroup rows, 2: MFMA
     int dn_G;           // lanes per row for kind 0
     int dn_rows;        // rows per down workgroup
     int n_rb;           // down row blocks
-    int ng, spg;        // slot groups
+    int ng, spg;        // slot groups of the MFMA down phase
 };
 
-constexpr int kGemvR = 2;     // rows per lane group (GEMV)
+constexpr int kGemvR = 2;     // rows per lane group (GEMV gate/up)
+constexpr int kDownRowsR = 1; // rows per lane group (GEMV down, slots split over waves)
 constexpr int kDownWgR = 4;   // rows per workgroup (whole-workgroup down)
+constexpr int kUpWgR = 0;     // rows per workgroup of the whole-workgroup gate/up kernel (0: lane groups)
+constexpr int kDownForceG = 0;  // lanes per down row (0: by row length)
+constexpr int kMfmaNT = 0;      // 1: force one 16-row tile per wave in the MFMA gate/up kernel
+constexpr int kUpWgMinChunks = 512;   // ... used when a row has at least this many chunks
 
 Shape plan_shape(int B, int K, int H, int I, int E, int n_shared, int dtype) {
     Shape s{};
@@ -611,28 +726,33 @@ Shape plan_shape(int B, int K, int H, int I, int E, int n_shared, int dtype) {
     s.mfma = dtype == STMOE_BF16 && B >= 8 && H % 64 == 0 && I % 64 == 0;
     s.gu_G = pick_group(H * esz / 16);
     const int cpr_i = I * esz / 16;
+    s.ng = s.spg = 1;
     if (s.mfma) {
         s.dn_kind = 2;
         s.dn_rows = kWaves * 16;
-    } else if (cpr_i >= 512 && H % kDownWgR == 0) {
+    } else if (cpr_i >= 512 && H % kDownWgR == 0 && s.slots < kWaves) {
         s.dn_kind = 1;
         s.dn_rows = kDownWgR;
     } else {
         s.dn_kind = 0;
-        s.dn_G = pick_group(cpr_i);
-        s.dn_rows = kWaves * (64 / s.dn_G) * kGemvR;
+        // 64 lanes per row once a row has 128 chunks: one row per wave pass
+        // gives more workgroups than lane groups of 16 or 32
+        s.dn_G = kDownForceG ? kDownForceG : (cpr_i >= 128 ? 64 : pick_group(cpr_i));
+        s.dn_rows = (64 / s.dn_G) * kDownRowsR;
     }
     s.n_rb = (H + s.dn_rows - 1) / s.dn_rows;
-    int ng = (kDownWgTarget + s.n_rb - 1) / s.n_rb;
-    if (ng > s.slots) ng = s.slots;
-    if (ng < 1) ng = 1;
-    s.spg = (s.slots + ng - 1) / ng;
-    s.ng = (s.slots + s.spg - 1) / s.spg;
+    if (s.mfma) {
+        int ng = (kDownWgTarget + s.n_rb - 1) / s.n_rb;
+        if (ng > s.slots) ng = s.slots;
+        if (ng < 1) ng = 1;
+        s.spg = (s.slots + ng - 1) / ng;
+        s.ng = (s.slots + s.spg - 1) / s.spg;
+    }
     return s;
 }
 
 struct WsLayout {
-    size_t act, part, tick, total;
+    size_t act, part, total;
 };
 
 WsLayout ws_layout(int B, int H, int I, const Shape& s) {
@@ -640,32 +760,47 @@ WsLayout ws_layout(int B, int H, int I, const Shape& s) {
     WsLayout w{};
     w.act = 0;
     w.part = up(size_t(s.slots) * B * I * sizeof(float));
-    w.tick = w.part + (s.ng > 1 ? up(size_t(s.ng) * B * H * sizeof(float)) : 0);
-    w.total = w.tick + up(size_t(s.n_rb) * sizeof(unsigned));
+    w.total = w.part + (s.ng > 1 ? up(size_t(s.ng) * B * H * sizeof(float)) : 0);
     return w;
 }
 
-template <bool BF, int G, int NB>
-int launch_gate_up(const FfnArgs& a, const Shape& s, hipStream_t st) {
-    const int rows = kWaves * (64 / G) * kGemvR;
+template <bool BF, int G, int NB, int R>
+int launch_gate_up_r(const FfnArgs& a, const Shape& s, hipStream_t st) {
+    const int rows = kWaves * (64 / G) * R;
     const int bps = (a.I + rows - 1) / rows;
-    hipLaunchKernelGGL((ffn_gate_up<BF, G, kGemvR, NB>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0,
-                       st, a, bps);
+    hipLaunchKernelGGL((ffn_gate_up<BF, G, R, NB>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a,
+                       bps);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }
 
+template <bool BF, int G, int NB>
+int launch_gate_up(const FfnArgs& a, const Shape& s, hipStream_t st) {
+    if constexpr (kUpWgR > 0) {
+        if (a.H * (BF ? 2 : 4) / 16 >= kUpWgMinChunks && a.I % kUpWgR == 0) {
+            const int bps = a.I / kUpWgR;
+            hipLaunchKernelGGL((ffn_gate_up_wg<BF, kUpWgR, NB>), dim3(unsigned(bps * s.slots)),
+                               dim3(kThreads), 0, st, a, bps);
+            STMOE_LAUNCHED();
+            return STMOE_OK;
+        }
+    }
+    // long rows: one row per lane group gives more workgroups in flight
+    if (a.H * (BF ? 2 : 4) / 16 >= 512) return launch_gate_up_r<BF, G, NB, 1>(a, s, st);
+    return launch_gate_up_r<BF, G, NB, kGemvR>(a, s, st);
+}
+
 template <bool BF, int NB>
 int launch_down(const FfnArgs& a, const Shape& s, hipStream_t st) {
-    const dim3 grid(unsigned(s.n_rb * s.ng));
+    const dim3 grid(unsigned(s.n_rb));
     if (s.dn_kind == 1) {
         hipLaunchKernelGGL((ffn_down_wg<BF, kDownWgR, NB>), grid, dim3(kThreads), 0, st, a);
     } else if (s.dn_G == 16) {
-        hipLaunchKernelGGL((ffn_down_rows<BF, 16, kGemvR, NB>), grid, dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((ffn_down_rows<BF, 16, kDownRowsR, NB>), grid, dim3(kThreads), 0, st, a);
     } else if (s.dn_G == 32) {
-        hipLaunchKernelGGL((ffn_down_rows<BF, 32, kGemvR, NB>), grid, dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((ffn_down_rows<BF, 32, kDownRowsR, NB>), grid, dim3(kThreads), 0, st, a);
     } else {
-        hipLaunchKernelGGL((ffn_down_rows<BF, 64, kGemvR, NB>), grid, dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((ffn_down_rows<BF, 64, kDownRowsR, NB>), grid, dim3(kThreads), 0, st, a);
     }
     STMOE_LAUNCHED();
     return STMOE_OK;
@@ -692,14 +827,26 @@ int launch_gemv_b(const FfnArgs& a, const Shape& s, hipStream_t st, hipEvent_t e
 }
 
 int launch_mfma(const FfnArgs& a, const Shape& s, hipStream_t st, hipEvent_t ev_mid) {
-    constexpr int NT = 1;
+    // two 16-row tiles per wave when that still leaves >= 1024 workgroups
+    constexpr int NT = 2;
     const int rows = kWaves * NT * 16;
-    const int bps = (a.I + rows - 1) / rows;
-    hipLaunchKernelGGL((ffn_gate_up_mfma<NT>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
+    if (a.I % rows != 0 || (a.I / rows) * s.slots < 1024 || kMfmaNT == 1) {
+        const int bps = a.I / (kWaves * 16);
+        hipLaunchKernelGGL((ffn_gate_up_mfma<1>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
+    } else {
+        const int bps = a.I / rows;
+        hipLaunchKernelGGL((ffn_gate_up_mfma<NT>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
+    }
     STMOE_LAUNCHED();
     if (ev_mid) STMOE_HIP(hipEventRecord(ev_mid, st));
-    hipLaunchKernelGGL((ffn_down_mfma<NT>), dim3(unsigned(s.n_rb * s.ng)), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((ffn_down_mfma<1>), dim3(unsigned(s.n_rb * s.ng)), dim3(kThreads), 0, st, a);
     STMOE_LAUNCHED();
+    if (s.ng > 1) {
+        const int n = a.B * a.H;
+        hipLaunchKernelGGL(ffn_reduce, dim3(unsigned((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                           a.part, s.ng, n, a.y);
+        STMOE_LAUNCHED();
+    }
     return STMOE_OK;
 }
 
@@ -731,7 +878,6 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
     a.n_shared = n_shared;
     a.act = base + L.act;
     a.part = reinterpret_cast<float*>(base + L.part);
-    a.tick = reinterpret_cast<unsigned*>(base + L.tick);
     a.y = y;
     a.n_experts = n_experts;
     a.ng = s.ng;

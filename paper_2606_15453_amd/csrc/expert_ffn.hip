@@ -24,9 +24,10 @@
 // from L1/L2; DPP / shuffle segment sums reduce.  For long down rows the
 // whole workgroup strides one row block (split-K over its four waves).
 // Batch >= 8: MFMA kernels (v_mfma_f32_16x16x32_bf16).  The tokens form the
-// 16-row A operand (padded with zeros), 16 weight rows the B operand; each
-// lane loads 32 contiguous bytes of one row per 64-element step, so a wave
-// reads 16 rows x 128 B per step.  The SwiGLU activation goes through bf16.
+// 16-row A operand (padded with zeros), 16 weight rows the B operand.  In
+// each 64-element step lane (n, q) loads elements 8q..8q+7 and 32+8q..32+8q+7
+// of row n, so every load instruction reads 16 full 64-byte row segments.
+// The SwiGLU activation goes through bf16.
 //
 // Every kernel rebuilds the slot plan (distinct selected experts ascending,
 // token masks) from topk_idx/topk_w in LDS: no host round trip, no planning
@@ -40,7 +41,8 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxShared = 8;
 constexpr int kMaxSlots = kMaxE + kMaxShared;
-constexpr int kDownWgTarget = 1024;   // workgroups the down phase aims for
+constexpr int kDownWgTarget = 256;    // workgroups the MFMA down phase aims for
+constexpr int kMfmaMinB = 8;          // batch from which the MFMA kernels run
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -532,13 +534,13 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int bloc
     const size_t rowb = size_t(a.H) * 2;
     const char* blob = slot_blob(a, p, j);
     const bool xrow = n < a.B;     // A operand row n = token n
-    const char* xs = reinterpret_cast<const char*>(a.x) + size_t(xrow ? n : 0) * rowb + q * 32;
+    const char* xs = reinterpret_cast<const char*>(a.x) + size_t(xrow ? n : 0) * rowb + q * 16;
     const char* wg[NT];
     const char* wu[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-        wg[t] = blob + size_t(i0 + t * 16 + n) * rowb + q * 32;
-        wu[t] = blob + size_t(a.I + i0 + t * 16 + n) * rowb + q * 32;
+        wg[t] = blob + size_t(i0 + t * 16 + n) * rowb + q * 16;
+        wu[t] = blob + size_t(a.I + i0 + t * 16 + n) * rowb + q * 16;
     }
     f32x4 dg[NT], du[NT];
 #pragma unroll
@@ -564,16 +566,16 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int bloc
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             ga0[t] = ld_bf8_stream(wg[t] + o0);
-            gb0[t] = ld_bf8_stream(wg[t] + o0 + 16);
+            gb0[t] = ld_bf8_stream(wg[t] + o0 + 64);
             ua0[t] = ld_bf8_stream(wu[t] + o0);
-            ub0[t] = ld_bf8_stream(wu[t] + o0 + 16);
+            ub0[t] = ld_bf8_stream(wu[t] + o0 + 64);
             ga1[t] = ld_bf8_stream(wg[t] + o1);
-            gb1[t] = ld_bf8_stream(wg[t] + o1 + 16);
+            gb1[t] = ld_bf8_stream(wg[t] + o1 + 64);
             ua1[t] = ld_bf8_stream(wu[t] + o1);
-            ub1[t] = ld_bf8_stream(wu[t] + o1 + 16);
+            ub1[t] = ld_bf8_stream(wu[t] + o1 + 64);
         }
-        const bf16x8 xa0 = xrow ? ld_bf8(xs + o0) : zero, xb0 = xrow ? ld_bf8(xs + o0 + 16) : zero;
-        const bf16x8 xa1 = xrow ? ld_bf8(xs + o1) : zero, xb1 = xrow ? ld_bf8(xs + o1 + 16) : zero;
+        const bf16x8 xa0 = xrow ? ld_bf8(xs + o0) : zero, xb0 = xrow ? ld_bf8(xs + o0 + 64) : zero;
+        const bf16x8 xa1 = xrow ? ld_bf8(xs + o1) : zero, xb1 = xrow ? ld_bf8(xs + o1 + 64) : zero;
         step(ga0, gb0, ua0, ub0, xa0, xb0);
         step(ga1, gb1, ua1, ub1, xa1, xb1);
     }
@@ -583,11 +585,11 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int bloc
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             ga0[t] = ld_bf8_stream(wg[t] + o0);
-            gb0[t] = ld_bf8_stream(wg[t] + o0 + 16);
+            gb0[t] = ld_bf8_stream(wg[t] + o0 + 64);
             ua0[t] = ld_bf8_stream(wu[t] + o0);
-            ub0[t] = ld_bf8_stream(wu[t] + o0 + 16);
+            ub0[t] = ld_bf8_stream(wu[t] + o0 + 64);
         }
-        const bf16x8 xa0 = xrow ? ld_bf8(xs + o0) : zero, xb0 = xrow ? ld_bf8(xs + o0 + 16) : zero;
+        const bf16x8 xa0 = xrow ? ld_bf8(xs + o0) : zero, xb0 = xrow ? ld_bf8(xs + o0 + 64) : zero;
         step(ga0, gb0, ua0, ub0, xa0, xb0);
     }
     // D layout: lane holds rows m = 4q + r (tokens) of column n (weight row)
@@ -606,6 +608,75 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int bloc
     }
 }
 
+// gate/up, split-K: one workgroup = 16 rows of one slot; wave w covers the
+// w-th quarter of the hidden dimension and the four partial tiles add up in
+// LDS (for shapes whose row count alone gives too few workgroups).
+__global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma_sk(FfnArgs a, int blocks_per_slot) {
+    __shared__ Plan p;
+    __shared__ float red[kWaves][2][64][4];
+    build_plan(a, p);
+    const int j = blockIdx.x / blocks_per_slot;
+    if (j >= p.n_slots) return;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n = lane & 15, q = lane >> 4;
+    const int i0 = (blockIdx.x % blocks_per_slot) * 16;   // I is a multiple of 16
+    const unsigned tm = p.tok[j];
+    const size_t rowb = size_t(a.H) * 2;
+    const char* blob = slot_blob(a, p, j);
+    const bool xrow = n < a.B;
+    const int hq = a.H / kWaves;                            // H is a multiple of 256
+    const size_t kbase = size_t(wave) * hq * 2 + q * 16;
+    const char* xs = reinterpret_cast<const char*>(a.x) + size_t(xrow ? n : 0) * rowb + kbase;
+    const char* wg = blob + size_t(i0 + n) * rowb + kbase;
+    const char* wu = blob + size_t(a.I + i0 + n) * rowb + kbase;
+    f32x4 dg = f32x4{0.f, 0.f, 0.f, 0.f}, du = dg;
+    const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    int h = 0;
+    for (; h + 64 < hq; h += 128) {
+        const size_t o0 = size_t(h) * 2, o1 = o0 + 128;
+        const bf16x8 ga0 = ld_bf8_stream(wg + o0), gb0 = ld_bf8_stream(wg + o0 + 64);
+        const bf16x8 ua0 = ld_bf8_stream(wu + o0), ub0 = ld_bf8_stream(wu + o0 + 64);
+        const bf16x8 ga1 = ld_bf8_stream(wg + o1), gb1 = ld_bf8_stream(wg + o1 + 64);
+        const bf16x8 ua1 = ld_bf8_stream(wu + o1), ub1 = ld_bf8_stream(wu + o1 + 64);
+        const bf16x8 xa0 = xrow ? ld_bf8(xs + o0) : zero, xb0 = xrow ? ld_bf8(xs + o0 + 64) : zero;
+        const bf16x8 xa1 = xrow ? ld_bf8(xs + o1) : zero, xb1 = xrow ? ld_bf8(xs + o1 + 64) : zero;
+        dg = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa0, ga0, dg, 0, 0, 0);
+        dg = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb0, gb0, dg, 0, 0, 0);
+        du = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa0, ua0, du, 0, 0, 0);
+        du = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb0, ub0, du, 0, 0, 0);
+        dg = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa1, ga1, dg, 0, 0, 0);
+        dg = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb1, gb1, dg, 0, 0, 0);
+        du = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa1, ua1, du, 0, 0, 0);
+        du = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb1, ub1, du, 0, 0, 0);
+    }
+    if (h < hq) {
+        const size_t o0 = size_t(h) * 2;
+        const bf16x8 ga0 = ld_bf8_stream(wg + o0), gb0 = ld_bf8_stream(wg + o0 + 64);
+        const bf16x8 ua0 = ld_bf8_stream(wu + o0), ub0 = ld_bf8_stream(wu + o0 + 64);
+        const bf16x8 xa0 = xrow ? ld_bf8(xs + o0) : zero, xb0 = xrow ? ld_bf8(xs + o0 + 64) : zero;
+        dg = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa0, ga0, dg, 0, 0, 0);
+        dg = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb0, gb0, dg, 0, 0, 0);
+        du = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa0, ua0, du, 0, 0, 0);
+        du = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb0, ub0, du, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) { red[wave][0][lane][r] = dg[r]; red[wave][1][lane][r] = du[r]; }
+    __syncthreads();
+    if (wave != 0) return;
+    uint16_t* act = reinterpret_cast<uint16_t*>(a.act) + size_t(j) * a.B * a.I;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int b = 4 * q + r;
+        if (b >= a.B) continue;
+        float g = 0.f, u = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) { g += red[w][0][lane][r]; u += red[w][1][lane][r]; }
+        const bool routed = (tm >> b) & 1u;
+        const float v = routed ? slot_weight(a, p, j, b) * silu(g) * u : 0.f;
+        act[size_t(b) * a.I + i0 + n] = f32_to_bf16_rne(v);
+    }
+}
+
 // down: each wave computes NT tiles of 16 output rows x 16 tokens, summing
 // the slots of its group (A operand = the slot's bf16 activations).
 template <int NT>
@@ -619,21 +690,22 @@ __global__ __launch_bounds__(kThreads) void ffn_down_mfma(FfnArgs a) {
     const int h0 = rb * rows_per_block + wave * NT * 16;
     if (blockIdx.x == 0 && threadIdx.x == 0 && a.n_experts)
         atomicAdd(a.n_experts, (unsigned long long)p.n_routed);
-    const bool live = h0 < a.H;   // H is a multiple of 16
+    const bool live = h0 < a.H;   // H is a multiple of 64 * NT
     const size_t rowb = size_t(a.I) * 2;
     const bool arow = n < a.B;
-    const int j0 = grp * a.spg, j1 = min(p.n_slots, j0 + a.spg);
+    // the selected slots split evenly over the groups (an empty group writes zeros)
+    const int j0 = grp * p.n_slots / a.ng, j1 = (grp + 1) * p.n_slots / a.ng;
     f32x4 d[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) d[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
     for (int j = j0; live && j < j1; ++j) {
-        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * 2 + q * 32;
+        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * 2 + q * 16;
         const char* wr[NT];
 #pragma unroll
         for (int t = 0; t < NT; ++t) wr[t] = wd + size_t(h0 + t * 16 + n) * rowb;
         const char* ar = reinterpret_cast<const char*>(a.act) +
-                         (size_t(j) * a.B + (arow ? n : 0)) * rowb + q * 32;
+                         (size_t(j) * a.B + (arow ? n : 0)) * rowb + q * 16;
         auto step = [&](const bf16x8 (&w0)[NT], const bf16x8 (&w1)[NT], const bf16x8& a0, const bf16x8& a1) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
@@ -648,12 +720,12 @@ __global__ __launch_bounds__(kThreads) void ffn_down_mfma(FfnArgs a) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 wa0[t] = ld_bf8_stream(wr[t] + o0);
-                wb0[t] = ld_bf8_stream(wr[t] + o0 + 16);
+                wb0[t] = ld_bf8_stream(wr[t] + o0 + 64);
                 wa1[t] = ld_bf8_stream(wr[t] + o1);
-                wb1[t] = ld_bf8_stream(wr[t] + o1 + 16);
+                wb1[t] = ld_bf8_stream(wr[t] + o1 + 64);
             }
-            const bf16x8 aa0 = arow ? ld_bf8(ar + o0) : zero, ab0 = arow ? ld_bf8(ar + o0 + 16) : zero;
-            const bf16x8 aa1 = arow ? ld_bf8(ar + o1) : zero, ab1 = arow ? ld_bf8(ar + o1 + 16) : zero;
+            const bf16x8 aa0 = arow ? ld_bf8(ar + o0) : zero, ab0 = arow ? ld_bf8(ar + o0 + 64) : zero;
+            const bf16x8 aa1 = arow ? ld_bf8(ar + o1) : zero, ab1 = arow ? ld_bf8(ar + o1 + 64) : zero;
             step(wa0, wb0, aa0, ab0);
             step(wa1, wb1, aa1, ab1);
         }
@@ -663,9 +735,9 @@ __global__ __launch_bounds__(kThreads) void ffn_down_mfma(FfnArgs a) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 wa0[t] = ld_bf8_stream(wr[t] + o0);
-                wb0[t] = ld_bf8_stream(wr[t] + o0 + 16);
+                wb0[t] = ld_bf8_stream(wr[t] + o0 + 64);
             }
-            const bf16x8 aa0 = arow ? ld_bf8(ar + o0) : zero, ab0 = arow ? ld_bf8(ar + o0 + 16) : zero;
+            const bf16x8 aa0 = arow ? ld_bf8(ar + o0) : zero, ab0 = arow ? ld_bf8(ar + o0 + 64) : zero;
             step(wa0, wb0, aa0, ab0);
         }
     }
@@ -679,13 +751,26 @@ __global__ __launch_bounds__(kThreads) void ffn_down_mfma(FfnArgs a) {
     }
 }
 
-// y = sum over slot groups of the MFMA down phase's partial sums, in group order.
-__global__ __launch_bounds__(kThreads) void ffn_reduce(const float* part, int ng, int n, float* y) {
+// y = sum over slot groups of the MFMA down phase's partial sums, in group
+// order; four outputs per thread, eight groups' loads in flight.
+__global__ __launch_bounds__(kThreads) void ffn_reduce(const float* part, int ng, int n4, float* y) {
     const int i = blockIdx.x * kThreads + threadIdx.x;
-    if (i >= n) return;
-    float s = 0.f;
-    for (int g = 0; g < ng; ++g) s += part[size_t(g) * n + i];
-    y[i] = s;
+    if (i >= n4) return;
+    const float4* p4 = reinterpret_cast<const float4*>(part);
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    int g = 0;
+    for (; g + 8 <= ng; g += 8) {
+        float4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = p4[size_t(g + u) * n4 + i];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) { s.x += v[u].x; s.y += v[u].y; s.z += v[u].z; s.w += v[u].w; }
+    }
+    for (; g < ng; ++g) {
+        const float4 v = p4[size_t(g) * n4 + i];
+        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
+    reinterpret_cast<float4*>(y)[i] = s;
 }
 
 // ============================================================================
@@ -709,6 +794,7 @@ struct Shape {
     int dn_rows;        // rows per down workgroup
     int n_rb;           // down row blocks
     int ng, spg;        // slot groups of the MFMA down phase
+    int dn_nt;          // 16-row tiles per wave of the MFMA down kernel
 };
 
 constexpr int kGemvR = 2;     // rows per lane group (GEMV gate/up)
@@ -717,19 +803,24 @@ constexpr int kDownWgR = 4;   // rows per workgroup (whole-workgroup down)
 constexpr int kUpWgR = 0;     // rows per workgroup of the whole-workgroup gate/up kernel (0: lane groups)
 constexpr int kDownForceG = 0;  // lanes per down row (0: by row length)
 constexpr int kMfmaNT = 0;      // 1: force one 16-row tile per wave in the MFMA gate/up kernel
+constexpr int kMfmaDownNT = 4;  // 16-row tiles per wave of the MFMA down kernel (1, 2 or 4)
+constexpr int kMfmaSplitKBelow = 2048;  // split-K MFMA gate/up when the tiled grid has fewer workgroups
 constexpr int kUpWgMinChunks = 512;   // ... used when a row has at least this many chunks
 
 Shape plan_shape(int B, int K, int H, int I, int E, int n_shared, int dtype) {
     Shape s{};
     const int esz = dtype == STMOE_BF16 ? 2 : 4;
     s.slots = (B * K < E ? B * K : E) + n_shared;
-    s.mfma = dtype == STMOE_BF16 && B >= 8 && H % 64 == 0 && I % 64 == 0;
+    s.mfma = dtype == STMOE_BF16 && B >= kMfmaMinB && H % 64 == 0 && I % 64 == 0;
     s.gu_G = pick_group(H * esz / 16);
     const int cpr_i = I * esz / 16;
     s.ng = s.spg = 1;
+    s.dn_nt = 1;
     if (s.mfma) {
         s.dn_kind = 2;
-        s.dn_rows = kWaves * 16;
+        // several row tiles per wave share each activation load
+        s.dn_nt = (H % (kWaves * 16 * kMfmaDownNT) == 0) ? kMfmaDownNT : 1;
+        s.dn_rows = kWaves * 16 * s.dn_nt;
     } else if (cpr_i >= 512 && H % kDownWgR == 0 && s.slots < kWaves) {
         s.dn_kind = 1;
         s.dn_rows = kDownWgR;
@@ -745,8 +836,8 @@ Shape plan_shape(int B, int K, int H, int I, int E, int n_shared, int dtype) {
         int ng = (kDownWgTarget + s.n_rb - 1) / s.n_rb;
         if (ng > s.slots) ng = s.slots;
         if (ng < 1) ng = 1;
+        s.ng = ng;
         s.spg = (s.slots + ng - 1) / ng;
-        s.ng = (s.slots + s.spg - 1) / s.spg;
     }
     return s;
 }
@@ -830,7 +921,10 @@ int launch_mfma(const FfnArgs& a, const Shape& s, hipStream_t st, hipEvent_t ev_
     // two 16-row tiles per wave when that still leaves >= 1024 workgroups
     constexpr int NT = 2;
     const int rows = kWaves * NT * 16;
-    if (a.I % rows != 0 || (a.I / rows) * s.slots < 1024 || kMfmaNT == 1) {
+    if ((a.I / (kWaves * 16)) * s.slots < kMfmaSplitKBelow && a.H % 256 == 0) {
+        const int bps = a.I / 16;
+        hipLaunchKernelGGL(ffn_gate_up_mfma_sk, dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
+    } else if (a.I % rows != 0 || (a.I / rows) * s.slots < 1024 || kMfmaNT == 1) {
         const int bps = a.I / (kWaves * 16);
         hipLaunchKernelGGL((ffn_gate_up_mfma<1>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
     } else {
@@ -839,12 +933,18 @@ int launch_mfma(const FfnArgs& a, const Shape& s, hipStream_t st, hipEvent_t ev_
     }
     STMOE_LAUNCHED();
     if (ev_mid) STMOE_HIP(hipEventRecord(ev_mid, st));
-    hipLaunchKernelGGL((ffn_down_mfma<1>), dim3(unsigned(s.n_rb * s.ng)), dim3(kThreads), 0, st, a);
+    const dim3 dgrid(unsigned(s.n_rb * s.ng));
+    if (s.dn_nt == 4)
+        hipLaunchKernelGGL((ffn_down_mfma<4>), dgrid, dim3(kThreads), 0, st, a);
+    else if (s.dn_nt == 2)
+        hipLaunchKernelGGL((ffn_down_mfma<2>), dgrid, dim3(kThreads), 0, st, a);
+    else
+        hipLaunchKernelGGL((ffn_down_mfma<1>), dgrid, dim3(kThreads), 0, st, a);
     STMOE_LAUNCHED();
     if (s.ng > 1) {
-        const int n = a.B * a.H;
-        hipLaunchKernelGGL(ffn_reduce, dim3(unsigned((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
-                           a.part, s.ng, n, a.y);
+        const int n4 = a.B * a.H / 4;   // H is a multiple of 64
+        hipLaunchKernelGGL(ffn_reduce, dim3(unsigned((n4 + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                           a.part, s.ng, n4, a.y);
         STMOE_LAUNCHED();
     }
     return STMOE_OK;

@@ -54,6 +54,10 @@ def parse():
                     help="decode tokens of the CPU oracle sample (0 skips it)")
     ap.add_argument("--counters", action="store_true",
                     help="run the fixed workload profiled by the rocprofv3 --pmc passes and exit")
+    ap.add_argument("--ffn-sweep", action="store_true",
+                    help="time moe_expert_ffn on every config shape (markdown table on stdout) and exit")
+    ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_CSV", "TITLE", "COMMAND"),
+                    help="print a markdown table of a rocprofv3 kernel_stats.csv and exit")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the markdown counter summary of two rocprofv3 --pmc runs and exit")
     return ap.parse_args()
@@ -153,6 +157,20 @@ def summarize_counters(fetch_csv, write_csv):
     print("\n".join(out))
 
 
+def summarize_stats(path, title, cmd):
+    import csv
+    print(f"# {title}\n")
+    print(f"Command (run from `/tmp` with `TMPDIR=/tmp`, repository at `$R`):\n\n```\n{cmd}\n```\n")
+    print("| kernel | calls | avg us | min us | max us | % of GPU time |")
+    print("|---|---|---|---|---|---|")
+    for r in csv.DictReader(open(path)):
+        name = r["Name"].replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        if len(name) > 70:
+            name = name[:67] + "..."
+        print(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+              f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+
+
 def counters_workload():
     """Fixed workload for the rocprofv3 --pmc passes: decode tokens of the
     resident Mixtral-shaped stack, then calibration copies of known size."""
@@ -175,6 +193,61 @@ def counters_workload():
     ctx.close()
     pred.close()
     log("counters workload done")
+
+
+def ffn_sweep(reps=50):
+    """Event-timed moe_expert_ffn per config shape: one seeded routing of B
+    tokens (top-K of E), every selected expert's blob generated in HBM."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    dev = "cuda:0"
+    print("| workload | B | distinct experts (+shared) | bytes per call | us per call | GB/s | of 8 TB/s | path |")
+    print("|---|---|---|---|---|---|---|---|")
+    for name in ("tiny", "mixtral", "qwen30b", "qwen30b-b8", "dsv2lite", "qwen235b"):
+        cfg = W.CONFIGS[name]
+        rng = np.random.default_rng(cfg.seed)
+        idx = np.stack([rng.choice(cfg.E, cfg.K, replace=False) for _ in range(cfg.B)]).astype(np.int32)
+        w = rng.random((cfg.B, cfg.K)).astype(np.float32)
+        sel = sorted(set(idx.ravel().tolist()))
+        tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+        store = torch.empty((len(sel) + cfg.n_shared, cfg.blob_elems), dtype=tdt, device=dev)
+        for k, e in enumerate(sel):
+            W.expert_blob_torch(cfg, 0, e, store[k])
+        for sh in range(cfg.n_shared):
+            W.expert_blob_torch(cfg, 0, sh, store[len(sel) + sh], shared=True)
+        ptrs = [store[0].data_ptr()] * cfg.E
+        for k, e in enumerate(sel):
+            ptrs[e] = store[k].data_ptr()
+        eptr = torch.tensor(ptrs, dtype=torch.int64, device=dev)
+        sptr = (torch.tensor([store[len(sel) + sh].data_ptr() for sh in range(cfg.n_shared)],
+                             dtype=torch.int64, device=dev) if cfg.n_shared else None)
+        dt = S.BF16 if cfg.dtype == "bf16" else S.F32
+        x = Workload._dev(W.to_storage(cfg, rng.normal(0, 1, (cfg.B, cfg.H))))
+        y = torch.empty((cfg.B, cfg.H), dtype=torch.float32, device=dev)
+        ws = torch.zeros(S.ffn_workspace_bytes(cfg.B, cfg.K, cfg.E, cfg.H, cfg.I, cfg.n_shared, dt),
+                         dtype=torch.uint8, device=dev)
+        ti, tw = torch.from_numpy(idx).to(dev), torch.from_numpy(w).to(dev)
+
+        def call():
+            S.expert_ffn(x, ti, tw, cfg.H, cfg.I, cfg.E, dt, eptr, y, ws, shared_ptrs=sptr,
+                         n_shared=cfg.n_shared)
+
+        for _ in range(3):
+            call()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        nbytes = (len(sel) + cfg.n_shared) * cfg.blob_bytes
+        gbps = nbytes / us / 1e3
+        path = "MFMA" if (cfg.B >= 8 and cfg.dtype == "bf16") else "GEMV"
+        print(f"| {cfg.name} | {cfg.B} | {len(sel)} (+{cfg.n_shared}) | {nbytes} | {us:.1f} | {gbps:.0f} | "
+              f"{gbps / PEAK_HBM_GBPS:.3f} | {path} |", flush=True)
+        del store
 
 
 def achievable_read_gbps(nbytes=4 << 30, reps=10):
@@ -422,6 +495,9 @@ def main():
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
         return
+    if args.summarize_stats:
+        summarize_stats(*args.summarize_stats)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (this build has no "
               f"multi-GPU path)", file=sys.stderr)
@@ -433,6 +509,9 @@ def main():
         sys.exit(2)
     if args.counters:
         counters_workload()
+        return
+    if args.ffn_sweep:
+        ffn_sweep()
         return
     cfg = W.CONFIGS[args.config]
     log(f"workload {cfg.name}")

@@ -54,6 +54,9 @@ def parse():
                     help="decode tokens of the CPU oracle sample (0 skips it)")
     ap.add_argument("--counters", action="store_true",
                     help="run the fixed workload profiled by the rocprofv3 --pmc passes and exit")
+    ap.add_argument("--predictor-sweep", action="store_true",
+                    help="replay planted traces through the GPU predictor for every config and the paper's "
+                         "Table 1 shapes; print recall/precision per ablation mode and exit")
     ap.add_argument("--ffn-sweep", action="store_true",
                     help="time moe_expert_ffn on every config shape (markdown table on stdout) and exit")
     ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_CSV", "TITLE", "COMMAND"),
@@ -193,6 +196,51 @@ def counters_workload():
     ctx.close()
     pred.close()
     log("counters workload done")
+
+
+def predictor_sweep():
+    """Prediction quality of the GPU predictor (stmoe_update / stmoe_predict)
+    on planted routing traces, per prediction source and with the online CCT
+    update on or off.  Recall = sum|A n P| / sum|A| (layers >= 1 and layer 0),
+    precision = sum|A n P| / sum|P|, |P| = mean predicted set per row."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    dev = "cuda:0"
+    cfgs = [W.CONFIGS[n] for n in ("tiny", "mixtral", "qwen30b", "qwen30b-b8", "dsv2lite", "qwen235b")]
+    cfgs += [W.table1_config(n) for n in W.TABLE1_SHAPES]
+    modes = [("CCT+HT", S.USE_BOTH, True), ("CCT+HT, no online update", S.USE_BOTH, False),
+             ("HT only", S.USE_HT, True), ("CCT only", S.USE_CCT, True)]
+    print("| workload | B | tokens | overlap / (K^2/E) | mode | recall l>=1 | recall l0 | precision | mean set |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for cfg in cfgs:
+        T = min(cfg.T, 128)
+        sel = W.planted_trace(cfg, n_tokens=cfg.P + T)
+        dec = sel[cfg.P:]
+        ov = np.mean([len(set(dec[t, b, l]) & set(dec[t - 1, b, l])) for t in range(1, T)
+                      for b in range(cfg.B) for l in range(cfg.L)])
+        ratio = ov / (cfg.K * cfg.K / cfg.E)
+        dsel = torch.from_numpy(np.ascontiguousarray(dec.transpose(0, 2, 1, 3))).to(dev)   # [T][L][B][K]
+        for mname, use, online in modes:
+            p = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+            p.profile(sel[:cfg.P])
+            p.predict(-1, None, use=use & S.USE_HT)
+            for t in range(T):
+                for l in range(cfg.L):
+                    cur = dsel[t, l]
+                    p.update(l, dsel[t, l - 1] if l else None, cur, online=online)
+                    if l + 1 < cfg.L:
+                        p.predict(l, cur, use=use)
+                    else:
+                        p.predict(-1, None, use=use & S.USE_HT)
+            st = p.stats()
+            p.close()
+            r1 = st[1:, 0].sum() / max(st[1:, 1].sum(), 1)
+            r0 = st[0, 0] / max(st[0, 1], 1)
+            prec = st[:, 0].sum() / max(st[:, 2].sum(), 1)
+            mset = st[:, 2].sum() / max(st[:, 1].sum() / cfg.K, 1)
+            print(f"| {cfg.name} | {cfg.B} | {T} | {ratio:.2f} | {mname} | {r1:.3f} | {r0:.3f} | {prec:.3f} | "
+                  f"{mset:.1f} |", flush=True)
 
 
 def ffn_sweep(reps=50):
@@ -512,6 +560,9 @@ def main():
         return
     if args.ffn_sweep:
         ffn_sweep()
+        return
+    if args.predictor_sweep:
+        predictor_sweep()
         return
     cfg = W.CONFIGS[args.config]
     log(f"workload {cfg.name}")

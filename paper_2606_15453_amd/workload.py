@@ -111,6 +111,36 @@ CONFIGS = {
 }
 
 
+def paper_matched_stay(E: int, K: int, ratio: float = 2.0) -> float:
+    """Stay probability whose expected consecutive-token overlap is `ratio`
+    times the independent-routing value K^2/E (Section 3.2 reports about 2x).
+
+    With stay probability p per slot the overlap is about p*K + (1-p)*K^2/E.
+    """
+    base = K * K / E
+    return (ratio - 1.0) * base / (K - base)
+
+
+#: Predictor-only shapes of the paper's evaluated models (Table 1: layers,
+#: experts, top-K).  Hidden sizes are not needed: only routing traces feed the
+#: predictor.  Routing statistics: paper-matched temporal overlap (2x random)
+#: and peaked spatial transitions.
+TABLE1_SHAPES = {
+    "qwen1.5-moe": dict(L=24, E=60, K=4),
+    "qwen2-moe": dict(L=28, E=64, K=6),
+    "deepseek-v2": dict(L=60, E=160, K=8),
+    "deepseek-moe": dict(L=60, E=128, K=8),
+}
+
+
+def table1_config(name: str, B: int = 1, T: int = 256, alpha: float = 0.05, seed: int = 2000) -> MoEConfig:
+    sh = TABLE1_SHAPES[name]
+    return MoEConfig(f"{name}-L{sh['L']}-E{sh['E']}-K{sh['K']}-B{B} (predictor only)", L=sh["L"], H=8, I=8,
+                     E=sh["E"], K=sh["K"], B=B, T=T, P=T // 4, C=sh["E"] // 4,
+                     p_stay=paper_matched_stay(sh["E"], sh["K"]), alpha=alpha,
+                     seed=seed + list(TABLE1_SHAPES).index(name))
+
+
 # ----------------------------------------------------------------------------
 # counter-based hash (MurmurHash3 fmix32), numpy and torch backends
 # ----------------------------------------------------------------------------

@@ -136,3 +136,12 @@ def test_import_export_roundtrip():
     assert np.array_equal(ci2, ci) and np.array_equal(cc2, cc) and np.array_equal(ht2, ht)
     with pytest.raises(S.StmoeError):
         p.import_tables(ci, np.full_like(cc, 4), ht)
+
+
+@pytest.mark.parametrize("name", ["qwen1.5-moe", "deepseek-v2"])
+def test_table1_shapes_parity(name):
+    """The paper's evaluated model shapes (Table 1: 60 experts top-4; 160 experts top-8)."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.table1_config(name, T=6).scaled(L=5, P=3)
+    sel = W.planted_trace(cfg)
+    _run(cfg.L, cfg.E, cfg.K, cfg.B, sel[:cfg.P], sel[cfg.P:])

@@ -97,3 +97,13 @@ def test_warm_sets():
     ws = W.warm_sets(cfg.scaled(C=3), prof)
     assert ws[0].tolist() == [0, 1, 2]
     assert ws[3].tolist() == [4, 5, 6]
+
+
+def test_paper_matched_stay_gives_twice_random_overlap():
+    """Section 3.2: consecutive tokens overlap about 2x the independent K^2/N."""
+    cfg = W.table1_config("qwen2-moe", T=200).scaled(L=3)
+    sel = W.planted_trace(cfg, n_tokens=200)
+    ov = np.mean([len(set(sel[t, 0, l]) & set(sel[t - 1, 0, l])) for t in range(1, 200) for l in range(cfg.L)])
+    ratio = ov / (cfg.K * cfg.K / cfg.E)
+    assert 1.5 < ratio < 3.0
+    assert abs(W.paper_matched_stay(64, 8, ratio=1.0)) < 1e-15

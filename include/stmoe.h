@@ -72,10 +72,11 @@ int stmoe_host_free(void* p);
  *   topk_idx device out [B][K] int32, in descending-logit order
  *   topk_w   device out [B][K] fp32
  *   logits   device out [B][E] fp32, or NULL
- *   ws       device workspace of moe_route_workspace_bytes(B, E) bytes that
- *            the caller zero-fills once before its first use; every call
- *            leaves it zero-filled again at kernel exit (a completion ticket)
- *   Calls sharing one workspace must be ordered on one stream.
+ *   ws       device workspace of moe_route_workspace_bytes(B, E) bytes (the
+ *            logits; no initial contents required)
+ *   Two launches on `stream`: logits (one workgroup per expert), then the
+ *   softmax / top-K tail.  Calls sharing one workspace must be ordered on
+ *   one stream.
  * ---------------------------------------------------------------------- */
 size_t moe_route_workspace_bytes(int B, int E);
 int moe_route_topk(const void* x, const void* w_gate, int B, int H, int E, int K,
@@ -299,12 +300,14 @@ int moe_ctx_set_prefetch(moe_ctx* ctx, int min_score, int max_per_layer);
 int moe_decode_token(moe_ctx* ctx, int token, const void* xs, float* ys, int mode);
 /* Last routing of each layer: host out idx [L][B][K] int32, w [L][B][K] fp32.  [sync] */
 int moe_ctx_last_routing(moe_ctx* ctx, int32_t* idx, float* w);
-/* Event timing of the expert-FFN kernels: enable = 1 starts recording
- * (resets totals), 0 stops.  moe_ctx_timing syncs and returns the summed
- * milliseconds of the gate/up kernel and of the down kernel (events recorded
- * on the compute stream before, between and after them), the number of FFN
- * calls and the summed number of distinct routed experts over those calls. */
-int moe_ctx_set_timing(moe_ctx* ctx, int enable);
+/* Event timing of the expert-FFN kernels.  every > 0 starts recording (and
+ * resets the totals): the FFN of every layer of each token whose index is a
+ * multiple of `every` is bracketed by events on the compute stream (before,
+ * between and after its two kernels); every = 0 stops.  moe_ctx_timing syncs
+ * and returns the summed milliseconds of the gate/up kernel and of the down
+ * kernel over the timed calls, the number of timed FFN calls and the summed
+ * number of distinct routed experts over those calls. */
+int moe_ctx_set_timing(moe_ctx* ctx, int every);
 int moe_ctx_timing(moe_ctx* ctx, double* up_ms, double* down_ms, int64_t* n_calls,
                    int64_t* n_experts);
 

@@ -63,8 +63,8 @@ struct moe_ctx {
     std::vector<const void*> host_table;   // [E] scratch for the cache's answers
     bool started = false;
     int last_token = -1, last_layer = -1;
-    // FFN timing
-    bool timing = false;
+    // FFN timing: events around the FFN of every `timing_every`-th token (0: off)
+    int timing_every = 0;
     std::vector<hipEvent_t> ev_pool;
     size_t ev_used = 0;
     unsigned long long* n_experts = nullptr;   // device counter
@@ -275,7 +275,8 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
     }
     // Com.: expert FFN (timed with events before, between and after its two kernels)
     hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
-    if (c->timing) {
+    const bool timed = c->timing_every > 0 && token % c->timing_every == 0;
+    if (timed) {
         e0 = next_event(c);
         e1 = next_event(c);
         e2 = next_event(c);
@@ -284,9 +285,9 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
     }
     if (int rc = ffn_launch(x, idx_l, w_l, B, K, c->H, c->I, E, c->dtype, c->tables + size_t(layer) * E,
                             c->n_shared ? c->shared + size_t(layer) * c->n_shared : nullptr, c->n_shared,
-                            y, c->ffn_ws, c->s, c->timing ? c->n_experts : nullptr, e1))
+                            y, c->ffn_ws, c->s, timed ? c->n_experts : nullptr, e1))
         return rc;
-    if (c->timing) {
+    if (timed) {
         STMOE_HIP(hipEventRecord(e2, c->s));
         ++c->n_calls;
     }
@@ -331,11 +332,12 @@ extern "C" int moe_ctx_last_routing(moe_ctx* c, int32_t* idx, float* w) {
     return STMOE_OK;
 }
 
-extern "C" int moe_ctx_set_timing(moe_ctx* c, int enable) {
+extern "C" int moe_ctx_set_timing(moe_ctx* c, int every) {
     clear_error();
     STMOE_CHECK(c, "null ctx");
+    STMOE_CHECK(every >= 0, "every must be >= 0");
     STMOE_HIP(hipStreamSynchronize(c->s));
-    c->timing = enable != 0;
+    c->timing_every = every;
     c->ev_used = 0;
     c->n_calls = 0;
     STMOE_HIP(hipMemset(c->n_experts, 0, sizeof(unsigned long long)));

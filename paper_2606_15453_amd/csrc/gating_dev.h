@@ -1,6 +1,8 @@
-// Gating device code (Section 2): per-expert logits, a completion ticket,
-// and the softmax / top-K tail that the last workgroup runs.  Shared by the
-// standalone router kernel and the fused router + predictor kernel.
+// Gating device code (Section 2): per-expert logits (one workgroup per
+// expert row) and the softmax / top-K tail (one workgroup).  They run as two
+// launches: the kernel boundary orders the logits before the tail, where a
+// device-scope fence per workgroup would write back the L2 of every XCD.
+// Shared by the standalone router and the decode path's router + predictor.
 #pragma once
 
 #include "common.h"
@@ -18,7 +20,6 @@ struct RouteArgs {
     float* w;
     float* logits;
     float* zbuf;        // [B][E] workspace
-    unsigned* ticket;   // workspace, zero between launches
 };
 
 template <bool BF16>
@@ -39,22 +40,18 @@ __device__ __forceinline__ void dot_chunk(const void* wrow, const void* xrow, in
     }
 }
 
-// Better candidate: larger logit, or equal logit and lower index.  NaN logits
-// rank below every number.
-__device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
-    if (bi < 0) return i >= 0;
-    if (i < 0) return false;
-    const bool vn = v != v, bn = bv != bv;
-    if (vn != bn) return bn;
-    if (v != bv) return v > bv;
-    return i < bi;
+// Total order on logits as unsigned keys: larger logit -> larger key; -0
+// and +0 are one value; NaN ranks below every number.  Equal keys are
+// broken by the lower expert index.
+__device__ __forceinline__ uint32_t order_key(float v) {
+    if (v != v) return 0u;
+    const uint32_t u = v == 0.f ? 0u : __float_as_uint(v);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Logits of expert row blockIdx.x for every token, written to the
-// workspace, then a completion ticket.  Returns true only in the workgroup
-// that took the last ticket (after an acquire fence); all its threads agree.
+// Logits of expert row blockIdx.x for every token, written to the workspace.
 template <bool BF16>
-__device__ bool logits_and_ticket(const RouteArgs& a, float (*part)[kThreads / 64], bool& last) {
+__device__ void expert_logits(const RouteArgs& a, float (*part)[kThreads / 64]) {
     const int e = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int esz = BF16 ? 2 : 4;
@@ -74,73 +71,66 @@ __device__ bool logits_and_ticket(const RouteArgs& a, float (*part)[kThreads / 6
         a.zbuf[tid * a.E + e] = z;
         if (a.logits) a.logits[tid * a.E + e] = z;
     }
-    // publish the logits, then take a ticket
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-        const unsigned t = atomicAdd(a.ticket, 1u);
-        last = (t == unsigned(gridDim.x) - 1);
-    }
-    __syncthreads();
-    if (!last) return false;
-    __threadfence();   // acquire: see every workgroup's logits
-    return true;
 }
 
-// Softmax and top-K of every batch row (one wave per row) in the last
-// workgroup.  Writes idx/w (and the selection to s_idx in LDS when given),
-// resets the ticket, and ends with a barrier.
-__device__ void softmax_topk_tail(const RouteArgs& a, int32_t* s_idx) {
+// Softmax and top-K of every batch row in one workgroup, from the logits z
+// ([B][E], global or LDS).  Each thread takes (row, expert) pairs and counts
+// the experts of its row that beat its own (larger key, or equal key and
+// lower index): a count below K is its output position, so the selection
+// comes out ordered (logit desc, index asc) with no serial rounds.  The row
+// max is the winner at position 0; one wave per row then forms the softmax
+// sum and the K weights.  Writes idx/w (and the selection to s_idx in LDS
+// when given) and ends with a barrier.
+__device__ void softmax_topk_tail(const RouteArgs& a, const float* z, int32_t* s_idx) {
+    constexpr int kRow = kMaxE;                   // LDS row stride of the keys
+    __shared__ __align__(16) uint32_t keys[kMaxB * kRow];
+    __shared__ int32_t win[kMaxB * kMaxK];
+    __shared__ float rowmax[kMaxB];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    for (int b = wave; b < a.B; b += kThreads / 64) {
-        float v[kMaxE / 64];
-        int id[kMaxE / 64];
-#pragma unroll
-        for (int j = 0; j < kMaxE / 64; ++j) {
-            const int ee = lane + 64 * j;
-            id[j] = ee < a.E ? ee : -1;
-            v[j] = ee < a.E ? a.zbuf[b * a.E + ee] : 0.f;
+    const int K = a.K, E = a.E, BE = a.B * a.E;
+    for (int i = tid; i < BE; i += kThreads) {
+        const int b = i / E, f = i - b * E;
+        keys[b * kRow + f] = order_key(z[i]);
+    }
+    __syncthreads();
+    for (int i = tid; i < BE; i += kThreads) {
+        const int b = i / E, f = i - b * E;
+        const uint32_t* row = keys + b * kRow;
+        const uint32_t mine = row[f];
+        int cnt = 0;
+        int g = 0;
+        for (; g + 4 <= E; g += 4) {
+            const uint4 k4 = *reinterpret_cast<const uint4*>(row + g);
+            cnt += (k4.x > mine) + (k4.y > mine) + (k4.z > mine) + (k4.w > mine);
+            cnt += (k4.x == mine && g < f) + (k4.y == mine && g + 1 < f) + (k4.z == mine && g + 2 < f) +
+                   (k4.w == mine && g + 3 < f);
         }
-        // max for the softmax (NaN-free inputs assumed for the weights)
-        float m = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < kMaxE / 64; ++j)
-            if (id[j] >= 0) m = fmaxf(m, v[j]);
-        for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-        float s = 0.f;
-#pragma unroll
-        for (int j = 0; j < kMaxE / 64; ++j)
-            if (id[j] >= 0) s += expf(v[j] - m);
-        s = wave_sum(s);
-
-        // after the butterfly every lane holds the winner; lane k keeps round k
-        float my_w = 0.f, wsum = 0.f;
-        int my_i = 0;
-        for (int k = 0; k < a.K; ++k) {
-            float bv = 0.f;
-            int bi = -1;
-#pragma unroll
-            for (int j = 0; j < kMaxE / 64; ++j)
-                if (better(v[j], id[j], bv, bi)) { bv = v[j]; bi = id[j]; }
-            for (int o = 32; o > 0; o >>= 1) {
-                const float ov = __shfl_xor(bv, o, 64);
-                const int oi = __shfl_xor(bi, o, 64);
-                if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-            }
-#pragma unroll
-            for (int j = 0; j < kMaxE / 64; ++j)
-                if (id[j] == bi) id[j] = -1;
-            const float p = expf(bv - m) / s;
-            wsum += p;
-            if (lane == k) { my_w = p; my_i = bi; }
-        }
-        if (lane < a.K) {
-            a.idx[b * a.K + lane] = my_i;
-            a.w[b * a.K + lane] = a.renorm ? my_w / wsum : my_w;
-            if (s_idx) s_idx[b * a.K + lane] = my_i;
+        for (; g < E; ++g) cnt += row[g] > mine || (row[g] == mine && g < f);
+        if (cnt < K) {
+            win[b * K + cnt] = f;
+            if (cnt == 0) rowmax[b] = z[i];
         }
     }
-    if (tid == 0) atomicExch(a.ticket, 0u);
+    __syncthreads();
+    for (int b = wave; b < a.B; b += kThreads / 64) {
+        // softmax sum (NaN-free inputs assumed for the weights)
+        const float m = rowmax[b];
+        float s = 0.f;
+        for (int f = lane; f < E; f += 64) s += expf(z[b * E + f] - m);
+        s = wave_sum(s);
+        float p = 0.f;
+        int e = 0;
+        if (lane < K) {
+            e = win[b * K + lane];
+            p = expf(z[b * E + e] - m) / s;
+        }
+        const float wsum = wave_sum(p);
+        if (lane < K) {
+            a.idx[b * K + lane] = e;
+            a.w[b * K + lane] = a.renorm ? p / wsum : p;
+            if (s_idx) s_idx[b * K + lane] = e;
+        }
+    }
     __syncthreads();
 }
 

@@ -35,9 +35,10 @@ __global__ __launch_bounds__(kThreads) void co_count_kernel(const int32_t* sel, 
 // Algorithm 1, selection: CCT_i[e] = the K largest counts of Co_i[e][*]
 // (equal counts -> lower index), all with confidence "10".
 __global__ __launch_bounds__(kThreads) void cct_build_kernel(const int32_t* co, int E, int K,
-                                                             uint8_t* idx, uint8_t* conf) {
+                                                             size_t stride, uint8_t* idx, uint8_t* conf) {
     __shared__ int32_t row[kMaxE];
     const size_t r = blockIdx.x;   // (pair, expert) row
+    const size_t out = (r / E) * stride + (r % E) * K;
     for (int f = threadIdx.x; f < E; f += kThreads) row[f] = co[r * E + f];
     __syncthreads();
     for (int f = threadIdx.x; f < E; f += kThreads) {
@@ -45,8 +46,8 @@ __global__ __launch_bounds__(kThreads) void cct_build_kernel(const int32_t* co, 
         int rank = 0;
         for (int g = 0; g < E; ++g) rank += (row[g] > c) || (row[g] == c && g < f);
         if (rank < K) {
-            idx[r * K + rank] = uint8_t(f);
-            conf[r * K + rank] = uint8_t(kConfInit);
+            idx[out + rank] = uint8_t(f);
+            conf[out + rank] = uint8_t(kConfInit);
         }
     }
 }
@@ -62,40 +63,48 @@ __device__ __forceinline__ void sorted_row(const int32_t* src, int K, uint8_t* d
 }
 
 __global__ __launch_bounds__(kThreads) void ht_init_kernel(const int32_t* sel_last, int B, int L,
-                                                           int K, uint8_t* ht) {
+                                                           int K, size_t stride, uint8_t* ht) {
     const int l = blockIdx.x, b = blockIdx.y;
-    sorted_row(sel_last + (size_t(b) * L + l) * K, K, ht + (size_t(l) * B + b) * K);
+    sorted_row(sel_last + (size_t(b) * L + l) * K, K, ht + size_t(l) * stride + size_t(b) * K);
 }
 
 // ------------------------------------------------------ update and predict
 __global__ __launch_bounds__(kThreads) void update_kernel(UpdateArgs a) {
-    __shared__ UpdateShared sh;
+    __shared__ TableShared sh;
+    Seg g[kMaxSegs];
+    stage(g, update_segs(a, sh, g));
     update_body(a, sh);
 }
 
 __global__ __launch_bounds__(kThreads) void predict_kernel(PredictArgs a) {
-    __shared__ PredictShared sh;
+    __shared__ TableShared sh;
+    Seg g[kMaxSegs];
+    stage(g, predict_segs(a, sh, g));
     predict_body(a, sh);
 }
 
-// One decode layer's router, verify/update and next-layer prediction in one
-// launch: the router's last workgroup keeps the selection in LDS and runs
-// the update and the prediction on it.
-template <bool BF16>
+// The decode path's router tail, verify/update and next-layer prediction in
+// one workgroup (after the router's logits launch).  One round of loads
+// brings the logits and every table into LDS; softmax/top-K writes the
+// selection there, and the update and the prediction run on it.
 __global__ __launch_bounds__(kThreads) void route_update_predict_kernel(gating::RouteArgs r, UpdateArgs u,
                                                                         PredictArgs p) {
-    __shared__ float part[kMaxB][kThreads / 64];
-    __shared__ bool last;
-    __shared__ int32_t sel[kMaxB * kMaxK];
-    __shared__ UpdateShared ush;
-    __shared__ PredictShared psh;
-    if (!gating::logits_and_ticket<BF16>(r, part, last)) return;
-    gating::softmax_topk_tail(r, sel);
-    u.sel_cur = sel;
-    update_body(u, ush);
+    __shared__ TableShared sh;
+    Seg g[kMaxSegs];
+    u.sel_cur = nullptr;     // the selection is produced in LDS
+    p.sel_cur = nullptr;
+    int n = 0;
+    g[n++] = seg(r.zbuf, sh.z, size_t(r.B) * r.E * sizeof(float));
+    n += update_segs(u, sh, g + n);
+    n += predict_segs(p, sh, g + n);
+    stage(g, n);
+    gating::softmax_topk_tail(r, sh.z, sh.sel);
+    update_body(u, sh);
+    // with one layer the prediction reads the HT row the update just wrote
+    if (p.ht_next && p.ht_next == u.ht)
+        for (int i = threadIdx.x; i < r.B * r.K; i += kThreads) sh.htn[i] = sh.htnew[i];
     __syncthreads();
-    if (p.cidx) p.sel_cur = sel;
-    predict_body(p, psh);
+    predict_body(p, sh);
 }
 
 int check_sel_host(const int32_t* sel, size_t rows, int E, int K) {
@@ -124,19 +133,22 @@ extern "C" int stmoe_create(int L, int E, int K, int B, stmoe_predictor** out) {
     auto* p = new stmoe_predictor();
     p->L = L; p->E = E; p->K = K; p->B = B;
     p->profiled = false;
+    p->cct_stride = round4(size_t(E) * K);
+    p->ht_stride = round4(size_t(B) * K);
+    p->pend_stride = round4(size_t(B) * E);
     const size_t pairs = size_t(L > 1 ? L - 1 : 1);
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMalloc(&p->co, pairs * E * E * sizeof(int32_t));
-    if (e == hipSuccess) e = hipMalloc(&p->cct_idx, pairs * E * K);
-    if (e == hipSuccess) e = hipMalloc(&p->cct_conf, pairs * E * K);
-    if (e == hipSuccess) e = hipMalloc(&p->ht, size_t(L) * B * K);
-    if (e == hipSuccess) e = hipMalloc(&p->pend, size_t(L) * B * E);
+    if (e == hipSuccess) e = hipMalloc(&p->cct_idx, pairs * p->cct_stride);
+    if (e == hipSuccess) e = hipMalloc(&p->cct_conf, pairs * p->cct_stride);
+    if (e == hipSuccess) e = hipMalloc(&p->ht, size_t(L) * p->ht_stride);
+    if (e == hipSuccess) e = hipMalloc(&p->pend, size_t(L) * p->pend_stride);
     if (e == hipSuccess) e = hipMalloc(&p->stats, size_t(L) * 3 * sizeof(unsigned long long));
     if (e == hipSuccess) e = hipMemset(p->co, 0, pairs * E * E * sizeof(int32_t));
-    if (e == hipSuccess) e = hipMemset(p->cct_idx, 0, pairs * E * K);
-    if (e == hipSuccess) e = hipMemset(p->cct_conf, 0, pairs * E * K);
-    if (e == hipSuccess) e = hipMemset(p->ht, 0, size_t(L) * B * K);
-    if (e == hipSuccess) e = hipMemset(p->pend, 0, size_t(L) * B * E);
+    if (e == hipSuccess) e = hipMemset(p->cct_idx, 0, pairs * p->cct_stride);
+    if (e == hipSuccess) e = hipMemset(p->cct_conf, 0, pairs * p->cct_stride);
+    if (e == hipSuccess) e = hipMemset(p->ht, 0, size_t(L) * p->ht_stride);
+    if (e == hipSuccess) e = hipMemset(p->pend, 0, size_t(L) * p->pend_stride);
     if (e == hipSuccess) e = hipMemset(p->stats, 0, size_t(L) * 3 * sizeof(unsigned long long));
     if (e == hipSuccess) e = hipDeviceSynchronize();
     if (e != hipSuccess) {
@@ -172,7 +184,7 @@ extern "C" int stmoe_profile(stmoe_predictor* p, const int32_t* sel, int P) {
     STMOE_HIP(hipMalloc(&dsel, n * sizeof(int32_t)));
     hipError_t e = hipMemcpy(dsel, sel, n * sizeof(int32_t), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemset(p->co, 0, pairs * E * E * sizeof(int32_t));
-    if (e == hipSuccess) e = hipMemset(p->pend, 0, size_t(L) * B * E);
+    if (e == hipSuccess) e = hipMemset(p->pend, 0, size_t(L) * p->pend_stride);
     if (e == hipSuccess) e = hipMemset(p->stats, 0, size_t(L) * 3 * sizeof(unsigned long long));
     if (e == hipSuccess && L > 1) {
         hipLaunchKernelGGL(co_count_kernel, dim3(P, L - 1), dim3(kThreads), 0, 0, dsel, P, B, L, E,
@@ -180,13 +192,13 @@ extern "C" int stmoe_profile(stmoe_predictor* p, const int32_t* sel, int P) {
         e = hipGetLastError();
         if (e == hipSuccess) {
             hipLaunchKernelGGL(cct_build_kernel, dim3(unsigned((L - 1) * E)), dim3(kThreads), 0, 0,
-                               p->co, E, K, p->cct_idx, p->cct_conf);
+                               p->co, E, K, p->cct_stride, p->cct_idx, p->cct_conf);
             e = hipGetLastError();
         }
     }
     if (e == hipSuccess) {
         hipLaunchKernelGGL(ht_init_kernel, dim3(L, B), dim3(kThreads), 0, 0,
-                           dsel + size_t(P - 1) * B * L * K, B, L, K, p->ht);
+                           dsel + size_t(P - 1) * B * L * K, B, L, K, p->ht_stride, p->ht);
         e = hipGetLastError();
     }
     if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -235,8 +247,10 @@ extern "C" int stmoe_predict(stmoe_predictor* p, int layer, const int32_t* sel_c
 }
 
 namespace stmoe {
+int launch_route_logits(const gating::RouteArgs& a, hipStream_t s);
+
 // Internal: router + verify/update at `layer` + prediction of the next layer
-// (layer 0 of the next token after the last layer) in one launch.  The
+// (layer 0 of the next token after the last layer) in two launches.  The
 // caller has validated the shapes; the routing workspace follows
 // moe_route_workspace_bytes.
 int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int renorm, int32_t* idx,
@@ -260,17 +274,13 @@ int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int
     r.w = w;
     r.logits = nullptr;
     r.zbuf = reinterpret_cast<float*>(route_ws);
-    r.ticket = reinterpret_cast<unsigned*>(reinterpret_cast<char*>(route_ws) +
-                                           (size_t(p->B) * p->E * sizeof(float) + 255) / 256 * 256);
     const UpdateArgs u = update_args(p, layer, sel_prev, idx, online);
     const PredictArgs q = layer + 1 < p->L
                               ? predict_args(p, layer, idx, use, nullptr, nullptr, max_score, ranked, n_ranked)
                               : predict_args(p, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr, max_score,
                                              ranked, n_ranked);
-    if (r.bf16)
-        hipLaunchKernelGGL(route_update_predict_kernel<true>, dim3(p->E), dim3(kThreads), 0, s, r, u, q);
-    else
-        hipLaunchKernelGGL(route_update_predict_kernel<false>, dim3(p->E), dim3(kThreads), 0, s, r, u, q);
+    if (int rc = launch_route_logits(r, s)) return rc;
+    hipLaunchKernelGGL(route_update_predict_kernel, dim3(1), dim3(kThreads), 0, s, r, u, q);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }
@@ -284,11 +294,12 @@ extern "C" int stmoe_export(stmoe_predictor* p, int32_t* co, uint8_t* cct_idx, u
     STMOE_HIP(hipDeviceSynchronize());
     if (co && pairs)
         STMOE_HIP(hipMemcpy(co, p->co, pairs * p->E * p->E * sizeof(int32_t), hipMemcpyDeviceToHost));
+    const size_t ek = size_t(p->E) * p->K, bk = size_t(p->B) * p->K;
     if (cct_idx && pairs)
-        STMOE_HIP(hipMemcpy(cct_idx, p->cct_idx, pairs * p->E * p->K, hipMemcpyDeviceToHost));
+        STMOE_HIP(hipMemcpy2D(cct_idx, ek, p->cct_idx, p->cct_stride, ek, pairs, hipMemcpyDeviceToHost));
     if (cct_conf && pairs)
-        STMOE_HIP(hipMemcpy(cct_conf, p->cct_conf, pairs * p->E * p->K, hipMemcpyDeviceToHost));
-    if (ht) STMOE_HIP(hipMemcpy(ht, p->ht, size_t(p->L) * p->B * p->K, hipMemcpyDeviceToHost));
+        STMOE_HIP(hipMemcpy2D(cct_conf, ek, p->cct_conf, p->cct_stride, ek, pairs, hipMemcpyDeviceToHost));
+    if (ht) STMOE_HIP(hipMemcpy2D(ht, bk, p->ht, p->ht_stride, bk, p->L, hipMemcpyDeviceToHost));
     return STMOE_OK;
 }
 
@@ -303,11 +314,12 @@ extern "C" int stmoe_import(stmoe_predictor* p, const uint8_t* cct_idx, const ui
     }
     for (size_t i = 0; i < size_t(p->L) * p->B * p->K; ++i) STMOE_CHECK(ht[i] < p->E, "HT index out of range");
     STMOE_HIP(hipDeviceSynchronize());
+    const size_t ek = size_t(p->E) * p->K, bk = size_t(p->B) * p->K;
     if (pairs) {
-        STMOE_HIP(hipMemcpy(p->cct_idx, cct_idx, pairs * p->E * p->K, hipMemcpyHostToDevice));
-        STMOE_HIP(hipMemcpy(p->cct_conf, cct_conf, pairs * p->E * p->K, hipMemcpyHostToDevice));
+        STMOE_HIP(hipMemcpy2D(p->cct_idx, p->cct_stride, cct_idx, ek, ek, pairs, hipMemcpyHostToDevice));
+        STMOE_HIP(hipMemcpy2D(p->cct_conf, p->cct_stride, cct_conf, ek, ek, pairs, hipMemcpyHostToDevice));
     }
-    STMOE_HIP(hipMemcpy(p->ht, ht, size_t(p->L) * p->B * p->K, hipMemcpyHostToDevice));
+    STMOE_HIP(hipMemcpy2D(p->ht, p->ht_stride, ht, bk, bk, p->L, hipMemcpyHostToDevice));
     p->profiled = true;
     return STMOE_OK;
 }

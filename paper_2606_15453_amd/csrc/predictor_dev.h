@@ -1,22 +1,30 @@
 // Predictor state and device code (Section 4.2): the Table Update
 // (Algorithm 3, with the HT overwrite and the hit count of the verify step)
 // and the Expert Predict function (Algorithm 2 with Eq. 1).  Shared by the
-// standalone predictor kernels and the fused router + predictor kernel.
-// Both bodies run in one 256-thread workgroup.
+// standalone predictor kernels and the decode path's router + predictor
+// kernel.  Both bodies run in one 256-thread workgroup on an LDS image of
+// the tables.
 #pragma once
 
 #include "common.h"
 
+// Per-layer byte tables start on 4-byte boundaries (strides rounded up) so
+// the kernels copy them into LDS as whole words.
 struct stmoe_predictor {
     int L, E, K, B;
+    size_t cct_stride;           // bytes per layer pair: E*K rounded up to 4
+    size_t ht_stride;            // bytes per layer: B*K rounded up to 4
+    size_t pend_stride;          // bytes per layer: B*E rounded up to 4
     int32_t* co;                 // [L-1][E][E] profiling co-activation counts
-    uint8_t* cct_idx;            // [L-1][E][K]
-    uint8_t* cct_conf;           // [L-1][E][K]
-    uint8_t* ht;                 // [L][B][K], each row sorted ascending
-    uint8_t* pend;               // [L][B][E] last prediction scores made for each layer
+    uint8_t* cct_idx;            // [L-1] x cct_stride, each [E][K]
+    uint8_t* cct_conf;           // [L-1] x cct_stride, each [E][K]
+    uint8_t* ht;                 // [L] x ht_stride, each [B][K], rows sorted ascending
+    uint8_t* pend;               // [L] x pend_stride, each [B][E]: last prediction per layer
     unsigned long long* stats;   // [L][3]: hits, |A|, |P|
     bool profiled;
 };
+
+inline size_t round4(size_t n) { return (n + 3) / 4 * 4; }
 
 namespace stmoe {
 namespace pred {
@@ -29,7 +37,7 @@ constexpr int kHtScore = 2;    // HT confidences stay at "10"
 
 struct UpdateArgs {
     const int32_t* sel_prev;   // [B][K] or null at layer 0
-    const int32_t* sel_cur;    // [B][K] (global or LDS)
+    const int32_t* sel_cur;    // [B][K], or null when the selection is already in LDS
     uint8_t* cidx;             // CCT_{layer-1} [E][K] or null
     uint8_t* cconf;
     uint8_t* ht;               // HT[layer] [B][K]
@@ -38,88 +46,8 @@ struct UpdateArgs {
     int B, E, K, online;
 };
 
-struct UpdateShared {
-    int32_t F[kMaxK];                 // actual set, ascending
-    uint8_t snap[kMaxK * kMaxK];      // entries before this row's update
-    uint8_t repl[kMaxK * kMaxK];      // slot is replaced
-    unsigned hits, npred;
-};
-
-// Algorithm 3 on CCT_{layer-1} for the entries selected at layer-1, rows
-// b = 0..B-1 in order; HT[layer][b] <- sorted selection; hits against the
-// prediction made for this layer.  One lane per (entry, slot).
-__device__ void update_body(const UpdateArgs& a, UpdateShared& sh) {
-    const int tid = threadIdx.x, K = a.K, KK = a.K * a.K;
-    if (tid == 0) { sh.hits = 0; sh.npred = 0; }
-    for (int b = 0; b < a.B; ++b) {
-        const int32_t* cur = a.sel_cur + b * K;
-        if (tid < K) {
-            const int v = cur[tid];
-            int rank = 0;
-            for (int j = 0; j < K; ++j) rank += cur[j] < v;
-            sh.F[rank] = v;
-        }
-        int e = 0, s = 0, conf = 0;
-        bool hit = false;
-        const bool upd = a.cidx != nullptr && a.online && tid < KK;
-        bool upd_ok = upd;
-        if (upd) {
-            e = a.sel_prev[b * K + tid / K];
-            s = tid % K;
-            upd_ok = e >= 0 && e < a.E;      // out-of-range selections are ignored
-            sh.snap[tid] = upd_ok ? a.cidx[e * K + s] : 0xff;
-            conf = upd_ok ? a.cconf[e * K + s] : 1;
-        }
-        __syncthreads();
-        if (upd) {
-            const int f = sh.snap[tid];
-            for (int j = 0; j < K; ++j) hit |= (sh.F[j] == f);
-            sh.repl[tid] = upd_ok && (!hit && conf == 0);
-        }
-        __syncthreads();
-        if (upd_ok) {
-            if (hit) {
-                conf = min(conf + 1, kConfMax);
-            } else if (conf > 0) {
-                conf -= 1;
-            } else {
-                // the rank-th expert of F (ascending) absent from the entry's snapshot
-                const int base = tid - s;
-                int rank = 0;
-                for (int q = 0; q < s; ++q) rank += sh.repl[base + q];
-                int pick = -1;
-                for (int j = 0; j < K && pick < 0; ++j) {
-                    bool held = false;
-                    for (int q = 0; q < K; ++q) held |= (sh.snap[base + q] == sh.F[j]);
-                    if (!held) {
-                        if (rank == 0) pick = sh.F[j];
-                        --rank;
-                    }
-                }
-                if (pick >= 0) a.cidx[e * K + s] = uint8_t(pick);
-                conf = kConfInit;
-            }
-            a.cconf[e * K + s] = uint8_t(conf);
-        }
-        // verification against the prediction made for this layer
-        if (tid < K && cur[tid] >= 0 && cur[tid] < a.E && a.pend[b * a.E + cur[tid]] >= kThreshold)
-            atomicAdd(&sh.hits, 1u);
-        for (int f = tid; f < a.E; f += kThreads)
-            if (a.pend[b * a.E + f] >= kThreshold) atomicAdd(&sh.npred, 1u);
-        if (tid < K) a.ht[b * K + tid] = uint8_t(sh.F[tid]);
-        // the next row may update the same entries: make this row's writes visible
-        __threadfence_block();
-        __syncthreads();
-    }
-    if (tid == 0) {
-        atomicAdd(&a.stats[0], (unsigned long long)sh.hits);
-        atomicAdd(&a.stats[1], (unsigned long long)(a.B * K));
-        atomicAdd(&a.stats[2], (unsigned long long)sh.npred);
-    }
-}
-
 struct PredictArgs {
-    const int32_t* sel_cur;    // [B][K] (global or LDS; unused when cidx is null)
+    const int32_t* sel_cur;    // [B][K], or null when in LDS or unused (cidx null)
     const uint8_t* cidx;       // CCT_layer [E][K] or null (layer -1 or HT-only)
     const uint8_t* cconf;
     const uint8_t* ht_next;    // HT[layer+1] [B][K] or null (CCT-only)
@@ -132,55 +60,302 @@ struct PredictArgs {
     int B, E, K;
 };
 
-struct PredictShared {
-    int sc[kMaxB * kMaxE];
-    int mx[kMaxE];
+// Scores rank through a 64-bin histogram.  With distinct experts in every
+// CCT entry a score is at most K * 3 + 2 = 50; larger ones (repeated experts
+// in an imported entry) take an exact O(E) ranking instead.
+constexpr int kScoreBins = 64;
+static_assert(kMaxK * kConfMax + kHtScore < kScoreBins, "score histogram too small");
+static_assert(kMaxE <= kThreads, "one expert per thread in the ranking");
+
+// LDS image of every table one update + predict touches.  The tables are
+// small (at most E*K = 4 KB each), so each kernel copies them in with one
+// round of independent loads and then works from LDS: the dependent chains
+// (selection -> CCT entry -> slot) cost LDS latency instead of HBM latency.
+struct TableShared {
+    union {
+        float z[kMaxB * kMaxE];       // router logits (fused kernel, before top-K)
+        int sc[kMaxB * kMaxE];        // prediction scores
+    };
+    __align__(16) uint8_t uidx[kMaxE * kMaxK];    // CCT_{layer-1} (update)
+    __align__(16) uint8_t uconf[kMaxE * kMaxK];
+    __align__(16) uint8_t pidx[kMaxE * kMaxK];    // CCT_layer (predict)
+    __align__(16) uint8_t pconf[kMaxE * kMaxK];
+    __align__(16) uint8_t pend[kMaxB * kMaxE];    // prediction made for this layer
+    __align__(16) uint8_t htn[kMaxB * kMaxK];     // HT[layer+1]
+    __align__(16) uint8_t htnew[kMaxB * kMaxK];   // HT[layer] after the update
+    __align__(16) int32_t prev[kMaxB * kMaxK];
+    __align__(16) int32_t sel[kMaxB * kMaxK];
+    int32_t F[kMaxK];                 // actual set of the current row, ascending
+    uint8_t snap[kMaxK * kMaxK];      // entries before this row's update
+    uint8_t repl[kMaxK * kMaxK];      // slot is replaced
+    uint8_t absent[kMaxK * kMaxK];    // F[slot] is absent from the entry's snapshot
+    int mx[kMaxE];                    // max score over rows
+    int whist[kThreads / 64][kScoreBins];  // per-wave histogram of candidate scores
+    int greater[kScoreBins];          // candidates scoring above each value
+    unsigned hits, npred;
 };
+
+// One contiguous global -> LDS copy of n 4-byte words (null src: nothing).
+struct Seg {
+    const uint32_t* src;
+    uint32_t* dst;
+    int n;
+};
+
+__device__ __forceinline__ Seg seg(const void* src, void* dst, size_t bytes) {
+    Seg g;
+    g.src = reinterpret_cast<const uint32_t*>(src);
+    g.dst = reinterpret_cast<uint32_t*>(dst);
+    g.n = src ? int((bytes + 3) / 4) : 0;
+    return g;
+}
+
+constexpr int kMaxSegs = 10;
+constexpr int kStageRegs = 4;   // words per thread per segment in one pass
+
+// Copy every segment into LDS.  In each pass a thread loads up to
+// kStageRegs words of every segment before its first LDS store, so the whole
+// copy is one memory round trip at decode sizes.  Ends with a barrier.
+__device__ void stage(const Seg* g, int nseg) {
+    int most = 0;
+#pragma unroll
+    for (int j = 0; j < kMaxSegs; ++j)
+        if (j < nseg) most = max(most, g[j].n);
+    for (int base = 0; base < most; base += kThreads * kStageRegs) {
+        uint32_t val[kMaxSegs][kStageRegs];
+#pragma unroll
+        for (int j = 0; j < kMaxSegs; ++j)
+#pragma unroll
+            for (int r = 0; r < kStageRegs; ++r) {
+                const int i = base + r * kThreads + int(threadIdx.x);
+                val[j][r] = j < nseg && i < g[j].n ? g[j].src[i] : 0u;
+            }
+#pragma unroll
+        for (int j = 0; j < kMaxSegs; ++j)
+#pragma unroll
+            for (int r = 0; r < kStageRegs; ++r) {
+                const int i = base + r * kThreads + int(threadIdx.x);
+                if (j < nseg && i < g[j].n) g[j].dst[i] = val[j][r];
+            }
+    }
+    __syncthreads();
+}
+
+// Segments for an update (always 5 slots, unused ones empty, so that the
+// slot positions are compile-time constants); returns the count.
+__device__ __forceinline__ int update_segs(const UpdateArgs& a, TableShared& sh, Seg* g) {
+    const int EK = a.E * a.K, BK = a.B * a.K;
+    const bool cct = a.cidx != nullptr && a.online;
+    int n = 0;
+    g[n++] = seg(cct ? a.cidx : nullptr, sh.uidx, EK);
+    g[n++] = seg(cct ? a.cconf : nullptr, sh.uconf, EK);
+    g[n++] = seg(cct ? a.sel_prev : nullptr, sh.prev, BK * sizeof(int32_t));
+    g[n++] = seg(a.pend, sh.pend, a.B * a.E);
+    g[n++] = seg(a.sel_cur, sh.sel, BK * sizeof(int32_t));
+    return n;
+}
+
+// Segments for a prediction (always 4 slots); returns the count.
+__device__ __forceinline__ int predict_segs(const PredictArgs& a, TableShared& sh, Seg* g) {
+    const int EK = a.E * a.K, BK = a.B * a.K;
+    int n = 0;
+    g[n++] = seg(a.cidx, sh.pidx, EK);
+    g[n++] = seg(a.cconf, sh.pconf, EK);
+    g[n++] = seg(a.ht_next, sh.htn, BK);
+    g[n++] = seg(a.cidx ? a.sel_cur : nullptr, sh.sel, BK * sizeof(int32_t));
+    return n;
+}
+
+// Algorithm 3 on CCT_{layer-1} for the entries selected at layer-1, rows
+// b = 0..B-1 in order; HT[layer][b] <- sorted selection; hits against the
+// prediction made for this layer.  One lane per (entry, slot).  Works on the
+// LDS image (staged by the caller), then writes the touched CCT entries, HT
+// and the hit counts back.  Loops over K run to kMaxK with a predicate so
+// their LDS reads issue together.  Ends with a barrier.
+__device__ void update_body(const UpdateArgs& a, TableShared& sh) {
+    const int tid = threadIdx.x, K = a.K, KK = a.K * a.K, E = a.E;
+    const bool cct = a.cidx != nullptr && a.online;
+    unsigned my_hits = 0, my_pred = 0;
+    if (tid == 0) { sh.hits = 0; sh.npred = 0; }
+    for (int b = 0; b < a.B; ++b) {
+        const int32_t* cur = sh.sel + b * K;
+        if (tid < K) {
+            const int v = cur[tid];
+            int rank = 0;
+#pragma unroll
+            for (int j = 0; j < kMaxK; ++j)
+                if (j < K) rank += cur[j] < v;
+            sh.F[rank] = v;
+        }
+        const bool upd = cct && tid < KK;
+        const int s = upd ? tid % K : 0, base = tid - s;
+        int e = 0, conf = 0;
+        bool upd_ok = upd;
+        if (upd) {
+            e = sh.prev[b * K + tid / K];
+            upd_ok = e >= 0 && e < E;      // out-of-range selections are ignored
+            sh.snap[tid] = upd_ok ? sh.uidx[e * K + s] : 0xff;
+            conf = upd_ok ? sh.uconf[e * K + s] : 1;
+        }
+        __syncthreads();
+        bool hit = false;
+        if (upd) {
+            const int f = sh.snap[tid], mine = sh.F[s];
+            bool held = false;
+#pragma unroll
+            for (int j = 0; j < kMaxK; ++j)
+                if (j < K) {
+                    hit |= sh.F[j] == f;
+                    held |= sh.snap[base + j] == mine;
+                }
+            sh.repl[tid] = upd_ok && (!hit && conf == 0);
+            sh.absent[tid] = !held;
+        }
+        __syncthreads();
+        if (upd_ok) {
+            if (hit) {
+                conf = min(conf + 1, kConfMax);
+            } else if (conf > 0) {
+                conf -= 1;
+            } else {
+                // the rank-th expert of F (ascending) absent from the entry's
+                // snapshot, rank = replaced slots before this one
+                int rank = 0, seen = 0, pick = -1;
+#pragma unroll
+                for (int q = 0; q < kMaxK; ++q)
+                    if (q < s) rank += sh.repl[base + q];
+#pragma unroll
+                for (int j = 0; j < kMaxK; ++j)
+                    if (j < K && sh.absent[base + j]) {
+                        if (seen == rank) pick = sh.F[j];
+                        ++seen;
+                    }
+                if (pick >= 0) sh.uidx[e * K + s] = uint8_t(pick);
+                conf = kConfInit;
+            }
+            sh.uconf[e * K + s] = uint8_t(conf);
+        }
+        // verification against the prediction made for this layer
+        if (tid < K && cur[tid] >= 0 && cur[tid] < E && sh.pend[b * E + cur[tid]] >= kThreshold) ++my_hits;
+        for (int f = tid; f < E; f += kThreads) my_pred += sh.pend[b * E + f] >= kThreshold;
+        if (tid < K) {
+            sh.htnew[b * K + tid] = uint8_t(sh.F[tid]);
+            a.ht[b * K + tid] = uint8_t(sh.F[tid]);
+        }
+        // the next row may update the same entries
+        __syncthreads();
+    }
+    if (cct) {
+        // write back every entry slot this layer's rows touched (duplicates
+        // carry the same final value)
+        for (int i = tid; i < a.B * KK; i += kThreads) {
+            const int e = sh.prev[i / K], s = i % K;
+            if (e >= 0 && e < E) {
+                a.cidx[e * K + s] = sh.uidx[e * K + s];
+                a.cconf[e * K + s] = sh.uconf[e * K + s];
+            }
+        }
+    }
+    if (my_hits) atomicAdd(&sh.hits, my_hits);
+    if (my_pred) atomicAdd(&sh.npred, my_pred);
+    __syncthreads();
+    if (tid == 0) {
+        atomicAdd(&a.stats[0], (unsigned long long)sh.hits);
+        atomicAdd(&a.stats[1], (unsigned long long)(a.B * K));
+        atomicAdd(&a.stats[2], (unsigned long long)sh.npred);
+    }
+}
 
 // Algorithm 2 with Eq. 1: score_b[f] = sum_{e in A[b]} conf of f in CCT[e]
 // + 2 [f in HT_next[b]]; PrefetchSet = {f : score >= 2}; the union over rows
 // ranked by (max score desc, index asc).  Integer atomics in LDS: exact.
-__device__ void predict_body(const PredictArgs& a, PredictShared& sh) {
-    const int tid = threadIdx.x, K = a.K, E = a.E;
+// Reads the LDS image (staged by the caller; htn holds HT[layer+1]).
+__device__ void predict_body(const PredictArgs& a, TableShared& sh) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int K = a.K, KK = a.K * a.K, E = a.E;
     for (int i = tid; i < a.B * E; i += kThreads) sh.sc[i] = 0;
+    for (int i = tid; i < (kThreads / 64) * kScoreBins; i += kThreads) (&sh.whist[0][0])[i] = 0;
     __syncthreads();
-    for (int b = 0; b < a.B; ++b) {
-        if (a.cidx && tid < K * K) {
-            const int e = a.sel_cur[b * K + tid / K], s = tid % K;
-            if (e >= 0 && e < E) atomicAdd(&sh.sc[b * E + a.cidx[e * K + s]], int(a.cconf[e * K + s]));
+    if (a.cidx) {
+        for (int i = tid; i < a.B * KK; i += kThreads) {
+            const int b = i / KK, e = sh.sel[b * K + (i % KK) / K], s = i % K;
+            const int f = e >= 0 && e < E ? sh.pidx[e * K + s] : E;
+            if (f < E) atomicAdd(&sh.sc[b * E + f], int(sh.pconf[e * K + s]));
         }
-        if (a.ht_next && tid < K) atomicAdd(&sh.sc[b * E + a.ht_next[b * K + tid]], kHtScore);
     }
+    if (a.ht_next)
+        for (int i = tid; i < a.B * K; i += kThreads)
+            if (sh.htn[i] < E) atomicAdd(&sh.sc[(i / K) * E + sh.htn[i]], kHtScore);
     __syncthreads();
     for (int i = tid; i < a.B * E; i += kThreads) {
         a.pend[i] = uint8_t(sh.sc[i]);
         if (a.score) a.score[i] = uint8_t(sh.sc[i]);
     }
-    for (int f = tid; f < E; f += kThreads) {
-        int m = 0;
-        for (int b = 0; b < a.B; ++b) m = max(m, sh.sc[b * E + f]);
-        sh.mx[f] = m;
+    // one expert per thread: max over rows, then its place in the ranking
+    const int f = tid;
+    int m = 0;
+    if (f < E) {
+#pragma unroll
+        for (int b = 0; b < kMaxB; ++b)
+            if (b < a.B) m = max(m, sh.sc[b * E + f]);
         if (a.mask) a.mask[f] = m >= kThreshold;
         if (a.max_score) a.max_score[f] = uint8_t(m);
     }
-    __syncthreads();
-    if (a.ranked || a.n_ranked) {
-        if (a.ranked)
-            for (int f = tid; f < E; f += kThreads) a.ranked[f] = -1;
-        __syncthreads();
-        for (int f = tid; f < E; f += kThreads) {
-            if (sh.mx[f] < kThreshold) continue;
-            int rank = 0;
-            for (int g = 0; g < E; ++g)
-                rank += sh.mx[g] >= kThreshold && (sh.mx[g] > sh.mx[f] || (sh.mx[g] == sh.mx[f] && g < f));
-            if (a.ranked) a.ranked[rank] = f;
+    if (!a.ranked && !a.n_ranked) return;
+    const bool cand = f < E && m >= kThreshold;
+    if (f < E) sh.mx[f] = m;
+    if (cand && m < kScoreBins) atomicAdd(&sh.whist[wave][m], 1);
+    if (__syncthreads_or(cand && m >= kScoreBins)) {
+        // exact fallback for out-of-histogram scores
+        int total = 0;
+        for (int g = 0; g < E; ++g) total += sh.mx[g] >= kThreshold;
+        if (a.ranked && f < E) {
+            if (cand) {
+                int rank = 0;
+                for (int g = 0; g < E; ++g)
+                    rank += sh.mx[g] >= kThreshold && (sh.mx[g] > m || (sh.mx[g] == m && g < f));
+                a.ranked[rank] = f;
+            }
+            if (f >= total) a.ranked[f] = -1;
         }
-        if (a.n_ranked && tid == 0) {
-            int count = 0;
-            for (int g = 0; g < E; ++g) count += sh.mx[g] >= kThreshold;
-            *a.n_ranked = count;
-        }
+        if (a.n_ranked && tid == 0) *a.n_ranked = total;
+        return;
     }
+    if (wave == 0) {
+        // greater[t] = candidates with score > t: suffix sum of the histogram
+        int h = 0;
+#pragma unroll
+        for (int w = 0; w < kThreads / 64; ++w) h += sh.whist[w][lane];
+        int suf = h;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_down(suf, o, 64);
+            if (lane + o < 64) suf += y;
+        }
+        sh.greater[lane] = suf - h;
+    }
+    __syncthreads();
+    // lanes of this wave with the same score and a lower index: equality of
+    // all six score bits, one ballot per bit
+    unsigned long long same = __ballot(cand);
+#pragma unroll
+    for (int bit = 0; bit < 6; ++bit) {
+        const bool on = (m >> bit) & 1;
+        const unsigned long long bm = __ballot(cand && on);
+        same &= on ? bm : ~bm;
+    }
+    const int total = sh.greater[kThreshold - 1];
+    if (a.ranked && f < E) {
+        if (cand) {
+            int rank = sh.greater[m] + __popcll(same & ((1ull << lane) - 1ull));
+#pragma unroll
+            for (int w = 0; w < kThreads / 64; ++w)
+                if (w < wave) rank += sh.whist[w][m];
+            a.ranked[rank] = f;
+        }
+        if (f >= total) a.ranked[f] = -1;
+    }
+    if (a.n_ranked && tid == 0) *a.n_ranked = total;
 }
 
 // Host-side construction of the per-layer argument blocks.
@@ -189,10 +364,10 @@ inline UpdateArgs update_args(stmoe_predictor* p, int layer, const int32_t* sel_
     UpdateArgs a;
     a.sel_prev = sel_prev;
     a.sel_cur = sel_cur;
-    a.cidx = layer >= 1 ? p->cct_idx + size_t(layer - 1) * p->E * p->K : nullptr;
-    a.cconf = layer >= 1 ? p->cct_conf + size_t(layer - 1) * p->E * p->K : nullptr;
-    a.ht = p->ht + size_t(layer) * p->B * p->K;
-    a.pend = p->pend + size_t(layer) * p->B * p->E;
+    a.cidx = layer >= 1 ? p->cct_idx + size_t(layer - 1) * p->cct_stride : nullptr;
+    a.cconf = layer >= 1 ? p->cct_conf + size_t(layer - 1) * p->cct_stride : nullptr;
+    a.ht = p->ht + size_t(layer) * p->ht_stride;
+    a.pend = p->pend + size_t(layer) * p->pend_stride;
     a.stats = p->stats + size_t(layer) * 3;
     a.B = p->B;
     a.E = p->E;
@@ -209,10 +384,10 @@ inline PredictArgs predict_args(stmoe_predictor* p, int layer, const int32_t* se
     const int tgt = layer + 1;
     PredictArgs a;
     a.sel_cur = sel_cur;
-    a.cidx = cct ? p->cct_idx + size_t(layer) * p->E * p->K : nullptr;
-    a.cconf = cct ? p->cct_conf + size_t(layer) * p->E * p->K : nullptr;
-    a.ht_next = (use & STMOE_USE_HT) ? p->ht + size_t(tgt) * p->B * p->K : nullptr;
-    a.pend = p->pend + size_t(tgt) * p->B * p->E;
+    a.cidx = cct ? p->cct_idx + size_t(layer) * p->cct_stride : nullptr;
+    a.cconf = cct ? p->cct_conf + size_t(layer) * p->cct_stride : nullptr;
+    a.ht_next = (use & STMOE_USE_HT) ? p->ht + size_t(tgt) * p->ht_stride : nullptr;
+    a.pend = p->pend + size_t(tgt) * p->pend_stride;
     a.score = score;
     a.mask = mask;
     a.max_score = max_score;

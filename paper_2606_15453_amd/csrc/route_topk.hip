@@ -1,11 +1,10 @@
 // Gating (Section 2): logits z = x W_g^T, softmax, top-K by logit.
 //
-// One launch.  Each workgroup computes the logits of one expert row for all
-// B tokens (256 lanes split H into 16-byte chunks, DPP wave sums, one LDS
-// combine), writes them to the workspace and takes a completion ticket.  The
-// workgroup that takes the last ticket runs softmax and top-K: one wave per
-// batch row, K rounds of a wave-wide arg-max (value desc, index asc).  That
-// workgroup also resets the ticket, so the workspace is zero again on exit.
+// Two launches.  route_logits_kernel: one workgroup per expert row computes
+// its logits for all B tokens (256 lanes split H into 16-byte chunks, DPP
+// wave sums, one LDS combine) into the workspace.  route_tail_kernel: one
+// workgroup runs softmax and top-K, one wave per batch row, K rounds of a
+// wave-wide arg-max (value desc, index asc).
 #include "gating_dev.h"
 
 namespace stmoe {
@@ -14,11 +13,13 @@ namespace {
 using namespace gating;
 
 template <bool BF16>
-__global__ __launch_bounds__(kThreads) void route_topk_kernel(RouteArgs a) {
+__global__ __launch_bounds__(kThreads) void route_logits_kernel(RouteArgs a) {
     __shared__ float part[kMaxB][kThreads / 64];
-    __shared__ bool last;
-    if (!logits_and_ticket<BF16>(a, part, last)) return;
-    softmax_topk_tail(a, nullptr);
+    expert_logits<BF16>(a, part);
+}
+
+__global__ __launch_bounds__(kThreads) void route_tail_kernel(RouteArgs a) {
+    softmax_topk_tail(a, a.zbuf, nullptr);
 }
 
 }  // namespace
@@ -30,8 +31,20 @@ using stmoe::gating::kThreads;
 
 extern "C" size_t moe_route_workspace_bytes(int B, int E) {
     if (B < 1 || E < 1) return 0;
-    return (size_t(B) * E * sizeof(float) + 255) / 256 * 256 + 256;
+    return (size_t(B) * E * sizeof(float) + 255) / 256 * 256;
 }
+
+namespace stmoe {
+// Launch the per-expert logits kernel (the first of the router's two launches).
+int launch_route_logits(const RouteArgs& a, hipStream_t s) {
+    if (a.bf16)
+        hipLaunchKernelGGL(route_logits_kernel<true>, dim3(a.E), dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(route_logits_kernel<false>, dim3(a.E), dim3(kThreads), 0, s, a);
+    STMOE_LAUNCHED();
+    return STMOE_OK;
+}
+}  // namespace stmoe
 
 extern "C" int moe_route_topk(const void* x, const void* w_gate, int B, int H, int E, int K,
                               int dtype, int renorm, int32_t* topk_idx, float* topk_w,
@@ -60,12 +73,8 @@ extern "C" int moe_route_topk(const void* x, const void* w_gate, int B, int H, i
     a.w = topk_w;
     a.logits = logits;
     a.zbuf = reinterpret_cast<float*>(ws);
-    a.ticket = reinterpret_cast<unsigned*>(reinterpret_cast<char*>(ws) +
-                                           (size_t(B) * E * sizeof(float) + 255) / 256 * 256);
-    if (a.bf16)
-        hipLaunchKernelGGL(route_topk_kernel<true>, dim3(E), dim3(kThreads), 0, as_stream(stream), a);
-    else
-        hipLaunchKernelGGL(route_topk_kernel<false>, dim3(E), dim3(kThreads), 0, as_stream(stream), a);
+    if (int rc = launch_route_logits(a, as_stream(stream))) return rc;
+    hipLaunchKernelGGL(route_tail_kernel, dim3(1), dim3(kThreads), 0, as_stream(stream), a);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }

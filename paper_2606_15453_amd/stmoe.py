@@ -404,8 +404,9 @@ class DecodeContext:
         _call("moe_ctx_last_routing", self.h, idx.ctypes.data, w.ctypes.data)
         return idx, w
 
-    def set_timing(self, on):
-        _call("moe_ctx_set_timing", self.h, int(on))
+    def set_timing(self, every):
+        """Time the FFN of every `every`-th token (0 stops; True means every token)."""
+        _call("moe_ctx_set_timing", self.h, int(every))
 
     def timing(self):
         """(gate/up kernel ms, down kernel ms, FFN calls, distinct routed experts) since set_timing(1)."""

@@ -145,3 +145,41 @@ def test_table1_shapes_parity(name):
     cfg = W.table1_config(name, T=6).scaled(L=5, P=3)
     sel = W.planted_trace(cfg)
     _run(cfg.L, cfg.E, cfg.K, cfg.B, sel[:cfg.P], sel[cfg.P:])
+
+
+def test_repeated_experts_in_imported_entries():
+    """Imported CCT entries may repeat an expert; scores then exceed K*3+2 and
+    the ranking takes its exact out-of-histogram path.  Same result as Eq. 1."""
+    import torch
+    from gpuhelp import DEV, i32
+    from oracle.stmoe_oracle import STPredictor
+    from paper_2606_15453_amd import stmoe as S
+    rng = np.random.default_rng(9)
+    L, E, K, B = 2, 32, 16, 2
+    ci = rng.integers(0, E, size=(L - 1, E, K))
+    ci[:, ::2, :] = rng.integers(0, 3, size=(L - 1, E // 2, K))   # experts 0..2 repeated
+    cc = rng.integers(0, 4, size=(L - 1, E, K))
+    ht = np.sort(np.stack([np.stack([rng.choice(E, K, replace=False) for _ in range(B)])
+                           for _ in range(L)]), axis=2)
+    sel = np.stack([rng.choice(E, K, replace=False) for _ in range(B)]).astype(np.int32)
+    ref = STPredictor(L, E, K, B)
+    ref.cct_idx, ref.cct_conf, ref.ht = ci.tolist(), cc.tolist(), ht.tolist()
+    sc = ref.predict(0, [list(r) for r in sel])
+    assert sc.max() >= 64 and sc.max() < 256
+    gp = S.Predictor(L, E, K, B)
+    gp.import_tables(ci.astype(np.uint8), cc.astype(np.uint8), ht.astype(np.uint8))
+    score = torch.zeros((B, E), dtype=torch.uint8, device=DEV)
+    mask = torch.zeros(E, dtype=torch.uint8, device=DEV)
+    mx = torch.zeros(E, dtype=torch.uint8, device=DEV)
+    ranked = torch.zeros(E, dtype=torch.int32, device=DEV)
+    nr = torch.zeros(1, dtype=torch.int32, device=DEV)
+    gp.predict(0, i32(sel), use=3, score=score, mask=mask, ranked=ranked, n_ranked=nr, max_score=mx)
+    torch.cuda.synchronize()
+    assert np.array_equal(score.cpu().numpy(), sc)
+    assert np.array_equal(mx.cpu().numpy(), sc.max(axis=0))
+    assert np.array_equal(mask.cpu().numpy(), (sc.max(axis=0) >= 2).astype(np.uint8))
+    rr = STPredictor.ranked_union(sc)
+    assert int(nr.item()) == len(rr)
+    r = ranked.cpu().numpy()
+    assert r[:len(rr)].tolist() == rr and np.all(r[len(rr):] == -1)
+    gp.close()

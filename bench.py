@@ -401,6 +401,13 @@ def hbm_resident(wl, steps, warmup):
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
     run_tokens(ctx, wl, 0, warmup, y, S.MODE_STMOE)
     torch.cuda.synchronize()
+    # host cost of issuing one layer (a short burst, so launches never block
+    # on a full queue): below the GPU time per layer means the GPU is the bound
+    n_issue = min(8, max(1, warmup))
+    t0 = time.perf_counter()
+    run_tokens(ctx, wl, 0, n_issue, y, S.MODE_STMOE)
+    host_us = (time.perf_counter() - t0) * 1e6 / (n_issue * cfg.L)
+    torch.cuda.synchronize()
     ctx.set_timing(TIMING_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -411,7 +418,8 @@ def hbm_resident(wl, steps, warmup):
     stats = pred.stats()
     ctx.close()
     pred.close()
-    return dict(seconds=dt, up_ms=up_ms, down_ms=down_ms, n_calls=n_calls, n_experts=n_exp, stats=stats)
+    return dict(seconds=dt, up_ms=up_ms, down_ms=down_ms, n_calls=n_calls, n_experts=n_exp, stats=stats,
+                host_issue_us_per_layer=host_us)
 
 
 def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
@@ -572,7 +580,8 @@ def main():
     r = hbm_resident(wl, args.steps, args.warmup)
     ms_per_step = 1e3 * r["seconds"] / args.steps
     value = cfg.B * args.steps / r["seconds"]
-    log(f"HBM-resident: {value:.2f} tok/s, {ms_per_step:.3f} ms/token")
+    log(f"HBM-resident: {value:.2f} tok/s, {ms_per_step:.3f} ms/token, "
+        f"host issue {r['host_issue_us_per_layer']:.1f} us/layer")
     esz = cfg.wbytes
     up_bytes = r["n_experts"] * 2 * cfg.H * cfg.I * esz + r["n_calls"] * cfg.n_shared * 2 * cfg.H * cfg.I * esz
     dn_bytes = r["n_experts"] * cfg.H * cfg.I * esz + r["n_calls"] * cfg.n_shared * cfg.H * cfg.I * esz
@@ -596,7 +605,8 @@ def main():
         "data": "synthetic (seeded planted-Markov routing, N(0, 0.02) expert weights)",
         "config": {"workload": cfg.name, "layers": cfg.L, "hidden": cfg.H, "intermediate": cfg.I,
                    "experts": cfg.E, "shared_experts": cfg.n_shared, "top_k": cfg.K, "global_batch": cfg.B,
-                   "mode": "all experts HBM-resident, ST-MoE predictor on", "parallelism": "none (1 GPU)"},
+                   "mode": "all experts HBM-resident, ST-MoE predictor on", "parallelism": "none (1 GPU)",
+                   "launch": "eager launches; predictor update/predict on a side stream beside the FFN"},
         "roofline": {
             "bound": "hbm", "kernel": "ffn_gate_up",
             "achieved": round(up_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
@@ -610,7 +620,11 @@ def main():
         "ffn_down": {"achieved_gbps": round(dn_gbps, 1), "frac": round(dn_gbps / PEAK_HBM_GBPS, 4),
                      "avg_launch_us": round(1e3 * r["down_ms"] / max(r["n_calls"], 1), 3)},
         "ffn_hbm_gbps": round(ffn_gbps, 1),
-        "step_hbm_gbps": round((up_bytes + dn_bytes) / r["seconds"] / 1e9, 1),
+        # expert-weight bytes per token from the event-timed tokens, over the whole timed region
+        "step_hbm_gbps": round((up_bytes + dn_bytes) / max(r["n_calls"] / cfg.L, 1e-9) * args.steps
+                               / r["seconds"] / 1e9, 1),
+        "layer_us": round(1e6 * r["seconds"] / args.steps / cfg.L, 2),
+        "host_issue_us_per_layer": round(r["host_issue_us_per_layer"], 2),
         "prediction": {
             "recall_layers_ge1": round(float(stats[1:, 0].sum() / max(stats[1:, 1].sum(), 1)), 4),
             "recall_layer0": round(float(stats[0, 0] / max(stats[0, 1], 1)), 4),

@@ -286,7 +286,12 @@ int moe_ctx_destroy(moe_ctx* ctx);
 /* One MoE layer for decode token `token`:
  *   x device [B][H] dtype; y device out [B][H] fp32.
  * With a cache, this call waits once on the host for the layer's routing
- * record (selected and predicted experts).  Without one it never waits.
+ * record (selected and predicted experts).  Without one it never waits, and
+ * in the prediction modes the table update and the next layer's prediction
+ * run on a stream of the context's own that waits for the layer's router
+ * and overlaps the FFN (the compute stream waits for that stream once per
+ * token, before selections it still reads are rewritten).  Layers are
+ * expected in order 0..L-1 per token; other orders are correct but wait.
  * Layer-0 predictions come from HT[0]; the prefetch for layer 0 of the next
  * token is issued at layer L-1. */
 int moe_decode_layer(moe_ctx* ctx, int token, int layer, const void* x, float* y, int mode);
@@ -296,8 +301,24 @@ int moe_decode_layer(moe_ctx* ctx, int token, int layer, const void* x, float* y
  * decides which).  Defaults: min_score = 2 (the paper's threshold) and
  * max_per_layer = the cache's slots per layer. */
 int moe_ctx_set_prefetch(moe_ctx* ctx, int min_score, int max_per_layer);
-/* All L layers of one token: xs device [L][B][H], ys device out [L][B][H]. */
+/* All L layers of one token: xs device [L][B][H], ys device out [L][B][H].
+ * With graph replay on (moe_ctx_set_graph), every call after the first whose
+ * token is not event-timed replays one HIP graph of the whole token: xs is
+ * copied into the context's input staging buffer, the graph runs, and the
+ * output staging buffer is copied to ys (a copy is skipped when the pointer
+ * is the staging buffer itself).  The graph is captured at the first such
+ * call and again when `mode` changes; results equal the eager calls. */
 int moe_decode_token(moe_ctx* ctx, int token, const void* xs, float* ys, int mode);
+/* Graph replay of moe_decode_token on (1) or off (0); contexts without a
+ * cache only.  Turning it on allocates the staging buffers (L*B*H elements
+ * of the storage dtype and L*B*H fp32) and an internal stream; the graph
+ * launch is ordered after earlier work on the compute stream and before
+ * later work on it by events.  [sync] */
+int moe_ctx_set_graph(moe_ctx* ctx, int on);
+/* The staging buffers of graph replay (device, owned by the context):
+ * x_stage [L][B][H] storage dtype, y_stage [L][B][H] fp32.  Writing the
+ * inputs there and passing these pointers avoids the two copies. */
+int moe_ctx_graph_buffers(moe_ctx* ctx, void** x_stage, float** y_stage);
 /* Last routing of each layer: host out idx [L][B][K] int32, w [L][B][K] fp32.  [sync] */
 int moe_ctx_last_routing(moe_ctx* ctx, int32_t* idx, float* w);
 /* Event timing of the expert-FFN kernels.  every > 0 starts recording (and

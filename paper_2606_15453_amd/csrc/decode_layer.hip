@@ -4,8 +4,10 @@
 //   -> expert computation (Com.) -> prefetch of the next layer's predicted
 //   experts (EP), overlapping the computation.
 //
-// Without a cache (every routed expert resident in HBM) the layer is a fixed
-// sequence of kernels on the compute stream and never waits on the host.
+// Without a cache (every routed expert resident in HBM) the layer never
+// waits on the host.  Only the router is on the FFN's critical path: the
+// verify/update and the next layer's prediction run on an internal side
+// stream that waits for the layer's selection and overlaps the FFN.
 // With a cache, the host reads one small routing record per layer (the
 // selection and the ranked prediction) because hipMemcpyAsync needs
 // host-known source addresses; that is the layer's only host wait.
@@ -23,6 +25,9 @@ int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int
                         float* w, void* route_ws, stmoe_predictor* p, int layer, const int32_t* sel_prev,
                         int use, int online, int32_t* ranked, int32_t* n_ranked, uint8_t* max_score,
                         hipStream_t s);
+int update_predict(stmoe_predictor* p, int layer, const int32_t* sel_prev, const int32_t* sel_cur,
+                   int use, int online, int32_t* ranked, int32_t* n_ranked, uint8_t* max_score,
+                   hipStream_t s);
 
 namespace {
 
@@ -48,6 +53,12 @@ struct moe_ctx {
     stmoe_predictor* pred = nullptr;
     expert_cache* cache = nullptr;
     hipStream_t s = nullptr;
+    // side stream of the predictor (no cache): ev_sel orders it after the
+    // layer's router; ev_side marks its queued work, which the compute stream
+    // waits for before selections it may still read are overwritten
+    hipStream_t side = nullptr;
+    hipEvent_t ev_sel = nullptr, ev_side = nullptr;
+    bool side_pending = false;
     int32_t* idx = nullptr;                // [L][B][K] device
     float* w = nullptr;                    // [L][B][K] device
     int32_t* ranked = nullptr;             // device: ranked [E], n_ranked [1], max scores [E] (uint8)
@@ -63,6 +74,17 @@ struct moe_ctx {
     std::vector<const void*> host_table;   // [E] scratch for the cache's answers
     bool started = false;
     int last_token = -1, last_layer = -1;
+    // one HIP graph per token (resident contexts): the whole layer sequence,
+    // side branch included, replays with one launch on the graph stream;
+    // inputs and outputs pass through the staging buffers
+    bool graph_on = false;
+    int graph_mode = -1;
+    hipStream_t gs = nullptr;
+    hipEvent_t ev_in = nullptr, ev_out = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t graph_exec = nullptr;
+    void* x_stage = nullptr;               // [L][B][H] dtype
+    float* y_stage = nullptr;              // [L][B][H] fp32
     // FFN timing: events around the FFN of every `timing_every`-th token (0: off)
     int timing_every = 0;
     std::vector<hipEvent_t> ev_pool;
@@ -80,6 +102,22 @@ uint8_t* max_scores(int32_t* ranked, int E) { return reinterpret_cast<uint8_t*>(
 void free_ctx(moe_ctx* c) {
     if (!c) return;
     if (c->s) (void)hipStreamSynchronize(c->s);
+    if (c->side) {
+        (void)hipStreamSynchronize(c->side);
+        (void)hipStreamDestroy(c->side);
+    }
+    if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
+    if (c->ev_side) (void)hipEventDestroy(c->ev_side);
+    if (c->gs) {
+        (void)hipStreamSynchronize(c->gs);
+        (void)hipStreamDestroy(c->gs);
+    }
+    if (c->graph_exec) (void)hipGraphExecDestroy(c->graph_exec);
+    if (c->graph) (void)hipGraphDestroy(c->graph);
+    if (c->ev_in) (void)hipEventDestroy(c->ev_in);
+    if (c->ev_out) (void)hipEventDestroy(c->ev_out);
+    (void)hipFree(c->x_stage);
+    (void)hipFree(c->y_stage);
     (void)hipFree(c->idx);
     (void)hipFree(c->w);
     (void)hipFree(c->ranked);
@@ -186,6 +224,11 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     if (e == hipSuccess) e = hipMalloc(&c->n_experts, sizeof(unsigned long long));
     if (e == hipSuccess) e = hipHostMalloc(&c->rec, size_t(c->B * c->K) * sizeof(int32_t) + ranked_bytes(c->E));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->rec_ev, hipEventDisableTiming);
+    if (e == hipSuccess && !cache && pred) {
+        e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_side, hipEventDisableTiming);
+    }
     if (e == hipSuccess) e = hipMemset(c->route_ws, 0, c->route_ws_bytes);
     if (e == hipSuccess) e = hipMemset(c->ffn_ws, 0, c->ffn_ws_bytes);
     if (e == hipSuccess) e = hipMemset(c->idx, 0, LBK * sizeof(int32_t));
@@ -212,12 +255,13 @@ extern "C" int moe_ctx_destroy(moe_ctx* c) {
     return STMOE_OK;
 }
 
-extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int mode) {
-    clear_error();
-    STMOE_CHECK(c && x && y, "null pointer");
-    STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
-    STMOE_CHECK(token >= 0, "token must be >= 0");
-    STMOE_CHECK(mode >= MOE_MODE_ON_DEMAND && mode <= MOE_MODE_CCT_ONLY, "bad mode");
+namespace {
+
+bool timed_token(const moe_ctx* c, int token) { return c->timing_every > 0 && token % c->timing_every == 0; }
+
+// One layer; `timing` permits the FFN events of timed tokens (off while a
+// graph is captured).  Arguments are checked by the callers.
+int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int mode, bool timing) {
     const int use = use_bits(mode);
     STMOE_CHECK(use == 0 || c->pred, "prediction modes need a predictor");
     const int L = c->L, B = c->B, K = c->K, E = c->E;
@@ -239,9 +283,29 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
         }
     }
 
-    // R + V + P: gating, verify/update against the previous layer and the
-    // next layer's prediction, fused into one launch
-    if (use) {
+    // R + V + P.  Without a cache: the router on the compute stream, then
+    // verify/update and prediction on the side stream, off the FFN's path.
+    // Side work still queued reads selections of this token's layers and the
+    // next one's; in the usual layer order it can only collide with this
+    // call from layer 0 on, so the compute stream waits for it once per token.
+    const bool in_order = layer == (c->last_layer + 1) % L;
+    if (c->side_pending && (layer == 0 || !in_order || !(use && c->side))) {
+        STMOE_HIP(hipEventRecord(c->ev_side, c->side));
+        STMOE_HIP(hipStreamWaitEvent(c->s, c->ev_side, 0));
+        c->side_pending = false;
+    }
+    if (use && c->side) {
+        if (int rc = moe_route_topk(x, c->router[layer], B, c->H, E, K, c->dtype, c->renorm, idx_l, w_l,
+                                    nullptr, c->route_ws, c->route_ws_bytes, c->s))
+            return rc;
+        STMOE_HIP(hipEventRecord(c->ev_sel, c->s));
+        STMOE_HIP(hipStreamWaitEvent(c->side, c->ev_sel, 0));
+        const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
+        if (int rc = update_predict(c->pred, layer, prev, idx_l, use, 1, nullptr, nullptr, nullptr, c->side))
+            return rc;
+        c->side_pending = true;
+    } else if (use) {
+        // with a cache the host reads the prediction: one fused launch pair
         const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
         if (int rc = fused_route_predict(x, c->router[layer], c->H, c->dtype, c->renorm, idx_l, w_l,
                                          c->route_ws, c->pred, layer, prev, use, 1, c->ranked,
@@ -275,7 +339,7 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
     }
     // Com.: expert FFN (timed with events before, between and after its two kernels)
     hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
-    const bool timed = c->timing_every > 0 && token % c->timing_every == 0;
+    const bool timed = timing && timed_token(c, token);
     if (timed) {
         e0 = next_event(c);
         e1 = next_event(c);
@@ -303,6 +367,120 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
     return STMOE_OK;
 }
 
+// The compute stream waits for side work still queued (it reads selections
+// that the next work rewrites).
+int join_side(moe_ctx* c) {
+    if (!c->side_pending) return STMOE_OK;
+    STMOE_HIP(hipEventRecord(c->ev_side, c->side));
+    STMOE_HIP(hipStreamWaitEvent(c->s, c->ev_side, 0));
+    c->side_pending = false;
+    return STMOE_OK;
+}
+
+// Capture all L layers of one token, reading x_stage and writing y_stage,
+// into c->graph_exec.  The capture runs on the graph stream (the compute
+// stream may be the null stream, which cannot be captured).
+int capture_token(moe_ctx* c, int token, int mode) {
+    if (c->graph_exec) (void)hipGraphExecDestroy(c->graph_exec);
+    if (c->graph) (void)hipGraphDestroy(c->graph);
+    c->graph_exec = nullptr;
+    c->graph = nullptr;
+    hipStream_t user = c->s;
+    c->s = c->gs;
+    STMOE_HIP(hipStreamBeginCapture(c->gs, hipStreamCaptureModeThreadLocal));
+    int rc = STMOE_OK;
+    for (int l = 0; l < c->L && rc == STMOE_OK; ++l) {
+        const char* x = reinterpret_cast<const char*>(c->x_stage) + size_t(l) * c->B * c->H * c->esz;
+        rc = decode_layer(c, token, l, x, c->y_stage + size_t(l) * c->B * c->H, mode, false);
+    }
+    if (rc == STMOE_OK) rc = join_side(c);      // the side branch rejoins inside the graph
+    hipGraph_t g = nullptr;
+    const hipError_t e = hipStreamEndCapture(c->gs, &g);
+    c->s = user;
+    c->side_pending = false;
+    if (rc != STMOE_OK || e != hipSuccess) {
+        if (g) (void)hipGraphDestroy(g);
+        if (rc == STMOE_OK) set_error(std::string("moe_decode_token: capture: ") + hipGetErrorString(e));
+        return rc != STMOE_OK ? rc : STMOE_EHIP;
+    }
+    const hipError_t ei = hipGraphInstantiate(&c->graph_exec, g, nullptr, nullptr, 0);
+    if (ei != hipSuccess) {
+        (void)hipGraphDestroy(g);
+        c->graph_exec = nullptr;
+        set_error(std::string("moe_decode_token: instantiate: ") + hipGetErrorString(ei));
+        return STMOE_EHIP;
+    }
+    c->graph = g;
+    c->graph_mode = mode;
+    return STMOE_OK;
+}
+
+int decode_token_graph(moe_ctx* c, int token, const void* xs, float* ys, int mode) {
+    if (int rc = join_side(c)) return rc;
+    if (!c->graph_exec || c->graph_mode != mode)
+        if (int rc = capture_token(c, token, mode)) return rc;
+    const size_t n = size_t(c->L) * c->B * c->H;
+    STMOE_HIP(hipEventRecord(c->ev_in, c->s));
+    STMOE_HIP(hipStreamWaitEvent(c->gs, c->ev_in, 0));
+    if (xs != c->x_stage)
+        STMOE_HIP(hipMemcpyAsync(c->x_stage, xs, n * c->esz, hipMemcpyDeviceToDevice, c->gs));
+    STMOE_HIP(hipGraphLaunch(c->graph_exec, c->gs));
+    if (ys != c->y_stage)
+        STMOE_HIP(hipMemcpyAsync(ys, c->y_stage, n * sizeof(float), hipMemcpyDeviceToDevice, c->gs));
+    STMOE_HIP(hipEventRecord(c->ev_out, c->gs));
+    STMOE_HIP(hipStreamWaitEvent(c->s, c->ev_out, 0));
+    c->last_token = token;
+    c->last_layer = c->L - 1;
+    return STMOE_OK;
+}
+
+}  // namespace
+
+extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int mode) {
+    clear_error();
+    STMOE_CHECK(c && x && y, "null pointer");
+    STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
+    STMOE_CHECK(token >= 0, "token must be >= 0");
+    STMOE_CHECK(mode >= MOE_MODE_ON_DEMAND && mode <= MOE_MODE_CCT_ONLY, "bad mode");
+    return decode_layer(c, token, layer, x, y, mode, true);
+}
+
+extern "C" int moe_ctx_set_graph(moe_ctx* c, int on) {
+    clear_error();
+    STMOE_CHECK(c, "null ctx");
+    STMOE_CHECK(!on || !c->cache, "graph replay needs a context without a cache");
+    STMOE_HIP(hipStreamSynchronize(c->s));
+    if (c->gs) STMOE_HIP(hipStreamSynchronize(c->gs));
+    if (c->graph_exec) (void)hipGraphExecDestroy(c->graph_exec);
+    if (c->graph) (void)hipGraphDestroy(c->graph);
+    c->graph_exec = nullptr;
+    c->graph = nullptr;
+    c->graph_mode = -1;
+    if (on && !c->gs) {
+        const size_t n = size_t(c->L) * c->B * c->H;
+        hipError_t e = hipStreamCreateWithFlags(&c->gs, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_in, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_out, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipMalloc(&c->x_stage, n * c->esz);
+        if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&c->y_stage), n * sizeof(float));
+        if (e != hipSuccess) {
+            set_error(std::string("moe_ctx_set_graph: ") + hipGetErrorString(e));
+            return e == hipErrorOutOfMemory ? STMOE_ENOMEM : STMOE_EHIP;
+        }
+    }
+    c->graph_on = on != 0;
+    return STMOE_OK;
+}
+
+extern "C" int moe_ctx_graph_buffers(moe_ctx* c, void** x_stage, float** y_stage) {
+    clear_error();
+    STMOE_CHECK(c && x_stage && y_stage, "null pointer");
+    STMOE_CHECK(c->graph_on, "graph replay is off");
+    *x_stage = c->x_stage;
+    *y_stage = c->y_stage;
+    return STMOE_OK;
+}
+
 extern "C" int moe_ctx_set_prefetch(moe_ctx* c, int min_score, int max_per_layer) {
     clear_error();
     STMOE_CHECK(c, "null ctx");
@@ -315,9 +493,14 @@ extern "C" int moe_ctx_set_prefetch(moe_ctx* c, int min_score, int max_per_layer
 extern "C" int moe_decode_token(moe_ctx* c, int token, const void* xs, float* ys, int mode) {
     clear_error();
     STMOE_CHECK(c && xs && ys, "null pointer");
+    STMOE_CHECK(token >= 0, "token must be >= 0");
+    STMOE_CHECK(mode >= MOE_MODE_ON_DEMAND && mode <= MOE_MODE_CCT_ONLY, "bad mode");
+    // graph replay once the first call has run (it seeds layer 0's
+    // prediction); event-timed tokens run eagerly
+    if (c->graph_on && c->started && !timed_token(c, token)) return decode_token_graph(c, token, xs, ys, mode);
     for (int l = 0; l < c->L; ++l) {
         const char* x = reinterpret_cast<const char*>(xs) + size_t(l) * c->B * c->H * c->esz;
-        if (int rc = moe_decode_layer(c, token, l, x, ys + size_t(l) * c->B * c->H, mode)) return rc;
+        if (int rc = decode_layer(c, token, l, x, ys + size_t(l) * c->B * c->H, mode, true)) return rc;
     }
     return STMOE_OK;
 }

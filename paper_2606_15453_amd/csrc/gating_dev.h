@@ -74,41 +74,53 @@ __device__ void expert_logits(const RouteArgs& a, float (*part)[kThreads / 64]) 
 }
 
 // Softmax and top-K of every batch row in one workgroup, from the logits z
-// ([B][E], global or LDS).  Each thread takes (row, expert) pairs and counts
-// the experts of its row that beat its own (larger key, or equal key and
+// ([B][E], global or LDS).  For each (row, expert) pair, T lanes split the
+// row and count the experts that beat it (larger key, or equal key and
 // lower index): a count below K is its output position, so the selection
 // comes out ordered (logit desc, index asc) with no serial rounds.  The row
 // max is the winner at position 0; one wave per row then forms the softmax
 // sum and the K weights.  Writes idx/w (and the selection to s_idx in LDS
 // when given) and ends with a barrier.
 __device__ void softmax_topk_tail(const RouteArgs& a, const float* z, int32_t* s_idx) {
-    constexpr int kRow = kMaxE;                   // LDS row stride of the keys
+    constexpr int kRow = kMaxE;                   // LDS row stride
     __shared__ __align__(16) uint32_t keys[kMaxB * kRow];
+    __shared__ float zl[kMaxB * kRow];
     __shared__ int32_t win[kMaxB * kMaxK];
     __shared__ float rowmax[kMaxB];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int K = a.K, E = a.E, BE = a.B * a.E;
-    for (int i = tid; i < BE; i += kThreads) {
-        const int b = i / E, f = i - b * E;
-        keys[b * kRow + f] = order_key(z[i]);
+    const int E4 = (E + 3) & ~3;
+    // keys padded with 0 up to a multiple of 4: a pad never beats a real key
+    // and never ties with a lower index
+    for (int i = tid; i < a.B * E4; i += kThreads) {
+        const int b = i / E4, f = i - b * E4;
+        const float v = f < E ? z[b * E + f] : 0.f;
+        keys[b * kRow + f] = f < E ? order_key(v) : 0u;
+        zl[b * kRow + f] = v;
     }
     __syncthreads();
-    for (int i = tid; i < BE; i += kThreads) {
+    int T = 1;                                    // lanes per pair (power of two)
+    while (T < 16 && BE * T * 2 <= kThreads) T *= 2;
+    const int n4 = E4 / 4;
+    for (int base = 0; base < BE * T; base += kThreads) {
+        const int t = base + tid, i = t / T, part = t & (T - 1);
         const int b = i / E, f = i - b * E;
-        const uint32_t* row = keys + b * kRow;
-        const uint32_t mine = row[f];
         int cnt = 0;
-        int g = 0;
-        for (; g + 4 <= E; g += 4) {
-            const uint4 k4 = *reinterpret_cast<const uint4*>(row + g);
-            cnt += (k4.x > mine) + (k4.y > mine) + (k4.z > mine) + (k4.w > mine);
-            cnt += (k4.x == mine && g < f) + (k4.y == mine && g + 1 < f) + (k4.z == mine && g + 2 < f) +
-                   (k4.w == mine && g + 3 < f);
+        if (i < BE) {
+            const uint32_t* row = keys + b * kRow;
+            const uint32_t mine = row[f];
+            for (int c = part; c < n4; c += T) {
+                const uint4 k = *reinterpret_cast<const uint4*>(row + 4 * c);
+                const int g = 4 * c;
+                cnt += (k.x > mine) + (k.y > mine) + (k.z > mine) + (k.w > mine);
+                cnt += (k.x == mine && g < f) + (k.y == mine && g + 1 < f) + (k.z == mine && g + 2 < f) +
+                       (k.w == mine && g + 3 < f);
+            }
         }
-        for (; g < E; ++g) cnt += row[g] > mine || (row[g] == mine && g < f);
-        if (cnt < K) {
+        for (int o = 1; o < T; o <<= 1) cnt += __shfl_xor(cnt, o, 64);
+        if (i < BE && part == 0 && cnt < K) {
             win[b * K + cnt] = f;
-            if (cnt == 0) rowmax[b] = z[i];
+            if (cnt == 0) rowmax[b] = zl[b * kRow + f];
         }
     }
     __syncthreads();
@@ -116,13 +128,13 @@ __device__ void softmax_topk_tail(const RouteArgs& a, const float* z, int32_t* s
         // softmax sum (NaN-free inputs assumed for the weights)
         const float m = rowmax[b];
         float s = 0.f;
-        for (int f = lane; f < E; f += 64) s += expf(z[b * E + f] - m);
+        for (int f = lane; f < E; f += 64) s += expf(zl[b * kRow + f] - m);
         s = wave_sum(s);
         float p = 0.f;
         int e = 0;
         if (lane < K) {
             e = win[b * K + lane];
-            p = expf(z[b * E + e] - m) / s;
+            p = expf(zl[b * kRow + e] - m) / s;
         }
         const float wsum = wave_sum(p);
         if (lane < K) {

@@ -107,6 +107,25 @@ __global__ __launch_bounds__(kThreads) void route_update_predict_kernel(gating::
     predict_body(p, sh);
 }
 
+// The decode path's verify/update and next-layer prediction without the
+// router (the selection is read from global memory): used where the router
+// runs as its own launches and this work overlaps the expert FFN.
+__global__ __launch_bounds__(kThreads) void update_predict_kernel(UpdateArgs u, PredictArgs p) {
+    __shared__ TableShared sh;
+    Seg g[kMaxSegs];
+    p.sel_cur = nullptr;     // the update's copy of the selection serves both
+    int n = 0;
+    n += update_segs(u, sh, g + n);
+    n += predict_segs(p, sh, g + n);
+    stage(g, n);
+    update_body(u, sh);
+    // with one layer the prediction reads the HT row the update just wrote
+    if (p.ht_next && p.ht_next == u.ht)
+        for (int i = threadIdx.x; i < u.B * u.K; i += kThreads) sh.htn[i] = sh.htnew[i];
+    __syncthreads();
+    predict_body(p, sh);
+}
+
 int check_sel_host(const int32_t* sel, size_t rows, int E, int K) {
     for (size_t r = 0; r < rows; ++r) {
         const int32_t* row = sel + r * K;
@@ -331,3 +350,25 @@ extern "C" int stmoe_stats(stmoe_predictor* p, int64_t* out) {
     STMOE_HIP(hipMemcpy(out, p->stats, size_t(p->L) * 3 * sizeof(int64_t), hipMemcpyDeviceToHost));
     return STMOE_OK;
 }
+
+namespace stmoe {
+// Internal: verify/update at `layer` from the selection sel_cur (device
+// [B][K]) + prediction of the next layer, one launch on `s`.  The caller has
+// validated the shapes.
+int update_predict(stmoe_predictor* p, int layer, const int32_t* sel_prev, const int32_t* sel_cur,
+                   int use, int online, int32_t* ranked, int32_t* n_ranked, uint8_t* max_score,
+                   hipStream_t s) {
+    if (!p->profiled) {
+        set_error("moe_decode_layer: predictor has not been profiled");
+        return STMOE_ESTATE;
+    }
+    const UpdateArgs u = update_args(p, layer, sel_prev, sel_cur, online);
+    const PredictArgs q = layer + 1 < p->L
+                              ? predict_args(p, layer, sel_cur, use, nullptr, nullptr, max_score, ranked, n_ranked)
+                              : predict_args(p, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr, max_score,
+                                             ranked, n_ranked);
+    hipLaunchKernelGGL(update_predict_kernel, dim3(1), dim3(kThreads), 0, s, u, q);
+    STMOE_LAUNCHED();
+    return STMOE_OK;
+}
+}  // namespace stmoe

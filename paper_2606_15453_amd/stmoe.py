@@ -100,6 +100,8 @@ _SIGS = {
     "moe_ctx_set_prefetch": (i32, [vp, i32, i32]),
     "moe_ctx_last_routing": (i32, [vp, vp, vp]),
     "moe_ctx_set_timing": (i32, [vp, i32]),
+    "moe_ctx_set_graph": (i32, [vp, i32]),
+    "moe_ctx_graph_buffers": (i32, [vp, P(vp), P(vp)]),
     "moe_ctx_timing": (i32, [vp, P(C.c_double), P(C.c_double), P(i64), P(i64)]),
     "stmoe_calib_copy": (i32, [vp, vp, sz, vp]),
     "stmoe_calib_read_out_words": (sz, [sz]),
@@ -407,6 +409,16 @@ class DecodeContext:
     def set_timing(self, every):
         """Time the FFN of every `every`-th token (0 stops; True means every token)."""
         _call("moe_ctx_set_timing", self.h, int(every))
+
+    def set_graph(self, on=True):
+        """Replay each token (after the first) as one HIP graph; no-cache contexts only."""
+        _call("moe_ctx_set_graph", self.h, int(bool(on)))
+
+    def graph_buffers(self):
+        """(x_stage, y_stage) device addresses of the graph's staging buffers."""
+        x, y = vp(), vp()
+        _call("moe_ctx_graph_buffers", self.h, C.byref(x), C.byref(y))
+        return x.value, y.value
 
     def timing(self):
         """(gate/up kernel ms, down kernel ms, FFN calls, distinct routed experts) since set_timing(1)."""

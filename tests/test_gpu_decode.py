@@ -122,6 +122,27 @@ def test_decode_resident_matches_oracle(name, over):
     assert np.array_equal(stats[:, 2], ref["npred"].sum(axis=0))
 
 
+@pytest.mark.parametrize("name,over,mode", [("tiny", dict(T=8), 2), ("tiny", dict(T=8), 3),
+                                             ("tiny", dict(L=1, T=6, P=2), 1),
+                                             ("qwen30b", dict(L=3, T=4, P=2, C=10), 3)])
+def test_decode_resident_ablations(name, over, mode):
+    """HT-only, CCT-only and a one-layer model on the resident path, where
+    the table update and prediction run beside the FFN: hit counts as in
+    the oracle."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    ref = _oracle(st, mode)
+    idx_hist, _, stats, _ = _run_gpu(st, mode, capped=False)
+    for t in range(cfg.T):
+        for l in range(cfg.L):
+            r = ref["idx"][t * cfg.L + l]
+            for b in range(cfg.B):
+                assert sorted(idx_hist[t][l][b].tolist()) == sorted(r[b].tolist())
+    assert np.array_equal(stats[:, 0], ref["hits"].sum(axis=0))
+    assert np.array_equal(stats[:, 2], ref["npred"].sum(axis=0))
+
+
 @pytest.mark.parametrize("name,over", CFGS)
 @pytest.mark.parametrize("mode", [0, 1, 2, 3])
 def test_decode_capped_counts_and_invariance(name, over, mode):
@@ -139,3 +160,60 @@ def test_decode_capped_counts_and_invariance(name, over, mode):
     n = ref["cache"].n
     assert cst == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
                        useful=n.useful, wasted=n.wasted)
+
+
+
+def _run_graph(st, mode, timing_every=0, staged=False):
+    """Resident run with graph replay and no host sync between tokens.  With
+    `staged`, inputs are written straight into the context's staging buffer
+    and outputs read from its twin (no copies inside the call)."""
+    import torch
+    from gpuhelp import DEV, storage_dtype
+    from paper_2606_15453_amd import stmoe as S
+    cfg = st.cfg
+    pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+    pred.profile(st.prof)
+    resident = [st.blobs[l][e].data_ptr() for l in range(cfg.L) for e in range(cfg.E)]
+    stream = torch.cuda.current_stream()
+    ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
+                          [g.data_ptr() for g in st.wg_dev], predictor=pred, resident_ptrs=resident,
+                          shared_ptrs=st.shared_ptrs(), n_shared=cfg.n_shared, stream=stream)
+    ctx.set_graph(True)
+    if timing_every:
+        ctx.set_timing(timing_every)
+    ys = [torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device=DEV) for _ in range(cfg.T)]
+    xp, yp = ctx.graph_buffers()
+    for t in range(cfg.T):
+        if staged:
+            x = st.x_dev[t].contiguous()
+            S.calib_copy(x.data_ptr(), xp, x.numel() * x.element_size(), stream.cuda_stream)
+            ctx.token(t, xp, yp, mode=mode)
+            S.calib_copy(yp, ys[t].data_ptr(), ys[t].numel() * 4, stream.cuda_stream)
+        else:
+            ctx.token(t, st.x_dev[t], ys[t], mode=mode)
+    torch.cuda.synchronize()
+    idx_last, _ = ctx.last_routing()
+    out = [y.cpu().numpy() for y in ys]
+    stats = pred.stats()
+    ctx.close()
+    pred.close()
+    return idx_last, out, stats
+
+
+@pytest.mark.parametrize("name,over,timing,staged", [("tiny", dict(T=12), 0, False),
+                                                    ("qwen30b", dict(L=4, T=8, P=3), 3, False),
+                                                    ("qwen30b-b8", dict(L=3, T=5, P=2), 2, True),
+                                                    ("dsv2lite", dict(L=3, T=5, P=2), 0, True)])
+def test_decode_graph_replay_matches_eager(name, over, timing, staged):
+    """Each token replayed as one HIP graph (event-timed tokens eager, the
+    first token eager) gives bit-identical outputs, the same final routing and
+    the same predictor hit counts as eager calls, over repeated replays."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    idx_hist, ys_eager, stats_eager, _ = _run_gpu(st, 1, capped=False)
+    idx_last, ys_graph, stats_graph = _run_graph(st, 1, timing_every=timing, staged=staged)
+    for t in range(cfg.T):
+        assert np.array_equal(ys_graph[t], ys_eager[t]), t
+    assert np.array_equal(idx_last, idx_hist[-1])
+    assert np.array_equal(stats_graph, stats_eager)

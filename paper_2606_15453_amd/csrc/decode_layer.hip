@@ -20,7 +20,9 @@
 namespace stmoe {
 int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, int H, int I, int E,
                int dtype, const void* const* eptr, const void* const* sptr, int n_shared,
-               float* y, void* ws, hipStream_t s, unsigned long long* n_experts, hipEvent_t ev_mid);
+               float* y, void* ws, hipStream_t s, unsigned long long* n_experts, hipEvent_t ev_mid,
+               const float* logits, int renorm);
+int route_logits(const void* x, const void* w_gate, int B, int H, int E, int dtype, float* z, hipStream_t s);
 int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int renorm, int32_t* idx,
                         float* w, void* route_ws, stmoe_predictor* p, int layer, const int32_t* sel_prev,
                         int use, int online, int32_t* ranked, int32_t* n_ranked, uint8_t* max_score,
@@ -283,8 +285,10 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         }
     }
 
-    // R + V + P.  Without a cache: the router on the compute stream, then
-    // verify/update and prediction on the side stream, off the FFN's path.
+    // R + V + P.  Without a cache: the router on the compute stream (for
+    // B*E <= 256 only its logits: the FFN's gate/up kernel does softmax and
+    // top-K), then verify/update and prediction on the side stream, off the
+    // FFN's path.
     // Side work still queued reads selections of this token's layers and the
     // next one's; in the usual layer order it can only collide with this
     // call from layer 0 on, so the compute stream waits for it once per token.
@@ -294,7 +298,11 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         STMOE_HIP(hipStreamWaitEvent(c->s, c->ev_side, 0));
         c->side_pending = false;
     }
-    if (use && c->side) {
+    const bool route_in_ffn = !c->cache && B * E <= kRouteInFfnMax;
+    float* zbuf = reinterpret_cast<float*>(c->route_ws);
+    if (route_in_ffn) {
+        if (int rc = route_logits(x, c->router[layer], B, c->H, E, c->dtype, zbuf, c->s)) return rc;
+    } else if (use && c->side) {
         if (int rc = moe_route_topk(x, c->router[layer], B, c->H, E, K, c->dtype, c->renorm, idx_l, w_l,
                                     nullptr, c->route_ws, c->route_ws_bytes, c->s))
             return rc;
@@ -349,11 +357,21 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
     }
     if (int rc = ffn_launch(x, idx_l, w_l, B, K, c->H, c->I, E, c->dtype, c->tables + size_t(layer) * E,
                             c->n_shared ? c->shared + size_t(layer) * c->n_shared : nullptr, c->n_shared,
-                            y, c->ffn_ws, c->s, timed ? c->n_experts : nullptr, e1))
+                            y, c->ffn_ws, c->s, timed ? c->n_experts : nullptr, e1,
+                            route_in_ffn ? zbuf : nullptr, c->renorm))
         return rc;
     if (timed) {
         STMOE_HIP(hipEventRecord(e2, c->s));
         ++c->n_calls;
+    }
+    if (route_in_ffn && use && c->side) {
+        // the selection exists once the FFN has run
+        STMOE_HIP(hipEventRecord(c->ev_sel, c->s));
+        STMOE_HIP(hipStreamWaitEvent(c->side, c->ev_sel, 0));
+        const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
+        if (int rc = update_predict(c->pred, layer, prev, idx_l, use, 1, nullptr, nullptr, nullptr, c->side))
+            return rc;
+        c->side_pending = true;
     }
     // EP: prefetch the next layer's predicted experts, overlapping the FFN
     if (c->cache) {

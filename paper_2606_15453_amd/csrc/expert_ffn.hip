@@ -33,6 +33,7 @@
 // token masks) from topk_idx/topk_w in LDS: no host round trip, no planning
 // launch.
 #include "common.h"
+#include "gating_dev.h"
 
 namespace stmoe {
 namespace {
@@ -59,6 +60,11 @@ struct FfnArgs {
     float* y;                        // [B][H]
     unsigned long long* n_experts;   // optional: += distinct routed experts (block 0)
     int ng, spg;                     // expert-slot groups of the down phase, slots per group
+    // optional routing prologue of the gate/up kernels: softmax + top-K of
+    // these router logits [B][E] (B*E <= kRouteInFfnMax); block 0 writes the
+    // selection to idx/w for the down kernel and the caller
+    const float* logits;
+    int renorm;
 };
 
 struct Plan {
@@ -70,15 +76,49 @@ struct Plan {
     int n_routed, n_slots;
 };
 
+// Gating (Section 2) inside a gate/up workgroup: the same steps and
+// arithmetic as the router tail, on rows of E rounded up to 4, into the
+// plan's idx/w; block 0 also publishes them.
+__device__ void route_into_plan(const FfnArgs& a, Plan& p) {
+    constexpr int kRouteRows = kRouteInFfnMax + 3 * kMaxB;
+    __shared__ __align__(16) uint32_t keys[kRouteRows];
+    __shared__ float zl[kRouteRows];
+    __shared__ int32_t win[kMaxB * kMaxK];
+    __shared__ float rowmax[kMaxB];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int row = (a.E + 3) & ~3;
+    gating::stage_keys(a.logits, a.B, a.E, row, keys, zl);
+    gating::rank_winners(keys, zl, a.B, a.E, a.K, row, win, rowmax);
+    for (int b = wave; b < a.B; b += kWaves) {
+        int e;
+        float wt;
+        gating::row_weights(zl, win, rowmax, b, a.E, a.K, row, a.renorm, e, wt);
+        if (lane < a.K) {
+            p.idx[b * a.K + lane] = e;
+            p.w[b * a.K + lane] = wt;
+            if (blockIdx.x == 0) {
+                const_cast<int32_t*>(a.idx)[b * a.K + lane] = e;
+                const_cast<float*>(a.w)[b * a.K + lane] = wt;
+            }
+        }
+    }
+}
+
 // Build the slot plan in LDS (all threads participate; ends with a barrier).
-// Slot order: selected routed experts ascending, then shared experts.
-__device__ void build_plan(const FfnArgs& a, Plan& p) {
+// Slot order: selected routed experts ascending, then shared experts.  With
+// `route` and router logits in the arguments the selection is computed here
+// (gate/up kernels); otherwise it is read from idx/w.
+__device__ void build_plan(const FfnArgs& a, Plan& p, bool route = false) {
     const int tid = threadIdx.x;
     const int BK = a.B * a.K;
-    for (int t = tid; t < BK; t += kThreads) {
-        const int e = a.idx[t];
-        p.idx[t] = (e >= 0 && e < a.E) ? e : -1;   // out-of-range entries are ignored
-        p.w[t] = a.w[t];
+    if (route && a.logits) {
+        route_into_plan(a, p);
+    } else {
+        for (int t = tid; t < BK; t += kThreads) {
+            const int e = a.idx[t];
+            p.idx[t] = (e >= 0 && e < a.E) ? e : -1;   // out-of-range entries are ignored
+            p.w[t] = a.w[t];
+        }
     }
     if (tid < kMaxE / 32) p.sel[tid] = 0u;
     for (int s = tid; s < kMaxSlots; s += kThreads) p.tok[s] = 0u;
@@ -192,7 +232,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 template <bool BF, int G, int R, int NB>
 __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_per_slot) {
     __shared__ Plan p;
-    build_plan(a, p);
+    build_plan(a, p, true);
     const int j = blockIdx.x / blocks_per_slot;
     if (j >= p.n_slots) return;
     const int rows_per_block = kWaves * (64 / G) * R;
@@ -274,7 +314,7 @@ template <bool BF, int R, int NB>
 __global__ __launch_bounds__(kThreads) void ffn_gate_up_wg(FfnArgs a, int blocks_per_slot) {
     __shared__ Plan p;
     __shared__ float red[kWaves][2][R][NB];
-    build_plan(a, p);
+    build_plan(a, p, true);
     const int j = blockIdx.x / blocks_per_slot;
     if (j >= p.n_slots) return;
     const int i0 = (blockIdx.x % blocks_per_slot) * R;
@@ -523,7 +563,7 @@ __global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
 template <int NT>
 __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int blocks_per_slot) {
     __shared__ Plan p;
-    build_plan(a, p);
+    build_plan(a, p, true);
     const int j = blockIdx.x / blocks_per_slot;
     if (j >= p.n_slots) return;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -614,7 +654,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int bloc
 __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma_sk(FfnArgs a, int blocks_per_slot) {
     __shared__ Plan p;
     __shared__ float red[kWaves][2][64][4];
-    build_plan(a, p);
+    build_plan(a, p, true);
     const int j = blockIdx.x / blocks_per_slot;
     if (j >= p.n_slots) return;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -958,9 +998,16 @@ size_t ffn_workspace_bytes(int B, int K, int E, int H, int I, int n_shared, int 
 }
 
 // Internal entry used by the decode-layer orchestration (no argument checks).
+// With `logits` (B*E <= kRouteInFfnMax) the gate/up kernel routes first and
+// idx/w are outputs, written before the down kernel reads them.
 int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, int H, int I, int E,
                int dtype, const void* const* eptr, const void* const* sptr, int n_shared,
-               float* y, void* ws, hipStream_t st, unsigned long long* n_experts, hipEvent_t ev_mid) {
+               float* y, void* ws, hipStream_t st, unsigned long long* n_experts, hipEvent_t ev_mid,
+               const float* logits, int renorm) {
+    if (logits && B * E > kRouteInFfnMax) {
+        set_error("ffn_launch: routing inside the FFN needs B*E <= 256");
+        return STMOE_EINVAL;
+    }
     const Shape s = plan_shape(B, K, H, I, E, n_shared, dtype);
     const WsLayout L = ws_layout(B, H, I, s);
     char* base = reinterpret_cast<char*>(ws);
@@ -982,6 +1029,8 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
     a.n_experts = n_experts;
     a.ng = s.ng;
     a.spg = s.spg;
+    a.logits = logits;
+    a.renorm = renorm;
     if (s.mfma) return launch_mfma(a, s, st, ev_mid);
     return dtype == STMOE_BF16 ? launch_gemv_b<true>(a, s, st, ev_mid)
                                : launch_gemv_b<false>(a, s, st, ev_mid);
@@ -1017,5 +1066,5 @@ extern "C" int moe_expert_ffn(const void* x, const int32_t* topk_idx, const floa
     STMOE_CHECK((reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(ws) & 255) == 0,
                 "x must be 16-byte and ws 256-byte aligned");
     return ffn_launch(x, topk_idx, topk_w, B, K, H, I, E, dtype, expert_ptrs, shared_ptrs, n_shared, y,
-                      ws, as_stream(stream), nullptr, nullptr);
+                      ws, as_stream(stream), nullptr, nullptr, nullptr, 0);
 }

@@ -73,74 +73,121 @@ __device__ void expert_logits(const RouteArgs& a, float (*part)[kThreads / 64]) 
     }
 }
 
-// Softmax and top-K of every batch row in one workgroup, from the logits z
-// ([B][E], global or LDS).  For each (row, expert) pair, T lanes split the
-// row and count the experts that beat it (larger key, or equal key and
-// lower index): a count below K is its output position, so the selection
-// comes out ordered (logit desc, index asc) with no serial rounds.  The row
-// max is the winner at position 0; one wave per row then forms the softmax
-// sum and the K weights.  Writes idx/w (and the selection to s_idx in LDS
-// when given) and ends with a barrier.
+// Softmax and top-K of every batch row in one workgroup, in three steps
+// that share LDS buffers passed by the caller (rows of `row` >= E rounded up
+// to 4 entries):
+//   stage_keys   logits -> order keys and values in LDS
+//   rank_winners for each (row, expert) pair, T lanes split the row and count
+//                the experts that beat it (larger key, or equal key and lower
+//                index): a count below K is its output position, so the
+//                selection comes out ordered (logit desc, index asc) with no
+//                serial rounds; the winner at position 0 gives the row max
+//   row_weights  one wave per row: softmax sum and the K weights.
+// The router tail and the expert FFN's routing prologue both run these, so
+// their selections and weights are bit-identical.
+
+// Keys padded with 0 up to a multiple of 4: a pad never beats a real key
+// and never ties with a lower index.  Ends with a barrier.
+__device__ void stage_keys(const float* z, int B, int E, int row, uint32_t* keys, float* zl) {
+    const int E4 = (E + 3) & ~3;
+    for (int i = threadIdx.x; i < B * E4; i += kThreads) {
+        const int b = i / E4, f = i - b * E4;
+        const float v = f < E ? z[b * E + f] : 0.f;
+        keys[b * row + f] = f < E ? order_key(v) : 0u;
+        zl[b * row + f] = v;
+    }
+    __syncthreads();
+}
+
+// win [B][K]: selected experts by position; rowmax [B].  Ends with a barrier.
+// The scan counts greater and equal keys (four row entries per LDS read,
+// four reads in flight); only a lane that met an equal key other than its
+// own rescans its row for equal keys at lower indices.
+__device__ void rank_winners(const uint32_t* keys, const float* zl, int B, int E, int K, int row,
+                             int32_t* win, float* rowmax) {
+    const int tid = threadIdx.x, BE = B * E;
+    int T = 1;                                    // lanes per pair (power of two)
+    while (T < 16 && BE * T * 2 <= kThreads) T *= 2;
+    const int n4 = ((E + 3) & ~3) / 4;
+    for (int base = 0; base < BE * T; base += kThreads) {
+        const int t = base + tid, i = t / T, part = t & (T - 1);
+        const int b = i / E, f = i - b * E;
+        int gt = 0, eq = 0;
+        const uint32_t* rk = keys + b * row;
+        const uint32_t mine = i < BE ? rk[f] : 0u;
+        if (i < BE) {
+            int c = part;
+            for (; c + 3 * T < n4; c += 4 * T) {
+                uint4 k[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) k[u] = *reinterpret_cast<const uint4*>(rk + 4 * (c + u * T));
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    gt += int(k[u].x > mine) + int(k[u].y > mine) + int(k[u].z > mine) + int(k[u].w > mine);
+                    eq += int(k[u].x == mine) + int(k[u].y == mine) + int(k[u].z == mine) + int(k[u].w == mine);
+                }
+            }
+            for (; c < n4; c += T) {
+                const uint4 k = *reinterpret_cast<const uint4*>(rk + 4 * c);
+                gt += int(k.x > mine) + int(k.y > mine) + int(k.z > mine) + int(k.w > mine);
+                eq += int(k.x == mine) + int(k.y == mine) + int(k.z == mine) + int(k.w == mine);
+            }
+        }
+        for (int o = 1; o < T; o <<= 1) {
+            gt += __shfl_xor(gt, o, 64);
+            eq += __shfl_xor(eq, o, 64);
+        }
+        if (i < BE && part == 0) {
+            int cnt = gt;
+            if (eq > 1)                           // ties: equal keys at lower indices rank higher
+                for (int g = 0; g < f; ++g) cnt += rk[g] == mine;
+            if (cnt < K) {
+                win[b * K + cnt] = f;
+                if (cnt == 0) rowmax[b] = zl[b * row + f];
+            }
+        }
+    }
+    __syncthreads();
+}
+
+// Softmax weights of the winners (NaN-free logits assumed): lanes k < K of
+// the row's wave get (expert, weight) of position k.  Whole wave calls it.
+__device__ __forceinline__ void row_weights(const float* zl, const int32_t* win, const float* rowmax, int b,
+                                            int E, int K, int row, int renorm, int& e, float& wt) {
+    const int lane = threadIdx.x & 63;
+    const float m = rowmax[b];
+    float s = 0.f;
+    for (int f = lane; f < E; f += 64) s += expf(zl[b * row + f] - m);
+    s = wave_sum(s);
+    float p = 0.f;
+    e = 0;
+    if (lane < K) {
+        e = win[b * K + lane];
+        p = expf(zl[b * row + e] - m) / s;
+    }
+    const float wsum = wave_sum(p);
+    wt = renorm ? p / wsum : p;
+}
+
+// The router tail: writes idx/w (and the selection to s_idx in LDS when
+// given) and ends with a barrier.
 __device__ void softmax_topk_tail(const RouteArgs& a, const float* z, int32_t* s_idx) {
-    constexpr int kRow = kMaxE;                   // LDS row stride
+    constexpr int kRow = kMaxE;
     __shared__ __align__(16) uint32_t keys[kMaxB * kRow];
     __shared__ float zl[kMaxB * kRow];
     __shared__ int32_t win[kMaxB * kMaxK];
     __shared__ float rowmax[kMaxB];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int K = a.K, E = a.E, BE = a.B * a.E;
-    const int E4 = (E + 3) & ~3;
-    // keys padded with 0 up to a multiple of 4: a pad never beats a real key
-    // and never ties with a lower index
-    for (int i = tid; i < a.B * E4; i += kThreads) {
-        const int b = i / E4, f = i - b * E4;
-        const float v = f < E ? z[b * E + f] : 0.f;
-        keys[b * kRow + f] = f < E ? order_key(v) : 0u;
-        zl[b * kRow + f] = v;
-    }
-    __syncthreads();
-    int T = 1;                                    // lanes per pair (power of two)
-    while (T < 16 && BE * T * 2 <= kThreads) T *= 2;
-    const int n4 = E4 / 4;
-    for (int base = 0; base < BE * T; base += kThreads) {
-        const int t = base + tid, i = t / T, part = t & (T - 1);
-        const int b = i / E, f = i - b * E;
-        int cnt = 0;
-        if (i < BE) {
-            const uint32_t* row = keys + b * kRow;
-            const uint32_t mine = row[f];
-            for (int c = part; c < n4; c += T) {
-                const uint4 k = *reinterpret_cast<const uint4*>(row + 4 * c);
-                const int g = 4 * c;
-                cnt += (k.x > mine) + (k.y > mine) + (k.z > mine) + (k.w > mine);
-                cnt += (k.x == mine && g < f) + (k.y == mine && g + 1 < f) + (k.z == mine && g + 2 < f) +
-                       (k.w == mine && g + 3 < f);
-            }
-        }
-        for (int o = 1; o < T; o <<= 1) cnt += __shfl_xor(cnt, o, 64);
-        if (i < BE && part == 0 && cnt < K) {
-            win[b * K + cnt] = f;
-            if (cnt == 0) rowmax[b] = zl[b * kRow + f];
-        }
-    }
-    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    stage_keys(z, a.B, a.E, kRow, keys, zl);
+    rank_winners(keys, zl, a.B, a.E, a.K, kRow, win, rowmax);
     for (int b = wave; b < a.B; b += kThreads / 64) {
-        // softmax sum (NaN-free inputs assumed for the weights)
-        const float m = rowmax[b];
-        float s = 0.f;
-        for (int f = lane; f < E; f += 64) s += expf(zl[b * kRow + f] - m);
-        s = wave_sum(s);
-        float p = 0.f;
-        int e = 0;
-        if (lane < K) {
-            e = win[b * K + lane];
-            p = expf(zl[b * kRow + e] - m) / s;
-        }
-        const float wsum = wave_sum(p);
-        if (lane < K) {
-            a.idx[b * K + lane] = e;
-            a.w[b * K + lane] = a.renorm ? p / wsum : p;
-            if (s_idx) s_idx[b * K + lane] = e;
+        int e;
+        float wt;
+        row_weights(zl, win, rowmax, b, a.E, a.K, kRow, a.renorm, e, wt);
+        if (lane < a.K) {
+            a.idx[b * a.K + lane] = e;
+            a.w[b * a.K + lane] = wt;
+            if (s_idx) s_idx[b * a.K + lane] = e;
         }
     }
     __syncthreads();

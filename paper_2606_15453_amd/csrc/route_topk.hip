@@ -78,3 +78,20 @@ extern "C" int moe_route_topk(const void* x, const void* w_gate, int B, int H, i
     STMOE_LAUNCHED();
     return STMOE_OK;
 }
+
+namespace stmoe {
+// Internal: the router's logits alone, z [B][E] fp32 (for callers that run
+// softmax / top-K elsewhere).  Shapes are validated by the caller.
+int route_logits(const void* x, const void* w_gate, int B, int H, int E, int dtype, float* z, hipStream_t s) {
+    RouteArgs a{};
+    a.x = x;
+    a.wg = w_gate;
+    a.B = B;
+    a.H = H;
+    a.E = E;
+    a.K = 1;
+    a.bf16 = dtype == STMOE_BF16;
+    a.zbuf = z;
+    return launch_route_logits(a, s);
+}
+}  // namespace stmoe

@@ -69,15 +69,21 @@ def parse():
 
 
 COUNTERS_MD = os.path.join(ROOT, "profiles", "ffn_gate_up_mixtral8x7b_b1_counters.md")
-FFN_SOURCE = os.path.join(ROOT, "paper_2606_15453_amd", "csrc", "expert_ffn.hip")
+FFN_SOURCES = [os.path.join(ROOT, "paper_2606_15453_amd", "csrc", f)
+               for f in ("expert_ffn.hip", "gating_dev.h", "common.h")]
 CALIB_BYTES = 1 << 30
 COUNTER_TOKENS = 20
 
 
 def ffn_source_sha():
+    """Hash of the sources the gate/up kernel is built from (the FFN kernels,
+    the gating steps of their routing prologue, the shared helpers)."""
     import hashlib
-    with open(FFN_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in FFN_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def committed_traffic():

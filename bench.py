@@ -52,8 +52,10 @@ def parse():
                     help="decode tokens per capped-cache mode (0 skips the offload runs)")
     ap.add_argument("--pinned-gb", type=float, default=56.0,
                     help="pinned host pool budget; larger stacks alias experts onto it")
-    ap.add_argument("--cpu-tokens", type=int, default=2,
-                    help="decode tokens of the CPU oracle sample (0 skips it)")
+    ap.add_argument("--cpu-tokens", type=int, default=64,
+                    help="at most this many decode tokens of the CPU oracle sample (0 skips it)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="the CPU oracle sample stops after the token that reaches this much timed work")
     ap.add_argument("--counters", action="store_true",
                     help="run the fixed workload profiled by the rocprofv3 --pmc passes and exit")
     ap.add_argument("--predictor-sweep", action="store_true",
@@ -421,11 +423,15 @@ def hbm_resident(wl, steps, warmup):
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     up_ms, down_ms, n_calls, n_exp = ctx.timing()
+    route_ms, _, ffn_ms, pred_ms, n_timed = ctx.stage_timing()
     stats = pred.stats()
     ctx.close()
     pred.close()
+    per = 1e3 / max(n_timed, 1)
+    stages = {"route_logits": round(route_ms * per, 2), "ffn_with_routing": round(ffn_ms * per, 2),
+              "predict_side_stream": round(pred_ms * per, 2)}
     return dict(seconds=dt, up_ms=up_ms, down_ms=down_ms, n_calls=n_calls, n_experts=n_exp, stats=stats,
-                host_issue_us_per_layer=host_us)
+                host_issue_us_per_layer=host_us, stages_us=stages)
 
 
 def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
@@ -465,6 +471,7 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
         pred.profile(wl.prof)
         ctx = make_ctx(wl, pred, cache)
         ctx.set_prefetch(min_score, max_pf)
+        ctx.set_timing(1)       # events on every layer: negligible next to ms-scale copies
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         run_tokens(ctx, wl, 0, n_tokens, y, mode)
@@ -472,6 +479,7 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
         demand.synchronize()
         side.synchronize()
         dt = time.perf_counter() - t0
+        route_ms, miss_ms, ffn_ms, _, n_timed = ctx.stage_timing()
         cst = cache.stats()
         st = pred.stats()
         copies = cst["demand"] + cst["overflow"] + cst["prefetch"]
@@ -480,7 +488,10 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
                    tokens_per_s=round(cfg.B * n_tokens / dt, 3),
                    ms_per_token=round(1e3 * dt / n_tokens, 3),
                    stall_ms_per_token=round(1e3 * dt / n_tokens - resident_ms_per_token, 3),
-                   h2d_copies=copies, h2d_gbps=round(copies * blob / dt / 1e9, 2), cache=cst)
+                   h2d_copies=copies, h2d_gbps=round(copies * blob / dt / 1e9, 2), cache=cst,
+                   stages_us_per_layer={"route_and_predict": round(1e3 * route_ms / max(n_timed, 1), 1),
+                                        "record_wait_and_missed_loads": round(1e3 * miss_ms / max(n_timed, 1), 1),
+                                        "ffn": round(1e3 * ffn_ms / max(n_timed, 1), 1)})
         if mode != S.MODE_ON_DEMAND:
             rec["recall_layers_ge1"] = round(float(st[1:, 0].sum() / max(st[1:, 1].sum(), 1)), 4)
             rec["recall_layer0"] = round(float(st[0, 0] / max(st[0, 1], 1)), 4)
@@ -502,12 +513,38 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
     return out
 
 
-def cpu_baseline(wl, n_tokens):
-    """The CPU oracle on the first n_tokens decode tokens of the same workload.
+def near_tie_rows(wl, warmup, steps, eps=1e-4):
+    """Routed rows of the timed tokens whose K-th and (K+1)-th router logits
+    (fp64) differ by less than eps: their expert set may legitimately differ
+    between fp32 and fp64 arithmetic."""
+    cfg = wl.cfg
+    if cfg.K >= cfg.E:
+        return {"rows": 0, "of": 0, "eps": eps}
+    from paper_2606_15453_amd import workload as W
+
+    def exact(a):   # stored values (bf16 bits or fp32) as float64
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64) if a.dtype == np.uint16 \
+            else a.astype(np.float64)
+
+    wg = [exact(W.to_storage(cfg, g)) for g in wl.wg_f64]
+    n, rows = 0, 0
+    for i in range(steps):
+        t = (warmup + i) % cfg.T
+        for l in range(cfg.L):
+            z = np.sort(exact(wl.x_store[t][l]) @ wg[l].T, axis=1)[:, ::-1]
+            n += int(np.sum(z[:, cfg.K - 1] - z[:, cfg.K] < eps))
+            rows += z.shape[0]
+    return {"rows": n, "of": rows, "eps": eps}
+
+
+def cpu_baseline(wl, max_tokens, target_s):
+    """The CPU oracle on the first decode tokens of the same workload, until
+    `target_s` seconds of timed work (at most max_tokens tokens).
 
     Timed: routing, predictor update/predict, cache policy and the fp64 FFN of
     every layer.  Not timed: preparing each layer's fp64 expert matrices (the
-    generator's GPU backend, copied to the host)."""
+    generator's GPU blobs widened to fp64 on the GPU and copied into pinned
+    host buffers)."""
     import torch
     from oracle.stmoe_oracle import STPredictor, CacheSim, decode_storage, moe_ffn, route
     cfg = wl.cfg
@@ -522,12 +559,22 @@ def cpu_baseline(wl, n_tokens):
     P_cur = pred.predict(-1, None)
     timed = 0.0
     n, Hh, Ii = cfg.H * cfg.I, cfg.H, cfg.I
+    n_bufs = min(cfg.B * cfg.K, cfg.E) + cfg.n_shared
+    bufs = [torch.empty(cfg.blob_elems, dtype=torch.float64, pin_memory=True) for _ in range(n_bufs)]
+    used = [0]
 
     def mats(blob):
-        b = blob.to(torch.float64).cpu().numpy()
+        buf = bufs[used[0]]
+        used[0] += 1
+        buf.copy_(blob.to(torch.float64))
+        b = buf.numpy()
         return b[:n].reshape(Ii, Hh), b[n:2 * n].reshape(Ii, Hh), b[2 * n:].reshape(Hh, Ii)
 
-    for t in range(n_tokens):
+    n_tokens = 0
+    for t in range(min(max_tokens, cfg.T)):
+        if timed >= target_s:
+            break
+        n_tokens += 1
         prev = None
         for l in range(cfg.L):
             x = decode_storage(wl.x_store[t][l])
@@ -539,6 +586,7 @@ def cpu_baseline(wl, n_tokens):
             U = sorted(set(v for s in cur for v in s))
             cache.acquire(l, U, t * cfg.L + l + 1)
             timed += time.perf_counter() - t0
+            used[0] = 0
             experts = {e: mats(wl.blobs[l * cfg.E + e]) for e in U}
             shared = [mats(wl.shared[l * cfg.n_shared + s]) for s in range(cfg.n_shared)]
             t0 = time.perf_counter()
@@ -547,11 +595,12 @@ def cpu_baseline(wl, n_tokens):
             timed += time.perf_counter() - t0
             prev, P_cur = cur, P_next
             del experts
+    del bufs
     return dict(value=round(cfg.B * n_tokens / timed, 4), unit="tokens/s", cores=int(cores),
                 kind="oracle", seconds=round(timed, 3),
                 sample=f"first {n_tokens} decode token(s) x {cfg.L} layers x batch {cfg.B} of the same "
-                       f"workload: fp64 routing, predictor, cache policy and SwiGLU FFN (expert matrix "
-                       f"preparation not timed)")
+                       f"workload: fp64 routing, predictor, cache policy and SwiGLU FFN, {timed:.1f} s of "
+                       f"timed CPU work (expert matrix preparation not timed)")
 
 
 def main():
@@ -630,6 +679,10 @@ def main():
         "step_hbm_gbps": round((up_bytes + dn_bytes) / max(r["n_calls"] / cfg.L, 1e-9) * args.steps
                                / r["seconds"] / 1e9, 1),
         "layer_us": round(1e6 * r["seconds"] / args.steps / cfg.L, 2),
+        # event-timed stages per layer (every 8th token); the side-stream
+        # predictor overlaps the FFN and the next router
+        "stages_us_per_layer": r["stages_us"],
+        "routing_near_tie_rows": near_tie_rows(wl, warmup=args.warmup, steps=args.steps),
         "host_issue_us_per_layer": round(r["host_issue_us_per_layer"], 2),
         "prediction": {
             "recall_layers_ge1": round(float(stats[1:, 0].sum() / max(stats[1:, 1].sum(), 1)), 4),
@@ -645,7 +698,7 @@ def main():
         out["offload"] = offload(wl, args.offload_tokens, ms_per_step, args.pinned_gb)
     if args.cpu_tokens > 0:
         t0 = time.time()
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens, args.cpu_seconds)
         log(f"cpu baseline {out['cpu_baseline']['value']} tok/s in {time.time() - t0:.1f}s wall")
     print(json.dumps(out), flush=True)
 

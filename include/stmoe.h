@@ -331,6 +331,17 @@ int moe_ctx_last_routing(moe_ctx* ctx, int32_t* idx, float* w);
 int moe_ctx_set_timing(moe_ctx* ctx, int every);
 int moe_ctx_timing(moe_ctx* ctx, double* up_ms, double* down_ms, int64_t* n_calls,
                    int64_t* n_experts);
+/* Stage times over the same timed layers (summed milliseconds, [sync]):
+ *   route_ms    the routing launches (with a cache: router + update + predict)
+ *   miss_ms     from routing to the FFN: the host's wait for the routing
+ *               record and the missed-expert loads (0 without a cache)
+ *   ffn_ms      both FFN kernels
+ *   predict_ms  update + predict on the side stream (no cache; overlaps the
+ *               FFN and the next layer's router, so it is not on the layer's
+ *               critical path)
+ * Any argument may be NULL. */
+int moe_ctx_stage_timing(moe_ctx* ctx, double* route_ms, double* miss_ms, double* ffn_ms,
+                         double* predict_ms, int64_t* n_calls);
 
 /* ------------------------------------------------------------------------
  * Measurement kernels of known traffic (not part of the decode path).

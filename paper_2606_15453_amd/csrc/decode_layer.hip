@@ -91,6 +91,13 @@ struct moe_ctx {
     int timing_every = 0;
     std::vector<hipEvent_t> ev_pool;
     size_t ev_used = 0;
+    // per timed layer: event indices into ev_pool (-1: not recorded)
+    struct TimedLayer {
+        int route0 = -1, route1 = -1;      // around the routing launches (compute stream)
+        int up0 = -1, mid = -1, down1 = -1;  // around the FFN's two kernels
+        int pred0 = -1, pred1 = -1;        // around update/predict on the side stream
+    };
+    std::vector<TimedLayer> timed_layers;
     unsigned long long* n_experts = nullptr;   // device counter
     int64_t n_calls = 0;
 };
@@ -176,10 +183,13 @@ int fetch_record(moe_ctx* c, const int32_t* idx_dev, bool with_ranked) {
     return STMOE_OK;
 }
 
+// Timing events are only read after a device-wide sync, so they skip the
+// system-scope fence (a cache writeback at every record that would stretch
+// the measured intervals).
 hipEvent_t next_event(moe_ctx* c) {
     if (c->ev_used == c->ev_pool.size()) {
         hipEvent_t e;
-        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
         c->ev_pool.push_back(e);
     }
     return c->ev_pool[c->ev_used++];
@@ -300,6 +310,20 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
     }
     const bool route_in_ffn = !c->cache && B * E <= kRouteInFfnMax;
     float* zbuf = reinterpret_cast<float*>(c->route_ws);
+    const bool timed = timing && timed_token(c, token);
+    moe_ctx::TimedLayer tl;
+    auto stamp_event = [&](int& slot, hipStream_t st) -> int {
+        hipEvent_t ev = next_event(c);
+        if (!ev) {
+            set_error("moe_decode_layer: hipEventCreate failed");
+            return STMOE_EHIP;
+        }
+        slot = int(c->ev_used - 1);
+        STMOE_HIP(hipEventRecord(ev, st));
+        return STMOE_OK;
+    };
+    if (timed)
+        if (int rc = stamp_event(tl.route0, c->s)) return rc;
     if (route_in_ffn) {
         if (int rc = route_logits(x, c->router[layer], B, c->H, E, c->dtype, zbuf, c->s)) return rc;
     } else if (use && c->side) {
@@ -309,8 +333,12 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         STMOE_HIP(hipEventRecord(c->ev_sel, c->s));
         STMOE_HIP(hipStreamWaitEvent(c->side, c->ev_sel, 0));
         const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
+        if (timed)
+            if (int rc = stamp_event(tl.pred0, c->side)) return rc;
         if (int rc = update_predict(c->pred, layer, prev, idx_l, use, 1, nullptr, nullptr, nullptr, c->side))
             return rc;
+        if (timed)
+            if (int rc = stamp_event(tl.pred1, c->side)) return rc;
         c->side_pending = true;
     } else if (use) {
         // with a cache the host reads the prediction: one fused launch pair
@@ -324,6 +352,10 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
                                     nullptr, c->route_ws, c->route_ws_bytes, c->s))
             return rc;
     }
+    // with a cache the routing record wait and the missed loads come next;
+    // without one the FFN follows directly and its first event ends routing
+    if (timed && c->cache)
+        if (int rc = stamp_event(tl.route1, c->s)) return rc;
     // ML: make the selection resident
     if (c->cache) {
         if (int rc = fetch_record(c, idx_l, use != 0)) return rc;
@@ -346,14 +378,13 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         if (int rc2 = set_table(c, layer, c->host_table)) return rc2;
     }
     // Com.: expert FFN (timed with events before, between and after its two kernels)
-    hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
-    const bool timed = timing && timed_token(c, token);
+    hipEvent_t e1 = nullptr;
     if (timed) {
-        e0 = next_event(c);
+        if (int rc = stamp_event(tl.up0, c->s)) return rc;
+        if (!c->cache) tl.route1 = tl.up0;
         e1 = next_event(c);
-        e2 = next_event(c);
-        if (!e0 || !e1 || !e2) { set_error("moe_decode_layer: hipEventCreate failed"); return STMOE_EHIP; }
-        STMOE_HIP(hipEventRecord(e0, c->s));
+        if (!e1) { set_error("moe_decode_layer: hipEventCreate failed"); return STMOE_EHIP; }
+        tl.mid = int(c->ev_used - 1);
     }
     if (int rc = ffn_launch(x, idx_l, w_l, B, K, c->H, c->I, E, c->dtype, c->tables + size_t(layer) * E,
                             c->n_shared ? c->shared + size_t(layer) * c->n_shared : nullptr, c->n_shared,
@@ -361,7 +392,7 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
                             route_in_ffn ? zbuf : nullptr, c->renorm))
         return rc;
     if (timed) {
-        STMOE_HIP(hipEventRecord(e2, c->s));
+        if (int rc = stamp_event(tl.down1, c->s)) return rc;
         ++c->n_calls;
     }
     if (route_in_ffn && use && c->side) {
@@ -369,10 +400,15 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         STMOE_HIP(hipEventRecord(c->ev_sel, c->s));
         STMOE_HIP(hipStreamWaitEvent(c->side, c->ev_sel, 0));
         const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
+        if (timed)
+            if (int rc = stamp_event(tl.pred0, c->side)) return rc;
         if (int rc = update_predict(c->pred, layer, prev, idx_l, use, 1, nullptr, nullptr, nullptr, c->side))
             return rc;
+        if (timed)
+            if (int rc = stamp_event(tl.pred1, c->side)) return rc;
         c->side_pending = true;
     }
+    if (timed) c->timed_layers.push_back(tl);
     // EP: prefetch the next layer's predicted experts, overlapping the FFN
     if (c->cache) {
         if (int rc = expert_cache_release(c->cache, layer, c->s)) return rc;
@@ -541,28 +577,56 @@ extern "C" int moe_ctx_set_timing(moe_ctx* c, int every) {
     c->timing_every = every;
     c->ev_used = 0;
     c->n_calls = 0;
+    c->timed_layers.clear();
     STMOE_HIP(hipMemset(c->n_experts, 0, sizeof(unsigned long long)));
     return STMOE_OK;
 }
+
+namespace {
+// Summed milliseconds between two recorded events of each timed layer.
+int sum_pairs(moe_ctx* c, int moe_ctx::TimedLayer::*a, int moe_ctx::TimedLayer::*b, double& out) {
+    out = 0.0;
+    for (const auto& t : c->timed_layers) {
+        if (t.*a < 0 || t.*b < 0) continue;
+        float ms = 0.f;
+        STMOE_HIP(hipEventElapsedTime(&ms, c->ev_pool[size_t(t.*a)], c->ev_pool[size_t(t.*b)]));
+        out += ms;
+    }
+    return STMOE_OK;
+}
+}  // namespace
 
 extern "C" int moe_ctx_timing(moe_ctx* c, double* up_ms, double* down_ms, int64_t* n_calls,
                               int64_t* n_experts) {
     clear_error();
     STMOE_CHECK(c, "null ctx");
-    STMOE_HIP(hipStreamSynchronize(c->s));
+    STMOE_HIP(hipDeviceSynchronize());
     double a = 0.0, b = 0.0;
-    for (size_t i = 0; i + 2 < c->ev_used; i += 3) {
-        float t0 = 0.f, t1 = 0.f;
-        STMOE_HIP(hipEventElapsedTime(&t0, c->ev_pool[i], c->ev_pool[i + 1]));
-        STMOE_HIP(hipEventElapsedTime(&t1, c->ev_pool[i + 1], c->ev_pool[i + 2]));
-        a += t0;
-        b += t1;
-    }
+    if (int rc = sum_pairs(c, &moe_ctx::TimedLayer::up0, &moe_ctx::TimedLayer::mid, a)) return rc;
+    if (int rc = sum_pairs(c, &moe_ctx::TimedLayer::mid, &moe_ctx::TimedLayer::down1, b)) return rc;
     unsigned long long ne = 0;
     STMOE_HIP(hipMemcpy(&ne, c->n_experts, sizeof(ne), hipMemcpyDeviceToHost));
     if (up_ms) *up_ms = a;
     if (down_ms) *down_ms = b;
     if (n_calls) *n_calls = c->n_calls;
     if (n_experts) *n_experts = int64_t(ne);
+    return STMOE_OK;
+}
+
+extern "C" int moe_ctx_stage_timing(moe_ctx* c, double* route_ms, double* miss_ms, double* ffn_ms,
+                                    double* predict_ms, int64_t* n_calls) {
+    clear_error();
+    STMOE_CHECK(c, "null ctx");
+    STMOE_HIP(hipDeviceSynchronize());
+    double r = 0.0, m = 0.0, f = 0.0, p = 0.0;
+    if (int rc = sum_pairs(c, &moe_ctx::TimedLayer::route0, &moe_ctx::TimedLayer::route1, r)) return rc;
+    if (int rc = sum_pairs(c, &moe_ctx::TimedLayer::route1, &moe_ctx::TimedLayer::up0, m)) return rc;
+    if (int rc = sum_pairs(c, &moe_ctx::TimedLayer::up0, &moe_ctx::TimedLayer::down1, f)) return rc;
+    if (int rc = sum_pairs(c, &moe_ctx::TimedLayer::pred0, &moe_ctx::TimedLayer::pred1, p)) return rc;
+    if (route_ms) *route_ms = r;
+    if (miss_ms) *miss_ms = m;
+    if (ffn_ms) *ffn_ms = f;
+    if (predict_ms) *predict_ms = p;
+    if (n_calls) *n_calls = c->n_calls;
     return STMOE_OK;
 }

@@ -44,6 +44,8 @@ constexpr int kMaxShared = 8;
 constexpr int kMaxSlots = kMaxE + kMaxShared;
 constexpr int kDownWgTarget = 256;    // workgroups the MFMA down phase aims for
 constexpr int kMfmaMinB = 8;          // batch from which the MFMA kernels run
+constexpr int kUpInFlight = 2;        // 16-byte chunks per row in flight per lane (GEMV gate/up)
+constexpr int kDownInFlight = 2;      // ... per row per lane in the whole-workgroup down kernel
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -271,20 +273,21 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
             }
         }
     };
+    constexpr int U = kUpInFlight;
     int c = g;
-    for (; c + G < cpr; c += 2 * G) {          // two chunks in flight per row
-        uint4 ga[R], ua[R], gb[R], ub[R];
+    for (; c + (U - 1) * G < cpr; c += U * G) {   // U chunks per row in flight
+        uint4 qg[U][R], qu[U][R];
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            ga[r] = ld_stream(wg + r * rowb + size_t(c) * 16);
-            ua[r] = ld_stream(wu + r * rowb + size_t(c) * 16);
-            gb[r] = ld_stream(wg + r * rowb + size_t(c + G) * 16);
-            ub[r] = ld_stream(wu + r * rowb + size_t(c + G) * 16);
-        }
-        compute(c, ga, ua);
-        compute(c + G, gb, ub);
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                qg[u][r] = ld_stream(wg + r * rowb + size_t(c + u * G) * 16);
+                qu[u][r] = ld_stream(wu + r * rowb + size_t(c + u * G) * 16);
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u) compute(c + u * G, qg[u], qu[u]);
     }
-    if (c < cpr) {
+    for (; c < cpr; c += G) {
         uint4 ga[R], ua[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -516,18 +519,18 @@ __global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
                 for (int r = 0; r < R; ++r) acc[r][b] = dotc<BF>(cw[r], cx, acc[r][b]);
             }
         };
+        constexpr int U = kDownInFlight;
         int c = tid;
-        for (; c + kThreads < cpr; c += 2 * kThreads) {
-            uint4 qa[R], qb[R];
+        for (; c + (U - 1) * kThreads < cpr; c += U * kThreads) {   // U chunks per row in flight
+            uint4 q[U][R];
 #pragma unroll
-            for (int r = 0; r < R; ++r) {
-                qa[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
-                qb[r] = ld_stream(wd + r * rowb + size_t(c + kThreads) * 16);
-            }
-            compute(c, qa);
-            compute(c + kThreads, qb);
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int r = 0; r < R; ++r) q[u][r] = ld_stream(wd + r * rowb + size_t(c + u * kThreads) * 16);
+#pragma unroll
+            for (int u = 0; u < U; ++u) compute(c + u * kThreads, q[u]);
         }
-        if (c < cpr) {
+        for (; c < cpr; c += kThreads) {
             uint4 qa[R];
 #pragma unroll
             for (int r = 0; r < R; ++r) qa[r] = ld_stream(wd + r * rowb + size_t(c) * 16);

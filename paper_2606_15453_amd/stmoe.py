@@ -103,6 +103,7 @@ _SIGS = {
     "moe_ctx_set_graph": (i32, [vp, i32]),
     "moe_ctx_graph_buffers": (i32, [vp, P(vp), P(vp)]),
     "moe_ctx_timing": (i32, [vp, P(C.c_double), P(C.c_double), P(i64), P(i64)]),
+    "moe_ctx_stage_timing": (i32, [vp, P(C.c_double), P(C.c_double), P(C.c_double), P(C.c_double), P(i64)]),
     "stmoe_calib_copy": (i32, [vp, vp, sz, vp]),
     "stmoe_calib_read_out_words": (sz, [sz]),
     "stmoe_calib_read": (i32, [vp, sz, vp, vp]),
@@ -426,6 +427,13 @@ class DecodeContext:
         nc, ne = i64(), i64()
         _call("moe_ctx_timing", self.h, C.byref(up), C.byref(down), C.byref(nc), C.byref(ne))
         return up.value, down.value, nc.value, ne.value
+
+    def stage_timing(self):
+        """(route ms, miss ms, FFN ms, side-stream predict ms, timed layers) since set_timing(every)."""
+        r, m, f, p = C.c_double(), C.c_double(), C.c_double(), C.c_double()
+        n = i64()
+        _call("moe_ctx_stage_timing", self.h, C.byref(r), C.byref(m), C.byref(f), C.byref(p), C.byref(n))
+        return r.value, m.value, f.value, p.value, n.value
 
 
 # ------------------------------------------------------------- measurement

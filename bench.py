@@ -56,6 +56,8 @@ def parse():
                     help="at most this many decode tokens of the CPU oracle sample (0 skips it)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="the CPU oracle sample stops after the token that reaches this much timed work")
+    ap.add_argument("--offload-sweep", default=None, metavar="C1,C2,...",
+                    help="capped-cache sweep over these per-layer budgets (markdown table; no JSON line)")
     ap.add_argument("--counters", action="store_true",
                     help="run the fixed workload profiled by the rocprofv3 --pmc passes and exit")
     ap.add_argument("--predictor-sweep", action="store_true",
@@ -434,12 +436,11 @@ def hbm_resident(wl, steps, warmup):
                 host_issue_us_per_layer=host_us, stages_us=stages)
 
 
-def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
-    """Capped HBM cache over a pinned host pool: on-demand vs ST-MoE prefetch.
-
-    The pool holds M = min(L*E, pinned budget / blob) distinct blobs; expert
-    (l, e) is copied from pool slot (l*E + e) mod M.  Every copy still moves a
-    whole blob over PCIe, so the timing is that of distinct experts."""
+def host_pool(wl, pinned_gb):
+    """Pinned host copies of the expert blobs.  The pool holds M = min(L*E,
+    pinned budget / blob) distinct blobs; expert (l, e) is copied from pool
+    slot (l*E + e) mod M.  Every copy still moves a whole blob over PCIe, so
+    the timing is that of distinct experts."""
     import torch
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
@@ -452,65 +453,136 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
     for i in range(M):
         host[i * blob:(i + 1) * blob].copy_(wl.blobs[i].view(torch.uint8))
     log(f"pinned host pool {pool.nbytes / 1e9:.1f} GB ({M} of {n_all} blobs) filled in {time.time() - t0:.1f}s")
-    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
-    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, blob, n_stage), dtype=torch.uint8, device="cuda:0")
-    demand, side = torch.cuda.Stream(), torch.cuda.Stream()
     ptrs = [pool.ptr + (i % M) * blob for i in range(n_all)]
+    return pool, ptrs, M
+
+
+def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_token):
+    """One capped-cache decode run: C slots per layer, the rest streamed from
+    the pinned host pool.  variant = (name, mode, min score, max prefetches
+    per layer, online CCT update)."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    cfg = wl.cfg
+    blob = cfg.blob_bytes
+    name, mode, min_score, max_pf, online = variant
+    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - C)
+    demand, side = streams
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
+    cache = S.ExpertCache(cfg.L, cfg.E, C, blob, n_stage, arena, ptrs, demand, side)
+    cache.warm(W_warm(wl, C))
+    pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+    pred.profile(wl.prof)
+    ctx = make_ctx(wl, pred, cache)
+    ctx.set_prefetch(min_score, max_pf)
+    ctx.set_online_update(online)
+    ctx.set_timing(1)       # events on every layer: negligible next to ms-scale copies
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run_tokens(ctx, wl, 0, n_tokens, y, mode)
+    torch.cuda.synchronize()
+    demand.synchronize()
+    side.synchronize()
+    dt = time.perf_counter() - t0
+    route_ms, miss_ms, ffn_ms, _, n_timed = ctx.stage_timing()
+    cst = cache.stats()
+    st = pred.stats()
+    copies = cst["demand"] + cst["overflow"] + cst["prefetch"]
+    rec = dict(tokens=n_tokens, seconds=round(dt, 4), prefetch_min_score=min_score,
+               prefetch_max_per_layer=max_pf, online_update=bool(online),
+               tokens_per_s=round(cfg.B * n_tokens / dt, 3),
+               ms_per_token=round(1e3 * dt / n_tokens, 3),
+               stall_ms_per_token=round(1e3 * dt / n_tokens - resident_ms_per_token, 3),
+               h2d_copies=copies, h2d_gbps=round(copies * blob / dt / 1e9, 2), cache=cst,
+               stages_us_per_layer={"route_and_predict": round(1e3 * route_ms / max(n_timed, 1), 1),
+                                    "record_wait_and_missed_loads": round(1e3 * miss_ms / max(n_timed, 1), 1),
+                                    "ffn": round(1e3 * ffn_ms / max(n_timed, 1), 1)})
+    if mode != S.MODE_ON_DEMAND:
+        rec["recall_layers_ge1"] = round(float(st[1:, 0].sum() / max(st[1:, 1].sum(), 1)), 4)
+        rec["recall_layer0"] = round(float(st[0, 0] / max(st[0, 1], 1)), 4)
+        rec["precision"] = round(float(st[:, 0].sum() / max(st[:, 2].sum(), 1)), 4)
+        rec["mean_predicted_per_row"] = round(float(st[:, 2].sum() / max(st[:, 1].sum() / cfg.K, 1)), 3)
+    log(f"offload C={C} {name}: {rec['tokens_per_s']} tok/s, {rec['ms_per_token']} ms/token, cache {cst}")
+    ctx.close()
+    pred.close()
+    cache.close()
+    return rec
+
+
+def W_warm(wl, C):
+    """Warm start for C slots per layer: the C experts most selected in profiling."""
+    from paper_2606_15453_amd import workload as W
+    if C == wl.cfg.C:
+        return wl.warm
+    return W.warm_sets(wl.cfg, wl.prof, C)
+
+
+def offload_variants(cfg):
+    from paper_2606_15453_amd import stmoe as S
+    return [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C, 1),
+            ("st_moe", S.MODE_STMOE, 2, cfg.C, 1),
+            ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K, 1),
+            ("ht_only", S.MODE_HT_ONLY, 2, cfg.C, 1),
+            ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C, 1)]
+
+
+def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
+    """Capped HBM cache over a pinned host pool: on-demand vs ST-MoE prefetch."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    cfg = wl.cfg
+    pool, ptrs, M = host_pool(wl, pinned_gb)
+    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
+    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
+                        device="cuda:0")
+    streams = (torch.cuda.Stream(), torch.cuda.Stream())
+    variants = offload_variants(cfg)
     out = {}
-    # (name, mode, min prediction score to prefetch, max prefetches per layer)
-    variants = [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C),
-                ("st_moe", S.MODE_STMOE, 2, cfg.C),
-                ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K),
-                ("ht_only", S.MODE_HT_ONLY, 2, cfg.C),
-                ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C)]
-    for name, mode, min_score, max_pf in variants:
-        cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, blob, n_stage, arena, ptrs, demand, side)
-        cache.warm(wl.warm)
-        pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
-        pred.profile(wl.prof)
-        ctx = make_ctx(wl, pred, cache)
-        ctx.set_prefetch(min_score, max_pf)
-        ctx.set_timing(1)       # events on every layer: negligible next to ms-scale copies
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        run_tokens(ctx, wl, 0, n_tokens, y, mode)
-        torch.cuda.synchronize()
-        demand.synchronize()
-        side.synchronize()
-        dt = time.perf_counter() - t0
-        route_ms, miss_ms, ffn_ms, _, n_timed = ctx.stage_timing()
-        cst = cache.stats()
-        st = pred.stats()
-        copies = cst["demand"] + cst["overflow"] + cst["prefetch"]
-        rec = dict(tokens=n_tokens, seconds=round(dt, 4), prefetch_min_score=min_score,
-                   prefetch_max_per_layer=max_pf,
-                   tokens_per_s=round(cfg.B * n_tokens / dt, 3),
-                   ms_per_token=round(1e3 * dt / n_tokens, 3),
-                   stall_ms_per_token=round(1e3 * dt / n_tokens - resident_ms_per_token, 3),
-                   h2d_copies=copies, h2d_gbps=round(copies * blob / dt / 1e9, 2), cache=cst,
-                   stages_us_per_layer={"route_and_predict": round(1e3 * route_ms / max(n_timed, 1), 1),
-                                        "record_wait_and_missed_loads": round(1e3 * miss_ms / max(n_timed, 1), 1),
-                                        "ffn": round(1e3 * ffn_ms / max(n_timed, 1), 1)})
-        if mode != S.MODE_ON_DEMAND:
-            rec["recall_layers_ge1"] = round(float(st[1:, 0].sum() / max(st[1:, 1].sum(), 1)), 4)
-            rec["recall_layer0"] = round(float(st[0, 0] / max(st[0, 1], 1)), 4)
-            rec["precision"] = round(float(st[:, 0].sum() / max(st[:, 2].sum(), 1)), 4)
-            rec["mean_predicted_per_row"] = round(float(st[:, 2].sum() / max(st[:, 1].sum() / cfg.K, 1)), 3)
-        out[name] = rec
-        log(f"offload {name}: {rec['tokens_per_s']} tok/s, {rec['ms_per_token']} ms/token, cache {cst}")
-        ctx.close()
-        pred.close()
-        cache.close()
+    for v in variants:
+        out[v[0]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)
     od = out["on_demand"]["stall_ms_per_token"]
     out["stall_reduction"] = {name: (round(1.0 - out[name]["stall_ms_per_token"] / od, 4) if od > 0 else None)
                               for name, *_ in variants if name != "on_demand"}
     out["cache_slots_per_layer"] = cfg.C
-    out["host_pool"] = {"distinct_blobs": M, "experts": n_all, "slot_of_expert": "(l*E + e) mod distinct_blobs"}
+    out["host_pool"] = {"distinct_blobs": M, "experts": cfg.L * cfg.E, "slot_of_expert": "(l*E + e) mod distinct_blobs"}
     out["h2d_link"] = "PCIe, pinned host memory, hipMemcpyAsync on demand/side streams"
     del arena
-    pool.close()
+    del pool
     return out
+
+
+def offload_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, budgets):
+    """Cache budget x predictor variant (with the online update on and off):
+    one markdown table of tokens/s, stall and copies."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    cfg = wl.cfg
+    pool, ptrs, M = host_pool(wl, pinned_gb)
+    cmax = max(budgets)
+    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - min(budgets))
+    arena = torch.empty(S.cache_arena_bytes(cfg.L, cmax, cfg.blob_bytes, n_stage), dtype=torch.uint8,
+                        device="cuda:0")
+    streams = (torch.cuda.Stream(), torch.cuda.Stream())
+    rows = []
+    for C in budgets:
+        variants = [(n, m, ms, (C if mp == cfg.C else mp), on) for n, m, ms, mp, on in offload_variants(cfg)]
+        variants.insert(2, ("st_moe_frozen_cct", S.MODE_STMOE, 2, C, 0))
+        base = None
+        for v in variants:
+            rec = offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)
+            if v[0] == "on_demand":
+                base = rec["stall_ms_per_token"]
+            red = 1.0 - rec["stall_ms_per_token"] / base if base and base > 0 else float("nan")
+            cst = rec["cache"]
+            rows.append(f"| {C} | {v[0]} | {rec['tokens_per_s']} | {rec['stall_ms_per_token']} | {red:+.3f} | "
+                        f"{cst['hits']} | {cst['demand'] + cst['overflow']} | {cst['prefetch']} | "
+                        f"{cst['useful']} | {rec.get('recall_layers_ge1', '-')} | {rec.get('precision', '-')} |")
+    del arena
+    del pool
+    head = [f"| C per layer | variant | tokens/s | stall ms/token | stall reduction vs on-demand | hits | "
+            f"demand + overflow copies | prefetch copies | useful prefetches | recall (l >= 1) | precision |",
+            "|---|---|---|---|---|---|---|---|---|---|---|"]
+    return head + rows
 
 
 def near_tie_rows(wl, warmup, steps, eps=1e-4):
@@ -632,6 +704,14 @@ def main():
     cfg = W.CONFIGS[args.config]
     log(f"workload {cfg.name}")
     wl = Workload(cfg)
+    if args.offload_sweep:
+        budgets = [int(c) for c in args.offload_sweep.split(",")]
+        r = hbm_resident(wl, 40, 5)
+        res_ms = 1e3 * r["seconds"] / 40
+        lines = offload_sweep(wl, max(args.offload_tokens, 1), res_ms, args.pinned_gb, budgets)
+        print(f"HBM-resident reference: {res_ms:.3f} ms/token; {max(args.offload_tokens, 1)} tokens per run")
+        print("\n".join(lines), flush=True)
+        return
     r = hbm_resident(wl, args.steps, args.warmup)
     ms_per_step = 1e3 * r["seconds"] / args.steps
     value = cfg.B * args.steps / r["seconds"]

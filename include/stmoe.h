@@ -301,6 +301,11 @@ int moe_decode_layer(moe_ctx* ctx, int token, int layer, const void* x, float* y
  * decides which).  Defaults: min_score = 2 (the paper's threshold) and
  * max_per_layer = the cache's slots per layer. */
 int moe_ctx_set_prefetch(moe_ctx* ctx, int min_score, int max_per_layer);
+/* Online CCT update (Algorithm 3, Section 4.2) during decode: on (1, the
+ * default) or frozen after profiling (0; HT rows are still overwritten with
+ * each selection).  An ablation switch; fails once a graph has been
+ * captured (the graph holds the setting it was captured with). */
+int moe_ctx_set_online_update(moe_ctx* ctx, int on);
 /* All L layers of one token: xs device [L][B][H], ys device out [L][B][H].
  * With graph replay on (moe_ctx_set_graph), every call after the first whose
  * token is not event-timed replays one HIP graph of the whole token: xs is

@@ -380,7 +380,7 @@ def stamp_of(t: int, l: int, L: int) -> int:
 
 
 def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=None,
-                     mode=MODE_STMOE, renorm=False, ffn_of=None, ffn_tokens=0):
+                     mode=MODE_STMOE, renorm=False, ffn_of=None, ffn_tokens=0, online=True):
     """Run the decode loop on the CPU.
 
     x_of(t, l) -> x [B][H] float64; wg_of(l) -> W_g [E][H] float64;
@@ -388,6 +388,8 @@ def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=N
     Per layer, in order: route; score this layer's prediction; Algorithm 3 on
     the previous layer pair and HT overwrite; predict the next layer (Eq. 1);
     demand-load the selection; FFN; prefetch the next layer's ranked set.
+    online=False freezes the CCTs after profiling (Algorithm 3's confidence
+    and replacement steps are skipped; HT is still overwritten).
     Returns a dict of per-(t, l) records and totals.
     """
     pred = STPredictor(L, E, K, B)
@@ -413,7 +415,7 @@ def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=N
             rec["npred"][t, l] = sum(len(p) for p in psets)
             rec["idx"].append(r["idx"])
             rec["w"].append(r["w"])
-            pred.update(l, prev, cur)
+            pred.update(l, prev, cur, online=online)
             if l + 1 < L:
                 P_next = pred.predict(l, cur, use_cct=use_cct, use_ht=use_ht)
             else:

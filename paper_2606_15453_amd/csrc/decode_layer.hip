@@ -72,6 +72,7 @@ struct moe_ctx {
     const void** shared = nullptr;         // [L][n_shared] device blob pointers
     int32_t* rec = nullptr;                // pinned host: idx [B][K], ranked [E], n_ranked, max scores [E] (uint8)
     int pf_min_score = 2, pf_max = 1 << 30;
+    int online = 1;                        // Algorithm 3's CCT update on (1) or frozen CCTs (0)
     hipEvent_t rec_ev = nullptr;
     std::vector<const void*> host_table;   // [E] scratch for the cache's answers
     bool started = false;
@@ -335,7 +336,7 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
         if (timed)
             if (int rc = stamp_event(tl.pred0, c->side)) return rc;
-        if (int rc = update_predict(c->pred, layer, prev, idx_l, use, 1, nullptr, nullptr, nullptr, c->side))
+        if (int rc = update_predict(c->pred, layer, prev, idx_l, use, c->online, nullptr, nullptr, nullptr, c->side))
             return rc;
         if (timed)
             if (int rc = stamp_event(tl.pred1, c->side)) return rc;
@@ -344,7 +345,7 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         // with a cache the host reads the prediction: one fused launch pair
         const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
         if (int rc = fused_route_predict(x, c->router[layer], c->H, c->dtype, c->renorm, idx_l, w_l,
-                                         c->route_ws, c->pred, layer, prev, use, 1, c->ranked,
+                                         c->route_ws, c->pred, layer, prev, use, c->online, c->ranked,
                                          c->ranked + E, max_scores(c->ranked, E), c->s))
             return rc;
     } else {
@@ -402,7 +403,7 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
         if (timed)
             if (int rc = stamp_event(tl.pred0, c->side)) return rc;
-        if (int rc = update_predict(c->pred, layer, prev, idx_l, use, 1, nullptr, nullptr, nullptr, c->side))
+        if (int rc = update_predict(c->pred, layer, prev, idx_l, use, c->online, nullptr, nullptr, nullptr, c->side))
             return rc;
         if (timed)
             if (int rc = stamp_event(tl.pred1, c->side)) return rc;
@@ -541,6 +542,14 @@ extern "C" int moe_ctx_set_prefetch(moe_ctx* c, int min_score, int max_per_layer
     STMOE_CHECK(min_score >= 0 && max_per_layer >= 0, "knobs must be >= 0");
     c->pf_min_score = min_score;
     c->pf_max = max_per_layer;
+    return STMOE_OK;
+}
+
+extern "C" int moe_ctx_set_online_update(moe_ctx* c, int on) {
+    clear_error();
+    STMOE_CHECK(c, "null ctx");
+    STMOE_CHECK(!c->graph_exec, "set the online update before graph replay captures a token");
+    c->online = on ? 1 : 0;
     return STMOE_OK;
 }
 

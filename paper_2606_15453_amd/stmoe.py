@@ -98,6 +98,7 @@ _SIGS = {
     "moe_decode_layer": (i32, [vp, i32, i32, vp, vp, i32]),
     "moe_decode_token": (i32, [vp, i32, vp, vp, i32]),
     "moe_ctx_set_prefetch": (i32, [vp, i32, i32]),
+    "moe_ctx_set_online_update": (i32, [vp, i32]),
     "moe_ctx_last_routing": (i32, [vp, vp, vp]),
     "moe_ctx_set_timing": (i32, [vp, i32]),
     "moe_ctx_set_graph": (i32, [vp, i32]),
@@ -397,6 +398,10 @@ class DecodeContext:
 
     def set_prefetch(self, min_score=2, max_per_layer=1 << 30):
         _call("moe_ctx_set_prefetch", self.h, min_score, max_per_layer)
+
+    def set_online_update(self, on=True):
+        """Algorithm 3's CCT update during decode on, or the CCTs frozen after profiling."""
+        _call("moe_ctx_set_online_update", self.h, int(bool(on)))
 
     def token(self, token, xs, ys, mode=MODE_STMOE):
         _call("moe_decode_token", self.h, token, _p(xs), _p(ys), mode)

@@ -32,7 +32,7 @@ class Stack:
         return [s.data_ptr() for l in range(self.cfg.L) for s in self.shared[l]]
 
 
-def _oracle(st, mode, C=None, ffn_tokens=0):
+def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True):
     from gpuhelp import expert_f64
     from oracle.stmoe_oracle import decode_reference, decode_storage, moe_ffn
     cfg = st.cfg
@@ -44,10 +44,10 @@ def _oracle(st, mode, C=None, ffn_tokens=0):
     return decode_reference(cfg.L, cfg.E, cfg.K, cfg.B, lambda t, l: decode_storage(st.x_store[t][l]),
                             lambda l: decode_storage(st.wg[l]), st.prof, cfg.T, C=C,
                             warm=None if C is None else st.warm, mode=mode, ffn_of=ffn_of,
-                            ffn_tokens=ffn_tokens)
+                            ffn_tokens=ffn_tokens, renorm=renorm, online=online)
 
 
-def _run_gpu(st, mode, capped):
+def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
@@ -73,13 +73,15 @@ def _run_gpu(st, mode, capped):
         cache.warm(st.warm)
         ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
                               [g.data_ptr() for g in st.wg_dev], predictor=pred, cache=cache,
-                              shared_ptrs=st.shared_ptrs(), n_shared=cfg.n_shared, stream=stream)
+                              shared_ptrs=st.shared_ptrs(), n_shared=cfg.n_shared, renorm=renorm,
+                              stream=stream)
     else:
         resident = [st.blobs[l][e].data_ptr() for l in range(cfg.L) for e in range(cfg.E)]
         ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
                               [g.data_ptr() for g in st.wg_dev], predictor=pred,
                               resident_ptrs=resident, shared_ptrs=st.shared_ptrs(),
-                              n_shared=cfg.n_shared, stream=stream)
+                              n_shared=cfg.n_shared, renorm=renorm, stream=stream)
+    ctx.set_online_update(online)
     idx_hist, ys = [], []
     for t in range(cfg.T):
         y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device=DEV)
@@ -89,6 +91,8 @@ def _run_gpu(st, mode, capped):
         ys.append(y.cpu().numpy())
     stats = pred.stats()
     cst = cache.stats() if cache else None
+    if tables is not None:
+        tables.append(pred.export())
     ctx.close()
     if cache:
         cache.close()
@@ -120,6 +124,35 @@ def test_decode_resident_matches_oracle(name, over):
     # hit statistics per layer: (hits, |A|, |P|)
     assert np.array_equal(stats[:, 0], ref["hits"].sum(axis=0))
     assert np.array_equal(stats[:, 2], ref["npred"].sum(axis=0))
+
+
+@pytest.mark.parametrize("over,renorm", [(dict(E=7, K=3, B=2, T=6, P=3), False),
+                                         (dict(E=64, K=4, B=4, T=4, P=2, C=16), False),
+                                         (dict(B=3, T=6, P=3), True)])
+def test_decode_resident_edge_shapes(over, renorm):
+    """The FFN's in-kernel gating at its edges: E not a multiple of 4 (padded
+    keys), B*E = 256 (the largest routed in-kernel), renormalised weights.
+    Selections, outputs and hit counts as in the oracle; the capped run (router
+    tail kernel) gives bit-identical outputs."""
+    from gpuhelp import rel_l2
+    from oracle.stmoe_oracle import MODE_STMOE
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["tiny"].scaled(**over)
+    st = Stack(cfg)
+    ref = _oracle(st, MODE_STMOE, ffn_tokens=cfg.T, renorm=renorm)
+    assert ref["tie_boundary"] == 0
+    idx_hist, ys, stats, _ = _run_gpu(st, 1, capped=False, renorm=renorm)
+    for t in range(cfg.T):
+        for l in range(cfg.L):
+            r = ref["idx"][t * cfg.L + l]
+            for b in range(cfg.B):
+                assert sorted(idx_hist[t][l][b].tolist()) == sorted(r[b].tolist())
+            assert rel_l2(ys[t][l], ref["y"][(t, l)]) <= 1e-2
+    assert np.array_equal(stats[:, 0], ref["hits"].sum(axis=0))
+    assert np.array_equal(stats[:, 2], ref["npred"].sum(axis=0))
+    _, ys_cap, _, _ = _run_gpu(st, 1, capped=True, renorm=renorm)
+    for t in range(cfg.T):
+        assert np.array_equal(ys_cap[t], ys[t]), t
 
 
 @pytest.mark.parametrize("name,over,mode", [("tiny", dict(T=8), 2), ("tiny", dict(T=8), 3),
@@ -217,3 +250,26 @@ def test_decode_graph_replay_matches_eager(name, over, timing, staged):
         assert np.array_equal(ys_graph[t], ys_eager[t]), t
     assert np.array_equal(idx_last, idx_hist[-1])
     assert np.array_equal(stats_graph, stats_eager)
+
+
+@pytest.mark.parametrize("name,over,capped", [("tiny", dict(T=8), False), ("qwen30b", dict(L=3, T=4, P=2, C=10), False),
+                                              ("qwen30b", dict(L=3, T=4, P=2, C=10), True)])
+def test_decode_online_update_off(name, over, capped):
+    """With the online update off the CCTs stay as profiled, HT still tracks
+    the selections, and the hit counts follow the oracle run the same way
+    (side-stream path without a cache, fused router tail with one)."""
+    from oracle.stmoe_oracle import MODE_STMOE, STPredictor
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    ref = _oracle(st, MODE_STMOE, C=cfg.C if capped else None, online=False)
+    tables = []
+    idx_hist, _, stats, cst = _run_gpu(st, 1, capped=capped, online=False, tables=tables)
+    assert np.array_equal(stats[:, 0], ref["hits"].sum(axis=0))
+    assert np.array_equal(stats[:, 2], ref["npred"].sum(axis=0))
+    prof = STPredictor(cfg.L, cfg.E, cfg.K, cfg.B)
+    prof.profile(st.prof)
+    _, ci, cc, _ = prof.tables()
+    _, gci, gcc, _ = tables[0]
+    assert np.array_equal(gci, ci) and np.array_equal(gcc, cc)
+

@@ -45,6 +45,8 @@ constexpr int kMaxSlots = kMaxE + kMaxShared;
 constexpr int kDownWgTarget = 256;    // workgroups the MFMA down phase aims for
 constexpr int kMfmaMinB = 8;          // batch from which the MFMA kernels run
 constexpr int kUpInFlight = 2;        // 16-byte chunks per row in flight per lane (GEMV gate/up)
+constexpr bool kStageX = true;        // GEMV gate/up: token activations staged in LDS ...
+constexpr int kXStageMax = 32768;     // ... when B*H*esz fits in this many bytes
 constexpr int kDownInFlight = 2;      // ... per row per lane in the whole-workgroup down kernel
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -231,10 +233,34 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 // GEMV path (batch < 8)
 // ============================================================================
 
-template <bool BF, int G, int R, int NB>
+// XL: the B token rows of x are staged in LDS (dynamic shared memory of
+// B*H*esz bytes) by the whole workgroup, their loads issued before the
+// routing prologue so both latencies overlap; every wave then reads x from
+// LDS instead of L1/L2.
+template <bool BF, int G, int R, int NB, bool XL>
 __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_per_slot) {
     __shared__ Plan p;
+    extern __shared__ uint4 x_lds[];
+    constexpr int esz = BF ? 2 : 4;
+    constexpr int kXRegs = kXStageMax / 16 / kThreads;
+    const int nx = XL ? a.B * a.H * esz / 16 : 0;
+    uint4 xr[kXRegs];
+    if (XL) {
+#pragma unroll
+        for (int u = 0; u < kXRegs; ++u) {
+            const int i = u * kThreads + int(threadIdx.x);
+            if (i < nx) xr[u] = ld_cached(reinterpret_cast<const char*>(a.x) + size_t(i) * 16);
+        }
+    }
     build_plan(a, p, true);
+    if (XL) {
+#pragma unroll
+        for (int u = 0; u < kXRegs; ++u) {
+            const int i = u * kThreads + int(threadIdx.x);
+            if (i < nx) x_lds[i] = xr[u];
+        }
+        __syncthreads();
+    }
     const int j = blockIdx.x / blocks_per_slot;
     if (j >= p.n_slots) return;
     const int rows_per_block = kWaves * (64 / G) * R;
@@ -243,7 +269,6 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
     const int i0 = (blockIdx.x % blocks_per_slot) * rows_per_block + (wave * (64 / G) + grp) * R;
     if (i0 >= a.I) return;   // I is a multiple of R: the group's rows are all valid
     const unsigned tm = p.tok[j];
-    constexpr int esz = BF ? 2 : 4;
     const size_t rowb = size_t(a.H) * esz;
     const char* blob = slot_blob(a, p, j);
     const char* wg = blob + size_t(i0) * rowb;
@@ -265,7 +290,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
         for (int b = 0; b < NB; ++b) {
             if (!((tm >> b) & 1u)) continue;
             Chunk<BF> cx;
-            cx.unpack(ld_cached(xs + b * rowb + size_t(c) * 16));
+            cx.unpack(XL ? x_lds[b * cpr + c] : ld_cached(xs + b * rowb + size_t(c) * 16));
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 accg[r][b] = dotc<BF>(cg[r], cx, accg[r][b]);
@@ -902,8 +927,13 @@ template <bool BF, int G, int NB, int R>
 int launch_gate_up_r(const FfnArgs& a, const Shape& s, hipStream_t st) {
     const int rows = kWaves * (64 / G) * R;
     const int bps = (a.I + rows - 1) / rows;
-    hipLaunchKernelGGL((ffn_gate_up<BF, G, R, NB>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a,
-                       bps);
+    const size_t xbytes = size_t(a.B) * a.H * (BF ? 2 : 4);
+    if (kStageX && xbytes <= size_t(kXStageMax))
+        hipLaunchKernelGGL((ffn_gate_up<BF, G, R, NB, true>), dim3(unsigned(bps * s.slots)), dim3(kThreads),
+                           unsigned(xbytes), st, a, bps);
+    else
+        hipLaunchKernelGGL((ffn_gate_up<BF, G, R, NB, false>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0,
+                           st, a, bps);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }

@@ -56,6 +56,8 @@ def parse():
                     help="at most this many decode tokens of the CPU oracle sample (0 skips it)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="the CPU oracle sample stops after the token that reaches this much timed work")
+    ap.add_argument("--offload-only", default=None, metavar="VARIANT",
+                    help="run only this capped-cache variant (for traces)")
     ap.add_argument("--offload-sweep", default=None, metavar="C1,C2,...",
                     help="capped-cache sweep over these per-layer budgets (markdown table; no JSON line)")
     ap.add_argument("--counters", action="store_true",
@@ -67,6 +69,8 @@ def parse():
                     help="time moe_expert_ffn on every config shape (markdown table on stdout) and exit")
     ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_CSV", "TITLE", "COMMAND"),
                     help="print a markdown table of a rocprofv3 kernel_stats.csv and exit")
+    ap.add_argument("--summarize-overlap", nargs=2, metavar=("KERNEL_CSV", "COPY_CSV"),
+                    help="copy/compute overlap of the capped-cache runs in a rocprofv3 trace")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the markdown counter summary of two rocprofv3 --pmc runs and exit")
     return ap.parse_args()
@@ -170,6 +174,73 @@ def summarize_counters(fetch_csv, write_csv):
         f"expert_ffn_source_sha: {ffn_source_sha()}",
     ]
     print("\n".join(out))
+
+
+def _union(iv):
+    """Merge intervals [(s, e)] into disjoint sorted ones."""
+    out = []
+    for s_, e_ in sorted(iv):
+        if out and s_ <= out[-1][1]:
+            out[-1][1] = max(out[-1][1], e_)
+        else:
+            out.append([s_, e_])
+    return out
+
+
+def _intersect_len(a, b):
+    """Total length of the intersection of two disjoint sorted interval lists."""
+    i = j = 0
+    tot = 0
+    while i < len(a) and j < len(b):
+        lo, hi = max(a[i][0], b[j][0]), min(a[i][1], b[j][1])
+        if hi > lo:
+            tot += hi - lo
+        if a[i][1] < b[j][1]:
+            i += 1
+        else:
+            j += 1
+    return tot
+
+
+def summarize_overlap(kernel_csv, copy_csv):
+    """Copy/compute overlap per capped-cache run of a rocprofv3 trace.
+
+    A run is a cluster of routing launches (gaps under 300 ms); its window runs
+    from its first routing launch to its last kernel, so the cache warm-up
+    copies before it are excluded.  Expert copies are the host-to-device
+    copies longer than 1 ms.  Overlap = time an expert copy is in flight while
+    an FFN kernel runs, over the time any expert copy is in flight."""
+    import csv
+    ks = [(r["Kernel_Name"], int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+          for r in csv.DictReader(open(kernel_csv)) if "stmoe" in r["Kernel_Name"]]
+    cs = [(int(r["Start_Timestamp"]), int(r["End_Timestamp"])) for r in csv.DictReader(open(copy_csv))
+          if r["Direction"].endswith("HOST_TO_DEVICE")]
+    cs = [c for c in cs if c[1] - c[0] > 1_000_000]
+    routes = sorted(s_ for n, s_, e_ in ks if "route" in n)
+    runs, cur = [], []
+    for t in routes:
+        if cur and t - cur[-1] > 300_000_000:
+            runs.append(cur)
+            cur = []
+        cur.append(t)
+    if cur:
+        runs.append(cur)
+    print("| run | window ms | expert copies | copy busy ms | FFN busy ms | copy time overlapped by FFN | "
+          "FFN time overlapped by copies |")
+    print("|---|---|---|---|---|---|---|")
+    for n_run, r in enumerate(runs):
+        w0 = r[0]
+        w1 = max(e_ for n, s_, e_ in ks if s_ >= w0 and s_ <= r[-1] + 300_000_000)
+        cp = _union([(max(a, w0), min(b, w1)) for a, b in cs if b > w0 and a < w1])
+        if not cp:
+            continue
+        ffn = _union([(s_, e_) for n, s_, e_ in ks if "ffn_" in n and e_ > w0 and s_ < w1])
+        cbusy = sum(b - a for a, b in cp)
+        fbusy = sum(b - a for a, b in ffn)
+        ov = _intersect_len(cp, ffn)
+        n_cp = sum(1 for a, b in cs if a >= w0 and a < w1)
+        print(f"| {n_run} | {(w1 - w0) / 1e6:.1f} | {n_cp} | {cbusy / 1e6:.1f} | {fbusy / 1e6:.1f} | "
+              f"{ov / max(cbusy, 1):.3f} | {ov / max(fbusy, 1):.3f} |")
 
 
 def summarize_stats(path, title, cmd):
@@ -526,7 +597,7 @@ def offload_variants(cfg):
             ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C, 1)]
 
 
-def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
+def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
     """Capped HBM cache over a pinned host pool: on-demand vs ST-MoE prefetch."""
     import torch
     from paper_2606_15453_amd import stmoe as S
@@ -536,7 +607,7 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb):
     arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
                         device="cuda:0")
     streams = (torch.cuda.Stream(), torch.cuda.Stream())
-    variants = offload_variants(cfg)
+    variants = [v for v in offload_variants(cfg) if only is None or v[0] in (only, "on_demand")]
     out = {}
     for v in variants:
         out[v[0]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)
@@ -680,6 +751,9 @@ def main():
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
         return
+    if args.summarize_overlap:
+        summarize_overlap(*args.summarize_overlap)
+        return
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats)
         return
@@ -775,7 +849,7 @@ def main():
     out["roofline"]["frac_of_achievable_read"] = round(up_gbps / read_gbps, 4)
     log(f"streaming-read probe: {read_gbps:.0f} GB/s")
     if args.offload_tokens > 0:
-        out["offload"] = offload(wl, args.offload_tokens, ms_per_step, args.pinned_gb)
+        out["offload"] = offload(wl, args.offload_tokens, ms_per_step, args.pinned_gb, args.offload_only)
     if args.cpu_tokens > 0:
         t0 = time.time()
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens, args.cpu_seconds)

@@ -279,7 +279,10 @@ typedef struct {
 
 typedef struct moe_ctx moe_ctx;
 
-/* cache may be NULL only when desc->resident_w is given. */
+/* cache may be NULL only when desc->resident_w is given.  pred (if given)
+ * and cache must have been created for the same L, E (and, for pred, K and
+ * B) as desc, and the cache's blob size must hold one expert
+ * (moe_blob_bytes(H, I, dtype)); otherwise STMOE_EINVAL. */
 int moe_ctx_create(const moe_model_desc* desc, stmoe_predictor* pred, expert_cache* cache,
                    void* compute_stream, moe_ctx** out);
 int moe_ctx_destroy(moe_ctx* ctx);

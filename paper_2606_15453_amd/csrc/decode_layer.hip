@@ -23,6 +23,8 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
                float* y, void* ws, hipStream_t s, unsigned long long* n_experts, hipEvent_t ev_mid,
                const float* logits, int renorm);
 int route_logits(const void* x, const void* w_gate, int B, int H, int E, int dtype, float* z, hipStream_t s);
+void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_bytes);
+void stmoe_shape(const stmoe_predictor* p, int* L, int* E, int* K, int* B);
 int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int renorm, int32_t* idx,
                         float* w, void* route_ws, stmoe_predictor* p, int layer, const int32_t* sel_prev,
                         int use, int online, int32_t* ranked, int32_t* n_ranked, uint8_t* max_score,
@@ -213,6 +215,19 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     STMOE_CHECK((cache == nullptr) != (d->resident_w == nullptr),
                 "give exactly one of a cache or resident expert pointers");
     for (int l = 0; l < d->L; ++l) STMOE_CHECK(d->router_w[l], "null router pointer");
+    if (pred) {
+        int pL, pE, pK, pB;
+        stmoe_shape(pred, &pL, &pE, &pK, &pB);
+        STMOE_CHECK(pL == d->L && pE == d->E && pK == d->K && pB == d->B,
+                    "the predictor was created for another L/E/K/B");
+    }
+    if (cache) {
+        int cL, cE;
+        size_t cblob;
+        expert_cache_shape(cache, &cL, &cE, &cblob);
+        STMOE_CHECK(cL == d->L && cE == d->E, "the cache was created for another L/E");
+        STMOE_CHECK(cblob >= moe_blob_bytes(d->H, d->I, d->dtype), "the cache's blobs are smaller than an expert");
+    }
     auto* c = new moe_ctx();
     c->L = d->L; c->E = d->E; c->K = d->K; c->B = d->B; c->H = d->H; c->I = d->I;
     c->n_shared = d->n_shared; c->dtype = d->dtype; c->renorm = d->renorm;
@@ -582,7 +597,8 @@ extern "C" int moe_ctx_set_timing(moe_ctx* c, int every) {
     clear_error();
     STMOE_CHECK(c, "null ctx");
     STMOE_CHECK(every >= 0, "every must be >= 0");
-    STMOE_HIP(hipStreamSynchronize(c->s));
+    // the side stream may still have to record events of earlier timed layers
+    STMOE_HIP(hipDeviceSynchronize());
     c->timing_every = every;
     c->ev_used = 0;
     c->n_calls = 0;

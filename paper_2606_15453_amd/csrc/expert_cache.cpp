@@ -207,6 +207,16 @@ struct expert_cache {
 };
 
 namespace stmoe {
+// Internal: the shape a cache was created with (checked by moe_ctx_create).
+void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_bytes) {
+    *L = c->L;
+    *E = c->E;
+    *blob_bytes = c->blob;
+}
+}  // namespace stmoe
+
+
+namespace stmoe {
 namespace {
 
 // Order a copy into slot `gid` on stream `s` after its previous copy and

@@ -676,6 +676,191 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int bloc
     }
 }
 
+// gate/up through LDS: each wave stages its rows (NT 16-row tiles of W_gate,
+// then the same of W_up) 128 elements at a time.  The loads read 256
+// contiguous bytes of a row per 16 lanes (four rows per instruction), which
+// streams better than loading the MFMA operand layout straight from HBM (16
+// rows x 64 bytes per instruction); the wave writes the segment to its own
+// padded LDS rows and reads the operands back in the layout of
+// v_mfma_f32_16x16x32_bf16 while the next segment's loads are in flight.
+// Waves never wait on each other (each owns its LDS region).
+constexpr int kLdsSegU4 = 16;         // 128 bf16 = 16 uint4 per row per step
+constexpr int kLdsPadU4 = 17;         // padded row stride in uint4: conflict-free reads
+
+// SK (split-K, NT = 1): the workgroup's four waves share the same 16 rows
+// and each covers a quarter of the hidden dimension; the partial tiles add
+// up in LDS (for shapes whose row count alone gives too few workgroups).
+template <int NT, bool SK>
+__global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma_lds(FfnArgs a, int blocks_per_slot) {
+    static_assert(!SK || NT == 1, "split-K runs one tile per wave");
+    __shared__ Plan p;
+    __shared__ float red[SK ? kWaves : 1][2][64][4];
+    extern __shared__ uint4 stage[];
+    build_plan(a, p, true);
+    const int j = blockIdx.x / blocks_per_slot;
+    if (j >= p.n_slots) return;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n = lane & 15, q = lane >> 4;
+    const int i0 = SK ? (blockIdx.x % blocks_per_slot) * 16
+                      : (blockIdx.x % blocks_per_slot) * (kWaves * NT * 16) + wave * NT * 16;
+    if (!SK && i0 >= a.I) return;   // I is a multiple of 16
+    constexpr int kRows = 2 * NT * 16;       // staged rows per wave: gate tiles, then up tiles
+    constexpr int kLoads = kRows / 4;        // load instructions per step (four rows each)
+    const int h_lo = SK ? wave * (a.H / kWaves) : 0;           // SK: H is a multiple of 512
+    const int h_hi = SK ? h_lo + a.H / kWaves : a.H;
+    const unsigned tm = p.tok[j];
+    const size_t rowb = size_t(a.H) * 2;
+    const char* blob = slot_blob(a, p, j);
+    uint4* my = stage + size_t(wave) * kRows * kLdsPadU4;
+    // loader mapping: lane (g, e) loads uint4 e of the segment of row 4r + g
+    const int g = lane >> 4, e = lane & 15;
+    const char* src[kLoads];
+#pragma unroll
+    for (int r = 0; r < kLoads; ++r) {
+        const int rr = 4 * r + g, m = rr / (NT * 16), t = rr % (NT * 16);
+        src[r] = blob + size_t(m * a.I + i0 + t) * rowb + size_t(h_lo + 8 * e) * 2;
+    }
+    const bool xrow = n < a.B;     // A operand row n = token n
+    const char* xs = reinterpret_cast<const char*>(a.x) + size_t(xrow ? n : 0) * rowb + q * 16;
+    const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    f32x4 dg[NT], du[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) dg[t] = du[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    uint4 ld[kLoads];
+#pragma unroll
+    for (int r = 0; r < kLoads; ++r) ld[r] = ld_stream(src[r]);
+    for (int h = h_lo; h < h_hi; h += 128) {
+        // the previous step's operand reads are done before its rows are overwritten
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int r = 0; r < kLoads; ++r) my[(4 * r + g) * kLdsPadU4 + e] = ld[r];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (h + 128 < h_hi) {
+            const size_t o = size_t(h + 128 - h_lo) * 2;
+#pragma unroll
+            for (int r = 0; r < kLoads; ++r) ld[r] = ld_stream(src[r] + o);
+        }
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            const size_t ox = size_t(h + 32 * kb) * 2;
+            const bf16x8 xv = xrow ? ld_bf8(xs + ox) : zero;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const bf16x8 gv = __builtin_bit_cast(bf16x8, my[(t * 16 + n) * kLdsPadU4 + kb * 4 + q]);
+                const bf16x8 uv = __builtin_bit_cast(bf16x8, my[((NT + t) * 16 + n) * kLdsPadU4 + kb * 4 + q]);
+                dg[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv, gv, dg[t], 0, 0, 0);
+                du[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv, uv, du[t], 0, 0, 0);
+            }
+        }
+    }
+    if (SK) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            red[SK ? wave : 0][0][lane][r] = dg[0][r];
+            red[SK ? wave : 0][1][lane][r] = du[0][r];
+        }
+        __syncthreads();
+        if (wave != 0) return;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float gs = 0.f, us = 0.f;
+#pragma unroll
+            for (int w = 0; w < (SK ? kWaves : 1); ++w) { gs += red[w][0][lane][r]; us += red[w][1][lane][r]; }
+            dg[0][r] = gs;
+            du[0][r] = us;
+        }
+    }
+    // D layout: lane holds rows m = 4q + r (tokens) of column n (weight row)
+    uint16_t* act = reinterpret_cast<uint16_t*>(a.act) + size_t(j) * a.B * a.I;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int b = 4 * q + r;
+        if (b >= a.B) continue;
+        const bool routed = (tm >> b) & 1u;
+        const float wb = routed ? slot_weight(a, p, j, b) : 0.f;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const float v = routed ? wb * silu(dg[t][r]) * du[t][r] : 0.f;
+            act[size_t(b) * a.I + i0 + t * 16 + n] = f32_to_bf16_rne(v);
+        }
+    }
+}
+
+// down through LDS: as the gate/up kernel, with W_down rows (length I) as the
+// staged operand and the slot's bf16 activations as the A operand, summing
+// the slots of the workgroup's group.
+template <int NT>
+__global__ __launch_bounds__(kThreads) void ffn_down_mfma_lds(FfnArgs a) {
+    __shared__ Plan p;
+    extern __shared__ uint4 stage[];
+    build_plan(a, p);
+    const int rb = blockIdx.x / a.ng, grp = blockIdx.x % a.ng;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n = lane & 15, q = lane >> 4;
+    const int rows_per_block = kWaves * NT * 16;
+    const int h0 = rb * rows_per_block + wave * NT * 16;
+    if (blockIdx.x == 0 && threadIdx.x == 0 && a.n_experts)
+        atomicAdd(a.n_experts, (unsigned long long)p.n_routed);
+    const bool live = h0 < a.H;   // H is a multiple of 64 * NT
+    constexpr int kRows = NT * 16;
+    constexpr int kLoads = kRows / 4;
+    const size_t rowb = size_t(a.I) * 2;
+    const bool arow = n < a.B;
+    const int g = lane >> 4, e = lane & 15;
+    uint4* my = stage + size_t(wave) * kRows * kLdsPadU4;
+    // the selected slots split evenly over the groups (an empty group writes zeros)
+    const int j0 = grp * p.n_slots / a.ng, j1 = (grp + 1) * p.n_slots / a.ng;
+    f32x4 d[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) d[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    for (int j = j0; live && j < j1; ++j) {
+        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * 2;
+        const char* src[kLoads];
+#pragma unroll
+        for (int r = 0; r < kLoads; ++r) src[r] = wd + size_t(h0 + 4 * r + g) * rowb + size_t(e) * 16;
+        const char* ar = reinterpret_cast<const char*>(a.act) +
+                         (size_t(j) * a.B + (arow ? n : 0)) * rowb + q * 16;
+        uint4 ld[kLoads];
+#pragma unroll
+        for (int r = 0; r < kLoads; ++r) ld[r] = ld_stream(src[r]);
+        for (int k = 0; k < a.I; k += 128) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int r = 0; r < kLoads; ++r) my[(4 * r + g) * kLdsPadU4 + e] = ld[r];
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            if (k + 128 < a.I) {
+                const size_t o = size_t(k + 128) * 2;
+#pragma unroll
+                for (int r = 0; r < kLoads; ++r) ld[r] = ld_stream(src[r] + o);
+            }
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                const bf16x8 av = arow ? ld_bf8(ar + size_t(k + 32 * kb) * 2) : zero;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const bf16x8 wv = __builtin_bit_cast(bf16x8, my[(t * 16 + n) * kLdsPadU4 + kb * 4 + q]);
+                    d[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, wv, d[t], 0, 0, 0);
+                }
+            }
+        }
+    }
+    float* out = a.ng == 1 ? a.y : a.part + size_t(grp) * a.B * a.H;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int b = 4 * q + r;
+        if (!live || b >= a.B) continue;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) out[size_t(b) * a.H + h0 + t * 16 + n] = d[t][r];
+    }
+}
+
 // gate/up, split-K: one workgroup = 16 rows of one slot; wave w covers the
 // w-th quarter of the hidden dimension and the four partial tiles add up in
 // LDS (for shapes whose row count alone gives too few workgroups).
@@ -873,6 +1058,9 @@ constexpr int kDownForceG = 0;  // lanes per down row (0: by row length)
 constexpr int kMfmaNT = 0;      // 1: force one 16-row tile per wave in the MFMA gate/up kernel
 constexpr int kMfmaDownNT = 4;  // 16-row tiles per wave of the MFMA down kernel (1, 2 or 4)
 constexpr int kMfmaSplitKBelow = 2048;  // split-K MFMA gate/up when the tiled grid has fewer workgroups
+constexpr bool kMfmaUpLds = true;       // MFMA gate/up stages weight rows through LDS (H % 128 == 0;
+                                        // split-K: H % 512 == 0)
+constexpr bool kMfmaDownLds = true;     // MFMA down stages W_down rows through LDS (I % 128 == 0)
 constexpr int kUpWgMinChunks = 512;   // ... used when a row has at least this many chunks
 
 Shape plan_shape(int B, int K, int H, int I, int E, int n_shared, int dtype) {
@@ -996,23 +1184,49 @@ int launch_mfma(const FfnArgs& a, const Shape& s, hipStream_t st, hipEvent_t ev_
     const int rows = kWaves * NT * 16;
     if ((a.I / (kWaves * 16)) * s.slots < kMfmaSplitKBelow && a.H % 256 == 0) {
         const int bps = a.I / 16;
-        hipLaunchKernelGGL(ffn_gate_up_mfma_sk, dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
+        if (kMfmaUpLds && a.H % 512 == 0) {
+            const unsigned lds = unsigned(kWaves * 2 * 16 * kLdsPadU4 * sizeof(uint4));
+            hipLaunchKernelGGL((ffn_gate_up_mfma_lds<1, true>), dim3(unsigned(bps * s.slots)), dim3(kThreads), lds,
+                               st, a, bps);
+        } else {
+            hipLaunchKernelGGL(ffn_gate_up_mfma_sk, dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
+        }
     } else if (a.I % rows != 0 || (a.I / rows) * s.slots < 1024 || kMfmaNT == 1) {
         const int bps = a.I / (kWaves * 16);
-        hipLaunchKernelGGL((ffn_gate_up_mfma<1>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
+        if (kMfmaUpLds && a.H % 128 == 0) {
+            const unsigned lds = unsigned(kWaves * 2 * 16 * kLdsPadU4 * sizeof(uint4));
+            hipLaunchKernelGGL((ffn_gate_up_mfma_lds<1, false>), dim3(unsigned(bps * s.slots)), dim3(kThreads), lds, st,
+                               a, bps);
+        } else {
+            hipLaunchKernelGGL((ffn_gate_up_mfma<1>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a,
+                               bps);
+        }
     } else {
         const int bps = a.I / rows;
-        hipLaunchKernelGGL((ffn_gate_up_mfma<NT>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a, bps);
+        if (kMfmaUpLds && a.H % 128 == 0) {
+            const unsigned lds = unsigned(kWaves * 2 * NT * 16 * kLdsPadU4 * sizeof(uint4));
+            hipLaunchKernelGGL((ffn_gate_up_mfma_lds<NT, false>), dim3(unsigned(bps * s.slots)), dim3(kThreads), lds, st,
+                               a, bps);
+        } else {
+            hipLaunchKernelGGL((ffn_gate_up_mfma<NT>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a,
+                               bps);
+        }
     }
     STMOE_LAUNCHED();
     if (ev_mid) STMOE_HIP(hipEventRecord(ev_mid, st));
     const dim3 dgrid(unsigned(s.n_rb * s.ng));
-    if (s.dn_nt == 4)
-        hipLaunchKernelGGL((ffn_down_mfma<4>), dgrid, dim3(kThreads), 0, st, a);
-    else if (s.dn_nt == 2)
-        hipLaunchKernelGGL((ffn_down_mfma<2>), dgrid, dim3(kThreads), 0, st, a);
-    else
-        hipLaunchKernelGGL((ffn_down_mfma<1>), dgrid, dim3(kThreads), 0, st, a);
+    const unsigned dlds = unsigned(kWaves * s.dn_nt * 16 * kLdsPadU4 * sizeof(uint4));
+    const bool dn_lds = kMfmaDownLds && a.I % 128 == 0;
+    if (s.dn_nt == 4) {
+        if (dn_lds) hipLaunchKernelGGL((ffn_down_mfma_lds<4>), dgrid, dim3(kThreads), dlds, st, a);
+        else hipLaunchKernelGGL((ffn_down_mfma<4>), dgrid, dim3(kThreads), 0, st, a);
+    } else if (s.dn_nt == 2) {
+        if (dn_lds) hipLaunchKernelGGL((ffn_down_mfma_lds<2>), dgrid, dim3(kThreads), dlds, st, a);
+        else hipLaunchKernelGGL((ffn_down_mfma<2>), dgrid, dim3(kThreads), 0, st, a);
+    } else {
+        if (dn_lds) hipLaunchKernelGGL((ffn_down_mfma_lds<1>), dgrid, dim3(kThreads), dlds, st, a);
+        else hipLaunchKernelGGL((ffn_down_mfma<1>), dgrid, dim3(kThreads), 0, st, a);
+    }
     STMOE_LAUNCHED();
     if (s.ng > 1) {
         const int n4 = a.B * a.H / 4;   // H is a multiple of 64

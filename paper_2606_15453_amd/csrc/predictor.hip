@@ -372,3 +372,13 @@ int update_predict(stmoe_predictor* p, int layer, const int32_t* sel_prev, const
     return STMOE_OK;
 }
 }  // namespace stmoe
+
+namespace stmoe {
+// Internal: the shape a predictor was created with (checked by moe_ctx_create).
+void stmoe_shape(const stmoe_predictor* p, int* L, int* E, int* K, int* B) {
+    *L = p->L;
+    *E = p->E;
+    *K = p->K;
+    *B = p->B;
+}
+}  // namespace stmoe

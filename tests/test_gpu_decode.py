@@ -273,3 +273,22 @@ def test_decode_online_update_off(name, over, capped):
     _, gci, gcc, _ = tables[0]
     assert np.array_equal(gci, ci) and np.array_equal(gcc, cc)
 
+
+
+def test_ctx_rejects_mismatched_predictor():
+    """A predictor made for another shape is refused before any device work."""
+    import torch
+    from gpuhelp import DEV, storage_dtype
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["tiny"]
+    st = Stack(cfg.scaled(T=2, P=2))
+    resident = [st.blobs[l][e].data_ptr() for l in range(cfg.L) for e in range(cfg.E)]
+    for shape in [(cfg.L, cfg.E * 2, cfg.K, cfg.B), (cfg.L + 1, cfg.E, cfg.K, cfg.B),
+                  (cfg.L, cfg.E, cfg.K, cfg.B + 1)]:
+        pred = S.Predictor(*shape)
+        with pytest.raises(S.StmoeError):
+            S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
+                            [g.data_ptr() for g in st.wg_dev], predictor=pred, resident_ptrs=resident,
+                            stream=torch.cuda.current_stream())
+        pred.close()

@@ -54,6 +54,20 @@ def test_ffn_parity(name, B):
     assert err <= TOL
 
 
+@pytest.mark.parametrize("H,I", [(4096, 1536), (4096, 1472), (4032, 1536)])
+def test_ffn_mfma_tiled_shapes(H, I):
+    """Batch 16 over 128 experts takes the tiled MFMA gate/up: through LDS with
+    two 16-row tiles per wave (H % 128 == 0, I % 128 == 0), with one tile
+    (I % 128 != 0), and the direct-load kernel (H % 128 != 0)."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen235b"].scaled(H=H, I=I, B=16)
+    idx, w, x = _inputs(cfg, 16, cfg.K, seed=H + I)
+    got, ref, err = _run_ffn(cfg, 2, idx, w, x)
+    print(f"H={H} I={I}: rel L2 {err:.3e}")
+    assert np.isfinite(got).all()
+    assert err <= TOL
+
+
 def test_ffn_parity_mixtral_shape():
     """Full Mixtral-8x7B expert shape (H 4096, I 14336), batch 1, top-2."""
     from paper_2606_15453_amd import workload as W

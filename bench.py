@@ -58,6 +58,8 @@ def parse():
                     help="the CPU oracle sample stops after the token that reaches this much timed work")
     ap.add_argument("--offload-only", default=None, metavar="VARIANT",
                     help="run only this capped-cache variant (for traces)")
+    ap.add_argument("--attention-sweep", default=None, metavar="CTX1,CTX2,...",
+                    help="capped cache with a decode-attention stand-in of these context lengths (markdown)")
     ap.add_argument("--offload-sweep", default=None, metavar="C1,C2,...",
                     help="capped-cache sweep over these per-layer budgets (markdown table; no JSON line)")
     ap.add_argument("--counters", action="store_true",
@@ -528,10 +530,12 @@ def host_pool(wl, pinned_gb):
     return pool, ptrs, M
 
 
-def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_token):
+def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_token, attn=None):
     """One capped-cache decode run: C slots per layer, the rest streamed from
     the pinned host pool.  variant = (name, mode, min score, max prefetches
-    per layer, online CCT update)."""
+    per layer, online CCT update).  attn = (kv buffer, bytes, out): a decode-
+    attention stand-in that streams `bytes` of KV cache on the compute stream
+    before every MoE layer (layers are then issued one by one)."""
     import torch
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
@@ -550,7 +554,15 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
     ctx.set_timing(1)       # events on every layer: negligible next to ms-scale copies
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run_tokens(ctx, wl, 0, n_tokens, y, mode)
+    if attn is None:
+        run_tokens(ctx, wl, 0, n_tokens, y, mode)
+    else:
+        kv, nbytes, out = attn
+        T = cfg.T
+        for t in range(n_tokens):
+            for l in range(cfg.L):
+                S.calib_read(kv, nbytes, out)
+                ctx.layer(t, l, wl.x[t % T][l], y[l], mode)
     torch.cuda.synchronize()
     demand.synchronize()
     side.synchronize()
@@ -620,6 +632,63 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
     del arena
     del pool
     return out
+
+
+# KV-cache bytes per context token per layer (K and V, bf16) of the models
+# whose expert shapes the configs use: grouped-query attention with 8 KV heads
+# of 128 (Mixtral-8x7B), 4 of 128 (Qwen3-30B-A3B), 4 of 128 (Qwen3-235B-A22B),
+# and DeepSeek-V2-Lite's compressed latent (512 + 64 rope dims, one head).
+KV_BYTES_PER_TOKEN = {"mixtral": 2 * 8 * 128 * 2, "qwen30b": 2 * 4 * 128 * 2, "qwen30b-b8": 2 * 4 * 128 * 2,
+                      "qwen235b": 2 * 4 * 128 * 2, "dsv2lite": (512 + 64) * 2, "tiny": 2 * 2 * 64 * 4}
+
+
+def attention_sweep(wl, key, n_tokens, resident_ms_per_token, pinned_gb, contexts):
+    """Capped cache with a decode-attention stand-in between MoE layers: the
+    prefetch issued after layer l overlaps layer l+1's attention.  Returns
+    markdown lines."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    cfg = wl.cfg
+    pool, ptrs, M = host_pool(wl, pinned_gb)
+    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
+    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
+                        device="cuda:0")
+    streams = (torch.cuda.Stream(), torch.cuda.Stream())
+    per_tok = KV_BYTES_PER_TOKEN[key] * cfg.B
+    rows = []
+    for ctx_len in contexts:
+        nbytes = (ctx_len * per_tok + 4095) // 4096 * 4096
+        attn = None
+        attn_us = 0.0
+        if nbytes:
+            kv = torch.zeros(nbytes, dtype=torch.uint8, device="cuda:0")
+            out = torch.empty(S.calib_read_out_words(nbytes), dtype=torch.int32, device="cuda:0")
+            attn = (kv, nbytes, out)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            S.calib_read(kv, nbytes, out)
+            e0.record()
+            for _ in range(20):
+                S.calib_read(kv, nbytes, out)
+            e1.record()
+            torch.cuda.synchronize()
+            attn_us = e0.elapsed_time(e1) * 1e3 / 20
+        base_ms = resident_ms_per_token + attn_us * cfg.L / 1e3
+        recs = {}
+        for v in offload_variants(cfg):
+            if v[0] not in ("on_demand", "st_moe", "st_moe_score4_maxK", "ht_only"):
+                continue
+            recs[v[0]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, base_ms, attn)
+        od = recs["on_demand"]["stall_ms_per_token"]
+        for name, rec in recs.items():
+            red = 1.0 - rec["stall_ms_per_token"] / od if od > 0 else float("nan")
+            rows.append(f"| {ctx_len} | {nbytes / 1e6:.1f} | {attn_us:.1f} | {name} | {rec['tokens_per_s']} | "
+                        f"{rec['ms_per_token']} | {rec['stall_ms_per_token']} | {red:+.3f} |")
+    del arena
+    del pool
+    head = ["| context tokens | KV MB per layer | attention stand-in us per layer | variant | tokens/s | "
+            "ms/token | stall ms/token (beyond resident + attention) | stall reduction vs on-demand |",
+            "|---|---|---|---|---|---|---|---|"]
+    return head + rows
 
 
 def offload_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, budgets):
@@ -778,6 +847,14 @@ def main():
     cfg = W.CONFIGS[args.config]
     log(f"workload {cfg.name}")
     wl = Workload(cfg)
+    if args.attention_sweep:
+        contexts = [int(c) for c in args.attention_sweep.split(",")]
+        r = hbm_resident(wl, 40, 5)
+        res_ms = 1e3 * r["seconds"] / 40
+        lines = attention_sweep(wl, args.config, max(args.offload_tokens, 1), res_ms, args.pinned_gb, contexts)
+        print(f"HBM-resident reference: {res_ms:.3f} ms/token; {max(args.offload_tokens, 1)} tokens per run")
+        print("\n".join(lines), flush=True)
+        return
     if args.offload_sweep:
         budgets = [int(c) for c in args.offload_sweep.split(",")]
         r = hbm_resident(wl, 40, 5)

@@ -32,6 +32,8 @@
 // Every kernel rebuilds the slot plan (distinct selected experts ascending,
 // token masks) from topk_idx/topk_w in LDS: no host round trip, no planning
 // launch.
+#include <type_traits>
+
 #include "common.h"
 #include "gating_dev.h"
 
@@ -80,6 +82,14 @@ struct Plan {
     int n_routed, n_slots;
 };
 
+// The plan of kernels whose waves walk many slots: each slot's blob pointer
+// is resolved once while the plan is built, so a slot's first weight loads
+// do not wait behind a table lookup.  Kernels that take one slot per
+// workgroup keep the smaller plan (LDS decides their occupancy).
+struct PlanB : Plan {
+    const char* blob[kMaxSlots];
+};
+
 // Gating (Section 2) inside a gate/up workgroup: the same steps and
 // arithmetic as the router tail, on rows of E rounded up to 4, into the
 // plan's idx/w; block 0 also publishes them.
@@ -112,7 +122,9 @@ __device__ void route_into_plan(const FfnArgs& a, Plan& p) {
 // Slot order: selected routed experts ascending, then shared experts.  With
 // `route` and router logits in the arguments the selection is computed here
 // (gate/up kernels); otherwise it is read from idx/w.
-__device__ void build_plan(const FfnArgs& a, Plan& p, bool route = false) {
+template <class P>
+__device__ void build_plan(const FfnArgs& a, P& p, bool route = false) {
+    constexpr bool kBlobs = std::is_same<P, PlanB>::value;
     const int tid = threadIdx.x;
     const int BK = a.B * a.K;
     if (route && a.logits) {
@@ -140,9 +152,11 @@ __device__ void build_plan(const FfnArgs& a, Plan& p, bool route = false) {
         for (int q = 0; q < (e >> 5); ++q) rank += __popc(p.sel[q]);
         atomicOr(&p.tok[rank], 1u << b);
         p.expert[rank] = e;
+        if constexpr (kBlobs) p.blob[rank] = reinterpret_cast<const char*>(a.eptr[e]);   // equal per rank
     }
     for (int s = tid; s < a.n_shared; s += kThreads) {
         p.expert[total + s] = -1 - s;
+        if constexpr (kBlobs) p.blob[total + s] = reinterpret_cast<const char*>(a.sptr[s]);
         p.tok[total + s] = (1u << a.B) - 1u;
     }
     if (tid == 0) {
@@ -165,6 +179,7 @@ __device__ __forceinline__ const char* slot_blob(const FfnArgs& a, const Plan& p
     const int e = p.expert[j];
     return reinterpret_cast<const char*>(e >= 0 ? a.eptr[e] : a.sptr[-1 - e]);
 }
+__device__ __forceinline__ const char* slot_blob(const FfnArgs&, const PlanB& p, int j) { return p.blob[j]; }
 
 template <bool BF>
 struct Chunk {
@@ -195,18 +210,27 @@ __device__ __forceinline__ float dotc(const Chunk<BF>& w, const Chunk<BF>& x, fl
     return acc;
 }
 
+// Weight rows are addressed through pointers read from memory (expert
+// tables, the slot plan), which the compiler cannot place in an address
+// space: loads through them would be FLAT instructions, which count against
+// the LDS wait counter too, so every LDS read behind them would wait for all
+// weight loads in flight.  They point into device memory: say so.
+typedef const __attribute__((address_space(1))) u32x4 gu32x4;
+__device__ __forceinline__ gu32x4* gmem(const char* p) { return (gu32x4*)(p); }
+
 __device__ __forceinline__ uint4 ld_stream(const char* p) {
-    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    const u32x4 v = __builtin_nontemporal_load(gmem(p));
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 __device__ __forceinline__ uint4 ld_cached(const char* p) {
-    return *reinterpret_cast<const uint4*>(p);
+    const u32x4 v = *gmem(p);
+    return make_uint4(v.x, v.y, v.z, v.w);
 }
 __device__ __forceinline__ bf16x8 ld_bf8_stream(const char* p) {
-    return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+    return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(gmem(p)));
 }
 __device__ __forceinline__ bf16x8 ld_bf8(const char* p) {
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
+    return __builtin_bit_cast(bf16x8, *gmem(p));
 }
 
 // Sum over a segment of G consecutive lanes (G = 16, 32 or 64); every lane
@@ -423,13 +447,16 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_wg(FfnArgs a, int blocks
     }
 }
 
-// Down, rows owned by lane groups (rows of at most 512 chunks): every wave
-// covers the workgroup's rows; the four waves split the slots (wave w takes
-// slots w, w+4, ...) and their sums are added in wave order through LDS.
+// Down, rows owned by lane groups: every wave covers the workgroup's rows
+// (R per lane group); the four waves split the slots (wave w takes slots w,
+// w+4, ...) and their sums are added in wave order through LDS.  Each
+// activation chunk a lane loads serves its R rows: the activations are fp32
+// and every workgroup reads all of them, so R sets how much L2 traffic the
+// weight rows carry along.
 template <bool BF, int G, int R, int NB>
 __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
     constexpr int kRows = (64 / G) * R;
-    __shared__ Plan p;
+    __shared__ PlanB p;
     __shared__ float red[kWaves][kRows][NB];
     build_plan(a, p);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -509,7 +536,7 @@ __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
 // through LDS.
 template <bool BF, int R, int NB>
 __global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
-    __shared__ Plan p;
+    __shared__ PlanB p;
     __shared__ float red[kWaves][R][NB];
     build_plan(a, p);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1048,10 +1075,10 @@ struct Shape {
     int n_rb;           // down row blocks
     int ng, spg;        // slot groups of the MFMA down phase
     int dn_nt;          // 16-row tiles per wave of the MFMA down kernel
+    int dn_R;           // rows per lane group of the GEMV down kernel
 };
 
-constexpr int kGemvR = 2;     // rows per lane group (GEMV gate/up)
-constexpr int kDownRowsR = 1; // rows per lane group (GEMV down, slots split over waves)
+constexpr int kDownRowsWgTarget = 1024;  // lane-group down: fewest workgroups more rows per group may leave
 constexpr int kDownWgR = 4;   // rows per workgroup (whole-workgroup down)
 constexpr int kUpWgR = 0;     // rows per workgroup of the whole-workgroup gate/up kernel (0: lane groups)
 constexpr int kDownForceG = 0;  // lanes per down row (0: by row length)
@@ -1085,7 +1112,14 @@ Shape plan_shape(int B, int K, int H, int I, int E, int n_shared, int dtype) {
         // 64 lanes per row once a row has 128 chunks: one row per wave pass
         // gives more workgroups than lane groups of 16 or 32
         s.dn_G = kDownForceG ? kDownForceG : (cpr_i >= 128 ? 64 : pick_group(cpr_i));
-        s.dn_rows = (64 / s.dn_G) * kDownRowsR;
+        // rows per lane group: as many as keep kDownRowsWgTarget workgroups
+        // (every workgroup re-reads all activations; more rows amortise them)
+        const int rmax = s.dn_G == 64 ? 4 : (s.dn_G == 32 ? 2 : 1);
+        s.dn_R = 1;
+        while (s.dn_R < rmax && H % ((64 / s.dn_G) * s.dn_R * 2) == 0 &&
+               H / ((64 / s.dn_G) * s.dn_R * 2) >= kDownRowsWgTarget)
+            s.dn_R *= 2;
+        s.dn_rows = (64 / s.dn_G) * s.dn_R;
     }
     s.n_rb = (H + s.dn_rows - 1) / s.dn_rows;
     if (s.mfma) {
@@ -1137,9 +1171,28 @@ int launch_gate_up(const FfnArgs& a, const Shape& s, hipStream_t st) {
             return STMOE_OK;
         }
     }
-    // long rows: one row per lane group gives more workgroups in flight
-    if (a.H * (BF ? 2 : 4) / 16 >= 512) return launch_gate_up_r<BF, G, NB, 1>(a, s, st);
-    return launch_gate_up_r<BF, G, NB, kGemvR>(a, s, st);
+    // every workgroup stages all token activations; from 4 token columns on
+    // two rows per lane group halve that traffic, below it one row per group
+    // gives more workgroups in flight (I is a multiple of 8)
+    if constexpr (NB >= 4) return launch_gate_up_r<BF, G, NB, 2>(a, s, st);
+    else return launch_gate_up_r<BF, G, NB, 1>(a, s, st);
+}
+
+template <bool BF, int NB>
+void launch_down_rows(const FfnArgs& a, const Shape& s, hipStream_t st) {
+    const dim3 grid(unsigned(s.n_rb));
+    if (s.dn_G == 16)
+        hipLaunchKernelGGL((ffn_down_rows<BF, 16, 1, NB>), grid, dim3(kThreads), 0, st, a);
+    else if (s.dn_G == 32 && s.dn_R == 2)
+        hipLaunchKernelGGL((ffn_down_rows<BF, 32, 2, NB>), grid, dim3(kThreads), 0, st, a);
+    else if (s.dn_G == 32)
+        hipLaunchKernelGGL((ffn_down_rows<BF, 32, 1, NB>), grid, dim3(kThreads), 0, st, a);
+    else if (s.dn_R == 4)
+        hipLaunchKernelGGL((ffn_down_rows<BF, 64, 4, NB>), grid, dim3(kThreads), 0, st, a);
+    else if (s.dn_R == 2)
+        hipLaunchKernelGGL((ffn_down_rows<BF, 64, 2, NB>), grid, dim3(kThreads), 0, st, a);
+    else
+        hipLaunchKernelGGL((ffn_down_rows<BF, 64, 1, NB>), grid, dim3(kThreads), 0, st, a);
 }
 
 template <bool BF, int NB>
@@ -1147,12 +1200,8 @@ int launch_down(const FfnArgs& a, const Shape& s, hipStream_t st) {
     const dim3 grid(unsigned(s.n_rb));
     if (s.dn_kind == 1) {
         hipLaunchKernelGGL((ffn_down_wg<BF, kDownWgR, NB>), grid, dim3(kThreads), 0, st, a);
-    } else if (s.dn_G == 16) {
-        hipLaunchKernelGGL((ffn_down_rows<BF, 16, kDownRowsR, NB>), grid, dim3(kThreads), 0, st, a);
-    } else if (s.dn_G == 32) {
-        hipLaunchKernelGGL((ffn_down_rows<BF, 32, kDownRowsR, NB>), grid, dim3(kThreads), 0, st, a);
     } else {
-        hipLaunchKernelGGL((ffn_down_rows<BF, 64, kDownRowsR, NB>), grid, dim3(kThreads), 0, st, a);
+        launch_down_rows<BF, NB>(a, s, st);
     }
     STMOE_LAUNCHED();
     return STMOE_OK;

@@ -251,6 +251,14 @@ int expert_cache_warm(expert_cache* c, const int32_t* warm);
 /* Issue prefetch copies on the side stream; returns the number of copies. */
 int expert_cache_prefetch(expert_cache* c, int layer, const int32_t* ranked, int n,
                           int64_t stamp);
+/* Link order of prefetch copies (Section 4.3.4 overlaps them with the
+ * current layer's work; the paper leaves their order against the missed
+ * loads open).  after_demand = 0 (default): they start when issued and share
+ * the host link with demand copies still in flight.  1: they wait for the
+ * demand copies of the latest acquire, so they only take the link once the
+ * current layer's missed experts are in.  Which copies happen, and the
+ * counts, do not change.  Returns STMOE_EINVAL for other values. */
+int expert_cache_set_prefetch_order(expert_cache* c, int after_demand);
 /* Make `needed` (host, n distinct experts) resident for a kernel on
  * `compute`: demand copies on the demand stream, `compute` waits for every
  * copy it needs; dev_table_out (host [E]) receives the device blob pointer

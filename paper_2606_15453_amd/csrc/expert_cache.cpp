@@ -202,6 +202,9 @@ struct expert_cache {
     std::vector<char> loaded_set, released_set;
     int stage_next = 0;
     std::vector<std::vector<int>> held;  // per layer: slots (global ids) read by the last acquire
+    hipEvent_t demand_done = nullptr;    // after the last acquire's demand copies
+    bool demand_done_set = false;
+    int after_demand = 0;                // prefetch copies wait for demand_done
 
     char* slot_ptr(int gid) const { return arena + size_t(gid) * blob; }
 };
@@ -277,6 +280,11 @@ extern "C" int expert_cache_create(int L, int E, int C, size_t blob_bytes, int n
             return STMOE_EHIP;
         }
     }
+    if (hipEventCreateWithFlags(&c->demand_done, hipEventDisableTiming) != hipSuccess) {
+        expert_cache_destroy(c);
+        set_error("expert_cache_create: hipEventCreateWithFlags failed");
+        return STMOE_EHIP;
+    }
     *out = c;
     return STMOE_OK;
 }
@@ -289,6 +297,7 @@ extern "C" int expert_cache_destroy(expert_cache* c) {
         if (e) (void)hipEventDestroy(e);
     for (auto e : c->released)
         if (e) (void)hipEventDestroy(e);
+    if (c->demand_done) (void)hipEventDestroy(c->demand_done);
     stmoe_policy_destroy(c->pol);
     delete c;
     return STMOE_OK;
@@ -325,6 +334,8 @@ extern "C" int expert_cache_prefetch(expert_cache* c, int layer, const int32_t* 
     if (int rc = check_list(ranked, n, c->E, true)) return rc;
     int32_t pairs[2 * kMaxE];
     const int m = policy_prefetch(c->pol, layer, ranked, n, stamp, pairs);
+    if (m > 0 && c->after_demand && c->demand_done_set)
+        STMOE_HIP(hipStreamWaitEvent(c->side, c->demand_done, 0));
     for (int i = 0; i < m; ++i) {
         const int e = pairs[2 * i], s = pairs[2 * i + 1];
         if (int rc = copy_into(c, layer * c->C + s, c->host[size_t(layer) * c->E + e], c->side)) return rc;
@@ -375,6 +386,10 @@ extern "C" int expert_cache_acquire(expert_cache* c, int layer, const int32_t* n
         if (int rc = copy_into(c, gid, c->host[size_t(layer) * c->E + e], c->demand)) return rc;
         gid_of[e] = gid;
     }
+    if (m > 0) {
+        STMOE_HIP(hipEventRecord(c->demand_done, c->demand));
+        c->demand_done_set = true;
+    }
     // every needed expert: the compute stream waits for its slot's last copy
     for (int i = 0; i < n; ++i) {
         const int e = needed[i];
@@ -389,6 +404,14 @@ extern "C" int expert_cache_acquire(expert_cache* c, int layer, const int32_t* n
         held.push_back(gid);
     }
     return n_hits;
+}
+
+extern "C" int expert_cache_set_prefetch_order(expert_cache* c, int after_demand) {
+    clear_error();
+    STMOE_CHECK(c, "null cache");
+    STMOE_CHECK(after_demand == 0 || after_demand == 1, "after_demand must be 0 or 1");
+    c->after_demand = after_demand;
+    return STMOE_OK;
 }
 
 extern "C" int expert_cache_release(expert_cache* c, int layer, void* compute) {

@@ -92,6 +92,7 @@ _SIGS = {
     "expert_cache_prefetch": (i32, [vp, i32, vp, i32, i64]),
     "expert_cache_acquire": (i32, [vp, i32, vp, i32, i64, P(vp), vp]),
     "expert_cache_release": (i32, [vp, i32, vp]),
+    "expert_cache_set_prefetch_order": (i32, [vp, i32]),
     "expert_cache_stats": (i32, [vp, P(CacheStats)]),
     "moe_ctx_create": (i32, [P(ModelDesc), vp, vp, vp, P(vp)]),
     "moe_ctx_destroy": (i32, [vp]),
@@ -357,6 +358,9 @@ class ExpertCache:
 
     def release(self, layer, compute_stream=None):
         _call("expert_cache_release", self.h, layer, _s(compute_stream))
+
+    def set_prefetch_order(self, after_demand):
+        _call("expert_cache_set_prefetch_order", self.h, int(after_demand))
 
     def stats(self):
         st = CacheStats()

@@ -47,7 +47,7 @@ def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True):
                             ffn_tokens=ffn_tokens, renorm=renorm, online=online)
 
 
-def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None):
+def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
@@ -71,6 +71,7 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None):
         keep += [arena, demand, side]
         cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, cfg.blob_bytes, n_stage, arena, host, demand, side)
         cache.warm(st.warm)
+        cache.set_prefetch_order(after_demand)
         ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
                               [g.data_ptr() for g in st.wg_dev], predictor=pred, cache=cache,
                               shared_ptrs=st.shared_ptrs(), n_shared=cfg.n_shared, renorm=renorm,
@@ -177,16 +178,17 @@ def test_decode_resident_ablations(name, over, mode):
 
 
 @pytest.mark.parametrize("name,over", CFGS)
-@pytest.mark.parametrize("mode", [0, 1, 2, 3])
-def test_decode_capped_counts_and_invariance(name, over, mode):
+@pytest.mark.parametrize("mode,after_demand", [(0, 0), (1, 0), (2, 0), (3, 0), (1, 1)])
+def test_decode_capped_counts_and_invariance(name, over, mode, after_demand):
     """At the capped budget the cache makes the oracle's decisions, and the
-    outputs are bit-identical to the all-resident run whatever the mode."""
+    outputs are bit-identical to the all-resident run whatever the mode and
+    the link order of prefetch copies."""
     from oracle.stmoe_oracle import decode_reference
     from paper_2606_15453_amd import workload as W
     cfg = W.CONFIGS[name].scaled(**over)
     st = Stack(cfg)
     _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
-    idx_hist, ys, stats, cst = _run_gpu(st, mode, capped=True)
+    idx_hist, ys, stats, cst = _run_gpu(st, mode, capped=True, after_demand=after_demand)
     for t in range(cfg.T):
         assert np.array_equal(ys[t], ys_res[t])
     ref = _oracle(st, mode, C=cfg.C)

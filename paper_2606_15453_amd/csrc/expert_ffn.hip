@@ -50,6 +50,8 @@ constexpr int kUpInFlight = 2;        // 16-byte chunks per row in flight per la
 constexpr bool kStageX = true;        // GEMV gate/up: token activations staged in LDS ...
 constexpr int kXStageMax = 32768;     // ... when B*H*esz fits in this many bytes
 constexpr int kDownInFlight = 2;      // ... per row per lane in the whole-workgroup down kernel
+constexpr int kDownCarryMaxNB = 4;    // lane-group down, one row per group: activations loaded with the
+                                      // weights up to this many tokens (more rows: the registers cost more)
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -447,6 +449,72 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_wg(FfnArgs a, int blocks
     }
 }
 
+// One slot's contribution to R down rows: chunk steps c0, c0 + S, ... of
+// the rows, U steps in flight.  With CARRY the activation chunks of the
+// slot's tokens are loaded together with the weight chunks, so a step costs
+// one memory round trip; otherwise they are loaded when the step is summed
+// (after its weights have arrived: two round trips, fewer registers).
+template <bool BF, int R, int NB, int U, bool CARRY>
+__device__ __forceinline__ void down_slot(const char* wd, size_t rowb, int cpr, int c0, int S,
+                                          const float* act, int B, int I, unsigned tm,
+                                          float (&acc)[R][NB]) {
+    constexpr int N = Chunk<BF>::N;
+    constexpr int NX = N / 4;                  // float4 per chunk and token
+    constexpr int NBX = CARRY ? NB : 1;
+    const float4* act4 = reinterpret_cast<const float4*>(act);
+    auto load_x = [&](int c, float4 (&xv)[NBX][NX]) {
+        if constexpr (CARRY) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+                if ((tm >> b) & 1u)
+#pragma unroll
+                    for (int q = 0; q < NX; ++q) xv[b][q] = act4[(size_t(b) * I + size_t(c) * N) / 4 + q];
+        }
+    };
+    auto compute = [&](int c, const uint4 (&w)[R], const float4 (&xv)[NBX][NX]) {
+        Chunk<BF> cw[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) cw[r].unpack(w[r]);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            if (!((tm >> b) & 1u)) continue;
+            Chunk<BF> cx;
+            if constexpr (CARRY) {
+#pragma unroll
+                for (int q = 0; q < NX; ++q) {
+                    cx.v[4 * q + 0] = xv[b][q].x; cx.v[4 * q + 1] = xv[b][q].y;
+                    cx.v[4 * q + 2] = xv[b][q].z; cx.v[4 * q + 3] = xv[b][q].w;
+                }
+            } else {
+                cx.load_f32(act + size_t(b) * I + c * N);
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[r][b] = dotc<BF>(cw[r], cx, acc[r][b]);
+        }
+    };
+    int c = c0;
+    for (; c + (U - 1) * S < cpr; c += U * S) {
+        uint4 q[U][R];
+        float4 xv[U][NBX][NX];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int r = 0; r < R; ++r) q[u][r] = ld_stream(wd + r * rowb + size_t(c + u * S) * 16);
+#pragma unroll
+        for (int u = 0; u < U; ++u) load_x(c + u * S, xv[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) compute(c + u * S, q[u], xv[u]);
+    }
+    for (; c < cpr; c += S) {
+        uint4 q[R];
+        float4 xv[NBX][NX];
+#pragma unroll
+        for (int r = 0; r < R; ++r) q[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
+        load_x(c, xv);
+        compute(c, q, xv);
+    }
+}
+
 // Down, rows owned by lane groups: every wave covers the workgroup's rows
 // (R per lane group); the four waves split the slots (wave w takes slots w,
 // w+4, ...) and their sums are added in wave order through LDS.  Each
@@ -477,41 +545,10 @@ __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
 
-    for (int j = wave; live && j < p.n_slots; j += kWaves) {
-        const unsigned tm = p.tok[j];
-        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb;
-        const float* act = reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I;
-        auto compute = [&](int c, const uint4 (&q)[R]) {
-            Chunk<BF> cw[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) cw[r].unpack(q[r]);
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                if (!((tm >> b) & 1u)) continue;
-                Chunk<BF> cx;
-                cx.load_f32(act + size_t(b) * a.I + c * N);
-#pragma unroll
-                for (int r = 0; r < R; ++r) acc[r][b] = dotc<BF>(cw[r], cx, acc[r][b]);
-            }
-        };
-        int c = g;
-        for (; c + G < cpr; c += 2 * G) {
-            uint4 qa[R], qb[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                qa[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
-                qb[r] = ld_stream(wd + r * rowb + size_t(c + G) * 16);
-            }
-            compute(c, qa);
-            compute(c + G, qb);
-        }
-        if (c < cpr) {
-            uint4 qa[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) qa[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
-            compute(c, qa);
-        }
-    }
+    for (int j = wave; live && j < p.n_slots; j += kWaves)
+        down_slot<BF, R, NB, 2, (R == 1 && NB <= kDownCarryMaxNB)>(
+            slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb, rowb, cpr, g, G,
+            reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I, a.B, a.I, p.tok[j], acc);
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -554,41 +591,10 @@ __global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
 
-    for (int j = 0; j < p.n_slots; ++j) {
-        const unsigned tm = p.tok[j];
-        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb;
-        const float* act = reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I;
-        auto compute = [&](int c, const uint4 (&q)[R]) {
-            Chunk<BF> cw[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) cw[r].unpack(q[r]);
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                if (!((tm >> b) & 1u)) continue;
-                Chunk<BF> cx;
-                cx.load_f32(act + size_t(b) * a.I + c * N);
-#pragma unroll
-                for (int r = 0; r < R; ++r) acc[r][b] = dotc<BF>(cw[r], cx, acc[r][b]);
-            }
-        };
-        constexpr int U = kDownInFlight;
-        int c = tid;
-        for (; c + (U - 1) * kThreads < cpr; c += U * kThreads) {   // U chunks per row in flight
-            uint4 q[U][R];
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int r = 0; r < R; ++r) q[u][r] = ld_stream(wd + r * rowb + size_t(c + u * kThreads) * 16);
-#pragma unroll
-            for (int u = 0; u < U; ++u) compute(c + u * kThreads, q[u]);
-        }
-        for (; c < cpr; c += kThreads) {
-            uint4 qa[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) qa[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
-            compute(c, qa);
-        }
-    }
+    for (int j = 0; j < p.n_slots; ++j)
+        down_slot<BF, R, NB, kDownInFlight, false>(
+            slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb, rowb, cpr, tid, kThreads,
+            reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I, a.B, a.I, p.tok[j], acc);
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll

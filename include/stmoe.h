@@ -259,6 +259,21 @@ int expert_cache_prefetch(expert_cache* c, int layer, const int32_t* ranked, int
  * current layer's missed experts are in.  Which copies happen, and the
  * counts, do not change.  Returns STMOE_EINVAL for other values. */
 int expert_cache_set_prefetch_order(expert_cache* c, int after_demand);
+/* Device-side decisions (Section 4.3.4's missed loading and prefetch
+ * without a host round trip).  on = 1: the policy state moves to device
+ * memory and moe_decode_layer takes its decisions in a one-workgroup kernel
+ * from the routing and the prediction on the device: the same policy and
+ * the same decisions and counts as the host path.  Missed experts are copied
+ * by a copy kernel on the compute stream, prefetches by one on the side
+ * stream; experts beyond the layer's slots (the host path's staging
+ * overflow) are read by the FFN straight from host memory, so the staging
+ * slots are not used.  Every host blob must be pinned host memory that the
+ * device maps at the same address (hipHostMalloc, torch pin_memory);
+ * otherwise STMOE_EINVAL and nothing changes.  While on,
+ * expert_cache_acquire / _prefetch / _warm return STMOE_ESTATE and
+ * expert_cache_stats reads the device counters.  on = 0 moves the state
+ * back to the host policy.  [sync] */
+int expert_cache_set_device_policy(expert_cache* c, int on);
 /* Make `needed` (host, n distinct experts) resident for a kernel on
  * `compute`: demand copies on the demand stream, `compute` waits for every
  * copy it needs; dev_table_out (host [E]) receives the device blob pointer

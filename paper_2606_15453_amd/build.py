@@ -17,7 +17,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SOURCES = ["util.cpp", "route_topk.hip", "predictor.hip", "expert_ffn.hip", "expert_cache.cpp",
-           "decode_layer.hip", "calib.hip"]
+           "cache_device.hip", "decode_layer.hip", "calib.hip"]
 LIB = os.path.join(HERE, "libstmoe.so")
 ARCH = "gfx950"
 

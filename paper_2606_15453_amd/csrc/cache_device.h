@@ -1,0 +1,45 @@
+// Device-side cache decisions: the expert cache's policy state lives in HBM
+// and a one-workgroup kernel per layer makes the missed-loading and prefetch
+// decisions from the routing and the prediction already on the device
+// (Section 4.3.4's "ML" and "EP" stages without a host round trip).  Copies
+// from pinned host memory run as copy kernels on the compute stream (missed
+// experts) and on the cache's side stream (prefetches); experts beyond the
+// layer's slots are read by the FFN straight from host memory.
+#pragma once
+
+#include "common.h"
+
+namespace stmoe {
+
+struct DeviceCache;
+
+// Host policy state handed over when device decisions are switched on and
+// taken back when they are switched off (both [sync]).
+struct PolicyState {
+    int L, E, C;
+    int32_t* slot;              // [L*C] expert in slot or -1
+    int64_t* last;              // [L*C] last use stamp
+    int32_t* where;             // [L*E] slot of expert or -1
+    char* pending;              // [L*E] prefetched, not yet verified
+    stmoe_cache_stats* st;
+};
+
+int device_cache_create(const PolicyState& ps, char* arena, size_t blob, const void* const* host_blobs,
+                        hipStream_t side, DeviceCache** out);
+int device_cache_download(DeviceCache* d, const PolicyState& ps);
+void device_cache_destroy(DeviceCache* d);
+int device_cache_stats(DeviceCache* d, stmoe_cache_stats* st);
+
+// One layer on `s` (the compute stream).  decide: the decisions for `layer`
+// (missed experts; none when BK == 0) and, with `ranked`, for `next`
+// (prefetch under the admission knobs), and the pointer table the FFN reads
+// (table [E]).
+// demand: the missed experts' copies.  prefetch: the copies for `next` on
+// the side stream, after everything enqueued on `s` so far.
+int device_cache_decide(DeviceCache* d, int layer, int next, const int32_t* idx, int BK,
+                        const int32_t* ranked, const int32_t* n_ranked, const uint8_t* max_score,
+                        int pf_min, int pf_max, int64_t stamp, const void** table, hipStream_t s);
+int device_cache_demand(DeviceCache* d, int layer, hipStream_t s);
+int device_cache_prefetch(DeviceCache* d, int next, hipStream_t s);
+
+}  // namespace stmoe

@@ -15,6 +15,7 @@
 #include <string>
 #include <vector>
 
+#include "cache_device.h"
 #include "common.h"
 
 namespace stmoe {
@@ -24,6 +25,8 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
                const float* logits, int renorm);
 int route_logits(const void* x, const void* w_gate, int B, int H, int E, int dtype, float* z, hipStream_t s);
 void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_bytes);
+DeviceCache* expert_cache_device(expert_cache* c);
+int expert_cache_after_demand(const expert_cache* c);
 void stmoe_shape(const stmoe_predictor* p, int* L, int* E, int* K, int* B);
 int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int renorm, int32_t* idx,
                         float* w, void* route_ws, stmoe_predictor* p, int layer, const int32_t* sel_prev,
@@ -304,7 +307,13 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
             if (int rc = stmoe_predict(c->pred, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr,
                                        max_scores(c->ranked, E), c->ranked, c->ranked + E, c->s))
                 return rc;
-            if (c->cache) {
+            if (DeviceCache* dc = c->cache ? expert_cache_device(c->cache) : nullptr) {
+                if (int rc = device_cache_decide(dc, 0, 0, nullptr, 0, c->ranked, c->ranked + E,
+                                                 max_scores(c->ranked, E), c->pf_min_score, c->pf_max,
+                                                 stamp - 1, c->tables, c->s))
+                    return rc;
+                if (int rc = device_cache_prefetch(dc, 0, c->s)) return rc;
+            } else if (c->cache) {
                 if (int rc = fetch_record(c, idx_l, true)) return rc;
                 if (int rc = prefetch_from_record(c, 0, stamp - 1)) return rc;
             }
@@ -373,7 +382,21 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
     if (timed && c->cache)
         if (int rc = stamp_event(tl.route1, c->s)) return rc;
     // ML: make the selection resident
-    if (c->cache) {
+    DeviceCache* dc = c->cache ? expert_cache_device(c->cache) : nullptr;
+    const bool pf_now = dc && use && L > 1;          // L == 1: after the FFN, which reads the same slots
+    if (dc) {
+        // device decisions: no host wait; the FFN reads the table they write
+        if (int rc = device_cache_decide(dc, layer, (layer + 1) % L, idx_l, B * K, use ? c->ranked : nullptr,
+                                         c->ranked + E, max_scores(c->ranked, E), c->pf_min_score, c->pf_max,
+                                         stamp, c->tables + size_t(layer) * E, c->s))
+            return rc;
+        const bool after_demand = expert_cache_after_demand(c->cache);
+        if (pf_now && !after_demand)
+            if (int rc = device_cache_prefetch(dc, (layer + 1) % L, c->s)) return rc;
+        if (int rc = device_cache_demand(dc, layer, c->s)) return rc;
+        if (pf_now && after_demand)
+            if (int rc = device_cache_prefetch(dc, (layer + 1) % L, c->s)) return rc;
+    } else if (c->cache) {
         if (int rc = fetch_record(c, idx_l, use != 0)) return rc;
         int needed[kMaxE];
         int n = 0;
@@ -426,7 +449,10 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
     }
     if (timed) c->timed_layers.push_back(tl);
     // EP: prefetch the next layer's predicted experts, overlapping the FFN
-    if (c->cache) {
+    if (dc) {
+        if (use && !pf_now)
+            if (int rc = device_cache_prefetch(dc, (layer + 1) % L, c->s)) return rc;
+    } else if (c->cache) {
         if (int rc = expert_cache_release(c->cache, layer, c->s)) return rc;
         if (use) {
             if (int rc = prefetch_from_record(c, (layer + 1) % L, stamp)) return rc;

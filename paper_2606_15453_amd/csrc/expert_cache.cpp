@@ -13,6 +13,7 @@
 #include <string>
 #include <vector>
 
+#include "cache_device.h"
 #include "common.h"
 
 struct stmoe_policy {
@@ -205,6 +206,7 @@ struct expert_cache {
     hipEvent_t demand_done = nullptr;    // after the last acquire's demand copies
     bool demand_done_set = false;
     int after_demand = 0;                // prefetch copies wait for demand_done
+    stmoe::DeviceCache* dev = nullptr;   // device-side decisions (null: the host decides)
 
     char* slot_ptr(int gid) const { return arena + size_t(gid) * blob; }
 };
@@ -216,6 +218,17 @@ void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_byte
     *E = c->E;
     *blob_bytes = c->blob;
 }
+// Internal: the device decisions when switched on, and the prefetch order.
+DeviceCache* expert_cache_device(expert_cache* c) { return c->dev; }
+int expert_cache_after_demand(const expert_cache* c) { return c->after_demand; }
+
+namespace {
+PolicyState policy_state(expert_cache* c) {
+    stmoe_policy* p = c->pol;
+    return PolicyState{p->L, p->E, p->C, p->slot.data(), p->last.data(), p->where.data(), p->pending.data(),
+                       &p->st};
+}
+}  // namespace
 }  // namespace stmoe
 
 
@@ -293,6 +306,7 @@ extern "C" int expert_cache_destroy(expert_cache* c) {
     if (!c) return STMOE_OK;
     if (c->demand) (void)hipStreamSynchronize(c->demand);
     if (c->side) (void)hipStreamSynchronize(c->side);
+    if (c->dev) stmoe::device_cache_destroy(c->dev);
     for (auto e : c->loaded)
         if (e) (void)hipEventDestroy(e);
     for (auto e : c->released)
@@ -306,6 +320,10 @@ extern "C" int expert_cache_destroy(expert_cache* c) {
 extern "C" int expert_cache_warm(expert_cache* c, const int32_t* warm) {
     clear_error();
     STMOE_CHECK(c && warm, "null pointer");
+    if (c->dev) {
+        set_error("expert_cache_warm: device decisions are on");
+        return STMOE_ESTATE;
+    }
     stmoe_policy* np = nullptr;
     if (int rc = stmoe_policy_create(c->L, c->E, c->C, warm, &np)) return rc;
     STMOE_HIP(hipStreamSynchronize(c->demand));
@@ -330,6 +348,10 @@ extern "C" int expert_cache_prefetch(expert_cache* c, int layer, const int32_t* 
                                      int64_t stamp) {
     clear_error();
     STMOE_CHECK(c, "null cache");
+    if (c->dev) {
+        set_error("expert_cache_prefetch: device decisions are on");
+        return STMOE_ESTATE;
+    }
     STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
     if (int rc = check_list(ranked, n, c->E, true)) return rc;
     int32_t pairs[2 * kMaxE];
@@ -348,6 +370,10 @@ extern "C" int expert_cache_acquire(expert_cache* c, int layer, const int32_t* n
     clear_error();
     STMOE_CHECK(c && dev_table_out, "null pointer");
     STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
+    if (c->dev) {
+        set_error("expert_cache_acquire: device decisions are on");
+        return STMOE_ESTATE;
+    }
     if (int rc = check_list(needed, n, c->E, true)) return rc;
     hipStream_t cs = as_stream(compute);
     int32_t pairs[2 * kMaxE];
@@ -406,6 +432,27 @@ extern "C" int expert_cache_acquire(expert_cache* c, int layer, const int32_t* n
     return n_hits;
 }
 
+extern "C" int expert_cache_set_device_policy(expert_cache* c, int on) {
+    clear_error();
+    STMOE_CHECK(c, "null cache");
+    STMOE_CHECK(on == 0 || on == 1, "on must be 0 or 1");
+    if (bool(on) == (c->dev != nullptr)) return STMOE_OK;
+    STMOE_HIP(hipStreamSynchronize(c->demand));
+    STMOE_HIP(hipStreamSynchronize(c->side));
+    if (on) {
+        for (auto& h : c->held) h.clear();
+        return stmoe::device_cache_create(stmoe::policy_state(c), c->arena, c->blob, c->host.data(), c->side,
+                                          &c->dev);
+    }
+    const int rc = stmoe::device_cache_download(c->dev, stmoe::policy_state(c));
+    stmoe::device_cache_destroy(c->dev);
+    c->dev = nullptr;
+    // every slot was last written and read on the device streams, now idle
+    std::fill(c->loaded_set.begin(), c->loaded_set.end(), 0);
+    std::fill(c->released_set.begin(), c->released_set.end(), 0);
+    return rc;
+}
+
 extern "C" int expert_cache_set_prefetch_order(expert_cache* c, int after_demand) {
     clear_error();
     STMOE_CHECK(c, "null cache");
@@ -429,6 +476,7 @@ extern "C" int expert_cache_release(expert_cache* c, int layer, void* compute) {
 extern "C" int expert_cache_stats(const expert_cache* c, stmoe_cache_stats* out) {
     clear_error();
     STMOE_CHECK(c && out, "null pointer");
+    if (c->dev) return stmoe::device_cache_stats(c->dev, out);
     *out = c->pol->st;
     return STMOE_OK;
 }

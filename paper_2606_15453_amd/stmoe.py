@@ -93,6 +93,7 @@ _SIGS = {
     "expert_cache_acquire": (i32, [vp, i32, vp, i32, i64, P(vp), vp]),
     "expert_cache_release": (i32, [vp, i32, vp]),
     "expert_cache_set_prefetch_order": (i32, [vp, i32]),
+    "expert_cache_set_device_policy": (i32, [vp, i32]),
     "expert_cache_stats": (i32, [vp, P(CacheStats)]),
     "moe_ctx_create": (i32, [P(ModelDesc), vp, vp, vp, P(vp)]),
     "moe_ctx_destroy": (i32, [vp]),
@@ -361,6 +362,9 @@ class ExpertCache:
 
     def set_prefetch_order(self, after_demand):
         _call("expert_cache_set_prefetch_order", self.h, int(after_demand))
+
+    def set_device_policy(self, on):
+        _call("expert_cache_set_device_policy", self.h, int(on))
 
     def stats(self):
         st = CacheStats()

@@ -47,7 +47,8 @@ def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True):
                             ffn_tokens=ffn_tokens, renorm=renorm, online=online)
 
 
-def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0):
+def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0, device=0,
+             device_until=None):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
@@ -72,6 +73,7 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
         cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, cfg.blob_bytes, n_stage, arena, host, demand, side)
         cache.warm(st.warm)
         cache.set_prefetch_order(after_demand)
+        cache.set_device_policy(device)
         ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
                               [g.data_ptr() for g in st.wg_dev], predictor=pred, cache=cache,
                               shared_ptrs=st.shared_ptrs(), n_shared=cfg.n_shared, renorm=renorm,
@@ -85,6 +87,8 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
     ctx.set_online_update(online)
     idx_hist, ys = [], []
     for t in range(cfg.T):
+        if cache is not None and device_until is not None and t == device_until:
+            cache.set_device_policy(0)       # the host policy takes over the device state
         y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device=DEV)
         ctx.token(t, st.x_dev[t], y, mode=mode)
         idx, _ = ctx.last_routing()
@@ -178,17 +182,19 @@ def test_decode_resident_ablations(name, over, mode):
 
 
 @pytest.mark.parametrize("name,over", CFGS)
-@pytest.mark.parametrize("mode,after_demand", [(0, 0), (1, 0), (2, 0), (3, 0), (1, 1)])
-def test_decode_capped_counts_and_invariance(name, over, mode, after_demand):
+@pytest.mark.parametrize("mode,after_demand,device", [(0, 0, 0), (1, 0, 0), (2, 0, 0), (3, 0, 0), (1, 1, 0),
+                                                      (0, 0, 1), (1, 0, 1), (3, 0, 1), (1, 1, 1)])
+def test_decode_capped_counts_and_invariance(name, over, mode, after_demand, device):
     """At the capped budget the cache makes the oracle's decisions, and the
-    outputs are bit-identical to the all-resident run whatever the mode and
-    the link order of prefetch copies."""
+    outputs are bit-identical to the all-resident run whatever the mode, the
+    link order of prefetch copies and where the decisions are taken (host or
+    device)."""
     from oracle.stmoe_oracle import decode_reference
     from paper_2606_15453_amd import workload as W
     cfg = W.CONFIGS[name].scaled(**over)
     st = Stack(cfg)
     _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
-    idx_hist, ys, stats, cst = _run_gpu(st, mode, capped=True, after_demand=after_demand)
+    idx_hist, ys, stats, cst = _run_gpu(st, mode, capped=True, after_demand=after_demand, device=device)
     for t in range(cfg.T):
         assert np.array_equal(ys[t], ys_res[t])
     ref = _oracle(st, mode, C=cfg.C)
@@ -196,6 +202,47 @@ def test_decode_capped_counts_and_invariance(name, over, mode, after_demand):
     assert cst == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
                        useful=n.useful, wasted=n.wasted)
 
+
+
+@pytest.mark.parametrize("name,over", [CFGS[1], CFGS[3]])
+def test_decode_device_policy_handover(name, over):
+    """Device decisions for the first tokens, then the host policy continues
+    from the state they left: counts still equal the oracle's and outputs the
+    all-resident run's."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    _, ys, _, cst = _run_gpu(st, 1, capped=True, device=1, device_until=cfg.T // 2)
+    for t in range(cfg.T):
+        assert np.array_equal(ys[t], ys_res[t])
+    n = _oracle(st, 1, C=cfg.C)["cache"].n
+    assert cst == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
+                       useful=n.useful, wasted=n.wasted)
+
+
+def test_device_policy_rejects_host_calls():
+    """While the device decides, the host-side cache calls are refused."""
+    import torch
+    from gpuhelp import DEV
+    from paper_2606_15453_amd import stmoe as S
+    L, E, C, blob = 2, 4, 2, 4096
+    host = [torch.zeros(blob, dtype=torch.uint8).pin_memory() for _ in range(L * E)]
+    arena = torch.empty(S.cache_arena_bytes(L, C, blob, 0), dtype=torch.uint8, device=DEV)
+    demand, side = torch.cuda.Stream(), torch.cuda.Stream()
+    cache = S.ExpertCache(L, E, C, blob, 0, arena, [h.data_ptr() for h in host], demand, side)
+    cache.warm(np.array([[0, 1], [2, 3]], dtype=np.int32))
+    cache.set_device_policy(1)
+    for call in (lambda: cache.acquire(0, [0], 1), lambda: cache.prefetch(0, [0], 1),
+                 lambda: cache.warm(np.array([[0, 1], [2, 3]], dtype=np.int32))):
+        with pytest.raises(S.StmoeError) as ei:
+            call()
+        assert ei.value.rc == S.ESTATE
+    assert cache.stats() == dict(hits=0, demand=0, overflow=0, prefetch=0, useful=0, wasted=0)
+    cache.set_device_policy(0)
+    hits, _ = cache.acquire(0, [0, 1], 1)
+    assert hits == 2
+    cache.close()
 
 
 def _run_graph(st, mode, timing_every=0, staged=False):

@@ -533,20 +533,22 @@ def host_pool(wl, pinned_gb):
 def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_token, attn=None):
     """One capped-cache decode run: C slots per layer, the rest streamed from
     the pinned host pool.  variant = (name, mode, min score, max prefetches
-    per layer, online CCT update, prefetch copies after the demand copies).  attn = (kv buffer, bytes, out): a decode-
+    per layer, online CCT update, prefetch copies after the demand copies,
+    decisions on the device).  attn = (kv buffer, bytes, out): a decode-
     attention stand-in that streams `bytes` of KV cache on the compute stream
     before every MoE layer (layers are then issued one by one)."""
     import torch
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
     blob = cfg.blob_bytes
-    name, mode, min_score, max_pf, online, after_demand = variant
+    name, mode, min_score, max_pf, online, after_demand, device = variant
     n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - C)
     demand, side = streams
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
     cache = S.ExpertCache(cfg.L, cfg.E, C, blob, n_stage, arena, ptrs, demand, side)
     cache.warm(W_warm(wl, C))
     cache.set_prefetch_order(after_demand)
+    cache.set_device_policy(device)
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(wl.prof)
     ctx = make_ctx(wl, pred, cache)
@@ -574,7 +576,7 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
     copies = cst["demand"] + cst["overflow"] + cst["prefetch"]
     rec = dict(tokens=n_tokens, seconds=round(dt, 4), prefetch_min_score=min_score,
                prefetch_max_per_layer=max_pf, online_update=bool(online),
-               prefetch_after_demand=bool(after_demand),
+               prefetch_after_demand=bool(after_demand), device_decisions=bool(device),
                tokens_per_s=round(cfg.B * n_tokens / dt, 3),
                ms_per_token=round(1e3 * dt / n_tokens, 3),
                stall_ms_per_token=round(1e3 * dt / n_tokens - resident_ms_per_token, 3),
@@ -604,13 +606,16 @@ def W_warm(wl, C):
 
 def offload_variants(cfg):
     from paper_2606_15453_amd import stmoe as S
-    return [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0),
-            ("st_moe", S.MODE_STMOE, 2, cfg.C, 1, 0),
-            ("st_moe_after_demand", S.MODE_STMOE, 2, cfg.C, 1, 1),
-            ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K, 1, 0),
-            ("st_moe_score4_maxK_after_demand", S.MODE_STMOE, 4, cfg.K, 1, 1),
-            ("ht_only", S.MODE_HT_ONLY, 2, cfg.C, 1, 0),
-            ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C, 1, 0)]
+    return [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 0),
+            ("st_moe", S.MODE_STMOE, 2, cfg.C, 1, 0, 0),
+            ("st_moe_after_demand", S.MODE_STMOE, 2, cfg.C, 1, 1, 0),
+            ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K, 1, 0, 0),
+            ("st_moe_score4_maxK_after_demand", S.MODE_STMOE, 4, cfg.K, 1, 1, 0),
+            ("ht_only", S.MODE_HT_ONLY, 2, cfg.C, 1, 0, 0),
+            ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C, 1, 0, 0),
+            ("on_demand_device", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 1),
+            ("st_moe_device", S.MODE_STMOE, 2, cfg.C, 1, 0, 1),
+            ("st_moe_score4_maxK_after_demand_device", S.MODE_STMOE, 4, cfg.K, 1, 1, 1)]
 
 
 def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
@@ -680,7 +685,7 @@ def attention_sweep(wl, key, n_tokens, resident_ms_per_token, pinned_gb, context
         recs = {}
         for v in offload_variants(cfg):
             if v[0] not in ("on_demand", "st_moe", "st_moe_score4_maxK", "st_moe_score4_maxK_after_demand",
-                            "ht_only"):
+                            "ht_only", "on_demand_device", "st_moe_score4_maxK_after_demand_device"):
                 continue
             recs[v[0]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, base_ms, attn)
         od = recs["on_demand"]["stall_ms_per_token"]
@@ -710,8 +715,9 @@ def offload_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, budgets):
     streams = (torch.cuda.Stream(), torch.cuda.Stream())
     rows = []
     for C in budgets:
-        variants = [(n, m, ms, (C if mp == cfg.C else mp), on, ad) for n, m, ms, mp, on, ad in offload_variants(cfg)]
-        variants.insert(3, ("st_moe_frozen_cct", S.MODE_STMOE, 2, C, 0, 0))
+        variants = [(n, m, ms, (C if mp == cfg.C else mp), on, ad, dv)
+                    for n, m, ms, mp, on, ad, dv in offload_variants(cfg)]
+        variants.insert(3, ("st_moe_frozen_cct", S.MODE_STMOE, 2, C, 0, 0, 0))
         base = None
         for v in variants:
             rec = offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)

@@ -759,6 +759,14 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma_lds(FfnArgs a, int 
     f32x4 dg[NT], du[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) dg[t] = du[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // A operand of a step, loaded one step ahead and issued before that
+    // step's weight rows: waiting for it never waits for a weight prefetch
+    bf16x8 xa[4], xn[4];
+    auto load_x = [&](int h, bf16x8 (&xv)[4]) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) xv[kb] = ld_bf8(xs + size_t(h + 32 * kb) * 2);
+    };
+    load_x(h_lo, xa);
     uint4 ld[kLoads];
 #pragma unroll
     for (int r = 0; r < kLoads; ++r) ld[r] = ld_stream(src[r]);
@@ -771,15 +779,16 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma_lds(FfnArgs a, int 
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        if (h + 128 < h_hi) {
+        const bool more = h + 128 < h_hi;
+        if (more) {
+            load_x(h + 128, xn);
             const size_t o = size_t(h + 128 - h_lo) * 2;
 #pragma unroll
             for (int r = 0; r < kLoads; ++r) ld[r] = ld_stream(src[r] + o);
         }
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
-            const size_t ox = size_t(h + 32 * kb) * 2;
-            const bf16x8 xv = xrow ? ld_bf8(xs + ox) : zero;
+            const bf16x8 xv = xrow ? xa[kb] : zero;
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const bf16x8 gv = __builtin_bit_cast(bf16x8, my[(t * 16 + n) * kLdsPadU4 + kb * 4 + q]);
@@ -787,6 +796,10 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma_lds(FfnArgs a, int 
                 dg[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv, gv, dg[t], 0, 0, 0);
                 du[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv, uv, du[t], 0, 0, 0);
             }
+        }
+        if (more) {
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) xa[kb] = xn[kb];
         }
     }
     if (SK) {
@@ -827,7 +840,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma_lds(FfnArgs a, int 
 // the slots of the workgroup's group.
 template <int NT>
 __global__ __launch_bounds__(kThreads) void ffn_down_mfma_lds(FfnArgs a) {
-    __shared__ Plan p;
+    __shared__ PlanB p;
     extern __shared__ uint4 stage[];
     build_plan(a, p);
     const int rb = blockIdx.x / a.ng, grp = blockIdx.x % a.ng;
@@ -850,38 +863,53 @@ __global__ __launch_bounds__(kThreads) void ffn_down_mfma_lds(FfnArgs a) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) d[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     const bf16x8 zero = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
-    for (int j = j0; live && j < j1; ++j) {
-        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * 2;
-        const char* src[kLoads];
+    // the group's (slot, 128-column step) pairs as one stream: the next
+    // step's activations and weight rows (the next slot's first ones at a
+    // slot's end) are in flight while the current step runs, activations
+    // issued first so that waiting for them never waits for weights
+    const int steps = a.I / 128;                   // I is a multiple of 128
+    const int total = live ? (j1 - j0) * steps : 0;
+    uint4 ld[kLoads];
+    bf16x8 av[4], an[4];
+    auto issue = [&](int j, int k, bf16x8 (&ax)[4]) {
+        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * 2 + size_t(k) * 2;
+        const char* ar = reinterpret_cast<const char*>(a.act) + (size_t(j) * a.B + (arow ? n : 0)) * rowb +
+                         q * 16 + size_t(k) * 2;
 #pragma unroll
-        for (int r = 0; r < kLoads; ++r) src[r] = wd + size_t(h0 + 4 * r + g) * rowb + size_t(e) * 16;
-        const char* ar = reinterpret_cast<const char*>(a.act) +
-                         (size_t(j) * a.B + (arow ? n : 0)) * rowb + q * 16;
-        uint4 ld[kLoads];
+        for (int kb = 0; kb < 4; ++kb) ax[kb] = ld_bf8(ar + size_t(32 * kb) * 2);
 #pragma unroll
-        for (int r = 0; r < kLoads; ++r) ld[r] = ld_stream(src[r]);
-        for (int k = 0; k < a.I; k += 128) {
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
+        for (int r = 0; r < kLoads; ++r) ld[r] = ld_stream(wd + size_t(h0 + 4 * r + g) * rowb + size_t(e) * 16);
+    };
+    int jn = j0, kn = 0;                            // next step to issue
+    if (total > 0) {
+        issue(jn, kn, av);
+        if ((kn += 128) == a.I) { kn = 0; ++jn; }
+    }
+    for (int s = 0; s < total; ++s) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
 #pragma unroll
-            for (int r = 0; r < kLoads; ++r) my[(4 * r + g) * kLdsPadU4 + e] = ld[r];
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            if (k + 128 < a.I) {
-                const size_t o = size_t(k + 128) * 2;
+        for (int r = 0; r < kLoads; ++r) my[(4 * r + g) * kLdsPadU4 + e] = ld[r];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        const bool more = s + 1 < total;
+        if (more) {
+            issue(jn, kn, an);
+            if ((kn += 128) == a.I) { kn = 0; ++jn; }
+        }
 #pragma unroll
-                for (int r = 0; r < kLoads; ++r) ld[r] = ld_stream(src[r] + o);
+        for (int kb = 0; kb < 4; ++kb) {
+            const bf16x8 ax = arow ? av[kb] : zero;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const bf16x8 wv = __builtin_bit_cast(bf16x8, my[(t * 16 + n) * kLdsPadU4 + kb * 4 + q]);
+                d[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ax, wv, d[t], 0, 0, 0);
             }
+        }
+        if (more) {
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                const bf16x8 av = arow ? ld_bf8(ar + size_t(k + 32 * kb) * 2) : zero;
-#pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const bf16x8 wv = __builtin_bit_cast(bf16x8, my[(t * 16 + n) * kLdsPadU4 + kb * 4 + q]);
-                    d[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, wv, d[t], 0, 0, 0);
-                }
-            }
+            for (int kb = 0; kb < 4; ++kb) av[kb] = an[kb];
         }
     }
     float* out = a.ng == 1 ? a.y : a.part + size_t(grp) * a.B * a.H;

@@ -63,7 +63,7 @@ struct FfnArgs {
     const void* const* eptr;         // [E] device blob pointers
     const void* const* sptr;         // [n_shared] or null
     int B, K, H, I, E, n_shared;
-    void* act;                       // [slots][B][I]: fp32 (GEMV) or bf16 (MFMA)
+    void* act;                       // [slots][B][I]: bf16 (MFMA; GEMV per act_bf16) or fp32
     float* part;                     // [ng][B][H] partial sums of the MFMA down phase (ng > 1)
     float* y;                        // [B][H]
     unsigned long long* n_experts;   // optional: += distinct routed experts (block 0)
@@ -205,6 +205,23 @@ struct Chunk {
     }
 };
 
+// Dot product of a packed 16-byte weight chunk with an unpacked chunk,
+// unpacking each weight as it is used (fewer live registers than unpacking
+// R rows up front).
+template <bool BF>
+__device__ __forceinline__ float dotq(const uint4& w, const Chunk<BF>& x, float acc) {
+    if constexpr (BF) {
+        acc = fmaf(bf16_lo(w.x), x.v[0], acc); acc = fmaf(bf16_hi(w.x), x.v[1], acc);
+        acc = fmaf(bf16_lo(w.y), x.v[2], acc); acc = fmaf(bf16_hi(w.y), x.v[3], acc);
+        acc = fmaf(bf16_lo(w.z), x.v[4], acc); acc = fmaf(bf16_hi(w.z), x.v[5], acc);
+        acc = fmaf(bf16_lo(w.w), x.v[6], acc); acc = fmaf(bf16_hi(w.w), x.v[7], acc);
+    } else {
+        acc = fmaf(__uint_as_float(w.x), x.v[0], acc); acc = fmaf(__uint_as_float(w.y), x.v[1], acc);
+        acc = fmaf(__uint_as_float(w.z), x.v[2], acc); acc = fmaf(__uint_as_float(w.w), x.v[3], acc);
+    }
+    return acc;
+}
+
 template <bool BF>
 __device__ __forceinline__ float dotc(const Chunk<BF>& w, const Chunk<BF>& x, float acc) {
 #pragma unroll
@@ -255,6 +272,16 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     return uint16_t((u + (((u >> 16) & 1u) + 0x7fffu)) >> 16);
 }
 
+// The SwiGLU activations of the GEMV path are stored as bf16 (rounded to
+// nearest even, as the MFMA path does) where the down kernel reading them
+// has the registers to unpack them (see act_bf16): one 16-byte chunk of
+// bf16 activations then matches one 16-byte chunk of a W_down row, and every
+// down workgroup, which re-reads them all, moves half the bytes.
+__device__ __forceinline__ void store_act(void* act, int act16, size_t i, float v) {
+    if (act16) reinterpret_cast<uint16_t*>(act)[i] = f32_to_bf16_rne(v);
+    else reinterpret_cast<float*>(act)[i] = v;
+}
+
 // ============================================================================
 // GEMV path (batch < 8)
 // ============================================================================
@@ -264,7 +291,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 // routing prologue so both latencies overlap; every wave then reads x from
 // LDS instead of L1/L2.
 template <bool BF, int G, int R, int NB, bool XL>
-__global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_per_slot) {
+__global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_per_slot, int act16) {
     __shared__ Plan p;
     extern __shared__ uint4 x_lds[];
     constexpr int esz = BF ? 2 : 4;
@@ -347,7 +374,6 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
         }
         compute(c, ga, ua);
     }
-    float* act = reinterpret_cast<float*>(a.act);
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
         if (!((tm >> b) & 1u)) continue;
@@ -356,7 +382,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
         for (int r = 0; r < R; ++r) {
             const float gs = seg_sum<G>(accg[r][b]);
             const float us = seg_sum<G>(accu[r][b]);
-            if (g == 0) act[(size_t(j) * a.B + b) * a.I + i0 + r] = wb * silu(gs) * us;
+            if (g == 0) store_act(a.act, act16, (size_t(j) * a.B + b) * a.I + i0 + r, wb * silu(gs) * us);
         }
     }
 }
@@ -365,7 +391,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
 // rows' chunks together (every lane issues all its loads of an iteration at
 // once), then the four waves' sums combine through LDS.
 template <bool BF, int R, int NB>
-__global__ __launch_bounds__(kThreads) void ffn_gate_up_wg(FfnArgs a, int blocks_per_slot) {
+__global__ __launch_bounds__(kThreads) void ffn_gate_up_wg(FfnArgs a, int blocks_per_slot, int act16) {
     __shared__ Plan p;
     __shared__ float red[kWaves][2][R][NB];
     build_plan(a, p, true);
@@ -443,8 +469,7 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_wg(FfnArgs a, int blocks
             float gs = 0.f, us = 0.f;
 #pragma unroll
             for (int w = 0; w < kWaves; ++w) { gs += red[w][0][r][b]; us += red[w][1][r][b]; }
-            float* act = reinterpret_cast<float*>(a.act);
-            act[(size_t(j) * a.B + b) * a.I + i0 + r] = slot_weight(a, p, j, b) * silu(gs) * us;
+            store_act(a.act, act16, (size_t(j) * a.B + b) * a.I + i0 + r, slot_weight(a, p, j, b) * silu(gs) * us);
         }
     }
 }
@@ -515,12 +540,60 @@ __device__ __forceinline__ void down_slot(const char* wd, size_t rowb, int cpr, 
     }
 }
 
+// down_slot for bf16 activations (16 bytes per chunk and token, the same
+// chunk layout as a W_down row; weights unpacked as they are used).
+template <bool BF, int R, int NB, int U, bool CARRY>
+__device__ __forceinline__ void down_slot16(const char* wd, size_t rowb, int cpr, int c0, int S,
+                                            const char* act, unsigned tm, float (&acc)[R][NB]) {
+    static_assert(BF, "bf16 activations go with bf16 weights");
+    constexpr int NBX = CARRY ? NB : 1;
+    // token b's activation row: rowb bytes, like a W_down row
+    auto load_x = [&](int c, uint4 (&xv)[NBX]) {
+        if constexpr (CARRY) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+                if ((tm >> b) & 1u) xv[b] = ld_cached(act + size_t(b) * rowb + size_t(c) * 16);
+        }
+    };
+    auto compute = [&](int c, const uint4 (&w)[R], const uint4 (&xv)[NBX]) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            if (!((tm >> b) & 1u)) continue;
+            Chunk<BF> cx;
+            if constexpr (CARRY) cx.unpack(xv[b]);
+            else cx.unpack(ld_cached(act + size_t(b) * rowb + size_t(c) * 16));
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[r][b] = dotq<BF>(w[r], cx, acc[r][b]);
+        }
+    };
+    int c = c0;
+    for (; c + (U - 1) * S < cpr; c += U * S) {
+        uint4 q[U][R];
+        uint4 xv[U][NBX];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int r = 0; r < R; ++r) q[u][r] = ld_stream(wd + r * rowb + size_t(c + u * S) * 16);
+#pragma unroll
+        for (int u = 0; u < U; ++u) load_x(c + u * S, xv[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) compute(c + u * S, q[u], xv[u]);
+    }
+    for (; c < cpr; c += S) {
+        uint4 q[R];
+        uint4 xv[NBX];
+#pragma unroll
+        for (int r = 0; r < R; ++r) q[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
+        load_x(c, xv);
+        compute(c, q, xv);
+    }
+}
+
 // Down, rows owned by lane groups: every wave covers the workgroup's rows
 // (R per lane group); the four waves split the slots (wave w takes slots w,
 // w+4, ...) and their sums are added in wave order through LDS.  Each
-// activation chunk a lane loads serves its R rows: the activations are fp32
-// and every workgroup reads all of them, so R sets how much L2 traffic the
-// weight rows carry along.
+// activation chunk a lane loads serves its R rows: every workgroup reads all
+// activations, so R sets how much L2 traffic the weight rows carry along.
 template <bool BF, int G, int R, int NB>
 __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
     constexpr int kRows = (64 / G) * R;
@@ -545,10 +618,16 @@ __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
 
-    for (int j = wave; live && j < p.n_slots; j += kWaves)
-        down_slot<BF, R, NB, 2, (R == 1 && NB <= kDownCarryMaxNB)>(
-            slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb, rowb, cpr, g, G,
-            reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I, a.B, a.I, p.tok[j], acc);
+    for (int j = wave; live && j < p.n_slots; j += kWaves) {
+        if constexpr (BF && R < 4)
+            down_slot16<BF, R, NB, 2, (R == 1 && NB <= kDownCarryMaxNB)>(
+                slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb, rowb, cpr, g, G,
+                reinterpret_cast<const char*>(a.act) + size_t(j) * a.B * rowb, p.tok[j], acc);
+        else
+            down_slot<BF, R, NB, 2, (R == 1 && NB <= kDownCarryMaxNB)>(
+                slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb, rowb, cpr, g, G,
+                reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I, a.B, a.I, p.tok[j], acc);
+    }
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -591,10 +670,17 @@ __global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[r][b] = 0.f;
 
-    for (int j = 0; j < p.n_slots; ++j)
-        down_slot<BF, R, NB, kDownInFlight, false>(
-            slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb, rowb, cpr, tid, kThreads,
-            reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I, a.B, a.I, p.tok[j], acc);
+    for (int j = 0; j < p.n_slots; ++j) {
+        const char* wd = slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb;
+        if constexpr (BF && NB <= 2)
+            down_slot16<BF, R, NB, kDownInFlight, false>(
+                wd, rowb, cpr, tid, kThreads, reinterpret_cast<const char*>(a.act) + size_t(j) * a.B * rowb,
+                p.tok[j], acc);
+        else
+            down_slot<BF, R, NB, kDownInFlight, false>(
+                wd, rowb, cpr, tid, kThreads, reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I,
+                a.B, a.I, p.tok[j], acc);
+    }
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll
@@ -1179,17 +1265,25 @@ WsLayout ws_layout(int B, int H, int I, const Shape& s) {
     return w;
 }
 
+// GEMV activations are bf16 for the lane-group down kernel below four rows
+// per group and the whole-workgroup one up to two token columns, fp32
+// otherwise (there the unpacking registers cost more than the traffic
+// saves); the gate/up launch writes what its down kernel reads.
+template <bool BF>
+int act_bf16(const Shape& s, int B) { return BF && (s.dn_kind == 1 ? B <= 2 : s.dn_R < 4); }
+
 template <bool BF, int G, int NB, int R>
 int launch_gate_up_r(const FfnArgs& a, const Shape& s, hipStream_t st) {
     const int rows = kWaves * (64 / G) * R;
     const int bps = (a.I + rows - 1) / rows;
     const size_t xbytes = size_t(a.B) * a.H * (BF ? 2 : 4);
+    const int act16 = act_bf16<BF>(s, a.B);
     if (kStageX && xbytes <= size_t(kXStageMax))
         hipLaunchKernelGGL((ffn_gate_up<BF, G, R, NB, true>), dim3(unsigned(bps * s.slots)), dim3(kThreads),
-                           unsigned(xbytes), st, a, bps);
+                           unsigned(xbytes), st, a, bps, act16);
     else
         hipLaunchKernelGGL((ffn_gate_up<BF, G, R, NB, false>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0,
-                           st, a, bps);
+                           st, a, bps, act16);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }
@@ -1200,7 +1294,7 @@ int launch_gate_up(const FfnArgs& a, const Shape& s, hipStream_t st) {
         if (a.H * (BF ? 2 : 4) / 16 >= kUpWgMinChunks && a.I % kUpWgR == 0) {
             const int bps = a.I / kUpWgR;
             hipLaunchKernelGGL((ffn_gate_up_wg<BF, kUpWgR, NB>), dim3(unsigned(bps * s.slots)),
-                               dim3(kThreads), 0, st, a, bps);
+                               dim3(kThreads), 0, st, a, bps, act_bf16<BF>(s, a.B));
             STMOE_LAUNCHED();
             return STMOE_OK;
         }

@@ -43,7 +43,8 @@ def _inputs(cfg, B, K, seed, distinct_rows=True):
 
 @pytest.mark.parametrize("name,B", [("tiny", 1), ("qwen30b", 1), ("qwen30b", 3), ("qwen30b-b8", 8),
                                     ("qwen30b-b8", 12), ("dsv2lite", 4), ("dsv2lite", 9),
-                                    ("qwen235b", 16), ("qwen235b", 9), ("qwen235b", 2), ("mixtral", 8)])
+                                    ("qwen235b", 16), ("qwen235b", 9), ("qwen235b", 2), ("qwen235b", 4),
+                                    ("mixtral", 4), ("mixtral", 8)])
 def test_ffn_parity(name, B):
     from paper_2606_15453_amd import workload as W
     cfg = W.CONFIGS[name].scaled(B=B)

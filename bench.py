@@ -56,8 +56,11 @@ def parse():
                     help="at most this many decode tokens of the CPU oracle sample (0 skips it)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="the CPU oracle sample stops after the token that reaches this much timed work")
-    ap.add_argument("--offload-only", default=None, metavar="VARIANT",
-                    help="run only this capped-cache variant (for traces)")
+    ap.add_argument("--offload-only", default=None, metavar="VARIANT[,VARIANT...]",
+                    help="run only these capped-cache variants (and on-demand loading)")
+    ap.add_argument("--hbm-pool-gb", type=float, default=80.0,
+                    help="for a stack larger than HBM: distinct expert blobs generated in HBM "
+                         "(expert (l, e) reads blob (l*E + e) mod their number)")
     ap.add_argument("--attention-sweep", default=None, metavar="CTX1,CTX2,...",
                     help="capped cache with a decode-attention stand-in of these context lengths (markdown)")
     ap.add_argument("--offload-sweep", default=None, metavar="C1,C2,...",
@@ -73,6 +76,8 @@ def parse():
                     help="print a markdown table of a rocprofv3 kernel_stats.csv and exit")
     ap.add_argument("--summarize-overlap", nargs=2, metavar=("KERNEL_CSV", "COPY_CSV"),
                     help="copy/compute overlap of the capped-cache runs in a rocprofv3 trace")
+    ap.add_argument("--summarize-offload", nargs="+", metavar="BENCH_JSON",
+                    help="print a markdown table of the capped-cache runs in bench JSON lines and exit")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the markdown counter summary of two rocprofv3 --pmc runs and exit")
     return ap.parse_args()
@@ -245,6 +250,34 @@ def summarize_overlap(kernel_csv, copy_csv):
               f"{ov / max(cbusy, 1):.3f} | {ov / max(fbusy, 1):.3f} |")
 
 
+def summarize_offload(paths):
+    """Markdown table of the capped-cache runs in bench JSON lines (one file
+    per workload): per variant, tokens/s, stall beyond the HBM-resident step,
+    its reduction against on-demand loading, copies and prediction quality."""
+    print("| workload | C of E | variant | tokens/s | ms per token | stall ms per token | stall reduction "
+          "vs on-demand | demand / overflow / prefetch (useful, wasted) copies | H2D GB/s | "
+          "recall l>=1 / l=0 / precision |")
+    print("|---|---|---|---|---|---|---|---|---|---|")
+    for p in paths:
+        d = json.loads(open(p).read().strip().splitlines()[-1])
+        o = d.get("offload")
+        if not o:
+            continue
+        cfg = d["config"]
+        red = o.get("stall_reduction", {})
+        for name, r in o.items():
+            if not isinstance(r, dict) or "tokens_per_s" not in r:
+                continue
+            c = r["cache"]
+            pq = (f"{r['recall_layers_ge1']:.3f} / {r['recall_layer0']:.3f} / {r['precision']:.3f}"
+                  if "recall_layers_ge1" in r else "-")
+            rd = red.get(name)
+            print(f"| {cfg['workload']} | {o['cache_slots_per_layer']} of {cfg['experts']} | {name} | "
+                  f"{r['tokens_per_s']} | {r['ms_per_token']} | {r['stall_ms_per_token']} | "
+                  f"{'-' if rd is None else f'{rd:+.3f}'} | {c['demand']} / {c['overflow']} / "
+                  f"{c['prefetch']} ({c['useful']}, {c['wasted']}) | {r['h2d_gbps']} | {pq} |")
+
+
 def summarize_stats(path, title, cmd):
     import csv
     print(f"# {title}\n")
@@ -403,9 +436,16 @@ def achievable_read_gbps(nbytes=4 << 30, reps=10):
 
 
 class Workload:
-    """Seeded synthetic inputs of one config, placed in HBM."""
+    """Seeded synthetic inputs of one config, placed in HBM.
 
-    def __init__(self, cfg):
+    hbm_blobs: for a stack whose experts do not fit in HBM (Qwen3-235B shapes,
+    454 GB), only this many distinct expert blobs are generated and expert
+    (l, e) reads blob (l*E + e) mod hbm_blobs.  Within a layer the E experts
+    stay distinct, so every timed read streams distinct HBM bytes; the values
+    are those of the first hbm_blobs experts.  x_tokens: hidden states for the
+    first x_tokens decode tokens only (their routing trace is unchanged)."""
+
+    def __init__(self, cfg, hbm_blobs=None, x_tokens=None):
         import torch
         from paper_2606_15453_amd import stmoe as S
         from paper_2606_15453_amd import workload as W
@@ -413,6 +453,9 @@ class Workload:
         dev = "cuda:0"
         self.dt = S.BF16 if cfg.dtype == "bf16" else S.F32
         tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+        self.n_blobs = cfg.L * cfg.E if hbm_blobs is None else min(cfg.L * cfg.E, hbm_blobs)
+        assert self.n_blobs >= cfg.E
+        self.T = cfg.T if x_tokens is None else min(cfg.T, x_tokens)
         t0 = time.time()
         self.sel = W.planted_trace(cfg)
         self.prof = W.profiling_selections(cfg, self.sel)
@@ -422,15 +465,15 @@ class Workload:
         self.wg_f64 = [W.router_rows_f64(cfg, l) for l in range(cfg.L)]
         self.wg = [self._dev(W.to_storage(cfg, g)) for g in self.wg_f64]
         xs = np.stack([np.stack([W.to_storage(cfg, W.hidden_f64(cfg, self.sel, cfg.P + t, l, self.wg_f64[l]))
-                                 for l in range(cfg.L)]) for t in range(cfg.T)])
+                                 for l in range(cfg.L)]) for t in range(self.T)])
         self.x_store = xs
         self.x = self._dev(xs)                              # [T][L][B][H]
-        log(f"router rows + hidden states in {time.time() - t0:.1f}s")
+        log(f"router rows + hidden states for {self.T} tokens in {time.time() - t0:.1f}s")
         t0 = time.time()
-        self.blobs = torch.empty((cfg.L * cfg.E, cfg.blob_elems), dtype=tdt, device=dev)
-        for l in range(cfg.L):
-            for e in range(cfg.E):
-                W.expert_blob_torch(cfg, l, e, self.blobs[l * cfg.E + e])
+        self.blobs = torch.empty((self.n_blobs, cfg.blob_elems), dtype=tdt, device=dev)
+        for i in range(self.n_blobs):
+            l, e = divmod(i, cfg.E)
+            W.expert_blob_torch(cfg, l, e, self.blobs[i])
         self.shared = None
         if cfg.n_shared:
             self.shared = torch.empty((cfg.L * cfg.n_shared, cfg.blob_elems), dtype=tdt, device=dev)
@@ -439,7 +482,8 @@ class Workload:
                     W.expert_blob_torch(cfg, l, s, self.shared[l * cfg.n_shared + s], shared=True)
         torch.cuda.synchronize()
         gb = self.blobs.numel() * self.blobs.element_size() / 1e9
-        log(f"{cfg.L * cfg.E} expert blobs ({gb:.1f} GB) generated in HBM in {time.time() - t0:.1f}s")
+        log(f"{self.n_blobs} of {cfg.L * cfg.E} expert blobs ({gb:.1f} GB) generated in HBM in "
+            f"{time.time() - t0:.1f}s")
 
     @staticmethod
     def _dev(a):
@@ -449,8 +493,15 @@ class Workload:
             return torch.from_numpy(a.view(np.int16)).to("cuda:0").view(torch.bfloat16)
         return torch.from_numpy(a).to("cuda:0")
 
+    @property
+    def aliased(self):
+        return self.n_blobs < self.cfg.L * self.cfg.E
+
+    def blob(self, l, e):
+        return self.blobs[(l * self.cfg.E + e) % self.n_blobs]
+
     def blob_ptr(self, l, e):
-        return self.blobs[l * self.cfg.E + e].data_ptr()
+        return self.blob(l, e).data_ptr()
 
     def shared_ptrs(self):
         if self.shared is None:
@@ -468,7 +519,7 @@ def make_ctx(wl, pred, cache=None):
 
 
 def run_tokens(ctx, wl, first, n, y, mode):
-    T = wl.cfg.T
+    T = wl.T
     for i in range(n):
         t = first + i
         ctx.token(t, wl.x[t % T], y, mode=mode)
@@ -519,7 +570,7 @@ def host_pool(wl, pinned_gb):
     cfg = wl.cfg
     blob = cfg.blob_bytes
     n_all = cfg.L * cfg.E
-    M = min(n_all, int(pinned_gb * 1e9) // blob)
+    M = min(wl.n_blobs, int(pinned_gb * 1e9) // blob)
     t0 = time.time()
     pool = S.PinnedHost(M * blob)
     host = pool.tensor()
@@ -561,7 +612,7 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
         run_tokens(ctx, wl, 0, n_tokens, y, mode)
     else:
         kv, nbytes, out = attn
-        T = cfg.T
+        T = wl.T
         for t in range(n_tokens):
             for l in range(cfg.L):
                 S.calib_read(kv, nbytes, out)
@@ -628,7 +679,8 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
     arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
                         device="cuda:0")
     streams = (torch.cuda.Stream(), torch.cuda.Stream())
-    variants = [v for v in offload_variants(cfg) if only is None or v[0] in (only, "on_demand")]
+    keep = None if only is None else set(only.split(",")) | {"on_demand"}
+    variants = [v for v in offload_variants(cfg) if keep is None or v[0] in keep]
     out = {}
     for v in variants:
         out[v[0]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)
@@ -752,7 +804,7 @@ def near_tie_rows(wl, warmup, steps, eps=1e-4):
     wg = [exact(W.to_storage(cfg, g)) for g in wl.wg_f64]
     n, rows = 0, 0
     for i in range(steps):
-        t = (warmup + i) % cfg.T
+        t = (warmup + i) % wl.T
         for l in range(cfg.L):
             z = np.sort(exact(wl.x_store[t][l]) @ wg[l].T, axis=1)[:, ::-1]
             n += int(np.sum(z[:, cfg.K - 1] - z[:, cfg.K] < eps))
@@ -794,7 +846,7 @@ def cpu_baseline(wl, max_tokens, target_s):
         return b[:n].reshape(Ii, Hh), b[n:2 * n].reshape(Ii, Hh), b[2 * n:].reshape(Hh, Ii)
 
     n_tokens = 0
-    for t in range(min(max_tokens, cfg.T)):
+    for t in range(min(max_tokens, wl.T)):
         if timed >= target_s:
             break
         n_tokens += 1
@@ -810,7 +862,7 @@ def cpu_baseline(wl, max_tokens, target_s):
             cache.acquire(l, U, t * cfg.L + l + 1)
             timed += time.perf_counter() - t0
             used[0] = 0
-            experts = {e: mats(wl.blobs[l * cfg.E + e]) for e in U}
+            experts = {e: mats(wl.blob(l, e)) for e in U}
             shared = [mats(wl.shared[l * cfg.n_shared + s]) for s in range(cfg.n_shared)]
             t0 = time.perf_counter()
             moe_ffn(x, r["idx"], r["w"], lambda e: experts[e], shared=shared)
@@ -837,6 +889,9 @@ def main():
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats)
         return
+    if args.summarize_offload:
+        summarize_offload(args.summarize_offload)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (this build has no "
               f"multi-GPU path)", file=sys.stderr)
@@ -857,7 +912,14 @@ def main():
         return
     cfg = W.CONFIGS[args.config]
     log(f"workload {cfg.name}")
-    wl = Workload(cfg)
+    total = torch.cuda.get_device_properties(0).total_memory
+    if cfg.L * cfg.E * cfg.blob_bytes > 0.8 * total:
+        # the stack does not fit in HBM: alias a pool of distinct blobs, and
+        # generate hidden states only for the tokens this run decodes
+        n_tok = max(args.warmup + args.steps, args.offload_tokens, 1)
+        wl = Workload(cfg, hbm_blobs=int(args.hbm_pool_gb * 1e9) // cfg.blob_bytes, x_tokens=n_tok)
+    else:
+        wl = Workload(cfg)
     if args.attention_sweep:
         contexts = [int(c) for c in args.attention_sweep.split(",")]
         r = hbm_resident(wl, 40, 5)
@@ -902,7 +964,11 @@ def main():
         "data": "synthetic (seeded planted-Markov routing, N(0, 0.02) expert weights)",
         "config": {"workload": cfg.name, "layers": cfg.L, "hidden": cfg.H, "intermediate": cfg.I,
                    "experts": cfg.E, "shared_experts": cfg.n_shared, "top_k": cfg.K, "global_batch": cfg.B,
-                   "mode": "all experts HBM-resident, ST-MoE predictor on", "parallelism": "none (1 GPU)",
+                   "mode": ("all experts HBM-resident, ST-MoE predictor on" if not wl.aliased else
+                            f"HBM-resident stand-in: {wl.n_blobs} distinct expert blobs in HBM, expert (l, e) "
+                            f"reads blob (l*E + e) mod {wl.n_blobs} (the stack does not fit in HBM); "
+                            f"ST-MoE predictor on"),
+                   "parallelism": "none (1 GPU)",
                    "launch": "eager launches; predictor update/predict on a side stream beside the FFN"},
         "roofline": {
             "bound": "hbm", "kernel": "ffn_gate_up",

@@ -23,10 +23,8 @@ struct RouteArgs {
 };
 
 template <bool BF16>
-__device__ __forceinline__ void dot_chunk(const void* wrow, const void* xrow, int c, float& acc) {
+__device__ __forceinline__ void dot_chunk(const uint4 wv, const uint4 xv, float& acc) {
     // one 16-byte chunk: 8 bf16 or 4 fp32 values of the row and of x
-    const uint4 wv = reinterpret_cast<const uint4*>(wrow)[c];
-    const uint4 xv = reinterpret_cast<const uint4*>(xrow)[c];
     if (BF16) {
         acc += bf16_lo(wv.x) * bf16_lo(xv.x) + bf16_hi(wv.x) * bf16_hi(xv.x);
         acc += bf16_lo(wv.y) * bf16_lo(xv.y) + bf16_hi(wv.y) * bf16_hi(xv.y);
@@ -49,27 +47,54 @@ __device__ __forceinline__ uint32_t order_key(float v) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Logits of expert row blockIdx.x for every token, written to the workspace.
-template <bool BF16>
+// Logits of expert row blockIdx.x for the tokens of row group blockIdx.y
+// (NB tokens per group), written to the workspace.  The 256 lanes split H
+// into 16-byte chunks, two chunks per step, and every chunk of the group's
+// tokens is loaded before any is used, so a workgroup costs one round of load
+// latency per step.  Each lane adds its chunks in ascending order, then a DPP
+// wave sum and an LDS combine in wave order: a token's logit does not depend
+// on NB or on the grid.
+template <bool BF16, int NB>
 __device__ void expert_logits(const RouteArgs& a, float (*part)[kThreads / 64]) {
-    const int e = blockIdx.x;
+    const int e = blockIdx.x, b0 = blockIdx.y * NB;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int esz = BF16 ? 2 : 4;
     const int chunks = a.H * esz / 16;
-    const char* wrow = reinterpret_cast<const char*>(a.wg) + size_t(e) * a.H * esz;
-    for (int b = 0; b < a.B; ++b) {
-        const char* xrow = reinterpret_cast<const char*>(a.x) + size_t(b) * a.H * esz;
-        float acc = 0.f;
-        for (int c = tid; c < chunks; c += kThreads) dot_chunk<BF16>(wrow, xrow, c, acc);
-        acc = wave_sum(acc);
-        if (lane == 0) part[b][wave] = acc;
+    const uint4* wrow = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(a.wg) + size_t(e) * a.H * esz);
+    const uint4* x = reinterpret_cast<const uint4*>(a.x);
+    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+    float acc[NB];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) acc[u] = 0.f;
+    for (int c = tid; c < chunks; c += 2 * kThreads) {
+        const bool two = c + kThreads < chunks;
+        const uint4 w0 = wrow[c];
+        const uint4 w1 = two ? wrow[c + kThreads] : zero;
+        uint4 x0[NB], x1[NB];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const bool in = b0 + u < a.B;
+            x0[u] = in ? x[size_t(b0 + u) * chunks + c] : zero;
+            x1[u] = in && two ? x[size_t(b0 + u) * chunks + c + kThreads] : zero;
+        }
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            dot_chunk<BF16>(w0, x0[u], acc[u]);
+            if (two) dot_chunk<BF16>(w1, x1[u], acc[u]);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        const float v = wave_sum(acc[u]);
+        if (lane == 0) part[u][wave] = v;
     }
     __syncthreads();
-    if (tid < a.B) {
+    if (tid < NB && b0 + tid < a.B) {
+        const int b = b0 + tid;
         float z = 0.f;
         for (int w = 0; w < kThreads / 64; ++w) z += part[tid][w];
-        a.zbuf[tid * a.E + e] = z;
-        if (a.logits) a.logits[tid * a.E + e] = z;
+        a.zbuf[b * a.E + e] = z;
+        if (a.logits) a.logits[b * a.E + e] = z;
     }
 }
 

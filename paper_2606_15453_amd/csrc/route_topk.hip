@@ -1,10 +1,11 @@
 // Gating (Section 2): logits z = x W_g^T, softmax, top-K by logit.
 //
 // Two launches.  route_logits_kernel: one workgroup per expert row computes
-// its logits for all B tokens (256 lanes split H into 16-byte chunks, DPP
-// wave sums, one LDS combine) into the workspace.  route_tail_kernel: one
-// workgroup runs softmax and top-K, one wave per batch row, K rounds of a
-// wave-wide arg-max (value desc, index asc).
+// its logits for all B tokens (256 lanes split H into 16-byte chunks, up to
+// eight tokens per round of loads, DPP wave sums, one LDS combine) into the
+// workspace.  route_tail_kernel: one workgroup per batch row ranks every
+// expert by counting the logits that beat it (value desc, index asc) and
+// forms the softmax weights of the winners.
 #include "gating_dev.h"
 
 namespace stmoe {
@@ -12,14 +13,34 @@ namespace {
 
 using namespace gating;
 
-template <bool BF16>
+template <bool BF16, int NB>
 __global__ __launch_bounds__(kThreads) void route_logits_kernel(RouteArgs a) {
-    __shared__ float part[kMaxB][kThreads / 64];
-    expert_logits<BF16>(a, part);
+    __shared__ float part[NB][kThreads / 64];
+    expert_logits<BF16, NB>(a, part);
 }
 
+// Tokens per workgroup: four (one load round each, E x ceil(B/4)
+// workgroups), fewer for smaller batches.
+template <bool BF16>
+void launch_logits(const RouteArgs& a, hipStream_t s) {
+    if (a.B <= 1)
+        hipLaunchKernelGGL((route_logits_kernel<BF16, 1>), dim3(a.E), dim3(kThreads), 0, s, a);
+    else if (a.B <= 2)
+        hipLaunchKernelGGL((route_logits_kernel<BF16, 2>), dim3(a.E), dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL((route_logits_kernel<BF16, 4>), dim3(a.E, (a.B + 3) / 4), dim3(kThreads), 0, s, a);
+}
+
+// One workgroup per batch row (blockIdx.x): the tail's steps on that row
+// alone.  Ranking, softmax sum and weights of a row do not depend on the
+// other rows, so the results equal a one-workgroup tail over all rows.
 __global__ __launch_bounds__(kThreads) void route_tail_kernel(RouteArgs a) {
-    softmax_topk_tail(a, a.zbuf, nullptr);
+    const int b = blockIdx.x;
+    RouteArgs r = a;
+    r.B = 1;
+    r.idx = a.idx + size_t(b) * a.K;
+    r.w = a.w + size_t(b) * a.K;
+    softmax_topk_tail(r, a.zbuf + size_t(b) * a.E, nullptr);
 }
 
 }  // namespace
@@ -38,9 +59,9 @@ namespace stmoe {
 // Launch the per-expert logits kernel (the first of the router's two launches).
 int launch_route_logits(const RouteArgs& a, hipStream_t s) {
     if (a.bf16)
-        hipLaunchKernelGGL(route_logits_kernel<true>, dim3(a.E), dim3(kThreads), 0, s, a);
+        launch_logits<true>(a, s);
     else
-        hipLaunchKernelGGL(route_logits_kernel<false>, dim3(a.E), dim3(kThreads), 0, s, a);
+        launch_logits<false>(a, s);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }
@@ -74,7 +95,7 @@ extern "C" int moe_route_topk(const void* x, const void* w_gate, int B, int H, i
     a.logits = logits;
     a.zbuf = reinterpret_cast<float*>(ws);
     if (int rc = launch_route_logits(a, as_stream(stream))) return rc;
-    hipLaunchKernelGGL(route_tail_kernel, dim3(1), dim3(kThreads), 0, as_stream(stream), a);
+    hipLaunchKernelGGL(route_tail_kernel, dim3(B), dim3(kThreads), 0, as_stream(stream), a);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }

@@ -47,6 +47,8 @@ constexpr int kMaxSlots = kMaxE + kMaxShared;
 constexpr int kDownWgTarget = 256;    // workgroups the MFMA down phase aims for
 constexpr int kMfmaMinB = 8;          // batch from which the MFMA kernels run
 constexpr int kUpInFlight = 2;        // 16-byte chunks per row in flight per lane (GEMV gate/up)
+constexpr int kShortRowChunks = 4;    // down rows with at most this many chunks per lane are short: ...
+constexpr int kDownInFlightShort = 4; // ... the lane-group down kernel loads a slot's chunks in one step
 constexpr bool kStageX = true;        // GEMV gate/up: token activations staged in LDS ...
 constexpr int kXStageMax = 32768;     // ... when B*H*esz fits in this many bytes
 constexpr int kDownInFlight = 2;      // ... per row per lane in the whole-workgroup down kernel
@@ -351,9 +353,11 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
             }
         }
     };
+    // U chunks per row in flight; the fewer than U left over go in one
+    // guarded step.  Chunks are summed in ascending order either way.
     constexpr int U = kUpInFlight;
     int c = g;
-    for (; c + (U - 1) * G < cpr; c += U * G) {   // U chunks per row in flight
+    for (; c + (U - 1) * G < cpr; c += U * G) {
         uint4 qg[U][R], qu[U][R];
 #pragma unroll
         for (int u = 0; u < U; ++u)
@@ -365,14 +369,19 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
 #pragma unroll
         for (int u = 0; u < U; ++u) compute(c + u * G, qg[u], qu[u]);
     }
-    for (; c < cpr; c += G) {
-        uint4 ga[R], ua[R];
+    if (c < cpr) {
+        uint4 qg[U][R], qu[U][R];
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            ga[r] = ld_stream(wg + r * rowb + size_t(c) * 16);
-            ua[r] = ld_stream(wu + r * rowb + size_t(c) * 16);
-        }
-        compute(c, ga, ua);
+        for (int u = 0; u < U; ++u)
+            if (c + u * G < cpr)
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    qg[u][r] = ld_stream(wg + r * rowb + size_t(c + u * G) * 16);
+                    qu[u][r] = ld_stream(wu + r * rowb + size_t(c + u * G) * 16);
+                }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c + u * G < cpr) compute(c + u * G, qg[u], qu[u]);
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -530,13 +539,20 @@ __device__ __forceinline__ void down_slot(const char* wd, size_t rowb, int cpr, 
 #pragma unroll
         for (int u = 0; u < U; ++u) compute(c + u * S, q[u], xv[u]);
     }
-    for (; c < cpr; c += S) {
-        uint4 q[R];
-        float4 xv[NBX][NX];
+    if (c < cpr) {      // fewer than U steps left: one guarded step
+        uint4 q[U][R];
+        float4 xv[U][NBX][NX];
 #pragma unroll
-        for (int r = 0; r < R; ++r) q[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
-        load_x(c, xv);
-        compute(c, q, xv);
+        for (int u = 0; u < U; ++u)
+            if (c + u * S < cpr)
+#pragma unroll
+                for (int r = 0; r < R; ++r) q[u][r] = ld_stream(wd + r * rowb + size_t(c + u * S) * 16);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c + u * S < cpr) load_x(c + u * S, xv[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c + u * S < cpr) compute(c + u * S, q[u], xv[u]);
     }
 }
 
@@ -579,13 +595,20 @@ __device__ __forceinline__ void down_slot16(const char* wd, size_t rowb, int cpr
 #pragma unroll
         for (int u = 0; u < U; ++u) compute(c + u * S, q[u], xv[u]);
     }
-    for (; c < cpr; c += S) {
-        uint4 q[R];
-        uint4 xv[NBX];
+    if (c < cpr) {      // fewer than U steps left: one guarded step
+        uint4 q[U][R];
+        uint4 xv[U][NBX];
 #pragma unroll
-        for (int r = 0; r < R; ++r) q[r] = ld_stream(wd + r * rowb + size_t(c) * 16);
-        load_x(c, xv);
-        compute(c, q, xv);
+        for (int u = 0; u < U; ++u)
+            if (c + u * S < cpr)
+#pragma unroll
+                for (int r = 0; r < R; ++r) q[u][r] = ld_stream(wd + r * rowb + size_t(c + u * S) * 16);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c + u * S < cpr) load_x(c + u * S, xv[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c + u * S < cpr) compute(c + u * S, q[u], xv[u]);
     }
 }
 
@@ -594,7 +617,7 @@ __device__ __forceinline__ void down_slot16(const char* wd, size_t rowb, int cpr
 // w+4, ...) and their sums are added in wave order through LDS.  Each
 // activation chunk a lane loads serves its R rows: every workgroup reads all
 // activations, so R sets how much L2 traffic the weight rows carry along.
-template <bool BF, int G, int R, int NB>
+template <bool BF, int G, int R, int NB, int U>
 __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
     constexpr int kRows = (64 / G) * R;
     __shared__ PlanB p;
@@ -620,11 +643,11 @@ __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
 
     for (int j = wave; live && j < p.n_slots; j += kWaves) {
         if constexpr (BF && R < 4)
-            down_slot16<BF, R, NB, 2, (R == 1 && NB <= kDownCarryMaxNB)>(
+            down_slot16<BF, R, NB, U, (R == 1 && NB <= kDownCarryMaxNB)>(
                 slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb, rowb, cpr, g, G,
                 reinterpret_cast<const char*>(a.act) + size_t(j) * a.B * rowb, p.tok[j], acc);
         else
-            down_slot<BF, R, NB, 2, (R == 1 && NB <= kDownCarryMaxNB)>(
+            down_slot<BF, R, NB, U, (R == 1 && NB <= kDownCarryMaxNB)>(
                 slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb, rowb, cpr, g, G,
                 reinterpret_cast<const float*>(a.act) + size_t(j) * a.B * a.I, a.B, a.I, p.tok[j], acc);
     }
@@ -1306,21 +1329,30 @@ int launch_gate_up(const FfnArgs& a, const Shape& s, hipStream_t st) {
     else return launch_gate_up_r<BF, G, NB, 1>(a, s, st);
 }
 
-template <bool BF, int NB>
-void launch_down_rows(const FfnArgs& a, const Shape& s, hipStream_t st) {
+template <bool BF, int NB, int U>
+void launch_down_rows_u(const FfnArgs& a, const Shape& s, hipStream_t st) {
     const dim3 grid(unsigned(s.n_rb));
     if (s.dn_G == 16)
-        hipLaunchKernelGGL((ffn_down_rows<BF, 16, 1, NB>), grid, dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((ffn_down_rows<BF, 16, 1, NB, U>), grid, dim3(kThreads), 0, st, a);
     else if (s.dn_G == 32 && s.dn_R == 2)
-        hipLaunchKernelGGL((ffn_down_rows<BF, 32, 2, NB>), grid, dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((ffn_down_rows<BF, 32, 2, NB, U>), grid, dim3(kThreads), 0, st, a);
     else if (s.dn_G == 32)
-        hipLaunchKernelGGL((ffn_down_rows<BF, 32, 1, NB>), grid, dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((ffn_down_rows<BF, 32, 1, NB, U>), grid, dim3(kThreads), 0, st, a);
     else if (s.dn_R == 4)
-        hipLaunchKernelGGL((ffn_down_rows<BF, 64, 4, NB>), grid, dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((ffn_down_rows<BF, 64, 4, NB, U>), grid, dim3(kThreads), 0, st, a);
     else if (s.dn_R == 2)
-        hipLaunchKernelGGL((ffn_down_rows<BF, 64, 2, NB>), grid, dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((ffn_down_rows<BF, 64, 2, NB, U>), grid, dim3(kThreads), 0, st, a);
     else
-        hipLaunchKernelGGL((ffn_down_rows<BF, 64, 1, NB>), grid, dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((ffn_down_rows<BF, 64, 1, NB, U>), grid, dim3(kThreads), 0, st, a);
+}
+
+// short rows (at most kShortRowChunks chunks per lane) load a slot's chunks in one step
+template <bool BF, int NB>
+void launch_down_rows(const FfnArgs& a, const Shape& s, hipStream_t st) {
+    if ((a.I * (BF ? 2 : 4) / 16 + s.dn_G - 1) / s.dn_G <= kShortRowChunks)
+        launch_down_rows_u<BF, NB, kDownInFlightShort>(a, s, st);
+    else
+        launch_down_rows_u<BF, NB, 2>(a, s, st);
 }
 
 template <bool BF, int NB>

@@ -54,23 +54,24 @@ class FullStack:
         return b[:n].reshape(cfg.I, cfg.H), b[n:2 * n].reshape(cfg.I, cfg.H), b[2 * n:].reshape(cfg.H, cfg.I)
 
 
-def _gpu_decode(st, n_tokens):
+def _gpu_decode(st, n_tokens, cache=None, mode=None):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
     cfg = st.cfg
+    mode = S.MODE_STMOE if mode is None else mode
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(st.prof)
-    resident = [st.blobs[i].data_ptr() for i in range(cfg.L * cfg.E)]
+    resident = None if cache else [st.blobs[i].data_ptr() for i in range(cfg.L * cfg.E)]
     shared = None if st.shared is None else [st.shared[i].data_ptr() for i in range(st.shared.shape[0])]
     ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
-                          [g.data_ptr() for g in st.wg_dev], predictor=pred, resident_ptrs=resident,
-                          shared_ptrs=shared, n_shared=cfg.n_shared)
+                          [g.data_ptr() for g in st.wg_dev], predictor=pred, cache=cache,
+                          resident_ptrs=resident, shared_ptrs=shared, n_shared=cfg.n_shared)
     ctx.set_timing(1)
     idx_hist, ys = [], []
     for t in range(n_tokens):
         y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device=DEV)
-        ctx.token(t, st.x_dev[t], y, mode=S.MODE_STMOE)
+        ctx.token(t, st.x_dev[t], y, mode=mode)
         idx, _ = ctx.last_routing()
         idx_hist.append(idx)
         ys.append(y)
@@ -128,5 +129,60 @@ def test_full_size_decode_matches_oracle(name):
             assert err <= TOL, (t, l, err)
             del experts, shared
     finally:
+        del st
+        torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("mode,device", [(0, 0), (1, 0), (1, 1)])
+def test_full_size_capped_cache(mode, device):
+    """DeepSeek-V2-Lite shapes at full size (26 layers, 64 routed experts of
+    17.3 MB in a pinned host pool, 24 HBM slots per layer, two shared experts
+    in HBM, batch 4), decoded as the bench's capped runs do: the cache's
+    copy counts equal the oracle's cache policy, and every output is
+    bit-identical to the all-resident run (on-demand loading and ST-MoE
+    prefetch; decisions on the host or on the device)."""
+    import torch
+    from gpuhelp import DEV
+    from oracle.stmoe_oracle import decode_reference, decode_storage
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["dsv2lite"]
+    print(f"[full-size capped] {cfg.name}: mode {mode}, device decisions {device}", flush=True)
+    st = FullStack(cfg, N_TOKENS)
+    pool = None
+    try:
+        _, ys_res, _, _ = _gpu_decode(st, N_TOKENS)
+        blob = cfg.blob_bytes
+        pool = S.PinnedHost(cfg.L * cfg.E * blob)
+        host = pool.tensor()
+        for i in range(cfg.L * cfg.E):
+            host[i * blob:(i + 1) * blob].copy_(st.blobs[i].view(torch.uint8))
+        n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
+        arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, blob, n_stage), dtype=torch.uint8, device=DEV)
+        demand, side = torch.cuda.Stream(), torch.cuda.Stream()
+        warm = W.warm_sets(cfg, st.prof)
+        cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, blob, n_stage, arena,
+                              [pool.ptr + i * blob for i in range(cfg.L * cfg.E)], demand, side)
+        cache.warm(warm)
+        cache.set_device_policy(device)
+        idx_hist, ys, _, _ = _gpu_decode(st, N_TOKENS, cache=cache, mode=mode)
+        demand.synchronize()
+        side.synchronize()
+        cst = cache.stats()
+        cache.close()
+        del arena
+        for t in range(N_TOKENS):
+            assert torch.equal(ys[t], ys_res[t]), t
+        ref = decode_reference(cfg.L, cfg.E, cfg.K, cfg.B, lambda t, l: decode_storage(st.x_store[t][l]),
+                               lambda l: decode_storage(st.wg[l]), st.prof, N_TOKENS, C=cfg.C, warm=warm,
+                               mode=mode)
+        assert ref["tie_boundary"] == 0
+        n = ref["cache"].n
+        print(f"[full-size capped] counts {cst}", flush=True)
+        assert cst == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
+                           useful=n.useful, wasted=n.wasted)
+    finally:
+        if pool is not None:
+            pool.close()
         del st
         torch.cuda.empty_cache()

@@ -256,9 +256,14 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     if (e == hipSuccess) e = hipHostMalloc(&c->rec, size_t(c->B * c->K) * sizeof(int32_t) + ranked_bytes(c->E));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->rec_ev, hipEventDisableTiming);
     if (e == hipSuccess && !cache && pred) {
+        // the side stream's events only order kernels of this device (the
+        // kernel boundaries make their writes visible): no system-scope fence,
+        // which would write back the caches at every record
         e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_side, hipEventDisableTiming);
+        if (e == hipSuccess)
+            e = hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming | hipEventDisableSystemFence);
+        if (e == hipSuccess)
+            e = hipEventCreateWithFlags(&c->ev_side, hipEventDisableTiming | hipEventDisableSystemFence);
     }
     if (e == hipSuccess) e = hipMemset(c->route_ws, 0, c->route_ws_bytes);
     if (e == hipSuccess) e = hipMemset(c->ffn_ws, 0, c->ffn_ws_bytes);

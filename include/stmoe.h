@@ -297,7 +297,11 @@ typedef struct {
     const void* const* router_w;   /* host [L] device pointers to W_g [E][H] */
     const void* const* shared_w;   /* host [L*n_shared] device blob pointers, or NULL */
     const void* const* resident_w; /* host [L*E] device blob pointers when every routed
-                                      expert is in HBM (cache must then be NULL) */
+                                      expert is in HBM (cache must then be NULL).  Read
+                                      once at create: when every layer's E pointers are
+                                      equally spaced (one stride for all layers), the FFN
+                                      computes blob addresses from the layer's first
+                                      pointer and the stride */
 } moe_model_desc;
 
 typedef struct moe_ctx moe_ctx;

@@ -22,7 +22,7 @@ namespace stmoe {
 int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, int H, int I, int E,
                int dtype, const void* const* eptr, const void* const* sptr, int n_shared,
                float* y, void* ws, hipStream_t s, unsigned long long* n_experts, hipEvent_t ev_mid,
-               const float* logits, int renorm);
+               const float* logits, int renorm, const void* ebase, size_t estride);
 int route_logits(const void* x, const void* w_gate, int B, int H, int E, int dtype, float* z, hipStream_t s);
 void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_bytes);
 DeviceCache* expert_cache_device(expert_cache* c);
@@ -57,6 +57,11 @@ struct moe_ctx {
     int L, E, K, B, H, I, n_shared, dtype, renorm;
     size_t esz;
     std::vector<const void*> router;       // [L]
+    // resident blobs at a fixed stride within every layer (one allocation,
+    // as the seeded stacks lay them out): the FFN computes expert e's blob
+    // as rbase[layer] + e * rstride instead of loading it from the table
+    std::vector<const char*> rbase;        // [L], empty if the table has no such layout
+    size_t rstride = 0;
     stmoe_predictor* pred = nullptr;
     expert_cache* cache = nullptr;
     hipStream_t s = nullptr;
@@ -240,6 +245,17 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     c->cache = cache;
     c->s = as_stream(compute_stream);
     c->host_table.assign(c->E, nullptr);
+    if (d->resident_w) {
+        auto at = [&](int l, int x) { return reinterpret_cast<uintptr_t>(d->resident_w[size_t(l) * d->E + x]); };
+        const uintptr_t stride = d->E > 1 ? at(0, 1) - at(0, 0) : 0;
+        bool strided = d->E == 1 || at(0, 1) > at(0, 0);
+        for (int l = 0; strided && l < d->L; ++l)
+            for (int x = 0; strided && x < d->E; ++x) strided = at(l, x) == at(l, 0) + uintptr_t(x) * stride;
+        if (strided) {
+            c->rstride = size_t(stride);
+            for (int l = 0; l < d->L; ++l) c->rbase.push_back(reinterpret_cast<const char*>(at(l, 0)));
+        }
+    }
     const size_t LBK = size_t(c->L) * c->B * c->K;
     c->route_ws_bytes = moe_route_workspace_bytes(c->B, c->E);
     c->ffn_ws_bytes = moe_expert_ffn_workspace_bytes(c->B, c->K, c->E, c->H, c->I, c->n_shared, c->dtype);
@@ -433,7 +449,8 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
     if (int rc = ffn_launch(x, idx_l, w_l, B, K, c->H, c->I, E, c->dtype, c->tables + size_t(layer) * E,
                             c->n_shared ? c->shared + size_t(layer) * c->n_shared : nullptr, c->n_shared,
                             y, c->ffn_ws, c->s, timed ? c->n_experts : nullptr, e1,
-                            route_in_ffn ? zbuf : nullptr, c->renorm))
+                            route_in_ffn ? zbuf : nullptr, c->renorm,
+                            c->rbase.empty() ? nullptr : c->rbase[size_t(layer)], c->rstride))
         return rc;
     if (timed) {
         if (int rc = stamp_event(tl.down1, c->s)) return rc;

@@ -63,6 +63,8 @@ struct FfnArgs {
     const int32_t* idx;              // [B][K]
     const float* w;                  // [B][K]
     const void* const* eptr;         // [E] device blob pointers
+    const char* ebase;               // or, when not null, expert e's blob at ebase + e * estride
+    size_t estride;
     const void* const* sptr;         // [n_shared] or null
     int B, K, H, I, E, n_shared;
     void* act;                       // [slots][B][I]: bf16 (MFMA; GEMV per act_bf16) or fp32
@@ -122,6 +124,12 @@ __device__ void route_into_plan(const FfnArgs& a, Plan& p) {
     }
 }
 
+// Routed expert e's blob: computed from a base and stride where the caller's
+// blobs are laid out that way (no dependent load from the pointer table).
+__device__ __forceinline__ const char* routed_blob(const FfnArgs& a, int e) {
+    return a.ebase ? a.ebase + size_t(e) * a.estride : reinterpret_cast<const char*>(a.eptr[e]);
+}
+
 // Build the slot plan in LDS (all threads participate; ends with a barrier).
 // Slot order: selected routed experts ascending, then shared experts.  With
 // `route` and router logits in the arguments the selection is computed here
@@ -156,7 +164,7 @@ __device__ void build_plan(const FfnArgs& a, P& p, bool route = false) {
         for (int q = 0; q < (e >> 5); ++q) rank += __popc(p.sel[q]);
         atomicOr(&p.tok[rank], 1u << b);
         p.expert[rank] = e;
-        if constexpr (kBlobs) p.blob[rank] = reinterpret_cast<const char*>(a.eptr[e]);   // equal per rank
+        if constexpr (kBlobs) p.blob[rank] = routed_blob(a, e);   // equal per rank
     }
     for (int s = tid; s < a.n_shared; s += kThreads) {
         p.expert[total + s] = -1 - s;
@@ -181,7 +189,7 @@ __device__ __forceinline__ float slot_weight(const FfnArgs& a, const Plan& p, in
 
 __device__ __forceinline__ const char* slot_blob(const FfnArgs& a, const Plan& p, int j) {
     const int e = p.expert[j];
-    return reinterpret_cast<const char*>(e >= 0 ? a.eptr[e] : a.sptr[-1 - e]);
+    return e >= 0 ? routed_blob(a, e) : reinterpret_cast<const char*>(a.sptr[-1 - e]);
 }
 __device__ __forceinline__ const char* slot_blob(const FfnArgs&, const PlanB& p, int j) { return p.blob[j]; }
 
@@ -1459,7 +1467,7 @@ size_t ffn_workspace_bytes(int B, int K, int E, int H, int I, int n_shared, int 
 int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, int H, int I, int E,
                int dtype, const void* const* eptr, const void* const* sptr, int n_shared,
                float* y, void* ws, hipStream_t st, unsigned long long* n_experts, hipEvent_t ev_mid,
-               const float* logits, int renorm) {
+               const float* logits, int renorm, const void* ebase, size_t estride) {
     if (logits && B * E > kRouteInFfnMax) {
         set_error("ffn_launch: routing inside the FFN needs B*E <= 256");
         return STMOE_EINVAL;
@@ -1472,6 +1480,8 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
     a.idx = idx;
     a.w = w;
     a.eptr = eptr;
+    a.ebase = reinterpret_cast<const char*>(ebase);
+    a.estride = estride;
     a.sptr = sptr;
     a.B = B;
     a.K = K;
@@ -1522,5 +1532,5 @@ extern "C" int moe_expert_ffn(const void* x, const int32_t* topk_idx, const floa
     STMOE_CHECK((reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(ws) & 255) == 0,
                 "x must be 16-byte and ws 256-byte aligned");
     return ffn_launch(x, topk_idx, topk_w, B, K, H, I, E, dtype, expert_ptrs, shared_ptrs, n_shared, y,
-                      ws, as_stream(stream), nullptr, nullptr, nullptr, 0);
+                      ws, as_stream(stream), nullptr, nullptr, nullptr, 0, nullptr, 0);
 }

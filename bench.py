@@ -58,6 +58,9 @@ def parse():
                     help="the CPU oracle sample stops after the token that reaches this much timed work")
     ap.add_argument("--offload-only", default=None, metavar="VARIANT[,VARIANT...]",
                     help="run only these capped-cache variants (and on-demand loading)")
+    ap.add_argument("--pool", choices=("host", "hbm"), default="host",
+                    help="backing pool of the capped cache: pinned host memory (PCIe) or the HBM-resident "
+                         "stack (device-to-device copies, a faster tier)")
     ap.add_argument("--hbm-pool-gb", type=float, default=80.0,
                     help="for a stack larger than HBM: distinct expert blobs generated in HBM "
                          "(expert (l, e) reads blob (l*E + e) mod their number)")
@@ -84,6 +87,7 @@ def parse():
 
 
 COUNTERS_MD = os.path.join(ROOT, "profiles", "ffn_gate_up_mixtral8x7b_b1_counters.md")
+POOL_TIER = "host"      # set from --pool
 FFN_SOURCES = [os.path.join(ROOT, "paper_2606_15453_amd", "csrc", f)
                for f in ("expert_ffn.hip", "gating_dev.h", "common.h")]
 CALIB_BYTES = 1 << 30
@@ -560,6 +564,16 @@ def hbm_resident(wl, steps, warmup):
                 host_issue_us_per_layer=host_us, stages_us=stages)
 
 
+def expert_pool(wl, pinned_gb, tier):
+    """The backing pool the capped cache copies from: pinned host memory over
+    PCIe ("host"), or the HBM-resident stack itself ("hbm", copies device to
+    device), which models a backing tier much faster than the host link."""
+    if tier == "hbm":
+        cfg = wl.cfg
+        return None, [wl.blob_ptr(l, e) for l in range(cfg.L) for e in range(cfg.E)], wl.n_blobs
+    return host_pool(wl, pinned_gb)
+
+
 def host_pool(wl, pinned_gb):
     """Pinned host copies of the expert blobs.  The pool holds M = min(L*E,
     pinned budget / blob) distinct blobs; expert (l, e) is copied from pool
@@ -674,7 +688,7 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
     import torch
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
-    pool, ptrs, M = host_pool(wl, pinned_gb)
+    pool, ptrs, M = expert_pool(wl, pinned_gb, POOL_TIER)
     n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
     arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
                         device="cuda:0")
@@ -689,7 +703,9 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
                               for name, *_ in variants if name != "on_demand"}
     out["cache_slots_per_layer"] = cfg.C
     out["host_pool"] = {"distinct_blobs": M, "experts": cfg.L * cfg.E, "slot_of_expert": "(l*E + e) mod distinct_blobs"}
-    out["h2d_link"] = "PCIe, pinned host memory, hipMemcpyAsync on demand/side streams"
+    out["h2d_link"] = ("PCIe, pinned host memory, hipMemcpyAsync on demand/side streams" if POOL_TIER == "host" else
+                       "device-to-device copies from the HBM-resident stack (a backing tier faster than PCIe)")
+    out["pool_tier"] = POOL_TIER
     del arena
     del pool
     return out
@@ -710,7 +726,7 @@ def attention_sweep(wl, key, n_tokens, resident_ms_per_token, pinned_gb, context
     import torch
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
-    pool, ptrs, M = host_pool(wl, pinned_gb)
+    pool, ptrs, M = expert_pool(wl, pinned_gb, POOL_TIER)
     n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
     arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
                         device="cuda:0")
@@ -759,7 +775,7 @@ def offload_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, budgets):
     import torch
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
-    pool, ptrs, M = host_pool(wl, pinned_gb)
+    pool, ptrs, M = expert_pool(wl, pinned_gb, POOL_TIER)
     cmax = max(budgets)
     n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - min(budgets))
     arena = torch.empty(S.cache_arena_bytes(cfg.L, cmax, cfg.blob_bytes, n_stage), dtype=torch.uint8,
@@ -910,6 +926,8 @@ def main():
     if args.predictor_sweep:
         predictor_sweep()
         return
+    global POOL_TIER
+    POOL_TIER = args.pool
     cfg = W.CONFIGS[args.config]
     log(f"workload {cfg.name}")
     total = torch.cuda.get_device_properties(0).total_memory

@@ -235,7 +235,10 @@ int stmoe_policy_stats(const stmoe_policy* p, stmoe_cache_stats* out);
  * reader and its previous copy have completed).
  *
  *   arena       device, at least expert_cache_arena_bytes(L, C, blob, n_stage)
- *   host_blobs  host array [L*E] of pinned host blob pointers
+ *   host_blobs  host array [L*E] of pinned host blob pointers.  Device
+ *               pointers are accepted too (the copies then run device to
+ *               device: a pool in another HBM region models a backing tier
+ *               much faster than the host link)
  *   n_stage     staging slots for overflow experts (>= 1 when a layer can
  *               select more distinct experts than C)
  * ---------------------------------------------------------------------- */
@@ -267,9 +270,9 @@ int expert_cache_set_prefetch_order(expert_cache* c, int after_demand);
  * by a copy kernel on the compute stream, prefetches by one on the side
  * stream; experts beyond the layer's slots (the host path's staging
  * overflow) are read by the FFN straight from host memory, so the staging
- * slots are not used.  Every host blob must be pinned host memory that the
- * device maps at the same address (hipHostMalloc, torch pin_memory);
- * otherwise STMOE_EINVAL and nothing changes.  While on,
+ * slots are not used.  Every pool blob must be device memory or pinned host
+ * memory that the device maps at the same address (hipHostMalloc, torch
+ * pin_memory); otherwise STMOE_EINVAL and nothing changes.  While on,
  * expert_cache_acquire / _prefetch / _warm return STMOE_ESTATE and
  * expert_cache_stats reads the device counters.  on = 0 moves the state
  * back to the host policy.  [sync] */

@@ -254,15 +254,17 @@ void free_dc(DeviceCache* d) {
 int device_cache_create(const PolicyState& ps, char* arena, size_t blob, const void* const* host_blobs,
                         hipStream_t side, DeviceCache** out) {
     STMOE_CHECK(ps.E <= kMaxE && ps.C <= kMaxE && blob % 16 == 0, "bad cache shape for device decisions");
-    // every host blob must be reachable from kernels at its own address
+    // every pool blob must be reachable from kernels at its own address:
+    // pinned host memory mapped at the same address, or device memory
     std::vector<const char*> hp(size_t(ps.L) * ps.E);
     for (size_t i = 0; i < hp.size(); ++i) {
         hipPointerAttribute_t at{};
-        if (hipPointerGetAttributes(&at, host_blobs[i]) != hipSuccess || at.type != hipMemoryTypeHost ||
+        if (hipPointerGetAttributes(&at, host_blobs[i]) != hipSuccess ||
+            (at.type != hipMemoryTypeHost && at.type != hipMemoryTypeDevice) ||
             at.devicePointer != host_blobs[i]) {
             (void)hipGetLastError();
-            set_error("expert_cache_set_device_policy: host blob " + std::to_string(i) +
-                      " is not pinned host memory mapped at its own address");
+            set_error("expert_cache_set_device_policy: pool blob " + std::to_string(i) +
+                      " is neither device memory nor pinned host memory mapped at its own address");
             return STMOE_EINVAL;
         }
         hp[i] = static_cast<const char*>(host_blobs[i]);

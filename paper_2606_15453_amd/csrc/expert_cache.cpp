@@ -240,7 +240,7 @@ namespace {
 int copy_into(expert_cache* c, int gid, const void* src, hipStream_t s) {
     if (c->loaded_set[gid]) STMOE_HIP(hipStreamWaitEvent(s, c->loaded[gid], 0));
     if (c->released_set[gid]) STMOE_HIP(hipStreamWaitEvent(s, c->released[gid], 0));
-    STMOE_HIP(hipMemcpyAsync(c->slot_ptr(gid), src, c->blob, hipMemcpyHostToDevice, s));
+    STMOE_HIP(hipMemcpyAsync(c->slot_ptr(gid), src, c->blob, hipMemcpyDefault, s));
     STMOE_HIP(hipEventRecord(c->loaded[gid], s));
     c->loaded_set[gid] = 1;
     return STMOE_OK;
@@ -335,7 +335,7 @@ extern "C" int expert_cache_warm(expert_cache* c, const int32_t* warm) {
             const int e = warm[l * c->C + s];
             if (e < 0) continue;
             STMOE_HIP(hipMemcpyAsync(c->slot_ptr(l * c->C + s), c->host[size_t(l) * c->E + e], c->blob,
-                                     hipMemcpyHostToDevice, c->demand));
+                                     hipMemcpyDefault, c->demand));
         }
     STMOE_HIP(hipStreamSynchronize(c->demand));
     std::fill(c->loaded_set.begin(), c->loaded_set.end(), 0);

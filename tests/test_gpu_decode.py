@@ -48,7 +48,7 @@ def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True):
 
 
 def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0, device=0,
-             device_until=None):
+             device_until=None, device_pool=False):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
@@ -62,7 +62,7 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
         host = []
         for l in range(cfg.L):
             for e in range(cfg.E):
-                h = st.blobs[l][e].cpu().pin_memory()
+                h = st.blobs[l][e] if device_pool else st.blobs[l][e].cpu().pin_memory()
                 keep.append(h)
                 host.append(h.data_ptr())
         n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
@@ -202,6 +202,24 @@ def test_decode_capped_counts_and_invariance(name, over, mode, after_demand, dev
     assert cst == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
                        useful=n.useful, wasted=n.wasted)
 
+
+
+@pytest.mark.parametrize("mode,device", [(0, 0), (1, 0), (1, 1)])
+def test_decode_capped_device_memory_pool(mode, device):
+    """A backing pool in device memory (copies run device to device): the same
+    decisions and counts as the oracle's policy and outputs bit-identical to
+    the all-resident run, with host or device decisions."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen30b"].scaled(L=4, T=6, P=3, C=10)
+    st = Stack(cfg)
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    _, ys, _, cst = _run_gpu(st, mode, capped=True, device=device, device_pool=True)
+    for t in range(cfg.T):
+        assert np.array_equal(ys[t], ys_res[t])
+    ref = _oracle(st, mode, C=cfg.C)
+    n = ref["cache"].n
+    assert cst == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
+                       useful=n.useful, wasted=n.wasted)
 
 
 @pytest.mark.parametrize("name,over", [CFGS[1], CFGS[3]])

@@ -51,6 +51,7 @@ constexpr int kShortRowChunks = 4;    // down rows with at most this many chunks
 constexpr int kDownInFlightShort = 4; // ... the lane-group down kernel loads a slot's chunks in one step
 constexpr bool kStageX = true;        // GEMV gate/up: token activations staged in LDS ...
 constexpr int kXStageMax = 32768;     // ... when B*H*esz fits in this many bytes
+constexpr int kStageXMaskedFromNB = 4;  // ... and from this many token columns only the slot's tokens
 constexpr int kDownInFlight = 2;      // ... per row per lane in the whole-workgroup down kernel
 constexpr int kDownCarryMaxNB = 4;    // lane-group down, one row per group: activations loaded with the
                                       // weights up to this many tokens (more rows: the registers cost more)
@@ -306,25 +307,39 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up(FfnArgs a, int blocks_pe
     extern __shared__ uint4 x_lds[];
     constexpr int esz = BF ? 2 : 4;
     constexpr int kXRegs = kXStageMax / 16 / kThreads;
+    // few token columns: every token, loads issued before the routing
+    // prologue; more: only the tokens routed to this workgroup's slot
+    // (typically one or two), after the plan names them
+    constexpr bool kMasked = XL && NB >= kStageXMaskedFromNB;
     const int nx = XL ? a.B * a.H * esz / 16 : 0;
+    const int cpx = a.H * esz / 16;
+    const char* xsrc = reinterpret_cast<const char*>(a.x);
     uint4 xr[kXRegs];
-    if (XL) {
+    if (XL && !kMasked) {
 #pragma unroll
         for (int u = 0; u < kXRegs; ++u) {
             const int i = u * kThreads + int(threadIdx.x);
-            if (i < nx) xr[u] = ld_cached(reinterpret_cast<const char*>(a.x) + size_t(i) * 16);
+            if (i < nx) xr[u] = ld_cached(xsrc + size_t(i) * 16);
         }
     }
     build_plan(a, p, true);
+    const int j = blockIdx.x / blocks_per_slot;
     if (XL) {
+        const unsigned tx = kMasked ? (j < p.n_slots ? p.tok[j] : 0u) : ~0u;
+        if (kMasked) {
+#pragma unroll
+            for (int u = 0; u < kXRegs; ++u) {
+                const int i = u * kThreads + int(threadIdx.x);
+                if (i < nx && ((tx >> (i / cpx)) & 1u)) xr[u] = ld_cached(xsrc + size_t(i) * 16);
+            }
+        }
 #pragma unroll
         for (int u = 0; u < kXRegs; ++u) {
             const int i = u * kThreads + int(threadIdx.x);
-            if (i < nx) x_lds[i] = xr[u];
+            if (i < nx && ((tx >> (i / cpx)) & 1u)) x_lds[i] = xr[u];
         }
         __syncthreads();
     }
-    const int j = blockIdx.x / blocks_per_slot;
     if (j >= p.n_slots) return;
     const int rows_per_block = kWaves * (64 / G) * R;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;

@@ -1249,7 +1249,7 @@ constexpr int kDownWgR = 4;   // rows per workgroup (whole-workgroup down)
 constexpr int kUpWgR = 0;     // rows per workgroup of the whole-workgroup gate/up kernel (0: lane groups)
 constexpr int kDownForceG = 0;  // lanes per down row (0: by row length)
 constexpr int kMfmaNT = 0;      // 1: force one 16-row tile per wave in the MFMA gate/up kernel
-constexpr int kMfmaDownNT = 4;  // 16-row tiles per wave of the MFMA down kernel (1, 2 or 4)
+constexpr int kMfmaDownNT = 2;  // 16-row tiles per wave of the MFMA down kernel (1, 2 or 4)
 constexpr int kMfmaSplitKBelow = 2048;  // split-K MFMA gate/up when the tiled grid has fewer workgroups
 constexpr bool kMfmaUpLds = true;       // MFMA gate/up stages weight rows through LDS (H % 128 == 0;
                                         // split-K: H % 512 == 0)

@@ -307,6 +307,7 @@ def counters_workload():
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(wl.prof)
     ctx = make_ctx(wl, pred)
+    ctx.set_predictor_batch(True)
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
     run_tokens(ctx, wl, 0, COUNTER_TOKENS, y, S.MODE_STMOE)
     torch.cuda.synchronize()
@@ -536,6 +537,7 @@ def hbm_resident(wl, steps, warmup):
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(wl.prof)
     ctx = make_ctx(wl, pred)
+    ctx.set_predictor_batch(True)     # the predictor's layers in one side-stream launch per token
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
     run_tokens(ctx, wl, 0, warmup, y, S.MODE_STMOE)
     torch.cuda.synchronize()
@@ -987,7 +989,8 @@ def main():
                             f"reads blob (l*E + e) mod {wl.n_blobs} (the stack does not fit in HBM); "
                             f"ST-MoE predictor on"),
                    "parallelism": "none (1 GPU)",
-                   "launch": "eager launches; predictor update/predict on a side stream beside the FFN"},
+                   "launch": "eager launches; the predictor's update/predict of every layer in one side-stream "
+                             "launch per token, overlapping the next token"},
         "roofline": {
             "bound": "hbm", "kernel": "ffn_gate_up",
             "achieved": round(up_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",

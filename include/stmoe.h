@@ -347,6 +347,18 @@ int moe_ctx_set_online_update(moe_ctx* ctx, int on);
  * is the staging buffer itself).  The graph is captured at the first such
  * call and again when `mode` changes; results equal the eager calls. */
 int moe_decode_token(moe_ctx* ctx, int token, const void* xs, float* ys, int mode);
+/* Per-token predictor launches for moe_decode_token (contexts without a
+ * cache, with a predictor; on = 1 or 0, default 0).  Without a cache the
+ * prediction feeds no copy, so the verify/update of every layer and its
+ * next-layer prediction (Algorithm 3, Eq. 1, in layer order) can run as one
+ * side-stream launch after the token's last layer instead of one launch per
+ * layer: the same tables and hit statistics, three host calls per token
+ * instead of three per layer.  Each token's selections go to a buffer of its
+ * parity, so the launch overlaps the next token; the compute stream waits
+ * for it two tokens later.  moe_decode_layer keeps per-layer launches.
+ * STMOE_EINVAL with a cache, without a predictor or with graph replay on.
+ * [sync] */
+int moe_ctx_set_predictor_batch(moe_ctx* ctx, int on);
 /* Graph replay of moe_decode_token on (1) or off (0); contexts without a
  * cache only.  Turning it on allocates the staging buffers (L*B*H elements
  * of the storage dtype and L*B*H fp32) and an internal stream; the graph

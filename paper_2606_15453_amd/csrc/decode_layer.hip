@@ -24,6 +24,9 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
                float* y, void* ws, hipStream_t s, unsigned long long* n_experts, hipEvent_t ev_mid,
                const float* logits, int renorm, const void* ebase, size_t estride);
 int route_logits(const void* x, const void* w_gate, int B, int H, int E, int dtype, float* z, hipStream_t s);
+size_t update_predict_seq_bytes(int L);
+int update_predict_seq_args(stmoe_predictor* p, const int32_t* idx_all, int use, int online, void* dev_args);
+int update_predict_seq(stmoe_predictor* p, const void* dev_args, hipStream_t s);
 void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_bytes);
 DeviceCache* expert_cache_device(expert_cache* c);
 int expert_cache_after_demand(const expert_cache* c);
@@ -71,8 +74,18 @@ struct moe_ctx {
     hipStream_t side = nullptr;
     hipEvent_t ev_sel = nullptr, ev_side = nullptr;
     bool side_pending = false;
-    int32_t* idx = nullptr;                // [L][B][K] device
-    float* w = nullptr;                    // [L][B][K] device
+    // per-token predictor work (resident contexts, moe_decode_token): the
+    // layers' selections go to the buffer of the token's parity, and one
+    // side-stream launch per token runs every layer's update and prediction;
+    // ev_tok[par] marks it, and the buffer is rewritten two tokens later
+    bool pred_batch = false;
+    int cur_par = 0, last_par = 0;
+    hipEvent_t ev_tok[2] = {nullptr, nullptr};
+    bool tok_pending[2] = {false, false};
+    void* seq_args[2] = {nullptr, nullptr};   // device arguments of update_predict_seq per parity
+    int seq_key[2] = {-1, -1};                // (use, online) they were built for
+    int32_t* idx = nullptr;                // [2][L][B][K] device (parity 0 unless pred_batch)
+    float* w = nullptr;                    // [2][L][B][K] device
     int32_t* ranked = nullptr;             // device: ranked [E], n_ranked [1], max scores [E] (uint8)
     void* route_ws = nullptr;
     size_t route_ws_bytes = 0;
@@ -128,6 +141,10 @@ void free_ctx(moe_ctx* c) {
     }
     if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
     if (c->ev_side) (void)hipEventDestroy(c->ev_side);
+    for (int i = 0; i < 2; ++i) {
+        if (c->ev_tok[i]) (void)hipEventDestroy(c->ev_tok[i]);
+        (void)hipFree(c->seq_args[i]);
+    }
     if (c->gs) {
         (void)hipStreamSynchronize(c->gs);
         (void)hipStreamDestroy(c->gs);
@@ -260,8 +277,8 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     c->route_ws_bytes = moe_route_workspace_bytes(c->B, c->E);
     c->ffn_ws_bytes = moe_expert_ffn_workspace_bytes(c->B, c->K, c->E, c->H, c->I, c->n_shared, c->dtype);
     hipError_t e = hipSuccess;
-    if (e == hipSuccess) e = hipMalloc(&c->idx, LBK * sizeof(int32_t));
-    if (e == hipSuccess) e = hipMalloc(&c->w, LBK * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(&c->idx, 2 * LBK * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMalloc(&c->w, 2 * LBK * sizeof(float));
     if (e == hipSuccess) e = hipMalloc(&c->ranked, ranked_bytes(c->E));
     if (e == hipSuccess) e = hipMalloc(&c->route_ws, c->route_ws_bytes);
     if (e == hipSuccess) e = hipMalloc(&c->ffn_ws, c->ffn_ws_bytes);
@@ -283,8 +300,8 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     }
     if (e == hipSuccess) e = hipMemset(c->route_ws, 0, c->route_ws_bytes);
     if (e == hipSuccess) e = hipMemset(c->ffn_ws, 0, c->ffn_ws_bytes);
-    if (e == hipSuccess) e = hipMemset(c->idx, 0, LBK * sizeof(int32_t));
-    if (e == hipSuccess) e = hipMemset(c->w, 0, LBK * sizeof(float));
+    if (e == hipSuccess) e = hipMemset(c->idx, 0, 2 * LBK * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(c->w, 0, 2 * LBK * sizeof(float));
     if (e == hipSuccess) e = hipMemset(c->tables, 0, size_t(c->L) * c->E * sizeof(void*));
     if (e == hipSuccess) e = hipMemset(c->n_experts, 0, sizeof(unsigned long long));
     if (e == hipSuccess && d->resident_w)
@@ -313,13 +330,16 @@ bool timed_token(const moe_ctx* c, int token) { return c->timing_every > 0 && to
 
 // One layer; `timing` permits the FFN events of timed tokens (off while a
 // graph is captured).  Arguments are checked by the callers.
-int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int mode, bool timing) {
+int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int mode, bool timing,
+                 bool defer_side = false) {
     const int use = use_bits(mode);
     STMOE_CHECK(use == 0 || c->pred, "prediction modes need a predictor");
     const int L = c->L, B = c->B, K = c->K, E = c->E;
     const int64_t stamp = int64_t(token) * L + layer + 1;
-    int32_t* idx_l = c->idx + size_t(layer) * B * K;
-    float* w_l = c->w + size_t(layer) * B * K;
+    const size_t pbase = size_t(c->cur_par) * L * B * K;
+    int32_t* idx_l = c->idx + pbase + size_t(layer) * B * K;
+    float* w_l = c->w + pbase + size_t(layer) * B * K;
+    c->last_par = c->cur_par;
 
     // first call: layer 0's prediction comes from the profiled HT[0]
     if (!c->started) {
@@ -376,19 +396,22 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         if (int rc = moe_route_topk(x, c->router[layer], B, c->H, E, K, c->dtype, c->renorm, idx_l, w_l,
                                     nullptr, c->route_ws, c->route_ws_bytes, c->s))
             return rc;
-        STMOE_HIP(hipEventRecord(c->ev_sel, c->s));
-        STMOE_HIP(hipStreamWaitEvent(c->side, c->ev_sel, 0));
-        const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
-        if (timed)
-            if (int rc = stamp_event(tl.pred0, c->side)) return rc;
-        if (int rc = update_predict(c->pred, layer, prev, idx_l, use, c->online, nullptr, nullptr, nullptr, c->side))
-            return rc;
-        if (timed)
-            if (int rc = stamp_event(tl.pred1, c->side)) return rc;
-        c->side_pending = true;
+        if (!defer_side) {
+            STMOE_HIP(hipEventRecord(c->ev_sel, c->s));
+            STMOE_HIP(hipStreamWaitEvent(c->side, c->ev_sel, 0));
+            const int32_t* prev = layer > 0 ? c->idx + pbase + size_t(layer - 1) * B * K : nullptr;
+            if (timed)
+                if (int rc = stamp_event(tl.pred0, c->side)) return rc;
+            if (int rc = update_predict(c->pred, layer, prev, idx_l, use, c->online, nullptr, nullptr, nullptr,
+                                        c->side))
+                return rc;
+            if (timed)
+                if (int rc = stamp_event(tl.pred1, c->side)) return rc;
+            c->side_pending = true;
+        }
     } else if (use) {
         // with a cache the host reads the prediction: one fused launch pair
-        const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
+        const int32_t* prev = layer > 0 ? c->idx + pbase + size_t(layer - 1) * B * K : nullptr;
         if (int rc = fused_route_predict(x, c->router[layer], c->H, c->dtype, c->renorm, idx_l, w_l,
                                          c->route_ws, c->pred, layer, prev, use, c->online, c->ranked,
                                          c->ranked + E, max_scores(c->ranked, E), c->s))
@@ -456,11 +479,11 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         if (int rc = stamp_event(tl.down1, c->s)) return rc;
         ++c->n_calls;
     }
-    if (route_in_ffn && use && c->side) {
+    if (route_in_ffn && use && c->side && !defer_side) {
         // the selection exists once the FFN has run
         STMOE_HIP(hipEventRecord(c->ev_sel, c->s));
         STMOE_HIP(hipStreamWaitEvent(c->side, c->ev_sel, 0));
-        const int32_t* prev = layer > 0 ? c->idx + size_t(layer - 1) * B * K : nullptr;
+        const int32_t* prev = layer > 0 ? c->idx + pbase + size_t(layer - 1) * B * K : nullptr;
         if (timed)
             if (int rc = stamp_event(tl.pred0, c->side)) return rc;
         if (int rc = update_predict(c->pred, layer, prev, idx_l, use, c->online, nullptr, nullptr, nullptr, c->side))
@@ -492,6 +515,57 @@ int join_side(moe_ctx* c) {
     STMOE_HIP(hipEventRecord(c->ev_side, c->side));
     STMOE_HIP(hipStreamWaitEvent(c->s, c->ev_side, 0));
     c->side_pending = false;
+    return STMOE_OK;
+}
+
+// The compute stream waits for the per-token predictor launch that still
+// reads the selection buffer of parity `par`.
+int wait_token_side(moe_ctx* c, int par) {
+    if (!c->tok_pending[par]) return STMOE_OK;
+    STMOE_HIP(hipStreamWaitEvent(c->s, c->ev_tok[par], 0));
+    c->tok_pending[par] = false;
+    return STMOE_OK;
+}
+
+// One token's predictor work in one side-stream launch (after its last
+// layer): every layer's verify/update and next-layer prediction, in layer
+// order, on the selections of parity c->cur_par.
+int token_side(moe_ctx* c, int token, int use) {
+    const int par = c->cur_par;
+    const int key = use * 2 + c->online;
+    if (c->seq_key[par] != key) {
+        if (!c->seq_args[par]) STMOE_HIP(hipMalloc(&c->seq_args[par], update_predict_seq_bytes(c->L)));
+        STMOE_HIP(hipStreamSynchronize(c->side));     // no launch still reads the old arguments
+        if (int rc = update_predict_seq_args(c->pred, c->idx + size_t(par) * c->L * c->B * c->K, use, c->online,
+                                             c->seq_args[par]))
+            return rc;
+        c->seq_key[par] = key;
+    }
+    STMOE_HIP(hipEventRecord(c->ev_sel, c->s));
+    STMOE_HIP(hipStreamWaitEvent(c->side, c->ev_sel, 0));
+    const bool timed = c->timing_every > 0 && token % c->timing_every == 0 && !c->timed_layers.empty();
+    int p0 = -1, p1 = -1;
+    auto stamp = [&](int& slot) -> int {
+        hipEvent_t ev = next_event(c);
+        if (!ev) {
+            set_error("moe_decode_token: hipEventCreate failed");
+            return STMOE_EHIP;
+        }
+        slot = int(c->ev_used - 1);
+        STMOE_HIP(hipEventRecord(ev, c->side));
+        return STMOE_OK;
+    };
+    if (timed)
+        if (int rc = stamp(p0)) return rc;
+    if (int rc = update_predict_seq(c->pred, c->seq_args[par], c->side)) return rc;
+    if (timed) {
+        if (int rc = stamp(p1)) return rc;
+        // the token's predictor time, reported with its last layer
+        c->timed_layers.back().pred0 = p0;
+        c->timed_layers.back().pred1 = p1;
+    }
+    STMOE_HIP(hipEventRecord(c->ev_tok[par], c->side));
+    c->tok_pending[par] = true;
     return STMOE_OK;
 }
 
@@ -535,6 +609,7 @@ int capture_token(moe_ctx* c, int token, int mode) {
 
 int decode_token_graph(moe_ctx* c, int token, const void* xs, float* ys, int mode) {
     if (int rc = join_side(c)) return rc;
+    c->cur_par = 0;
     if (!c->graph_exec || c->graph_mode != mode)
         if (int rc = capture_token(c, token, mode)) return rc;
     const size_t n = size_t(c->L) * c->B * c->H;
@@ -560,13 +635,36 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
     STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
     STMOE_CHECK(token >= 0, "token must be >= 0");
     STMOE_CHECK(mode >= MOE_MODE_ON_DEMAND && mode <= MOE_MODE_CCT_ONLY, "bad mode");
+    // single layers use the parity-0 selection buffer and per-layer predictor work
+    c->cur_par = 0;
+    if (int rc = wait_token_side(c, 0)) return rc;
     return decode_layer(c, token, layer, x, y, mode, true);
+}
+
+extern "C" int moe_ctx_set_predictor_batch(moe_ctx* c, int on) {
+    clear_error();
+    STMOE_CHECK(c, "null ctx");
+    STMOE_CHECK(on == 0 || on == 1, "on must be 0 or 1");
+    STMOE_CHECK(!on || (!c->cache && c->side), "per-token predictor launches need a context without a cache "
+                                               "and with a predictor");
+    STMOE_CHECK(!on || !c->graph_on, "per-token predictor launches and graph replay exclude each other");
+    STMOE_HIP(hipDeviceSynchronize());
+    if (on && !c->ev_tok[0]) {
+        for (int i = 0; i < 2; ++i)
+            STMOE_HIP(hipEventCreateWithFlags(&c->ev_tok[i], hipEventDisableTiming | hipEventDisableSystemFence));
+    }
+    c->tok_pending[0] = c->tok_pending[1] = false;
+    c->side_pending = false;
+    c->pred_batch = on != 0;
+    c->cur_par = 0;
+    return STMOE_OK;
 }
 
 extern "C" int moe_ctx_set_graph(moe_ctx* c, int on) {
     clear_error();
     STMOE_CHECK(c, "null ctx");
     STMOE_CHECK(!on || !c->cache, "graph replay needs a context without a cache");
+    STMOE_CHECK(!on || !c->pred_batch, "per-token predictor launches and graph replay exclude each other");
     STMOE_HIP(hipStreamSynchronize(c->s));
     if (c->gs) STMOE_HIP(hipStreamSynchronize(c->gs));
     if (c->graph_exec) (void)hipGraphExecDestroy(c->graph_exec);
@@ -624,10 +722,18 @@ extern "C" int moe_decode_token(moe_ctx* c, int token, const void* xs, float* ys
     // graph replay once the first call has run (it seeds layer 0's
     // prediction); event-timed tokens run eagerly
     if (c->graph_on && c->started && !timed_token(c, token)) return decode_token_graph(c, token, xs, ys, mode);
+    // per-token predictor work: this token's selections go to its parity's
+    // buffer, which the launch of two tokens ago may still be reading
+    const int use = use_bits(mode);
+    const bool batch = c->pred_batch && use != 0;
+    c->cur_par = batch ? (token & 1) : 0;
+    if (int rc = wait_token_side(c, c->cur_par)) return rc;
     for (int l = 0; l < c->L; ++l) {
         const char* x = reinterpret_cast<const char*>(xs) + size_t(l) * c->B * c->H * c->esz;
-        if (int rc = decode_layer(c, token, l, x, ys + size_t(l) * c->B * c->H, mode, true)) return rc;
+        if (int rc = decode_layer(c, token, l, x, ys + size_t(l) * c->B * c->H, mode, true, batch)) return rc;
     }
+    if (batch)
+        if (int rc = token_side(c, token, use)) return rc;
     return STMOE_OK;
 }
 
@@ -636,8 +742,9 @@ extern "C" int moe_ctx_last_routing(moe_ctx* c, int32_t* idx, float* w) {
     STMOE_CHECK(c, "null ctx");
     STMOE_HIP(hipStreamSynchronize(c->s));
     const size_t n = size_t(c->L) * c->B * c->K;
-    if (idx) STMOE_HIP(hipMemcpy(idx, c->idx, n * sizeof(int32_t), hipMemcpyDeviceToHost));
-    if (w) STMOE_HIP(hipMemcpy(w, c->w, n * sizeof(float), hipMemcpyDeviceToHost));
+    const size_t off = size_t(c->last_par) * n;
+    if (idx) STMOE_HIP(hipMemcpy(idx, c->idx + off, n * sizeof(int32_t), hipMemcpyDeviceToHost));
+    if (w) STMOE_HIP(hipMemcpy(w, c->w + off, n * sizeof(float), hipMemcpyDeviceToHost));
     return STMOE_OK;
 }
 

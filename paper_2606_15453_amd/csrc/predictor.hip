@@ -126,6 +126,37 @@ __global__ __launch_bounds__(kThreads) void update_predict_kernel(UpdateArgs u, 
     predict_body(p, sh);
 }
 
+// One layer's arguments of the sequential kernel below.
+struct UpdPred {
+    UpdateArgs u;
+    PredictArgs p;
+};
+
+// The verify/update and next-layer prediction of every layer of one token,
+// in layer order, in one workgroup: each layer runs the steps of
+// update_predict_kernel on the arguments built for it; the barrier between
+// layers orders the tables one layer writes before the next layer stages
+// them.
+__global__ __launch_bounds__(kThreads) void update_predict_seq_kernel(const UpdPred* args, int n) {
+    __shared__ TableShared sh;
+    for (int l = 0; l < n; ++l) {
+        const UpdateArgs u = args[l].u;
+        PredictArgs p = args[l].p;
+        Seg g[kMaxSegs];
+        p.sel_cur = nullptr;     // the update's copy of the selection serves both
+        int k = 0;
+        k += update_segs(u, sh, g + k);
+        k += predict_segs(p, sh, g + k);
+        stage(g, k);
+        update_body(u, sh);
+        if (p.ht_next && p.ht_next == u.ht)
+            for (int i = threadIdx.x; i < u.B * u.K; i += kThreads) sh.htn[i] = sh.htnew[i];
+        __syncthreads();
+        predict_body(p, sh);
+        __syncthreads();
+    }
+}
+
 int check_sel_host(const int32_t* sel, size_t rows, int E, int K) {
     for (size_t r = 0; r < rows; ++r) {
         const int32_t* row = sel + r * K;
@@ -374,6 +405,41 @@ int update_predict(stmoe_predictor* p, int layer, const int32_t* sel_prev, const
 }  // namespace stmoe
 
 namespace stmoe {
+// Internal: device bytes of the per-layer arguments of update_predict_seq.
+size_t update_predict_seq_bytes(int L) { return size_t(L) * sizeof(UpdPred); }
+
+// Internal: build the arguments of every layer for the selections idx_all
+// (device [L][B][K]) into dev_args (device, update_predict_seq_bytes(L));
+// synchronous.
+int update_predict_seq_args(stmoe_predictor* p, const int32_t* idx_all, int use, int online, void* dev_args) {
+    std::vector<UpdPred> v(size_t(p->L));
+    const size_t bk = size_t(p->B) * p->K;
+    for (int l = 0; l < p->L; ++l) {
+        const int32_t* cur = idx_all + size_t(l) * bk;
+        const int32_t* prev = l > 0 ? idx_all + size_t(l - 1) * bk : nullptr;
+        v[size_t(l)].u = update_args(p, l, prev, cur, online);
+        v[size_t(l)].p = l + 1 < p->L
+                             ? predict_args(p, l, cur, use, nullptr, nullptr, nullptr, nullptr, nullptr)
+                             : predict_args(p, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr, nullptr, nullptr,
+                                            nullptr);
+    }
+    STMOE_HIP(hipMemcpy(dev_args, v.data(), v.size() * sizeof(UpdPred), hipMemcpyHostToDevice));
+    return STMOE_OK;
+}
+
+// Internal: one token's verify/update and predictions for every layer, in
+// layer order, one launch on `s` (the arguments from update_predict_seq_args).
+int update_predict_seq(stmoe_predictor* p, const void* dev_args, hipStream_t s) {
+    if (!p->profiled) {
+        set_error("moe_decode_token: predictor has not been profiled");
+        return STMOE_ESTATE;
+    }
+    hipLaunchKernelGGL(update_predict_seq_kernel, dim3(1), dim3(kThreads), 0, s,
+                       static_cast<const UpdPred*>(dev_args), p->L);
+    STMOE_LAUNCHED();
+    return STMOE_OK;
+}
+
 // Internal: the shape a predictor was created with (checked by moe_ctx_create).
 void stmoe_shape(const stmoe_predictor* p, int* L, int* E, int* K, int* B) {
     *L = p->L;

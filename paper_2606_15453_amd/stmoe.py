@@ -101,6 +101,7 @@ _SIGS = {
     "moe_decode_token": (i32, [vp, i32, vp, vp, i32]),
     "moe_ctx_set_prefetch": (i32, [vp, i32, i32]),
     "moe_ctx_set_online_update": (i32, [vp, i32]),
+    "moe_ctx_set_predictor_batch": (i32, [vp, i32]),
     "moe_ctx_last_routing": (i32, [vp, vp, vp]),
     "moe_ctx_set_timing": (i32, [vp, i32]),
     "moe_ctx_set_graph": (i32, [vp, i32]),
@@ -423,6 +424,11 @@ class DecodeContext:
     def set_timing(self, every):
         """Time the FFN of every `every`-th token (0 stops; True means every token)."""
         _call("moe_ctx_set_timing", self.h, int(every))
+
+    def set_predictor_batch(self, on=True):
+        """One side-stream predictor launch per token (every layer's update and
+        prediction, in order) instead of one per layer; contexts without a cache."""
+        _call("moe_ctx_set_predictor_batch", self.h, int(bool(on)))
 
     def set_graph(self, on=True):
         """Replay each token (after the first) as one HIP graph; no-cache contexts only."""

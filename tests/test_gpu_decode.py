@@ -48,7 +48,7 @@ def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True):
 
 
 def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0, device=0,
-             device_until=None, device_pool=False):
+             device_until=None, device_pool=False, batch=False):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
@@ -85,6 +85,8 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
                               resident_ptrs=resident, shared_ptrs=st.shared_ptrs(),
                               n_shared=cfg.n_shared, renorm=renorm, stream=stream)
     ctx.set_online_update(online)
+    if batch:
+        ctx.set_predictor_batch(True)
     idx_hist, ys = [], []
     for t in range(cfg.T):
         if cache is not None and device_until is not None and t == device_until:
@@ -202,6 +204,56 @@ def test_decode_capped_counts_and_invariance(name, over, mode, after_demand, dev
     assert cst == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
                        useful=n.useful, wasted=n.wasted)
 
+
+
+@pytest.mark.parametrize("name,over", CFGS)
+@pytest.mark.parametrize("mode,online", [(1, True), (2, True), (3, True), (1, False)])
+def test_decode_per_token_predictor_launch(name, over, mode, online):
+    """One predictor launch per token (every layer's update and prediction in
+    layer order, selections in per-parity buffers) gives the per-layer
+    launches' selections, outputs, hit statistics and tables, which match the
+    oracle (the per-layer tests)."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    t_layer, t_token = [], []
+    idx_a, ys_a, stats_a, _ = _run_gpu(st, mode, capped=False, online=online, tables=t_layer)
+    idx_b, ys_b, stats_b, _ = _run_gpu(st, mode, capped=False, online=online, tables=t_token, batch=True)
+    for t in range(cfg.T):
+        assert np.array_equal(idx_a[t], idx_b[t]), t
+        assert np.array_equal(ys_a[t], ys_b[t]), t
+    assert np.array_equal(stats_a, stats_b)
+    for a, b in zip(t_layer[0], t_token[0]):
+        assert np.array_equal(a, b)
+    ref = _oracle(st, mode, online=online)
+    assert np.array_equal(stats_b[:, 0], ref["hits"].sum(axis=0))
+    assert np.array_equal(stats_b[:, 2], ref["npred"].sum(axis=0))
+
+
+def test_per_token_predictor_launch_rejections():
+    """Per-token predictor launches need a context without a cache and
+    exclude graph replay."""
+    import torch
+    from gpuhelp import DEV, storage_dtype
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["tiny"].scaled(T=2, P=2)
+    st = Stack(cfg)
+    pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+    pred.profile(st.prof)
+    ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
+                          [g.data_ptr() for g in st.wg_dev], predictor=pred,
+                          resident_ptrs=[st.blobs[l][e].data_ptr() for l in range(cfg.L) for e in range(cfg.E)])
+    ctx.set_graph(True)
+    with pytest.raises(S.StmoeError):
+        ctx.set_predictor_batch(True)
+    ctx.set_graph(False)
+    ctx.set_predictor_batch(True)
+    with pytest.raises(S.StmoeError):
+        ctx.set_graph(True)
+    ctx.set_predictor_batch(False)
+    ctx.close()
+    pred.close()
 
 
 @pytest.mark.parametrize("mode,device", [(0, 0), (1, 0), (1, 1)])

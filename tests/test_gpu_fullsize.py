@@ -1,9 +1,9 @@
 """Parity at the full workload sizes, in the launch configuration the decode
 benchmark times: every expert of the whole stack resident in HBM, one
 moe_decode_token call per token (router logits, gate/up with its routing
-prologue, down, the predictor's update and prediction on the side stream,
-HIP events around the FFN), for the first decode tokens of the seeded
-workload.
+prologue, down, the predictor's update and prediction of every layer in one
+side-stream launch per token, HIP events around the FFN), for the first
+decode tokens of the seeded workload.
 
 Checked against the oracle: the selection of every (token, layer, row)
 (bit-exact, rows with an fp64 near-tie excluded and counted), the predictor's
@@ -68,6 +68,8 @@ def _gpu_decode(st, n_tokens, cache=None, mode=None):
                           [g.data_ptr() for g in st.wg_dev], predictor=pred, cache=cache,
                           resident_ptrs=resident, shared_ptrs=shared, n_shared=cfg.n_shared)
     ctx.set_timing(1)
+    if cache is None:
+        ctx.set_predictor_batch(True)    # as the bench's resident runs
     idx_hist, ys = [], []
     for t in range(n_tokens):
         y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device=DEV)

@@ -911,7 +911,7 @@ def main():
         summarize_offload(args.summarize_offload)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (this build has no "
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (this implementation has no "
               f"multi-GPU path)", file=sys.stderr)
         sys.exit(2)
     import torch

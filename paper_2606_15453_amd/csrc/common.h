@@ -47,9 +47,10 @@ constexpr int kMaxE = 256;
 constexpr int kMaxK = 16;
 constexpr int kMaxB = 16;
 constexpr int kMaxH = 16384;
-// batch x experts up to which the expert FFN's gate/up kernel can run the
-// gating itself (one logit per thread of a workgroup)
-constexpr int kRouteInFfnMax = 256;
+// batch x experts up to which the expert FFN's gate/up kernel runs the
+// gating itself (every gate/up workgroup ranks the logits, so beyond this the
+// separate router tail costs less than the larger prologue)
+constexpr int kRouteInFfnMax = 128;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 

@@ -362,7 +362,7 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
     }
 
     // R + V + P.  Without a cache: the router on the compute stream (for
-    // B*E <= 256 only its logits: the FFN's gate/up kernel does softmax and
+    // B*E <= 128 only its logits: the FFN's gate/up kernel does softmax and
     // top-K), then verify/update and prediction on the side stream, off the
     // FFN's path.
     // Side work still queued reads selections of this token's layers and the

@@ -1484,7 +1484,7 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
                float* y, void* ws, hipStream_t st, unsigned long long* n_experts, hipEvent_t ev_mid,
                const float* logits, int renorm, const void* ebase, size_t estride) {
     if (logits && B * E > kRouteInFfnMax) {
-        set_error("ffn_launch: routing inside the FFN needs B*E <= 256");
+        set_error("ffn_launch: routing inside the FFN needs B*E <= 128");
         return STMOE_EINVAL;
     }
     const Shape s = plan_shape(B, K, H, I, E, n_shared, dtype);

@@ -38,6 +38,12 @@ PEAK_HBM_GBPS = 8000.0
 TIMING_EVERY = 8
 
 
+def timing_cadence(steps):
+    """Tokens between event-timed tokens: TIMING_EVERY, or 1 when the timed
+    region is too short to hold a multiple of it."""
+    return TIMING_EVERY if steps >= TIMING_EVERY else 1
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -548,7 +554,10 @@ def hbm_resident(wl, steps, warmup):
     run_tokens(ctx, wl, 0, n_issue, y, S.MODE_STMOE)
     host_us = (time.perf_counter() - t0) * 1e6 / (n_issue * cfg.L)
     torch.cuda.synchronize()
-    ctx.set_timing(TIMING_EVERY)
+    # event-time every TIMING_EVERY-th token, or every token of a short run
+    # (the cadence counts from the first timed token)
+    every = timing_cadence(steps)
+    ctx.set_timing(every)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     run_tokens(ctx, wl, warmup, steps, y, S.MODE_STMOE)
@@ -999,7 +1008,8 @@ def main():
             "bytes_per_launch": int(up_bytes / max(r["n_calls"], 1)),
             "avg_launch_us": round(1e3 * r["up_ms"] / max(r["n_calls"], 1), 3),
             "launches": r["n_calls"],
-            "event_sampling": f"HIP events around the FFN launches of every {TIMING_EVERY}th token of the timed region",
+            "event_sampling": f"HIP events around the FFN launches of every {timing_cadence(args.steps)}th token "
+                              f"of the timed region",
         },
         "ffn_down": {"achieved_gbps": round(dn_gbps, 1), "frac": round(dn_gbps / PEAK_HBM_GBPS, 4),
                      "avg_launch_us": round(1e3 * r["down_ms"] / max(r["n_calls"], 1), 3)},

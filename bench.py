@@ -1008,8 +1008,9 @@ def main():
             "bytes_per_launch": int(up_bytes / max(r["n_calls"], 1)),
             "avg_launch_us": round(1e3 * r["up_ms"] / max(r["n_calls"], 1), 3),
             "launches": r["n_calls"],
-            "event_sampling": f"HIP events around the FFN launches of every {timing_cadence(args.steps)}th token "
-                              f"of the timed region",
+            "event_sampling": ("HIP events around the FFN launches of "
+                               + (f"every {timing_cadence(args.steps)}th token" if timing_cadence(args.steps) > 1
+                                  else "every token") + " of the timed region"),
         },
         "ffn_down": {"achieved_gbps": round(dn_gbps, 1), "frac": round(dn_gbps / PEAK_HBM_GBPS, 4),
                      "avg_launch_us": round(1e3 * r["down_ms"] / max(r["n_calls"], 1), 3)},

@@ -5,19 +5,26 @@ benchmark's CPU-baseline leg may import or call this module.  The product path
 never does, and this module imports nothing from the product package: it takes
 the seeded input arrays as arguments and shares no code with the HIP path.
 
-Arithmetic: float64 for every floating-point step, Python ints for the
-prediction tables.  Each function names the passage of the paper it follows.
+Arithmetic: float64 for every floating-point step, integer numpy arrays for
+the prediction tables.  Each function names the passage of the paper it
+follows and states it in its own terms (set and membership-matrix form), not
+as a transcription of the printed listings.
 
 Parity status per function (see the pins under ``tests/``):
   router_logits / softmax_rows / topk_rows / route   pinned (invariants, brute force)
   swiglu_expert / moe_ffn                            pinned (explicit triple loop, special cases)
   STPredictor.profile / update / predict             pinned (hand-worked example, invariants,
-                                                      closed form K^2/N, special cases)
-  CacheSim                                           pinned (hand-worked trace, invariants,
+                                                      closed form K^2/N, special cases,
+                                                      exhaustive update check on E = 4)
+  CacheSim, admitted, warm_from_profile              pinned (hand-worked traces, invariants,
                                                       exhaustive optimum lower bound)
-  decode_reference (the per-layer loop)              pinned through its parts; its overall
-                                                      hit rate on synthetic inputs has no
-                                                      paper value: parity unpinned
+  decode_reference (the per-layer loop)              pinned (hand-worked five-token run:
+                                                      per-token hits, scores, tables, the
+                                                      capped cache's copy log in both modes,
+                                                      frozen tables; planted slips fail it).
+                                                      Its hit rates and stall on synthetic
+                                                      inputs have no paper value: those
+                                                      absolute numbers are parity unpinned
 """
 from __future__ import annotations
 
@@ -152,105 +159,120 @@ def moe_ffn(x: np.ndarray, idx: np.ndarray, w: np.ndarray, expert, shared=()):
 
 class STPredictor:
     """Cross-layer Correlation Tables (one per adjacent layer pair) and a
-    per-layer, per-batch-row History Table.
+    per-layer, per-batch-row History Table (Section 4.2).
 
-    cct_idx[i][e][s], cct_conf[i][e][s]: slot s of CCT entry e for the layer
-    pair (i, i+1); ht[l][b]: the previous token's selection at layer l for
-    batch row b, kept sorted ascending (it is a set).
+    cct_idx[i][e][s], cct_conf[i][e][s]  (int64 arrays [L-1][E][K]): slot s of
+        the CCT entry of expert e for the layer pair (i, i+1);
+    ht[l][b]  (int64 array [L][B][K]): the previous token's selection at layer
+        l for batch row b, sorted ascending (it is a set; its confidence is
+        fixed at 2);
+    co[i]  (int64 array [L-1][E][E]): the profiling co-activation counts.
     """
 
     def __init__(self, L: int, E: int, K: int, B: int = 1):
         self.L, self.E, self.K, self.B = L, E, K, B
-        self.co = [[[0] * E for _ in range(E)] for _ in range(L - 1)]
-        self.cct_idx = [[[0] * K for _ in range(E)] for _ in range(L - 1)]
-        self.cct_conf = [[[0] * K for _ in range(E)] for _ in range(L - 1)]
-        self.ht = [[[] for _ in range(B)] for _ in range(L)]
+        self.co = np.zeros((max(L - 1, 0), E, E), np.int64)
+        self.cct_idx = np.zeros((max(L - 1, 0), E, K), np.int64)
+        self.cct_conf = np.zeros((max(L - 1, 0), E, K), np.int64)
+        self.ht = np.zeros((L, B, K), np.int64)
 
-    # Algorithm 1 (and the HT initialisation of Section 4.1 / Fig. framework)
+    def _indicator(self, sets) -> np.ndarray:
+        """Rows of 0/1 membership vectors over the E experts."""
+        sets = np.asarray(sets, np.int64).reshape(-1, self.K)
+        m = np.zeros((sets.shape[0], self.E), np.int64)
+        np.put_along_axis(m, sets, 1, axis=1)
+        return m
+
     def profile(self, sel) -> None:
-        """sel[p][b][l][k]: the profiling tokens' selections.
+        """Build the tables from the profiling tokens (Algorithm 1; HT from
+        Section 4.1 and the framework figure).
 
-        Co[i][e][f] counts, over all profiling tokens and batch rows, how often
-        expert e at layer i and expert f at layer i+1 were selected together.
-        CCT[i][e] keeps the K largest counts (ties and all-zero tails: lower
-        index first) with confidence 2.  HT[l][b] is the last profiling token's
-        selection.
+        sel[p][b][l][k]: the profiling tokens' selections.  With X_l the
+        matrix of membership vectors of layer l's selections (one row per
+        (token, batch row)), the co-activation counts of the pair (i, i+1) are
+        X_i^T X_{i+1}: entry (e, f) counts the rows that chose e at layer i
+        and f at layer i+1.  The CCT entry of e keeps the K experts with the
+        largest counts (equal counts: lower index first, which also fixes the
+        choice among all-zero tails), each with confidence 2.  The HT holds
+        the last profiling token's selections.
         """
-        sel = np.asarray(sel)
+        sel = np.asarray(sel, np.int64)
         P = sel.shape[0]
+        X = [self._indicator(sel[:, :, l, :]) for l in range(self.L)]
         for i in range(self.L - 1):
-            co = self.co[i]
-            for p in range(P):
-                for b in range(self.B):
-                    for e in sel[p, b, i]:
-                        for f in sel[p, b, i + 1]:
-                            co[int(e)][int(f)] += 1
+            self.co[i] = X[i].T @ X[i + 1]
             for e in range(self.E):
-                order = sorted(range(self.E), key=lambda f: (-co[e][f], f))
-                self.cct_idx[i][e] = order[:self.K]
-                self.cct_conf[i][e] = [CONF_INIT] * self.K
-        for l in range(self.L):
-            for b in range(self.B):
-                self.ht[l][b] = sorted(int(v) for v in sel[P - 1, b, l])
+                # a stable sort on the negated counts keeps index order on ties
+                self.cct_idx[i, e] = np.argsort(-self.co[i, e], kind="stable")[:self.K]
+            self.cct_conf[i] = CONF_INIT
+        self.ht[:] = np.sort(sel[P - 1].transpose(1, 0, 2), axis=2)
 
-    # Algorithm 3 on one CCT entry
-    def _update_entry(self, i: int, e: int, F) -> None:
-        """Table update of one CCT entry e of pair i against the actual set F.
+    def load_tables(self, cct_idx, cct_conf, ht) -> None:
+        """Replace the CCTs and the HT (e.g. with planted wrong predictions)."""
+        self.cct_idx[:] = np.asarray(cct_idx, np.int64)
+        self.cct_conf[:] = np.asarray(cct_conf, np.int64)
+        self.ht[:] = np.sort(np.asarray(ht, np.int64), axis=2)
 
-        Hit: confidence + 1, saturating at 3.  Miss: confidence - 1 while it is
-        above 0; at 0 the slot is replaced by an expert of F that the entry did
-        not hold before this update (candidates in ascending order, consumed one
-        per replaced slot, slots visited in ascending order), with confidence 2.
+    def update_entry(self, i: int, e: int, F) -> None:
+        """Table update of one CCT entry against the actual next-layer set F
+        (Algorithm 3; the CCT paragraph of Section 4.2).
+
+        The entry's experts found in F are confirmed: their 2-bit confidence
+        rises by one, saturating at 3.  Experts not in F lose one confidence
+        level while they have one; those already at 0 make way for experts of
+        F that the entry does not hold: the slots being replaced, taken in
+        slot order, receive those experts in ascending order, with the initial
+        confidence 2.  There are never more such slots than candidates (each
+        unconfirmed slot leaves one expert of F unmatched), so the entry stays
+        a set of K distinct experts.
         """
-        row, conf = self.cct_idx[i][e], self.cct_conf[i][e]
-        Fs = set(int(f) for f in F)
-        fresh = sorted(Fs - set(row))
-        nxt = 0
-        for s in range(self.K):
-            if row[s] in Fs:
-                conf[s] = min(conf[s] + 1, CONF_MAX)
-            elif conf[s] > 0:
-                conf[s] -= 1
-            else:
-                row[s] = fresh[nxt]
-                nxt += 1
-                conf[s] = CONF_INIT
+        row, conf = self.cct_idx[i, e], self.cct_conf[i, e]
+        Fs = np.asarray(sorted(int(f) for f in F), np.int64)
+        confirmed = np.isin(row, Fs)
+        replaced = ~confirmed & (conf == 0)
+        newcomers = np.setdiff1d(Fs, row)           # sorted, not held by the entry
+        conf[:] = np.where(confirmed, np.minimum(conf + 1, CONF_MAX), conf - 1)
+        row[replaced] = newcomers[:int(replaced.sum())]
+        conf[replaced] = CONF_INIT
 
     def update(self, layer: int, prev_sets, cur_sets, online: bool = True) -> None:
-        """Verify step at ``layer`` (Section 4.3.4): Algorithm 3 on CCT[layer-1]
-        for every expert of the previous layer's selection, batch rows in order
-        b = 0..B-1; then HT[layer][b] <- this token's selection."""
+        """Verify step at ``layer`` (Section 4.3.4, V): every CCT entry of the
+        pair (layer-1, layer) that the previous layer selected is updated
+        against this layer's selection (batch rows in order b = 0..B-1); then
+        HT[layer][b] is overwritten with this token's selection.  online=False
+        freezes the CCTs (the HT is still overwritten)."""
         if layer >= 1 and online:
             for b in range(self.B):
                 for e in prev_sets[b]:
-                    self._update_entry(layer - 1, int(e), cur_sets[b])
+                    self.update_entry(layer - 1, int(e), cur_sets[b])
         for b in range(self.B):
-            self.ht[layer][b] = sorted(int(v) for v in cur_sets[b])
+            self.ht[layer, b] = sorted(int(v) for v in cur_sets[b])
 
-    # Algorithm 2 + Eq. 1
     def predict(self, layer: int, cur_sets, use_cct: bool = True, use_ht: bool = True):
-        """Scores for layer+1 from this token's selection at ``layer``.
+        """Eq. 1 scores of every expert for layer+1, per batch row.
 
-        score_b[f] = sum over e in A_layer[b] of the confidence of f in CCT[layer][e]
-                     + 2 if f is in HT[layer+1][b]                       (Eq. 1)
-        layer == -1 predicts layer 0 from HT[0] alone (no earlier layer).
-        Returns an int array [B][E].
+        The spatial part sums, over the experts e selected at ``layer``, the
+        confidence with which CCT[layer][e] names each candidate; the temporal
+        part adds the fixed HT confidence 2 to the experts that the previous
+        token selected at layer+1.  layer == -1 scores layer 0 from HT[0]
+        alone (no earlier layer).  Returns an int64 array [B][E].
         """
         tgt = layer + 1
-        sc = np.zeros((self.B, self.E), dtype=np.int64)
+        sc = np.zeros((self.B, self.E), np.int64)
         for b in range(self.B):
             if use_cct and layer >= 0:
-                for e in cur_sets[b]:
-                    for s in range(self.K):
-                        sc[b, self.cct_idx[layer][int(e)][s]] += self.cct_conf[layer][int(e)][s]
+                A = np.asarray([int(e) for e in cur_sets[b]], np.int64)
+                sc[b] += np.bincount(self.cct_idx[layer, A].ravel(),
+                                     weights=self.cct_conf[layer, A].ravel(),
+                                     minlength=self.E).astype(np.int64)
             if use_ht:
-                for f in self.ht[tgt][b]:
-                    sc[b, f] += HT_SCORE
+                sc[b, self.ht[tgt, b]] += HT_SCORE
         return sc
 
     @staticmethod
     def prefetch_sets(scores):
-        """Per-row PrefetchSet {f : score >= 2} (Algorithm 2)."""
+        """Per-row PrefetchSet: the experts whose score reaches the threshold 2
+        (Algorithm 2 and the text after it)."""
         return [sorted(int(f) for f in np.nonzero(scores[b] >= THRESHOLD)[0])
                 for b in range(scores.shape[0])]
 
@@ -262,11 +284,8 @@ class STPredictor:
         return sorted(cand, key=lambda f: (-int(m[f]), f))
 
     def tables(self):
-        """(co [L-1][E][E], cct_idx [L-1][E][K], cct_conf [L-1][E][K], ht [L][B][K]) arrays."""
-        return (np.array(self.co, np.int64).reshape(self.L - 1, self.E, self.E),
-                np.array(self.cct_idx, np.int64).reshape(self.L - 1, self.E, self.K),
-                np.array(self.cct_conf, np.int64).reshape(self.L - 1, self.E, self.K),
-                np.array(self.ht, np.int64).reshape(self.L, self.B, self.K))
+        """Copies of (co [L-1][E][E], cct_idx [L-1][E][K], cct_conf [L-1][E][K], ht [L][B][K])."""
+        return self.co.copy(), self.cct_idx.copy(), self.cct_conf.copy(), self.ht.copy()
 
 
 # ----------------------------------------------------------------------------
@@ -359,12 +378,14 @@ class CacheSim:
         for f, c in where.items():
             if c >= 0:
                 self.last[l][c] = stamp
+        hits = len(U) - len(demand) - len(overflow)
+        useful, wasted = len(self.pending[l] & keep), len(self.pending[l] - keep)
         self.n.demand += len(demand)
         self.n.overflow += len(overflow)
-        self.n.useful += len(self.pending[l] & keep)
-        self.n.wasted += len(self.pending[l] - keep)
+        self.n.useful += useful
+        self.n.wasted += wasted
         self.pending[l] = set()
-        self.n.log.append(("A", l, stamp, tuple(demand), tuple(overflow)))
+        self.n.log.append(("A", l, stamp, tuple(demand), tuple(overflow), hits, useful, wasted))
         return where, demand, overflow
 
 
@@ -379,8 +400,32 @@ def stamp_of(t: int, l: int, L: int) -> int:
     return t * L + l + 1
 
 
+def admitted(scores, min_score: int = THRESHOLD, max_per_layer=None):
+    """The prefix of the ranked union (max score desc, index asc) whose max
+    score reaches ``min_score``, at most ``max_per_layer`` long: the experts a
+    prefetch is issued for.  min_score = 2 with no cap is the paper's
+    PrefetchSet (Algorithm 2); larger values are an admission ablation."""
+    m = np.asarray(scores).max(axis=0)
+    out = [f for f in STPredictor.ranked_union(scores) if m[f] >= min_score]
+    return out if max_per_layer is None else out[:max_per_layer]
+
+
+def warm_from_profile(prof_sel, L: int, E: int, C: int):
+    """Initial cache residency: per layer, the C experts selected most often
+    by the profiling tokens (count desc, index asc), -1 padding when C > E.
+    sel[p][b][l][k] -> int64 [L][C]."""
+    prof_sel = np.asarray(prof_sel, np.int64)
+    out = np.full((L, C), -1, np.int64)
+    for l in range(L):
+        cnt = np.bincount(prof_sel[:, :, l, :].ravel(), minlength=E)
+        order = sorted(range(E), key=lambda e: (-int(cnt[e]), e))[:min(C, E)]
+        out[l, :len(order)] = order
+    return out
+
+
 def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=None,
-                     mode=MODE_STMOE, renorm=False, ffn_of=None, ffn_tokens=0, online=True):
+                     mode=MODE_STMOE, renorm=False, ffn_of=None, ffn_tokens=0, online=True,
+                     tables=None, min_score=THRESHOLD, max_per_layer=None):
     """Run the decode loop on the CPU.
 
     x_of(t, l) -> x [B][H] float64; wg_of(l) -> W_g [E][H] float64;
@@ -390,10 +435,15 @@ def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=N
     demand-load the selection; FFN; prefetch the next layer's ranked set.
     online=False freezes the CCTs after profiling (Algorithm 3's confidence
     and replacement steps are skipped; HT is still overwritten).
+    tables=(cct_idx, cct_conf, ht) replaces the profiled tables before the
+    first token (planted wrong predictions).  min_score / max_per_layer are
+    the prefetch admission knobs of ``admitted``.
     Returns a dict of per-(t, l) records and totals.
     """
     pred = STPredictor(L, E, K, B)
     pred.profile(prof_sel)
+    if tables is not None:
+        pred.load_tables(*tables)
     use_cct = mode in (MODE_STMOE, MODE_CCT_ONLY)
     use_ht = mode in (MODE_STMOE, MODE_HT_ONLY)
     cache = CacheSim(L, E, C, warm) if C is not None else None
@@ -402,7 +452,7 @@ def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=N
     rec = dict(idx=[], w=[], scores=[], hits=np.zeros((n_tokens, L), np.int64),
                npred=np.zeros((n_tokens, L), np.int64), tie_boundary=0, tie_order=0, y={})
     if cache is not None and mode != MODE_ON_DEMAND:
-        cache.prefetch(0, STPredictor.ranked_union(P_cur), stamp_of(-1, L - 1, L))
+        cache.prefetch(0, admitted(P_cur, min_score, max_per_layer), stamp_of(-1, L - 1, L))
     for t in range(n_tokens):
         prev = None
         for l in range(L):
@@ -428,7 +478,7 @@ def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=N
                 rec["y"][(t, l)] = ffn_of(l)(x_of(t, l), r["idx"], r["w"])
             if cache is not None and mode != MODE_ON_DEMAND:
                 nl = (l + 1) % L
-                cache.prefetch(nl, STPredictor.ranked_union(P_next), stamp_of(t, l, L))
+                cache.prefetch(nl, admitted(P_next, min_score, max_per_layer), stamp_of(t, l, L))
             prev, P_cur = cur, P_next
     rec["predictor"] = pred
     rec["cache"] = cache

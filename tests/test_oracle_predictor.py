@@ -19,7 +19,7 @@ def _load(name):
 
 def _pairs(p, i):
     idx, conf = p.cct_idx[i], p.cct_conf[i]
-    return [[[idx[e][s], conf[e][s]] for s in range(p.K)] for e in range(p.E)]
+    return [[[int(idx[e][s]), int(conf[e][s])] for s in range(p.K)] for e in range(p.E)]
 
 
 def test_worked_example_replay():
@@ -27,9 +27,9 @@ def test_worked_example_replay():
     p = STPredictor(g["L"], g["E"], g["K"], g["B"])
     prof = np.array([[[tok[0], tok[1]]] for tok in g["profiling"]])     # [P][B=1][L][K]
     p.profile(prof)
-    assert p.co[0] == g["co_after_profile"]
+    assert p.co[0].tolist() == g["co_after_profile"]
     assert _pairs(p, 0) == g["cct_after_profile"]
-    assert [p.ht[l][0] for l in range(2)] == g["ht_after_profile"]
+    assert [p.ht[l][0].tolist() for l in range(2)] == g["ht_after_profile"]
     hits0 = hits1 = npred1 = 0
     for step in g["decode"]:
         sc0 = p.predict(-1, None)
@@ -51,7 +51,7 @@ def test_worked_example_replay():
         hits0 += h0
         hits1 += h1
         npred1 += len(P1)
-    assert [p.ht[l][0] for l in range(2)] == g["final_ht"]
+    assert [p.ht[l][0].tolist() for l in range(2)] == g["final_ht"]
     n = len(g["decode"]) * g["K"]
     assert [hits0, n] == g["recall_l0"]
     assert [hits1, n] == g["recall_l1"]
@@ -74,8 +74,8 @@ def test_double_replacement():
     p = STPredictor(2, d["E"], d["K"], 1)
     p.cct_idx[0][0] = [s[0] for s in d["row"]]
     p.cct_conf[0][0] = [s[1] for s in d["row"]]
-    p._update_entry(0, 0, d["F"])
-    assert [[p.cct_idx[0][0][s], p.cct_conf[0][0][s]] for s in range(d["K"])] == d["after"]
+    p.update_entry(0, 0, d["F"])
+    assert [[int(p.cct_idx[0][0][s]), int(p.cct_conf[0][0][s])] for s in range(d["K"])] == d["after"]
 
 
 def _random_trace(rng, n, B, L, E, K):
@@ -108,13 +108,13 @@ def test_invariants_random_trace(E, K, B):
         for l in range(L):
             cur = [sorted(sel[t, b, l].tolist()) for b in range(B)]
             p.update(l, prev, cur)
-            assert all(p.ht[l][b] == cur[b] for b in range(B))
+            assert all(p.ht[l][b].tolist() == cur[b] for b in range(B))
             if l + 1 < L:
                 sc = p.predict(l, cur)
                 assert sc.max() <= 3 * K + 2
                 for b in range(B):
                     ps = set(STPredictor.prefetch_sets(sc)[b])
-                    assert set(p.ht[l + 1][b]) <= ps          # HT members always reach 2
+                    assert set(p.ht[l + 1][b].tolist()) <= ps  # HT members always reach 2
             prev = cur
         _, idx, conf, _ = p.tables()
         assert ((conf >= 0) & (conf <= 3)).all()
@@ -213,8 +213,8 @@ def test_update_against_exhaustive_reading_small():
                 p = STPredictor(2, E, K, 1)
                 p.cct_idx[0][0] = list(row)
                 p.cct_conf[0][0] = list(confs)
-                p._update_entry(0, 0, F)
-                new, nc = p.cct_idx[0][0], p.cct_conf[0][0]
+                p.update_entry(0, 0, F)
+                new, nc = p.cct_idx[0][0].tolist(), p.cct_conf[0][0].tolist()
                 assert len(set(new)) == K
                 for s in range(K):
                     if row[s] in F:

@@ -87,7 +87,13 @@ def parse():
                     help="copy/compute overlap of the capped-cache runs in a rocprofv3 trace")
     ap.add_argument("--summarize-offload", nargs="+", metavar="BENCH_JSON",
                     help="print a markdown table of the capped-cache runs in bench JSON lines and exit")
-    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+    ap.add_argument("--policy-bound", default=None, metavar="CONFIG[,CONFIG...]",
+                    help="time-model bound of one-layer-lookahead prefetch policies on the planted traces")
+    ap.add_argument("--policy-attn", default="0", metavar="MS1,MS2,...",
+                    help="attention windows (ms per layer) for --policy-bound")
+    ap.add_argument("--summarize-gaps", nargs=3, metavar=("KERNEL_TRACE_CSV", "TITLE", "COMMAND"),
+                    help="print the compute-queue gap analysis of a rocprofv3 kernel trace as markdown")
+    ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "META_JSON"),
                     help="print the markdown counter summary of two rocprofv3 --pmc runs and exit")
     return ap.parse_args()
 
@@ -138,7 +144,11 @@ def counter_means(path, counter):
     return {k: (s / n, n) for k, (s, n) in acc.items()}
 
 
-def summarize_counters(fetch_csv, write_csv):
+def summarize_counters(fetch_csv, write_csv, meta_json):
+    """Markdown summary of the FETCH_SIZE / WRITE_SIZE passes over the counters
+    workload; meta_json is the file counters_workload wrote (shapes, FFN calls
+    and distinct experts of the profiled tokens)."""
+    meta = json.load(open(meta_json))
     f = counter_means(fetch_csv, "FETCH_SIZE")
     w = counter_means(write_csv, "WRITE_SIZE")
 
@@ -158,21 +168,29 @@ def summarize_counters(fetch_csv, write_csv):
     kw = CALIB_BYTES / (cw * 1024.0)
     up_bytes = gf * 1024 * kf + gw * 1024 * kw
     dn_bytes = df * 1024 * kf + dw * 1024 * kw
-    alg_up = 2 * 2 * 4096 * 14336 * 2
-    alg_dn = 2 * 4096 * 14336 * 2
-    cmd_f = ("rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/pmc_fetch -o fetch --output-format csv "
-             "-- python -u $R/bench.py --counters")
+    # algorithmic weight bytes per FFN call: distinct routed experts (+ shared)
+    per_call = (meta["n_experts"] + meta["n_calls"] * meta["n_shared"]) / meta["n_calls"]
+    mat = meta["H"] * meta["I"] * meta["esz"]
+    alg_up = per_call * 2 * mat
+    alg_dn = per_call * mat
+    cfg = meta["config"]
+    cmd_f = (f"rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/pmc_fetch -o fetch --output-format csv "
+             f"-- python -u $R/bench.py --counters --config {cfg}")
     cmd_w = cmd_f.replace("FETCH_SIZE", "WRITE_SIZE").replace("pmc_fetch", "pmc_write").replace("-o fetch", "-o write")
     out = [
-        "# HBM traffic counters: ffn_gate_up / ffn_down, Mixtral-8x7B shapes, batch 1",
+        f"# HBM traffic counters: ffn_gate_up / ffn_down, {meta['title']}",
         "",
         "Commands (run from `/tmp` with `TMPDIR=/tmp`, repository at `$R`), one counter per run:",
         "",
-        "```", cmd_f, cmd_w, "```",
+        "```", cmd_f, cmd_w,
+        f"python bench.py --summarize-counters <fetch counter_collection.csv> <write counter_collection.csv> "
+        f"$R/gpurun_out/counters_{cfg}.json",
+        "```",
         "",
-        f"The profiled workload runs {COUNTER_TOKENS} decode tokens of the HBM-resident stack (2 experts",
-        f"per layer) and then {CALIB_BYTES >> 30} GiB copies with `stmoe_calib_copy` (reads and writes exactly",
-        f"{CALIB_BYTES} bytes each).  Counters are in KiB per dispatch.",
+        f"The profiled workload runs {COUNTER_TOKENS} decode tokens of the HBM-resident stack ({per_call:.2f} "
+        f"experts per FFN call on average, shared included) and then {CALIB_BYTES >> 30} GiB copies with "
+        f"`stmoe_calib_copy` (reads and writes exactly {CALIB_BYTES} bytes each).  Counters are in KiB per "
+        f"dispatch.",
         "",
         "| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB |",
         "|---|---|---|---|",
@@ -182,14 +200,66 @@ def summarize_counters(fetch_csv, write_csv):
         "",
         f"Scale factors from the copy kernel: fetch {kf:.4f} bytes per counted byte, write {kw:.4f}.",
         "",
-        f"ffn_gate_up: measured {up_bytes / 1e6:.1f} MB per launch against {alg_up / 1e6:.1f} MB algorithmic "
+        f"ffn_gate_up: measured {up_bytes / 1e6:.2f} MB per launch against {alg_up / 1e6:.2f} MB algorithmic "
         f"({up_bytes / alg_up:.4f}x).",
-        f"ffn_down: measured {dn_bytes / 1e6:.1f} MB per launch against {alg_dn / 1e6:.1f} MB algorithmic "
+        f"ffn_down: measured {dn_bytes / 1e6:.2f} MB per launch against {alg_dn / 1e6:.2f} MB algorithmic "
         f"({dn_bytes / alg_dn:.4f}x).",
         "",
         f"traffic_bytes_per_launch: {int(round(up_bytes))}",
         f"expert_ffn_source_sha: {ffn_source_sha()}",
     ]
+    print("\n".join(out))
+
+
+DECODE_KERNELS = ("route_logits_kernel", "route_tail_kernel", "route_update_predict_kernel", "ffn_gate_up",
+                  "ffn_down", "ffn_reduce", "update_predict", "decide_kernel", "blit_kernel", "set_table_kernel")
+
+
+def summarize_gaps(trace_csv, title, cmd, skip_frac=0.25):
+    """Kernel-trace gap analysis of the decode layer on the compute queue:
+    per kernel its average duration and the average idle time between the
+    previous decode kernel's end and its start.  The window runs from the
+    first to the last decode kernel on that queue; its first `skip_frac` of
+    dispatches (warm-up) is dropped."""
+    import csv
+    rows = list(csv.DictReader(open(trace_csv)))
+    key_q = "Queue_Id" if "Queue_Id" in rows[0] else "Stream_Id"
+
+    def short(n):
+        n = n.replace("(anonymous namespace)::", "").replace("void ", "").replace("stmoe::", "")
+        return n.split("(")[0].split("<")[0]
+
+    rows = [dict(name=short(r["Kernel_Name"]), q=r[key_q], s=int(r["Start_Timestamp"]),
+                 e=int(r["End_Timestamp"])) for r in rows if r.get("End_Timestamp")]
+    rows.sort(key=lambda r: r["s"])
+    is_dec = lambda r: r["name"].startswith(DECODE_KERNELS)
+    ffn_q = max(set(r["q"] for r in rows if r["name"].startswith("ffn_gate_up")),
+                key=lambda q: sum(1 for r in rows if r["q"] == q))
+    comp = [r for r in rows if r["q"] == ffn_q]
+    idx = [i for i, r in enumerate(comp) if is_dec(r)]
+    comp = [r for r in comp[idx[0]:idx[-1] + 1] if is_dec(r)]
+    comp = comp[int(len(comp) * skip_frac):]
+    while comp and not comp[0]["name"].startswith(("route", "ffn_gate_up")):
+        comp = comp[1:]
+    acc = {}
+    for prev, cur in zip(comp, comp[1:]):
+        d = acc.setdefault(cur["name"], [0, 0.0, 0.0])
+        d[0] += 1
+        d[1] += (cur["e"] - cur["s"]) / 1e3
+        d[2] += max(cur["s"] - prev["e"], 0) / 1e3
+    span = (comp[-1]["e"] - comp[0]["e"]) / 1e3
+    busy = sum((r["e"] - r["s"]) / 1e3 for r in comp[1:])
+    n_up = max(sum(1 for r in comp[1:] if r["name"].startswith("ffn_gate_up")), 1)
+    out = [f"# {title}", "",
+           "Command (run from `/tmp` with `TMPDIR=/tmp`, repository at `$R`):", "", "```", cmd,
+           f"python bench.py --summarize-gaps <kernel_trace.csv> '<title>' '<command>'", "```", "",
+           f"Compute queue, decode kernels only (the timed run's window, first {int(skip_frac * 100)}% dropped): "
+           f"{len(comp)} dispatches, {n_up} layers.", "",
+           "| kernel | dispatches | avg duration us | avg idle before it us |", "|---|---|---|---|"]
+    for name, (n, dur, gap) in sorted(acc.items(), key=lambda kv: -kv[1][1]):
+        out.append(f"| `{name}` | {n} | {dur / n:.2f} | {gap / n:.2f} |")
+    out += ["", f"Per layer: {span / n_up:.2f} us of wall time on the compute queue, {busy / n_up:.2f} us of it "
+                f"inside kernels ({busy / span:.3f})."]
     print("\n".join(out))
 
 
@@ -302,21 +372,25 @@ def summarize_stats(path, title, cmd):
               f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
 
 
-def counters_workload():
+def counters_workload(config="mixtral"):
     """Fixed workload for the rocprofv3 --pmc passes: decode tokens of the
-    resident Mixtral-shaped stack, then calibration copies of known size."""
+    resident stack of `config` (Mixtral shapes by default), then calibration
+    copies of known size.  Writes gpurun_out/counters_<config>.json with the
+    shapes, FFN calls and distinct experts of the profiled tokens."""
     import torch
     from paper_2606_15453_amd import stmoe as S
     from paper_2606_15453_amd import workload as W
-    cfg = W.CONFIGS["mixtral"]
+    cfg = W.CONFIGS[config]
     wl = Workload(cfg)
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(wl.prof)
     ctx = make_ctx(wl, pred)
     ctx.set_predictor_batch(True)
+    ctx.set_timing(1)
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
     run_tokens(ctx, wl, 0, COUNTER_TOKENS, y, S.MODE_STMOE)
     torch.cuda.synchronize()
+    _, _, n_calls, n_experts = ctx.timing()
     src = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda:0")
     dst = torch.empty_like(src)
     for _ in range(5):
@@ -324,6 +398,11 @@ def counters_workload():
     torch.cuda.synchronize()
     ctx.close()
     pred.close()
+    os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+    meta = dict(config=config, title=f"{cfg.name}, batch {cfg.B}", H=cfg.H, I=cfg.I, esz=cfg.wbytes,
+                n_shared=cfg.n_shared, n_calls=int(n_calls), n_experts=int(n_experts))
+    with open(os.path.join(ROOT, "gpurun_out", f"counters_{config}.json"), "w") as f:
+        json.dump(meta, f)
     log("counters workload done")
 
 
@@ -427,18 +506,19 @@ def ffn_sweep(reps=50):
         del store
 
 
-def achievable_read_gbps(nbytes=4 << 30, reps=10):
-    """Streaming-read bandwidth of stmoe_calib_read (the FFN's load pattern), event-timed."""
+def achievable_read_gbps(nbytes=4 << 30, reps=10, pattern=0):
+    """Streaming-read bandwidth of stmoe_calib_read with the FFN's loads, event-timed:
+    pattern 0 a grid-stride sweep, 1 a contiguous 256 KiB region per workgroup."""
     import torch
     from paper_2606_15453_amd import stmoe as S
     src = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
     src.zero_()
-    out = torch.empty(S.calib_read_out_words(nbytes), dtype=torch.int32, device="cuda:0")
-    S.calib_read(src, nbytes, out)
+    out = torch.empty(S.calib_read_out_words(nbytes, pattern), dtype=torch.int32, device="cuda:0")
+    S.calib_read(src, nbytes, out, pattern=pattern)
     s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s0.record()
     for _ in range(reps):
-        S.calib_read(src, nbytes, out)
+        S.calib_read(src, nbytes, out, pattern=pattern)
     s1.record()
     torch.cuda.synchronize()
     ms = s0.elapsed_time(s1)
@@ -470,7 +550,7 @@ class Workload:
         t0 = time.time()
         self.sel = W.planted_trace(cfg)
         self.prof = W.profiling_selections(cfg, self.sel)
-        self.warm = W.warm_sets(cfg, self.prof)
+        self.warm = S.warm_sets(self.prof, cfg.E, cfg.C)
         log(f"planted trace {self.sel.shape} in {time.time() - t0:.1f}s")
         t0 = time.time()
         self.wg_f64 = [W.router_rows_f64(cfg, l) for l in range(cfg.L)]
@@ -617,14 +697,16 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
     blob = cfg.blob_bytes
-    name, mode, min_score, max_pf, online, after_demand, device = variant
-    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - C)
+    name, mode, min_score, max_pf, online, after_demand, device, staged = variant
+    n_stage = staging_slots(cfg, C)
     demand, side = streams
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
     cache = S.ExpertCache(cfg.L, cfg.E, C, blob, n_stage, arena, ptrs, demand, side)
     cache.warm(W_warm(wl, C))
     cache.set_prefetch_order(after_demand)
     cache.set_device_policy(device)
+    if staged:
+        cache.set_staged_prefetch(staged)
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(wl.prof)
     ctx = make_ctx(wl, pred, cache)
@@ -650,7 +732,7 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
     cst = cache.stats()
     st = pred.stats()
     copies = cst["demand"] + cst["overflow"] + cst["prefetch"]
-    rec = dict(tokens=n_tokens, seconds=round(dt, 4), prefetch_min_score=min_score,
+    rec = dict(tokens=n_tokens, seconds=round(dt, 4), prefetch_min_score=min_score, staged_per_layer=staged,
                prefetch_max_per_layer=max_pf, online_update=bool(online),
                prefetch_after_demand=bool(after_demand), device_decisions=bool(device),
                tokens_per_s=round(cfg.B * n_tokens / dt, 3),
@@ -674,24 +756,39 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
 
 def W_warm(wl, C):
     """Warm start for C slots per layer: the C experts most selected in profiling."""
-    from paper_2606_15453_amd import workload as W
+    from paper_2606_15453_amd import stmoe as S
     if C == wl.cfg.C:
         return wl.warm
-    return W.warm_sets(wl.cfg, wl.prof, C)
+    return S.warm_sets(wl.prof, wl.cfg.E, C)
 
 
 def offload_variants(cfg):
     from paper_2606_15453_amd import stmoe as S
-    return [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 0),
-            ("st_moe", S.MODE_STMOE, 2, cfg.C, 1, 0, 0),
-            ("st_moe_after_demand", S.MODE_STMOE, 2, cfg.C, 1, 1, 0),
-            ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K, 1, 0, 0),
-            ("st_moe_score4_maxK_after_demand", S.MODE_STMOE, 4, cfg.K, 1, 1, 0),
-            ("ht_only", S.MODE_HT_ONLY, 2, cfg.C, 1, 0, 0),
-            ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C, 1, 0, 0),
-            ("on_demand_device", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 1),
-            ("st_moe_device", S.MODE_STMOE, 2, cfg.C, 1, 0, 1),
-            ("st_moe_score4_maxK_after_demand_device", S.MODE_STMOE, 4, cfg.K, 1, 1, 1)]
+    # (name, mode, min score, max prefetches per layer, online update, prefetch after the
+    #  missed loads, device decisions, staged prefetches per layer (0: into evicted slots))
+    return [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 0, 0),
+            ("st_moe", S.MODE_STMOE, 2, cfg.C, 1, 0, 0, 0),
+            ("st_moe_after_demand", S.MODE_STMOE, 2, cfg.C, 1, 1, 0, 0),
+            ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K, 1, 0, 0, 0),
+            ("st_moe_score4_maxK_after_demand", S.MODE_STMOE, 4, cfg.K, 1, 1, 0, 0),
+            ("ht_only", S.MODE_HT_ONLY, 2, cfg.C, 1, 0, 0, 0),
+            ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C, 1, 0, 0, 0),
+            ("on_demand_device", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 1, 0),
+            ("st_moe_device", S.MODE_STMOE, 2, cfg.C, 1, 0, 1, 0),
+            ("st_moe_score4_maxK_after_demand_device", S.MODE_STMOE, 4, cfg.K, 1, 1, 1, 0),
+            ("st_moe_staged", S.MODE_STMOE, 2, cfg.C, 1, 1, 1, STAGED_PER_LAYER(cfg)),
+            ("st_moe_staged1", S.MODE_STMOE, 2, cfg.C, 1, 1, 1, 1)]
+
+
+def STAGED_PER_LAYER(cfg):
+    """Staged prefetches per layer: the experts one token selects (K), at most 8."""
+    return min(cfg.K, 8)
+
+
+def staging_slots(cfg, C):
+    """Staging slots of the cache arena: the host path's overflow ring, and two
+    sets of staged prefetches."""
+    return max(0, min(cfg.B * cfg.K, cfg.E) - C, 2 * STAGED_PER_LAYER(cfg))
 
 
 def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
@@ -700,8 +797,8 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
     pool, ptrs, M = expert_pool(wl, pinned_gb, POOL_TIER)
-    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
-    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
+    n_stage = staging_slots(cfg, cfg.C)
+    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.E, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
                         device="cuda:0")
     streams = (torch.cuda.Stream(), torch.cuda.Stream())
     keep = None if only is None else set(only.split(",")) | {"on_demand"}
@@ -738,8 +835,8 @@ def attention_sweep(wl, key, n_tokens, resident_ms_per_token, pinned_gb, context
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
     pool, ptrs, M = expert_pool(wl, pinned_gb, POOL_TIER)
-    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
-    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
+    n_stage = staging_slots(cfg, cfg.C)
+    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.E, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
                         device="cuda:0")
     streams = (torch.cuda.Stream(), torch.cuda.Stream())
     per_tok = KV_BYTES_PER_TOKEN[key] * cfg.B
@@ -763,8 +860,8 @@ def attention_sweep(wl, key, n_tokens, resident_ms_per_token, pinned_gb, context
         base_ms = resident_ms_per_token + attn_us * cfg.L / 1e3
         recs = {}
         for v in offload_variants(cfg):
-            if v[0] not in ("on_demand", "st_moe", "st_moe_score4_maxK", "st_moe_score4_maxK_after_demand",
-                            "ht_only", "on_demand_device", "st_moe_score4_maxK_after_demand_device"):
+            if v[0] not in ("on_demand", "st_moe", "st_moe_score4_maxK_after_demand", "on_demand_device",
+                            "st_moe_score4_maxK_after_demand_device", "st_moe_staged", "st_moe_staged1"):
                 continue
             recs[v[0]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, base_ms, attn)
         od = recs["on_demand"]["stall_ms_per_token"]
@@ -788,15 +885,15 @@ def offload_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, budgets):
     cfg = wl.cfg
     pool, ptrs, M = expert_pool(wl, pinned_gb, POOL_TIER)
     cmax = max(budgets)
-    n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - min(budgets))
-    arena = torch.empty(S.cache_arena_bytes(cfg.L, cmax, cfg.blob_bytes, n_stage), dtype=torch.uint8,
+    n_stage = staging_slots(cfg, min(budgets))
+    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.E, cmax, cfg.blob_bytes, n_stage), dtype=torch.uint8,
                         device="cuda:0")
     streams = (torch.cuda.Stream(), torch.cuda.Stream())
     rows = []
     for C in budgets:
-        variants = [(n, m, ms, (C if mp == cfg.C else mp), on, ad, dv)
-                    for n, m, ms, mp, on, ad, dv in offload_variants(cfg)]
-        variants.insert(3, ("st_moe_frozen_cct", S.MODE_STMOE, 2, C, 0, 0, 0))
+        variants = [(n, m, ms, (C if mp == cfg.C else mp), on, ad, dv, sg)
+                    for n, m, ms, mp, on, ad, dv, sg in offload_variants(cfg)]
+        variants.insert(3, ("st_moe_frozen_cct", S.MODE_STMOE, 2, C, 0, 0, 0, 0))
         base = None
         for v in variants:
             rec = offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)
@@ -839,7 +936,303 @@ def near_tie_rows(wl, warmup, steps, eps=1e-4):
     return {"rows": n, "of": rows, "eps": eps}
 
 
-def cpu_baseline(wl, max_tokens, target_s):
+# ---------------------------------------------------------------------------
+# Policy bound: what prefetching with one layer of lookahead can win on this
+# link, priced by a time model (CPU arithmetic on the routing trace and the
+# GPU predictor's predictions; no kernel timing beyond the measured inputs).
+# ---------------------------------------------------------------------------
+
+class _Link:
+    """One host-to-device link serving copies first in, first out."""
+
+    def __init__(self, copy_ms):
+        self.copy_ms = copy_ms
+        self.free = 0.0
+
+    def put(self, t, ms=None):
+        ms = self.copy_ms if ms is None else ms
+        self.free = max(self.free, t) + ms
+        return self.free
+
+
+class _Lru:
+    """Per-layer C-slot cache: least recently used with protection of the
+    current set (the library's policy), or the offline optimum (evict the
+    expert whose next use in this layer is farthest)."""
+
+    def __init__(self, warm, C, future=None):
+        self.slots = [list(w) for w in warm]
+        self.last = [[0] * C for _ in warm]
+        self.C = C
+        self.future = future          # future[l] = list over tokens of sets, for the offline optimum
+
+    def victim(self, l, keep, t=None):
+        cands = [c for c in range(self.C) if self.slots[l][c] < 0 or self.slots[l][c] not in keep]
+        if not cands:
+            return -1
+        if self.future is None:
+            return min(cands, key=lambda c: (self.last[l][c], c))
+
+        def nxt(e):
+            for tt in range(t + 1, len(self.future[l])):
+                if e in self.future[l][tt]:
+                    return tt
+            return 1 << 30
+        return max(cands, key=lambda c: (nxt(self.slots[l][c]) if self.slots[l][c] >= 0 else 1 << 31, -c))
+
+    def acquire(self, l, U, stamp, t=None):
+        keep = set(U)
+        misses, overflow = [], []
+        for f in U:
+            if f in self.slots[l]:
+                self.last[l][self.slots[l].index(f)] = stamp
+                continue
+            c = self.victim(l, keep, t)
+            if c < 0:
+                overflow.append(f)
+                continue
+            self.slots[l][c] = f
+            self.last[l][c] = stamp
+            misses.append(f)
+        return misses, overflow
+
+    def prefetch(self, l, ranked, stamp, t=None):
+        ranked = ranked[:self.C]
+        keep = set(ranked)
+        out = []
+        for f in ranked:
+            if f in self.slots[l]:
+                continue
+            c = self.victim(l, keep, t)
+            if c < 0:
+                break
+            self.slots[l][c] = f
+            self.last[l][c] = stamp
+            out.append(f)
+        return out
+
+
+def simulate_policy(trace, preds, L, C, warm, copy_ms, layer_ms, attn_ms, policy, max_staged=None):
+    """Time model of the capped decode loop.  trace[t][l]: distinct selected
+    experts; preds[t][l]: the admitted ranking for the layer after (t, l).
+    Per layer: the attention window (attn_ms), routing and decisions, the
+    missed copies on the link (the FFN waits for every copy it needs), the FFN
+    (layer_ms covers routing and FFN), and the next layer's prefetches queued
+    on the link behind this layer's missed copies.
+
+    policy: "demand" (no prefetch), "evict" (prefetch into LRU victims, the
+    copies run to the end), "staged" (prefetch into spare buffers without
+    eviction, cancelled when the next layer's routing shows them unused),
+    "perfect_evict" / "perfect_staged" (the same with the exact next-layer
+    selection as the prediction), "optimum" (offline-optimal replacement, no
+    prefetch).  Returns (stall ms per token, copies started, copy-ms wasted)."""
+    T = len(trace)
+    future = [[trace[t][l] for t in range(T)] for l in range(L)] if policy == "optimum" else None
+    cache = _Lru(warm, C, future)
+    link = _Link(copy_ms)
+    clock, copies, wasted = 0.0, 0, 0.0
+    pend = {}                     # layer -> [(expert, start, end)] prefetch copies issued for it
+    perfect = policy.startswith("perfect")
+    staged = policy.endswith("staged")
+    for t in range(T):
+        for l in range(L):
+            clock += attn_ms
+            route_end = clock + 0.05 * layer_ms
+            U = trace[t][l]
+            stamp = t * L + l + 1
+            jobs = pend.pop(l, [])
+            ready = route_end
+            if staged:
+                # the link at route_end: unused staged copies stop there; the used ones go on
+                keep = [j for j in jobs if j[0] in U]
+                drop = [j for j in jobs if j[0] not in U]
+                for f, s0, e0 in drop:
+                    wasted += max(0.0, min(e0, route_end) - s0)
+                # only this layer's staged copies can still be on the link here
+                link.free = min(link.free, route_end)
+                for f, s0, e0 in keep:
+                    rest = e0 - max(s0, route_end) if e0 > route_end else 0.0
+                    end = link.put(route_end, rest) if rest > 0 else e0
+                    ready = max(ready, end)
+                staged_ok = {j[0] for j in keep}
+                misses, overflow = cache.acquire(l, U, stamp, t)
+                for f in misses + overflow:
+                    if f in staged_ok:
+                        continue
+                    ready = max(ready, link.put(route_end))
+                    copies += 1
+            else:
+                inflight = {f: e0 for f, _, e0 in jobs}
+                for f, s0, e0 in jobs:
+                    if f not in U:
+                        wasted += e0 - s0
+                misses, overflow = cache.acquire(l, U, stamp, t)
+                for f in U:
+                    if f in inflight and f not in misses:
+                        ready = max(ready, inflight[f])
+                for f in misses + overflow:
+                    ready = max(ready, link.put(route_end))
+                    copies += 1
+            clock = ready + 0.95 * layer_ms
+            # prefetch for the next layer, behind this layer's missed copies
+            if policy == "demand" or policy == "optimum":
+                continue
+            nl, nt = (l + 1) % L, t + (l + 1) // L
+            if perfect:
+                if nt >= T:
+                    continue
+                ranked = [f for f in trace[nt][nl]]
+            else:
+                ranked = preds[t][l]
+            if staged:
+                resident = set(cache.slots[nl])
+                cand = [f for f in ranked if f not in resident][:max_staged or C]
+                out = []
+                for f in cand:
+                    end = link.put(route_end)
+                    out.append((f, end - copy_ms, end))
+                    copies += 1
+                pend[nl] = out
+            else:
+                got = cache.prefetch(nl, ranked, stamp, t)
+                out = []
+                for f in got:
+                    end = link.put(route_end)
+                    out.append((f, end - copy_ms, end))
+                    copies += 1
+                pend[nl] = out
+    ideal = T * L * (attn_ms + layer_ms)
+    return (clock - ideal) / T, copies, wasted
+
+
+def policy_bound(names, n_tokens, attn_list):
+    """Markdown table of simulate_policy over the planted traces, with the GPU
+    predictor's rankings (paper threshold) and measured inputs: the H2D copy
+    time of one expert (pinned host -> HBM, event-timed) and the layer time of
+    the HBM-resident decode (router + FFN, event-timed on one layer's call)."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    dev = "cuda:0"
+    out = ["| workload | attention ms/layer | policy | copies | wasted copy-ms | stall ms/token | "
+           "stall vs on-demand |", "|---|---|---|---|---|---|---|"]
+    for name in names:
+        cfg = W.CONFIGS[name]
+        T = min(n_tokens, cfg.T)
+        sel = W.planted_trace(cfg, n_tokens=cfg.P + T)
+        prof = sel[:cfg.P]
+        dec = sel[cfg.P:]
+        trace = [[sorted(set(int(v) for b in range(cfg.B) for v in dec[t, b, l])) for l in range(cfg.L)]
+                 for t in range(T)]
+        # the GPU predictor's admitted rankings (paper threshold, capped at C)
+        p = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+        p.profile(prof)
+        ranked = torch.zeros(cfg.E, dtype=torch.int32, device=dev)
+        nr = torch.zeros(1, dtype=torch.int32, device=dev)
+        dsel = torch.from_numpy(np.ascontiguousarray(dec.transpose(0, 2, 1, 3))).to(dev)
+        preds = []
+        for t in range(T):
+            row = []
+            for l in range(cfg.L):
+                cur = dsel[t, l]
+                p.update(l, dsel[t, l - 1] if l else None, cur)
+                if l + 1 < cfg.L:
+                    p.predict(l, cur, use=S.USE_BOTH, ranked=ranked, n_ranked=nr)
+                else:
+                    p.predict(-1, None, use=S.USE_HT, ranked=ranked, n_ranked=nr)
+                n = int(nr.item())
+                row.append(ranked[:n].cpu().tolist())
+            preds.append(row)
+        p.close()
+        # measured inputs: one expert's H2D copy, one layer's resident routing + FFN
+        blob = cfg.blob_bytes
+        host = torch.empty(blob, dtype=torch.uint8).pin_memory()
+        devb = torch.empty(blob, dtype=torch.uint8, device=dev)
+        devb.copy_(host, non_blocking=True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            devb.copy_(host, non_blocking=True)
+        e1.record()
+        torch.cuda.synchronize()
+        copy_ms = e0.elapsed_time(e1) / 5
+        del host, devb
+        layer_ms = ffn_layer_ms(cfg)
+        warm = S.warm_sets(prof, cfg.E, cfg.C)
+        log(f"policy bound {name}: copy {copy_ms:.3f} ms, layer {layer_ms:.4f} ms, {T} tokens")
+        for attn in attn_list:
+            base = None
+            for pol in ("demand", "evict", "staged", "perfect_evict", "perfect_staged", "optimum"):
+                stall, copies, wasted = simulate_policy(trace, preds, cfg.L, cfg.C, warm, copy_ms, layer_ms,
+                                                        attn, pol, max_staged=cfg.C)
+                if base is None:
+                    base = stall
+                out.append(f"| {cfg.name} (copy {copy_ms:.3f} ms, layer {layer_ms:.3f} ms) | {attn:.2f} | {pol} | "
+                           f"{copies} | {wasted:.1f} | {stall:.2f} | {1 - stall / base:+.3f} |")
+    return out
+
+
+def ffn_layer_ms(cfg, reps=20):
+    """Event-timed routing + expert FFN of one layer at the config's shape
+    (the distinct experts of one seeded routing generated in HBM)."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    dev = "cuda:0"
+    rng = np.random.default_rng(cfg.seed)
+    idx = np.stack([rng.choice(cfg.E, cfg.K, replace=False) for _ in range(cfg.B)]).astype(np.int32)
+    w = rng.random((cfg.B, cfg.K)).astype(np.float32)
+    selx = sorted(set(idx.ravel().tolist()))
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    store = torch.empty((len(selx) + cfg.n_shared, cfg.blob_elems), dtype=tdt, device=dev)
+    for k, e in enumerate(selx):
+        W.expert_blob_torch(cfg, 0, e, store[k])
+    for sh in range(cfg.n_shared):
+        W.expert_blob_torch(cfg, 0, sh, store[len(selx) + sh], shared=True)
+    ptrs = [store[0].data_ptr()] * cfg.E
+    for k, e in enumerate(selx):
+        ptrs[e] = store[k].data_ptr()
+    eptr = torch.tensor(ptrs, dtype=torch.int64, device=dev)
+    sptr = (torch.tensor([store[len(selx) + sh].data_ptr() for sh in range(cfg.n_shared)], dtype=torch.int64,
+                         device=dev) if cfg.n_shared else None)
+    dt = S.BF16 if cfg.dtype == "bf16" else S.F32
+    x = Workload._dev(W.to_storage(cfg, rng.normal(0, 1, (cfg.B, cfg.H))))
+    wg = Workload._dev(W.router_rows(cfg, 0))
+    y = torch.empty((cfg.B, cfg.H), dtype=torch.float32, device=dev)
+    ws = torch.zeros(S.ffn_workspace_bytes(cfg.B, cfg.K, cfg.E, cfg.H, cfg.I, cfg.n_shared, dt),
+                     dtype=torch.uint8, device=dev)
+    rws = torch.zeros(S.route_workspace_bytes(cfg.B, cfg.E), dtype=torch.uint8, device=dev)
+    ti, tw = torch.from_numpy(idx).to(dev), torch.from_numpy(w).to(dev)
+    ri, rw = torch.empty_like(ti), torch.empty_like(tw)
+
+    def call():
+        S.route_topk(x, wg, cfg.K, ri, rw, rws, dtype=dt)
+        S.expert_ffn(x, ti, tw, cfg.H, cfg.I, cfg.E, dt, eptr, y, ws, shared_ptrs=sptr, n_shared=cfg.n_shared)
+
+    for _ in range(3):
+        call()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    del store
+    return e0.elapsed_time(e1) / reps
+
+
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), or None."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline_run(wl, max_tokens, target_s):
     """The CPU oracle on the first decode tokens of the same workload, until
     `target_s` seconds of timed work (at most max_tokens tokens).
 
@@ -848,17 +1241,12 @@ def cpu_baseline(wl, max_tokens, target_s):
     generator's GPU blobs widened to fp64 on the GPU and copied into pinned
     host buffers)."""
     import torch
-    from oracle.stmoe_oracle import STPredictor, CacheSim, decode_storage, moe_ffn, route
+    from oracle.stmoe_oracle import STPredictor, CacheSim, admitted, decode_storage, moe_ffn, route, \
+        warm_from_profile
     cfg = wl.cfg
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:
-        cores = os.cpu_count()
     pred = STPredictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(wl.prof)
-    cache = CacheSim(cfg.L, cfg.E, cfg.C, wl.warm)
-    P_cur = pred.predict(-1, None)
+    cache = CacheSim(cfg.L, cfg.E, cfg.C, warm_from_profile(wl.prof, cfg.L, cfg.E, cfg.C))
     timed = 0.0
     n, Hh, Ii = cfg.H * cfg.I, cfg.H, cfg.I
     n_bufs = min(cfg.B * cfg.K, cfg.E) + cfg.n_shared
@@ -893,22 +1281,47 @@ def cpu_baseline(wl, max_tokens, target_s):
             shared = [mats(wl.shared[l * cfg.n_shared + s]) for s in range(cfg.n_shared)]
             t0 = time.perf_counter()
             moe_ffn(x, r["idx"], r["w"], lambda e: experts[e], shared=shared)
-            cache.prefetch((l + 1) % cfg.L, STPredictor.ranked_union(P_next), t * cfg.L + l + 1)
+            cache.prefetch((l + 1) % cfg.L, admitted(P_next), t * cfg.L + l + 1)
             timed += time.perf_counter() - t0
-            prev, P_cur = cur, P_next
+            prev = cur
             del experts
     del bufs
-    return dict(value=round(cfg.B * n_tokens / timed, 4), unit="tokens/s", cores=int(cores),
-                kind="oracle", seconds=round(timed, 3),
-                sample=f"first {n_tokens} decode token(s) x {cfg.L} layers x batch {cfg.B} of the same "
-                       f"workload: fp64 routing, predictor, cache policy and SwiGLU FFN, {timed:.1f} s of "
-                       f"timed CPU work (expert matrix preparation not timed)")
+    return n_tokens, timed
+
+
+def cpu_baseline(wl, max_tokens, target_s):
+    """The oracle timed twice on the host: with every core its BLAS library
+    uses, and single-threaded (BLAS limited to one thread)."""
+    cfg = wl.cfg
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+    except ImportError:
+        threadpool_info = threadpool_limits = None
+    cores = os.cpu_count()
+    if threadpool_info is not None:
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    n_all, t_all = cpu_baseline_run(wl, max_tokens, target_s)
+    single = None
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            n_one, t_one = cpu_baseline_run(wl, max_tokens, target_s)
+        single = dict(value=round(cfg.B * n_one / t_one, 4), seconds=round(t_one, 3), tokens=n_one, cores=1)
+    return dict(value=round(cfg.B * n_all / t_all, 4), unit="tokens/s", cores=int(cores),
+                kind="oracle", seconds=round(t_all, 3), single_thread=single,
+                host_cpus=os.cpu_count(), cpu_model=cpu_model(),
+                sample=f"first {n_all} decode token(s) x {cfg.L} layers x batch {cfg.B} of the same "
+                       f"workload: fp64 routing, predictor, cache policy and SwiGLU FFN, {t_all:.1f} s of "
+                       f"timed CPU work on {cores} BLAS threads (expert matrix preparation not timed); "
+                       f"single_thread: the same with BLAS limited to one thread")
 
 
 def main():
     args = parse()
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
+        return
+    if args.summarize_gaps:
+        summarize_gaps(*args.summarize_gaps)
         return
     if args.summarize_overlap:
         summarize_overlap(*args.summarize_overlap)
@@ -929,7 +1342,12 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
     if args.counters:
-        counters_workload()
+        counters_workload(args.config)
+        return
+    if args.policy_bound:
+        lines = policy_bound(args.policy_bound.split(","), max(args.offload_tokens, 1),
+                             [float(a) for a in args.policy_attn.split(",")])
+        print("\n".join(lines), flush=True)
         return
     if args.ffn_sweep:
         ffn_sweep()
@@ -1030,10 +1448,14 @@ def main():
             "precision": round(float(stats[:, 0].sum() / max(stats[:, 2].sum(), 1)), 4),
         },
     }
-    read_gbps = achievable_read_gbps()
-    out["achievable_read_gbps"] = round(read_gbps, 1)
+    read_stride = achievable_read_gbps(pattern=0)
+    read_blocked = achievable_read_gbps(pattern=1)
+    read_gbps = max(read_stride, read_blocked)
+    out["achievable_read_gbps"] = {"grid_stride": round(read_stride, 1), "contiguous_per_workgroup":
+                                   round(read_blocked, 1)}
     out["roofline"]["frac_of_achievable_read"] = round(up_gbps / read_gbps, 4)
-    log(f"streaming-read probe: {read_gbps:.0f} GB/s")
+    log(f"streaming-read probes: grid stride {read_stride:.0f} GB/s, contiguous per workgroup "
+        f"{read_blocked:.0f} GB/s")
     if args.offload_tokens > 0:
         out["offload"] = offload(wl, args.offload_tokens, ms_per_step, args.pinned_gb, args.offload_only)
     if args.cpu_tokens > 0:

@@ -17,9 +17,15 @@
  *     nothing on the device.
  *   - "device" pointers are HIP device allocations of the current device;
  *     "host" pointers are ordinary (or pinned, where stated) host memory.
- *   - The caller owns every buffer it passes and every stream.  The library
- *     owns only the opaque handles it creates (and the device tables behind
- *     them) and frees them in the matching destroy call.
+ *   - The caller owns every device buffer and every stream.  Device memory a
+ *     handle needs (predictor tables, decode-context buffers, cache slots and
+ *     the cache's decision state) comes from a caller workspace sized by the
+ *     matching *_workspace_bytes / *_arena_bytes query and passed to the
+ *     create call; the library never allocates or frees device memory.  It
+ *     owns only the opaque host-side handles (and, for the decode context,
+ *     one small pinned host record, events and internal streams), released
+ *     by the matching destroy call.  A workspace must stay allocated, and
+ *     must not be touched by the caller, until the handle is destroyed.
  *   - `stream` arguments are hipStream_t values passed as void* (NULL is the
  *     default stream).  Calls are asynchronous on that stream unless marked
  *     [sync].
@@ -51,7 +57,7 @@ typedef enum { STMOE_F32 = 0, STMOE_BF16 = 1 } stmoe_dtype;
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* stmoe_last_error(void);
-/* ABI version of this header: 1. */
+/* ABI version of this header: 2. */
 int stmoe_abi_version(void);
 
 /* Pinned host memory for the expert pool (exact size, hipHostMalloc; not
@@ -97,8 +103,13 @@ typedef struct stmoe_predictor stmoe_predictor;
 /* Prediction sources, for the ablation of Section 5 (temporal / spatial). */
 enum { STMOE_USE_CCT = 1, STMOE_USE_HT = 2, STMOE_USE_BOTH = 3 };
 
-/* Allocate the device tables of a predictor (zeroed).  [sync] */
-int stmoe_create(int L, int E, int K, int B, stmoe_predictor** out);
+/* Device bytes of a predictor's workspace (its tables, hit statistics and
+ * the staging area of the profiling selections); 0 for an invalid shape. */
+size_t stmoe_workspace_bytes(int L, int E, int K, int B);
+/* Create a predictor whose tables live in dev_ws (device, 256-byte aligned,
+ * at least stmoe_workspace_bytes(L, E, K, B) bytes; zeroed here).  [sync] */
+int stmoe_create(int L, int E, int K, int B, void* dev_ws, size_t ws_bytes, stmoe_predictor** out);
+/* Release the handle (the workspace stays the caller's). */
 int stmoe_destroy(stmoe_predictor* p);
 
 /* Algorithm 1 and the HT initialisation (Section 4.1).  [sync]
@@ -107,7 +118,8 @@ int stmoe_destroy(stmoe_predictor* p);
  * For each pair i, Co_i[e][f] counts tokens and rows that selected e at
  * layer i and f at layer i+1; CCT_i[e] takes the K largest counts (equal
  * counts -> lower index) with confidence 2; HT[l][b] <- sel[P-1][b][l].
- * Resets the hit statistics. */
+ * Resets the hit statistics.  The selections pass through the workspace's
+ * staging area in chunks of whole tokens. */
 int stmoe_profile(stmoe_predictor* p, const int32_t* sel, int P);
 
 /* Verify + table update at `layer` (Algorithm 3; Section 4.3.4).
@@ -143,12 +155,16 @@ int stmoe_predict(stmoe_predictor* p, int layer, const int32_t* sel_cur, int use
 
 /* Copy the tables to host memory (any pointer may be NULL).  [sync]
  *   co [L-1][E][E] int32, cct_idx / cct_conf [L-1][E][K] uint8,
- *   ht [L][B][K] uint8 */
+ *   ht [L][B][K] int32 (rows ascending) */
 int stmoe_export(stmoe_predictor* p, int32_t* co, uint8_t* cct_idx, uint8_t* cct_conf,
-                 uint8_t* ht);
-/* Replace the CCT and HT with host copies (same layouts).  [sync] */
+                 int32_t* ht);
+/* Replace the CCT and HT with host copies (same layouts).  Every CCT entry
+ * must name K distinct experts < E with confidences in 0..3, and every HT
+ * row K distinct experts < E (stored sorted); otherwise STMOE_EINVAL and
+ * nothing changes.  Distinct entries bound every Eq. 1 score by 3K + 2.
+ * [sync] */
 int stmoe_import(stmoe_predictor* p, const uint8_t* cct_idx, const uint8_t* cct_conf,
-                 const uint8_t* ht);
+                 const int32_t* ht);
 
 /* Hit statistics per layer since stmoe_profile, host out [L][3] int64:
  * (sum |A intersect P|, sum |A|, sum |P|) over batch rows.  [sync] */
@@ -211,6 +227,12 @@ typedef struct {
     int64_t hits, demand, overflow, prefetch, useful, wasted;
 } stmoe_cache_stats;
 
+/* Initial residency of a cache (Section 4.1 stages experts before decode;
+ * the paper names no choice): per layer the C experts most often selected by
+ * the profiling tokens, count desc then index asc, -1 padding when C > E.
+ *   sel host [P][B][L][K] int32 (each < E); out host [L][C] int32.  [host] */
+int expert_cache_warm_sets(const int32_t* sel, int P, int B, int L, int K, int E, int C, int32_t* out);
+
 int stmoe_policy_create(int L, int E, int C, const int32_t* warm /* host [L][C], -1 = empty */,
                         stmoe_policy** out);
 int stmoe_policy_destroy(stmoe_policy* p);
@@ -234,7 +256,9 @@ int stmoe_policy_stats(const stmoe_policy* p, stmoe_cache_stats* out);
  * reuse is ordered by events (a slot is overwritten only after its last
  * reader and its previous copy have completed).
  *
- *   arena       device, at least expert_cache_arena_bytes(L, C, blob, n_stage)
+ *   arena       device, 256-byte aligned, at least
+ *               expert_cache_arena_bytes(L, E, C, blob, n_stage): the L*C slots and
+ *               n_stage staging slots, then the state of device-side decisions
  *   host_blobs  host array [L*E] of pinned host blob pointers.  Device
  *               pointers are accepted too (the copies then run device to
  *               device: a pool in another HBM region models a backing tier
@@ -244,7 +268,7 @@ int stmoe_policy_stats(const stmoe_policy* p, stmoe_cache_stats* out);
  * ---------------------------------------------------------------------- */
 typedef struct expert_cache expert_cache;
 
-size_t expert_cache_arena_bytes(int L, int C, size_t blob_bytes, int n_stage);
+size_t expert_cache_arena_bytes(int L, int E, int C, size_t blob_bytes, int n_stage);
 int expert_cache_create(int L, int E, int C, size_t blob_bytes, int n_stage, void* arena,
                         size_t arena_bytes, const void* const* host_blobs, void* demand_stream,
                         void* side_stream, expert_cache** out);
@@ -277,6 +301,24 @@ int expert_cache_set_prefetch_order(expert_cache* c, int after_demand);
  * expert_cache_stats reads the device counters.  on = 0 moves the state
  * back to the host policy.  [sync] */
 int expert_cache_set_device_policy(expert_cache* c, int on);
+/* Staged prefetch (device decisions only; Section 4.1 prefetches predicted
+ * experts, Section 4.3.4 overlaps the transfer with computation).  n > 0:
+ * instead of evicting slots, the next layer's admitted predicted experts
+ * that are not resident (at most n, ranked order) are copied into spare
+ * staging blocks of the arena (2n of the n_stage staging slots: two sets
+ * alternate between consecutive layers) after the layer's missed loads.  At
+ * the next layer's decisions a staged expert that was selected is used from
+ * its block: when it takes a slot (the slot the missed load would take) the
+ * two blocks swap places, with no copy; otherwise the FFN reads the staging
+ * block.  Staged experts that were not selected are cancelled: their copy
+ * stops at its next check.  Residency and the slots' contents evolve exactly
+ * as with on-demand loading; counts: prefetch = staged copies issued, useful
+ * = staged experts selected, wasted = cancelled, demand and overflow = the
+ * other misses.  n = 0 returns to prefetching into slots.  Once staged
+ * prefetches have run, switching device decisions off returns STMOE_ESTATE
+ * (slots may live in other arena blocks).  STMOE_ESTATE without device
+ * decisions; STMOE_EINVAL if 2n > n_stage.  [sync] */
+int expert_cache_set_staged_prefetch(expert_cache* c, int n_per_layer);
 /* Make `needed` (host, n distinct experts) resident for a kernel on
  * `compute`: demand copies on the demand stream, `compute` waits for every
  * copy it needs; dev_table_out (host [E]) receives the device blob pointer
@@ -309,12 +351,18 @@ typedef struct {
 
 typedef struct moe_ctx moe_ctx;
 
+/* Device bytes of a context's workspace: routing records, the routing and
+ * FFN workspaces, expert pointer tables, the per-token predictor arguments
+ * and the graph-replay staging buffers; 0 for an invalid description. */
+size_t moe_ctx_workspace_bytes(const moe_model_desc* desc);
 /* cache may be NULL only when desc->resident_w is given.  pred (if given)
  * and cache must have been created for the same L, E (and, for pred, K and
  * B) as desc, and the cache's blob size must hold one expert
- * (moe_blob_bytes(H, I, dtype)); otherwise STMOE_EINVAL. */
+ * (moe_blob_bytes(H, I, dtype)); otherwise STMOE_EINVAL.  dev_ws: device,
+ * 256-byte aligned, at least moe_ctx_workspace_bytes(desc) bytes (zeroed
+ * here).  [sync] */
 int moe_ctx_create(const moe_model_desc* desc, stmoe_predictor* pred, expert_cache* cache,
-                   void* compute_stream, moe_ctx** out);
+                   void* compute_stream, void* dev_ws, size_t ws_bytes, moe_ctx** out);
 int moe_ctx_destroy(moe_ctx* ctx);
 /* One MoE layer for decode token `token`:
  *   x device [B][H] dtype; y device out [B][H] fp32.
@@ -326,8 +374,23 @@ int moe_ctx_destroy(moe_ctx* ctx);
  * token, before selections it still reads are rewritten).  Layers are
  * expected in order 0..L-1 per token; other orders are correct but wait.
  * Layer-0 predictions come from HT[0]; the prefetch for layer 0 of the next
- * token is issued at layer L-1. */
-int moe_decode_layer(moe_ctx* ctx, int token, int layer, const void* x, float* y, int mode);
+ * token is issued at layer L-1.
+ * rep (host, or NULL): when given, the call waits for the layer's work on
+ * every stream and fills the report below. */
+typedef struct {
+    int32_t B, K;
+    int32_t idx[16 * 16];       /* [B][K] the layer's selection, descending logit */
+    float w[16 * 16];           /* [B][K] its gate weights */
+    int32_t n_ranked;           /* experts predicted for the next layer (score >= 2),
+                                   -1 when the mode predicts nothing */
+    int32_t ranked[256];        /* their ranking (max score over rows desc, index asc),
+                                   -1 padding */
+    int64_t pred_stats[3];      /* this layer's predictor statistics since profiling:
+                                   sum |A n P|, sum |A|, sum |P| (0 without a predictor) */
+    stmoe_cache_stats cache;    /* cache counters so far (0 without a cache) */
+} moe_layer_report;
+int moe_decode_layer(moe_ctx* ctx, int token, int layer, const void* x, float* y, int mode,
+                     moe_layer_report* rep);
 /* Prefetch admission (cache only).  A predicted expert is prefetched only if
  * its prediction score (max over rows, Eq. 1) is at least min_score, and at
  * most max_per_layer experts are prefetched per layer (the ranked order
@@ -360,10 +423,11 @@ int moe_decode_token(moe_ctx* ctx, int token, const void* xs, float* ys, int mod
  * [sync] */
 int moe_ctx_set_predictor_batch(moe_ctx* ctx, int on);
 /* Graph replay of moe_decode_token on (1) or off (0); contexts without a
- * cache only.  Turning it on allocates the staging buffers (L*B*H elements
- * of the storage dtype and L*B*H fp32) and an internal stream; the graph
- * launch is ordered after earlier work on the compute stream and before
- * later work on it by events.  [sync] */
+ * cache only.  The staging buffers (L*B*H elements of the storage dtype and
+ * L*B*H fp32) are part of the context's workspace; turning replay on
+ * creates an internal stream.  The graph launch is ordered after earlier
+ * work on the compute stream and before later work on it by events.
+ * [sync] */
 int moe_ctx_set_graph(moe_ctx* ctx, int on);
 /* The staging buffers of graph replay (device, owned by the context):
  * x_stage [L][B][H] storage dtype, y_stage [L][B][H] fp32.  Writing the
@@ -399,12 +463,14 @@ int moe_ctx_stage_timing(moe_ctx* ctx, double* route_ms, double* miss_ms, double
  *     aligned): reads and writes exactly `bytes`; used to turn the
  *     FETCH_SIZE / WRITE_SIZE hardware counters into bytes.
  *   stmoe_calib_read: streams `bytes` with the expert FFN's non-temporal
- *     16-byte loads; out (device, stmoe_calib_read_out_words(bytes) words)
- *     receives one checksum word per workgroup.
+ *     16-byte loads; out (device, stmoe_calib_read_out_words(bytes, pattern)
+ *     words) receives one checksum word per workgroup.  pattern 0: a
+ *     grid-stride sweep; 1: every workgroup reads one contiguous 256 KiB
+ *     region (the way the FFN's workgroups read an expert's rows).
  * ---------------------------------------------------------------------- */
 int stmoe_calib_copy(const void* src, void* dst, size_t bytes, void* stream);
-size_t stmoe_calib_read_out_words(size_t bytes);
-int stmoe_calib_read(const void* src, size_t bytes, unsigned* out, void* stream);
+size_t stmoe_calib_read_out_words(size_t bytes, int pattern);
+int stmoe_calib_read(const void* src, size_t bytes, int pattern, unsigned* out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -314,10 +314,17 @@ class CacheSim:
     (last_use, slot); with no such slot the copy streams through staging
     without admission.  Then every resident expert of U gets last_use = stamp.
     Residency counts from copy issue, so counts do not depend on timing.
+
+    staged = n > 0 (an alternative use of the same prediction): prefetch copies
+    the first n ranked experts that are not resident aside, changing no slot;
+    acquire then decides exactly as without prefetching, except that a staged
+    expert needs no copy (useful); staged experts not selected are wasted.
     """
 
-    def __init__(self, L: int, E: int, C: int, warm=None):
+    def __init__(self, L: int, E: int, C: int, warm=None, staged: int = 0):
         self.L, self.E, self.C = L, E, C
+        self.staged = staged
+        self.stage = [[] for _ in range(L)]
         self.slot = [[-1] * C for _ in range(L)]
         self.last = [[0] * C for _ in range(L)]
         self.pending = [set() for _ in range(L)]
@@ -340,6 +347,14 @@ class CacheSim:
         return min(cands, key=lambda c: (self.last[l][c], c))
 
     def prefetch(self, l: int, ranked, stamp: int):
+        if self.staged:
+            # staged: the first `staged` ranked experts that are not resident are
+            # copied aside; no slot changes hands
+            copies = [f for f in (int(v) for v in ranked) if self._where(l, f) < 0][:self.staged]
+            self.stage[l] = copies
+            self.n.prefetch += len(copies)
+            self.n.log.append(("P", l, stamp, tuple((f, -1) for f in copies)))
+            return [(f, -1) for f in copies]
         ranked = [int(f) for f in ranked][:self.C]
         keep = set(ranked)
         copies = []
@@ -361,6 +376,7 @@ class CacheSim:
         U = sorted(set(int(f) for f in U))
         keep = set(U)
         where, demand, overflow = {}, [], []
+        staged = set(self.stage[l])
         for f in U:
             c = self._where(l, f)
             if c >= 0:
@@ -369,17 +385,23 @@ class CacheSim:
                 continue
             c = self._victim(l, keep)
             if c < 0:
-                overflow.append(f)
+                if f not in staged:           # a staged expert is used from its staging copy
+                    overflow.append(f)
                 where[f] = -1
                 continue
             self.slot[l][c] = f
-            demand.append((f, c))
+            if f not in staged:               # a staged expert takes the slot without a copy
+                demand.append((f, c))
             where[f] = c
         for f, c in where.items():
             if c >= 0:
                 self.last[l][c] = stamp
-        hits = len(U) - len(demand) - len(overflow)
-        useful, wasted = len(self.pending[l] & keep), len(self.pending[l] - keep)
+        hits = sum(1 for f in U if f not in staged) - len(demand) - len(overflow)
+        if self.staged:
+            useful, wasted = len(staged & keep), len(staged - keep)
+            self.stage[l] = []
+        else:
+            useful, wasted = len(self.pending[l] & keep), len(self.pending[l] - keep)
         self.n.demand += len(demand)
         self.n.overflow += len(overflow)
         self.n.useful += useful
@@ -425,7 +447,7 @@ def warm_from_profile(prof_sel, L: int, E: int, C: int):
 
 def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=None,
                      mode=MODE_STMOE, renorm=False, ffn_of=None, ffn_tokens=0, online=True,
-                     tables=None, min_score=THRESHOLD, max_per_layer=None):
+                     tables=None, min_score=THRESHOLD, max_per_layer=None, staged=0):
     """Run the decode loop on the CPU.
 
     x_of(t, l) -> x [B][H] float64; wg_of(l) -> W_g [E][H] float64;
@@ -437,7 +459,8 @@ def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=N
     and replacement steps are skipped; HT is still overwritten).
     tables=(cct_idx, cct_conf, ht) replaces the profiled tables before the
     first token (planted wrong predictions).  min_score / max_per_layer are
-    the prefetch admission knobs of ``admitted``.
+    the prefetch admission knobs of ``admitted``; staged > 0 stages prefetches
+    aside instead of evicting (CacheSim).
     Returns a dict of per-(t, l) records and totals.
     """
     pred = STPredictor(L, E, K, B)
@@ -446,7 +469,7 @@ def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=N
         pred.load_tables(*tables)
     use_cct = mode in (MODE_STMOE, MODE_CCT_ONLY)
     use_ht = mode in (MODE_STMOE, MODE_HT_ONLY)
-    cache = CacheSim(L, E, C, warm) if C is not None else None
+    cache = CacheSim(L, E, C, warm, staged) if C is not None else None
     # layer 0 of the first token is predicted from the profiled HT[0]
     P_cur = pred.predict(-1, None, use_cct=False, use_ht=use_ht)
     rec = dict(idx=[], w=[], scores=[], hits=np.zeros((n_tokens, L), np.int64),

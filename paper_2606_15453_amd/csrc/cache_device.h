@@ -24,8 +24,16 @@ struct PolicyState {
     stmoe_cache_stats* st;
 };
 
-int device_cache_create(const PolicyState& ps, char* arena, size_t blob, const void* const* host_blobs,
-                        hipStream_t side, DeviceCache** out);
+// Bytes of device decision state for a cache of L layers, E experts and C
+// slots per layer (part of the cache arena).
+size_t device_cache_state_bytes(int L, int E, int C);
+// `state`: device_cache_state_bytes(L, E, C) bytes of the cache arena,
+// 256-byte aligned; the decisions keep their state there.
+int device_cache_create(const PolicyState& ps, char* arena, size_t blob, int n_stage,
+                        const void* const* host_blobs, char* state, hipStream_t side, DeviceCache** out);
+// Staged prefetch with ns positions per parity (0: prefetch into slots).  [sync]
+int device_cache_set_staged(DeviceCache* d, int ns);
+int device_cache_staged(const DeviceCache* d);
 int device_cache_download(DeviceCache* d, const PolicyState& ps);
 void device_cache_destroy(DeviceCache* d);
 int device_cache_stats(DeviceCache* d, stmoe_cache_stats* st);

@@ -8,6 +8,16 @@
 // k-th missed (or non-resident ranked) expert takes the k-th victim in
 // (last use, slot) order: the kernel ranks slots and experts in parallel
 // instead of searching once per copy.
+//
+// Staged prefetch (an alternative to prefetching into evicted slots): the
+// predicted experts of the next layer are copied into spare staging blocks,
+// evicting nothing, after the layer's missed loads.  At the next layer's
+// decisions a staged expert that was selected is served from its block: if
+// it takes a slot, the slot's block and the staging block swap places (no
+// copy); staged experts that were not selected are cancelled, and their copy
+// kernel stops at its next check.  Residency therefore evolves exactly as
+// with on-demand loading; the staged copies only move bytes earlier, while
+// the link would otherwise idle during the layer's computation.
 #include <vector>
 
 #include "cache_device.h"
@@ -20,8 +30,11 @@ constexpr int kBlitWgs = 64;     // copy kernel workgroups (enough to fill the h
 
 struct Copy {
     const char* src;             // device-accessible host blob
-    char* dst;                   // HBM slot
+    char* dst;                   // HBM block
+    const int32_t* cancel;       // null, or a flag that stops the copy once set
 };
+
+constexpr int kStageMax = kMaxE;  // staging positions per parity
 
 struct DecideArgs {
     int L, E, C, layer, next, BK, pf_min, pf_max;
@@ -42,8 +55,16 @@ struct DecideArgs {
     const void** table;          // [E] for `layer`
     Copy* demand;                // [kMaxE]
     int32_t* n_demand;
-    Copy* pf;                    // [C] for `next`
+    Copy* pf;                    // [kMaxE] for `next`
     int32_t* n_pf;               // for `next`
+    int32_t* blk;                // [L*C] arena block of each slot
+    // staged prefetch (ns > 0): two parities of ns positions; ctl = {parity
+    // issued last, target layer of parity 0 and 1, count of parity 0 and 1}
+    int ns;
+    int32_t* sblk;               // [2][kStageMax] arena block of each position
+    int32_t* sexp;               // [2][kStageMax] staged expert
+    int32_t* cancel;             // [2][kStageMax]
+    int32_t* ctl;                // [5]
 };
 
 // Exclusive rank of a flag among the workgroup's threads (thread order) and
@@ -96,9 +117,9 @@ __device__ void place(const DecideArgs& a, int l, int c, int f, int old) {
     a.where[l * a.E + f] = c;
 }
 
-__device__ char* slot_ptr(const DecideArgs& a, int l, int c) {
-    return a.arena + (size_t(l) * a.C + c) * a.blob;
-}
+__device__ char* block_ptr(const DecideArgs& a, int b) { return a.arena + size_t(b) * a.blob; }
+
+__device__ char* slot_ptr(const DecideArgs& a, int l, int c) { return block_ptr(a, a.blk[l * a.C + c]); }
 
 __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
     __shared__ unsigned char keep[kMaxE];
@@ -107,50 +128,85 @@ __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
     __shared__ int vic[kMaxE];
     __shared__ int64_t lastl[kMaxE];
     __shared__ int wsum[kT / 64];
-    __shared__ int cnt[2];
+    __shared__ int cnt[3];               // used prefetches, wasted prefetches, staged overflow
     __shared__ int n_adm;
+    __shared__ int spos[kMaxE];          // staging position of a staged expert of this layer, or -1
     const int t = threadIdx.x;
     const int l = a.layer;
+    const bool staged = a.ns > 0;
+    // the staged list consumed here is the last one issued, if it targets this layer
+    const int cur = staged ? a.ctl[0] : 0;
+    const int n_cons = staged && a.demand_on && a.ctl[1 + cur] == l ? a.ctl[3 + cur] : 0;
 
     // ---- missed experts of layer l (the selection U = distinct idx)
     if (a.demand_on) {
-        if (t < a.E) keep[t] = 0;
-        if (t < 2) cnt[t] = 0;
+        if (t < a.E) {
+            keep[t] = 0;
+            spos[t] = -1;
+        }
+        if (t < 3) cnt[t] = 0;
         __syncthreads();
         for (int i = t; i < a.BK; i += kT) {
             const int e = a.idx[i];
             if (e >= 0 && e < a.E) keep[e] = 1;
         }
+        for (int j = t; j < n_cons; j += kT) spos[a.sexp[cur * kStageMax + j]] = j;
         __syncthreads();
         const bool inU = t < a.E && keep[t];
         const int wh = t < a.E ? a.where[l * a.E + t] : -1;
         const bool hit = inU && wh >= 0, miss = inU && wh < 0;
+        const int sj = t < a.E ? spos[t] : -1;           // staged for this layer
         const int nV = rank_victims(a, l, keep, occ, lastl, evl, vic, wsum);
-        int n_hit, n_miss;
+        int n_hit, n_miss, n_dem;
         (void)flag_rank(hit, wsum, n_hit);
         const int mr = flag_rank(miss, wsum, n_miss);      // ascending expert order
-        const int n_placed = n_miss < nV ? n_miss : nV;
+        const bool dem = miss && mr < nV && sj < 0;        // a copy of its own
+        const int dr = flag_rank(dem, wsum, n_dem);
         int c = hit ? wh : -1;
         if (miss && mr < nV) {
             c = vic[mr];
             place(a, l, c, t, occ[c]);
-            a.demand[mr] = Copy{a.host[l * a.E + t], slot_ptr(a, l, c)};
+            if (sj >= 0) {
+                // the staged block becomes the slot's block; the slot's old block is the position's
+                const int old = a.blk[l * a.C + c];
+                a.blk[l * a.C + c] = a.sblk[cur * kStageMax + sj];
+                a.sblk[cur * kStageMax + sj] = old;
+            } else {
+                a.demand[dr] = Copy{a.host[l * a.E + t], slot_ptr(a, l, c), nullptr};
+            }
         }
+        if (miss && mr >= nV && sj >= 0) atomicAdd(&cnt[2], 1);
         if (c >= 0) a.last[l * a.C + c] = a.stamp;
-        // the FFN reads resident experts from their slot, overflow from host memory
-        if (inU) a.table[t] = c >= 0 ? static_cast<const void*>(slot_ptr(a, l, c)) : a.host[l * a.E + t];
-        if (t < a.E && a.pending[l * a.E + t]) {
+        // the FFN reads resident experts from their slot, staged overflow from its
+        // staging block, other overflow from host memory
+        if (inU)
+            a.table[t] = c >= 0    ? static_cast<const void*>(slot_ptr(a, l, c))
+                         : sj >= 0 ? static_cast<const void*>(block_ptr(a, a.sblk[cur * kStageMax + sj]))
+                                   : static_cast<const void*>(a.host[l * a.E + t]);
+        if (!staged && t < a.E && a.pending[l * a.E + t]) {
             atomicAdd(&cnt[keep[t] ? 0 : 1], 1);
             a.pending[l * a.E + t] = 0;
         }
+        // staged experts: selected ones were used; the others are cancelled
+        for (int j = t; j < n_cons; j += kT) {
+            const int e = a.sexp[cur * kStageMax + j];
+            if (keep[e]) {
+                atomicAdd(&cnt[0], 1);
+            } else {
+                atomicAdd(&cnt[1], 1);
+                __hip_atomic_store(a.cancel + cur * kStageMax + j, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
         __syncthreads();
         if (t == 0) {
-            *a.n_demand = n_placed;
+            const int n_placed = n_miss < nV ? n_miss : nV;
+            *a.n_demand = n_dem;
             a.stats[0] += n_hit;
-            a.stats[1] += n_placed;
-            a.stats[2] += n_miss - n_placed;
+            a.stats[1] += n_dem;
             a.stats[4] += cnt[0];
             a.stats[5] += cnt[1];
+            // overflow: misses without a slot that were not staged
+            a.stats[2] += n_miss - n_placed - cnt[2];
         }
     }
     if (!a.ranked) return;
@@ -168,6 +224,28 @@ __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
     }
     if (t < a.E) keep[t] = 0;
     __syncthreads();
+    if (staged) {
+        // the first ns admitted experts not resident in `next`, into the other parity
+        const int nx = cur ^ 1;
+        const bool nonres = t < n_adm && a.where[lp * a.E + f] < 0;
+        int n_nonres;
+        const int j = flag_rank(nonres, wsum, n_nonres);
+        const int n_st = n_nonres < a.ns ? n_nonres : a.ns;
+        if (nonres && j < a.ns) {
+            a.sexp[nx * kStageMax + j] = f;
+            __hip_atomic_store(a.cancel + nx * kStageMax + j, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            a.pf[j] = Copy{a.host[lp * a.E + f], block_ptr(a, a.sblk[nx * kStageMax + j]),
+                           a.cancel + nx * kStageMax + j};
+        }
+        if (t == 0) {
+            *a.n_pf = n_st;
+            a.stats[3] += n_st;
+            a.ctl[1 + nx] = lp;
+            a.ctl[3 + nx] = n_st;
+            a.ctl[0] = nx;
+        }
+        return;
+    }
     const int m = n_adm < a.C ? n_adm : a.C;
     const bool ranked_in = t < m;                       // f is valid here
     if (ranked_in) keep[f] = 1;
@@ -182,7 +260,7 @@ __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
         place(a, lp, cs, f, occ[cs]);
         a.last[lp * a.C + cs] = a.stamp;
         a.pending[lp * a.E + f] = 1;
-        a.pf[j] = Copy{a.host[lp * a.E + f], slot_ptr(a, lp, cs)};
+        a.pf[j] = Copy{a.host[lp * a.E + f], slot_ptr(a, lp, cs), nullptr};
     }
     if (t == 0) {
         *a.n_pf = copies;
@@ -190,7 +268,9 @@ __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
     }
 }
 
-// Copy the listed blobs (16-byte chunks, four in flight per thread).
+// Copy the listed blobs (16-byte chunks, four in flight per thread).  A copy
+// with a cancel flag stops at the first check after the flag is set (every
+// 4 x 16 bytes per thread); the kernel never waits on the flag.
 __global__ __launch_bounds__(256) void blit_kernel(const Copy* list, const int32_t* n, size_t chunks) {
     typedef const __attribute__((address_space(1))) u32x4 gsrc;
     typedef __attribute__((address_space(1))) u32x4 gdst;
@@ -199,14 +279,17 @@ __global__ __launch_bounds__(256) void blit_kernel(const Copy* list, const int32
     for (int i = 0; i < nc; ++i) {
         gsrc* src = (gsrc*)(list[i].src);
         gdst* dst = (gdst*)(list[i].dst);
+        const int32_t* cancel = list[i].cancel;
         size_t k = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
         for (; k + 3 * stride < chunks; k += 4 * stride) {
+            if (cancel && __hip_atomic_load(cancel, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
             u32x4 v[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) v[u] = __builtin_nontemporal_load(src + k + u * stride);
 #pragma unroll
             for (int u = 0; u < 4; ++u) __builtin_nontemporal_store(v[u], dst + k + u * stride);
         }
+        if (cancel && __hip_atomic_load(cancel, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) continue;
         for (; k < chunks; k += stride) __builtin_nontemporal_store(__builtin_nontemporal_load(src + k), dst + k);
     }
 }
@@ -227,8 +310,16 @@ struct DeviceCache {
     const char** host = nullptr;     // [L*E]
     Copy* demand = nullptr;          // [kMaxE]
     int32_t* n_demand = nullptr;
-    Copy* pf = nullptr;              // [L][C]
+    Copy* pf = nullptr;              // [L][kMaxE]
     int32_t* n_pf = nullptr;         // [L]
+    int32_t* blk = nullptr;          // [L*C]
+    int32_t* sblk = nullptr;         // [2][kStageMax]
+    int32_t* sexp = nullptr;         // [2][kStageMax]
+    int32_t* cancel = nullptr;       // [2][kStageMax]
+    int32_t* ctl = nullptr;          // [5]
+    int n_blocks = 0;                // arena blocks: L*C slots + staging
+    int ns = 0;                      // staged positions per parity (0: prefetch into slots)
+    bool permuted = false;           // staged prefetches have swapped slot blocks
     // ordering: decisions made (compute stream), prefetch of layer l done (side)
     hipEvent_t ev_decided = nullptr;
     std::vector<hipEvent_t> pf_done;
@@ -240,19 +331,48 @@ namespace {
 void free_dc(DeviceCache* d) {
     if (!d) return;
     if (d->side) (void)hipStreamSynchronize(d->side);
-    for (void* p : {(void*)d->slot, (void*)d->last, (void*)d->where, (void*)d->pending, (void*)d->stats,
-                    (void*)d->host, (void*)d->demand, (void*)d->n_demand, (void*)d->pf, (void*)d->n_pf})
-        if (p) (void)hipFree(p);
     if (d->ev_decided) (void)hipEventDestroy(d->ev_decided);
     for (auto e : d->pf_done)
         if (e) (void)hipEventDestroy(e);
-    delete d;
+    delete d;       // the state lives in the cache's arena
+}
+
+// Layout of the decision state inside the cache arena (256-byte aligned).
+struct StateLayout {
+    size_t slot, last, where, pending, stats, host, demand, n_demand, pf, n_pf, blk, sblk, sexp, cancel, ctl,
+        total;
+};
+
+StateLayout state_layout(int L, int E, int C) {
+    StateLayout y{};
+    const size_t LC = size_t(L) * C, LE = size_t(L) * E;
+    size_t off = 0;
+    auto take = [&](size_t n) { const size_t at = off; off = (off + n + 255) / 256 * 256; return at; };
+    y.slot = take(LC * 4);
+    y.last = take(LC * 8);
+    y.where = take(LE * 4);
+    y.pending = take(LE * 4);
+    y.stats = take(6 * sizeof(long long));
+    y.host = take(LE * sizeof(char*));
+    y.demand = take(kMaxE * sizeof(Copy));
+    y.n_demand = take(4);
+    y.pf = take(size_t(L) * kMaxE * sizeof(Copy));
+    y.n_pf = take(size_t(L) * 4);
+    y.blk = take(LC * 4);
+    y.sblk = take(2 * kStageMax * 4);
+    y.sexp = take(2 * kStageMax * 4);
+    y.cancel = take(2 * kStageMax * 4);
+    y.ctl = take(5 * 4);
+    y.total = off;
+    return y;
 }
 
 }  // namespace
 
-int device_cache_create(const PolicyState& ps, char* arena, size_t blob, const void* const* host_blobs,
-                        hipStream_t side, DeviceCache** out) {
+size_t device_cache_state_bytes(int L, int E, int C) { return state_layout(L, E, C).total; }
+
+int device_cache_create(const PolicyState& ps, char* arena, size_t blob, int n_stage,
+                        const void* const* host_blobs, char* state, hipStream_t side, DeviceCache** out) {
     STMOE_CHECK(ps.E <= kMaxE && ps.C <= kMaxE && blob % 16 == 0, "bad cache shape for device decisions");
     // every pool blob must be reachable from kernels at its own address:
     // pinned host memory mapped at the same address, or device memory
@@ -272,17 +392,27 @@ int device_cache_create(const PolicyState& ps, char* arena, size_t blob, const v
     auto* d = new DeviceCache();
     d->L = ps.L; d->E = ps.E; d->C = ps.C; d->blob = blob; d->arena = arena; d->side = side;
     const size_t LC = size_t(ps.L) * ps.C, LE = size_t(ps.L) * ps.E;
-    hipError_t e = hipMalloc(&d->slot, LC * 4);
-    if (e == hipSuccess) e = hipMalloc(&d->last, LC * 8);
-    if (e == hipSuccess) e = hipMalloc(&d->where, LE * 4);
-    if (e == hipSuccess) e = hipMalloc(&d->pending, LE * 4);
-    if (e == hipSuccess) e = hipMalloc(&d->stats, 6 * sizeof(long long));
-    if (e == hipSuccess) e = hipMalloc(&d->host, LE * sizeof(char*));
-    if (e == hipSuccess) e = hipMalloc(&d->demand, kMaxE * sizeof(Copy));
-    if (e == hipSuccess) e = hipMalloc(&d->n_demand, 4);
-    if (e == hipSuccess) e = hipMalloc(&d->pf, LC * sizeof(Copy));
-    if (e == hipSuccess) e = hipMalloc(&d->n_pf, size_t(ps.L) * 4);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&d->ev_decided, hipEventDisableTiming);
+    const StateLayout y = state_layout(ps.L, ps.E, ps.C);
+    d->slot = reinterpret_cast<int32_t*>(state + y.slot);
+    d->last = reinterpret_cast<int64_t*>(state + y.last);
+    d->where = reinterpret_cast<int32_t*>(state + y.where);
+    d->pending = reinterpret_cast<int32_t*>(state + y.pending);
+    d->stats = reinterpret_cast<long long*>(state + y.stats);
+    d->host = reinterpret_cast<const char**>(state + y.host);
+    d->demand = reinterpret_cast<Copy*>(state + y.demand);
+    d->n_demand = reinterpret_cast<int32_t*>(state + y.n_demand);
+    d->pf = reinterpret_cast<Copy*>(state + y.pf);
+    d->n_pf = reinterpret_cast<int32_t*>(state + y.n_pf);
+    d->blk = reinterpret_cast<int32_t*>(state + y.blk);
+    d->sblk = reinterpret_cast<int32_t*>(state + y.sblk);
+    d->sexp = reinterpret_cast<int32_t*>(state + y.sexp);
+    d->cancel = reinterpret_cast<int32_t*>(state + y.cancel);
+    d->ctl = reinterpret_cast<int32_t*>(state + y.ctl);
+    d->n_blocks = int(LC) + n_stage;
+    std::vector<int32_t> blk(LC);
+    for (size_t i = 0; i < LC; ++i) blk[i] = int32_t(i);
+    const int32_t ctl[5] = {0, -1, -1, 0, 0};
+    hipError_t e = hipEventCreateWithFlags(&d->ev_decided, hipEventDisableTiming);
     d->pf_done.assign(ps.L, nullptr);
     d->pf_set.assign(ps.L, 0);
     for (int l = 0; e == hipSuccess && l < ps.L; ++l) e = hipEventCreateWithFlags(&d->pf_done[l], hipEventDisableTiming);
@@ -298,6 +428,9 @@ int device_cache_create(const PolicyState& ps, char* arena, size_t blob, const v
     if (e == hipSuccess) e = hipMemcpy(d->host, hp.data(), LE * sizeof(char*), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemset(d->n_demand, 0, 4);
     if (e == hipSuccess) e = hipMemset(d->n_pf, 0, size_t(ps.L) * 4);
+    if (e == hipSuccess) e = hipMemcpy(d->blk, blk.data(), LC * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d->ctl, ctl, sizeof(ctl), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(d->cancel, 0, 2 * kStageMax * 4);
     if (e != hipSuccess) {
         set_error(std::string("expert_cache_set_device_policy: ") + hipGetErrorString(e));
         free_dc(d);
@@ -310,6 +443,11 @@ int device_cache_create(const PolicyState& ps, char* arena, size_t blob, const v
 int device_cache_download(DeviceCache* d, const PolicyState& ps) {
     STMOE_HIP(hipStreamSynchronize(d->side));
     STMOE_HIP(hipDeviceSynchronize());
+    if (d->permuted) {
+        set_error("expert_cache_set_device_policy: staged prefetches have moved slots to other arena blocks; "
+                  "the host policy cannot take the cache over");
+        return STMOE_ESTATE;
+    }
     const size_t LC = size_t(d->L) * d->C, LE = size_t(d->L) * d->E;
     std::vector<int32_t> pend(LE);
     long long st[6];
@@ -324,6 +462,27 @@ int device_cache_download(DeviceCache* d, const PolicyState& ps) {
 }
 
 void device_cache_destroy(DeviceCache* d) { free_dc(d); }
+
+int device_cache_set_staged(DeviceCache* d, int ns) {
+    STMOE_CHECK(ns >= 0 && ns <= kStageMax && d->n_blocks - d->L * d->C >= 2 * ns,
+                "staged prefetch needs 2 * n staging slots in the cache arena");
+    STMOE_HIP(hipStreamSynchronize(d->side));
+    STMOE_HIP(hipDeviceSynchronize());
+    if (ns > 0) {
+        // the staging blocks follow the slot blocks; positions of both parities
+        std::vector<int32_t> sblk(2 * kStageMax, -1);
+        for (int p = 0; p < 2; ++p)
+            for (int j = 0; j < ns; ++j) sblk[size_t(p) * kStageMax + j] = d->L * d->C + p * ns + j;
+        const int32_t ctl[5] = {0, -1, -1, 0, 0};
+        STMOE_HIP(hipMemcpy(d->sblk, sblk.data(), sblk.size() * 4, hipMemcpyHostToDevice));
+        STMOE_HIP(hipMemcpy(d->ctl, ctl, sizeof(ctl), hipMemcpyHostToDevice));
+        d->permuted = true;
+    }
+    d->ns = ns;
+    return STMOE_OK;
+}
+
+int device_cache_staged(const DeviceCache* d) { return d->ns; }
 
 int device_cache_stats(DeviceCache* d, stmoe_cache_stats* out) {
     STMOE_HIP(hipStreamSynchronize(d->side));
@@ -349,7 +508,8 @@ int device_cache_decide(DeviceCache* d, int layer, int next, const int32_t* idx,
     a.idx = idx; a.ranked = ranked; a.n_ranked = n_ranked; a.max_score = max_score;
     a.host = d->host; a.arena = d->arena; a.blob = d->blob; a.table = table;
     a.demand = d->demand; a.n_demand = d->n_demand;
-    a.pf = d->pf + size_t(next) * d->C; a.n_pf = d->n_pf + next;
+    a.pf = d->pf + size_t(next) * kMaxE; a.n_pf = d->n_pf + next;
+    a.blk = d->blk; a.ns = d->ns; a.sblk = d->sblk; a.sexp = d->sexp; a.cancel = d->cancel; a.ctl = d->ctl;
     hipLaunchKernelGGL(decide_kernel, dim3(1), dim3(kT), 0, s, a);
     STMOE_LAUNCHED();
     return STMOE_OK;
@@ -369,7 +529,7 @@ int device_cache_prefetch(DeviceCache* d, int next, hipStream_t s) {
     // when it reads them too)
     STMOE_HIP(hipEventRecord(d->ev_decided, s));
     STMOE_HIP(hipStreamWaitEvent(d->side, d->ev_decided, 0));
-    hipLaunchKernelGGL(blit_kernel, dim3(kBlitWgs), dim3(256), 0, d->side, d->pf + size_t(next) * d->C,
+    hipLaunchKernelGGL(blit_kernel, dim3(kBlitWgs), dim3(256), 0, d->side, d->pf + size_t(next) * kMaxE,
                        d->n_pf + next, d->blob / 16);
     STMOE_LAUNCHED();
     STMOE_HIP(hipEventRecord(d->pf_done[next], d->side));

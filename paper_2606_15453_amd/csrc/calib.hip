@@ -4,7 +4,11 @@
 //                      factor that turns those counters into bytes.
 //   stmoe_calib_read   reads n bytes with the same non-temporal 16-byte loads
 //                      as the expert FFN and writes one word per workgroup:
-//                      the achievable streaming-read bandwidth of the chip.
+//                      the achievable streaming-read bandwidth of the chip,
+//                      for two access patterns: a grid-stride sweep (every
+//                      load instruction of the grid covers consecutive
+//                      bytes), or each workgroup reading one contiguous
+//                      256 KiB region as an expert's rows are read.
 #include "common.h"
 
 namespace stmoe {
@@ -38,6 +42,40 @@ __global__ __launch_bounds__(kThreads) void calib_read_kernel(const char* src, s
     if (threadIdx.x == 0) out[blockIdx.x] = w[0] ^ w[1] ^ w[2] ^ w[3];
 }
 
+// Workgroup w reads the contiguous 16-byte chunks [w*kBlockChunks,
+// (w+1)*kBlockChunks): eight loads per thread in flight, each instruction
+// covering 4 KiB of consecutive bytes.
+constexpr size_t kBlockChunks = (size_t(256) << 10) / 16;
+
+__global__ __launch_bounds__(kThreads) void calib_read_blocked_kernel(const char* src, size_t n, unsigned* out) {
+    const u32x4* base = reinterpret_cast<const u32x4*>(src);
+    const size_t lo = size_t(blockIdx.x) * kBlockChunks;
+    const size_t hi = lo + kBlockChunks < n ? lo + kBlockChunks : n;
+    unsigned acc = 0;
+    size_t i = lo + threadIdx.x;
+    for (; i + 7 * kThreads < hi; i += 8 * kThreads) {
+        u32x4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(base + i + u * kThreads);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
+    for (; i < hi; i += kThreads) {
+        const u32x4 a = __builtin_nontemporal_load(base + i);
+        acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    }
+    for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o, 64);
+    __shared__ unsigned w[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) w[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) out[blockIdx.x] = w[0] ^ w[1] ^ w[2] ^ w[3];
+}
+
+unsigned blocked_grid_for(size_t n16) {
+    const size_t g = (n16 + kBlockChunks - 1) / kBlockChunks;
+    return unsigned(g < 1 ? 1 : g);
+}
+
 unsigned grid_for(size_t n16) {
     size_t g = (n16 + kThreads - 1) / kThreads;
     if (g > 8192) g = 8192;
@@ -61,15 +99,22 @@ extern "C" int stmoe_calib_copy(const void* src, void* dst, size_t bytes, void* 
     return STMOE_OK;
 }
 
-extern "C" size_t stmoe_calib_read_out_words(size_t bytes) { return grid_for(bytes / 16); }
+extern "C" size_t stmoe_calib_read_out_words(size_t bytes, int pattern) {
+    return pattern == 1 ? blocked_grid_for(bytes / 16) : grid_for(bytes / 16);
+}
 
-extern "C" int stmoe_calib_read(const void* src, size_t bytes, unsigned* out, void* stream) {
+extern "C" int stmoe_calib_read(const void* src, size_t bytes, int pattern, unsigned* out, void* stream) {
     clear_error();
     STMOE_CHECK(src && out && bytes > 0 && bytes % 16 == 0, "null pointer or size not a multiple of 16");
     STMOE_CHECK((reinterpret_cast<uintptr_t>(src) & 15) == 0, "src must be 16-byte aligned");
+    STMOE_CHECK(pattern == 0 || pattern == 1, "pattern must be 0 (grid stride) or 1 (contiguous per workgroup)");
     const size_t n = bytes / 16;
-    hipLaunchKernelGGL(calib_read_kernel, dim3(grid_for(n)), dim3(kThreads), 0, as_stream(stream),
-                       reinterpret_cast<const char*>(src), n, out);
+    if (pattern == 1)
+        hipLaunchKernelGGL(calib_read_blocked_kernel, dim3(blocked_grid_for(n)), dim3(kThreads), 0,
+                           as_stream(stream), reinterpret_cast<const char*>(src), n, out);
+    else
+        hipLaunchKernelGGL(calib_read_kernel, dim3(grid_for(n)), dim3(kThreads), 0, as_stream(stream),
+                           reinterpret_cast<const char*>(src), n, out);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }

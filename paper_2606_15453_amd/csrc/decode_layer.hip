@@ -25,8 +25,8 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
                const float* logits, int renorm, const void* ebase, size_t estride);
 int route_logits(const void* x, const void* w_gate, int B, int H, int E, int dtype, float* z, hipStream_t s);
 size_t update_predict_seq_bytes(int L);
-int update_predict_seq_args(stmoe_predictor* p, const int32_t* idx_all, int use, int online, void* dev_args);
-int update_predict_seq(stmoe_predictor* p, const void* dev_args, hipStream_t s);
+int update_predict_seq_args(stmoe_predictor* p, const int32_t* idx_all, void* dev_args);
+int update_predict_seq(stmoe_predictor* p, const void* dev_args, int use, int online, hipStream_t s);
 void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_bytes);
 DeviceCache* expert_cache_device(expert_cache* c);
 int expert_cache_after_demand(const expert_cache* c);
@@ -83,7 +83,6 @@ struct moe_ctx {
     hipEvent_t ev_tok[2] = {nullptr, nullptr};
     bool tok_pending[2] = {false, false};
     void* seq_args[2] = {nullptr, nullptr};   // device arguments of update_predict_seq per parity
-    int seq_key[2] = {-1, -1};                // (use, online) they were built for
     int32_t* idx = nullptr;                // [2][L][B][K] device (parity 0 unless pred_batch)
     float* w = nullptr;                    // [2][L][B][K] device
     int32_t* ranked = nullptr;             // device: ranked [E], n_ranked [1], max scores [E] (uint8)
@@ -95,6 +94,7 @@ struct moe_ctx {
     const void** shared = nullptr;         // [L][n_shared] device blob pointers
     int32_t* rec = nullptr;                // pinned host: idx [B][K], ranked [E], n_ranked, max scores [E] (uint8)
     int pf_min_score = 2, pf_max = 1 << 30;
+    bool want_ranked = false;              // a report asks for the side path's ranked prediction
     int online = 1;                        // Algorithm 3's CCT update on (1) or frozen CCTs (0)
     hipEvent_t rec_ev = nullptr;
     std::vector<const void*> host_table;   // [E] scratch for the cache's answers
@@ -141,10 +141,8 @@ void free_ctx(moe_ctx* c) {
     }
     if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
     if (c->ev_side) (void)hipEventDestroy(c->ev_side);
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i)
         if (c->ev_tok[i]) (void)hipEventDestroy(c->ev_tok[i]);
-        (void)hipFree(c->seq_args[i]);
-    }
     if (c->gs) {
         (void)hipStreamSynchronize(c->gs);
         (void)hipStreamDestroy(c->gs);
@@ -153,20 +151,53 @@ void free_ctx(moe_ctx* c) {
     if (c->graph) (void)hipGraphDestroy(c->graph);
     if (c->ev_in) (void)hipEventDestroy(c->ev_in);
     if (c->ev_out) (void)hipEventDestroy(c->ev_out);
-    (void)hipFree(c->x_stage);
-    (void)hipFree(c->y_stage);
-    (void)hipFree(c->idx);
-    (void)hipFree(c->w);
-    (void)hipFree(c->ranked);
-    (void)hipFree(c->route_ws);
-    (void)hipFree(c->ffn_ws);
-    (void)hipFree(c->tables);
-    (void)hipFree(c->shared);
-    (void)hipFree(c->n_experts);
     if (c->rec) (void)hipHostFree(c->rec);
     if (c->rec_ev) (void)hipEventDestroy(c->rec_ev);
     for (auto e : c->ev_pool) (void)hipEventDestroy(e);
-    delete c;
+    delete c;       // device buffers live in the caller's workspace
+}
+
+// Layout of a context's device workspace (every region 256-byte aligned).
+struct CtxLayout {
+    size_t idx, w, ranked, route_ws, ffn_ws, tables, shared, n_experts, seq_args, x_stage, y_stage, total;
+    size_t route_ws_bytes, ffn_ws_bytes, seq_bytes;
+};
+
+CtxLayout ctx_layout(const moe_model_desc* d) {
+    CtxLayout y{};
+    const size_t LBK = size_t(d->L) * d->B * d->K, LBH = size_t(d->L) * d->B * d->H;
+    const size_t esz = d->dtype == STMOE_BF16 ? 2 : 4;
+    y.route_ws_bytes = moe_route_workspace_bytes(d->B, d->E);
+    y.ffn_ws_bytes = moe_expert_ffn_workspace_bytes(d->B, d->K, d->E, d->H, d->I, d->n_shared, d->dtype);
+    y.seq_bytes = update_predict_seq_bytes(d->L);
+    size_t off = 0;
+    auto take = [&](size_t n) { const size_t at = off; off = (off + n + 255) / 256 * 256; return at; };
+    y.idx = take(2 * LBK * sizeof(int32_t));
+    y.w = take(2 * LBK * sizeof(float));
+    y.ranked = take(ranked_bytes(d->E));
+    y.route_ws = take(y.route_ws_bytes);
+    y.ffn_ws = take(y.ffn_ws_bytes);
+    y.tables = take(size_t(d->L) * d->E * sizeof(void*));
+    y.shared = take(size_t(d->L) * d->n_shared * sizeof(void*));
+    y.n_experts = take(sizeof(unsigned long long));
+    y.seq_args = take(2 * y.seq_bytes);
+    y.x_stage = take(LBH * esz);
+    y.y_stage = take(LBH * sizeof(float));
+    y.total = off;
+    return y;
+}
+
+int check_desc(const moe_model_desc* d) {
+    STMOE_CHECK(d && d->router_w, "null pointer");
+    STMOE_CHECK(d->L >= 1 && d->E >= 1 && d->E <= kMaxE, "bad L/E");
+    STMOE_CHECK(d->K >= 1 && d->K <= d->E && d->K <= kMaxK, "bad K");
+    STMOE_CHECK(d->B >= 1 && d->B <= kMaxB, "bad B");
+    STMOE_CHECK(d->H >= 8 && d->H % 8 == 0 && d->H <= kMaxH, "bad H");
+    STMOE_CHECK(d->I >= 8 && d->I % 8 == 0, "bad I");
+    STMOE_CHECK(d->n_shared >= 0 && d->n_shared <= 8, "bad n_shared");
+    STMOE_CHECK(d->n_shared == 0 || d->shared_w, "shared_w is required when n_shared > 0");
+    STMOE_CHECK(d->dtype == STMOE_BF16 || d->dtype == STMOE_F32, "bad dtype");
+    return STMOE_OK;
 }
 
 int use_bits(int mode) {
@@ -225,21 +256,22 @@ hipEvent_t next_event(moe_ctx* c) {
 
 }  // namespace
 
+extern "C" size_t moe_ctx_workspace_bytes(const moe_model_desc* d) {
+    if (!d || check_desc(d) != STMOE_OK) return 0;
+    return ctx_layout(d).total;
+}
+
 extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, expert_cache* cache,
-                              void* compute_stream, moe_ctx** out) {
+                              void* compute_stream, void* dev_ws, size_t ws_bytes, moe_ctx** out) {
     clear_error();
-    STMOE_CHECK(d && out && d->router_w, "null pointer");
-    STMOE_CHECK(d->L >= 1 && d->E >= 1 && d->E <= kMaxE, "bad L/E");
-    STMOE_CHECK(d->K >= 1 && d->K <= d->E && d->K <= kMaxK, "bad K");
-    STMOE_CHECK(d->B >= 1 && d->B <= kMaxB, "bad B");
-    STMOE_CHECK(d->H >= 8 && d->H % 8 == 0 && d->H <= kMaxH, "bad H");
-    STMOE_CHECK(d->I >= 8 && d->I % 8 == 0, "bad I");
-    STMOE_CHECK(d->n_shared >= 0 && d->n_shared <= 8, "bad n_shared");
-    STMOE_CHECK(d->n_shared == 0 || d->shared_w, "shared_w is required when n_shared > 0");
-    STMOE_CHECK(d->dtype == STMOE_BF16 || d->dtype == STMOE_F32, "bad dtype");
+    STMOE_CHECK(out && dev_ws, "null pointer");
+    if (int rc = check_desc(d)) return rc;
     STMOE_CHECK((cache == nullptr) != (d->resident_w == nullptr),
                 "give exactly one of a cache or resident expert pointers");
     for (int l = 0; l < d->L; ++l) STMOE_CHECK(d->router_w[l], "null router pointer");
+    const CtxLayout y = ctx_layout(d);
+    STMOE_CHECK(ws_bytes >= y.total, "workspace smaller than moe_ctx_workspace_bytes()");
+    STMOE_CHECK(reinterpret_cast<uintptr_t>(dev_ws) % 256 == 0, "workspace must be 256-byte aligned");
     if (pred) {
         int pL, pE, pK, pB;
         stmoe_shape(pred, &pL, &pE, &pK, &pB);
@@ -273,20 +305,22 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
             for (int l = 0; l < d->L; ++l) c->rbase.push_back(reinterpret_cast<const char*>(at(l, 0)));
         }
     }
-    const size_t LBK = size_t(c->L) * c->B * c->K;
-    c->route_ws_bytes = moe_route_workspace_bytes(c->B, c->E);
-    c->ffn_ws_bytes = moe_expert_ffn_workspace_bytes(c->B, c->K, c->E, c->H, c->I, c->n_shared, c->dtype);
-    hipError_t e = hipSuccess;
-    if (e == hipSuccess) e = hipMalloc(&c->idx, 2 * LBK * sizeof(int32_t));
-    if (e == hipSuccess) e = hipMalloc(&c->w, 2 * LBK * sizeof(float));
-    if (e == hipSuccess) e = hipMalloc(&c->ranked, ranked_bytes(c->E));
-    if (e == hipSuccess) e = hipMalloc(&c->route_ws, c->route_ws_bytes);
-    if (e == hipSuccess) e = hipMalloc(&c->ffn_ws, c->ffn_ws_bytes);
-    if (e == hipSuccess) e = hipMalloc(&c->tables, size_t(c->L) * c->E * sizeof(void*));
-    if (e == hipSuccess && c->n_shared)
-        e = hipMalloc(&c->shared, size_t(c->L) * c->n_shared * sizeof(void*));
-    if (e == hipSuccess) e = hipMalloc(&c->n_experts, sizeof(unsigned long long));
-    if (e == hipSuccess) e = hipHostMalloc(&c->rec, size_t(c->B * c->K) * sizeof(int32_t) + ranked_bytes(c->E));
+    char* base = static_cast<char*>(dev_ws);
+    c->idx = reinterpret_cast<int32_t*>(base + y.idx);
+    c->w = reinterpret_cast<float*>(base + y.w);
+    c->ranked = reinterpret_cast<int32_t*>(base + y.ranked);
+    c->route_ws = base + y.route_ws;
+    c->route_ws_bytes = y.route_ws_bytes;
+    c->ffn_ws = base + y.ffn_ws;
+    c->ffn_ws_bytes = y.ffn_ws_bytes;
+    c->tables = reinterpret_cast<const void**>(base + y.tables);
+    c->shared = c->n_shared ? reinterpret_cast<const void**>(base + y.shared) : nullptr;
+    c->n_experts = reinterpret_cast<unsigned long long*>(base + y.n_experts);
+    c->seq_args[0] = base + y.seq_args;
+    c->seq_args[1] = base + y.seq_args + y.seq_bytes;
+    c->x_stage = base + y.x_stage;
+    c->y_stage = reinterpret_cast<float*>(base + y.y_stage);
+    hipError_t e = hipHostMalloc(&c->rec, size_t(c->B * c->K) * sizeof(int32_t) + ranked_bytes(c->E));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->rec_ev, hipEventDisableTiming);
     if (e == hipSuccess && !cache && pred) {
         // the side stream's events only order kernels of this device (the
@@ -298,12 +332,7 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
         if (e == hipSuccess)
             e = hipEventCreateWithFlags(&c->ev_side, hipEventDisableTiming | hipEventDisableSystemFence);
     }
-    if (e == hipSuccess) e = hipMemset(c->route_ws, 0, c->route_ws_bytes);
-    if (e == hipSuccess) e = hipMemset(c->ffn_ws, 0, c->ffn_ws_bytes);
-    if (e == hipSuccess) e = hipMemset(c->idx, 0, 2 * LBK * sizeof(int32_t));
-    if (e == hipSuccess) e = hipMemset(c->w, 0, 2 * LBK * sizeof(float));
-    if (e == hipSuccess) e = hipMemset(c->tables, 0, size_t(c->L) * c->E * sizeof(void*));
-    if (e == hipSuccess) e = hipMemset(c->n_experts, 0, sizeof(unsigned long long));
+    if (e == hipSuccess) e = hipMemset(dev_ws, 0, y.total);
     if (e == hipSuccess && d->resident_w)
         e = hipMemcpy(c->tables, d->resident_w, size_t(c->L) * c->E * sizeof(void*), hipMemcpyHostToDevice);
     if (e == hipSuccess && c->n_shared)
@@ -314,6 +343,16 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
         set_error(std::string("moe_ctx_create: ") + hipGetErrorString(e));
         free_ctx(c);
         return e == hipErrorOutOfMemory ? STMOE_ENOMEM : STMOE_EHIP;
+    }
+    // the per-token predictor launch reads each parity's selections through
+    // arguments built once here
+    if (pred) {
+        const size_t LBK = size_t(c->L) * c->B * c->K;
+        for (int par = 0; par < 2; ++par)
+            if (int rc = update_predict_seq_args(pred, c->idx + par * LBK, c->seq_args[par])) {
+                free_ctx(c);
+                return rc;
+            }
     }
     *out = c;
     return STMOE_OK;
@@ -327,6 +366,16 @@ extern "C" int moe_ctx_destroy(moe_ctx* c) {
 namespace {
 
 bool timed_token(const moe_ctx* c, int token) { return c->timing_every > 0 && token % c->timing_every == 0; }
+
+// Verify/update and the next layer's prediction on the side stream; the
+// ranked prediction is kept only when a layer report asks for it.
+int side_update_predict(moe_ctx* c, int layer, const int32_t* prev, const int32_t* idx_l, int use) {
+    const int E = c->E;
+    if (c->want_ranked)
+        return update_predict(c->pred, layer, prev, idx_l, use, c->online, c->ranked, c->ranked + E,
+                              max_scores(c->ranked, E), c->side);
+    return update_predict(c->pred, layer, prev, idx_l, use, c->online, nullptr, nullptr, nullptr, c->side);
+}
 
 // One layer; `timing` permits the FFN events of timed tokens (off while a
 // graph is captured).  Arguments are checked by the callers.
@@ -402,9 +451,7 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
             const int32_t* prev = layer > 0 ? c->idx + pbase + size_t(layer - 1) * B * K : nullptr;
             if (timed)
                 if (int rc = stamp_event(tl.pred0, c->side)) return rc;
-            if (int rc = update_predict(c->pred, layer, prev, idx_l, use, c->online, nullptr, nullptr, nullptr,
-                                        c->side))
-                return rc;
+            if (int rc = side_update_predict(c, layer, prev, idx_l, use)) return rc;
             if (timed)
                 if (int rc = stamp_event(tl.pred1, c->side)) return rc;
             c->side_pending = true;
@@ -486,8 +533,7 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         const int32_t* prev = layer > 0 ? c->idx + pbase + size_t(layer - 1) * B * K : nullptr;
         if (timed)
             if (int rc = stamp_event(tl.pred0, c->side)) return rc;
-        if (int rc = update_predict(c->pred, layer, prev, idx_l, use, c->online, nullptr, nullptr, nullptr, c->side))
-            return rc;
+        if (int rc = side_update_predict(c, layer, prev, idx_l, use)) return rc;
         if (timed)
             if (int rc = stamp_event(tl.pred1, c->side)) return rc;
         c->side_pending = true;
@@ -532,15 +578,6 @@ int wait_token_side(moe_ctx* c, int par) {
 // order, on the selections of parity c->cur_par.
 int token_side(moe_ctx* c, int token, int use) {
     const int par = c->cur_par;
-    const int key = use * 2 + c->online;
-    if (c->seq_key[par] != key) {
-        if (!c->seq_args[par]) STMOE_HIP(hipMalloc(&c->seq_args[par], update_predict_seq_bytes(c->L)));
-        STMOE_HIP(hipStreamSynchronize(c->side));     // no launch still reads the old arguments
-        if (int rc = update_predict_seq_args(c->pred, c->idx + size_t(par) * c->L * c->B * c->K, use, c->online,
-                                             c->seq_args[par]))
-            return rc;
-        c->seq_key[par] = key;
-    }
     STMOE_HIP(hipEventRecord(c->ev_sel, c->s));
     STMOE_HIP(hipStreamWaitEvent(c->side, c->ev_sel, 0));
     const bool timed = c->timing_every > 0 && token % c->timing_every == 0 && !c->timed_layers.empty();
@@ -557,7 +594,7 @@ int token_side(moe_ctx* c, int token, int use) {
     };
     if (timed)
         if (int rc = stamp(p0)) return rc;
-    if (int rc = update_predict_seq(c->pred, c->seq_args[par], c->side)) return rc;
+    if (int rc = update_predict_seq(c->pred, c->seq_args[par], use, c->online, c->side)) return rc;
     if (timed) {
         if (int rc = stamp(p1)) return rc;
         // the token's predictor time, reported with its last layer
@@ -629,7 +666,38 @@ int decode_token_graph(moe_ctx* c, int token, const void* xs, float* ys, int mod
 
 }  // namespace
 
-extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int mode) {
+namespace {
+// The report of the layer just issued: waits for its work on every stream.
+int fill_report(moe_ctx* c, int layer, int mode, moe_layer_report* rep) {
+    STMOE_HIP(hipStreamSynchronize(c->s));
+    if (c->side) STMOE_HIP(hipStreamSynchronize(c->side));
+    const size_t bk = size_t(c->B) * c->K;
+    *rep = moe_layer_report{};
+    rep->B = c->B;
+    rep->K = c->K;
+    STMOE_HIP(hipMemcpy(rep->idx, c->idx + size_t(layer) * bk, bk * sizeof(int32_t), hipMemcpyDeviceToHost));
+    STMOE_HIP(hipMemcpy(rep->w, c->w + size_t(layer) * bk, bk * sizeof(float), hipMemcpyDeviceToHost));
+    for (int e = 0; e < kMaxE; ++e) rep->ranked[e] = -1;
+    rep->n_ranked = -1;
+    if (use_bits(mode) && c->pred) {
+        std::vector<int32_t> r(size_t(c->E) + 1);
+        STMOE_HIP(hipMemcpy(r.data(), c->ranked, r.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+        rep->n_ranked = r[size_t(c->E)];
+        for (int e = 0; e < c->E; ++e) rep->ranked[e] = r[size_t(e)];
+    }
+    if (c->pred) {
+        std::vector<int64_t> st(size_t(c->L) * 3);
+        if (int rc = stmoe_stats(c->pred, st.data())) return rc;
+        for (int i = 0; i < 3; ++i) rep->pred_stats[i] = st[size_t(layer) * 3 + i];
+    }
+    if (c->cache)
+        if (int rc = expert_cache_stats(c->cache, &rep->cache)) return rc;
+    return STMOE_OK;
+}
+}  // namespace
+
+extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int mode,
+                                moe_layer_report* rep) {
     clear_error();
     STMOE_CHECK(c && x && y, "null pointer");
     STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
@@ -638,7 +706,11 @@ extern "C" int moe_decode_layer(moe_ctx* c, int token, int layer, const void* x,
     // single layers use the parity-0 selection buffer and per-layer predictor work
     c->cur_par = 0;
     if (int rc = wait_token_side(c, 0)) return rc;
-    return decode_layer(c, token, layer, x, y, mode, true);
+    c->want_ranked = rep != nullptr;
+    const int rc = decode_layer(c, token, layer, x, y, mode, true);
+    c->want_ranked = false;
+    if (rc != STMOE_OK || !rep) return rc;
+    return fill_report(c, layer, mode, rep);
 }
 
 extern "C" int moe_ctx_set_predictor_batch(moe_ctx* c, int on) {
@@ -673,15 +745,13 @@ extern "C" int moe_ctx_set_graph(moe_ctx* c, int on) {
     c->graph = nullptr;
     c->graph_mode = -1;
     if (on && !c->gs) {
-        const size_t n = size_t(c->L) * c->B * c->H;
+        // the staging buffers are part of the context's workspace
         hipError_t e = hipStreamCreateWithFlags(&c->gs, hipStreamNonBlocking);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_in, hipEventDisableTiming);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_out, hipEventDisableTiming);
-        if (e == hipSuccess) e = hipMalloc(&c->x_stage, n * c->esz);
-        if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&c->y_stage), n * sizeof(float));
         if (e != hipSuccess) {
             set_error(std::string("moe_ctx_set_graph: ") + hipGetErrorString(e));
-            return e == hipErrorOutOfMemory ? STMOE_ENOMEM : STMOE_EHIP;
+            return STMOE_EHIP;
         }
     }
     c->graph_on = on != 0;

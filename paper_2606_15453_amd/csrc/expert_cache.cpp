@@ -151,6 +151,29 @@ extern "C" int stmoe_policy_create(int L, int E, int C, const int32_t* warm, stm
     return STMOE_OK;
 }
 
+extern "C" int expert_cache_warm_sets(const int32_t* sel, int P, int B, int L, int K, int E, int C,
+                                     int32_t* out) {
+    clear_error();
+    STMOE_CHECK(sel && out, "null pointer");
+    STMOE_CHECK(P >= 1 && B >= 1 && L >= 1 && K >= 1 && E >= 1 && E <= kMaxE && C >= 1, "bad shape");
+    std::vector<int64_t> cnt(E);
+    std::vector<int> order(E);
+    for (int l = 0; l < L; ++l) {
+        std::fill(cnt.begin(), cnt.end(), 0);
+        for (int p = 0; p < P; ++p)
+            for (int b = 0; b < B; ++b)
+                for (int k = 0; k < K; ++k) {
+                    const int e = sel[((size_t(p) * B + b) * L + l) * K + k];
+                    STMOE_CHECK(e >= 0 && e < E, "selection index out of range");
+                    ++cnt[e];
+                }
+        for (int e = 0; e < E; ++e) order[e] = e;
+        std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return cnt[x] > cnt[y]; });
+        for (int c = 0; c < C; ++c) out[size_t(l) * C + c] = c < E ? order[c] : -1;
+    }
+    return STMOE_OK;
+}
+
 extern "C" int stmoe_policy_destroy(stmoe_policy* p) {
     delete p;
     return STMOE_OK;
@@ -220,7 +243,10 @@ void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_byte
 }
 // Internal: the device decisions when switched on, and the prefetch order.
 DeviceCache* expert_cache_device(expert_cache* c) { return c->dev; }
-int expert_cache_after_demand(const expert_cache* c) { return c->after_demand; }
+int expert_cache_after_demand(const expert_cache* c) {
+    // staged prefetches only take the link once the missed loads are in
+    return c->after_demand || (c->dev && device_cache_staged(c->dev) > 0);
+}
 
 namespace {
 PolicyState policy_state(expert_cache* c) {
@@ -249,9 +275,15 @@ int copy_into(expert_cache* c, int gid, const void* src, hipStream_t s) {
 }  // namespace
 }  // namespace stmoe
 
-extern "C" size_t expert_cache_arena_bytes(int L, int C, size_t blob_bytes, int n_stage) {
-    if (L < 1 || C < 1 || n_stage < 0) return 0;
-    return (size_t(L) * C + n_stage) * blob_bytes;
+namespace {
+size_t slots_bytes(int L, int C, size_t blob_bytes, int n_stage) {
+    return ((size_t(L) * C + n_stage) * blob_bytes + 255) / 256 * 256;
+}
+}  // namespace
+
+extern "C" size_t expert_cache_arena_bytes(int L, int E, int C, size_t blob_bytes, int n_stage) {
+    if (L < 1 || E < 1 || E > kMaxE || C < 1 || C > E || n_stage < 0) return 0;
+    return slots_bytes(L, C, blob_bytes, n_stage) + stmoe::device_cache_state_bytes(L, E, C);
 }
 
 extern "C" int expert_cache_create(int L, int E, int C, size_t blob_bytes, int n_stage, void* arena,
@@ -263,8 +295,8 @@ extern "C" int expert_cache_create(int L, int E, int C, size_t blob_bytes, int n
     STMOE_CHECK(n_stage >= 0 && n_stage <= kMaxE, "n_stage must be in [0, 256]");
     STMOE_CHECK(blob_bytes > 0 && blob_bytes % 16 == 0, "blob_bytes must be a positive multiple of 16");
     STMOE_CHECK((reinterpret_cast<uintptr_t>(arena) & 255) == 0, "arena must be 256-byte aligned");
-    if (arena_bytes < expert_cache_arena_bytes(L, C, blob_bytes, n_stage)) {
-        set_error("expert_cache_create: arena smaller than (L*C + n_stage) * blob_bytes");
+    if (arena_bytes < expert_cache_arena_bytes(L, E, C, blob_bytes, n_stage)) {
+        set_error("expert_cache_create: arena smaller than expert_cache_arena_bytes()");
         return STMOE_ECAPACITY;
     }
     for (size_t i = 0; i < size_t(L) * E; ++i) STMOE_CHECK(host_blobs[i], "null host blob pointer");
@@ -441,16 +473,30 @@ extern "C" int expert_cache_set_device_policy(expert_cache* c, int on) {
     STMOE_HIP(hipStreamSynchronize(c->side));
     if (on) {
         for (auto& h : c->held) h.clear();
-        return stmoe::device_cache_create(stmoe::policy_state(c), c->arena, c->blob, c->host.data(), c->side,
+        return stmoe::device_cache_create(stmoe::policy_state(c), c->arena, c->blob, c->n_stage, c->host.data(),
+                                          c->arena + slots_bytes(c->L, c->C, c->blob, c->n_stage), c->side,
                                           &c->dev);
     }
     const int rc = stmoe::device_cache_download(c->dev, stmoe::policy_state(c));
+    if (rc != STMOE_OK) return rc;       // the device keeps deciding
     stmoe::device_cache_destroy(c->dev);
     c->dev = nullptr;
     // every slot was last written and read on the device streams, now idle
     std::fill(c->loaded_set.begin(), c->loaded_set.end(), 0);
     std::fill(c->released_set.begin(), c->released_set.end(), 0);
     return rc;
+}
+
+extern "C" int expert_cache_set_staged_prefetch(expert_cache* c, int n_per_layer) {
+    clear_error();
+    STMOE_CHECK(c, "null cache");
+    if (!c->dev) {
+        set_error("expert_cache_set_staged_prefetch: needs device-side decisions");
+        return STMOE_ESTATE;
+    }
+    STMOE_CHECK(n_per_layer >= 0 && 2 * n_per_layer <= c->n_stage,
+                "n_per_layer must be in [0, n_stage / 2]");
+    return stmoe::device_cache_set_staged(c->dev, n_per_layer);
 }
 
 extern "C" int expert_cache_set_prefetch_order(expert_cache* c, int after_demand) {

@@ -7,6 +7,7 @@
 // x K slots (at most 256 lanes, one lane per slot), and the prediction sums
 // K x K contributions into per-row score bins in LDS with integer atomics,
 // which is exact and order-free.
+#include <algorithm>
 #include <vector>
 
 #include "gating_dev.h"
@@ -137,11 +138,20 @@ struct UpdPred {
 // update_predict_kernel on the arguments built for it; the barrier between
 // layers orders the tables one layer writes before the next layer stages
 // them.
-__global__ __launch_bounds__(kThreads) void update_predict_seq_kernel(const UpdPred* args, int n) {
+// The arguments are built for both prediction sources with the online
+// update on; `use` and `online` select the ablation at launch time.
+__global__ __launch_bounds__(kThreads) void update_predict_seq_kernel(const UpdPred* args, int n, int use,
+                                                                      int online) {
     __shared__ TableShared sh;
     for (int l = 0; l < n; ++l) {
-        const UpdateArgs u = args[l].u;
+        UpdateArgs u = args[l].u;
         PredictArgs p = args[l].p;
+        u.online = online;
+        if (!(use & STMOE_USE_CCT)) {
+            p.cidx = nullptr;
+            p.cconf = nullptr;
+        }
+        if (!(use & STMOE_USE_HT)) p.ht_next = nullptr;
         Seg g[kMaxSegs];
         p.sel_cur = nullptr;     // the update's copy of the selection serves both
         int k = 0;
@@ -173,52 +183,85 @@ int check_sel_host(const int32_t* sel, size_t rows, int E, int K) {
 
 using namespace stmoe;
 
-extern "C" int stmoe_create(int L, int E, int K, int B, stmoe_predictor** out) {
-    clear_error();
-    STMOE_CHECK(out, "null output");
+namespace {
+
+// Layout of a predictor's device workspace: every table at a 256-byte
+// aligned offset, then the staging area of the profiling selections (at
+// least one token's [B][L][K], at least 1 MiB).
+struct PredLayout {
+    size_t co, cct_idx, cct_conf, ht, pend, stats, stage, stage_bytes, total;
+};
+
+size_t align256(size_t n) { return (n + 255) / 256 * 256; }
+
+PredLayout pred_layout(int L, int E, int K, int B) {
+    PredLayout y{};
+    const size_t pairs = size_t(L > 1 ? L - 1 : 1);
+    size_t off = 0;
+    auto take = [&](size_t n) { const size_t at = off; off = align256(off + n); return at; };
+    y.co = take(pairs * E * E * sizeof(int32_t));
+    y.cct_idx = take(pairs * round4(size_t(E) * K));
+    y.cct_conf = take(pairs * round4(size_t(E) * K));
+    y.ht = take(size_t(L) * round4(size_t(B) * K));
+    y.pend = take(size_t(L) * round4(size_t(B) * E));
+    y.stats = take(size_t(L) * 3 * sizeof(unsigned long long));
+    const size_t token = size_t(B) * L * K * sizeof(int32_t);
+    y.stage_bytes = std::max(token, size_t(1) << 20) / token * token;
+    y.stage = take(y.stage_bytes);
+    y.total = off;
+    return y;
+}
+
+int check_shape(int L, int E, int K, int B) {
     STMOE_CHECK(L >= 1 && L <= 4096, "L must be in [1, 4096]");
     STMOE_CHECK(E >= 1 && E <= kMaxE, "E must be in [1, 256]");
     STMOE_CHECK(K >= 1 && K <= E && K <= kMaxK, "K must be in [1, min(E, 16)]");
     STMOE_CHECK(B >= 1 && B <= kMaxB, "B must be in [1, 16]");
+    return STMOE_OK;
+}
+
+}  // namespace
+
+extern "C" size_t stmoe_workspace_bytes(int L, int E, int K, int B) {
+    if (check_shape(L, E, K, B) != STMOE_OK) return 0;
+    return pred_layout(L, E, K, B).total;
+}
+
+extern "C" int stmoe_create(int L, int E, int K, int B, void* dev_ws, size_t ws_bytes, stmoe_predictor** out) {
+    clear_error();
+    STMOE_CHECK(out && dev_ws, "null pointer");
+    if (int rc = check_shape(L, E, K, B)) return rc;
+    const PredLayout y = pred_layout(L, E, K, B);
+    STMOE_CHECK(ws_bytes >= y.total, "workspace smaller than stmoe_workspace_bytes()");
+    STMOE_CHECK(reinterpret_cast<uintptr_t>(dev_ws) % 256 == 0, "workspace must be 256-byte aligned");
+    char* base = static_cast<char*>(dev_ws);
     auto* p = new stmoe_predictor();
     p->L = L; p->E = E; p->K = K; p->B = B;
     p->profiled = false;
     p->cct_stride = round4(size_t(E) * K);
     p->ht_stride = round4(size_t(B) * K);
     p->pend_stride = round4(size_t(B) * E);
-    const size_t pairs = size_t(L > 1 ? L - 1 : 1);
-    hipError_t e = hipSuccess;
-    if (e == hipSuccess) e = hipMalloc(&p->co, pairs * E * E * sizeof(int32_t));
-    if (e == hipSuccess) e = hipMalloc(&p->cct_idx, pairs * p->cct_stride);
-    if (e == hipSuccess) e = hipMalloc(&p->cct_conf, pairs * p->cct_stride);
-    if (e == hipSuccess) e = hipMalloc(&p->ht, size_t(L) * p->ht_stride);
-    if (e == hipSuccess) e = hipMalloc(&p->pend, size_t(L) * p->pend_stride);
-    if (e == hipSuccess) e = hipMalloc(&p->stats, size_t(L) * 3 * sizeof(unsigned long long));
-    if (e == hipSuccess) e = hipMemset(p->co, 0, pairs * E * E * sizeof(int32_t));
-    if (e == hipSuccess) e = hipMemset(p->cct_idx, 0, pairs * p->cct_stride);
-    if (e == hipSuccess) e = hipMemset(p->cct_conf, 0, pairs * p->cct_stride);
-    if (e == hipSuccess) e = hipMemset(p->ht, 0, size_t(L) * p->ht_stride);
-    if (e == hipSuccess) e = hipMemset(p->pend, 0, size_t(L) * p->pend_stride);
-    if (e == hipSuccess) e = hipMemset(p->stats, 0, size_t(L) * 3 * sizeof(unsigned long long));
+    p->co = reinterpret_cast<int32_t*>(base + y.co);
+    p->cct_idx = reinterpret_cast<uint8_t*>(base + y.cct_idx);
+    p->cct_conf = reinterpret_cast<uint8_t*>(base + y.cct_conf);
+    p->ht = reinterpret_cast<uint8_t*>(base + y.ht);
+    p->pend = reinterpret_cast<uint8_t*>(base + y.pend);
+    p->stats = reinterpret_cast<unsigned long long*>(base + y.stats);
+    p->stage = reinterpret_cast<int32_t*>(base + y.stage);
+    p->stage_bytes = y.stage_bytes;
+    hipError_t e = hipMemset(dev_ws, 0, y.stage);
     if (e == hipSuccess) e = hipDeviceSynchronize();
     if (e != hipSuccess) {
         set_error(std::string("stmoe_create: ") + hipGetErrorString(e));
-        stmoe_destroy(p);
-        return e == hipErrorOutOfMemory ? STMOE_ENOMEM : STMOE_EHIP;
+        delete p;
+        return STMOE_EHIP;
     }
     *out = p;
     return STMOE_OK;
 }
 
 extern "C" int stmoe_destroy(stmoe_predictor* p) {
-    if (!p) return STMOE_OK;
-    (void)hipFree(p->co);
-    (void)hipFree(p->cct_idx);
-    (void)hipFree(p->cct_conf);
-    (void)hipFree(p->ht);
-    (void)hipFree(p->pend);
-    (void)hipFree(p->stats);
-    delete p;
+    delete p;       // the tables live in the caller's workspace
     return STMOE_OK;
 }
 
@@ -228,31 +271,35 @@ extern "C" int stmoe_profile(stmoe_predictor* p, const int32_t* sel, int P) {
     STMOE_CHECK(P >= 1, "P must be >= 1");
     const int L = p->L, E = p->E, K = p->K, B = p->B;
     if (int rc = check_sel_host(sel, size_t(P) * B * L, E, K)) return rc;
-    const size_t n = size_t(P) * B * L * K;
+    const size_t tok = size_t(B) * L * K;                 // int32 per profiling token
+    const int chunk = int(p->stage_bytes / (tok * sizeof(int32_t)));
     const size_t pairs = size_t(L > 1 ? L - 1 : 1);
-    int32_t* dsel = nullptr;
-    STMOE_HIP(hipMalloc(&dsel, n * sizeof(int32_t)));
-    hipError_t e = hipMemcpy(dsel, sel, n * sizeof(int32_t), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemset(p->co, 0, pairs * E * E * sizeof(int32_t));
+    // the legacy null stream orders the blocking copies and the kernels
+    hipError_t e = hipMemset(p->co, 0, pairs * E * E * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(p->pend, 0, size_t(L) * p->pend_stride);
     if (e == hipSuccess) e = hipMemset(p->stats, 0, size_t(L) * 3 * sizeof(unsigned long long));
-    if (e == hipSuccess && L > 1) {
-        hipLaunchKernelGGL(co_count_kernel, dim3(P, L - 1), dim3(kThreads), 0, 0, dsel, P, B, L, E,
-                           K, p->co);
-        e = hipGetLastError();
-        if (e == hipSuccess) {
-            hipLaunchKernelGGL(cct_build_kernel, dim3(unsigned((L - 1) * E)), dim3(kThreads), 0, 0,
-                               p->co, E, K, p->cct_stride, p->cct_idx, p->cct_conf);
+    int last_at = 0;
+    for (int t0 = 0; t0 < P && e == hipSuccess; t0 += chunk) {
+        const int n = std::min(chunk, P - t0);
+        e = hipMemcpy(p->stage, sel + size_t(t0) * tok, size_t(n) * tok * sizeof(int32_t), hipMemcpyHostToDevice);
+        if (e == hipSuccess && L > 1) {
+            hipLaunchKernelGGL(co_count_kernel, dim3(n, L - 1), dim3(kThreads), 0, 0, p->stage, n, B, L, E, K,
+                               p->co);
             e = hipGetLastError();
         }
+        last_at = P - 1 - t0;                             // the last token's row within the final chunk
+    }
+    if (e == hipSuccess && L > 1) {
+        hipLaunchKernelGGL(cct_build_kernel, dim3(unsigned((L - 1) * E)), dim3(kThreads), 0, 0,
+                           p->co, E, K, p->cct_stride, p->cct_idx, p->cct_conf);
+        e = hipGetLastError();
     }
     if (e == hipSuccess) {
-        hipLaunchKernelGGL(ht_init_kernel, dim3(L, B), dim3(kThreads), 0, 0,
-                           dsel + size_t(P - 1) * B * L * K, B, L, K, p->ht_stride, p->ht);
+        hipLaunchKernelGGL(ht_init_kernel, dim3(L, B), dim3(kThreads), 0, 0, p->stage + size_t(last_at) * tok,
+                           B, L, K, p->ht_stride, p->ht);
         e = hipGetLastError();
     }
     if (e == hipSuccess) e = hipDeviceSynchronize();
-    (void)hipFree(dsel);
     if (e != hipSuccess) {
         set_error(std::string("stmoe_profile: ") + hipGetErrorString(e));
         return STMOE_EHIP;
@@ -337,7 +384,7 @@ int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int
 }  // namespace stmoe
 
 extern "C" int stmoe_export(stmoe_predictor* p, int32_t* co, uint8_t* cct_idx, uint8_t* cct_conf,
-                            uint8_t* ht) {
+                            int32_t* ht) {
     clear_error();
     STMOE_CHECK(p, "null predictor");
     const size_t pairs = size_t(p->L > 1 ? p->L - 1 : 0);
@@ -349,27 +396,50 @@ extern "C" int stmoe_export(stmoe_predictor* p, int32_t* co, uint8_t* cct_idx, u
         STMOE_HIP(hipMemcpy2D(cct_idx, ek, p->cct_idx, p->cct_stride, ek, pairs, hipMemcpyDeviceToHost));
     if (cct_conf && pairs)
         STMOE_HIP(hipMemcpy2D(cct_conf, ek, p->cct_conf, p->cct_stride, ek, pairs, hipMemcpyDeviceToHost));
-    if (ht) STMOE_HIP(hipMemcpy2D(ht, bk, p->ht, p->ht_stride, bk, p->L, hipMemcpyDeviceToHost));
+    if (ht) {
+        std::vector<uint8_t> h(size_t(p->L) * bk);
+        STMOE_HIP(hipMemcpy2D(h.data(), bk, p->ht, p->ht_stride, bk, p->L, hipMemcpyDeviceToHost));
+        for (size_t i = 0; i < h.size(); ++i) ht[i] = h[i];
+    }
     return STMOE_OK;
 }
 
 extern "C" int stmoe_import(stmoe_predictor* p, const uint8_t* cct_idx, const uint8_t* cct_conf,
-                            const uint8_t* ht) {
+                            const int32_t* ht) {
     clear_error();
     STMOE_CHECK(p && cct_idx && cct_conf && ht, "null pointer");
+    const int E = p->E, K = p->K;
     const size_t pairs = size_t(p->L > 1 ? p->L - 1 : 0);
-    for (size_t i = 0; i < pairs * p->E * p->K; ++i) {
-        STMOE_CHECK(cct_idx[i] < p->E, "CCT index out of range");
-        STMOE_CHECK(cct_conf[i] <= 3, "CCT confidence out of range");
+    // an entry names K distinct experts (Algorithm 1 builds it so and Algorithm 3
+    // keeps it so), which bounds every Eq. 1 score by 3K + 2
+    for (size_t r = 0; r < pairs * E; ++r) {
+        const uint8_t* row = cct_idx + r * K;
+        for (int k = 0; k < K; ++k) {
+            STMOE_CHECK(row[k] < E, "CCT index out of range");
+            STMOE_CHECK(cct_conf[r * K + k] <= 3, "CCT confidence out of range");
+            for (int j = 0; j < k; ++j) STMOE_CHECK(row[j] != row[k], "CCT entry repeats an expert");
+        }
     }
-    for (size_t i = 0; i < size_t(p->L) * p->B * p->K; ++i) STMOE_CHECK(ht[i] < p->E, "HT index out of range");
+    const size_t bk = size_t(p->B) * K;
+    std::vector<uint8_t> h(size_t(p->L) * bk);
+    for (size_t r = 0; r < size_t(p->L) * p->B; ++r) {
+        const int32_t* row = ht + r * K;
+        for (int k = 0; k < K; ++k) {
+            STMOE_CHECK(row[k] >= 0 && row[k] < E, "HT index out of range");
+            for (int j = 0; j < k; ++j) STMOE_CHECK(row[j] != row[k], "HT row repeats an expert");
+        }
+        // HT rows are kept sorted ascending
+        std::vector<int32_t> v(row, row + K);
+        std::sort(v.begin(), v.end());
+        for (int k = 0; k < K; ++k) h[r * K + k] = uint8_t(v[size_t(k)]);
+    }
     STMOE_HIP(hipDeviceSynchronize());
-    const size_t ek = size_t(p->E) * p->K, bk = size_t(p->B) * p->K;
+    const size_t ek = size_t(E) * K;
     if (pairs) {
         STMOE_HIP(hipMemcpy2D(p->cct_idx, p->cct_stride, cct_idx, ek, ek, pairs, hipMemcpyHostToDevice));
         STMOE_HIP(hipMemcpy2D(p->cct_conf, p->cct_stride, cct_conf, ek, ek, pairs, hipMemcpyHostToDevice));
     }
-    STMOE_HIP(hipMemcpy2D(p->ht, p->ht_stride, ht, bk, bk, p->L, hipMemcpyHostToDevice));
+    STMOE_HIP(hipMemcpy2D(p->ht, p->ht_stride, h.data(), bk, bk, p->L, hipMemcpyHostToDevice));
     p->profiled = true;
     return STMOE_OK;
 }
@@ -409,18 +479,18 @@ namespace stmoe {
 size_t update_predict_seq_bytes(int L) { return size_t(L) * sizeof(UpdPred); }
 
 // Internal: build the arguments of every layer for the selections idx_all
-// (device [L][B][K]) into dev_args (device, update_predict_seq_bytes(L));
-// synchronous.
-int update_predict_seq_args(stmoe_predictor* p, const int32_t* idx_all, int use, int online, void* dev_args) {
+// (device [L][B][K]) into dev_args (device, update_predict_seq_bytes(L)),
+// for both prediction sources with the online update on; synchronous.
+int update_predict_seq_args(stmoe_predictor* p, const int32_t* idx_all, void* dev_args) {
     std::vector<UpdPred> v(size_t(p->L));
     const size_t bk = size_t(p->B) * p->K;
     for (int l = 0; l < p->L; ++l) {
         const int32_t* cur = idx_all + size_t(l) * bk;
         const int32_t* prev = l > 0 ? idx_all + size_t(l - 1) * bk : nullptr;
-        v[size_t(l)].u = update_args(p, l, prev, cur, online);
+        v[size_t(l)].u = update_args(p, l, prev, cur, 1);
         v[size_t(l)].p = l + 1 < p->L
-                             ? predict_args(p, l, cur, use, nullptr, nullptr, nullptr, nullptr, nullptr)
-                             : predict_args(p, -1, nullptr, use & STMOE_USE_HT, nullptr, nullptr, nullptr, nullptr,
+                             ? predict_args(p, l, cur, STMOE_USE_BOTH, nullptr, nullptr, nullptr, nullptr, nullptr)
+                             : predict_args(p, -1, nullptr, STMOE_USE_HT, nullptr, nullptr, nullptr, nullptr,
                                             nullptr);
     }
     STMOE_HIP(hipMemcpy(dev_args, v.data(), v.size() * sizeof(UpdPred), hipMemcpyHostToDevice));
@@ -429,13 +499,13 @@ int update_predict_seq_args(stmoe_predictor* p, const int32_t* idx_all, int use,
 
 // Internal: one token's verify/update and predictions for every layer, in
 // layer order, one launch on `s` (the arguments from update_predict_seq_args).
-int update_predict_seq(stmoe_predictor* p, const void* dev_args, hipStream_t s) {
+int update_predict_seq(stmoe_predictor* p, const void* dev_args, int use, int online, hipStream_t s) {
     if (!p->profiled) {
         set_error("moe_decode_token: predictor has not been profiled");
         return STMOE_ESTATE;
     }
     hipLaunchKernelGGL(update_predict_seq_kernel, dim3(1), dim3(kThreads), 0, s,
-                       static_cast<const UpdPred*>(dev_args), p->L);
+                       static_cast<const UpdPred*>(dev_args), p->L, use, online ? 1 : 0);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }

@@ -21,6 +21,8 @@ struct stmoe_predictor {
     uint8_t* ht;                 // [L] x ht_stride, each [B][K], rows sorted ascending
     uint8_t* pend;               // [L] x pend_stride, each [B][E]: last prediction per layer
     unsigned long long* stats;   // [L][3]: hits, |A|, |P|
+    int32_t* stage;              // profiling selections staged in chunks of whole tokens
+    size_t stage_bytes;
     bool profiled;
 };
 

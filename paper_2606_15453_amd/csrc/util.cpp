@@ -16,7 +16,7 @@ using namespace stmoe;
 
 extern "C" const char* stmoe_last_error(void) { return g_last_error.c_str(); }
 
-extern "C" int stmoe_abi_version(void) { return 1; }
+extern "C" int stmoe_abi_version(void) { return 2; }
 
 extern "C" int stmoe_host_alloc(size_t bytes, void** out) {
     clear_error();

@@ -54,6 +54,20 @@ class CacheStats(C.Structure):
         return {n: int(getattr(self, n)) for n, _ in self._fields_}
 
 
+class LayerReport(C.Structure):
+    _fields_ = [("B", i32), ("K", i32), ("idx", i32 * 256), ("w", C.c_float * 256),
+                ("n_ranked", i32), ("ranked", i32 * 256), ("pred_stats", i64 * 3),
+                ("cache", CacheStats)]
+
+    def as_dict(self):
+        bk = self.B * self.K
+        n = self.n_ranked
+        return dict(idx=np.array(self.idx[:bk], np.int32).reshape(self.B, self.K),
+                    w=np.array(self.w[:bk], np.float32).reshape(self.B, self.K),
+                    n_ranked=n, ranked=list(self.ranked[:max(n, 0)]),
+                    pred_stats=tuple(self.pred_stats), cache=self.cache.as_dict())
+
+
 class ModelDesc(C.Structure):
     _fields_ = [("L", i32), ("E", i32), ("K", i32), ("B", i32), ("H", i32), ("I", i32),
                 ("n_shared", i32), ("dtype", i32), ("renorm", i32),
@@ -67,7 +81,8 @@ _SIGS = {
     "stmoe_host_free": (i32, [vp]),
     "moe_route_workspace_bytes": (sz, [i32, i32]),
     "moe_route_topk": (i32, [vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp]),
-    "stmoe_create": (i32, [i32, i32, i32, i32, P(vp)]),
+    "stmoe_workspace_bytes": (sz, [i32, i32, i32, i32]),
+    "stmoe_create": (i32, [i32, i32, i32, i32, vp, sz, P(vp)]),
     "stmoe_destroy": (i32, [vp]),
     "stmoe_profile": (i32, [vp, vp, i32]),
     "stmoe_update": (i32, [vp, i32, vp, vp, i32, vp]),
@@ -79,13 +94,14 @@ _SIGS = {
     "moe_pack_expert": (i32, [vp, vp, vp, i32, i32, i32, vp]),
     "moe_expert_ffn_workspace_bytes": (sz, [i32, i32, i32, i32, i32, i32, i32]),
     "moe_expert_ffn": (i32, [vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp, sz, vp]),
+    "expert_cache_warm_sets": (i32, [vp, i32, i32, i32, i32, i32, i32, vp]),
     "stmoe_policy_create": (i32, [i32, i32, i32, vp, P(vp)]),
     "stmoe_policy_destroy": (i32, [vp]),
     "stmoe_policy_prefetch": (i32, [vp, i32, vp, i32, i64, vp]),
     "stmoe_policy_acquire": (i32, [vp, i32, vp, i32, i64, vp, vp]),
     "stmoe_policy_slots": (i32, [vp, vp]),
     "stmoe_policy_stats": (i32, [vp, P(CacheStats)]),
-    "expert_cache_arena_bytes": (sz, [i32, i32, sz, i32]),
+    "expert_cache_arena_bytes": (sz, [i32, i32, i32, sz, i32]),
     "expert_cache_create": (i32, [i32, i32, i32, sz, i32, vp, sz, P(vp), vp, vp, P(vp)]),
     "expert_cache_destroy": (i32, [vp]),
     "expert_cache_warm": (i32, [vp, vp]),
@@ -94,10 +110,12 @@ _SIGS = {
     "expert_cache_release": (i32, [vp, i32, vp]),
     "expert_cache_set_prefetch_order": (i32, [vp, i32]),
     "expert_cache_set_device_policy": (i32, [vp, i32]),
+    "expert_cache_set_staged_prefetch": (i32, [vp, i32]),
     "expert_cache_stats": (i32, [vp, P(CacheStats)]),
-    "moe_ctx_create": (i32, [P(ModelDesc), vp, vp, vp, P(vp)]),
+    "moe_ctx_workspace_bytes": (sz, [P(ModelDesc)]),
+    "moe_ctx_create": (i32, [P(ModelDesc), vp, vp, vp, vp, sz, P(vp)]),
     "moe_ctx_destroy": (i32, [vp]),
-    "moe_decode_layer": (i32, [vp, i32, i32, vp, vp, i32]),
+    "moe_decode_layer": (i32, [vp, i32, i32, vp, vp, i32, P(LayerReport)]),
     "moe_decode_token": (i32, [vp, i32, vp, vp, i32]),
     "moe_ctx_set_prefetch": (i32, [vp, i32, i32]),
     "moe_ctx_set_online_update": (i32, [vp, i32]),
@@ -109,8 +127,8 @@ _SIGS = {
     "moe_ctx_timing": (i32, [vp, P(C.c_double), P(C.c_double), P(i64), P(i64)]),
     "moe_ctx_stage_timing": (i32, [vp, P(C.c_double), P(C.c_double), P(C.c_double), P(C.c_double), P(i64)]),
     "stmoe_calib_copy": (i32, [vp, vp, sz, vp]),
-    "stmoe_calib_read_out_words": (sz, [sz]),
-    "stmoe_calib_read": (i32, [vp, sz, vp, vp]),
+    "stmoe_calib_read_out_words": (sz, [sz, i32]),
+    "stmoe_calib_read": (i32, [vp, sz, i32, vp, vp]),
 }
 
 for _name, (_res, _args) in _SIGS.items():
@@ -163,6 +181,13 @@ def abi_version() -> int:
     return _lib.stmoe_abi_version()
 
 
+def device_workspace(nbytes, device="cuda:0"):
+    """A zeroed device buffer of at least `nbytes` whose returned address is
+    256-byte aligned: (tensor keeping it alive, aligned address)."""
+    t = torch.zeros(int(nbytes) + 256, dtype=torch.uint8, device=device)
+    return t, (t.data_ptr() + 255) // 256 * 256
+
+
 class PinnedHost:
     """A pinned host block of exactly `nbytes` (stmoe_host_alloc), viewable as a
     CPU uint8 tensor; freed on close()."""
@@ -203,11 +228,21 @@ def route_topk(x, w_gate, K, idx, w, ws, renorm=False, logits=None, stream=None,
 
 
 # ------------------------------------------------------------- predictor
+def predictor_workspace_bytes(L, E, K, B):
+    return _lib.stmoe_workspace_bytes(L, E, K, B)
+
+
 class Predictor:
+    """stmoe_predictor over a device workspace this object allocates (torch)."""
+
     def __init__(self, L, E, K, B):
         self.L, self.E, self.K, self.B = L, E, K, B
+        nbytes = _lib.stmoe_workspace_bytes(L, E, K, B)
+        if nbytes == 0:
+            raise StmoeError("stmoe_workspace_bytes", EINVAL)
+        self._ws, ptr = device_workspace(nbytes)
         h = vp()
-        _call("stmoe_create", L, E, K, B, C.byref(h))
+        _call("stmoe_create", L, E, K, B, ptr, nbytes, C.byref(h))
         self.h = h
 
     def close(self):
@@ -239,14 +274,14 @@ class Predictor:
         co = np.zeros((pr, E, E), np.int32)
         ci = np.zeros((pr, E, K), np.uint8)
         cc = np.zeros((pr, E, K), np.uint8)
-        ht = np.zeros((L, B, K), np.uint8)
+        ht = np.zeros((L, B, K), np.int32)
         _call("stmoe_export", self.h, co.ctypes.data, ci.ctypes.data, cc.ctypes.data, ht.ctypes.data)
         return co, ci, cc, ht
 
     def import_tables(self, cct_idx, cct_conf, ht):
         ci = np.ascontiguousarray(cct_idx, np.uint8)
         cc = np.ascontiguousarray(cct_conf, np.uint8)
-        h = np.ascontiguousarray(ht, np.uint8)
+        h = np.ascontiguousarray(ht, np.int32)
         _call("stmoe_import", self.h, ci.ctypes.data, cc.ctypes.data, h.ctypes.data)
 
     def stats(self):
@@ -279,6 +314,15 @@ def expert_ffn(x, idx, w, H, I, E, dtype, expert_ptrs, y, ws, shared_ptrs=None, 
 
 
 # ------------------------------------------------------------- cache policy
+def warm_sets(sel, E, C_):
+    """expert_cache_warm_sets: per layer the C most-profiled experts ([L][C], -1 padding)."""
+    sel = _i32(sel)
+    P_, B_, L_, K_ = sel.shape
+    out = np.zeros((L_, C_), np.int32)
+    _call("expert_cache_warm_sets", sel.ctypes.data, P_, B_, L_, K_, E, C_, out.ctypes.data)
+    return out
+
+
 class Policy:
     def __init__(self, L, E, C_, warm=None):
         self.L, self.E, self.C = L, E, C_
@@ -318,8 +362,8 @@ class Policy:
 
 
 # ------------------------------------------------------------- HBM cache
-def cache_arena_bytes(L, C_, blob, n_stage):
-    return _lib.expert_cache_arena_bytes(L, C_, blob, n_stage)
+def cache_arena_bytes(L, E, C_, blob, n_stage):
+    return _lib.expert_cache_arena_bytes(L, E, C_, blob, n_stage)
 
 
 class ExpertCache:
@@ -367,6 +411,10 @@ class ExpertCache:
     def set_device_policy(self, on):
         _call("expert_cache_set_device_policy", self.h, int(on))
 
+    def set_staged_prefetch(self, n_per_layer):
+        """Prefetch into spare staging blocks (at most n per layer), cancelled when unused."""
+        _call("expert_cache_set_staged_prefetch", self.h, int(n_per_layer))
+
     def stats(self):
         st = CacheStats()
         _call("expert_cache_stats", self.h, C.byref(st))
@@ -385,9 +433,13 @@ class DecodeContext:
         self._shared = None if not n_shared else (vp * (L * n_shared))(*[int(p) for p in shared_ptrs])
         d = ModelDesc(L, E, K, B, H, I, n_shared, dtype, int(renorm), self._router,
                       self._shared, self._resident)
+        nbytes = _lib.moe_ctx_workspace_bytes(C.byref(d))
+        if nbytes == 0:
+            raise StmoeError("moe_ctx_workspace_bytes", EINVAL)
+        self._ws, ptr = device_workspace(nbytes)
         h = vp()
         _call("moe_ctx_create", C.byref(d), predictor.h if predictor else None,
-              cache.h if cache else None, _s(stream), C.byref(h))
+              cache.h if cache else None, _s(stream), ptr, nbytes, C.byref(h))
         self.h = h
         self._keep = (predictor, cache)
 
@@ -402,8 +454,12 @@ class DecodeContext:
         except Exception:
             pass
 
-    def layer(self, token, layer, x, y, mode=MODE_STMOE):
-        _call("moe_decode_layer", self.h, token, layer, _p(x), _p(y), mode)
+    def layer(self, token, layer, x, y, mode=MODE_STMOE, report=False):
+        """One layer; with report=True waits for it and returns its moe_layer_report as a dict."""
+        rep = LayerReport() if report else None
+        _call("moe_decode_layer", self.h, token, layer, _p(x), _p(y), mode,
+              C.byref(rep) if report else None)
+        return rep.as_dict() if report else None
 
     def set_prefetch(self, min_score=2, max_per_layer=1 << 30):
         _call("moe_ctx_set_prefetch", self.h, min_score, max_per_layer)
@@ -460,9 +516,10 @@ def calib_copy(src, dst, nbytes, stream=None):
     _call("stmoe_calib_copy", _p(src), _p(dst), nbytes, _s(stream))
 
 
-def calib_read(src, nbytes, out, stream=None):
-    _call("stmoe_calib_read", _p(src), nbytes, _p(out), _s(stream))
+def calib_read(src, nbytes, out, stream=None, pattern=0):
+    """Streaming read of nbytes: pattern 0 grid stride, 1 contiguous 256 KiB per workgroup."""
+    _call("stmoe_calib_read", _p(src), nbytes, int(pattern), _p(out), _s(stream))
 
 
-def calib_read_out_words(nbytes):
-    return _lib.stmoe_calib_read_out_words(nbytes)
+def calib_read_out_words(nbytes, pattern=0):
+    return _lib.stmoe_calib_read_out_words(nbytes, int(pattern))

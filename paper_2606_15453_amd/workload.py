@@ -401,16 +401,3 @@ def to_storage(cfg: MoEConfig, a_f64: np.ndarray) -> np.ndarray:
 def profiling_selections(cfg: MoEConfig, planted: np.ndarray) -> np.ndarray:
     """The P profiling tokens' selections sel[p][b][l][k] (the planted sets)."""
     return np.ascontiguousarray(planted[:cfg.P])
-
-
-def warm_sets(cfg: MoEConfig, prof: np.ndarray, C: int | None = None) -> np.ndarray:
-    """Initial cache residency per layer: the C experts most often selected
-    during profiling (count desc, index asc); -1 pads.  Returns int32 [L][C]."""
-    C = cfg.C if C is None else C
-    out = np.full((cfg.L, C), -1, dtype=np.int32)
-    for l in range(cfg.L):
-        cnt = np.bincount(prof[:, :, l, :].ravel(), minlength=cfg.E)
-        order = sorted(range(cfg.E), key=lambda e: (-int(cnt[e]), e))
-        take = order[:min(C, cfg.E)]
-        out[l, :len(take)] = take
-    return out

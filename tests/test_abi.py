@@ -104,3 +104,39 @@ def test_policy_rejects_bad_lists():
         p.prefetch(0, [9], 1)
     with pytest.raises(S.StmoeError):
         p.acquire(5, [1], 1)
+
+
+@pytest.mark.parametrize("P,B,L,K,E,C", [(5, 1, 4, 2, 8, 3), (16, 4, 3, 6, 64, 24), (3, 2, 2, 8, 16, 20)])
+def test_warm_sets_match_oracle(P, B, L, K, E, C):
+    """The library's initial residency equals the oracle's (count desc, index asc, -1 padding)."""
+    from oracle.stmoe_oracle import warm_from_profile
+    rng = np.random.default_rng(P * 1000 + E)
+    sel = np.stack([np.stack([np.stack([rng.choice(E, K, replace=False) for _ in range(L)])
+                              for _ in range(B)]) for _ in range(P)]).astype(np.int32)
+    assert np.array_equal(S.warm_sets(sel, E, C), warm_from_profile(sel, L, E, C))
+
+
+def test_workspace_queries_and_rejections_without_device_work():
+    """Every device buffer comes from the caller: the size queries are host-only,
+    and the create calls reject a missing or short workspace before touching the
+    device."""
+    import ctypes as C_
+    n = S._lib.stmoe_workspace_bytes(94, 128, 8, 16)
+    assert n > 0 and n % 256 == 0
+    assert S._lib.stmoe_workspace_bytes(2, 300, 8, 1) == 0          # E > 256
+    h = C_.c_void_p()
+    assert S._lib.stmoe_create(4, 8, 2, 1, None, 1 << 20, C_.byref(h)) == S.EINVAL
+    assert S._lib.stmoe_create(4, 8, 2, 1, 256, 16, C_.byref(h)) == S.EINVAL
+    assert "workspace" in S._lib.stmoe_last_error().decode()
+    assert S._lib.stmoe_create(4, 8, 2, 1, 256 + 4, 1 << 30, C_.byref(h)) == S.EINVAL   # misaligned
+    assert S.cache_arena_bytes(4, 8, 3, 4096, 1) >= (4 * 3 + 1) * 4096
+    assert S.cache_arena_bytes(4, 8, 9, 4096, 1) == 0                                  # C > E
+    router = (C_.c_void_p * 4)(*([16] * 4))
+    resident = (C_.c_void_p * 32)(*([16] * 32))
+    d = S.ModelDesc(4, 8, 2, 1, 256, 512, 0, S.F32, 0, router, None, resident)
+    nb = S._lib.moe_ctx_workspace_bytes(C_.byref(d))
+    assert nb > 0 and nb % 256 == 0
+    assert S._lib.moe_ctx_create(C_.byref(d), None, None, None, None, nb, C_.byref(h)) == S.EINVAL
+    assert S._lib.moe_ctx_create(C_.byref(d), None, None, None, 256, nb - 256, C_.byref(h)) == S.EINVAL
+    bad = S.ModelDesc(4, 8, 9, 1, 256, 512, 0, S.F32, 0, router, None, resident)        # K > E
+    assert S._lib.moe_ctx_workspace_bytes(C_.byref(bad)) == 0

@@ -26,13 +26,18 @@ class Stack:
         self.x_store = xs
         self.x_dev = [to_dev(np.stack(xs[t])) for t in range(cfg.T)]      # [L][B][H] per token
         self.prof = W.profiling_selections(cfg, self.sel)
-        self.warm = W.warm_sets(cfg, self.prof)
+        from oracle.stmoe_oracle import warm_from_profile
+        from paper_2606_15453_amd import stmoe as S
+        self.warm = S.warm_sets(self.prof, cfg.E, cfg.C)
+        self.warm_ref = warm_from_profile(self.prof, cfg.L, cfg.E, cfg.C)
+        assert np.array_equal(self.warm, self.warm_ref)
 
     def shared_ptrs(self):
         return [s.data_ptr() for l in range(self.cfg.L) for s in self.shared[l]]
 
 
-def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True):
+def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True, tables=None, min_score=2,
+            max_per_layer=None, staged=0):
     from gpuhelp import expert_f64
     from oracle.stmoe_oracle import decode_reference, decode_storage, moe_ffn
     cfg = st.cfg
@@ -43,18 +48,53 @@ def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True):
 
     return decode_reference(cfg.L, cfg.E, cfg.K, cfg.B, lambda t, l: decode_storage(st.x_store[t][l]),
                             lambda l: decode_storage(st.wg[l]), st.prof, cfg.T, C=C,
-                            warm=None if C is None else st.warm, mode=mode, ffn_of=ffn_of,
-                            ffn_tokens=ffn_tokens, renorm=renorm, online=online)
+                            warm=None if C is None else st.warm_ref, mode=mode, ffn_of=ffn_of,
+                            ffn_tokens=ffn_tokens, renorm=renorm, online=online, tables=tables,
+                            min_score=min_score, max_per_layer=max_per_layer, staged=staged)
+
+
+def _counts(n):
+    return dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
+                useful=n.useful, wasted=n.wasted)
+
+
+def _cumulative_after_layers(cache, L):
+    """The oracle cache's cumulative counts after each decode layer (t, l): its
+    acquire and the prefetch issued at the end of that layer."""
+    out, c = [], dict(hits=0, demand=0, overflow=0, prefetch=0, useful=0, wasted=0)
+    log = list(cache.n.log)
+    i = 0
+    if log and log[0][0] == "P":                             # the first token's layer-0 prefetch
+        c["prefetch"] += len(log[0][3])
+        i = 1
+    while i < len(log):
+        ent = log[i]
+        assert ent[0] == "A"
+        c["demand"] += len(ent[3])
+        c["overflow"] += len(ent[4])
+        c["hits"] += ent[5]
+        c["useful"] += ent[6]
+        c["wasted"] += ent[7]
+        i += 1
+        if i < len(log) and log[i][0] == "P":
+            c["prefetch"] += len(log[i][3])
+            i += 1
+        out.append(dict(c))
+    return out
 
 
 def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0, device=0,
-             device_until=None, device_pool=False, batch=False):
+             device_until=None, device_pool=False, batch=False, C=None, import_tables=None,
+             admission=None, layerwise=False, attn_bytes=0, reports=None, staged=0):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
     cfg = st.cfg
+    C = cfg.C if C is None else C
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(st.prof)
+    if import_tables is not None:
+        pred.import_tables(*import_tables)
     stream = torch.cuda.current_stream()
     cache = None
     keep = []
@@ -65,15 +105,17 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
                 h = st.blobs[l][e] if device_pool else st.blobs[l][e].cpu().pin_memory()
                 keep.append(h)
                 host.append(h.data_ptr())
-        n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - cfg.C)
-        arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.C, cfg.blob_bytes, n_stage),
+        n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - C, 2 * staged)
+        arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.E, C, cfg.blob_bytes, n_stage),
                             dtype=torch.uint8, device=DEV)
         demand, side = torch.cuda.Stream(), torch.cuda.Stream()
         keep += [arena, demand, side]
-        cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, cfg.blob_bytes, n_stage, arena, host, demand, side)
-        cache.warm(st.warm)
+        cache = S.ExpertCache(cfg.L, cfg.E, C, cfg.blob_bytes, n_stage, arena, host, demand, side)
+        cache.warm(st.warm if C == cfg.C else S.warm_sets(st.prof, cfg.E, C))
         cache.set_prefetch_order(after_demand)
         cache.set_device_policy(device)
+        if staged:
+            cache.set_staged_prefetch(staged)
         ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
                               [g.data_ptr() for g in st.wg_dev], predictor=pred, cache=cache,
                               shared_ptrs=st.shared_ptrs(), n_shared=cfg.n_shared, renorm=renorm,
@@ -87,12 +129,27 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
     ctx.set_online_update(online)
     if batch:
         ctx.set_predictor_batch(True)
+    if admission is not None:
+        ctx.set_prefetch(*admission)
+    if attn_bytes:
+        # decode-attention stand-in: a KV-sized stream on the compute stream before every layer
+        kv = torch.zeros(attn_bytes, dtype=torch.uint8, device=DEV)
+        kv_out = torch.empty(S.calib_read_out_words(attn_bytes), dtype=torch.int32, device=DEV)
+        keep += [kv, kv_out]
     idx_hist, ys = [], []
     for t in range(cfg.T):
         if cache is not None and device_until is not None and t == device_until:
             cache.set_device_policy(0)       # the host policy takes over the device state
         y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device=DEV)
-        ctx.token(t, st.x_dev[t], y, mode=mode)
+        if layerwise:
+            for l in range(cfg.L):
+                if attn_bytes:
+                    S.calib_read(kv, attn_bytes, kv_out, stream=stream)
+                rep = ctx.layer(t, l, st.x_dev[t][l], y[l], mode=mode, report=reports is not None)
+                if reports is not None:
+                    reports.append(rep)
+        else:
+            ctx.token(t, st.x_dev[t], y, mode=mode)
         idx, _ = ctx.last_routing()
         idx_hist.append(idx)
         ys.append(y.cpu().numpy())
@@ -298,7 +355,7 @@ def test_device_policy_rejects_host_calls():
     from paper_2606_15453_amd import stmoe as S
     L, E, C, blob = 2, 4, 2, 4096
     host = [torch.zeros(blob, dtype=torch.uint8).pin_memory() for _ in range(L * E)]
-    arena = torch.empty(S.cache_arena_bytes(L, C, blob, 0), dtype=torch.uint8, device=DEV)
+    arena = torch.empty(S.cache_arena_bytes(L, E, C, blob, 0), dtype=torch.uint8, device=DEV)
     demand, side = torch.cuda.Stream(), torch.cuda.Stream()
     cache = S.ExpertCache(L, E, C, blob, 0, arena, [h.data_ptr() for h in host], demand, side)
     cache.warm(np.array([[0, 1], [2, 3]], dtype=np.int32))
@@ -411,3 +468,181 @@ def test_ctx_rejects_mismatched_predictor():
                             [g.data_ptr() for g in st.wg_dev], predictor=pred, resident_ptrs=resident,
                             stream=torch.cuda.current_stream())
         pred.close()
+
+
+# ---------------------------------------------------------------------------
+# The per-layer entry point (moe_decode_layer) with its report, layer by
+# layer, with and without a decode-attention stand-in between layers.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,over", [CFGS[0], CFGS[1], CFGS[3]])
+@pytest.mark.parametrize("capped,device,mode,attn", [(False, 0, 1, 0), (False, 0, 1, 1 << 24),
+                                                     (True, 0, 1, 0), (True, 1, 1, 1 << 24),
+                                                     (True, 1, 0, 0), (True, 0, 3, 1 << 24)])
+def test_decode_layer_by_layer(name, over, capped, device, mode, attn):
+    """moe_decode_layer called once per layer gives the selections and outputs
+    of moe_decode_token bit for bit; each layer's report matches the oracle's
+    loop: the selection, the layer's hit and prediction counts, the ranked
+    prediction for the next layer and the cache counters so far."""
+    from oracle.stmoe_oracle import STPredictor, admitted
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    print(f"[layerwise] {cfg.name} capped={capped} device={device} mode={mode} attn={attn}", flush=True)
+    idx_tok, ys_tok, stats_tok, cst_tok = _run_gpu(st, mode, capped=capped, device=device)
+    reps = []
+    idx_lay, ys_lay, stats_lay, cst_lay = _run_gpu(st, mode, capped=capped, device=device, layerwise=True,
+                                                   attn_bytes=attn, reports=reps)
+    for t in range(cfg.T):
+        assert np.array_equal(idx_tok[t], idx_lay[t]), t
+        assert np.array_equal(ys_tok[t], ys_lay[t]), t
+    assert np.array_equal(stats_tok, stats_lay)
+    assert cst_tok == cst_lay
+    ref = _oracle(st, mode, C=cfg.C if capped else None)
+    assert ref["tie_boundary"] == 0
+    cum = _cumulative_after_layers(ref["cache"], cfg.L) if capped else None
+    prev = np.zeros((cfg.L, 3), np.int64)
+    for t in range(cfg.T):
+        for l in range(cfg.L):
+            rep = reps[t * cfg.L + l]
+            r = ref["idx"][t * cfg.L + l]
+            for b in range(cfg.B):
+                assert sorted(rep["idx"][b].tolist()) == sorted(r[b].tolist()), (t, l, b)
+            ps = np.array(rep["pred_stats"])
+            assert ps[0] - prev[l, 0] == ref["hits"][t, l], (t, l)
+            assert ps[2] - prev[l, 2] == ref["npred"][t, l], (t, l)
+            prev[l] = ps
+            if mode:
+                assert rep["ranked"] == STPredictor.ranked_union(ref["scores"][t * cfg.L + l]), (t, l)
+            else:
+                assert rep["n_ranked"] == -1
+            if capped:
+                assert rep["cache"] == cum[t * cfg.L + l], (t, l)
+    if capped:
+        assert cst_lay == _counts(ref["cache"].n)
+
+
+# ---------------------------------------------------------------------------
+# Fault injection: correctness never depends on the prediction (Section 4.1:
+# prefetching must not change what the model computes).  Wrong tables are
+# planted through stmoe_import; capacities at their extremes.
+# ---------------------------------------------------------------------------
+
+def _planted_tables(cfg, kind, st):
+    """(cct_idx, cct_conf, ht) after profiling, with the planted fault."""
+    from oracle.stmoe_oracle import STPredictor
+    p = STPredictor(cfg.L, cfg.E, cfg.K, cfg.B)
+    p.profile(st.prof)
+    _, ci, cc, ht = p.tables()
+    if kind in ("zero_conf", "both"):
+        cc[:] = 0
+    if kind in ("wiped_ht", "both"):
+        ht[:] = np.arange(cfg.E - cfg.K, cfg.E)
+    return ci, cc, ht
+
+
+@pytest.mark.parametrize("kind", ["zero_conf", "wiped_ht", "both"])
+@pytest.mark.parametrize("cap", ["K", "E"])
+@pytest.mark.parametrize("device", [0, 1])
+def test_fault_injection_outputs_and_counts(kind, cap, device):
+    """Zeroed CCT confidences and/or an HT of wrong experts, at cache
+    capacities C = K and C = E: outputs are bit-identical to on-demand loading
+    (and to the all-resident run), and the copy counts equal the oracle's
+    with the same planted tables."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen30b"].scaled(L=4, T=6, P=3, C=10) if cap == "K" else W.CONFIGS["tiny"].scaled(T=8)
+    C = cfg.K if cap == "K" else cfg.E
+    st = Stack(cfg)
+    tabs = _planted_tables(cfg, kind, st)
+    print(f"[fault] {kind} C={C} device={device}", flush=True)
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    _, ys_dem, _, cst_dem = _run_gpu(st, 0, capped=True, device=device, C=C)
+    _, ys, stats, cst = _run_gpu(st, 1, capped=True, device=device, C=C,
+                                 import_tables=(tabs[0].astype(np.uint8), tabs[1].astype(np.uint8), tabs[2]))
+    for t in range(cfg.T):
+        assert np.array_equal(ys[t], ys_dem[t]), t
+        assert np.array_equal(ys[t], ys_res[t]), t
+    from oracle.stmoe_oracle import warm_from_profile
+    st.warm_ref = warm_from_profile(st.prof, cfg.L, cfg.E, C)
+    ref = _oracle(st, 1, C=C, tables=tabs)
+    assert cst == _counts(ref["cache"].n)
+    assert np.array_equal(stats[:, 0], ref["hits"].sum(axis=0))
+    assert cst_dem == _counts(_oracle(st, 0, C=C)["cache"].n)
+    if C == cfg.E:
+        assert cst["demand"] == 0 and cst["overflow"] == 0 and cst["prefetch"] == 0
+
+
+@pytest.mark.parametrize("device", [0, 1])
+@pytest.mark.parametrize("min_score,max_per_layer", [(4, None), (2, 1), (4, 8), (7, 3)])
+def test_admission_knobs_match_oracle(device, min_score, max_per_layer):
+    """The prefetch admission knobs (minimum Eq. 1 score, at most N prefetches
+    per layer) take the oracle's admitted prefix: same counts; outputs as the
+    all-resident run."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen30b"].scaled(L=4, T=6, P=3, C=10)
+    st = Stack(cfg)
+    mpl = max_per_layer if max_per_layer is not None else 1 << 30
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    _, ys, _, cst = _run_gpu(st, 1, capped=True, device=device, admission=(min_score, mpl))
+    for t in range(cfg.T):
+        assert np.array_equal(ys[t], ys_res[t]), t
+    ref = _oracle(st, 1, C=cfg.C, min_score=min_score, max_per_layer=max_per_layer)
+    assert cst == _counts(ref["cache"].n)
+
+
+# ---------------------------------------------------------------------------
+# Staged prefetch: predicted experts copied into spare blocks, cancelled when
+# the next layer's routing does not select them; residency as on demand.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,over", CFGS)
+@pytest.mark.parametrize("mode,n_staged,admission,layerwise", [(1, 1, None, False), (1, 4, None, False),
+                                                               (3, 2, None, False), (1, 2, (4, 8), False),
+                                                               (1, 3, None, True)])
+def test_decode_capped_staged_prefetch(name, over, mode, n_staged, admission, layerwise):
+    """Staged prefetch (device decisions): the copy counts equal the oracle's
+    staged cache, the hits equal on-demand loading's (residency is unchanged
+    by staging), and the outputs are bit-identical to the all-resident run,
+    per token and layer by layer with a decode-attention stand-in."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    print(f"[staged] {cfg.name} mode={mode} n={n_staged} admission={admission} layerwise={layerwise}", flush=True)
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    _, ys, _, cst = _run_gpu(st, mode, capped=True, device=1, staged=n_staged,
+                             admission=None if admission is None else admission,
+                             layerwise=layerwise, attn_bytes=(1 << 22) if layerwise else 0)
+    for t in range(cfg.T):
+        assert np.array_equal(ys[t], ys_res[t]), t
+    ms, mpl = (2, None) if admission is None else admission
+    ref = _oracle(st, mode, C=cfg.C, staged=n_staged, min_score=ms, max_per_layer=mpl)
+    assert cst == _counts(ref["cache"].n)
+    dem = _oracle(st, 0, C=cfg.C)["cache"]
+    assert cst["hits"] == dem.n.hits
+    assert ref["cache"].slot == dem.slot
+
+
+def test_staged_prefetch_rejections():
+    """Staged prefetch needs device decisions and 2n staging slots; once it has
+    run, the host policy cannot take the cache over."""
+    import torch
+    from gpuhelp import DEV
+    from paper_2606_15453_amd import stmoe as S
+    L, E, C, blob = 2, 4, 2, 4096
+    host = [torch.zeros(blob, dtype=torch.uint8).pin_memory() for _ in range(L * E)]
+    arena = torch.empty(S.cache_arena_bytes(L, E, C, blob, 2), dtype=torch.uint8, device=DEV)
+    demand, side = torch.cuda.Stream(), torch.cuda.Stream()
+    cache = S.ExpertCache(L, E, C, blob, 2, arena, [h.data_ptr() for h in host], demand, side)
+    cache.warm(np.array([[0, 1], [2, 3]], dtype=np.int32))
+    with pytest.raises(S.StmoeError) as ei:
+        cache.set_staged_prefetch(1)
+    assert ei.value.rc == S.ESTATE
+    cache.set_device_policy(1)
+    with pytest.raises(S.StmoeError) as ei:
+        cache.set_staged_prefetch(2)                 # needs 4 staging slots
+    assert ei.value.rc == S.EINVAL
+    cache.set_staged_prefetch(1)
+    with pytest.raises(S.StmoeError) as ei:
+        cache.set_device_policy(0)
+    assert ei.value.rc == S.ESTATE
+    cache.close()

@@ -147,27 +147,41 @@ def test_table1_shapes_parity(name):
     _run(cfg.L, cfg.E, cfg.K, cfg.B, sel[:cfg.P], sel[cfg.P:])
 
 
-def test_repeated_experts_in_imported_entries():
-    """Imported CCT entries may repeat an expert; scores then exceed K*3+2 and
-    the ranking takes its exact out-of-histogram path.  Same result as Eq. 1."""
+def test_import_rejects_repeated_experts_and_max_score_is_exact():
+    """An imported CCT entry or HT row that repeats an expert is refused (Eq. 1
+    scores stay within 3K + 2).  At K = 16 with every confidence at 3 and every
+    entry holding the same 16 experts, the top score reaches 3K + 2 = 50 and
+    the ranking matches Eq. 1."""
     import torch
     from gpuhelp import DEV, i32
     from oracle.stmoe_oracle import STPredictor
     from paper_2606_15453_amd import stmoe as S
     rng = np.random.default_rng(9)
     L, E, K, B = 2, 32, 16, 2
-    ci = rng.integers(0, E, size=(L - 1, E, K))
-    ci[:, ::2, :] = rng.integers(0, 3, size=(L - 1, E // 2, K))   # experts 0..2 repeated
-    cc = rng.integers(0, 4, size=(L - 1, E, K))
+    gp = S.Predictor(L, E, K, B)
+    ci = np.stack([np.stack([rng.permutation(E)[:K] for _ in range(E)]) for _ in range(L - 1)])
+    cc = np.full((L - 1, E, K), 3)
     ht = np.sort(np.stack([np.stack([rng.choice(E, K, replace=False) for _ in range(B)])
                            for _ in range(L)]), axis=2)
+    bad = ci.copy()
+    bad[0, 5, 3] = bad[0, 5, 0]
+    with pytest.raises(S.StmoeError) as ei:
+        gp.import_tables(bad, cc, ht)
+    assert ei.value.rc == S.EINVAL
+    badh = ht.copy()
+    badh[1, 0, 1] = badh[1, 0, 0]
+    with pytest.raises(S.StmoeError) as ei:
+        gp.import_tables(ci, cc, badh)
+    assert ei.value.rc == S.EINVAL
+    # every entry names experts 0..15 with confidence 3; HT rows hold expert 0
+    ci[:] = np.arange(K)
+    ht[1, 0] = np.arange(K)
     sel = np.stack([rng.choice(E, K, replace=False) for _ in range(B)]).astype(np.int32)
     ref = STPredictor(L, E, K, B)
-    ref.cct_idx, ref.cct_conf, ref.ht = ci.tolist(), cc.tolist(), ht.tolist()
+    ref.load_tables(ci, cc, ht)
     sc = ref.predict(0, [list(r) for r in sel])
-    assert sc.max() >= 64 and sc.max() < 256
-    gp = S.Predictor(L, E, K, B)
-    gp.import_tables(ci.astype(np.uint8), cc.astype(np.uint8), ht.astype(np.uint8))
+    assert sc.max() == 3 * K + 2
+    gp.import_tables(ci.astype(np.uint8), cc.astype(np.uint8), ht)
     score = torch.zeros((B, E), dtype=torch.uint8, device=DEV)
     mask = torch.zeros(E, dtype=torch.uint8, device=DEV)
     mx = torch.zeros(E, dtype=torch.uint8, device=DEV)
@@ -182,4 +196,24 @@ def test_repeated_experts_in_imported_entries():
     assert int(nr.item()) == len(rr)
     r = ranked.cpu().numpy()
     assert r[:len(rr)].tolist() == rr and np.all(r[len(rr):] == -1)
+    gp.close()
+
+
+def test_profile_spans_staging_chunks():
+    """Profiling selections pass through the workspace's staging area in
+    chunks of whole tokens (here 3 tokens of 300 layers x 16 rows x top-16 per
+    chunk, 7 tokens): counts, tables and the HT from the last token as the
+    oracle's."""
+    from oracle.stmoe_oracle import STPredictor
+    from paper_2606_15453_amd import stmoe as S
+    rng = np.random.default_rng(12)
+    L, E, K, B, P = 300, 64, 16, 16, 7
+    sel = np.stack([np.stack([np.stack([rng.choice(E, K, replace=False) for _ in range(L)])
+                              for _ in range(B)]) for _ in range(P)]).astype(np.int32)
+    gp = S.Predictor(L, E, K, B)
+    gp.profile(sel)
+    ref = STPredictor(L, E, K, B)
+    ref.profile(sel)
+    for a, b in zip(gp.export(), ref.tables()):
+        assert np.array_equal(a, b)
     gp.close()

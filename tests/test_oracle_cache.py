@@ -109,3 +109,52 @@ def test_on_demand_policy_is_not_better_than_optimum():
             c.acquire(0, U, i + 1)
         opt = _optimal_misses([tuple(s) for s in seq], C, (0, 1))
         assert c.n.demand + c.n.overflow >= opt
+
+
+def test_hand_worked_staged_trace():
+    with open(os.path.join(GOLD, "cache_trace_staged.json")) as f:
+        g = json.load(f)
+    c = CacheSim(g["L"], g["E"], g["C"], g["warm"], staged=g["staged"])
+    for st in g["steps"]:
+        if st["op"] == "A":
+            c.acquire(0, st["set"], st["stamp"])
+        else:
+            c.prefetch(0, st["set"], st["stamp"])
+        ent = c.n.log[-1]
+        got = [ent[0], ent[1], ent[2], [list(x) for x in ent[3]]]
+        if ent[0] == "A":
+            got += [list(ent[4]), ent[5], ent[6], ent[7]]
+        assert got == st["log"]
+    assert c.slot == g["final_slots"]
+    n = c.n
+    assert dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch, useful=n.useful,
+                wasted=n.wasted) == g["counts"]
+
+
+@pytest.mark.parametrize("E,C,K,S", [(8, 3, 2, 1), (16, 4, 5, 3), (32, 6, 4, 8)])
+def test_staged_prefetch_keeps_on_demand_residency(E, C, K, S):
+    """With staged prefetch the slots evolve exactly as with on-demand loading
+    (same hits), and every miss is either a demand copy, an overflow or a used
+    staged copy."""
+    rng = np.random.default_rng(E * 7 + S)
+    L = 3
+    warm = [list(range(C)) for _ in range(L)]
+    st = CacheSim(L, E, C, warm, staged=S)
+    od = CacheSim(L, E, C, warm)
+    tot = 0
+    stamp = 0
+    for t in range(40):
+        for l in range(L):
+            stamp += 1
+            U = sorted(rng.choice(E, size=K, replace=False).tolist())
+            tot += len(U)
+            st.acquire(l, U, stamp)
+            od.acquire(l, U, stamp)
+            assert st.slot == od.slot
+            ranked = rng.permutation(E)[:int(rng.integers(0, E))].tolist()
+            st.prefetch((l + 1) % L, ranked, stamp)
+    assert st.n.hits == od.n.hits
+    assert st.n.hits + st.n.demand + st.n.overflow + st.n.useful == tot
+    assert st.n.demand + st.n.overflow + st.n.useful == od.n.demand + od.n.overflow
+    outstanding = sum(len(x) for x in st.stage)
+    assert st.n.useful + st.n.wasted + outstanding == st.n.prefetch

@@ -50,13 +50,13 @@ def _pairs(pred):
     return [[[int(idx[0, e, s]), int(conf[0, e, s])] for s in range(K)] for e in range(E)]
 
 
-def _log(cache):
+def _log(cache, full=False):
     out = []
     for ent in cache.n.log:
         if ent[0] == "P":
             out.append(["P", ent[1], ent[2], [list(c) for c in ent[3]]])
         else:
-            out.append(["A", ent[1], ent[2], [list(c) for c in ent[3]], list(ent[4])])
+            out.append(["A", ent[1], ent[2], [list(c) for c in ent[3]], list(ent[4])] + (list(ent[5:]) if full else []))
     return out
 
 
@@ -128,6 +128,17 @@ def test_capped_loop_stmoe():
 
 def test_capped_loop_on_demand():
     assert mismatches_capped(MODE_ON_DEMAND) == []
+
+
+def test_capped_loop_staged():
+    """Staged prefetch inside the loop: the slots follow the on-demand trace
+    exactly, the staged copies are the first non-resident ranked experts."""
+    cp = D["capped"]
+    rec = _run(len(G["decode"]), C=cp["C"], warm=cp["warm"], mode=MODE_STMOE, staged=2)
+    assert _log(rec["cache"], full=True) == cp["staged2_log"]
+    assert _counts(rec["cache"]) == cp["staged2_counts"]
+    dem = _run(len(G["decode"]), C=cp["C"], warm=cp["warm"], mode=MODE_ON_DEMAND)
+    assert rec["cache"].slot == dem["cache"].slot
 
 
 def test_warm_start_policy():

@@ -92,9 +92,11 @@ def test_router_recovers_planted_sets(name):
 
 
 def test_warm_sets():
-    cfg = W.CONFIGS["tiny"]
+    """Initial residency by profiling counts (the oracle's policy; the library's
+    is checked against it in test_abi)."""
+    from oracle.stmoe_oracle import warm_from_profile
     prof = np.array([[[[0, 1], [2, 3], [1, 2], [4, 5]]], [[[0, 2], [2, 3], [1, 2], [4, 6]]]])
-    ws = W.warm_sets(cfg.scaled(C=3), prof)
+    ws = warm_from_profile(prof, 4, 8, 3)
     assert ws[0].tolist() == [0, 1, 2]
     assert ws[3].tolist() == [4, 5, 6]
 

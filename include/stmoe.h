@@ -209,6 +209,23 @@ int moe_expert_ffn(const void* x, const int32_t* topk_idx, const float* topk_w, 
                    const void* const* shared_ptrs, int n_shared, float* y, void* ws,
                    size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * expert FFN as moe_expert_ffn, with the workspace taken from a 16 MiB
+ * scratch array that the library holds on each GPU it runs on (until the
+ * process ends) instead of a caller buffer.  It allocates nothing and calls
+ * no allocating routine.  Shapes whose moe_expert_ffn_workspace_bytes exceeds
+ * 16 MiB (16777216 bytes) return STMOE_ENOMEM before any device work; every
+ * configuration named in this library's documentation fits (the largest,
+ * batch 16 x top-8 of 128 experts, hidden 4096, intermediate 1536, needs
+ * 14.7 MB).  All calls on one GPU share its scratch array: calls that overlap
+ * in time on that GPU (different streams, different threads) race and must
+ * be serialised by the caller; the array keeps the last call's contents and
+ * needs no initial contents.  Arguments as moe_expert_ffn. */
+int moe_expert_ffn_noalloc(const void* x, const int32_t* topk_idx, const float* topk_w, int B, int K,
+                           int H, int I, int E, int dtype, const void* const* expert_ptrs,
+                           const void* const* shared_ptrs, int n_shared, float* y, void* stream);
+
 /* ------------------------------------------------------------------------
  * Expert cache policy (host only, no HIP calls): per-layer partition of C
  * slots, least recently used with protection of the current set.

@@ -32,10 +32,16 @@
 // Every kernel rebuilds the slot plan (distinct selected experts ascending,
 // token masks) from topk_idx/topk_w in LDS: no host round trip, no planning
 // launch.
+#include <mutex>
 #include <type_traits>
 
 #include "common.h"
 #include "gating_dev.h"
+
+// Workspace of moe_expert_ffn_noalloc: one copy per GPU, held until the
+// process ends.  In host code this name is a stand-in, not a device address;
+// the device address comes from hipGetSymbolAddress (see noalloc_scratch).
+static __device__ __align__(256) unsigned char scratch[size_t(16) << 20];
 
 namespace stmoe {
 namespace {
@@ -1548,4 +1554,57 @@ extern "C" int moe_expert_ffn(const void* x, const int32_t* topk_idx, const floa
                 "x must be 16-byte and ws 256-byte aligned");
     return ffn_launch(x, topk_idx, topk_w, B, K, H, I, E, dtype, expert_ptrs, shared_ptrs, n_shared, y,
                       ws, as_stream(stream), nullptr, nullptr, nullptr, 0, nullptr, 0);
+}
+
+namespace {
+
+constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];      // device address of `scratch` per device (null until resolved)
+
+// The current device's address of `scratch`, resolved once per device with
+// that device current.
+int noalloc_scratch(void** out) {
+    int dev = -1;
+    STMOE_HIP(hipGetDevice(&dev));
+    STMOE_CHECK(dev >= 0 && dev < kMaxDevices, "device ordinal beyond the library's table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* p = nullptr;
+        STMOE_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        STMOE_CHECK(p != nullptr, "hipGetSymbolAddress returned no address");
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return STMOE_OK;
+}
+
+}  // namespace
+
+extern "C" int moe_expert_ffn_noalloc(const void* x, const int32_t* topk_idx, const float* topk_w, int B,
+                                      int K, int H, int I, int E, int dtype, const void* const* expert_ptrs,
+                                      const void* const* shared_ptrs, int n_shared, float* y, void* stream) {
+    clear_error();
+    STMOE_CHECK(x && topk_idx && topk_w && expert_ptrs && y, "null pointer");
+    STMOE_CHECK(B >= 1 && B <= kMaxB, "B must be in [1, 16]");
+    STMOE_CHECK(E >= 1 && E <= kMaxE, "E must be in [1, 256]");
+    STMOE_CHECK(K >= 1 && K <= E && K <= kMaxK, "K must be in [1, min(E, 16)]");
+    STMOE_CHECK(H >= 8 && H % 8 == 0 && H <= kMaxH, "H must be a multiple of 8 in [8, 16384]");
+    STMOE_CHECK(I >= 8 && I % 8 == 0, "I must be a positive multiple of 8");
+    STMOE_CHECK(n_shared >= 0 && n_shared <= kMaxShared, "n_shared must be in [0, 8]");
+    STMOE_CHECK(n_shared == 0 || shared_ptrs, "shared_ptrs is required when n_shared > 0");
+    STMOE_CHECK(dtype == STMOE_BF16 || dtype == STMOE_F32, "dtype must be STMOE_BF16 or STMOE_F32");
+    const size_t need = moe_expert_ffn_workspace_bytes(B, K, E, H, I, n_shared, dtype);
+    if (need > kNoAllocScratchBytes) {
+        set_error("moe_expert_ffn_noalloc: this shape needs " + std::to_string(need) +
+                  " bytes of workspace; the library's scratch holds " + std::to_string(kNoAllocScratchBytes) +
+                  " (use moe_expert_ffn with a caller workspace)");
+        return STMOE_ENOMEM;
+    }
+    STMOE_CHECK((reinterpret_cast<uintptr_t>(x) & 15) == 0, "x must be 16-byte aligned");
+    void* ws = nullptr;
+    if (int rc = noalloc_scratch(&ws)) return rc;
+    return ffn_launch(x, topk_idx, topk_w, B, K, H, I, E, dtype, expert_ptrs, shared_ptrs, n_shared, y, ws,
+                      as_stream(stream), nullptr, nullptr, nullptr, 0, nullptr, 0);
 }

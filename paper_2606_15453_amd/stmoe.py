@@ -94,6 +94,7 @@ _SIGS = {
     "moe_pack_expert": (i32, [vp, vp, vp, i32, i32, i32, vp]),
     "moe_expert_ffn_workspace_bytes": (sz, [i32, i32, i32, i32, i32, i32, i32]),
     "moe_expert_ffn": (i32, [vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp, sz, vp]),
+    "moe_expert_ffn_noalloc": (i32, [vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp]),
     "expert_cache_warm_sets": (i32, [vp, i32, i32, i32, i32, i32, i32, vp]),
     "stmoe_policy_create": (i32, [i32, i32, i32, vp, P(vp)]),
     "stmoe_policy_destroy": (i32, [vp]),
@@ -311,6 +312,14 @@ def expert_ffn(x, idx, w, H, I, E, dtype, expert_ptrs, y, ws, shared_ptrs=None, 
     B, K = idx.shape
     _call("moe_expert_ffn", _p(x), _p(idx), _p(w), B, K, H, I, E, dtype, _p(expert_ptrs),
           _p(shared_ptrs), n_shared, _p(y), _p(ws), ws.numel() * ws.element_size(), _s(stream))
+
+
+def expert_ffn_noalloc(x, idx, w, H, I, E, dtype, expert_ptrs, y, shared_ptrs=None, n_shared=0,
+                       stream=None):
+    """moe_expert_ffn_noalloc: the expert FFN on the library's per-GPU scratch (no workspace)."""
+    B, K = idx.shape
+    _call("moe_expert_ffn_noalloc", _p(x), _p(idx), _p(w), B, K, H, I, E, dtype, _p(expert_ptrs),
+          _p(shared_ptrs), n_shared, _p(y), _s(stream))
 
 
 # ------------------------------------------------------------- cache policy

@@ -655,6 +655,16 @@ def hbm_resident(wl, steps, warmup):
                 host_issue_us_per_layer=host_us, stages_us=stages)
 
 
+#: host-to-HBM copy rate (GB/s): the latest on-demand run's copied bytes over its time
+LINK_GBPS = [55.0]
+
+
+def attn_window_s(attn):
+    """Seconds per layer of the decode-attention stand-in (kv buffer, bytes, out): its bytes
+    at the HBM streaming rate."""
+    return attn[1] / (6.0e12)
+
+
 def expert_pool(wl, pinned_gb, tier):
     """The backing pool the capped cache copies from: pinned host memory over
     PCIe ("host"), or the HBM-resident stack itself ("hbm", copies device to
@@ -697,16 +707,20 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
     blob = cfg.blob_bytes
-    name, mode, min_score, max_pf, online, after_demand, device, staged = variant
+    name, mode, min_score, max_pf, online, after_demand, device, staged, head = variant
     n_stage = staging_slots(cfg, C)
     demand, side = streams
+    if head < 0:
+        # the layer's compute window (routing, FFN, attention) at the link's rate
+        window_s = resident_ms_per_token / cfg.L * 1e-3 + (attn_window_s(attn) if attn else 0.0)
+        head = min(blob, max(1 << 16, int(LINK_GBPS[0] * 1e9 * window_s) // 4096 * 4096))
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
     cache = S.ExpertCache(cfg.L, cfg.E, C, blob, n_stage, arena, ptrs, demand, side)
     cache.warm(W_warm(wl, C))
     cache.set_prefetch_order(after_demand)
     cache.set_device_policy(device)
     if staged:
-        cache.set_staged_prefetch(staged)
+        cache.set_staged_prefetch(staged, head)
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(wl.prof)
     ctx = make_ctx(wl, pred, cache)
@@ -733,6 +747,7 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
     st = pred.stats()
     copies = cst["demand"] + cst["overflow"] + cst["prefetch"]
     rec = dict(tokens=n_tokens, seconds=round(dt, 4), prefetch_min_score=min_score, staged_per_layer=staged,
+               staged_head_bytes=(head if staged and not device else None),
                prefetch_max_per_layer=max_pf, online_update=bool(online),
                prefetch_after_demand=bool(after_demand), device_decisions=bool(device),
                tokens_per_s=round(cfg.B * n_tokens / dt, 3),
@@ -747,6 +762,8 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
         rec["recall_layer0"] = round(float(st[0, 0] / max(st[0, 1], 1)), 4)
         rec["precision"] = round(float(st[:, 0].sum() / max(st[:, 2].sum(), 1)), 4)
         rec["mean_predicted_per_row"] = round(float(st[:, 2].sum() / max(st[:, 1].sum() / cfg.K, 1)), 3)
+    if mode == S.MODE_ON_DEMAND and not device and copies > 0:
+        LINK_GBPS[0] = rec["h2d_gbps"]
     log(f"offload C={C} {name}: {rec['tokens_per_s']} tok/s, {rec['ms_per_token']} ms/token, cache {cst}")
     ctx.close()
     pred.close()
@@ -765,19 +782,23 @@ def W_warm(wl, C):
 def offload_variants(cfg):
     from paper_2606_15453_amd import stmoe as S
     # (name, mode, min score, max prefetches per layer, online update, prefetch after the
-    #  missed loads, device decisions, staged prefetches per layer (0: into evicted slots))
-    return [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 0, 0),
-            ("st_moe", S.MODE_STMOE, 2, cfg.C, 1, 0, 0, 0),
-            ("st_moe_after_demand", S.MODE_STMOE, 2, cfg.C, 1, 1, 0, 0),
-            ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K, 1, 0, 0, 0),
-            ("st_moe_score4_maxK_after_demand", S.MODE_STMOE, 4, cfg.K, 1, 1, 0, 0),
-            ("ht_only", S.MODE_HT_ONLY, 2, cfg.C, 1, 0, 0, 0),
-            ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C, 1, 0, 0, 0),
-            ("on_demand_device", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 1, 0),
-            ("st_moe_device", S.MODE_STMOE, 2, cfg.C, 1, 0, 1, 0),
-            ("st_moe_score4_maxK_after_demand_device", S.MODE_STMOE, 4, cfg.K, 1, 1, 1, 0),
-            ("st_moe_staged", S.MODE_STMOE, 2, cfg.C, 1, 1, 1, STAGED_PER_LAYER(cfg)),
-            ("st_moe_staged1", S.MODE_STMOE, 2, cfg.C, 1, 1, 1, 1)]
+    #  missed loads, device decisions, staged prefetches per layer (0: into evicted slots),
+    #  bytes of a staged expert copied up front with host decisions (-1: the layer's
+    #  compute window at the link's rate; 0: all of it))
+    n_st = STAGED_PER_LAYER(cfg)
+    return [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 0, 0, 0),
+            ("st_moe", S.MODE_STMOE, 2, cfg.C, 1, 0, 0, 0, 0),
+            ("st_moe_after_demand", S.MODE_STMOE, 2, cfg.C, 1, 1, 0, 0, 0),
+            ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K, 1, 0, 0, 0, 0),
+            ("st_moe_score4_maxK_after_demand", S.MODE_STMOE, 4, cfg.K, 1, 1, 0, 0, 0),
+            ("ht_only", S.MODE_HT_ONLY, 2, cfg.C, 1, 0, 0, 0, 0),
+            ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C, 1, 0, 0, 0, 0),
+            ("st_moe_staged_host", S.MODE_STMOE, 2, cfg.C, 1, 1, 0, n_st, -1),
+            ("st_moe_staged_host_full", S.MODE_STMOE, 2, cfg.C, 1, 1, 0, n_st, 0),
+            ("on_demand_device", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 1, 0, 0),
+            ("st_moe_device", S.MODE_STMOE, 2, cfg.C, 1, 0, 1, 0, 0),
+            ("st_moe_score4_maxK_after_demand_device", S.MODE_STMOE, 4, cfg.K, 1, 1, 1, 0, 0),
+            ("st_moe_staged_device", S.MODE_STMOE, 2, cfg.C, 1, 1, 1, n_st, 0)]
 
 
 def STAGED_PER_LAYER(cfg):
@@ -788,7 +809,7 @@ def STAGED_PER_LAYER(cfg):
 def staging_slots(cfg, C):
     """Staging slots of the cache arena: the host path's overflow ring, and two
     sets of staged prefetches."""
-    return max(0, min(cfg.B * cfg.K, cfg.E) - C, 2 * STAGED_PER_LAYER(cfg))
+    return max(0, min(cfg.B * cfg.K, cfg.E) - C) + 2 * STAGED_PER_LAYER(cfg)
 
 
 def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
@@ -861,7 +882,7 @@ def attention_sweep(wl, key, n_tokens, resident_ms_per_token, pinned_gb, context
         recs = {}
         for v in offload_variants(cfg):
             if v[0] not in ("on_demand", "st_moe", "st_moe_score4_maxK_after_demand", "on_demand_device",
-                            "st_moe_score4_maxK_after_demand_device", "st_moe_staged", "st_moe_staged1"):
+                            "st_moe_staged_host", "st_moe_staged_host_full", "st_moe_staged_device"):
                 continue
             recs[v[0]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, base_ms, attn)
         od = recs["on_demand"]["stall_ms_per_token"]
@@ -891,9 +912,9 @@ def offload_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, budgets):
     streams = (torch.cuda.Stream(), torch.cuda.Stream())
     rows = []
     for C in budgets:
-        variants = [(n, m, ms, (C if mp == cfg.C else mp), on, ad, dv, sg)
-                    for n, m, ms, mp, on, ad, dv, sg in offload_variants(cfg)]
-        variants.insert(3, ("st_moe_frozen_cct", S.MODE_STMOE, 2, C, 0, 0, 0, 0))
+        variants = [(n, m, ms, (C if mp == cfg.C else mp), on, ad, dv, sg, hd)
+                    for n, m, ms, mp, on, ad, dv, sg, hd in offload_variants(cfg)]
+        variants.insert(3, ("st_moe_frozen_cct", S.MODE_STMOE, 2, C, 0, 0, 0, 0, 0))
         base = None
         for v in variants:
             rec = offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)

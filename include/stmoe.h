@@ -318,24 +318,30 @@ int expert_cache_set_prefetch_order(expert_cache* c, int after_demand);
  * expert_cache_stats reads the device counters.  on = 0 moves the state
  * back to the host policy.  [sync] */
 int expert_cache_set_device_policy(expert_cache* c, int on);
-/* Staged prefetch (device decisions only; Section 4.1 prefetches predicted
- * experts, Section 4.3.4 overlaps the transfer with computation).  n > 0:
- * instead of evicting slots, the next layer's admitted predicted experts
- * that are not resident (at most n, ranked order) are copied into spare
- * staging blocks of the arena (2n of the n_stage staging slots: two sets
- * alternate between consecutive layers) after the layer's missed loads.  At
- * the next layer's decisions a staged expert that was selected is used from
- * its block: when it takes a slot (the slot the missed load would take) the
- * two blocks swap places, with no copy; otherwise the FFN reads the staging
- * block.  Staged experts that were not selected are cancelled: their copy
- * stops at its next check.  Residency and the slots' contents evolve exactly
- * as with on-demand loading; counts: prefetch = staged copies issued, useful
- * = staged experts selected, wasted = cancelled, demand and overflow = the
- * other misses.  n = 0 returns to prefetching into slots.  Once staged
- * prefetches have run, switching device decisions off returns STMOE_ESTATE
- * (slots may live in other arena blocks).  STMOE_ESTATE without device
- * decisions; STMOE_EINVAL if 2n > n_stage.  [sync] */
-int expert_cache_set_staged_prefetch(expert_cache* c, int n_per_layer);
+/* Staged prefetch (Section 4.1 prefetches predicted experts, Section 4.3.4
+ * overlaps the transfer with computation).  n > 0: instead of evicting
+ * slots, the next layer's admitted predicted experts that are not resident
+ * (at most n, ranked order) are copied into spare staging blocks of the
+ * arena (2n of the n_stage staging slots: two sets alternate between
+ * consecutive layers) once the layer's missed loads are in.  At the next
+ * layer's decisions a staged expert that was selected is used from its
+ * block: when it takes a slot (the slot the missed load would take) the two
+ * blocks swap places, with no copy; otherwise the FFN reads the staging
+ * block.  Residency evolves exactly as with on-demand loading; counts:
+ * prefetch = staged experts, useful = staged experts selected, wasted = the
+ * others, demand and overflow = the other misses.
+ *   Device decisions: the staged copy kernel stops an unselected copy at its
+ *   next check once the next layer's decisions cancel it (head_bytes unused).
+ *   Host decisions: the first head_bytes of each staged expert are copied
+ *   (hipMemcpyAsync on the side stream) when it is staged, the rest only once
+ *   the next layer selects it; head_bytes = 0 or >= the blob copies it whole.
+ *   The remaining overflow ring is n_stage - 2n slots.
+ * n = 0 returns to prefetching into slots.  Once staged prefetches have moved
+ * slots to other arena blocks, switching between host and device decisions
+ * returns STMOE_ESTATE (and, with host decisions, so does changing n until
+ * expert_cache_warm reloads the cache).  STMOE_EINVAL if 2n > n_stage.
+ * [sync] */
+int expert_cache_set_staged_prefetch(expert_cache* c, int n_per_layer, size_t head_bytes);
 /* Make `needed` (host, n distinct experts) resident for a kernel on
  * `compute`: demand copies on the demand stream, `compute` waits for every
  * copy it needs; dev_table_out (host [E]) receives the device blob pointer

@@ -44,9 +44,16 @@ int device_cache_stats(DeviceCache* d, stmoe_cache_stats* st);
 // (table [E]).
 // demand: the missed experts' copies.  prefetch: the copies for `next` on
 // the side stream, after everything enqueued on `s` so far.
+// Stamps are read on the device: *tok * L + stamp_add (tok: device int64).
 int device_cache_decide(DeviceCache* d, int layer, int next, const int32_t* idx, int BK,
                         const int32_t* ranked, const int32_t* n_ranked, const uint8_t* max_score,
-                        int pf_min, int pf_max, int64_t stamp, const void** table, hipStream_t s);
+                        int pf_min, int pf_max, const int64_t* tok, int64_t stamp_add, const void** table,
+                        hipStream_t s);
+// `s` waits for all work queued so far on the side stream.
+int device_cache_join(DeviceCache* d, hipStream_t s);
+// Forget the prefetch completion events (all side work is known to be
+// ordered before what follows: a joined graph replay or capture).
+void device_cache_forget_waits(DeviceCache* d);
 int device_cache_demand(DeviceCache* d, int layer, hipStream_t s);
 int device_cache_prefetch(DeviceCache* d, int next, hipStream_t s);
 

@@ -18,6 +18,7 @@
 // kernel stops at its next check.  Residency therefore evolves exactly as
 // with on-demand loading; the staged copies only move bytes earlier, while
 // the link would otherwise idle during the layer's computation.
+#include <algorithm>
 #include <vector>
 
 #include "cache_device.h"
@@ -39,7 +40,9 @@ constexpr int kStageMax = kMaxE;  // staging positions per parity
 struct DecideArgs {
     int L, E, C, layer, next, BK, pf_min, pf_max;
     int demand_on;               // 0: only the prefetch decisions (no selection yet)
-    int64_t stamp;
+    const int64_t* tok;          // device: the decode token (stamps are tok * L + stamp_add)
+    int64_t stamp_add;
+    int64_t stamp;               // set in the kernel
     int32_t* slot;
     int64_t* last;
     int32_t* where;
@@ -134,6 +137,7 @@ __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
     const int t = threadIdx.x;
     const int l = a.layer;
     const bool staged = a.ns > 0;
+    a.stamp = *a.tok * a.L + a.stamp_add;
     // the staged list consumed here is the last one issued, if it targets this layer
     const int cur = staged ? a.ctl[0] : 0;
     const int n_cons = staged && a.demand_on && a.ctl[1 + cur] == l ? a.ctl[3 + cur] : 0;
@@ -320,8 +324,9 @@ struct DeviceCache {
     int n_blocks = 0;                // arena blocks: L*C slots + staging
     int ns = 0;                      // staged positions per parity (0: prefetch into slots)
     bool permuted = false;           // staged prefetches have swapped slot blocks
-    // ordering: decisions made (compute stream), prefetch of layer l done (side)
-    hipEvent_t ev_decided = nullptr;
+    // ordering: decisions made (compute stream), prefetch of layer l done (side),
+    // all side work joined back (graph capture and replay)
+    hipEvent_t ev_decided = nullptr, ev_join = nullptr;
     std::vector<hipEvent_t> pf_done;
     std::vector<char> pf_set;
 };
@@ -332,6 +337,7 @@ void free_dc(DeviceCache* d) {
     if (!d) return;
     if (d->side) (void)hipStreamSynchronize(d->side);
     if (d->ev_decided) (void)hipEventDestroy(d->ev_decided);
+    if (d->ev_join) (void)hipEventDestroy(d->ev_join);
     for (auto e : d->pf_done)
         if (e) (void)hipEventDestroy(e);
     delete d;       // the state lives in the cache's arena
@@ -413,6 +419,7 @@ int device_cache_create(const PolicyState& ps, char* arena, size_t blob, int n_s
     for (size_t i = 0; i < LC; ++i) blk[i] = int32_t(i);
     const int32_t ctl[5] = {0, -1, -1, 0, 0};
     hipError_t e = hipEventCreateWithFlags(&d->ev_decided, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&d->ev_join, hipEventDisableTiming);
     d->pf_done.assign(ps.L, nullptr);
     d->pf_set.assign(ps.L, 0);
     for (int l = 0; e == hipSuccess && l < ps.L; ++l) e = hipEventCreateWithFlags(&d->pf_done[l], hipEventDisableTiming);
@@ -493,9 +500,18 @@ int device_cache_stats(DeviceCache* d, stmoe_cache_stats* out) {
     return STMOE_OK;
 }
 
+int device_cache_join(DeviceCache* d, hipStream_t s) {
+    STMOE_HIP(hipEventRecord(d->ev_join, d->side));
+    STMOE_HIP(hipStreamWaitEvent(s, d->ev_join, 0));
+    return STMOE_OK;
+}
+
+void device_cache_forget_waits(DeviceCache* d) { std::fill(d->pf_set.begin(), d->pf_set.end(), char(0)); }
+
 int device_cache_decide(DeviceCache* d, int layer, int next, const int32_t* idx, int BK,
                         const int32_t* ranked, const int32_t* n_ranked, const uint8_t* max_score,
-                        int pf_min, int pf_max, int64_t stamp, const void** table, hipStream_t s) {
+                        int pf_min, int pf_max, const int64_t* tok, int64_t stamp_add, const void** table,
+                        hipStream_t s) {
     STMOE_CHECK(layer >= 0 && layer < d->L && next >= 0 && next < d->L && BK >= 0 && BK <= kT,
                 "bad layer or selection size");
     STMOE_CHECK(BK > 0 || ranked, "nothing to decide");
@@ -503,7 +519,7 @@ int device_cache_decide(DeviceCache* d, int layer, int next, const int32_t* idx,
     if (ranked && d->pf_set[next]) STMOE_HIP(hipStreamWaitEvent(s, d->pf_done[next], 0));
     DecideArgs a{};
     a.L = d->L; a.E = d->E; a.C = d->C; a.layer = layer; a.next = next; a.BK = BK;
-    a.pf_min = pf_min; a.pf_max = pf_max; a.stamp = stamp; a.demand_on = BK > 0;
+    a.pf_min = pf_min; a.pf_max = pf_max; a.tok = tok; a.stamp_add = stamp_add; a.demand_on = BK > 0;
     a.slot = d->slot; a.last = d->last; a.where = d->where; a.pending = d->pending; a.stats = d->stats;
     a.idx = idx; a.ranked = ranked; a.n_ranked = n_ranked; a.max_score = max_score;
     a.host = d->host; a.arena = d->arena; a.blob = d->blob; a.table = table;

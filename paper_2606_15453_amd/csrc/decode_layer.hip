@@ -51,6 +51,11 @@ __global__ void set_table_kernel(PtrTable t, const void** dst, int E) {
     for (int e = threadIdx.x; e < E; e += blockDim.x) dst[e] = t.p[e];
 }
 
+// The device copy of the decode token that the cache's decisions stamp with
+// (a replayed graph advances it by one per token).
+__global__ void set_token_kernel(int64_t* tok, int64_t v) { *tok = v; }
+__global__ void next_token_kernel(int64_t* tok) { *tok += 1; }
+
 }  // namespace
 }  // namespace stmoe
 
@@ -93,6 +98,9 @@ struct moe_ctx {
     const void** tables = nullptr;         // [L][E] device blob pointers
     const void** shared = nullptr;         // [L][n_shared] device blob pointers
     int32_t* rec = nullptr;                // pinned host: idx [B][K], ranked [E], n_ranked, max scores [E] (uint8)
+    int64_t* tok = nullptr;                // device: decode token of the cache's stamps
+    int64_t tok_value = -1;                // what *tok holds once the queued work has run
+    bool capturing = false;                // a token's layers are being captured into a graph
     int pf_min_score = 2, pf_max = 1 << 30;
     bool want_ranked = false;              // a report asks for the side path's ranked prediction
     int online = 1;                        // Algorithm 3's CCT update on (1) or frozen CCTs (0)
@@ -159,7 +167,7 @@ void free_ctx(moe_ctx* c) {
 
 // Layout of a context's device workspace (every region 256-byte aligned).
 struct CtxLayout {
-    size_t idx, w, ranked, route_ws, ffn_ws, tables, shared, n_experts, seq_args, x_stage, y_stage, total;
+    size_t idx, w, ranked, route_ws, ffn_ws, tables, shared, n_experts, seq_args, x_stage, y_stage, tok, total;
     size_t route_ws_bytes, ffn_ws_bytes, seq_bytes;
 };
 
@@ -183,6 +191,7 @@ CtxLayout ctx_layout(const moe_model_desc* d) {
     y.seq_args = take(2 * y.seq_bytes);
     y.x_stage = take(LBH * esz);
     y.y_stage = take(LBH * sizeof(float));
+    y.tok = take(sizeof(int64_t));
     y.total = off;
     return y;
 }
@@ -320,6 +329,7 @@ extern "C" int moe_ctx_create(const moe_model_desc* d, stmoe_predictor* pred, ex
     c->seq_args[1] = base + y.seq_args + y.seq_bytes;
     c->x_stage = base + y.x_stage;
     c->y_stage = reinterpret_cast<float*>(base + y.y_stage);
+    c->tok = reinterpret_cast<int64_t*>(base + y.tok);
     hipError_t e = hipHostMalloc(&c->rec, size_t(c->B * c->K) * sizeof(int32_t) + ranked_bytes(c->E));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->rec_ev, hipEventDisableTiming);
     if (e == hipSuccess && !cache && pred) {
@@ -389,6 +399,14 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
     int32_t* idx_l = c->idx + pbase + size_t(layer) * B * K;
     float* w_l = c->w + pbase + size_t(layer) * B * K;
     c->last_par = c->cur_par;
+    // device decisions stamp with the token held on the device (a graph
+    // replay advances it); eager calls set it when it differs
+    DeviceCache* dcache = c->cache ? expert_cache_device(c->cache) : nullptr;
+    if (dcache && !c->capturing && c->tok_value != token) {
+        hipLaunchKernelGGL(set_token_kernel, dim3(1), dim3(1), 0, c->s, c->tok, int64_t(token));
+        STMOE_LAUNCHED();
+        c->tok_value = token;
+    }
 
     // first call: layer 0's prediction comes from the profiled HT[0]
     if (!c->started) {
@@ -400,7 +418,7 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
             if (DeviceCache* dc = c->cache ? expert_cache_device(c->cache) : nullptr) {
                 if (int rc = device_cache_decide(dc, 0, 0, nullptr, 0, c->ranked, c->ranked + E,
                                                  max_scores(c->ranked, E), c->pf_min_score, c->pf_max,
-                                                 stamp - 1, c->tables, c->s))
+                                                 c->tok, layer, c->tables, c->s))
                     return rc;
                 if (int rc = device_cache_prefetch(dc, 0, c->s)) return rc;
             } else if (c->cache) {
@@ -479,7 +497,7 @@ int decode_layer(moe_ctx* c, int token, int layer, const void* x, float* y, int 
         // device decisions: no host wait; the FFN reads the table they write
         if (int rc = device_cache_decide(dc, layer, (layer + 1) % L, idx_l, B * K, use ? c->ranked : nullptr,
                                          c->ranked + E, max_scores(c->ranked, E), c->pf_min_score, c->pf_max,
-                                         stamp, c->tables + size_t(layer) * E, c->s))
+                                         c->tok, layer + 1, c->tables + size_t(layer) * E, c->s))
             return rc;
         const bool after_demand = expert_cache_after_demand(c->cache);
         if (pf_now && !after_demand)
@@ -616,17 +634,34 @@ int capture_token(moe_ctx* c, int token, int mode) {
     c->graph = nullptr;
     hipStream_t user = c->s;
     c->s = c->gs;
+    DeviceCache* dc = c->cache ? expert_cache_device(c->cache) : nullptr;
+    if (dc) {
+        // the graph starts from a state with every earlier copy done: the
+        // graph stream waits for the cache's side work, and the capture does
+        // not refer to completion events recorded outside it
+        if (int rc = device_cache_join(dc, c->gs)) { c->s = user; return rc; }
+        device_cache_forget_waits(dc);
+    }
     STMOE_HIP(hipStreamBeginCapture(c->gs, hipStreamCaptureModeThreadLocal));
+    c->capturing = true;
     int rc = STMOE_OK;
     for (int l = 0; l < c->L && rc == STMOE_OK; ++l) {
         const char* x = reinterpret_cast<const char*>(c->x_stage) + size_t(l) * c->B * c->H * c->esz;
         rc = decode_layer(c, token, l, x, c->y_stage + size_t(l) * c->B * c->H, mode, false);
     }
     if (rc == STMOE_OK) rc = join_side(c);      // the side branch rejoins inside the graph
+    if (rc == STMOE_OK && dc) {
+        // the next replay stamps the next token; the prefetch copies rejoin
+        hipLaunchKernelGGL(next_token_kernel, dim3(1), dim3(1), 0, c->gs, c->tok);
+        if (hipGetLastError() != hipSuccess) rc = STMOE_EHIP;
+        if (rc == STMOE_OK) rc = device_cache_join(dc, c->gs);
+    }
+    c->capturing = false;
     hipGraph_t g = nullptr;
     const hipError_t e = hipStreamEndCapture(c->gs, &g);
     c->s = user;
     c->side_pending = false;
+    if (dc) device_cache_forget_waits(dc);     // events recorded in the capture are graph nodes
     if (rc != STMOE_OK || e != hipSuccess) {
         if (g) (void)hipGraphDestroy(g);
         if (rc == STMOE_OK) set_error(std::string("moe_decode_token: capture: ") + hipGetErrorString(e));
@@ -647,11 +682,26 @@ int capture_token(moe_ctx* c, int token, int mode) {
 int decode_token_graph(moe_ctx* c, int token, const void* xs, float* ys, int mode) {
     if (int rc = join_side(c)) return rc;
     c->cur_par = 0;
+    DeviceCache* dc = c->cache ? expert_cache_device(c->cache) : nullptr;
+    if (c->cache && !dc) {
+        set_error("moe_decode_token: graph replay with a cache needs device-side decisions");
+        return STMOE_ESTATE;
+    }
     if (!c->graph_exec || c->graph_mode != mode)
         if (int rc = capture_token(c, token, mode)) return rc;
     const size_t n = size_t(c->L) * c->B * c->H;
     STMOE_HIP(hipEventRecord(c->ev_in, c->s));
     STMOE_HIP(hipStreamWaitEvent(c->gs, c->ev_in, 0));
+    if (dc) {
+        // earlier eager work of the cache's side stream, and the token stamp
+        if (int rc = device_cache_join(dc, c->gs)) return rc;
+        device_cache_forget_waits(dc);
+        if (c->tok_value != token) {
+            hipLaunchKernelGGL(set_token_kernel, dim3(1), dim3(1), 0, c->gs, c->tok, int64_t(token));
+            STMOE_LAUNCHED();
+        }
+        c->tok_value = token + 1;      // the graph advances the device token
+    }
     if (xs != c->x_stage)
         STMOE_HIP(hipMemcpyAsync(c->x_stage, xs, n * c->esz, hipMemcpyDeviceToDevice, c->gs));
     STMOE_HIP(hipGraphLaunch(c->graph_exec, c->gs));
@@ -735,7 +785,8 @@ extern "C" int moe_ctx_set_predictor_batch(moe_ctx* c, int on) {
 extern "C" int moe_ctx_set_graph(moe_ctx* c, int on) {
     clear_error();
     STMOE_CHECK(c, "null ctx");
-    STMOE_CHECK(!on || !c->cache, "graph replay needs a context without a cache");
+    STMOE_CHECK(!on || !c->cache || expert_cache_device(c->cache),
+                "graph replay with a cache needs device-side decisions");
     STMOE_CHECK(!on || !c->pred_batch, "per-token predictor launches and graph replay exclude each other");
     STMOE_HIP(hipStreamSynchronize(c->s));
     if (c->gs) STMOE_HIP(hipStreamSynchronize(c->gs));

@@ -215,6 +215,11 @@ extern "C" int stmoe_policy_stats(const stmoe_policy* p, stmoe_cache_stats* out)
 // device-backed cache
 // ---------------------------------------------------------------------------
 
+// The arena holds L*C + n_stage blocks of one blob each.  Slot s of layer l
+// lives in block blk[l*C + s] (block l*C + s until staged prefetches swap
+// blocks).  The last 2*ns staging blocks hold staged prefetches (two sets
+// that alternate between consecutive layers); the others form the ring that
+// overflow experts stream through.  Events are per block.
 struct expert_cache {
     stmoe_policy* pol = nullptr;
     int L = 0, E = 0, C = 0, n_stage = 0;
@@ -222,16 +227,26 @@ struct expert_cache {
     char* arena = nullptr;
     std::vector<const void*> host;       // [L*E]
     hipStream_t demand = nullptr, side = nullptr;
-    std::vector<hipEvent_t> loaded, released;   // [L*C + n_stage]
+    std::vector<hipEvent_t> loaded, released;   // [L*C + n_stage] per block
     std::vector<char> loaded_set, released_set;
+    std::vector<int> blk;                // [L*C] block of each slot
     int stage_next = 0;
-    std::vector<std::vector<int>> held;  // per layer: slots (global ids) read by the last acquire
+    std::vector<std::vector<int>> held;  // per layer: blocks read by the last acquire
     hipEvent_t demand_done = nullptr;    // after the last acquire's demand copies
     bool demand_done_set = false;
     int after_demand = 0;                // prefetch copies wait for demand_done
     stmoe::DeviceCache* dev = nullptr;   // device-side decisions (null: the host decides)
+    // staged prefetch with host decisions: ns positions per set, the first
+    // `head` bytes of a staged expert copied when it is staged, the rest once
+    // the next layer selects it
+    int ns = 0;
+    size_t head = 0;
+    std::vector<int> sblk, sexp;         // [2][ns] block and staged expert of each position
+    int cur = 0, stg_layer[2] = {-1, -1}, stg_n[2] = {0, 0};
+    bool permuted = false;               // some slot lives outside its home block
 
-    char* slot_ptr(int gid) const { return arena + size_t(gid) * blob; }
+    char* block_ptr(int b) const { return arena + size_t(b) * blob; }
+    int ring() const { return n_stage - 2 * ns; }
 };
 
 namespace stmoe {
@@ -261,15 +276,30 @@ PolicyState policy_state(expert_cache* c) {
 namespace stmoe {
 namespace {
 
-// Order a copy into slot `gid` on stream `s` after its previous copy and
-// its last reader, then issue it and record the slot's loaded event.
-int copy_into(expert_cache* c, int gid, const void* src, hipStream_t s) {
-    if (c->loaded_set[gid]) STMOE_HIP(hipStreamWaitEvent(s, c->loaded[gid], 0));
-    if (c->released_set[gid]) STMOE_HIP(hipStreamWaitEvent(s, c->released[gid], 0));
-    STMOE_HIP(hipMemcpyAsync(c->slot_ptr(gid), src, c->blob, hipMemcpyDefault, s));
-    STMOE_HIP(hipEventRecord(c->loaded[gid], s));
-    c->loaded_set[gid] = 1;
+// Order a copy of bytes [off, off + n) of a blob into block `b` on stream
+// `s` after the block's previous copy and its last reader, then issue it and
+// record the block's loaded event.
+int copy_into(expert_cache* c, int b, const void* src, hipStream_t s, size_t off = 0, size_t n = 0) {
+    if (n == 0) n = c->blob - off;
+    if (c->loaded_set[b]) STMOE_HIP(hipStreamWaitEvent(s, c->loaded[b], 0));
+    if (c->released_set[b]) STMOE_HIP(hipStreamWaitEvent(s, c->released[b], 0));
+    STMOE_HIP(hipMemcpyAsync(c->block_ptr(b) + off, static_cast<const char*>(src) + off, n, hipMemcpyDefault, s));
+    STMOE_HIP(hipEventRecord(c->loaded[b], s));
+    c->loaded_set[b] = 1;
     return STMOE_OK;
+}
+
+void reset_blocks(expert_cache* c) {
+    for (size_t i = 0; i < c->blk.size(); ++i) c->blk[i] = int(i);
+    c->sblk.assign(size_t(2) * c->ns, 0);
+    c->sexp.assign(size_t(2) * c->ns, -1);
+    for (int p = 0; p < 2; ++p)
+        for (int j = 0; j < c->ns; ++j) c->sblk[size_t(p) * c->ns + j] = c->L * c->C + c->ring() + p * c->ns + j;
+    c->cur = 0;
+    c->stg_layer[0] = c->stg_layer[1] = -1;
+    c->stg_n[0] = c->stg_n[1] = 0;
+    c->stage_next = 0;
+    c->permuted = false;
 }
 
 }  // namespace
@@ -317,6 +347,8 @@ extern "C" int expert_cache_create(int L, int E, int C, size_t blob_bytes, int n
     c->loaded_set.assign(n, 0);
     c->released_set.assign(n, 0);
     c->held.assign(L, {});
+    c->blk.assign(size_t(L) * C, 0);
+    reset_blocks(c);
     for (size_t i = 0; i < n; ++i) {
         if (hipEventCreateWithFlags(&c->loaded[i], hipEventDisableTiming) != hipSuccess ||
             hipEventCreateWithFlags(&c->released[i], hipEventDisableTiming) != hipSuccess) {
@@ -362,11 +394,12 @@ extern "C" int expert_cache_warm(expert_cache* c, const int32_t* warm) {
     STMOE_HIP(hipStreamSynchronize(c->side));
     stmoe_policy_destroy(c->pol);
     c->pol = np;
+    reset_blocks(c);
     for (int l = 0; l < c->L; ++l)
         for (int s = 0; s < c->C; ++s) {
             const int e = warm[l * c->C + s];
             if (e < 0) continue;
-            STMOE_HIP(hipMemcpyAsync(c->slot_ptr(l * c->C + s), c->host[size_t(l) * c->E + e], c->blob,
+            STMOE_HIP(hipMemcpyAsync(c->block_ptr(c->blk[l * c->C + s]), c->host[size_t(l) * c->E + e], c->blob,
                                      hipMemcpyDefault, c->demand));
         }
     STMOE_HIP(hipStreamSynchronize(c->demand));
@@ -386,13 +419,36 @@ extern "C" int expert_cache_prefetch(expert_cache* c, int layer, const int32_t* 
     }
     STMOE_CHECK(layer >= 0 && layer < c->L, "layer out of range");
     if (int rc = check_list(ranked, n, c->E, true)) return rc;
+    if (c->ns > 0) {
+        // staged: the first ns ranked experts not resident, into the other set
+        // of staging blocks; no slot changes hands.  They take the link only
+        // once the latest missed loads are in.
+        const int nx = c->cur ^ 1;
+        int k = 0;
+        for (int i = 0; i < n && k < c->ns; ++i) {
+            const int f = ranked[i];
+            if (c->pol->where[layer * c->E + f] >= 0) continue;
+            if (k == 0 && c->demand_done_set) STMOE_HIP(hipStreamWaitEvent(c->side, c->demand_done, 0));
+            const int b = c->sblk[size_t(nx) * c->ns + k];
+            c->sexp[size_t(nx) * c->ns + k] = f;
+            const size_t first = c->head > 0 && c->head < c->blob ? c->head : c->blob;
+            if (int rc = copy_into(c, b, c->host[size_t(layer) * c->E + f], c->side, 0, first)) return rc;
+            ++k;
+        }
+        c->stg_layer[nx] = layer;
+        c->stg_n[nx] = k;
+        c->cur = nx;
+        c->pol->st.prefetch += k;
+        (void)stamp;
+        return k;
+    }
     int32_t pairs[2 * kMaxE];
     const int m = policy_prefetch(c->pol, layer, ranked, n, stamp, pairs);
     if (m > 0 && c->after_demand && c->demand_done_set)
         STMOE_HIP(hipStreamWaitEvent(c->side, c->demand_done, 0));
     for (int i = 0; i < m; ++i) {
         const int e = pairs[2 * i], s = pairs[2 * i + 1];
-        if (int rc = copy_into(c, layer * c->C + s, c->host[size_t(layer) * c->E + e], c->side)) return rc;
+        if (int rc = copy_into(c, c->blk[layer * c->C + s], c->host[size_t(layer) * c->E + e], c->side)) return rc;
     }
     return m;
 }
@@ -422,44 +478,75 @@ extern "C" int expert_cache_acquire(expert_cache* c, int layer, const int32_t* n
             evictable += (e < 0 || !keep[e]);
         }
         const int overflow = missing > evictable ? missing - evictable : 0;
-        if (overflow > c->n_stage) {
+        if (overflow > c->ring()) {
             set_error("expert_cache_acquire: more overflow experts than staging slots");
             return STMOE_ECAPACITY;
         }
     }
+    // the staged set issued for this layer (if the last one targets it)
+    std::vector<int> spos(c->E, -1);
+    const int cur = c->cur;
+    const int n_cons = c->ns > 0 && c->stg_layer[cur] == layer ? c->stg_n[cur] : 0;
+    for (int j = 0; j < n_cons; ++j) spos[c->sexp[size_t(cur) * c->ns + j]] = j;
     const int m = policy_acquire(c->pol, layer, needed, n, stamp, pairs, &n_hits);
     auto& held = c->held[layer];
     held.clear();
-    // demand copies and overflow staging
-    std::vector<int> gid_of(c->E, -1);
+    // demand copies, overflow staging and used staged copies
+    std::vector<int> blk_of(c->E, -1);
     for (int i = 0; i < m; ++i) {
         const int e = pairs[2 * i], s = pairs[2 * i + 1];
-        int gid;
-        if (s >= 0) {
-            gid = layer * c->C + s;
-        } else {
-            gid = c->L * c->C + c->stage_next;
-            c->stage_next = (c->stage_next + 1) % c->n_stage;
+        const int j = spos[e];
+        if (j >= 0) {
+            // a staged copy serves this miss: its remaining bytes follow on the
+            // side stream; with a slot, the staging block becomes the slot's
+            int& pos = c->sblk[size_t(cur) * c->ns + j];
+            const int b = pos;
+            if (c->head > 0 && c->head < c->blob)
+                if (int rc = copy_into(c, b, c->host[size_t(layer) * c->E + e], c->side, c->head)) return rc;
+            if (s >= 0) {
+                pos = c->blk[layer * c->C + s];
+                c->blk[layer * c->C + s] = b;
+                c->permuted = true;
+                --c->pol->st.demand;
+            } else {
+                --c->pol->st.overflow;
+            }
+            ++c->pol->st.useful;
+            blk_of[e] = b;
+            continue;
         }
-        if (int rc = copy_into(c, gid, c->host[size_t(layer) * c->E + e], c->demand)) return rc;
-        gid_of[e] = gid;
+        int b;
+        if (s >= 0) {
+            b = c->blk[layer * c->C + s];
+        } else {
+            b = c->L * c->C + c->stage_next;
+            c->stage_next = (c->stage_next + 1) % c->ring();
+        }
+        if (int rc = copy_into(c, b, c->host[size_t(layer) * c->E + e], c->demand)) return rc;
+        blk_of[e] = b;
+    }
+    if (n_cons > 0) {
+        std::vector<char> keep(c->E, 0);
+        for (int i = 0; i < n; ++i) keep[needed[i]] = 1;
+        for (int j = 0; j < n_cons; ++j) c->pol->st.wasted += !keep[c->sexp[size_t(cur) * c->ns + j]];
+        c->stg_layer[cur] = -1;
     }
     if (m > 0) {
         STMOE_HIP(hipEventRecord(c->demand_done, c->demand));
         c->demand_done_set = true;
     }
-    // every needed expert: the compute stream waits for its slot's last copy
+    // every needed expert: the compute stream waits for its block's last copy
     for (int i = 0; i < n; ++i) {
         const int e = needed[i];
         const int s = c->pol->where[layer * c->E + e];
-        const int gid = s >= 0 ? layer * c->C + s : gid_of[e];
-        if (gid < 0) {
-            set_error("expert_cache_acquire: internal error, expert without a slot");
+        const int b = blk_of[e] >= 0 ? blk_of[e] : (s >= 0 ? c->blk[layer * c->C + s] : -1);
+        if (b < 0) {
+            set_error("expert_cache_acquire: internal error, expert without a block");
             return STMOE_ESTATE;
         }
-        dev_table_out[e] = c->slot_ptr(gid);
-        if (c->loaded_set[gid]) STMOE_HIP(hipStreamWaitEvent(cs, c->loaded[gid], 0));
-        held.push_back(gid);
+        dev_table_out[e] = c->block_ptr(b);
+        if (c->loaded_set[b]) STMOE_HIP(hipStreamWaitEvent(cs, c->loaded[b], 0));
+        held.push_back(b);
     }
     return n_hits;
 }
@@ -472,6 +559,11 @@ extern "C" int expert_cache_set_device_policy(expert_cache* c, int on) {
     STMOE_HIP(hipStreamSynchronize(c->demand));
     STMOE_HIP(hipStreamSynchronize(c->side));
     if (on) {
+        if (c->permuted || c->ns > 0) {
+            set_error("expert_cache_set_device_policy: staged prefetches with host decisions are on, or have "
+                      "moved slots to other arena blocks; device decisions cannot take the cache over");
+            return STMOE_ESTATE;
+        }
         for (auto& h : c->held) h.clear();
         return stmoe::device_cache_create(stmoe::policy_state(c), c->arena, c->blob, c->n_stage, c->host.data(),
                                           c->arena + slots_bytes(c->L, c->C, c->blob, c->n_stage), c->side,
@@ -487,16 +579,29 @@ extern "C" int expert_cache_set_device_policy(expert_cache* c, int on) {
     return rc;
 }
 
-extern "C" int expert_cache_set_staged_prefetch(expert_cache* c, int n_per_layer) {
+extern "C" int expert_cache_set_staged_prefetch(expert_cache* c, int n_per_layer, size_t head_bytes) {
     clear_error();
     STMOE_CHECK(c, "null cache");
-    if (!c->dev) {
-        set_error("expert_cache_set_staged_prefetch: needs device-side decisions");
+    STMOE_CHECK(n_per_layer >= 0 && n_per_layer <= kMaxE, "n_per_layer must be in [0, 256]");
+    if (c->dev) {
+        STMOE_CHECK(2 * n_per_layer <= c->n_stage, "n_per_layer must be in [0, n_stage / 2]");
+        return stmoe::device_cache_set_staged(c->dev, n_per_layer);
+    }
+    // host decisions: the overflow ring keeps what the staged sets leave
+    STMOE_CHECK(2 * n_per_layer <= c->n_stage, "n_per_layer must be in [0, n_stage / 2]");
+    if (c->permuted && n_per_layer != c->ns) {
+        set_error("expert_cache_set_staged_prefetch: staged prefetches have moved slots to other arena blocks; "
+                  "reload the cache with expert_cache_warm before changing the staged count");
         return STMOE_ESTATE;
     }
-    STMOE_CHECK(n_per_layer >= 0 && 2 * n_per_layer <= c->n_stage,
-                "n_per_layer must be in [0, n_stage / 2]");
-    return stmoe::device_cache_set_staged(c->dev, n_per_layer);
+    STMOE_HIP(hipStreamSynchronize(c->demand));
+    STMOE_HIP(hipStreamSynchronize(c->side));
+    if (n_per_layer != c->ns) {
+        c->ns = n_per_layer;
+        reset_blocks(c);       // nothing is permuted: slots stay in their home blocks
+    }
+    c->head = head_bytes;
+    return STMOE_OK;
 }
 
 extern "C" int expert_cache_set_prefetch_order(expert_cache* c, int after_demand) {

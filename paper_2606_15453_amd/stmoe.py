@@ -111,7 +111,7 @@ _SIGS = {
     "expert_cache_release": (i32, [vp, i32, vp]),
     "expert_cache_set_prefetch_order": (i32, [vp, i32]),
     "expert_cache_set_device_policy": (i32, [vp, i32]),
-    "expert_cache_set_staged_prefetch": (i32, [vp, i32]),
+    "expert_cache_set_staged_prefetch": (i32, [vp, i32, sz]),
     "expert_cache_stats": (i32, [vp, P(CacheStats)]),
     "moe_ctx_workspace_bytes": (sz, [P(ModelDesc)]),
     "moe_ctx_create": (i32, [P(ModelDesc), vp, vp, vp, vp, sz, P(vp)]),
@@ -420,9 +420,10 @@ class ExpertCache:
     def set_device_policy(self, on):
         _call("expert_cache_set_device_policy", self.h, int(on))
 
-    def set_staged_prefetch(self, n_per_layer):
-        """Prefetch into spare staging blocks (at most n per layer), cancelled when unused."""
-        _call("expert_cache_set_staged_prefetch", self.h, int(n_per_layer))
+    def set_staged_prefetch(self, n_per_layer, head_bytes=0):
+        """Prefetch into spare staging blocks (at most n per layer); unused ones are cancelled
+        (device decisions) or stop after their first head_bytes (host decisions)."""
+        _call("expert_cache_set_staged_prefetch", self.h, int(n_per_layer), int(head_bytes))
 
     def stats(self):
         st = CacheStats()

@@ -85,7 +85,8 @@ def _cumulative_after_layers(cache, L):
 
 def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0, device=0,
              device_until=None, device_pool=False, batch=False, C=None, import_tables=None,
-             admission=None, layerwise=False, attn_bytes=0, reports=None, staged=0):
+             admission=None, layerwise=False, attn_bytes=0, reports=None, staged=0, head=0, graph=False,
+             timing_every=0):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
@@ -105,7 +106,7 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
                 h = st.blobs[l][e] if device_pool else st.blobs[l][e].cpu().pin_memory()
                 keep.append(h)
                 host.append(h.data_ptr())
-        n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - C, 2 * staged)
+        n_stage = max(0, min(cfg.B * cfg.K, cfg.E) - C) + 2 * staged
         arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.E, C, cfg.blob_bytes, n_stage),
                             dtype=torch.uint8, device=DEV)
         demand, side = torch.cuda.Stream(), torch.cuda.Stream()
@@ -115,7 +116,7 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
         cache.set_prefetch_order(after_demand)
         cache.set_device_policy(device)
         if staged:
-            cache.set_staged_prefetch(staged)
+            cache.set_staged_prefetch(staged, head)
         ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
                               [g.data_ptr() for g in st.wg_dev], predictor=pred, cache=cache,
                               shared_ptrs=st.shared_ptrs(), n_shared=cfg.n_shared, renorm=renorm,
@@ -131,6 +132,10 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
         ctx.set_predictor_batch(True)
     if admission is not None:
         ctx.set_prefetch(*admission)
+    if graph:
+        ctx.set_graph(True)
+    if timing_every:
+        ctx.set_timing(timing_every)
     if attn_bytes:
         # decode-attention stand-in: a KV-sized stream on the compute stream before every layer
         kv = torch.zeros(attn_bytes, dtype=torch.uint8, device=DEV)
@@ -596,20 +601,25 @@ def test_admission_knobs_match_oracle(device, min_score, max_per_layer):
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("name,over", CFGS)
-@pytest.mark.parametrize("mode,n_staged,admission,layerwise", [(1, 1, None, False), (1, 4, None, False),
-                                                               (3, 2, None, False), (1, 2, (4, 8), False),
-                                                               (1, 3, None, True)])
-def test_decode_capped_staged_prefetch(name, over, mode, n_staged, admission, layerwise):
-    """Staged prefetch (device decisions): the copy counts equal the oracle's
-    staged cache, the hits equal on-demand loading's (residency is unchanged
-    by staging), and the outputs are bit-identical to the all-resident run,
-    per token and layer by layer with a decode-attention stand-in."""
+@pytest.mark.parametrize("mode,n_staged,admission,layerwise,device,head",
+                         [(1, 1, None, False, 1, 0), (1, 4, None, False, 1, 0), (3, 2, None, False, 1, 0),
+                          (1, 2, (4, 8), False, 1, 0), (1, 3, None, True, 1, 0),
+                          (1, 1, None, False, 0, 0), (1, 4, None, False, 0, 4096), (3, 2, None, False, 0, 1 << 16),
+                          (1, 2, (4, 8), False, 0, 12288), (1, 3, None, True, 0, 65536)])
+def test_decode_capped_staged_prefetch(name, over, mode, n_staged, admission, layerwise, device, head):
+    """Staged prefetch (device decisions with cancelled copy kernels; host
+    decisions with a head copy and the rest on use): the copy counts equal the
+    oracle's staged cache, the hits equal on-demand loading's (residency is
+    unchanged by staging), and the outputs are bit-identical to the
+    all-resident run, per token and layer by layer with a decode-attention
+    stand-in."""
     from paper_2606_15453_amd import workload as W
     cfg = W.CONFIGS[name].scaled(**over)
     st = Stack(cfg)
-    print(f"[staged] {cfg.name} mode={mode} n={n_staged} admission={admission} layerwise={layerwise}", flush=True)
+    print(f"[staged] {cfg.name} mode={mode} n={n_staged} admission={admission} layerwise={layerwise} "
+          f"device={device} head={head}", flush=True)
     _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
-    _, ys, _, cst = _run_gpu(st, mode, capped=True, device=1, staged=n_staged,
+    _, ys, _, cst = _run_gpu(st, mode, capped=True, device=device, staged=n_staged, head=head,
                              admission=None if admission is None else admission,
                              layerwise=layerwise, attn_bytes=(1 << 22) if layerwise else 0)
     for t in range(cfg.T):
@@ -623,8 +633,8 @@ def test_decode_capped_staged_prefetch(name, over, mode, n_staged, admission, la
 
 
 def test_staged_prefetch_rejections():
-    """Staged prefetch needs device decisions and 2n staging slots; once it has
-    run, the host policy cannot take the cache over."""
+    """Staged prefetch needs 2n staging slots; once staged prefetches run,
+    decisions cannot move between host and device."""
     import torch
     from gpuhelp import DEV
     from paper_2606_15453_amd import stmoe as S
@@ -635,8 +645,13 @@ def test_staged_prefetch_rejections():
     cache = S.ExpertCache(L, E, C, blob, 2, arena, [h.data_ptr() for h in host], demand, side)
     cache.warm(np.array([[0, 1], [2, 3]], dtype=np.int32))
     with pytest.raises(S.StmoeError) as ei:
-        cache.set_staged_prefetch(1)
+        cache.set_staged_prefetch(2)                 # host decisions: needs 4 staging slots
+    assert ei.value.rc == S.EINVAL
+    cache.set_staged_prefetch(1, 1024)
+    with pytest.raises(S.StmoeError) as ei:
+        cache.set_device_policy(1)                   # host staged prefetch is on
     assert ei.value.rc == S.ESTATE
+    cache.set_staged_prefetch(0)
     cache.set_device_policy(1)
     with pytest.raises(S.StmoeError) as ei:
         cache.set_staged_prefetch(2)                 # needs 4 staging slots
@@ -645,4 +660,56 @@ def test_staged_prefetch_rejections():
     with pytest.raises(S.StmoeError) as ei:
         cache.set_device_policy(0)
     assert ei.value.rc == S.ESTATE
+    cache.close()
+
+
+# ---------------------------------------------------------------------------
+# HIP graph replay of the capped decode step with device-side decisions
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("mode,staged,timing_every", [(0, 0, 0), (1, 0, 0), (1, 0, 3), (1, 2, 0), (3, 0, 4),
+                                                      (1, 2, 3)])
+def test_graph_replay_capped_device_decisions(mode, staged, timing_every):
+    """With device-side cache decisions the whole token (routing, predictor,
+    decisions, copy kernels, FFN, prefetch copies) replays as one HIP graph;
+    the stamps of the cache policy come from a device token counter that the
+    graph advances.  Selections, outputs, predictor statistics and cache
+    counts are bit-identical to eager calls and match the oracle, also with
+    event-timed (eager) tokens interleaved with replays."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen30b"].scaled(L=4, T=9, P=3, C=10)
+    st = Stack(cfg)
+    print(f"[graph] mode={mode} staged={staged} timing_every={timing_every}", flush=True)
+    idx_e, ys_e, stats_e, cst_e = _run_gpu(st, mode, capped=True, device=1, staged=staged)
+    idx_g, ys_g, stats_g, cst_g = _run_gpu(st, mode, capped=True, device=1, staged=staged, graph=True,
+                                           timing_every=timing_every)
+    for t in range(cfg.T):
+        assert np.array_equal(idx_g[t], idx_e[t]), t
+        assert np.array_equal(ys_g[t], ys_e[t]), t
+    assert np.array_equal(stats_g, stats_e)
+    assert cst_g == cst_e
+    ref = _oracle(st, mode, C=cfg.C, staged=staged)
+    assert cst_g == _counts(ref["cache"].n)
+
+
+def test_graph_replay_refuses_host_decisions():
+    import torch
+    from gpuhelp import DEV, storage_dtype
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["tiny"].scaled(T=2, P=2)
+    st = Stack(cfg)
+    host = [st.blobs[l][e].cpu().pin_memory() for l in range(cfg.L) for e in range(cfg.E)]
+    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.E, cfg.C, cfg.blob_bytes, 0), dtype=torch.uint8, device=DEV)
+    demand, side = torch.cuda.Stream(), torch.cuda.Stream()
+    cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, cfg.blob_bytes, 0, arena, [h.data_ptr() for h in host], demand, side)
+    cache.warm(st.warm)
+    ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
+                          [g.data_ptr() for g in st.wg_dev], cache=cache)
+    with pytest.raises(S.StmoeError) as ei:
+        ctx.set_graph(True)
+    assert ei.value.rc == S.EINVAL
+    cache.set_device_policy(1)
+    ctx.set_graph(True)
+    ctx.close()
     cache.close()

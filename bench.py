@@ -696,24 +696,26 @@ def host_pool(wl, pinned_gb):
     return pool, ptrs, M
 
 
-def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_token, attn=None):
+def offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token, attn=None):
     """One capped-cache decode run: C slots per layer, the rest streamed from
-    the pinned host pool.  variant = (name, mode, min score, max prefetches
-    per layer, online CCT update, prefetch copies after the demand copies,
-    decisions on the device).  attn = (kv buffer, bytes, out): a decode-
-    attention stand-in that streams `bytes` of KV cache on the compute stream
-    before every MoE layer (layers are then issued one by one)."""
+    the pinned host pool, with the settings of `v` (see variant()).  attn =
+    (kv buffer, bytes, out): a decode-attention stand-in that streams `bytes`
+    of KV cache on the compute stream before every MoE layer (layers are then
+    issued one by one)."""
     import torch
     from paper_2606_15453_amd import stmoe as S
     cfg = wl.cfg
     blob = cfg.blob_bytes
-    name, mode, min_score, max_pf, online, after_demand, device, staged, head = variant
+    name, mode, min_score, online, after_demand = v["name"], v["mode"], v["min_score"], v["online"], v["after_demand"]
+    device, staged, head, graph = v["device"], v["staged"], v["head"], v["graph"]
+    max_pf = C if v["max_pf"] is None else v["max_pf"]
     n_stage = staging_slots(cfg, C)
     demand, side = streams
     if head < 0:
-        # the layer's compute window (routing, FFN, attention) at the link's rate
+        # the layer's compute window (routing, FFN, attention) at the link's
+        # rate, shared by the experts staged for one layer
         window_s = resident_ms_per_token / cfg.L * 1e-3 + (attn_window_s(attn) if attn else 0.0)
-        head = min(blob, max(1 << 16, int(LINK_GBPS[0] * 1e9 * window_s) // 4096 * 4096))
+        head = min(blob, max(1 << 16, int(LINK_GBPS[0] * 1e9 * window_s / max(staged, 1)) // 4096 * 4096))
     y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device="cuda:0")
     cache = S.ExpertCache(cfg.L, cfg.E, C, blob, n_stage, arena, ptrs, demand, side)
     cache.warm(W_warm(wl, C))
@@ -726,7 +728,10 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
     ctx = make_ctx(wl, pred, cache)
     ctx.set_prefetch(min_score, max_pf)
     ctx.set_online_update(online)
-    ctx.set_timing(1)       # events on every layer: negligible next to ms-scale copies
+    if graph:
+        ctx.set_graph(True)     # event timing would run the tokens eagerly: no stage times
+    else:
+        ctx.set_timing(1)       # events on every layer: negligible next to ms-scale copies
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     if attn is None:
@@ -746,14 +751,25 @@ def offload_run(wl, C, arena, ptrs, streams, variant, n_tokens, resident_ms_per_
     cst = cache.stats()
     st = pred.stats()
     copies = cst["demand"] + cst["overflow"] + cst["prefetch"]
+    # bytes moved over the link: whole blobs, except staged copies (host decisions: the head of
+    # every staged expert, the rest of the used ones; device decisions: cancelled copies stop
+    # at an unrecorded point, so no byte count)
+    if not staged:
+        h2d_bytes = copies * blob
+    elif not device:
+        hb = head if 0 < head < blob else blob
+        h2d_bytes = (cst["demand"] + cst["overflow"]) * blob + cst["prefetch"] * hb + cst["useful"] * (blob - hb)
+    else:
+        h2d_bytes = None
     rec = dict(tokens=n_tokens, seconds=round(dt, 4), prefetch_min_score=min_score, staged_per_layer=staged,
-               staged_head_bytes=(head if staged and not device else None),
+               staged_head_bytes=(head if staged and not device else None), graph_replay=bool(graph),
                prefetch_max_per_layer=max_pf, online_update=bool(online),
                prefetch_after_demand=bool(after_demand), device_decisions=bool(device),
                tokens_per_s=round(cfg.B * n_tokens / dt, 3),
                ms_per_token=round(1e3 * dt / n_tokens, 3),
                stall_ms_per_token=round(1e3 * dt / n_tokens - resident_ms_per_token, 3),
-               h2d_copies=copies, h2d_gbps=round(copies * blob / dt / 1e9, 2), cache=cst,
+               h2d_copies=copies, h2d_gbps=(None if h2d_bytes is None else round(h2d_bytes / dt / 1e9, 2)),
+               cache=cst,
                stages_us_per_layer={"route_and_predict": round(1e3 * route_ms / max(n_timed, 1), 1),
                                     "record_wait_and_missed_loads": round(1e3 * miss_ms / max(n_timed, 1), 1),
                                     "ffn": round(1e3 * ffn_ms / max(n_timed, 1), 1)})
@@ -779,31 +795,42 @@ def W_warm(wl, C):
     return S.warm_sets(wl.prof, wl.cfg.E, C)
 
 
+def variant(name, mode, min_score=2, max_pf=None, online=1, after_demand=0, device=0, staged=0, head=0,
+            graph=0):
+    """One capped-cache run's settings: prediction mode, admission (min score,
+    at most max_pf prefetches per layer; None = the cache's slots), online
+    CCT update, prefetch copies after the missed loads, device-side
+    decisions, staged prefetches per layer (0: prefetch into evicted slots),
+    bytes of each staged expert copied up front with host decisions (-1: the
+    layer's compute window at the link's rate, shared by the staged experts;
+    0: all of it), and HIP graph replay of each token."""
+    return dict(name=name, mode=mode, min_score=min_score, max_pf=max_pf, online=online,
+                after_demand=after_demand, device=device, staged=staged, head=head, graph=graph)
+
+
 def offload_variants(cfg):
     from paper_2606_15453_amd import stmoe as S
-    # (name, mode, min score, max prefetches per layer, online update, prefetch after the
-    #  missed loads, device decisions, staged prefetches per layer (0: into evicted slots),
-    #  bytes of a staged expert copied up front with host decisions (-1: the layer's
-    #  compute window at the link's rate; 0: all of it))
     n_st = STAGED_PER_LAYER(cfg)
-    return [("on_demand", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 0, 0, 0),
-            ("st_moe", S.MODE_STMOE, 2, cfg.C, 1, 0, 0, 0, 0),
-            ("st_moe_after_demand", S.MODE_STMOE, 2, cfg.C, 1, 1, 0, 0, 0),
-            ("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K, 1, 0, 0, 0, 0),
-            ("st_moe_score4_maxK_after_demand", S.MODE_STMOE, 4, cfg.K, 1, 1, 0, 0, 0),
-            ("ht_only", S.MODE_HT_ONLY, 2, cfg.C, 1, 0, 0, 0, 0),
-            ("cct_only", S.MODE_CCT_ONLY, 2, cfg.C, 1, 0, 0, 0, 0),
-            ("st_moe_staged_host", S.MODE_STMOE, 2, cfg.C, 1, 1, 0, n_st, -1),
-            ("st_moe_staged_host_full", S.MODE_STMOE, 2, cfg.C, 1, 1, 0, n_st, 0),
-            ("on_demand_device", S.MODE_ON_DEMAND, 2, cfg.C, 1, 0, 1, 0, 0),
-            ("st_moe_device", S.MODE_STMOE, 2, cfg.C, 1, 0, 1, 0, 0),
-            ("st_moe_score4_maxK_after_demand_device", S.MODE_STMOE, 4, cfg.K, 1, 1, 1, 0, 0),
-            ("st_moe_staged_device", S.MODE_STMOE, 2, cfg.C, 1, 1, 1, n_st, 0)]
+    return [variant("on_demand", S.MODE_ON_DEMAND),
+            variant("st_moe", S.MODE_STMOE),
+            variant("st_moe_after_demand", S.MODE_STMOE, after_demand=1),
+            variant("st_moe_score4_maxK", S.MODE_STMOE, 4, cfg.K),
+            variant("st_moe_score4_maxK_after_demand", S.MODE_STMOE, 4, cfg.K, after_demand=1),
+            variant("ht_only", S.MODE_HT_ONLY),
+            variant("cct_only", S.MODE_CCT_ONLY),
+            variant("st_moe_staged_host", S.MODE_STMOE, after_demand=1, staged=n_st, head=-1),
+            variant("st_moe_staged_host1", S.MODE_STMOE, after_demand=1, staged=1, head=-1),
+            variant("on_demand_device", S.MODE_ON_DEMAND, device=1),
+            variant("st_moe_device", S.MODE_STMOE, device=1),
+            variant("st_moe_score4_maxK_after_demand_device", S.MODE_STMOE, 4, cfg.K, after_demand=1, device=1),
+            variant("st_moe_staged_device", S.MODE_STMOE, after_demand=1, device=1, staged=n_st),
+            variant("on_demand_device_graph", S.MODE_ON_DEMAND, device=1, graph=1),
+            variant("st_moe_staged_device_graph", S.MODE_STMOE, after_demand=1, device=1, staged=n_st, graph=1)]
 
 
 def STAGED_PER_LAYER(cfg):
-    """Staged prefetches per layer: the experts one token selects (K), at most 8."""
-    return min(cfg.K, 8)
+    """Staged prefetches per layer: two (the time model gains little beyond two)."""
+    return min(cfg.K, 2)
 
 
 def staging_slots(cfg, C):
@@ -823,13 +850,13 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
                         device="cuda:0")
     streams = (torch.cuda.Stream(), torch.cuda.Stream())
     keep = None if only is None else set(only.split(",")) | {"on_demand"}
-    variants = [v for v in offload_variants(cfg) if keep is None or v[0] in keep]
+    variants = [v for v in offload_variants(cfg) if keep is None or v["name"] in keep]
     out = {}
     for v in variants:
-        out[v[0]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)
+        out[v["name"]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)
     od = out["on_demand"]["stall_ms_per_token"]
-    out["stall_reduction"] = {name: (round(1.0 - out[name]["stall_ms_per_token"] / od, 4) if od > 0 else None)
-                              for name, *_ in variants if name != "on_demand"}
+    out["stall_reduction"] = {v["name"]: (round(1.0 - out[v["name"]]["stall_ms_per_token"] / od, 4) if od > 0
+                                          else None) for v in variants if v["name"] != "on_demand"}
     out["cache_slots_per_layer"] = cfg.C
     out["host_pool"] = {"distinct_blobs": M, "experts": cfg.L * cfg.E, "slot_of_expert": "(l*E + e) mod distinct_blobs"}
     out["h2d_link"] = ("PCIe, pinned host memory, hipMemcpyAsync on demand/side streams" if POOL_TIER == "host" else
@@ -881,10 +908,10 @@ def attention_sweep(wl, key, n_tokens, resident_ms_per_token, pinned_gb, context
         base_ms = resident_ms_per_token + attn_us * cfg.L / 1e3
         recs = {}
         for v in offload_variants(cfg):
-            if v[0] not in ("on_demand", "st_moe", "st_moe_score4_maxK_after_demand", "on_demand_device",
-                            "st_moe_staged_host", "st_moe_staged_host_full", "st_moe_staged_device"):
+            if v["name"] not in ("on_demand", "st_moe", "st_moe_score4_maxK_after_demand", "on_demand_device",
+                                 "st_moe_staged_host", "st_moe_staged_host1", "st_moe_staged_device"):
                 continue
-            recs[v[0]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, base_ms, attn)
+            recs[v["name"]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, base_ms, attn)
         od = recs["on_demand"]["stall_ms_per_token"]
         for name, rec in recs.items():
             red = 1.0 - rec["stall_ms_per_token"] / od if od > 0 else float("nan")
@@ -912,17 +939,16 @@ def offload_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, budgets):
     streams = (torch.cuda.Stream(), torch.cuda.Stream())
     rows = []
     for C in budgets:
-        variants = [(n, m, ms, (C if mp == cfg.C else mp), on, ad, dv, sg, hd)
-                    for n, m, ms, mp, on, ad, dv, sg, hd in offload_variants(cfg)]
-        variants.insert(3, ("st_moe_frozen_cct", S.MODE_STMOE, 2, C, 0, 0, 0, 0, 0))
+        variants = [v for v in offload_variants(cfg) if not v["graph"]]
+        variants.insert(3, variant("st_moe_frozen_cct", S.MODE_STMOE, online=0))
         base = None
         for v in variants:
             rec = offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)
-            if v[0] == "on_demand":
+            if v["name"] == "on_demand":
                 base = rec["stall_ms_per_token"]
             red = 1.0 - rec["stall_ms_per_token"] / base if base and base > 0 else float("nan")
             cst = rec["cache"]
-            rows.append(f"| {C} | {v[0]} | {rec['tokens_per_s']} | {rec['stall_ms_per_token']} | {red:+.3f} | "
+            rows.append(f"| {C} | {v['name']} | {rec['tokens_per_s']} | {rec['stall_ms_per_token']} | {red:+.3f} | "
                         f"{cst['hits']} | {cst['demand'] + cst['overflow']} | {cst['prefetch']} | "
                         f"{cst['useful']} | {rec.get('recall_layers_ge1', '-')} | {rec.get('precision', '-')} |")
     del arena

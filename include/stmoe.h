@@ -445,12 +445,20 @@ int moe_decode_token(moe_ctx* ctx, int token, const void* xs, float* ys, int mod
  * STMOE_EINVAL with a cache, without a predictor or with graph replay on.
  * [sync] */
 int moe_ctx_set_predictor_batch(moe_ctx* ctx, int on);
-/* Graph replay of moe_decode_token on (1) or off (0); contexts without a
- * cache only.  The staging buffers (L*B*H elements of the storage dtype and
- * L*B*H fp32) are part of the context's workspace; turning replay on
+/* Graph replay of moe_decode_token on (1) or off (0): contexts without a
+ * cache, or with a cache whose decisions are on the device
+ * (expert_cache_set_device_policy); a host-decision cache returns
+ * STMOE_EINVAL here (and STMOE_ESTATE at a replay, if its decisions moved
+ * back to the host).  With a cache the graph holds the whole token: routing,
+ * predictor, the cache's decisions, its copy kernels and the side stream's
+ * prefetch copies, which rejoin before the graph ends; the cache policy's
+ * stamps come from a device copy of the token that each replay advances (an
+ * eager call, or a replay for a token that does not follow the last one,
+ * sets it first).  The staging buffers (L*B*H elements of the storage dtype
+ * and L*B*H fp32) are part of the context's workspace; turning replay on
  * creates an internal stream.  The graph launch is ordered after earlier
- * work on the compute stream and before later work on it by events.
- * [sync] */
+ * work on the compute stream (and, with a cache, on its side stream) and
+ * before later work on the compute stream by events.  [sync] */
 int moe_ctx_set_graph(moe_ctx* ctx, int on);
 /* The staging buffers of graph replay (device, owned by the context):
  * x_stage [L][B][H] storage dtype, y_stage [L][B][H] fp32.  Writing the

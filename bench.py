@@ -80,7 +80,14 @@ def parse():
                     help="replay planted traces through the GPU predictor for every config and the paper's "
                          "Table 1 shapes; print recall/precision per ablation mode and exit")
     ap.add_argument("--ffn-sweep", action="store_true",
-                    help="time moe_expert_ffn on every config shape (markdown table on stdout) and exit")
+                    help="time moe_expert_ffn on every config shape, weights in no cache (markdown table on "
+                         "stdout) and exit")
+    ap.add_argument("--read-floor", action="store_true",
+                    help="time one streaming-read launch per size, bytes in no cache (markdown table) and exit")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("KERNEL_TRACE_CSV", "TITLE", "COMMAND"),
+                    help="median kernel durations per kernel and grid size of a rocprofv3 kernel trace")
+    ap.add_argument("--summarize-floor", nargs=2, metavar=("READ_FLOOR_TRACE_CSV", "FFN_SWEEP_TRACE_CSV"),
+                    help="the read floor by size beside the FFN sweep's kernels (markdown)")
     ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_CSV", "TITLE", "COMMAND"),
                     help="print a markdown table of a rocprofv3 kernel_stats.csv and exit")
     ap.add_argument("--summarize-overlap", nargs=2, metavar=("KERNEL_CSV", "COPY_CSV"),
@@ -451,33 +458,53 @@ def predictor_sweep():
                   f"{mset:.1f} |", flush=True)
 
 
-def ffn_sweep(reps=50):
+SWEEP_CONFIGS = ("tiny", "mixtral", "qwen30b", "qwen30b-b8", "dsv2lite", "qwen235b")
+
+
+def sweep_routing(cfg):
+    """The FFN sweep's seeded routing of one config: B rows of K distinct
+    experts, their weights, and the sorted distinct experts."""
+    rng = np.random.default_rng(cfg.seed)
+    idx = np.stack([rng.choice(cfg.E, cfg.K, replace=False) for _ in range(cfg.B)]).astype(np.int32)
+    w = rng.random((cfg.B, cfg.K)).astype(np.float32)
+    return rng, idx, w, sorted(set(idx.ravel().tolist()))
+
+
+def ffn_sweep(calls=60, cold_bytes=2 << 30):
     """Event-timed moe_expert_ffn per config shape: one seeded routing of B
-    tokens (top-K of E), every selected expert's blob generated in HBM."""
+    tokens (top-K of E).  Each call reads a different copy of the selected
+    experts' blobs, cycling over at least `cold_bytes` (well above the 256 MB
+    Infinity Cache), so no call finds its weights in a cache, as in decode,
+    where every layer reads other experts.  The per-call time includes the
+    launch gaps; the kernel durations come from a kernel trace of this run."""
     import torch
     from paper_2606_15453_amd import stmoe as S
     from paper_2606_15453_amd import workload as W
     dev = "cuda:0"
-    print("| workload | B | distinct experts (+shared) | bytes per call | us per call | GB/s | of 8 TB/s | path |")
-    print("|---|---|---|---|---|---|---|---|")
-    for name in ("tiny", "mixtral", "qwen30b", "qwen30b-b8", "dsv2lite", "qwen235b"):
+    print("| workload | B | distinct experts (+shared) | bytes per call | copies cycled | us per call | GB/s | "
+          "of 8 TB/s | path |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for name in SWEEP_CONFIGS:
         cfg = W.CONFIGS[name]
-        rng = np.random.default_rng(cfg.seed)
-        idx = np.stack([rng.choice(cfg.E, cfg.K, replace=False) for _ in range(cfg.B)]).astype(np.int32)
-        w = rng.random((cfg.B, cfg.K)).astype(np.float32)
-        sel = sorted(set(idx.ravel().tolist()))
+        rng, idx, w, sel = sweep_routing(cfg)
+        nb = len(sel) + cfg.n_shared
+        n_sets = max(2, -(-cold_bytes // (nb * cfg.blob_bytes)))
         tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-        store = torch.empty((len(sel) + cfg.n_shared, cfg.blob_elems), dtype=tdt, device=dev)
+        store = torch.empty((n_sets, nb, cfg.blob_elems), dtype=tdt, device=dev)
         for k, e in enumerate(sel):
-            W.expert_blob_torch(cfg, 0, e, store[k])
+            W.expert_blob_torch(cfg, 0, e, store[0, k])
         for sh in range(cfg.n_shared):
-            W.expert_blob_torch(cfg, 0, sh, store[len(sel) + sh], shared=True)
-        ptrs = [store[0].data_ptr()] * cfg.E
-        for k, e in enumerate(sel):
-            ptrs[e] = store[k].data_ptr()
-        eptr = torch.tensor(ptrs, dtype=torch.int64, device=dev)
-        sptr = (torch.tensor([store[len(sel) + sh].data_ptr() for sh in range(cfg.n_shared)],
-                             dtype=torch.int64, device=dev) if cfg.n_shared else None)
+            W.expert_blob_torch(cfg, 0, sh, store[0, len(sel) + sh], shared=True)
+        for c in range(1, n_sets):
+            store[c].copy_(store[0])
+        eptr, sptr = [], []
+        for c in range(n_sets):
+            ptrs = [store[c, 0].data_ptr()] * cfg.E
+            for k, e in enumerate(sel):
+                ptrs[e] = store[c, k].data_ptr()
+            eptr.append(torch.tensor(ptrs, dtype=torch.int64, device=dev))
+            sptr.append(torch.tensor([store[c, len(sel) + sh].data_ptr() for sh in range(cfg.n_shared)],
+                                     dtype=torch.int64, device=dev) if cfg.n_shared else None)
         dt = S.BF16 if cfg.dtype == "bf16" else S.F32
         x = Workload._dev(W.to_storage(cfg, rng.normal(0, 1, (cfg.B, cfg.H))))
         y = torch.empty((cfg.B, cfg.H), dtype=torch.float32, device=dev)
@@ -485,25 +512,147 @@ def ffn_sweep(reps=50):
                          dtype=torch.uint8, device=dev)
         ti, tw = torch.from_numpy(idx).to(dev), torch.from_numpy(w).to(dev)
 
-        def call():
-            S.expert_ffn(x, ti, tw, cfg.H, cfg.I, cfg.E, dt, eptr, y, ws, shared_ptrs=sptr,
+        def call(c):
+            S.expert_ffn(x, ti, tw, cfg.H, cfg.I, cfg.E, dt, eptr[c % n_sets], y, ws, shared_ptrs=sptr[c % n_sets],
                          n_shared=cfg.n_shared)
 
-        for _ in range(3):
-            call()
+        for c in range(2):
+            call(c)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        for _ in range(reps):
-            call()
+        for c in range(2, 2 + calls):
+            call(c)
         e1.record()
         torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) * 1e3 / reps
-        nbytes = (len(sel) + cfg.n_shared) * cfg.blob_bytes
+        us = e0.elapsed_time(e1) * 1e3 / calls
+        nbytes = nb * cfg.blob_bytes
         gbps = nbytes / us / 1e3
         path = "MFMA" if (cfg.B >= 8 and cfg.dtype == "bf16") else "GEMV"
-        print(f"| {cfg.name} | {cfg.B} | {len(sel)} (+{cfg.n_shared}) | {nbytes} | {us:.1f} | {gbps:.0f} | "
+        print(f"| {cfg.name} | {cfg.B} | {len(sel)} (+{cfg.n_shared}) | {nbytes} | {n_sets} | {us:.1f} | {gbps:.0f} | "
               f"{gbps / PEAK_HBM_GBPS:.3f} | {path} |", flush=True)
         del store
+
+
+READ_FLOOR_MIB = (24, 48, 96, 144, 224, 448)
+
+
+def read_floor(sizes_mib=READ_FLOOR_MIB, reps=40, buf_bytes=4 << 30):
+    """The shortest time one launch needs to stream n bytes that are in no
+    cache: stmoe_calib_read with 32 KiB (pattern 2) and 256 KiB (pattern 1)
+    per workgroup, every launch on a different region of a 4 GiB buffer.
+    Event-timed over back-to-back launches (launch gaps included); the kernel
+    durations come from a kernel trace of this run."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    dev = "cuda:0"
+    src = torch.empty(buf_bytes, dtype=torch.uint8, device=dev)
+    src.zero_()
+    top = max(sizes_mib) << 20
+    out = torch.empty(max(S.calib_read_out_words(top, 2), S.calib_read_out_words(top, 1)), dtype=torch.int32,
+                      device=dev)
+    print("| MiB per launch | bytes per workgroup | workgroups | us per launch (events, gaps included) | GB/s |")
+    print("|---|---|---|---|---|")
+    for mib in sizes_mib:
+        n = mib << 20
+        for pattern, region in ((2, 32 << 10), (1, 256 << 10)):
+            offs = [((k * n) % (buf_bytes - n)) & ~((256 << 10) - 1) for k in range(reps + 2)]
+            assert all(o + n <= buf_bytes for o in offs)
+            for o in offs[:2]:
+                S.calib_read(src[o:], n, out, pattern=pattern)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for o in offs[2:]:
+                S.calib_read(src[o:], n, out, pattern=pattern)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            print(f"| {mib} | {region >> 10} KiB | {S.calib_read_out_words(n, pattern)} | {us:.2f} | "
+                  f"{n / us / 1e3:.0f} |", flush=True)
+    del src
+
+
+def trace_groups(path, pause_ns=1_000_000):
+    """This library's kernels in a rocprofv3 kernel trace, grouped by run
+    (launches separated by more than `pause_ns` of idle time start a new
+    one: input generation between shapes), kernel and workgroup count, in
+    order of appearance: {(run, name, workgroups): [durations in us]}."""
+    import csv
+    groups = {}
+    run, last_end = 0, None
+    for r in sorted(csv.DictReader(open(path)), key=lambda r: int(r["Start_Timestamp"])):
+        name = r["Kernel_Name"].replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        if not name.startswith("stmoe::"):
+            continue
+        t0, t1 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+        if last_end is not None and t0 - last_end > pause_ns:
+            run += 1
+        last_end = t1
+        wgs = int(r["Grid_Size_X"]) // max(int(r["Workgroup_Size_X"]), 1)
+        groups.setdefault((run, name, wgs), []).append((t1 - t0) / 1e3)
+    return groups
+
+
+def _median_kept(t):
+    kept = sorted(t[len(t) // 4:])
+    return kept[len(kept) // 2], kept
+
+
+def summarize_floor(rf_csv, fs_csv):
+    """Markdown: the read floor by bytes per launch (32 KiB per workgroup
+    launches of --read-floor) beside every FFN kernel of --ffn-sweep, both
+    from kernel traces (median duration per group)."""
+    from paper_2606_15453_amd import workload as W
+    pts = sorted((wgs * (32 << 10), _median_kept(t)[0]) for (_, n, wgs), t in trace_groups(rf_csv).items()
+                 if n.endswith("<2048ul>"))
+
+    def floor_us(nbytes):     # above the largest size: that size's rate
+        if nbytes >= pts[-1][0]:
+            return pts[-1][1] * nbytes / pts[-1][0]
+        for (b0, t0), (b1, t1) in zip(pts, pts[1:]):
+            if b0 <= nbytes <= b1:
+                return t0 + (t1 - t0) * (nbytes - b0) / (b1 - b0)
+
+    print("Read floor (one `stmoe_calib_read` launch, 32 KiB per workgroup, bytes in no cache):\n")
+    print("| MiB per launch | median us | GB/s | of 8 TB/s |")
+    print("|---|---|---|---|")
+    for b, t in pts:
+        print(f"| {b >> 20} | {t:.2f} | {b / t / 1e3:.0f} | {b / t / 1e3 / PEAK_HBM_GBPS:.3f} |")
+    groups = trace_groups(fs_csv)
+    runs = sorted({k[0] for k in groups})
+    assert len(runs) == len(SWEEP_CONFIGS), (len(runs), "runs in the FFN sweep trace")
+    print("\nExpert FFN kernels of the sweep (weights in no cache; floor interpolated linearly between the sizes "
+          "above, none below the smallest):\n")
+    print("| workload | kernel | workgroups | algorithmic MB | median us | GB/s | floor us | of floor | of 8 TB/s |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for run, name in zip(runs, SWEEP_CONFIGS):
+        cfg = W.CONFIGS[name]
+        _, _, _, sel = sweep_routing(cfg)
+        esz = 2 if cfg.dtype == "bf16" else 4
+        nb = len(sel) + cfg.n_shared
+        for (r, kname, wgs), t in groups.items():
+            if r != run or "reduce" in kname:
+                continue
+            nbytes = nb * (2 if "gate_up" in kname else 1) * cfg.H * cfg.I * esz
+            med = _median_kept(t)[0]
+            short = kname.replace("stmoe::", "")
+            fl = f"{floor_us(nbytes):.2f} | {floor_us(nbytes) / med:.3f}" if nbytes >= pts[0][0] else "- | -"
+            print(f"| {cfg.name} | `{short}` | {wgs} | {nbytes / 1e6:.1f} | {med:.2f} | {nbytes / med / 1e3:.0f} | "
+                  f"{fl} | {nbytes / med / 1e3 / PEAK_HBM_GBPS:.3f} |")
+
+
+def summarize_trace(path, title, cmd, pause_ns=1_000_000):
+    """Median kernel durations of this library's kernels in a rocprofv3
+    kernel trace, per run, kernel and grid size (see trace_groups); the first
+    quarter of each group's launches is dropped (first touch of the
+    buffers)."""
+    groups = trace_groups(path, pause_ns)
+    print(f"# {title}\n")
+    print(f"Command (run from `/tmp` with `TMPDIR=/tmp`, repository at `$R`):\n\n```\n{cmd}\n```\n")
+    print("| kernel | workgroups | launches | median us | min us | max us |")
+    print("|---|---|---|---|---|---|")
+    for (_, name, wgs), t in groups.items():
+        med, kept = _median_kept(t)
+        print(f"| `{name}` | {wgs} | {len(kept)} | {med:.2f} | {kept[0]:.2f} | {kept[-1]:.2f} |")
 
 
 def achievable_read_gbps(nbytes=4 << 30, reps=10, pattern=0):
@@ -1376,6 +1525,12 @@ def main():
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats)
         return
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace)
+        return
+    if args.summarize_floor:
+        summarize_floor(*args.summarize_floor)
+        return
     if args.summarize_offload:
         summarize_offload(args.summarize_offload)
         return
@@ -1398,6 +1553,9 @@ def main():
         return
     if args.ffn_sweep:
         ffn_sweep()
+        return
+    if args.read_floor:
+        read_floor()
         return
     if args.predictor_sweep:
         predictor_sweep()

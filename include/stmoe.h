@@ -497,7 +497,10 @@ int moe_ctx_stage_timing(moe_ctx* ctx, double* route_ms, double* miss_ms, double
  *     16-byte loads; out (device, stmoe_calib_read_out_words(bytes, pattern)
  *     words) receives one checksum word per workgroup.  pattern 0: a
  *     grid-stride sweep; 1: every workgroup reads one contiguous 256 KiB
- *     region (the way the FFN's workgroups read an expert's rows).
+ *     region (the way the FFN's workgroups read an expert's rows); 2: the
+ *     same with 32 KiB regions, one round of eight loads per thread (the
+ *     shortest time one launch needs to stream `bytes`).  Other patterns
+ *     return STMOE_EINVAL.
  * ---------------------------------------------------------------------- */
 int stmoe_calib_copy(const void* src, void* dst, size_t bytes, void* stream);
 size_t stmoe_calib_read_out_words(size_t bytes, int pattern);

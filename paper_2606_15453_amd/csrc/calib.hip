@@ -8,7 +8,8 @@
 //                      for two access patterns: a grid-stride sweep (every
 //                      load instruction of the grid covers consecutive
 //                      bytes), or each workgroup reading one contiguous
-//                      256 KiB region as an expert's rows are read.
+//                      region (256 KiB, or 32 KiB as one round of eight
+//                      loads per thread) as an expert's rows are read.
 #include "common.h"
 
 namespace stmoe {
@@ -45,8 +46,7 @@ __global__ __launch_bounds__(kThreads) void calib_read_kernel(const char* src, s
 // Workgroup w reads the contiguous 16-byte chunks [w*kBlockChunks,
 // (w+1)*kBlockChunks): eight loads per thread in flight, each instruction
 // covering 4 KiB of consecutive bytes.
-constexpr size_t kBlockChunks = (size_t(256) << 10) / 16;
-
+template <size_t kBlockChunks>
 __global__ __launch_bounds__(kThreads) void calib_read_blocked_kernel(const char* src, size_t n, unsigned* out) {
     const u32x4* base = reinterpret_cast<const u32x4*>(src);
     const size_t lo = size_t(blockIdx.x) * kBlockChunks;
@@ -71,8 +71,14 @@ __global__ __launch_bounds__(kThreads) void calib_read_blocked_kernel(const char
     if (threadIdx.x == 0) out[blockIdx.x] = w[0] ^ w[1] ^ w[2] ^ w[3];
 }
 
-unsigned blocked_grid_for(size_t n16) {
-    const size_t g = (n16 + kBlockChunks - 1) / kBlockChunks;
+constexpr size_t kBigBlockChunks = (size_t(256) << 10) / 16;    // pattern 1
+constexpr size_t kSmallBlockChunks = (size_t(32) << 10) / 16;   // pattern 2
+
+size_t block_chunks(int pattern) { return pattern == 1 ? kBigBlockChunks : kSmallBlockChunks; }
+
+unsigned blocked_grid_for(size_t n16, int pattern) {
+    const size_t c = block_chunks(pattern);
+    const size_t g = (n16 + c - 1) / c;
     return unsigned(g < 1 ? 1 : g);
 }
 
@@ -100,18 +106,23 @@ extern "C" int stmoe_calib_copy(const void* src, void* dst, size_t bytes, void* 
 }
 
 extern "C" size_t stmoe_calib_read_out_words(size_t bytes, int pattern) {
-    return pattern == 1 ? blocked_grid_for(bytes / 16) : grid_for(bytes / 16);
+    return pattern == 1 || pattern == 2 ? blocked_grid_for(bytes / 16, pattern) : grid_for(bytes / 16);
 }
 
 extern "C" int stmoe_calib_read(const void* src, size_t bytes, int pattern, unsigned* out, void* stream) {
     clear_error();
     STMOE_CHECK(src && out && bytes > 0 && bytes % 16 == 0, "null pointer or size not a multiple of 16");
     STMOE_CHECK((reinterpret_cast<uintptr_t>(src) & 15) == 0, "src must be 16-byte aligned");
-    STMOE_CHECK(pattern == 0 || pattern == 1, "pattern must be 0 (grid stride) or 1 (contiguous per workgroup)");
+    STMOE_CHECK(pattern >= 0 && pattern <= 2,
+                "pattern must be 0 (grid stride), 1 (256 KiB per workgroup) or 2 (32 KiB per workgroup)");
     const size_t n = bytes / 16;
+    STMOE_CHECK(pattern == 0 || blocked_grid_for(n, pattern) < (1u << 31), "too many workgroups");
     if (pattern == 1)
-        hipLaunchKernelGGL(calib_read_blocked_kernel, dim3(blocked_grid_for(n)), dim3(kThreads), 0,
-                           as_stream(stream), reinterpret_cast<const char*>(src), n, out);
+        hipLaunchKernelGGL(calib_read_blocked_kernel<kBigBlockChunks>, dim3(blocked_grid_for(n, 1)), dim3(kThreads),
+                           0, as_stream(stream), reinterpret_cast<const char*>(src), n, out);
+    else if (pattern == 2)
+        hipLaunchKernelGGL(calib_read_blocked_kernel<kSmallBlockChunks>, dim3(blocked_grid_for(n, 2)),
+                           dim3(kThreads), 0, as_stream(stream), reinterpret_cast<const char*>(src), n, out);
     else
         hipLaunchKernelGGL(calib_read_kernel, dim3(grid_for(n)), dim3(kThreads), 0, as_stream(stream),
                            reinterpret_cast<const char*>(src), n, out);

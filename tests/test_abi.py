@@ -46,6 +46,12 @@ def test_invalid_arguments_rejected_without_device_work():
     assert rc == S.EINVAL      # shared experts without pointers
     assert S._lib.stmoe_predict(None, 0, None, 3, None, None, None, None, None, None) == S.EINVAL
     assert S.blob_bytes(4096, 14336, S.BF16) == 3 * 4096 * 14336 * 2
+    # read probe: one word per workgroup (256 KiB or 32 KiB regions), unknown patterns refused
+    assert S.calib_read_out_words(1 << 30, 1) == 4096
+    assert S.calib_read_out_words(1 << 30, 2) == 32768
+    assert S.calib_read_out_words((32 << 10) + 16, 2) == 2
+    assert S._lib.stmoe_calib_read(256, 1 << 20, 3, 256, None) == S.EINVAL
+    assert S._lib.stmoe_calib_read(256 + 8, 1 << 20, 2, 256, None) == S.EINVAL      # misaligned
 
 
 def test_pack_expert_is_concatenation():

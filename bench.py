@@ -86,6 +86,8 @@ def parse():
                     help="time one streaming-read launch per size, bytes in no cache (markdown table) and exit")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("KERNEL_TRACE_CSV", "TITLE", "COMMAND"),
                     help="median kernel durations per kernel and grid size of a rocprofv3 kernel trace")
+    ap.add_argument("--summarize-policy", metavar="POLICY_BOUND_MD",
+                    help="pivot a --policy-bound table by workload, link rate and attention window")
     ap.add_argument("--summarize-floor", nargs=2, metavar=("READ_FLOOR_TRACE_CSV", "FFN_SWEEP_TRACE_CSV"),
                     help="the read floor by size beside the FFN sweep's kernels (markdown)")
     ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_CSV", "TITLE", "COMMAND"),
@@ -98,6 +100,8 @@ def parse():
                     help="time-model bound of one-layer-lookahead prefetch policies on the planted traces")
     ap.add_argument("--policy-attn", default="0", metavar="MS1,MS2,...",
                     help="attention windows (ms per layer) for --policy-bound")
+    ap.add_argument("--policy-link", default="measured", metavar="GBPS1,GBPS2,...",
+                    help="link rates for --policy-bound: 'measured' and/or GB/s (copy time = blob bytes / rate)")
     ap.add_argument("--summarize-gaps", nargs=3, metavar=("KERNEL_TRACE_CSV", "TITLE", "COMMAND"),
                     help="print the compute-queue gap analysis of a rocprofv3 kernel trace as markdown")
     ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "META_JSON"),
@@ -1301,17 +1305,20 @@ def simulate_policy(trace, preds, L, C, warm, copy_ms, layer_ms, attn_ms, policy
     return (clock - ideal) / T, copies, wasted
 
 
-def policy_bound(names, n_tokens, attn_list):
+def policy_bound(names, n_tokens, attn_list, links=("measured",)):
     """Markdown table of simulate_policy over the planted traces, with the GPU
     predictor's rankings (paper threshold) and measured inputs: the H2D copy
     time of one expert (pinned host -> HBM, event-timed) and the layer time of
-    the HBM-resident decode (router + FFN, event-timed on one layer's call)."""
+    the HBM-resident decode (router + FFN, event-timed on one layer's call).
+    links: "measured" and/or link rates in GB/s; a rate replaces the measured
+    copy time by blob bytes / rate (the sensitivity of each policy to the
+    bandwidth of the tier the experts come from)."""
     import torch
     from paper_2606_15453_amd import stmoe as S
     from paper_2606_15453_amd import workload as W
     dev = "cuda:0"
-    out = ["| workload | attention ms/layer | policy | copies | wasted copy-ms | stall ms/token | "
-           "stall vs on-demand |", "|---|---|---|---|---|---|---|"]
+    out = ["| workload | link GB/s | copy ms | attention ms/layer | policy | copies | wasted copy-ms | "
+           "stall ms/token | stall vs on-demand |", "|---|---|---|---|---|---|---|---|---|"]
     for name in names:
         cfg = W.CONFIGS[name]
         T = min(n_tokens, cfg.T)
@@ -1356,16 +1363,38 @@ def policy_bound(names, n_tokens, attn_list):
         layer_ms = ffn_layer_ms(cfg)
         warm = S.warm_sets(prof, cfg.E, cfg.C)
         log(f"policy bound {name}: copy {copy_ms:.3f} ms, layer {layer_ms:.4f} ms, {T} tokens")
-        for attn in attn_list:
-            base = None
-            for pol in ("demand", "evict", "staged", "perfect_evict", "perfect_staged", "optimum"):
-                stall, copies, wasted = simulate_policy(trace, preds, cfg.L, cfg.C, warm, copy_ms, layer_ms,
-                                                        attn, pol, max_staged=cfg.C)
-                if base is None:
-                    base = stall
-                out.append(f"| {cfg.name} (copy {copy_ms:.3f} ms, layer {layer_ms:.3f} ms) | {attn:.2f} | {pol} | "
-                           f"{copies} | {wasted:.1f} | {stall:.2f} | {1 - stall / base:+.3f} |")
+        for link in links:
+            cms = copy_ms if link == "measured" else blob / (float(link) * 1e6)
+            rate = f"{blob / cms / 1e6:.0f}" + (" (measured)" if link == "measured" else "")
+            for attn in attn_list:
+                base = None
+                for pol in ("demand", "evict", "staged", "perfect_evict", "perfect_staged", "optimum"):
+                    stall, copies, wasted = simulate_policy(trace, preds, cfg.L, cfg.C, warm, cms, layer_ms,
+                                                            attn, pol, max_staged=cfg.C)
+                    if base is None:
+                        base = stall
+                    rel = f"{1 - stall / base:+.3f}" if base > 1e-9 else "-"
+                    out.append(f"| {cfg.name} (layer {layer_ms:.3f} ms) | {rate} | {cms:.4f} | {attn:.2f} | {pol} | "
+                               f"{copies} | {wasted:.1f} | {stall:.2f} | {rel} |")
     return out
+
+
+def summarize_policy(path):
+    """Pivot of a --policy-bound table: per workload, link rate and attention
+    window, the on-demand stall and each policy's stall reduction against it."""
+    tab = {}
+    for line in open(path):
+        c = [x.strip() for x in line.strip().strip("|").split("|")]
+        if len(c) != 9 or c[0] == "workload" or c[0].startswith("---"):
+            continue
+        key = (c[0].split(" (")[0], c[1].split(" ")[0] + (" (measured)" if "measured" in c[1] else ""), c[3])
+        tab.setdefault(key, {})[c[4]] = (float(c[7]), c[8])
+    pols = ("evict", "staged", "perfect_evict", "perfect_staged", "optimum")
+    print("| workload | link GB/s | attention ms/layer | on-demand stall ms/token | "
+          + " | ".join(pols) + " |")
+    print("|---" * (4 + len(pols)) + "|")
+    for (w, link, attn), v in tab.items():
+        print(f"| {w} | {link} | {attn} | {v['demand'][0]:.2f} | " + " | ".join(v[p][1] for p in pols) + " |")
 
 
 def ffn_layer_ms(cfg, reps=20):
@@ -1531,6 +1560,9 @@ def main():
     if args.summarize_floor:
         summarize_floor(*args.summarize_floor)
         return
+    if args.summarize_policy:
+        summarize_policy(args.summarize_policy)
+        return
     if args.summarize_offload:
         summarize_offload(args.summarize_offload)
         return
@@ -1548,7 +1580,7 @@ def main():
         return
     if args.policy_bound:
         lines = policy_bound(args.policy_bound.split(","), max(args.offload_tokens, 1),
-                             [float(a) for a in args.policy_attn.split(",")])
+                             [float(a) for a in args.policy_attn.split(",")], args.policy_link.split(","))
         print("\n".join(lines), flush=True)
         return
     if args.ffn_sweep:

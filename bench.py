@@ -1158,18 +1158,26 @@ class _Link:
 class _Lru:
     """Per-layer C-slot cache: least recently used with protection of the
     current set (the library's policy), or the offline optimum (evict the
-    expert whose next use in this layer is farthest)."""
+    expert whose next use in this layer is farthest), or, for the online
+    alternatives, the least frequently used (counts seeded from profiling,
+    +1 per token that selects the expert) or the lowest score of a given
+    per-expert vector, ties by least recent use."""
 
-    def __init__(self, warm, C, future=None):
+    def __init__(self, warm, C, future=None, counts=None):
         self.slots = [list(w) for w in warm]
         self.last = [[0] * C for _ in warm]
         self.C = C
         self.future = future          # future[l] = list over tokens of sets, for the offline optimum
+        self.freq = None if counts is None else [list(r) for r in counts]
 
-    def victim(self, l, keep, t=None):
+    def victim(self, l, keep, t=None, score=None):
         cands = [c for c in range(self.C) if self.slots[l][c] < 0 or self.slots[l][c] not in keep]
         if not cands:
             return -1
+        if score is not None or self.freq is not None:
+            val = score if score is not None else self.freq[l]
+            return min(cands, key=lambda c: (val[self.slots[l][c]] if self.slots[l][c] >= 0 else -1,
+                                             self.last[l][c], c))
         if self.future is None:
             return min(cands, key=lambda c: (self.last[l][c], c))
 
@@ -1180,20 +1188,23 @@ class _Lru:
             return 1 << 30
         return max(cands, key=lambda c: (nxt(self.slots[l][c]) if self.slots[l][c] >= 0 else 1 << 31, -c))
 
-    def acquire(self, l, U, stamp, t=None):
+    def acquire(self, l, U, stamp, t=None, score=None):
         keep = set(U)
         misses, overflow = [], []
         for f in U:
             if f in self.slots[l]:
                 self.last[l][self.slots[l].index(f)] = stamp
                 continue
-            c = self.victim(l, keep, t)
+            c = self.victim(l, keep, t, score)
             if c < 0:
                 overflow.append(f)
                 continue
             self.slots[l][c] = f
             self.last[l][c] = stamp
             misses.append(f)
+        if self.freq is not None:
+            for f in U:
+                self.freq[l][f] += 1
         return misses, overflow
 
     def prefetch(self, l, ranked, stamp, t=None):
@@ -1212,7 +1223,11 @@ class _Lru:
         return out
 
 
-def simulate_policy(trace, preds, L, C, warm, copy_ms, layer_ms, attn_ms, policy, max_staged=None):
+NO_PREFETCH = ("demand", "optimum", "demand_lfu", "demand_cct")
+
+
+def simulate_policy(trace, preds, L, C, warm, copy_ms, layer_ms, attn_ms, policy, max_staged=None,
+                    counts=None, cct=None):
     """Time model of the capped decode loop.  trace[t][l]: distinct selected
     experts; preds[t][l]: the admitted ranking for the layer after (t, l).
     Per layer: the attention window (attn_ms), routing and decisions, the
@@ -1225,10 +1240,14 @@ def simulate_policy(trace, preds, L, C, warm, copy_ms, layer_ms, attn_ms, policy
     eviction, cancelled when the next layer's routing shows them unused),
     "perfect_evict" / "perfect_staged" (the same with the exact next-layer
     selection as the prediction), "optimum" (offline-optimal replacement, no
-    prefetch).  Returns (stall ms per token, copies started, copy-ms wasted)."""
+    prefetch); online replacement alternatives without prefetch: "demand_lfu"
+    (least frequently used, counts[l][e] seeds), "demand_cct" (evict the
+    expert with the lowest Eq. 1 spatial score from the previous layer's
+    current selection through cct = (cct_idx, cct_conf); layer 0 by counts).
+    Returns (stall ms per token, copies started, copy-ms wasted)."""
     T = len(trace)
     future = [[trace[t][l] for t in range(T)] for l in range(L)] if policy == "optimum" else None
-    cache = _Lru(warm, C, future)
+    cache = _Lru(warm, C, future, counts if policy == "demand_lfu" else None)
     link = _Link(copy_ms)
     clock, copies, wasted = 0.0, 0, 0.0
     pend = {}                     # layer -> [(expert, start, end)] prefetch copies issued for it
@@ -1266,7 +1285,16 @@ def simulate_policy(trace, preds, L, C, warm, copy_ms, layer_ms, attn_ms, policy
                 for f, s0, e0 in jobs:
                     if f not in U:
                         wasted += e0 - s0
-                misses, overflow = cache.acquire(l, U, stamp, t)
+                score = None
+                if policy == "demand_cct":
+                    if l == 0:
+                        score = list(counts[0])
+                    else:
+                        sc = np.zeros(len(counts[l]))
+                        for f in trace[t][l - 1]:
+                            np.add.at(sc, np.asarray(cct[0][l - 1][f], np.int64), np.asarray(cct[1][l - 1][f]))
+                        score = sc.tolist()
+                misses, overflow = cache.acquire(l, U, stamp, t, score)
                 for f in U:
                     if f in inflight and f not in misses:
                         ready = max(ready, inflight[f])
@@ -1275,7 +1303,7 @@ def simulate_policy(trace, preds, L, C, warm, copy_ms, layer_ms, attn_ms, policy
                     copies += 1
             clock = ready + 0.95 * layer_ms
             # prefetch for the next layer, behind this layer's missed copies
-            if policy == "demand" or policy == "optimum":
+            if policy in NO_PREFETCH:
                 continue
             nl, nt = (l + 1) % L, t + (l + 1) // L
             if perfect:
@@ -1305,6 +1333,9 @@ def simulate_policy(trace, preds, L, C, warm, copy_ms, layer_ms, attn_ms, policy
     return (clock - ideal) / T, copies, wasted
 
 
+POLICIES = ("demand", "evict", "staged", "perfect_evict", "perfect_staged", "optimum", "demand_lfu", "demand_cct")
+
+
 def policy_bound(names, n_tokens, attn_list, links=("measured",)):
     """Markdown table of simulate_policy over the planted traces, with the GPU
     predictor's rankings (paper threshold) and measured inputs: the H2D copy
@@ -1330,6 +1361,11 @@ def policy_bound(names, n_tokens, attn_list, links=("measured",)):
         # the GPU predictor's admitted rankings (paper threshold, capped at C)
         p = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
         p.profile(prof)
+        _, cct_idx, cct_conf, _ = p.export()          # the profiled tables, for demand_cct
+        counts = np.zeros((cfg.L, cfg.E), np.int64)     # profiling tokens that select each expert
+        for t in range(cfg.P):
+            for l in range(cfg.L):
+                counts[l, np.unique(prof[t, :, l])] += 1
         ranked = torch.zeros(cfg.E, dtype=torch.int32, device=dev)
         nr = torch.zeros(1, dtype=torch.int32, device=dev)
         dsel = torch.from_numpy(np.ascontiguousarray(dec.transpose(0, 2, 1, 3))).to(dev)
@@ -1368,9 +1404,10 @@ def policy_bound(names, n_tokens, attn_list, links=("measured",)):
             rate = f"{blob / cms / 1e6:.0f}" + (" (measured)" if link == "measured" else "")
             for attn in attn_list:
                 base = None
-                for pol in ("demand", "evict", "staged", "perfect_evict", "perfect_staged", "optimum"):
+                for pol in POLICIES:
                     stall, copies, wasted = simulate_policy(trace, preds, cfg.L, cfg.C, warm, cms, layer_ms,
-                                                            attn, pol, max_staged=cfg.C)
+                                                            attn, pol, max_staged=cfg.C, counts=counts,
+                                                            cct=(cct_idx, cct_conf))
                     if base is None:
                         base = stall
                     rel = f"{1 - stall / base:+.3f}" if base > 1e-9 else "-"
@@ -1389,7 +1426,7 @@ def summarize_policy(path):
             continue
         key = (c[0].split(" (")[0], c[1].split(" ")[0] + (" (measured)" if "measured" in c[1] else ""), c[3])
         tab.setdefault(key, {})[c[4]] = (float(c[7]), c[8])
-    pols = ("evict", "staged", "perfect_evict", "perfect_staged", "optimum")
+    pols = [p for p in POLICIES[1:] if any(p in v for v in tab.values())]
     print("| workload | link GB/s | attention ms/layer | on-demand stall ms/token | "
           + " | ".join(pols) + " |")
     print("|---" * (4 + len(pols)) + "|")

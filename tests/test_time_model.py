@@ -9,7 +9,7 @@ import pytest
 
 import bench
 
-POLICIES = ("demand", "evict", "staged", "perfect_evict", "perfect_staged", "optimum")
+POLICIES = bench.POLICIES
 
 
 def test_hand_trace_one_layer_one_slot():
@@ -39,7 +39,9 @@ def _random_case(seed, L=3, E=8, C=3, K=2, T=12):
 def test_properties_on_random_traces(seed):
     trace, preds, warm, L, C = _random_case(seed)
     for pol in POLICIES:
-        st, _, _ = bench.simulate_policy(trace, preds, L, C, warm, 0.0, 0.05, 0.0, pol, max_staged=C)
+        st, _, _ = bench.simulate_policy(trace, preds, L, C, warm, 0.0, 0.05, 0.0, pol, max_staged=C,
+                                         counts=[[1] * 8 for _ in range(L)],
+                                         cct=([[[e] for e in range(8)]] * (L - 1), [[[1] for e in range(8)]] * (L - 1)))
         assert st == pytest.approx(0.0, abs=1e-9), pol
     demand = bench.simulate_policy(trace, preds, L, C, warm, 0.3, 0.05, 0.0, "demand")
     optimum = bench.simulate_policy(trace, preds, L, C, warm, 0.3, 0.05, 0.0, "optimum")
@@ -57,3 +59,23 @@ def test_everything_resident_copies_nothing():
     trace, preds, _, L, _ = _random_case(3)
     warm = [list(range(8)) for _ in range(L)]
     assert bench.simulate_policy(trace, preds, L, 8, warm, 1.0, 0.05, 0.0, "demand") == pytest.approx((0.0, 0, 0.0))
+
+
+def test_online_replacement_hand_traces():
+    # one layer, slots holding 0 and 1 (both unused so far); tokens select 2, then 0
+    trace, none = [[[2]], [[0]]], [[[]], [[]]]
+    # least recently used breaks the tie by slot and evicts 0, which the next token needs
+    assert bench.simulate_policy(trace, none, 1, 2, [[0, 1]], 1.0, 0.1, 0.0, "demand") == pytest.approx((1.0, 2, 0.0))
+    # profiling counts favour 0: least frequently used evicts 1 instead
+    assert bench.simulate_policy(trace, none, 1, 2, [[0, 1]], 1.0, 0.1, 0.0, "demand_lfu",
+                                 counts=[[10, 0, 5]]) == pytest.approx((0.5, 1, 0.0))
+    # two layers; layer 0 always selects expert 0, whose CCT entry names expert 2 for layer 1
+    # (confidence 3): layer 1 evicts expert 1 rather than 2, which the next token selects
+    trace2 = [[[0], [0]], [[0], [2]]]
+    warm2 = [[0, 1], [2, 1]]
+    cct = ([[[2], [0], [0]]], [[[3], [0], [0]]])
+    none2 = [[[], []], [[], []]]
+    lru = bench.simulate_policy(trace2, none2, 2, 2, warm2, 1.0, 0.1, 0.0, "demand")
+    cct_run = bench.simulate_policy(trace2, none2, 2, 2, warm2, 1.0, 0.1, 0.0, "demand_cct",
+                                    counts=[[1, 1, 1], [1, 1, 1]], cct=cct)
+    assert lru[1] == 2 and cct_run[1] == 1

@@ -860,7 +860,7 @@ def offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token,
     cfg = wl.cfg
     blob = cfg.blob_bytes
     name, mode, min_score, online, after_demand = v["name"], v["mode"], v["min_score"], v["online"], v["after_demand"]
-    device, staged, head, graph = v["device"], v["staged"], v["head"], v["graph"]
+    device, staged, head, graph, freq = v["device"], v["staged"], v["head"], v["graph"], v["freq"]
     max_pf = C if v["max_pf"] is None else v["max_pf"]
     n_stage = staging_slots(cfg, C)
     demand, side = streams
@@ -873,6 +873,8 @@ def offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token,
     cache = S.ExpertCache(cfg.L, cfg.E, C, blob, n_stage, arena, ptrs, demand, side)
     cache.warm(W_warm(wl, C))
     cache.set_prefetch_order(after_demand)
+    if freq:
+        cache.set_counts(S.use_counts(wl.prof, cfg.E))
     cache.set_device_policy(device)
     if staged:
         cache.set_staged_prefetch(staged, head)
@@ -918,6 +920,7 @@ def offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token,
                staged_head_bytes=(head if staged and not device else None), graph_replay=bool(graph),
                prefetch_max_per_layer=max_pf, online_update=bool(online),
                prefetch_after_demand=bool(after_demand), device_decisions=bool(device),
+               eviction="frequency-aware" if freq else "least recently used",
                tokens_per_s=round(cfg.B * n_tokens / dt, 3),
                ms_per_token=round(1e3 * dt / n_tokens, 3),
                stall_ms_per_token=round(1e3 * dt / n_tokens - resident_ms_per_token, 3),
@@ -949,16 +952,17 @@ def W_warm(wl, C):
 
 
 def variant(name, mode, min_score=2, max_pf=None, online=1, after_demand=0, device=0, staged=0, head=0,
-            graph=0):
+            graph=0, freq=0):
     """One capped-cache run's settings: prediction mode, admission (min score,
     at most max_pf prefetches per layer; None = the cache's slots), online
     CCT update, prefetch copies after the missed loads, device-side
     decisions, staged prefetches per layer (0: prefetch into evicted slots),
     bytes of each staged expert copied up front with host decisions (-1: the
     layer's compute window at the link's rate, shared by the staged experts;
-    0: all of it), and HIP graph replay of each token."""
+    0: all of it), HIP graph replay of each token, and frequency-aware eviction
+    (use counts seeded from profiling) instead of least recently used."""
     return dict(name=name, mode=mode, min_score=min_score, max_pf=max_pf, online=online,
-                after_demand=after_demand, device=device, staged=staged, head=head, graph=graph)
+                after_demand=after_demand, device=device, staged=staged, head=head, graph=graph, freq=freq)
 
 
 def offload_variants(cfg):
@@ -978,7 +982,10 @@ def offload_variants(cfg):
             variant("st_moe_score4_maxK_after_demand_device", S.MODE_STMOE, 4, cfg.K, after_demand=1, device=1),
             variant("st_moe_staged_device", S.MODE_STMOE, after_demand=1, device=1, staged=n_st),
             variant("on_demand_device_graph", S.MODE_ON_DEMAND, device=1, graph=1),
-            variant("st_moe_staged_device_graph", S.MODE_STMOE, after_demand=1, device=1, staged=n_st, graph=1)]
+            variant("st_moe_staged_device_graph", S.MODE_STMOE, after_demand=1, device=1, staged=n_st, graph=1),
+            variant("on_demand_freq", S.MODE_ON_DEMAND, freq=1),
+            variant("on_demand_device_freq", S.MODE_ON_DEMAND, device=1, freq=1),
+            variant("st_moe_staged_host_freq", S.MODE_STMOE, after_demand=1, staged=n_st, head=-1, freq=1)]
 
 
 def STAGED_PER_LAYER(cfg):
@@ -1062,7 +1069,8 @@ def attention_sweep(wl, key, n_tokens, resident_ms_per_token, pinned_gb, context
         recs = {}
         for v in offload_variants(cfg):
             if v["name"] not in ("on_demand", "st_moe", "st_moe_score4_maxK_after_demand", "on_demand_device",
-                                 "st_moe_staged_host", "st_moe_staged_host1", "st_moe_staged_device"):
+                                 "st_moe_staged_host", "st_moe_staged_host1", "st_moe_staged_device",
+                                 "on_demand_device_freq"):
                 continue
             recs[v["name"]] = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, base_ms, attn)
         od = recs["on_demand"]["stall_ms_per_token"]

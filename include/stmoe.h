@@ -249,6 +249,12 @@ typedef struct {
  * the profiling tokens, count desc then index asc, -1 padding when C > E.
  *   sel host [P][B][L][K] int32 (each < E); out host [L][C] int32.  [host] */
 int expert_cache_warm_sets(const int32_t* sel, int P, int B, int L, int K, int E, int C, int32_t* out);
+/* Seeds of frequency-aware eviction (this implementation's alternative to
+ * least recently used; the paper's buffer has no replacement rule): per layer
+ * the number of profiling tokens whose selection (any batch row) contains
+ * each expert.  sel host [P][B][L][K] int32 (each < E); out host [L][E]
+ * int64.  [host] */
+int expert_cache_use_counts(const int32_t* sel, int P, int B, int L, int K, int E, int64_t* out);
 
 int stmoe_policy_create(int L, int E, int C, const int32_t* warm /* host [L][C], -1 = empty */,
                         stmoe_policy** out);
@@ -264,6 +270,12 @@ int stmoe_policy_acquire(stmoe_policy* p, int layer, const int32_t* needed, int 
 /* slot_expert host out [L][C] (-1 = empty) */
 int stmoe_policy_slots(const stmoe_policy* p, int32_t* slot_expert);
 int stmoe_policy_stats(const stmoe_policy* p, stmoe_cache_stats* out);
+/* Replacement rule.  counts host [L][E] int64 (each >= 0, else STMOE_EINVAL):
+ * frequency-aware eviction seeded with these use counts; victims are taken
+ * by the smallest (use count of the slot's expert, last use, slot), an empty
+ * slot counting -1, and every acquire adds 1 to the count of each expert it
+ * is given.  counts NULL: least recently used (the default).  [host] */
+int stmoe_policy_set_counts(stmoe_policy* p, const int64_t* counts);
 
 /* ------------------------------------------------------------------------
  * HBM expert cache (Section 4.1 prefetch staging; Section 4.3.4 missed
@@ -303,6 +315,11 @@ int expert_cache_prefetch(expert_cache* c, int layer, const int32_t* ranked, int
  * current layer's missed experts are in.  Which copies happen, and the
  * counts, do not change.  Returns STMOE_EINVAL for other values. */
 int expert_cache_set_prefetch_order(expert_cache* c, int after_demand);
+/* The cache's replacement rule, as stmoe_policy_set_counts (host decisions;
+ * with device decisions the counts move to device memory and the decision
+ * kernel keeps them, also under graph replay).  expert_cache_warm keeps the
+ * rule and the counts.  [sync] with device decisions, [host] otherwise. */
+int expert_cache_set_counts(expert_cache* c, const int64_t* counts);
 /* Device-side decisions (Section 4.3.4's missed loading and prefetch
  * without a host round trip).  on = 1: the policy state moves to device
  * memory and moe_decode_layer takes its decisions in a one-workgroup kernel

@@ -16,8 +16,9 @@ Parity status per function (see the pins under ``tests/``):
   STPredictor.profile / update / predict             pinned (hand-worked example, invariants,
                                                       closed form K^2/N, special cases,
                                                       exhaustive update check on E = 4)
-  CacheSim, admitted, warm_from_profile              pinned (hand-worked traces, invariants,
-                                                      exhaustive optimum lower bound)
+  CacheSim, admitted, warm_from_profile, use_counts  pinned (hand-worked traces, invariants,
+                                                      exhaustive optimum lower bound; the
+                                                      frequency-aware rule by a hand trace)
   decode_reference (the per-layer loop)              pinned (hand-worked five-token run:
                                                       per-token hits, scores, tables, the
                                                       capped cache's copy log in both modes,
@@ -319,11 +320,18 @@ class CacheSim:
     the first n ranked experts that are not resident aside, changing no slot;
     acquire then decides exactly as without prefetching, except that a staged
     expert needs no copy (useful); staged experts not selected are wasted.
+
+    counts [L][E] (frequency-aware eviction, an alternative replacement rule):
+    the victim is the evictable slot with the smallest (use count of its
+    expert, last_use, slot), an empty slot counting -1; every acquire adds 1
+    to the count of each expert it is given.  counts=None: least recently
+    used as above.
     """
 
-    def __init__(self, L: int, E: int, C: int, warm=None, staged: int = 0):
+    def __init__(self, L: int, E: int, C: int, warm=None, staged: int = 0, counts=None):
         self.L, self.E, self.C = L, E, C
         self.staged = staged
+        self.freq = None if counts is None else [[int(v) for v in row] for row in counts]
         self.stage = [[] for _ in range(L)]
         self.slot = [[-1] * C for _ in range(L)]
         self.last = [[0] * C for _ in range(L)]
@@ -344,6 +352,11 @@ class CacheSim:
         cands = [c for c in range(self.C) if self.slot[l][c] not in keep]
         if not cands:
             return -1
+        if self.freq is not None:
+            def uses(c):
+                e = self.slot[l][c]
+                return self.freq[l][e] if e >= 0 else -1
+            return min(cands, key=lambda c: (uses(c), self.last[l][c], c))
         return min(cands, key=lambda c: (self.last[l][c], c))
 
     def prefetch(self, l: int, ranked, stamp: int):
@@ -407,6 +420,9 @@ class CacheSim:
         self.n.useful += useful
         self.n.wasted += wasted
         self.pending[l] = set()
+        if self.freq is not None:
+            for f in U:
+                self.freq[l][f] += 1
         self.n.log.append(("A", l, stamp, tuple(demand), tuple(overflow), hits, useful, wasted))
         return where, demand, overflow
 
@@ -445,9 +461,21 @@ def warm_from_profile(prof_sel, L: int, E: int, C: int):
     return out
 
 
+def use_counts(prof_sel, L: int, E: int):
+    """Seeds of frequency-aware eviction: per layer, the number of profiling
+    tokens whose selection (any batch row) contains each expert.
+    sel[p][b][l][k] -> int64 [L][E]."""
+    prof_sel = np.asarray(prof_sel, np.int64)
+    out = np.zeros((L, E), np.int64)
+    for p in range(prof_sel.shape[0]):
+        for l in range(L):
+            out[l, np.unique(prof_sel[p, :, l, :])] += 1
+    return out
+
+
 def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=None,
                      mode=MODE_STMOE, renorm=False, ffn_of=None, ffn_tokens=0, online=True,
-                     tables=None, min_score=THRESHOLD, max_per_layer=None, staged=0):
+                     tables=None, min_score=THRESHOLD, max_per_layer=None, staged=0, counts=None):
     """Run the decode loop on the CPU.
 
     x_of(t, l) -> x [B][H] float64; wg_of(l) -> W_g [E][H] float64;
@@ -460,7 +488,8 @@ def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=N
     tables=(cct_idx, cct_conf, ht) replaces the profiled tables before the
     first token (planted wrong predictions).  min_score / max_per_layer are
     the prefetch admission knobs of ``admitted``; staged > 0 stages prefetches
-    aside instead of evicting (CacheSim).
+    aside instead of evicting, counts switches the cache to frequency-aware
+    eviction (CacheSim).
     Returns a dict of per-(t, l) records and totals.
     """
     pred = STPredictor(L, E, K, B)
@@ -469,7 +498,7 @@ def decode_reference(L, E, K, B, x_of, wg_of, prof_sel, n_tokens, C=None, warm=N
         pred.load_tables(*tables)
     use_cct = mode in (MODE_STMOE, MODE_CCT_ONLY)
     use_ht = mode in (MODE_STMOE, MODE_HT_ONLY)
-    cache = CacheSim(L, E, C, warm, staged) if C is not None else None
+    cache = CacheSim(L, E, C, warm, staged, counts) if C is not None else None
     # layer 0 of the first token is predicted from the profiled HT[0]
     P_cur = pred.predict(-1, None, use_cct=False, use_ht=use_ht)
     rec = dict(idx=[], w=[], scores=[], hits=np.zeros((n_tokens, L), np.int64),

@@ -21,6 +21,8 @@ struct PolicyState {
     int64_t* last;              // [L*C] last use stamp
     int32_t* where;             // [L*E] slot of expert or -1
     char* pending;              // [L*E] prefetched, not yet verified
+    int64_t* freq;              // [L*E] use counts
+    int* use_freq;              // 1: frequency-aware eviction
     stmoe_cache_stats* st;
 };
 
@@ -33,6 +35,9 @@ int device_cache_create(const PolicyState& ps, char* arena, size_t blob, int n_s
                         const void* const* host_blobs, char* state, hipStream_t side, DeviceCache** out);
 // Staged prefetch with ns positions per parity (0: prefetch into slots).  [sync]
 int device_cache_set_staged(DeviceCache* d, int ns);
+// Frequency-aware eviction with these use counts ([L*E] host), or least
+// recently used (counts null).  [sync]
+int device_cache_set_counts(DeviceCache* d, const int64_t* counts);
 int device_cache_staged(const DeviceCache* d);
 int device_cache_download(DeviceCache* d, const PolicyState& ps);
 void device_cache_destroy(DeviceCache* d);

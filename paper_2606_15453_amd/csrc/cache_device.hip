@@ -1,13 +1,14 @@
 // Device-side cache decisions (see cache_device.h).  The policy is the host
 // policy's (expert_cache.cpp): per-layer slot partitions; a missed expert
 // takes the evictable slot (empty, or holding an expert outside the current
-// selection) with the smallest (last use, slot); a prefetch walks the
-// admitted ranking and takes victims the same way among slots outside the
-// ranked set, stopping when none is left; residency counts from copy issue.
-// Evictions within one call never change the other candidates' keys, so the
-// k-th missed (or non-resident ranked) expert takes the k-th victim in
-// (last use, slot) order: the kernel ranks slots and experts in parallel
-// instead of searching once per copy.
+// selection) with the smallest (last use, slot), or, frequency-aware, the
+// smallest (use count, last use, slot) with an empty slot counting -1; a
+// prefetch walks the admitted ranking and takes victims the same way among
+// slots outside the ranked set, stopping when none is left; residency counts
+// from copy issue.  Evictions within one call never change the other
+// candidates' keys, so the k-th missed (or non-resident ranked) expert takes
+// the k-th victim in key order: the kernel ranks slots and experts in
+// parallel instead of searching once per copy.
 //
 // Staged prefetch (an alternative to prefetching into evicted slots): the
 // predicted experts of the next layer are copied into spare staging blocks,
@@ -68,6 +69,9 @@ struct DecideArgs {
     int32_t* sexp;               // [2][kStageMax] staged expert
     int32_t* cancel;             // [2][kStageMax]
     int32_t* ctl;                // [5]
+    int64_t* freq;               // [L*E] use counts
+    const int32_t* use_freq;     // 1: frequency-aware eviction (read on the device, so a
+                                 // captured graph follows later changes)
 };
 
 // Exclusive rank of a flag among the workgroup's threads (thread order) and
@@ -90,22 +94,26 @@ __device__ int flag_rank(bool f, int* wsum, int& total) {
 }
 
 // Victims of layer l given the protected set `keep`: vic[r] = the slot of
-// rank r among evictable slots by (last use, slot); returns their number.
-// occ[c] receives each slot's occupant.  Ends with a barrier.
+// rank r among evictable slots by (last use, slot), or (uses, last use,
+// slot) when frequency-aware; returns their number.  occ[c] receives each
+// slot's occupant.  Ends with a barrier.
 __device__ int rank_victims(const DecideArgs& a, int l, const unsigned char* keep, int* occ,
-                            int64_t* lastl, unsigned char* evl, int* vic, int* wsum) {
+                            int64_t* lastl, int64_t* usel, unsigned char* evl, int* vic, int* wsum) {
     const int t = threadIdx.x;
+    const bool by_uses = *a.use_freq != 0;
     if (t < a.C) {
         const int e = a.slot[l * a.C + t];
         occ[t] = e;
         lastl[t] = a.last[l * a.C + t];
+        usel[t] = !by_uses ? 0 : e >= 0 ? a.freq[size_t(l) * a.E + e] : -1;
         evl[t] = e < 0 || !keep[e];
     }
     __syncthreads();
     if (t < a.C && evl[t]) {
-        const int64_t lt = lastl[t];
+        const int64_t lt = lastl[t], ut = usel[t];
         int r = 0;
-        for (int c = 0; c < a.C; ++c) r += evl[c] && (lastl[c] < lt || (lastl[c] == lt && c < t));
+        for (int c = 0; c < a.C; ++c)
+            r += evl[c] && (usel[c] < ut || (usel[c] == ut && (lastl[c] < lt || (lastl[c] == lt && c < t))));
         vic[r] = t;
     }
     int n;
@@ -130,6 +138,7 @@ __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
     __shared__ int occ[kMaxE];
     __shared__ int vic[kMaxE];
     __shared__ int64_t lastl[kMaxE];
+    __shared__ int64_t usel[kMaxE];
     __shared__ int wsum[kT / 64];
     __shared__ int cnt[3];               // used prefetches, wasted prefetches, staged overflow
     __shared__ int n_adm;
@@ -160,7 +169,7 @@ __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
         const int wh = t < a.E ? a.where[l * a.E + t] : -1;
         const bool hit = inU && wh >= 0, miss = inU && wh < 0;
         const int sj = t < a.E ? spos[t] : -1;           // staged for this layer
-        const int nV = rank_victims(a, l, keep, occ, lastl, evl, vic, wsum);
+        const int nV = rank_victims(a, l, keep, occ, lastl, usel, evl, vic, wsum);
         int n_hit, n_miss, n_dem;
         (void)flag_rank(hit, wsum, n_hit);
         const int mr = flag_rank(miss, wsum, n_miss);      // ascending expert order
@@ -181,6 +190,7 @@ __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
         }
         if (miss && mr >= nV && sj >= 0) atomicAdd(&cnt[2], 1);
         if (c >= 0) a.last[l * a.C + c] = a.stamp;
+        if (inU && *a.use_freq) a.freq[size_t(l) * a.E + t] += 1;   // after this layer's victims
         // the FFN reads resident experts from their slot, staged overflow from its
         // staging block, other overflow from host memory
         if (inU)
@@ -254,7 +264,7 @@ __global__ __launch_bounds__(kT) void decide_kernel(DecideArgs a) {
     const bool ranked_in = t < m;                       // f is valid here
     if (ranked_in) keep[f] = 1;
     __syncthreads();
-    const int nV2 = rank_victims(a, lp, keep, occ, lastl, evl, vic, wsum);
+    const int nV2 = rank_victims(a, lp, keep, occ, lastl, usel, evl, vic, wsum);
     const bool nonres = ranked_in && a.where[lp * a.E + f] < 0;
     int n_nonres;
     const int j = flag_rank(nonres, wsum, n_nonres);    // ranking order
@@ -321,6 +331,8 @@ struct DeviceCache {
     int32_t* sexp = nullptr;         // [2][kStageMax]
     int32_t* cancel = nullptr;       // [2][kStageMax]
     int32_t* ctl = nullptr;          // [5]
+    int64_t* freq = nullptr;         // [L*E]
+    int32_t* use_freq = nullptr;     // [1]
     int n_blocks = 0;                // arena blocks: L*C slots + staging
     int ns = 0;                      // staged positions per parity (0: prefetch into slots)
     bool permuted = false;           // staged prefetches have swapped slot blocks
@@ -346,7 +358,7 @@ void free_dc(DeviceCache* d) {
 // Layout of the decision state inside the cache arena (256-byte aligned).
 struct StateLayout {
     size_t slot, last, where, pending, stats, host, demand, n_demand, pf, n_pf, blk, sblk, sexp, cancel, ctl,
-        total;
+        freq, use_freq, total;
 };
 
 StateLayout state_layout(int L, int E, int C) {
@@ -369,6 +381,8 @@ StateLayout state_layout(int L, int E, int C) {
     y.sexp = take(2 * kStageMax * 4);
     y.cancel = take(2 * kStageMax * 4);
     y.ctl = take(5 * 4);
+    y.freq = take(LE * 8);
+    y.use_freq = take(4);
     y.total = off;
     return y;
 }
@@ -414,6 +428,8 @@ int device_cache_create(const PolicyState& ps, char* arena, size_t blob, int n_s
     d->sexp = reinterpret_cast<int32_t*>(state + y.sexp);
     d->cancel = reinterpret_cast<int32_t*>(state + y.cancel);
     d->ctl = reinterpret_cast<int32_t*>(state + y.ctl);
+    d->freq = reinterpret_cast<int64_t*>(state + y.freq);
+    d->use_freq = reinterpret_cast<int32_t*>(state + y.use_freq);
     d->n_blocks = int(LC) + n_stage;
     std::vector<int32_t> blk(LC);
     for (size_t i = 0; i < LC; ++i) blk[i] = int32_t(i);
@@ -438,6 +454,9 @@ int device_cache_create(const PolicyState& ps, char* arena, size_t blob, int n_s
     if (e == hipSuccess) e = hipMemcpy(d->blk, blk.data(), LC * 4, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(d->ctl, ctl, sizeof(ctl), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemset(d->cancel, 0, 2 * kStageMax * 4);
+    const int32_t uf = *ps.use_freq;
+    if (e == hipSuccess) e = hipMemcpy(d->freq, ps.freq, LE * 8, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d->use_freq, &uf, 4, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         set_error(std::string("expert_cache_set_device_policy: ") + hipGetErrorString(e));
         free_dc(d);
@@ -463,6 +482,10 @@ int device_cache_download(DeviceCache* d, const PolicyState& ps) {
     STMOE_HIP(hipMemcpy(ps.where, d->where, LE * 4, hipMemcpyDeviceToHost));
     STMOE_HIP(hipMemcpy(pend.data(), d->pending, LE * 4, hipMemcpyDeviceToHost));
     STMOE_HIP(hipMemcpy(st, d->stats, sizeof(st), hipMemcpyDeviceToHost));
+    int32_t uf = 0;
+    STMOE_HIP(hipMemcpy(ps.freq, d->freq, LE * 8, hipMemcpyDeviceToHost));
+    STMOE_HIP(hipMemcpy(&uf, d->use_freq, 4, hipMemcpyDeviceToHost));
+    *ps.use_freq = uf;
     for (size_t i = 0; i < LE; ++i) ps.pending[i] = char(pend[i] != 0);
     *ps.st = stmoe_cache_stats{st[0], st[1], st[2], st[3], st[4], st[5]};
     return STMOE_OK;
@@ -490,6 +513,18 @@ int device_cache_set_staged(DeviceCache* d, int ns) {
 }
 
 int device_cache_staged(const DeviceCache* d) { return d->ns; }
+
+int device_cache_set_counts(DeviceCache* d, const int64_t* counts) {
+    STMOE_HIP(hipStreamSynchronize(d->side));
+    STMOE_HIP(hipDeviceSynchronize());
+    const size_t LE = size_t(d->L) * d->E;
+    std::vector<int64_t> v(LE, 0);
+    if (counts) std::copy(counts, counts + LE, v.begin());
+    const int32_t uf = counts != nullptr;
+    STMOE_HIP(hipMemcpy(d->freq, v.data(), LE * 8, hipMemcpyHostToDevice));
+    STMOE_HIP(hipMemcpy(d->use_freq, &uf, 4, hipMemcpyHostToDevice));
+    return STMOE_OK;
+}
 
 int device_cache_stats(DeviceCache* d, stmoe_cache_stats* out) {
     STMOE_HIP(hipStreamSynchronize(d->side));
@@ -526,6 +561,7 @@ int device_cache_decide(DeviceCache* d, int layer, int next, const int32_t* idx,
     a.demand = d->demand; a.n_demand = d->n_demand;
     a.pf = d->pf + size_t(next) * kMaxE; a.n_pf = d->n_pf + next;
     a.blk = d->blk; a.ns = d->ns; a.sblk = d->sblk; a.sexp = d->sexp; a.cancel = d->cancel; a.ctl = d->ctl;
+    a.freq = d->freq; a.use_freq = d->use_freq;
     hipLaunchKernelGGL(decide_kernel, dim3(1), dim3(kT), 0, s, a);
     STMOE_LAUNCHED();
     return STMOE_OK;

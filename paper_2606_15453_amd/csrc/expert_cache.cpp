@@ -5,8 +5,8 @@
 //
 // stmoe_policy is the pure decision logic (no HIP calls): per-layer slot
 // partitions, least recently used with protection of the current ranked or
-// selected set, residency counted from copy issue so decisions never depend
-// on timing.  expert_cache wraps it with slots in an HBM arena, a demand and
+// selected set (or, frequency-aware, least used first, then least recently),
+// residency counted from copy issue so decisions never depend on timing.  expert_cache wraps it with slots in an HBM arena, a demand and
 // a side stream, and two events per slot (last copy into it, last reader of
 // it) that order every reuse.
 #include <algorithm>
@@ -22,14 +22,31 @@ struct stmoe_policy {
     std::vector<int64_t> last;      // [L*C] last use stamp
     std::vector<int> where;         // [L*E] slot of expert or -1
     std::vector<char> pending;      // [L*E] prefetched, not yet verified
+    std::vector<int64_t> freq;      // [L*E] use counts (frequency-aware eviction)
+    int use_freq = 0;               // 1: victims by (uses, last use, slot); 0: (last use, slot)
     stmoe_cache_stats st{};
 
+    int64_t uses(int l, int c) const {
+        const int e = slot[l * C + c];
+        return e >= 0 ? freq[size_t(l) * E + e] : -1;
+    }
     int victim(int l, const std::vector<char>& keep) const {
         int best = -1;
         for (int c = 0; c < C; ++c) {
             const int e = slot[l * C + c];
             if (e >= 0 && keep[e]) continue;
-            if (best < 0 || last[l * C + c] < last[l * C + best]) best = c;
+            if (best < 0) {
+                best = c;
+                continue;
+            }
+            if (use_freq) {
+                const int64_t u = uses(l, c), ub = uses(l, best);
+                if (u != ub) {
+                    if (u < ub) best = c;
+                    continue;
+                }
+            }
+            if (last[l * C + c] < last[l * C + best]) best = c;
         }
         return best;
     }
@@ -109,6 +126,8 @@ int policy_acquire(stmoe_policy* p, int l, const int32_t* needed, int n, int64_t
         ++p->st.demand;
     }
     for (int c : used) p->last[l * p->C + c] = stamp;
+    if (p->use_freq)
+        for (int f : U) ++p->freq[size_t(l) * p->E + f];
     for (int e = 0; e < p->E; ++e) {
         if (!p->pending[l * p->E + e]) continue;
         if (keep[e]) ++p->st.useful; else ++p->st.wasted;
@@ -134,6 +153,7 @@ extern "C" int stmoe_policy_create(int L, int E, int C, const int32_t* warm, stm
     p->last.assign(size_t(L) * C, 0);
     p->where.assign(size_t(L) * E, -1);
     p->pending.assign(size_t(L) * E, 0);
+    p->freq.assign(size_t(L) * E, 0);
     if (warm) {
         for (int l = 0; l < L; ++l)
             for (int c = 0; c < C; ++c) {
@@ -171,6 +191,46 @@ extern "C" int expert_cache_warm_sets(const int32_t* sel, int P, int B, int L, i
         std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return cnt[x] > cnt[y]; });
         for (int c = 0; c < C; ++c) out[size_t(l) * C + c] = c < E ? order[c] : -1;
     }
+    return STMOE_OK;
+}
+
+namespace stmoe {
+namespace {
+int policy_set_counts(stmoe_policy* p, const int64_t* counts) {
+    if (counts)
+        for (size_t i = 0; i < size_t(p->L) * p->E; ++i)
+            STMOE_CHECK(counts[i] >= 0, "use counts must be >= 0");
+    p->use_freq = counts != nullptr;
+    if (counts) std::copy(counts, counts + size_t(p->L) * p->E, p->freq.begin());
+    else std::fill(p->freq.begin(), p->freq.end(), 0);
+    return STMOE_OK;
+}
+}  // namespace
+}  // namespace stmoe
+
+extern "C" int stmoe_policy_set_counts(stmoe_policy* p, const int64_t* counts) {
+    clear_error();
+    STMOE_CHECK(p, "null policy");
+    return policy_set_counts(p, counts);
+}
+
+extern "C" int expert_cache_use_counts(const int32_t* sel, int P, int B, int L, int K, int E, int64_t* out) {
+    clear_error();
+    STMOE_CHECK(sel && out, "null pointer");
+    STMOE_CHECK(P >= 1 && B >= 1 && L >= 1 && K >= 1 && E >= 1 && E <= kMaxE, "bad shape");
+    std::fill(out, out + size_t(L) * E, int64_t(0));
+    std::vector<int> seen(E, -1);
+    for (int l = 0; l < L; ++l)
+        for (int p = 0; p < P; ++p)
+            for (int b = 0; b < B; ++b)
+                for (int k = 0; k < K; ++k) {
+                    const int e = sel[((size_t(p) * B + b) * L + l) * K + k];
+                    STMOE_CHECK(e >= 0 && e < E, "selection index out of range");
+                    const int key = l * P + p;              // once per (layer, token)
+                    if (seen[e] == key) continue;
+                    seen[e] = key;
+                    ++out[size_t(l) * E + e];
+                }
     return STMOE_OK;
 }
 
@@ -267,7 +327,7 @@ namespace {
 PolicyState policy_state(expert_cache* c) {
     stmoe_policy* p = c->pol;
     return PolicyState{p->L, p->E, p->C, p->slot.data(), p->last.data(), p->where.data(), p->pending.data(),
-                       &p->st};
+                       p->freq.data(), &p->use_freq, &p->st};
 }
 }  // namespace
 }  // namespace stmoe
@@ -392,6 +452,8 @@ extern "C" int expert_cache_warm(expert_cache* c, const int32_t* warm) {
     if (int rc = stmoe_policy_create(c->L, c->E, c->C, warm, &np)) return rc;
     STMOE_HIP(hipStreamSynchronize(c->demand));
     STMOE_HIP(hipStreamSynchronize(c->side));
+    np->use_freq = c->pol->use_freq;       // the replacement rule and its counts stay
+    np->freq = c->pol->freq;
     stmoe_policy_destroy(c->pol);
     c->pol = np;
     reset_blocks(c);
@@ -602,6 +664,15 @@ extern "C" int expert_cache_set_staged_prefetch(expert_cache* c, int n_per_layer
     }
     c->head = head_bytes;
     return STMOE_OK;
+}
+
+extern "C" int expert_cache_set_counts(expert_cache* c, const int64_t* counts) {
+    clear_error();
+    STMOE_CHECK(c, "null cache");
+    if (counts)
+        for (size_t i = 0; i < size_t(c->L) * c->E; ++i) STMOE_CHECK(counts[i] >= 0, "use counts must be >= 0");
+    if (c->dev) return stmoe::device_cache_set_counts(c->dev, counts);
+    return policy_set_counts(c->pol, counts);
 }
 
 extern "C" int expert_cache_set_prefetch_order(expert_cache* c, int after_demand) {

@@ -96,6 +96,9 @@ _SIGS = {
     "moe_expert_ffn": (i32, [vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp, sz, vp]),
     "moe_expert_ffn_noalloc": (i32, [vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp]),
     "expert_cache_warm_sets": (i32, [vp, i32, i32, i32, i32, i32, i32, vp]),
+    "expert_cache_use_counts": (i32, [vp, i32, i32, i32, i32, i32, vp]),
+    "stmoe_policy_set_counts": (i32, [vp, vp]),
+    "expert_cache_set_counts": (i32, [vp, vp]),
     "stmoe_policy_create": (i32, [i32, i32, i32, vp, P(vp)]),
     "stmoe_policy_destroy": (i32, [vp]),
     "stmoe_policy_prefetch": (i32, [vp, i32, vp, i32, i64, vp]),
@@ -332,6 +335,22 @@ def warm_sets(sel, E, C_):
     return out
 
 
+def use_counts(sel, E):
+    """expert_cache_use_counts: per layer, profiling tokens selecting each expert ([L][E] int64)."""
+    sel = _i32(sel)
+    P_, B_, L_, K_ = sel.shape
+    out = np.zeros((L_, E), np.int64)
+    _call("expert_cache_use_counts", sel.ctypes.data, P_, B_, L_, K_, E, out.ctypes.data)
+    return out
+
+
+def _counts_ptr(counts):
+    if counts is None:
+        return None, None
+    a = np.ascontiguousarray(counts, np.int64)
+    return a, a.ctypes.data
+
+
 class Policy:
     def __init__(self, L, E, C_, warm=None):
         self.L, self.E, self.C = L, E, C_
@@ -363,6 +382,10 @@ class Policy:
         out = np.zeros((self.L, self.C), np.int32)
         _call("stmoe_policy_slots", self.h, out.ctypes.data)
         return out
+
+    def set_counts(self, counts):
+        keep, ptr = _counts_ptr(counts)
+        _call("stmoe_policy_set_counts", self.h, ptr)
 
     def stats(self):
         st = CacheStats()
@@ -419,6 +442,11 @@ class ExpertCache:
 
     def set_device_policy(self, on):
         _call("expert_cache_set_device_policy", self.h, int(on))
+
+    def set_counts(self, counts):
+        """Frequency-aware eviction seeded with counts [L][E], or least recently used (None)."""
+        keep, ptr = _counts_ptr(counts)
+        _call("expert_cache_set_counts", self.h, ptr)
 
     def set_staged_prefetch(self, n_per_layer, head_bytes=0):
         """Prefetch into spare staging blocks (at most n per layer); unused ones are cancelled

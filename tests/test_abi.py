@@ -77,12 +77,15 @@ def test_policy_hand_trace():
     assert p.stats() == g["counts"]
 
 
+@pytest.mark.parametrize("freq", [False, True])
 @pytest.mark.parametrize("E,C,K,L", [(8, 3, 2, 4), (128, 32, 8, 3), (64, 24, 6, 2), (16, 16, 4, 2)])
-def test_policy_matches_oracle_on_random_traces(E, C, K, L):
+def test_policy_matches_oracle_on_random_traces(E, C, K, L, freq):
     rng = np.random.default_rng(E * 100 + C)
     warm = [sorted(rng.choice(E, size=C, replace=False).tolist()) for _ in range(L)]
-    ref = CacheSim(L, E, C, warm)
+    counts = rng.integers(0, 6, size=(L, E)) if freq else None
+    ref = CacheSim(L, E, C, warm, counts=counts)
     p = S.Policy(L, E, C, warm)
+    p.set_counts(counts)
     for t in range(60):
         for l in range(L):
             stamp = t * L + l + 1
@@ -100,6 +103,25 @@ def test_policy_matches_oracle_on_random_traces(E, C, K, L):
     n = ref.n
     assert p.stats() == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
                              useful=n.useful, wasted=n.wasted)
+
+
+@pytest.mark.parametrize("P,B,L,K,E", [(5, 1, 4, 2, 8), (16, 4, 3, 6, 64), (3, 2, 2, 8, 16)])
+def test_use_counts_match_oracle(P, B, L, K, E):
+    from oracle.stmoe_oracle import use_counts
+    rng = np.random.default_rng(P * 7 + E)
+    sel = np.stack([np.stack([np.stack([rng.choice(E, K, replace=False) for _ in range(L)])
+                              for _ in range(B)]) for _ in range(P)]).astype(np.int32)
+    assert np.array_equal(S.use_counts(sel, E), use_counts(sel, L, E))
+
+
+def test_policy_counts_rejected_and_cleared():
+    p = S.Policy(1, 4, 2, [[0, 1]])
+    with pytest.raises(S.StmoeError):
+        p.set_counts([[0, -1, 0, 0]])
+    p.set_counts([[5, 1, 0, 0]])
+    assert p.acquire(0, [2], 1)[0] == [(2, 1)]          # expert 1 has fewer uses
+    p.set_counts(None)                                    # back to least recently used
+    assert p.acquire(0, [3], 2)[0] == [(3, 0)]          # slot 0 (expert 0) was used least recently
 
 
 def test_policy_rejects_bad_lists():

@@ -37,9 +37,9 @@ class Stack:
 
 
 def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True, tables=None, min_score=2,
-            max_per_layer=None, staged=0):
+            max_per_layer=None, staged=0, freq=False):
     from gpuhelp import expert_f64
-    from oracle.stmoe_oracle import decode_reference, decode_storage, moe_ffn
+    from oracle.stmoe_oracle import decode_reference, decode_storage, moe_ffn, use_counts
     cfg = st.cfg
 
     def ffn_of(l):
@@ -50,7 +50,8 @@ def _oracle(st, mode, C=None, ffn_tokens=0, renorm=False, online=True, tables=No
                             lambda l: decode_storage(st.wg[l]), st.prof, cfg.T, C=C,
                             warm=None if C is None else st.warm_ref, mode=mode, ffn_of=ffn_of,
                             ffn_tokens=ffn_tokens, renorm=renorm, online=online, tables=tables,
-                            min_score=min_score, max_per_layer=max_per_layer, staged=staged)
+                            min_score=min_score, max_per_layer=max_per_layer, staged=staged,
+                            counts=use_counts(st.prof, cfg.L, cfg.E) if freq else None)
 
 
 def _counts(n):
@@ -86,7 +87,7 @@ def _cumulative_after_layers(cache, L):
 def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0, device=0,
              device_until=None, device_pool=False, batch=False, C=None, import_tables=None,
              admission=None, layerwise=False, attn_bytes=0, reports=None, staged=0, head=0, graph=False,
-             timing_every=0):
+             timing_every=0, freq=None):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
@@ -114,7 +115,13 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
         cache = S.ExpertCache(cfg.L, cfg.E, C, cfg.blob_bytes, n_stage, arena, host, demand, side)
         cache.warm(st.warm if C == cfg.C else S.warm_sets(st.prof, cfg.E, C))
         cache.set_prefetch_order(after_demand)
+        # frequency-aware eviction: counts set before the device takes the state over, or after
+        counts = S.use_counts(st.prof, cfg.E) if freq else None
+        if freq == "before":
+            cache.set_counts(counts)
         cache.set_device_policy(device)
+        if freq == "after":
+            cache.set_counts(counts)
         if staged:
             cache.set_staged_prefetch(staged, head)
         ctx = S.DecodeContext(cfg.L, cfg.E, cfg.K, cfg.B, cfg.H, cfg.I, storage_dtype(cfg),
@@ -266,6 +273,43 @@ def test_decode_capped_counts_and_invariance(name, over, mode, after_demand, dev
     assert cst == dict(hits=n.hits, demand=n.demand, overflow=n.overflow, prefetch=n.prefetch,
                        useful=n.useful, wasted=n.wasted)
 
+
+
+@pytest.mark.parametrize("name,over", CFGS)
+@pytest.mark.parametrize("mode,device,staged,when", [(0, 0, 0, "before"), (1, 0, 0, "after"), (1, 0, 2, "before"),
+                                                     (0, 1, 0, "before"), (1, 1, 0, "after"), (1, 1, 2, "before")])
+def test_decode_capped_frequency_aware(name, over, mode, device, staged, when):
+    """Frequency-aware eviction (use counts seeded from profiling): the
+    oracle's decisions and counts with host or device decisions, prefetch into
+    slots or staged, the counts set before or after the device takes over; the
+    outputs stay bit-identical to the all-resident run."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    _, ys, _, cst = _run_gpu(st, mode, capped=True, device=device, staged=staged, freq=when)
+    for t in range(cfg.T):
+        assert np.array_equal(ys[t], ys_res[t])
+    ref = _oracle(st, mode, C=cfg.C, staged=staged, freq=True)
+    assert cst == _counts(ref["cache"].n)
+
+
+@pytest.mark.parametrize("name,over", [CFGS[1], CFGS[2]])
+def test_decode_frequency_aware_handover_and_graph(name, over):
+    """The use counts move with the policy state (device decisions handed back
+    to the host mid-run) and live in device memory under graph replay: counts
+    as the oracle's, outputs bit-identical to the all-resident run."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS[name].scaled(**over)
+    st = Stack(cfg)
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    ref = _counts(_oracle(st, 1, C=cfg.C, freq=True)["cache"].n)
+    _, ys_a, _, cst_a = _run_gpu(st, 1, capped=True, device=1, device_until=2, freq="before")
+    _, ys_b, _, cst_b = _run_gpu(st, 1, capped=True, device=1, graph=True, freq="after")
+    for t in range(cfg.T):
+        assert np.array_equal(ys_a[t], ys_res[t])
+        assert np.array_equal(ys_b[t], ys_res[t])
+    assert cst_a == ref and cst_b == ref
 
 
 @pytest.mark.parametrize("name,over", CFGS)

@@ -158,3 +158,60 @@ def test_staged_prefetch_keeps_on_demand_residency(E, C, K, S):
     assert st.n.demand + st.n.overflow + st.n.useful == od.n.demand + od.n.overflow
     outstanding = sum(len(x) for x in st.stage)
     assert st.n.useful + st.n.wasted + outstanding == st.n.prefetch
+
+
+def test_frequency_aware_eviction_hand_trace():
+    """counts seed the use counts; a victim has the smallest (uses, last use,
+    slot); every acquire adds 1 to each expert it is given.  Worked by hand:
+    E = 4, C = 2, slots [0, 1], counts [5, 1, 0, 0]."""
+    c = CacheSim(1, 4, 2, [[0, 1]], counts=[[5, 1, 0, 0]])
+    # {2}: expert 1 (1 use) goes, not expert 0 (5 uses), although both were last used at 0
+    assert c.acquire(0, [2], 1)[1] == [(2, 1)]
+    # {3}: expert 2 now has 1 use, expert 0 still 5
+    assert c.acquire(0, [3], 2)[1] == [(3, 1)]
+    # {0, 2}: 0 hits; 2 replaces 3 (the only slot outside the set)
+    assert c.acquire(0, [0, 2], 3)[1] == [(2, 1)]
+    # {1}: counts 0:6 1:1 2:2 3:1; slots hold 0 (6) and 2 (2): 2 goes
+    assert c.acquire(0, [1], 4)[1] == [(1, 1)]
+    # a prefetch of {3} evicts by the same rule (1 has 2 uses, 0 has 6)
+    assert c.prefetch(0, [3], 5) == [(3, 1)]
+    assert c.acquire(0, [3], 6)[1] == []
+    assert c.slot == [[0, 3]]
+    assert c.freq == [[6, 2, 2, 2]]
+    n = c.n
+    assert (n.hits, n.demand, n.overflow, n.prefetch, n.useful, n.wasted) == (2, 4, 0, 1, 1, 0)
+    # least recently used on the same first step evicts slot 0 (tie on last use, lower slot)
+    lru = CacheSim(1, 4, 2, [[0, 1]])
+    assert lru.acquire(0, [2], 1)[1] == [(2, 0)]
+
+
+def test_frequency_aware_eviction_fills_empty_slots_first():
+    c = CacheSim(1, 4, 3, [[0, -1, 1]], counts=[[0, 0, 0, 0]])
+    assert c.acquire(0, [2], 1)[1] == [(2, 1)]
+    # then the slot of least uses: 0 and 1 have none, 2 has one; tie on last use -> slot 0
+    assert c.acquire(0, [3], 2)[1] == [(3, 0)]
+
+
+def test_use_counts_by_hand():
+    from oracle.stmoe_oracle import use_counts
+    # three profiling tokens, two rows, one layer, top-1: {1, 1}, {0, 2}, {2, 2}
+    sel = np.array([[[[1]], [[1]]], [[[0]], [[2]]], [[[2]], [[2]]]])
+    assert use_counts(sel, 1, 4).tolist() == [[1, 1, 2, 0]]
+
+
+@pytest.mark.parametrize("E,C,K", [(8, 3, 2), (16, 4, 5)])
+def test_frequency_aware_invariants(E, C, K):
+    rng = np.random.default_rng(E * C)
+    L = 2
+    c = CacheSim(L, E, C, [list(range(C)) for _ in range(L)], counts=np.zeros((L, E), np.int64))
+    tot = 0
+    for t in range(40):
+        for l in range(L):
+            U = _random_sets(rng, 1, E, K)[0]
+            tot += len(U)
+            c.acquire(l, U, t * L + l + 1)
+            s = [v for v in c.slot[l] if v >= 0]
+            assert len(s) == len(set(s))
+    assert c.n.hits + c.n.demand + c.n.overflow == tot
+    # every acquire counted each of its experts once
+    assert sum(map(sum, c.freq)) == tot

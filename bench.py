@@ -346,9 +346,9 @@ def summarize_offload(paths):
     per workload): per variant, tokens/s, stall beyond the HBM-resident step,
     its reduction against on-demand loading, copies and prediction quality."""
     print("| workload | C of E | variant | tokens/s | ms per token | stall ms per token | stall reduction "
-          "vs on-demand | demand / overflow / prefetch (useful, wasted) copies | H2D GB/s | "
-          "recall l>=1 / l=0 / precision |")
-    print("|---|---|---|---|---|---|---|---|---|---|")
+          "vs on-demand | vs on-demand, same decisions and eviction | demand / overflow / prefetch (useful, "
+          "wasted) copies | H2D GB/s | recall l>=1 / l=0 / precision |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|")
     for p in paths:
         d = json.loads(open(p).read().strip().splitlines()[-1])
         o = d.get("offload")
@@ -356,16 +356,22 @@ def summarize_offload(paths):
             continue
         cfg = d["config"]
         red = o.get("stall_reduction", {})
-        for name, r in o.items():
-            if not isinstance(r, dict) or "tokens_per_s" not in r:
-                continue
+        runs = {n: r for n, r in o.items() if isinstance(r, dict) and "tokens_per_s" in r}
+
+        def policy(r):
+            return (r.get("device_decisions"), r.get("graph_replay"), r.get("eviction", "least recently used"))
+        base = {policy(r): r for n, r in runs.items() if n.startswith("on_demand")}
+        for name, r in runs.items():
             c = r["cache"]
             pq = (f"{r['recall_layers_ge1']:.3f} / {r['recall_layer0']:.3f} / {r['precision']:.3f}"
                   if "recall_layers_ge1" in r else "-")
             rd = red.get(name)
+            b = base.get(policy(r))
+            same = ("-" if name.startswith("on_demand") or b is None or b["stall_ms_per_token"] <= 0 else
+                    f"{1.0 - r['stall_ms_per_token'] / b['stall_ms_per_token']:+.3f}")
             print(f"| {cfg['workload']} | {o['cache_slots_per_layer']} of {cfg['experts']} | {name} | "
                   f"{r['tokens_per_s']} | {r['ms_per_token']} | {r['stall_ms_per_token']} | "
-                  f"{'-' if rd is None else f'{rd:+.3f}'} | {c['demand']} / {c['overflow']} / "
+                  f"{'-' if rd is None else f'{rd:+.3f}'} | {same} | {c['demand']} / {c['overflow']} / "
                   f"{c['prefetch']} ({c['useful']}, {c['wasted']}) | {r['h2d_gbps']} | {pq} |")
 
 
@@ -1017,6 +1023,16 @@ def offload(wl, n_tokens, resident_ms_per_token, pinned_gb, only=None):
     od = out["on_demand"]["stall_ms_per_token"]
     out["stall_reduction"] = {v["name"]: (round(1.0 - out[v["name"]]["stall_ms_per_token"] / od, 4) if od > 0
                                           else None) for v in variants if v["name"] != "on_demand"}
+    # prefetch against on-demand loading with the same decision site, graph use and eviction rule
+    base_of = {(v["device"], v["graph"], v["freq"]): v["name"] for v in variants if v["mode"] == S.MODE_ON_DEMAND}
+    same = {}
+    for v in variants:
+        b = base_of.get((v["device"], v["graph"], v["freq"]))
+        if v["mode"] != S.MODE_ON_DEMAND and b is not None:
+            ob = out[b]["stall_ms_per_token"]
+            same[v["name"]] = {"against": b, "reduction": round(1.0 - out[v["name"]]["stall_ms_per_token"] / ob, 4)
+                               if ob > 0 else None}
+    out["stall_reduction_vs_same_policy_on_demand"] = same
     out["cache_slots_per_layer"] = cfg.C
     out["host_pool"] = {"distinct_blobs": M, "experts": cfg.L * cfg.E, "slot_of_expert": "(l*E + e) mod distinct_blobs"}
     out["h2d_link"] = ("PCIe, pinned host memory, hipMemcpyAsync on demand/side streams" if POOL_TIER == "host" else

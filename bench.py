@@ -76,6 +76,9 @@ def parse():
                     help="capped-cache sweep over these per-layer budgets (markdown table; no JSON line)")
     ap.add_argument("--counters", action="store_true",
                     help="run the fixed workload profiled by the rocprofv3 --pmc passes and exit")
+    ap.add_argument("--counters-meta", default=None, metavar="JSON",
+                    help="where --counters writes the profiled workload's shapes and call counts "
+                         "(default counters_<config>.json in the working directory)")
     ap.add_argument("--predictor-sweep", action="store_true",
                     help="replay planted traces through the GPU predictor for every config and the paper's "
                          "Table 1 shapes; print recall/precision per ablation mode and exit")
@@ -185,17 +188,18 @@ def summarize_counters(fetch_csv, write_csv, meta_json):
     alg_up = per_call * 2 * mat
     alg_dn = per_call * mat
     cfg = meta["config"]
-    cmd_f = (f"rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/pmc_fetch -o fetch --output-format csv "
-             f"-- python -u $R/bench.py --counters --config {cfg}")
+    cmd_f = (f"rocprofv3 --pmc FETCH_SIZE -d $OUT/pmc_fetch -o fetch --output-format csv "
+             f"-- python -u $R/bench.py --counters --config {cfg} --counters-meta $OUT/counters_{cfg}.json")
     cmd_w = cmd_f.replace("FETCH_SIZE", "WRITE_SIZE").replace("pmc_fetch", "pmc_write").replace("-o fetch", "-o write")
     out = [
         f"# HBM traffic counters: ffn_gate_up / ffn_down, {meta['title']}",
         "",
-        "Commands (run from `/tmp` with `TMPDIR=/tmp`, repository at `$R`), one counter per run:",
+        "Commands (run from `/tmp` with `TMPDIR=/tmp`, repository at `$R`, output directory `$OUT`), one "
+        "counter per run:",
         "",
         "```", cmd_f, cmd_w,
         f"python bench.py --summarize-counters <fetch counter_collection.csv> <write counter_collection.csv> "
-        f"$R/gpurun_out/counters_{cfg}.json",
+        f"$OUT/counters_{cfg}.json",
         "```",
         "",
         f"The profiled workload runs {COUNTER_TOKENS} decode tokens of the HBM-resident stack ({per_call:.2f} "
@@ -389,11 +393,12 @@ def summarize_stats(path, title, cmd):
               f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
 
 
-def counters_workload(config="mixtral"):
+def counters_workload(config="mixtral", meta_path=None):
     """Fixed workload for the rocprofv3 --pmc passes: decode tokens of the
     resident stack of `config` (Mixtral shapes by default), then calibration
-    copies of known size.  Writes gpurun_out/counters_<config>.json with the
-    shapes, FFN calls and distinct experts of the profiled tokens."""
+    copies of known size.  Writes the shapes, FFN calls and distinct experts
+    of the profiled tokens as JSON to meta_path (default
+    counters_<config>.json in the working directory)."""
     import torch
     from paper_2606_15453_amd import stmoe as S
     from paper_2606_15453_amd import workload as W
@@ -415,10 +420,12 @@ def counters_workload(config="mixtral"):
     torch.cuda.synchronize()
     ctx.close()
     pred.close()
-    os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
     meta = dict(config=config, title=f"{cfg.name}, batch {cfg.B}", H=cfg.H, I=cfg.I, esz=cfg.wbytes,
                 n_shared=cfg.n_shared, n_calls=int(n_calls), n_experts=int(n_experts))
-    with open(os.path.join(ROOT, "gpurun_out", f"counters_{config}.json"), "w") as f:
+    path = meta_path or f"counters_{config}.json"
+    if os.path.dirname(path):
+        os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w") as f:
         json.dump(meta, f)
     log("counters workload done")
 
@@ -1637,7 +1644,7 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
     if args.counters:
-        counters_workload(args.config)
+        counters_workload(args.config, args.counters_meta)
         return
     if args.policy_bound:
         lines = policy_bound(args.policy_bound.split(","), max(args.offload_tokens, 1),

@@ -135,21 +135,24 @@ def test_full_size_decode_matches_oracle(name):
         torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("mode,device", [(0, 0), (1, 0), (1, 1)])
-def test_full_size_capped_cache(mode, device):
+@pytest.mark.parametrize("mode,device,freq", [(0, 0, False), (1, 0, False), (1, 1, False), (0, 1, True),
+                                             (1, 0, True)])
+def test_full_size_capped_cache(mode, device, freq):
     """DeepSeek-V2-Lite shapes at full size (26 layers, 64 routed experts of
     17.3 MB in a pinned host pool, 24 HBM slots per layer, two shared experts
     in HBM, batch 4), decoded as the bench's capped runs do: the cache's
     copy counts equal the oracle's cache policy, and every output is
     bit-identical to the all-resident run (on-demand loading and ST-MoE
-    prefetch; decisions on the host or on the device)."""
+    prefetch; decisions on the host or on the device; least recently used or
+    frequency-aware eviction)."""
     import torch
     from gpuhelp import DEV
-    from oracle.stmoe_oracle import decode_reference, decode_storage, warm_from_profile
+    from oracle.stmoe_oracle import decode_reference, decode_storage, use_counts, warm_from_profile
     from paper_2606_15453_amd import stmoe as S
     from paper_2606_15453_amd import workload as W
     cfg = W.CONFIGS["dsv2lite"]
-    print(f"[full-size capped] {cfg.name}: mode {mode}, device decisions {device}", flush=True)
+    print(f"[full-size capped] {cfg.name}: mode {mode}, device decisions {device}, frequency-aware {freq}",
+          flush=True)
     st = FullStack(cfg, N_TOKENS)
     pool = None
     try:
@@ -168,6 +171,11 @@ def test_full_size_capped_cache(mode, device):
         cache = S.ExpertCache(cfg.L, cfg.E, cfg.C, blob, n_stage, arena,
                               [pool.ptr + i * blob for i in range(cfg.L * cfg.E)], demand, side)
         cache.warm(warm)
+        counts_ref = use_counts(st.prof, cfg.L, cfg.E) if freq else None
+        if freq:
+            counts = S.use_counts(st.prof, cfg.E)
+            assert np.array_equal(counts, counts_ref)
+            cache.set_counts(counts)
         cache.set_device_policy(device)
         idx_hist, ys, _, _ = _gpu_decode(st, N_TOKENS, cache=cache, mode=mode)
         demand.synchronize()
@@ -179,7 +187,7 @@ def test_full_size_capped_cache(mode, device):
             assert torch.equal(ys[t], ys_res[t]), t
         ref = decode_reference(cfg.L, cfg.E, cfg.K, cfg.B, lambda t, l: decode_storage(st.x_store[t][l]),
                                lambda l: decode_storage(st.wg[l]), st.prof, N_TOKENS, C=cfg.C, warm=warm_ref,
-                               mode=mode)
+                               mode=mode, counts=counts_ref)
         assert ref["tie_boundary"] == 0
         n = ref["cache"].n
         print(f"[full-size capped] counts {cst}", flush=True)

@@ -89,6 +89,8 @@ def parse():
                     help="time one streaming-read launch per size, bytes in no cache (markdown table) and exit")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("KERNEL_TRACE_CSV", "TITLE", "COMMAND"),
                     help="median kernel durations per kernel and grid size of a rocprofv3 kernel trace")
+    ap.add_argument("--summarize-mfma", nargs=2, metavar=("COUNTER_CSV", "COMMAND"),
+                    help="MfmaUtil / bf16 MFMA operations of the MFMA kernels in a rocprofv3 --pmc pass")
     ap.add_argument("--summarize-policy", metavar="POLICY_BOUND_MD",
                     help="pivot a --policy-bound table by workload, link rate and attention window")
     ap.add_argument("--summarize-floor", nargs=2, metavar=("READ_FLOOR_TRACE_CSV", "FFN_SWEEP_TRACE_CSV"),
@@ -156,6 +158,31 @@ def counter_means(path, counter):
         s, n = acc.get(name, (0.0, 0))
         acc[name] = (s + v, n + 1)
     return {k: (s / n, n) for k, (s, n) in acc.items()}
+
+
+def summarize_mfma(path, cmd):
+    """Markdown: MfmaUtil and bf16 MFMA operations of the MFMA kernels in a
+    rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_BF16 pass, per kernel
+    and grid (one row per shape of the FFN sweep)."""
+    import csv
+    acc = {}
+    for r in csv.DictReader(open(path)):
+        name = r["Kernel_Name"].replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        if "mfma" not in name:
+            continue
+        key = (name.replace("stmoe::", ""), r.get("Grid_Size", "?"))
+        d = acc.setdefault(key, {})
+        s, n = d.get(r["Counter_Name"], (0.0, 0))
+        d[r["Counter_Name"]] = (s + float(r["Counter_Value"]), n + 1)
+    print("MFMA utilisation of the batched kernels (one counter pass over the FFN sweep):\n")
+    print(f"```\n{cmd}\n```\n")
+    print("| kernel | grid (threads) | dispatches | MfmaUtil (% of SIMD cycles with the MFMA unit busy) | "
+          "MFMA bf16 flops per dispatch (MOPS x 512) |")
+    print("|---|---|---|---|---|")
+    for (name, grid), d in acc.items():
+        u, n = d.get("MfmaUtil", (0.0, 0))
+        m, nm = d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", (0.0, 0))
+        print(f"| `{name}` | {grid} | {n} | {u / max(n, 1):.2f} | {m / max(nm, 1) * 512 / 1e9:.2f} G |")
 
 
 def summarize_counters(fetch_csv, write_csv, meta_json):
@@ -1630,6 +1657,9 @@ def main():
         return
     if args.summarize_policy:
         summarize_policy(args.summarize_policy)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma)
         return
     if args.summarize_offload:
         summarize_offload(args.summarize_offload)

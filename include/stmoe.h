@@ -439,8 +439,7 @@ int moe_decode_layer(moe_ctx* ctx, int token, int layer, const void* x, float* y
 int moe_ctx_set_prefetch(moe_ctx* ctx, int min_score, int max_per_layer);
 /* Online CCT update (Algorithm 3, Section 4.2) during decode: on (1, the
  * default) or frozen after profiling (0; HT rows are still overwritten with
- * each selection).  An ablation switch; fails once a graph has been
- * captured (the graph holds the setting it was captured with). */
+ * each selection).  An ablation switch. */
 int moe_ctx_set_online_update(moe_ctx* ctx, int on);
 /* All L layers of one token: xs device [L][B][H], ys device out [L][B][H].
  * With graph replay on (moe_ctx_set_graph), every call after the first whose
@@ -448,7 +447,10 @@ int moe_ctx_set_online_update(moe_ctx* ctx, int on);
  * copied into the context's input staging buffer, the graph runs, and the
  * output staging buffer is copied to ys (a copy is skipped when the pointer
  * is the staging buffer itself).  The graph is captured at the first such
- * call and again when `mode` changes; results equal the eager calls. */
+ * call and again when `mode`, a setting of the context (moe_ctx_set_prefetch,
+ * moe_ctx_set_online_update) or the cache's configuration (warm start,
+ * decision site, staged prefetch, prefetch order, replacement rule) has
+ * changed since; results equal the eager calls. */
 int moe_decode_token(moe_ctx* ctx, int token, const void* xs, float* ys, int mode);
 /* Per-token predictor launches for moe_decode_token (contexts without a
  * cache, with a predictor; on = 1 or 0, default 0).  Without a cache the

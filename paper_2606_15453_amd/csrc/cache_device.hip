@@ -504,10 +504,24 @@ int device_cache_set_staged(DeviceCache* d, int ns) {
     STMOE_HIP(hipStreamSynchronize(d->side));
     STMOE_HIP(hipDeviceSynchronize());
     if (ns > 0) {
-        // the staging blocks follow the slot blocks; positions of both parities
+        // the staging positions of both parities take the blocks no slot
+        // holds (staged prefetches may have swapped blocks between slots and
+        // staging positions before)
+        const size_t LC = size_t(d->L) * d->C;
+        std::vector<int32_t> blk(LC);
+        STMOE_HIP(hipMemcpy(blk.data(), d->blk, LC * 4, hipMemcpyDeviceToHost));
+        std::vector<char> held(size_t(d->n_blocks), 0);
+        for (int32_t b : blk) held[size_t(b)] = 1;
+        std::vector<int32_t> spare;
+        for (int b = 0; b < d->n_blocks; ++b)
+            if (!held[size_t(b)]) spare.push_back(b);
+        if (spare.size() < size_t(2 * ns)) {
+            set_error("expert_cache_set_staged_prefetch: internal error, too few spare blocks");
+            return STMOE_ESTATE;
+        }
         std::vector<int32_t> sblk(2 * kStageMax, -1);
         for (int p = 0; p < 2; ++p)
-            for (int j = 0; j < ns; ++j) sblk[size_t(p) * kStageMax + j] = d->L * d->C + p * ns + j;
+            for (int j = 0; j < ns; ++j) sblk[size_t(p) * kStageMax + j] = spare[size_t(p) * ns + j];
         const int32_t ctl[5] = {0, -1, -1, 0, 0};
         STMOE_HIP(hipMemcpy(d->sblk, sblk.data(), sblk.size() * 4, hipMemcpyHostToDevice));
         STMOE_HIP(hipMemcpy(d->ctl, ctl, sizeof(ctl), hipMemcpyHostToDevice));

@@ -30,6 +30,7 @@ int update_predict_seq(stmoe_predictor* p, const void* dev_args, int use, int on
 void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_bytes);
 DeviceCache* expert_cache_device(expert_cache* c);
 int expert_cache_after_demand(const expert_cache* c);
+uint64_t expert_cache_version(const expert_cache* c);
 void stmoe_shape(const stmoe_predictor* p, int* L, int* E, int* K, int* B);
 int fused_route_predict(const void* x, const void* w_gate, int H, int dtype, int renorm, int32_t* idx,
                         float* w, void* route_ws, stmoe_predictor* p, int layer, const int32_t* sel_prev,
@@ -113,6 +114,9 @@ struct moe_ctx {
     // inputs and outputs pass through the staging buffers
     bool graph_on = false;
     int graph_mode = -1;
+    uint64_t settings = 0;                 // bumped by the setters whose values a captured graph bakes in
+    uint64_t graph_settings = 0;           // ... and their value when the graph was captured,
+    uint64_t graph_cache_version = 0;      // with the cache's configuration version then
     hipStream_t gs = nullptr;
     hipEvent_t ev_in = nullptr, ev_out = nullptr;
     hipGraph_t graph = nullptr;
@@ -624,6 +628,13 @@ int token_side(moe_ctx* c, int token, int use) {
     return STMOE_OK;
 }
 
+// A captured graph bakes in the context's knobs and the cache's
+// configuration: it is stale once either changed.
+bool graph_stale(const moe_ctx* c) {
+    return c->graph_settings != c->settings ||
+           (c->cache && c->graph_cache_version != expert_cache_version(c->cache));
+}
+
 // Capture all L layers of one token, reading x_stage and writing y_stage,
 // into c->graph_exec.  The capture runs on the graph stream (the compute
 // stream may be the null stream, which cannot be captured).
@@ -676,6 +687,8 @@ int capture_token(moe_ctx* c, int token, int mode) {
     }
     c->graph = g;
     c->graph_mode = mode;
+    c->graph_settings = c->settings;
+    c->graph_cache_version = c->cache ? expert_cache_version(c->cache) : 0;
     return STMOE_OK;
 }
 
@@ -687,7 +700,7 @@ int decode_token_graph(moe_ctx* c, int token, const void* xs, float* ys, int mod
         set_error("moe_decode_token: graph replay with a cache needs device-side decisions");
         return STMOE_ESTATE;
     }
-    if (!c->graph_exec || c->graph_mode != mode)
+    if (!c->graph_exec || c->graph_mode != mode || graph_stale(c))
         if (int rc = capture_token(c, token, mode)) return rc;
     const size_t n = size_t(c->L) * c->B * c->H;
     STMOE_HIP(hipEventRecord(c->ev_in, c->s));
@@ -824,14 +837,15 @@ extern "C" int moe_ctx_set_prefetch(moe_ctx* c, int min_score, int max_per_layer
     STMOE_CHECK(min_score >= 0 && max_per_layer >= 0, "knobs must be >= 0");
     c->pf_min_score = min_score;
     c->pf_max = max_per_layer;
+    ++c->settings;
     return STMOE_OK;
 }
 
 extern "C" int moe_ctx_set_online_update(moe_ctx* c, int on) {
     clear_error();
     STMOE_CHECK(c, "null ctx");
-    STMOE_CHECK(!c->graph_exec, "set the online update before graph replay captures a token");
     c->online = on ? 1 : 0;
+    ++c->settings;
     return STMOE_OK;
 }
 

@@ -304,6 +304,7 @@ struct expert_cache {
     std::vector<int> sblk, sexp;         // [2][ns] block and staged expert of each position
     int cur = 0, stg_layer[2] = {-1, -1}, stg_n[2] = {0, 0};
     bool permuted = false;               // some slot lives outside its home block
+    uint64_t version = 0;                // bumped by every change of the cache's settings
 
     char* block_ptr(int b) const { return arena + size_t(b) * blob; }
     int ring() const { return n_stage - 2 * ns; }
@@ -318,6 +319,9 @@ void expert_cache_shape(const expert_cache* c, int* L, int* E, size_t* blob_byte
 }
 // Internal: the device decisions when switched on, and the prefetch order.
 DeviceCache* expert_cache_device(expert_cache* c) { return c->dev; }
+// Internal: changes whenever a setting that a captured decode graph bakes in
+// may have changed (residency, decision site, staged count, link order).
+uint64_t expert_cache_version(const expert_cache* c) { return c->version; }
 int expert_cache_after_demand(const expert_cache* c) {
     // staged prefetches only take the link once the missed loads are in
     return c->after_demand || (c->dev && device_cache_staged(c->dev) > 0);
@@ -444,6 +448,7 @@ extern "C" int expert_cache_destroy(expert_cache* c) {
 extern "C" int expert_cache_warm(expert_cache* c, const int32_t* warm) {
     clear_error();
     STMOE_CHECK(c && warm, "null pointer");
+    ++c->version;
     if (c->dev) {
         set_error("expert_cache_warm: device decisions are on");
         return STMOE_ESTATE;
@@ -617,6 +622,7 @@ extern "C" int expert_cache_set_device_policy(expert_cache* c, int on) {
     clear_error();
     STMOE_CHECK(c, "null cache");
     STMOE_CHECK(on == 0 || on == 1, "on must be 0 or 1");
+    ++c->version;
     if (bool(on) == (c->dev != nullptr)) return STMOE_OK;
     STMOE_HIP(hipStreamSynchronize(c->demand));
     STMOE_HIP(hipStreamSynchronize(c->side));
@@ -644,6 +650,7 @@ extern "C" int expert_cache_set_device_policy(expert_cache* c, int on) {
 extern "C" int expert_cache_set_staged_prefetch(expert_cache* c, int n_per_layer, size_t head_bytes) {
     clear_error();
     STMOE_CHECK(c, "null cache");
+    ++c->version;
     STMOE_CHECK(n_per_layer >= 0 && n_per_layer <= kMaxE, "n_per_layer must be in [0, 256]");
     if (c->dev) {
         STMOE_CHECK(2 * n_per_layer <= c->n_stage, "n_per_layer must be in [0, n_stage / 2]");
@@ -669,6 +676,7 @@ extern "C" int expert_cache_set_staged_prefetch(expert_cache* c, int n_per_layer
 extern "C" int expert_cache_set_counts(expert_cache* c, const int64_t* counts) {
     clear_error();
     STMOE_CHECK(c, "null cache");
+    ++c->version;
     if (counts)
         for (size_t i = 0; i < size_t(c->L) * c->E; ++i) STMOE_CHECK(counts[i] >= 0, "use counts must be >= 0");
     if (c->dev) return stmoe::device_cache_set_counts(c->dev, counts);
@@ -679,6 +687,7 @@ extern "C" int expert_cache_set_prefetch_order(expert_cache* c, int after_demand
     clear_error();
     STMOE_CHECK(c, "null cache");
     STMOE_CHECK(after_demand == 0 || after_demand == 1, "after_demand must be 0 or 1");
+    ++c->version;
     c->after_demand = after_demand;
     return STMOE_OK;
 }

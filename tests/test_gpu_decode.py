@@ -87,7 +87,7 @@ def _cumulative_after_layers(cache, L):
 def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0, device=0,
              device_until=None, device_pool=False, batch=False, C=None, import_tables=None,
              admission=None, layerwise=False, attn_bytes=0, reports=None, staged=0, head=0, graph=False,
-             timing_every=0, freq=None):
+             timing_every=0, freq=None, between=None):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
@@ -152,6 +152,8 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
     for t in range(cfg.T):
         if cache is not None and device_until is not None and t == device_until:
             cache.set_device_policy(0)       # the host policy takes over the device state
+        if between is not None:
+            between(t, ctx, cache)
         y = torch.empty((cfg.L, cfg.B, cfg.H), dtype=torch.float32, device=DEV)
         if layerwise:
             for l in range(cfg.L):
@@ -734,6 +736,40 @@ def test_graph_replay_capped_device_decisions(mode, staged, timing_every):
     assert cst_g == cst_e
     ref = _oracle(st, mode, C=cfg.C, staged=staged)
     assert cst_g == _counts(ref["cache"].n)
+
+
+def test_graph_replay_follows_setting_changes():
+    """Settings changed between replayed tokens (prefetch admission, the online
+    update, the staged count, the replacement rule) take effect at the next
+    token, as in eager calls: selections, outputs, predictor statistics and
+    cache counts equal an eager run with the same changes."""
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen30b"].scaled(L=4, T=10, P=3, C=10)
+    st = Stack(cfg)
+
+    def between(t, ctx, cache):
+        if t == 2:
+            ctx.set_prefetch(4, cfg.K)
+        if t == 4:
+            ctx.set_online_update(False)
+        if t == 6:
+            cache.set_staged_prefetch(1, 0)
+        if t == 8:
+            cache.set_counts(S.use_counts(st.prof, cfg.E))
+
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    print("[graph settings] eager", flush=True)
+    idx_e, ys_e, stats_e, cst_e = _run_gpu(st, 1, capped=True, device=1, staged=2, between=between)
+    for t in range(cfg.T):
+        assert np.array_equal(ys_e[t], ys_res[t]), t      # staging blocks never alias a slot
+    print("[graph settings] replay", flush=True)
+    idx_g, ys_g, stats_g, cst_g = _run_gpu(st, 1, capped=True, device=1, staged=2, graph=True, between=between)
+    for t in range(cfg.T):
+        assert np.array_equal(idx_g[t], idx_e[t]), t
+        assert np.array_equal(ys_g[t], ys_e[t]), t
+    assert np.array_equal(stats_g, stats_e)
+    assert cst_g == cst_e
 
 
 def test_graph_replay_refuses_host_decisions():

@@ -72,6 +72,9 @@ def parse():
                          "(expert (l, e) reads blob (l*E + e) mod their number)")
     ap.add_argument("--attention-sweep", default=None, metavar="CTX1,CTX2,...",
                     help="capped cache with a decode-attention stand-in of these context lengths (markdown)")
+    ap.add_argument("--copy-sweep", default=None, metavar="W1,W2,...",
+                    help="capped cache with device decisions at these copy-kernel workgroup counts: the expert "
+                         "tier's bandwidth as a measured sweep (markdown table; with --pool hbm up to TB/s)")
     ap.add_argument("--offload-sweep", default=None, metavar="C1,C2,...",
                     help="capped-cache sweep over these per-layer budgets (markdown table; no JSON line)")
     ap.add_argument("--counters", action="store_true",
@@ -916,6 +919,8 @@ def offload_run(wl, C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token,
     if freq:
         cache.set_counts(S.use_counts(wl.prof, cfg.E))
     cache.set_device_policy(device)
+    if v.get("copy_wgs"):
+        cache.set_copy_workgroups(v["copy_wgs"], v["copy_wgs"])
     if staged:
         cache.set_staged_prefetch(staged, head)
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
@@ -992,17 +997,19 @@ def W_warm(wl, C):
 
 
 def variant(name, mode, min_score=2, max_pf=None, online=1, after_demand=0, device=0, staged=0, head=0,
-            graph=0, freq=0):
+            graph=0, freq=0, copy_wgs=0):
     """One capped-cache run's settings: prediction mode, admission (min score,
     at most max_pf prefetches per layer; None = the cache's slots), online
     CCT update, prefetch copies after the missed loads, device-side
     decisions, staged prefetches per layer (0: prefetch into evicted slots),
     bytes of each staged expert copied up front with host decisions (-1: the
     layer's compute window at the link's rate, shared by the staged experts;
-    0: all of it), HIP graph replay of each token, and frequency-aware eviction
-    (use counts seeded from profiling) instead of least recently used."""
+    0: all of it), HIP graph replay of each token, frequency-aware eviction
+    (use counts seeded from profiling) instead of least recently used, and the
+    copy kernels' workgroups with device decisions (0: the defaults)."""
     return dict(name=name, mode=mode, min_score=min_score, max_pf=max_pf, online=online,
-                after_demand=after_demand, device=device, staged=staged, head=head, graph=graph, freq=freq)
+                after_demand=after_demand, device=device, staged=staged, head=head, graph=graph, freq=freq,
+                copy_wgs=copy_wgs)
 
 
 def offload_variants(cfg):
@@ -1167,6 +1174,59 @@ def offload_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, budgets):
     head = [f"| C per layer | variant | tokens/s | stall ms/token | stall reduction vs on-demand | hits | "
             f"demand + overflow copies | prefetch copies | useful prefetches | recall (l >= 1) | precision |",
             "|---|---|---|---|---|---|---|---|---|---|---|"]
+    return head + rows
+
+
+def copy_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, workgroups):
+    """The expert tier's bandwidth as a measured sweep: with device decisions
+    the copy kernels' workgroup count sets the copy rate (from the pinned host
+    pool, or from the HBM pool with --pool hbm, up to TB/s).  Per count: the
+    rate of stmoe_calib_copy_grid on the same pool, then on-demand loading,
+    ST-MoE prefetch (into slots and staged) and frequency-aware on-demand
+    loading, all with that many copy workgroups.  Markdown lines."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    cfg = wl.cfg
+    pool, ptrs, M = expert_pool(wl, pinned_gb, POOL_TIER)
+    n_stage = staging_slots(cfg, cfg.C)
+    arena = torch.empty(S.cache_arena_bytes(cfg.L, cfg.E, cfg.C, cfg.blob_bytes, n_stage), dtype=torch.uint8,
+                        device="cuda:0")
+    streams = (torch.cuda.Stream(), torch.cuda.Stream())
+    dst = torch.empty(cfg.blob_bytes, dtype=torch.uint8, device="cuda:0")
+    n_st = STAGED_PER_LAYER(cfg)
+    rows = []
+    for n in workgroups:
+        srcs = [ptrs[(7919 * i) % len(ptrs)] for i in range(8)]
+        S.calib_copy_grid(srcs[0], dst.data_ptr(), cfg.blob_bytes, n)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for src in srcs:
+            S.calib_copy_grid(src, dst.data_ptr(), cfg.blob_bytes, n)
+        e1.record()
+        torch.cuda.synchronize()
+        gbps = len(srcs) * cfg.blob_bytes / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        vs = [variant("on_demand_device", S.MODE_ON_DEMAND, device=1, copy_wgs=n),
+              variant("st_moe_device", S.MODE_STMOE, device=1, copy_wgs=n),
+              variant("st_moe_staged_device", S.MODE_STMOE, after_demand=1, device=1, staged=n_st, copy_wgs=n),
+              variant("on_demand_device_freq", S.MODE_ON_DEMAND, device=1, freq=1, copy_wgs=n)]
+        base = None
+        for v in vs:
+            rec = offload_run(wl, cfg.C, arena, ptrs, streams, v, n_tokens, resident_ms_per_token)
+            if base is None:
+                base = rec["stall_ms_per_token"]
+            red = 1.0 - rec["stall_ms_per_token"] / base if base > 0 else float("nan")
+            c = rec["cache"]
+            rows.append(f"| {n} | {gbps:.1f} | {v['name']} | {rec['tokens_per_s']} | {rec['stall_ms_per_token']} | "
+                        f"{red:+.3f} | {c['demand']} / {c['overflow']} / {c['prefetch']} ({c['useful']}, "
+                        f"{c['wasted']}) |")
+            log(f"copy sweep {n} workgroups ({gbps:.1f} GB/s) {v['name']}: {rec['tokens_per_s']} tok/s")
+    del arena, dst
+    del pool
+    head = [f"HBM-resident reference: {resident_ms_per_token:.3f} ms/token; {n_tokens} tokens per run; pool: "
+            f"{POOL_TIER}",
+            "| copy workgroups | copy GB/s | variant | tokens/s | stall ms/token | stall reduction vs on-demand "
+            "(same copy rate) | demand / overflow / prefetch (useful, wasted) copies |",
+            "|---|---|---|---|---|---|---|"]
     return head + rows
 
 
@@ -1708,6 +1768,13 @@ def main():
         res_ms = 1e3 * r["seconds"] / 40
         lines = attention_sweep(wl, args.config, max(args.offload_tokens, 1), res_ms, args.pinned_gb, contexts)
         print(f"HBM-resident reference: {res_ms:.3f} ms/token; {max(args.offload_tokens, 1)} tokens per run")
+        print("\n".join(lines), flush=True)
+        return
+    if args.copy_sweep:
+        r = hbm_resident(wl, 40, 5)
+        res_ms = 1e3 * r["seconds"] / 40
+        lines = copy_sweep(wl, max(args.offload_tokens, 1), res_ms, args.pinned_gb,
+                           [int(c) for c in args.copy_sweep.split(",")])
         print("\n".join(lines), flush=True)
         return
     if args.offload_sweep:

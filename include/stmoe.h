@@ -320,6 +320,14 @@ int expert_cache_set_prefetch_order(expert_cache* c, int after_demand);
  * kernel keeps them, also under graph replay).  expert_cache_warm keeps the
  * rule and the counts.  [sync] with device decisions, [host] otherwise. */
 int expert_cache_set_counts(expert_cache* c, const int64_t* counts);
+/* Workgroups of the copy kernels that move experts with device decisions:
+ * missed loads (default 64, enough to fill the host link) and prefetches
+ * (default 16: fewer leave the concurrent FFN most of the chip); 0 restores
+ * a default, values above 1024 return STMOE_EINVAL.  Fewer workgroups lower
+ * the achieved copy rate (a throttled link for bandwidth sweeps); more raise
+ * it for a pool in device memory.  Kept across device-policy switches; host
+ * decisions copy with DMA and ignore it.  [host] */
+int expert_cache_set_copy_workgroups(expert_cache* c, int demand, int prefetch);
 /* Device-side decisions (Section 4.3.4's missed loading and prefetch
  * without a host round trip).  on = 1: the policy state moves to device
  * memory and moe_decode_layer takes its decisions in a one-workgroup kernel
@@ -522,6 +530,11 @@ int moe_ctx_stage_timing(moe_ctx* ctx, double* route_ms, double* miss_ms, double
  *     return STMOE_EINVAL.
  * ---------------------------------------------------------------------- */
 int stmoe_calib_copy(const void* src, void* dst, size_t bytes, void* stream);
+/* The same copy on `workgroups` workgroups (1..1024, else STMOE_EINVAL) with
+ * the expert cache's copy-kernel access pattern (four 16-byte chunks in
+ * flight per thread, non-temporal): the copy rate that workgroup count
+ * reaches, from pinned host memory or device memory. */
+int stmoe_calib_copy_grid(const void* src, void* dst, size_t bytes, int workgroups, void* stream);
 size_t stmoe_calib_read_out_words(size_t bytes, int pattern);
 int stmoe_calib_read(const void* src, size_t bytes, int pattern, unsigned* out, void* stream);
 

@@ -38,6 +38,9 @@ int device_cache_set_staged(DeviceCache* d, int ns);
 // Frequency-aware eviction with these use counts ([L*E] host), or least
 // recently used (counts null).  [sync]
 int device_cache_set_counts(DeviceCache* d, const int64_t* counts);
+// Workgroups of the copy kernels for missed loads and prefetches (0: the
+// defaults, 64 and 16).  Takes effect for copies launched afterwards.
+void device_cache_set_copy_workgroups(DeviceCache* d, int demand, int prefetch);
 int device_cache_staged(const DeviceCache* d);
 int device_cache_download(DeviceCache* d, const PolicyState& ps);
 void device_cache_destroy(DeviceCache* d);

@@ -338,6 +338,8 @@ struct DeviceCache {
     int32_t* ctl = nullptr;          // [5]
     int64_t* freq = nullptr;         // [L*E]
     int32_t* use_freq = nullptr;     // [1]
+    int demand_wgs = kBlitWgs;       // copy kernel workgroups: missed loads ...
+    int prefetch_wgs = kPrefetchWgs; // ... and prefetches
     int n_blocks = 0;                // arena blocks: L*C slots + staging
     int ns = 0;                      // staged positions per parity (0: prefetch into slots)
     bool permuted = false;           // staged prefetches have swapped slot blocks
@@ -533,6 +535,11 @@ int device_cache_set_staged(DeviceCache* d, int ns) {
 
 int device_cache_staged(const DeviceCache* d) { return d->ns; }
 
+void device_cache_set_copy_workgroups(DeviceCache* d, int demand, int prefetch) {
+    d->demand_wgs = demand > 0 ? demand : kBlitWgs;
+    d->prefetch_wgs = prefetch > 0 ? prefetch : kPrefetchWgs;
+}
+
 int device_cache_set_counts(DeviceCache* d, const int64_t* counts) {
     STMOE_HIP(hipStreamSynchronize(d->side));
     STMOE_HIP(hipDeviceSynchronize());
@@ -589,7 +596,8 @@ int device_cache_decide(DeviceCache* d, int layer, int next, const int32_t* idx,
 int device_cache_demand(DeviceCache* d, int layer, hipStream_t s) {
     // slots of `layer` written by an earlier prefetch are read from here on
     if (d->pf_set[layer]) STMOE_HIP(hipStreamWaitEvent(s, d->pf_done[layer], 0));
-    hipLaunchKernelGGL(blit_kernel, dim3(kBlitWgs), dim3(256), 0, s, d->demand, d->n_demand, d->blob / 16);
+    hipLaunchKernelGGL(blit_kernel, dim3(unsigned(d->demand_wgs)), dim3(256), 0, s, d->demand, d->n_demand,
+                       d->blob / 16);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }
@@ -600,7 +608,7 @@ int device_cache_prefetch(DeviceCache* d, int next, hipStream_t s) {
     // when it reads them too)
     STMOE_HIP(hipEventRecord(d->ev_decided, s));
     STMOE_HIP(hipStreamWaitEvent(d->side, d->ev_decided, 0));
-    hipLaunchKernelGGL(blit_kernel, dim3(kPrefetchWgs), dim3(256), 0, d->side, d->pf + size_t(next) * kMaxE,
+    hipLaunchKernelGGL(blit_kernel, dim3(unsigned(d->prefetch_wgs)), dim3(256), 0, d->side, d->pf + size_t(next) * kMaxE,
                        d->n_pf + next, d->blob / 16);
     STMOE_LAUNCHED();
     STMOE_HIP(hipEventRecord(d->pf_done[next], d->side));

@@ -2,6 +2,10 @@
 //   stmoe_calib_copy   reads n bytes and writes n bytes (16-byte vector copy);
 //                      its FETCH_SIZE / WRITE_SIZE counter readings give the
 //                      factor that turns those counters into bytes.
+//   stmoe_calib_copy_grid  the same copy on a given number of workgroups,
+//                      four 16-byte chunks in flight per thread, non-temporal
+//                      (the access pattern of the expert cache's copy kernels):
+//                      the copy rate a given workgroup count reaches.
 //   stmoe_calib_read   reads n bytes with the same non-temporal 16-byte loads
 //                      as the expert FFN and writes one word per workgroup:
 //                      the achievable streaming-read bandwidth of the chip,
@@ -20,6 +24,19 @@ constexpr int kThreads = 256;
 __global__ __launch_bounds__(kThreads) void calib_copy_kernel(const uint4* src, uint4* dst, size_t n) {
     const size_t stride = size_t(gridDim.x) * kThreads;
     for (size_t i = size_t(blockIdx.x) * kThreads + threadIdx.x; i < n; i += stride) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(kThreads) void calib_copy4_kernel(const u32x4* src, u32x4* dst, size_t n) {
+    const size_t stride = size_t(gridDim.x) * kThreads;
+    size_t k = size_t(blockIdx.x) * kThreads + threadIdx.x;
+    for (; k + 3 * stride < n; k += 4 * stride) {
+        u32x4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = __builtin_nontemporal_load(src + k + u * stride);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) __builtin_nontemporal_store(v[u], dst + k + u * stride);
+    }
+    for (; k < n; k += stride) __builtin_nontemporal_store(__builtin_nontemporal_load(src + k), dst + k);
 }
 
 __global__ __launch_bounds__(kThreads) void calib_read_kernel(const char* src, size_t n, unsigned* out) {
@@ -101,6 +118,18 @@ extern "C" int stmoe_calib_copy(const void* src, void* dst, size_t bytes, void* 
     const size_t n = bytes / 16;
     hipLaunchKernelGGL(calib_copy_kernel, dim3(grid_for(n)), dim3(kThreads), 0, as_stream(stream),
                        reinterpret_cast<const uint4*>(src), reinterpret_cast<uint4*>(dst), n);
+    STMOE_LAUNCHED();
+    return STMOE_OK;
+}
+
+extern "C" int stmoe_calib_copy_grid(const void* src, void* dst, size_t bytes, int workgroups, void* stream) {
+    clear_error();
+    STMOE_CHECK(src && dst && bytes > 0 && bytes % 16 == 0, "null pointer or size not a multiple of 16");
+    STMOE_CHECK((reinterpret_cast<uintptr_t>(src) & 15) == 0 && (reinterpret_cast<uintptr_t>(dst) & 15) == 0,
+                "pointers must be 16-byte aligned");
+    STMOE_CHECK(workgroups >= 1 && workgroups <= 1024, "workgroups must be in [1, 1024]");
+    hipLaunchKernelGGL(calib_copy4_kernel, dim3(unsigned(workgroups)), dim3(kThreads), 0, as_stream(stream),
+                       reinterpret_cast<const u32x4*>(src), reinterpret_cast<u32x4*>(dst), bytes / 16);
     STMOE_LAUNCHED();
     return STMOE_OK;
 }

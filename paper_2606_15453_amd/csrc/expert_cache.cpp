@@ -305,6 +305,7 @@ struct expert_cache {
     int cur = 0, stg_layer[2] = {-1, -1}, stg_n[2] = {0, 0};
     bool permuted = false;               // some slot lives outside its home block
     uint64_t version = 0;                // bumped by every change of the cache's settings
+    int copy_wgs[2] = {0, 0};            // device decisions: copy kernel workgroups (0: defaults)
 
     char* block_ptr(int b) const { return arena + size_t(b) * blob; }
     int ring() const { return n_stage - 2 * ns; }
@@ -633,9 +634,12 @@ extern "C" int expert_cache_set_device_policy(expert_cache* c, int on) {
             return STMOE_ESTATE;
         }
         for (auto& h : c->held) h.clear();
-        return stmoe::device_cache_create(stmoe::policy_state(c), c->arena, c->blob, c->n_stage, c->host.data(),
-                                          c->arena + slots_bytes(c->L, c->C, c->blob, c->n_stage), c->side,
-                                          &c->dev);
+        const int rc = stmoe::device_cache_create(stmoe::policy_state(c), c->arena, c->blob, c->n_stage,
+                                                  c->host.data(), c->arena + slots_bytes(c->L, c->C, c->blob,
+                                                                                         c->n_stage),
+                                                  c->side, &c->dev);
+        if (rc == STMOE_OK) stmoe::device_cache_set_copy_workgroups(c->dev, c->copy_wgs[0], c->copy_wgs[1]);
+        return rc;
     }
     const int rc = stmoe::device_cache_download(c->dev, stmoe::policy_state(c));
     if (rc != STMOE_OK) return rc;       // the device keeps deciding
@@ -681,6 +685,18 @@ extern "C" int expert_cache_set_counts(expert_cache* c, const int64_t* counts) {
         for (size_t i = 0; i < size_t(c->L) * c->E; ++i) STMOE_CHECK(counts[i] >= 0, "use counts must be >= 0");
     if (c->dev) return stmoe::device_cache_set_counts(c->dev, counts);
     return policy_set_counts(c->pol, counts);
+}
+
+extern "C" int expert_cache_set_copy_workgroups(expert_cache* c, int demand, int prefetch) {
+    clear_error();
+    STMOE_CHECK(c, "null cache");
+    STMOE_CHECK(demand >= 0 && demand <= 1024 && prefetch >= 0 && prefetch <= 1024,
+                "workgroup counts must be in [0, 1024]");
+    ++c->version;
+    c->copy_wgs[0] = demand;
+    c->copy_wgs[1] = prefetch;
+    if (c->dev) stmoe::device_cache_set_copy_workgroups(c->dev, demand, prefetch);
+    return STMOE_OK;
 }
 
 extern "C" int expert_cache_set_prefetch_order(expert_cache* c, int after_demand) {

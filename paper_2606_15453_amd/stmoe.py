@@ -132,6 +132,8 @@ _SIGS = {
     "moe_ctx_stage_timing": (i32, [vp, P(C.c_double), P(C.c_double), P(C.c_double), P(C.c_double), P(i64)]),
     "stmoe_calib_copy": (i32, [vp, vp, sz, vp]),
     "stmoe_calib_read_out_words": (sz, [sz, i32]),
+    "stmoe_calib_copy_grid": (i32, [vp, vp, sz, i32, vp]),
+    "expert_cache_set_copy_workgroups": (i32, [vp, i32, i32]),
     "stmoe_calib_read": (i32, [vp, sz, i32, vp, vp]),
 }
 
@@ -443,6 +445,10 @@ class ExpertCache:
     def set_device_policy(self, on):
         _call("expert_cache_set_device_policy", self.h, int(on))
 
+    def set_copy_workgroups(self, demand=0, prefetch=0):
+        """Copy-kernel workgroups with device decisions (0: defaults)."""
+        _call("expert_cache_set_copy_workgroups", self.h, int(demand), int(prefetch))
+
     def set_counts(self, counts):
         """Frequency-aware eviction seeded with counts [L][E], or least recently used (None)."""
         keep, ptr = _counts_ptr(counts)
@@ -557,6 +563,11 @@ def calib_copy(src, dst, nbytes, stream=None):
 def calib_read(src, nbytes, out, stream=None, pattern=0):
     """Streaming read of nbytes: pattern 0 grid stride, 1 contiguous 256 KiB per workgroup."""
     _call("stmoe_calib_read", _p(src), nbytes, int(pattern), _p(out), _s(stream))
+
+
+def calib_copy_grid(src_ptr, dst_ptr, nbytes, workgroups, stream=None):
+    """stmoe_calib_copy_grid between raw device-accessible addresses."""
+    _call("stmoe_calib_copy_grid", src_ptr, dst_ptr, nbytes, int(workgroups), _s(stream))
 
 
 def calib_read_out_words(nbytes, pattern=0):

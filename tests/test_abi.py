@@ -52,6 +52,9 @@ def test_invalid_arguments_rejected_without_device_work():
     assert S.calib_read_out_words((32 << 10) + 16, 2) == 2
     assert S._lib.stmoe_calib_read(256, 1 << 20, 3, 256, None) == S.EINVAL
     assert S._lib.stmoe_calib_read(256 + 8, 1 << 20, 2, 256, None) == S.EINVAL      # misaligned
+    assert S._lib.stmoe_calib_copy_grid(256, 512, 1 << 20, 0, None) == S.EINVAL     # workgroups in [1, 1024]
+    assert S._lib.stmoe_calib_copy_grid(256, 512, 1 << 20, 1025, None) == S.EINVAL
+    assert S._lib.expert_cache_set_copy_workgroups(None, 4, 4) == S.EINVAL
 
 
 def test_pack_expert_is_concatenation():

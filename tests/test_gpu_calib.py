@@ -31,3 +31,15 @@ def test_calib_read_checksums(pattern, nbytes):
         assert n_out == -(-nbytes // REGION[pattern])
         for w in range(n_out):
             assert got[w] == np.bitwise_xor.reduce(words[w * r:(w + 1) * r]), w
+
+
+@pytest.mark.parametrize("workgroups", [1, 3, 64, 1024])
+@pytest.mark.parametrize("nbytes", [16, (1 << 20) + 48, 9 << 20])
+def test_calib_copy_grid_copies_every_byte(workgroups, nbytes):
+    rng = np.random.default_rng(workgroups + nbytes)
+    src = torch.from_numpy(rng.integers(0, 256, nbytes, dtype=np.uint8)).to(DEV)
+    dst = torch.zeros(nbytes + 64, dtype=torch.uint8, device=DEV)
+    S.calib_copy_grid(src.data_ptr(), dst.data_ptr(), nbytes, workgroups)
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:nbytes], src)
+    assert int(dst[nbytes:].sum()) == 0          # nothing written past the end

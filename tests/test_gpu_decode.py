@@ -87,7 +87,7 @@ def _cumulative_after_layers(cache, L):
 def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_demand=0, device=0,
              device_until=None, device_pool=False, batch=False, C=None, import_tables=None,
              admission=None, layerwise=False, attn_bytes=0, reports=None, staged=0, head=0, graph=False,
-             timing_every=0, freq=None, between=None):
+             timing_every=0, freq=None, between=None, copy_wgs=None):
     import torch
     from gpuhelp import DEV, storage_dtype
     from paper_2606_15453_amd import stmoe as S
@@ -119,6 +119,8 @@ def _run_gpu(st, mode, capped, renorm=False, online=True, tables=None, after_dem
         counts = S.use_counts(st.prof, cfg.E) if freq else None
         if freq == "before":
             cache.set_counts(counts)
+        if copy_wgs is not None:
+            cache.set_copy_workgroups(*copy_wgs)
         cache.set_device_policy(device)
         if freq == "after":
             cache.set_counts(counts)
@@ -736,6 +738,21 @@ def test_graph_replay_capped_device_decisions(mode, staged, timing_every):
     assert cst_g == cst_e
     ref = _oracle(st, mode, C=cfg.C, staged=staged)
     assert cst_g == _counts(ref["cache"].n)
+
+
+@pytest.mark.parametrize("copy_wgs,staged", [((1, 1), 0), ((3, 2), 0), ((200, 100), 0), ((2, 1), 2)])
+def test_decode_copy_workgroups(copy_wgs, staged):
+    """The copy kernels' workgroup counts (device decisions) change the copy
+    rate, not the decisions: counts as the oracle's and outputs bit-identical
+    to the all-resident run."""
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen30b"].scaled(L=4, T=6, P=3, C=10)
+    st = Stack(cfg)
+    _, ys_res, _, _ = _run_gpu(st, 1, capped=False)
+    _, ys, _, cst = _run_gpu(st, 1, capped=True, device=1, staged=staged, copy_wgs=copy_wgs)
+    for t in range(cfg.T):
+        assert np.array_equal(ys[t], ys_res[t])
+    assert cst == _counts(_oracle(st, 1, C=cfg.C, staged=staged)["cache"].n)
 
 
 def test_graph_replay_follows_setting_changes():

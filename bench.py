@@ -85,6 +85,9 @@ def parse():
     ap.add_argument("--predictor-sweep", action="store_true",
                     help="replay planted traces through the GPU predictor for every config and the paper's "
                          "Table 1 shapes; print recall/precision per ablation mode and exit")
+    ap.add_argument("--predictor-spread", action="store_true",
+                    help="recall/precision of the full predictor per workload over three trace seeds (markdown) "
+                         "and exit")
     ap.add_argument("--ffn-sweep", action="store_true",
                     help="time moe_expert_ffn on every config shape, weights in no cache (markdown table on "
                          "stdout) and exit")
@@ -458,6 +461,47 @@ def counters_workload(config="mixtral", meta_path=None):
     with open(path, "w") as f:
         json.dump(meta, f)
     log("counters workload done")
+
+
+def predictor_spread(seed_offsets=(0, 100, 200)):
+    """Recall and precision of the full predictor (CCT + HT, online update)
+    per workload over planted traces drawn with three seeds (the workload's,
+    +100, +200): mean and range.  Markdown lines."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    from paper_2606_15453_amd import workload as W
+    dev = "cuda:0"
+    out = ["| workload | seeds | recall l>=1 mean (min-max) | recall l0 mean (min-max) | precision mean (min-max) |",
+           "|---|---|---|---|---|"]
+    for name in ("tiny", "mixtral", "qwen30b", "qwen30b-b8", "dsv2lite", "qwen235b"):
+        vals = []
+        for off in seed_offsets:
+            cfg = W.CONFIGS[name].scaled(seed=W.CONFIGS[name].seed + off)
+            T = min(cfg.T, 128)
+            sel = W.planted_trace(cfg, n_tokens=cfg.P + T)
+            dsel = torch.from_numpy(np.ascontiguousarray(sel[cfg.P:].transpose(0, 2, 1, 3))).to(dev)
+            p = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
+            p.profile(sel[:cfg.P])
+            p.predict(-1, None, use=S.USE_HT)
+            for t in range(T):
+                for l in range(cfg.L):
+                    cur = dsel[t, l]
+                    p.update(l, dsel[t, l - 1] if l else None, cur)
+                    if l + 1 < cfg.L:
+                        p.predict(l, cur, use=S.USE_BOTH)
+                    else:
+                        p.predict(-1, None, use=S.USE_HT)
+            st = p.stats()
+            p.close()
+            vals.append((st[1:, 0].sum() / max(st[1:, 1].sum(), 1), st[0, 0] / max(st[0, 1], 1),
+                         st[:, 0].sum() / max(st[:, 2].sum(), 1)))
+        v = np.array(vals)
+        cells = [f"{v[:, i].mean():.3f} ({v[:, i].min():.3f}-{v[:, i].max():.3f})" for i in range(3)]
+        base = W.CONFIGS[name].seed
+        out.append(f"| {W.CONFIGS[name].name} | {', '.join(str(base + o) for o in seed_offsets)} | "
+                   + " | ".join(cells) + " |")
+        log(f"predictor spread {name} done")
+    return out
 
 
 def predictor_sweep():
@@ -1749,6 +1793,9 @@ def main():
         return
     if args.predictor_sweep:
         predictor_sweep()
+        return
+    if args.predictor_spread:
+        print("\n".join(predictor_spread()), flush=True)
         return
     global POOL_TIER
     POOL_TIER = args.pool

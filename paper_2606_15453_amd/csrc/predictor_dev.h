@@ -87,10 +87,7 @@ struct TableShared {
     __align__(16) uint8_t htnew[kMaxB * kMaxK];   // HT[layer] after the update
     __align__(16) int32_t prev[kMaxB * kMaxK];
     __align__(16) int32_t sel[kMaxB * kMaxK];
-    int32_t F[kMaxK];                 // actual set of the current row, ascending
-    uint8_t snap[kMaxK * kMaxK];      // entries before this row's update
-    uint8_t repl[kMaxK * kMaxK];      // slot is replaced
-    uint8_t absent[kMaxK * kMaxK];    // F[slot] is absent from the entry's snapshot
+    __align__(16) int32_t Fs[kMaxB * kMaxK];  // every row's actual set, ascending (row stride kMaxK)
     int mx[kMaxE];                    // max score over rows
     int whist[kThreads / 64][kScoreBins];  // per-wave histogram of candidate scores
     int greater[kScoreBins];          // candidates scoring above each value
@@ -168,89 +165,126 @@ __device__ __forceinline__ int predict_segs(const PredictArgs& a, TableShared& s
     return n;
 }
 
-// Algorithm 3 on CCT_{layer-1} for the entries selected at layer-1, rows
-// b = 0..B-1 in order; HT[layer][b] <- sorted selection; hits against the
-// prediction made for this layer.  One lane per (entry, slot).  Works on the
-// LDS image (staged by the caller), then writes the touched CCT entries, HT
-// and the hit counts back.  Loops over K run to kMaxK with a predicate so
-// their LDS reads issue together.  Ends with a barrier.
-__device__ void update_body(const UpdateArgs& a, TableShared& sh) {
-    const int tid = threadIdx.x, K = a.K, KK = a.K * a.K, E = a.E;
-    const bool cct = a.cidx != nullptr && a.online;
-    unsigned my_hits = 0, my_pred = 0;
-    if (tid == 0) { sh.hits = 0; sh.npred = 0; }
+// Algorithm 3 on CCT_{layer-1} for rows b = 0..B-1 in order.  Lane t of a
+// group of GS lanes (one wave holds whole groups) owns slot s = t % GS of
+// entry g = t / GS, the g-th expert of A_{layer-1}[b]; the entries of one row
+// are distinct, so the groups of a row are independent and only the order of
+// rows is serial.  Each lane reads its entry's whole snapshot with its own
+// slot (one LDS round trip per row: the next row's entry index is loaded a
+// row ahead, since the update never writes it), and the group's replaced
+// slots and absent experts meet in two ballots.  With GS = 8 (K <= 8) every
+// group sits in wave 0 and rows follow each other without a workgroup
+// barrier (a wave's LDS accesses complete in order); with GS = 16 groups
+// span the four waves and a barrier separates rows.  Loops run to GS with
+// reads that stay inside the LDS arrays, so their reads issue together.
+template <int GS>
+__device__ __forceinline__ void cct_rows(const UpdateArgs& a, TableShared& sh) {
+    constexpr bool one_wave = GS * GS <= 64;
+    const int t = threadIdx.x, K = a.K, E = a.E;
+    const int g = t / GS, s = t % GS, first = (t & 63) - s;
+    const bool on = g < K && s < K;
+    if (one_wave && t >= 64) return;
+    const unsigned gmask = (1u << K) - 1u;
+    int e = on ? sh.prev[g] : -1;
     for (int b = 0; b < a.B; ++b) {
-        const int32_t* cur = sh.sel + b * K;
-        if (tid < K) {
-            const int v = cur[tid];
-            int rank = 0;
+        const bool ok = e >= 0 && e < E;      // out-of-range selections are ignored
+        const int ec = ok ? e : 0;
+        const int32_t* F = sh.Fs + b * kMaxK;
+        const uint8_t* entry = sh.uidx + ec * K;   // + j < kMaxE * kMaxK for j < GS
+        int Fv[GS], snap[GS];
 #pragma unroll
-            for (int j = 0; j < kMaxK; ++j)
-                if (j < K) rank += cur[j] < v;
-            sh.F[rank] = v;
+        for (int j = 0; j < GS; ++j) {
+            Fv[j] = F[j];
+            snap[j] = entry[j];
         }
-        const bool upd = cct && tid < KK;
-        const int s = upd ? tid % K : 0, base = tid - s;
-        int e = 0, conf = 0;
-        bool upd_ok = upd;
-        if (upd) {
-            e = sh.prev[b * K + tid / K];
-            upd_ok = e >= 0 && e < E;      // out-of-range selections are ignored
-            sh.snap[tid] = upd_ok ? sh.uidx[e * K + s] : 0xff;
-            conf = upd_ok ? sh.uconf[e * K + s] : 1;
-        }
-        __syncthreads();
-        bool hit = false;
-        if (upd) {
-            const int f = sh.snap[tid], mine = sh.F[s];
-            bool held = false;
+        const int mine = F[s], f = entry[s];
+        int conf = sh.uconf[ec * K + s];
+        const int e_next = on && b + 1 < a.B ? sh.prev[(b + 1) * K + g] : -1;
+        bool hit = false, held = false;
 #pragma unroll
-            for (int j = 0; j < kMaxK; ++j)
-                if (j < K) {
-                    hit |= sh.F[j] == f;
-                    held |= sh.snap[base + j] == mine;
-                }
-            sh.repl[tid] = upd_ok && (!hit && conf == 0);
-            sh.absent[tid] = !held;
+        for (int j = 0; j < GS; ++j) {
+            hit |= j < K && Fv[j] == f;
+            held |= j < K && snap[j] == mine;
         }
-        __syncthreads();
-        if (upd_ok) {
+        // slots replaced in this entry, and experts of F absent from it
+        const unsigned long long rm = __ballot(ok && !hit && conf == 0);
+        const unsigned long long am = __ballot(on && !held);
+        if (ok) {
             if (hit) {
                 conf = min(conf + 1, kConfMax);
             } else if (conf > 0) {
                 conf -= 1;
             } else {
-                // the rank-th expert of F (ascending) absent from the entry's
-                // snapshot, rank = replaced slots before this one
-                int rank = 0, seen = 0, pick = -1;
+                // the rank-th absent expert of F (ascending), rank = replaced
+                // slots before this one
+                const int rank = __popc(unsigned(rm >> first) & gmask & ((1u << s) - 1u));
+                unsigned abs_ = unsigned(am >> first) & gmask;
 #pragma unroll
-                for (int q = 0; q < kMaxK; ++q)
-                    if (q < s) rank += sh.repl[base + q];
+                for (int q = 0; q < GS; ++q)
+                    if (q < rank) abs_ &= abs_ - 1u;
+                const int at = __ffs(abs_) - 1;
+                int pick = 0;
 #pragma unroll
-                for (int j = 0; j < kMaxK; ++j)
-                    if (j < K && sh.absent[base + j]) {
-                        if (seen == rank) pick = sh.F[j];
-                        ++seen;
-                    }
-                if (pick >= 0) sh.uidx[e * K + s] = uint8_t(pick);
+                for (int j = 0; j < GS; ++j) pick = j == at ? Fv[j] : pick;
+                if (abs_) sh.uidx[e * K + s] = uint8_t(pick);
                 conf = kConfInit;
             }
             sh.uconf[e * K + s] = uint8_t(conf);
         }
-        // verification against the prediction made for this layer
-        if (tid < K && cur[tid] >= 0 && cur[tid] < E && sh.pend[b * E + cur[tid]] >= kThreshold) ++my_hits;
-        for (int f = tid; f < E; f += kThreads) my_pred += sh.pend[b * E + f] >= kThreshold;
-        if (tid < K) {
-            sh.htnew[b * K + tid] = uint8_t(sh.F[tid]);
-            a.ht[b * K + tid] = uint8_t(sh.F[tid]);
-        }
+        e = e_next;
         // the next row may update the same entries
-        __syncthreads();
+        if (one_wave)
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        else
+            __syncthreads();
     }
+}
+
+// The verify step and Algorithm 3 for one layer: hits of the selection
+// against the prediction made for this layer, HT[layer][b] <- sorted
+// selection, then the CCT_{layer-1} entries of every row (cct_rows).  Works
+// on the LDS image (staged by the caller), then writes the touched CCT
+// entries, HT and the hit counts back.  Ends with a barrier.
+__device__ void update_body(const UpdateArgs& a, TableShared& sh) {
+    const int tid = threadIdx.x, K = a.K, E = a.E, BK = a.B * K;
+    const bool cct = a.cidx != nullptr && a.online;
+    // every row sorted ascending: a lane per selected expert finds its rank
+    // (reads past the last row stay inside sel: B, K <= 16)
+    for (int i = tid; i < BK; i += kThreads) {
+        const int32_t* row = sh.sel + (i / K) * K;
+        const int v = sh.sel[i];
+        int rank = 0;
+#pragma unroll
+        for (int j = 0; j < kMaxK; ++j) {
+            const int w = row[j];
+            rank += j < K && w < v;
+        }
+        sh.Fs[(i / K) * kMaxK + rank] = v;
+    }
+    unsigned my_hits = 0, my_pred = 0;
+    for (int i = tid; i < BK; i += kThreads) {
+        const int v = sh.sel[i];
+        if (v >= 0 && v < E) my_hits += sh.pend[(i / K) * E + v] >= kThreshold;
+    }
+    for (int i = tid; i < a.B * E; i += kThreads) my_pred += sh.pend[i] >= kThreshold;
+    if (tid == 0) { sh.hits = 0; sh.npred = 0; }
+    __syncthreads();
+    for (int i = tid; i < BK; i += kThreads) {
+        const uint8_t v = uint8_t(sh.Fs[(i / K) * kMaxK + i % K]);
+        sh.htnew[i] = v;
+        a.ht[i] = v;
+    }
+    if (cct) {
+        if (K <= 8)
+            cct_rows<8>(a, sh);
+        else
+            cct_rows<16>(a, sh);
+    }
+    __syncthreads();
     if (cct) {
         // write back every entry slot this layer's rows touched (duplicates
         // carry the same final value)
-        for (int i = tid; i < a.B * KK; i += kThreads) {
+        for (int i = tid; i < a.B * K * K; i += kThreads) {
             const int e = sh.prev[i / K], s = i % K;
             if (e >= 0 && e < E) {
                 a.cidx[e * K + s] = sh.uidx[e * K + s];
@@ -298,8 +332,10 @@ __device__ void predict_body(const PredictArgs& a, TableShared& sh) {
     int m = 0;
     if (f < E) {
 #pragma unroll
-        for (int b = 0; b < kMaxB; ++b)
-            if (b < a.B) m = max(m, sh.sc[b * E + f]);
+        for (int b = 0; b < kMaxB; ++b) {
+            const int v = sh.sc[b * E + f];      // inside sc for every b < kMaxB
+            m = max(m, b < a.B ? v : 0);
+        }
         if (a.mask) a.mask[f] = m >= kThreshold;
         if (a.max_score) a.max_score[f] = uint8_t(m);
     }

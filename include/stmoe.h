@@ -190,7 +190,9 @@ int moe_pack_expert(const void* w_gate, const void* w_up, const void* w_down, in
  * result does not depend on where the blobs live.
  *
  *   x            device [B][H] dtype
- *   topk_idx     device [B][K] int32 (< E), topk_w device [B][K] fp32
+ *   topk_idx     device [B][K] int32 (< E), topk_w device [B][K] fp32; an
+ *                entry outside [0, E) is ignored, and an expert repeated
+ *                within a row counts once, with its first entry's weight
  *   expert_ptrs  device array [E] of device blob pointers; only selected
  *                experts' entries are read
  *   shared_ptrs  device array [n_shared] of device blob pointers, or NULL

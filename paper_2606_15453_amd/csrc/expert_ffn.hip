@@ -53,6 +53,8 @@ constexpr int kMaxSlots = kMaxE + kMaxShared;
 constexpr int kDownWgTarget = 256;    // workgroups the MFMA down phase aims for
 constexpr int kMfmaMinB = 8;          // batch from which the MFMA kernels run
 constexpr int kUpInFlight = 2;        // 16-byte chunks per row in flight per lane (GEMV gate/up)
+constexpr bool kUpB1 = true;           // batch 1: the gate/up kernel that finds its slot in registers
+constexpr int kUpB1RouteMaxE = 64;     // ... and routes in registers up to this many experts
 constexpr int kShortRowChunks = 4;    // down rows with at most this many chunks per lane are short: ...
 constexpr int kDownInFlightShort = 4; // ... the lane-group down kernel loads a slot's chunks in one step
 constexpr bool kStageX = true;        // GEMV gate/up: token activations staged in LDS ...
@@ -509,6 +511,194 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_wg(FfnArgs a, int blocks
             for (int w = 0; w < kWaves; ++w) { gs += red[w][0][r][b]; us += red[w][1][r][b]; }
             store_act(a.act, act16, (size_t(j) * a.B + b) * a.I + i0 + r, slot_weight(a, p, j, b) * silu(gs) * us);
         }
+    }
+}
+
+// ---------------------------------------------------------------- batch 1
+// One token: every routed slot serves it, so the slot plan reduces to the
+// selection ordered by expert index.  The batch-1 gate/up kernel finds its
+// slot in registers, each wave on its own (no LDS plan, no barrier), and
+// loads the token's activation chunks beside the weight chunks; chunks are
+// summed in the lane-group kernel's order, so the activations are
+// bit-identical to that kernel's.
+
+// Value of lane `src` (uniform) of v: a scalar read, no LDS traffic.
+__device__ __forceinline__ int lane_i(int v, int src) { return __builtin_amdgcn_readlane(v, src); }
+__device__ __forceinline__ float lane_f(float v, int src) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src));
+}
+
+// n-th set bit (n >= 0) of a uniform 64-bit mask, or -1.
+__device__ __forceinline__ int nth_bit(unsigned long long m, int n) {
+    for (int q = 0; q < n && m; ++q) m &= m - 1ull;
+    return m ? __ffsll(m) - 1 : -1;
+}
+
+// Selection given: lane k < K holds idx[k].  Slots are the row's distinct
+// valid experts ascending; a repeated expert takes the weight of its first
+// entry (build_plan and slot_weight do the same).  Returns slot j's expert
+// (or -1 when j is not a routed slot) and the routed slot count.
+__device__ __forceinline__ int b1_given(const FfnArgs& a, int j, float& wj, int& n_routed) {
+    const int K = a.K, lane = threadIdx.x & 63;
+    int v = -1;
+    float wv = 0.f;
+    if (lane < K) {
+        v = a.idx[lane];
+        wv = a.w[lane];
+    }
+    const bool valid = lane < K && v >= 0 && v < a.E;
+    bool first = valid;
+#pragma unroll
+    for (int r = 0; r < kMaxK; ++r) first &= !(r < lane && lane_i(v, r) == v);
+    const unsigned long long fm = __ballot(first);
+    int place = 0;
+#pragma unroll
+    for (int r = 0; r < kMaxK; ++r) place += ((fm >> r) & 1ull) && lane_i(v, r) < v;
+    n_routed = __popcll(fm);
+    if (j >= n_routed) return -1;
+    const int src = __ffsll(__ballot(first && place == j)) - 1;
+    wj = lane_f(wv, src);
+    return lane_i(v, src);
+}
+
+// Router logits given (E <= 128): the router tail's softmax / top-K in
+// registers, lanes f and f + 64 holding expert f and f + 64.  The same order
+// keys and the same count of the keys that beat each expert (larger key, or
+// equal key at a lower index) give the same winners; the softmax sum takes
+// each lane's terms in the tail's order into the same wave sum, and lane k
+// holds the probability of the position-k winner as in the tail, so the
+// weights are bit-identical too.  Block 0 publishes idx/w.
+__device__ __forceinline__ int b1_routed(const FfnArgs& a, int j, float& wj, int& n_routed) {
+    const int E = a.E, K = a.K, lane = threadIdx.x & 63;
+    const float z0 = lane < E ? a.logits[lane] : 0.f;
+    const float z1 = lane + 64 < E ? a.logits[lane + 64] : 0.f;
+    const uint32_t k0 = lane < E ? gating::order_key(z0) : 0u;
+    const uint32_t k1 = lane + 64 < E ? gating::order_key(z1) : 0u;
+    int c0 = 0, c1 = 0;
+    const int e0 = E < 64 ? E : 64;
+#pragma unroll 8
+    for (int g = 0; g < e0; ++g) {
+        const uint32_t kg = uint32_t(lane_i(int(k0), g));
+        c0 += kg > k0 || (kg == k0 && g < lane);
+        c1 += kg > k1;
+    }
+#pragma unroll 8
+    for (int g = 64; g < E; ++g) {
+        const uint32_t kg = uint32_t(lane_i(int(k1), g - 64));
+        c0 += kg > k0;
+        c1 += kg > k1 || (kg == k1 && g < lane + 64);
+    }
+    const bool w0 = lane < E && c0 < K, w1 = lane + 64 < E && c1 < K;
+    const unsigned long long W0 = __ballot(w0), W1 = __ballot(w1);
+    // the row max is the logit of the position-0 winner
+    const unsigned long long t0 = __ballot(w0 && c0 == 0), t1 = __ballot(w1 && c1 == 0);
+    const float m = t0 ? lane_f(z0, __ffsll(t0) - 1) : lane_f(z1, __ffsll(t1) - 1);
+    float s = 0.f;
+    if (lane < E) s += expf(z0 - m);
+    if (lane + 64 < E) s += expf(z1 - m);
+    s = wave_sum(s);
+    // lane k < K: expert and probability of the position-k winner
+    int ek = 0;
+    for (int k = 0; k < K; ++k) {
+        const unsigned long long q0 = __ballot(w0 && c0 == k), q1 = __ballot(w1 && c1 == k);
+        const int f = q0 ? __ffsll(q0) - 1 : 64 + __ffsll(q1) - 1;
+        if (lane == k) ek = f;
+    }
+    const float zk0 = __shfl(z0, ek & 63, 64), zk1 = __shfl(z1, ek & 63, 64);
+    float p = 0.f;
+    if (lane < K) p = expf((ek < 64 ? zk0 : zk1) - m) / s;
+    const float wsum = wave_sum(p);
+    const float wt = a.renorm ? p / wsum : p;
+    if (blockIdx.x == 0 && threadIdx.x < K) {
+        const_cast<int32_t*>(a.idx)[lane] = ek;
+        const_cast<float*>(a.w)[lane] = wt;
+    }
+    n_routed = __popcll(W0) + __popcll(W1);
+    if (j >= n_routed) return -1;
+    const int n0 = __popcll(W0);
+    const int e = j < n0 ? nth_bit(W0, j) : 64 + nth_bit(W1, j - n0);
+    const int pos = e < 64 ? lane_i(c0, e) : lane_i(c1, e - 64);
+    wj = lane_f(wt, pos);
+    return e;
+}
+
+template <bool BF, int G, int R>
+__global__ __launch_bounds__(kThreads) void ffn_gate_up_b1(FfnArgs a, int blocks_per_slot, int act16) {
+    constexpr int esz = BF ? 2 : 4;
+    constexpr int U = kUpInFlight;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int j = blockIdx.x / blocks_per_slot;
+    float wj = 1.f;
+    int n_routed = 0;
+    const int e = a.logits ? b1_routed(a, j, wj, n_routed) : b1_given(a, j, wj, n_routed);
+    const char* blob;
+    if (e >= 0) {
+        blob = routed_blob(a, e);
+    } else if (j < n_routed + a.n_shared) {
+        wj = 1.f;
+        blob = reinterpret_cast<const char*>(a.sptr[j - n_routed]);
+    } else {
+        return;
+    }
+    const int grp = lane / G, g = lane % G;
+    const int i0 = (blockIdx.x % blocks_per_slot) * (kWaves * (64 / G) * R) + (wave * (64 / G) + grp) * R;
+    if (i0 >= a.I) return;   // I is a multiple of R
+    const size_t rowb = size_t(a.H) * esz;
+    const char* wg = blob + size_t(i0) * rowb;
+    const char* wu = blob + size_t(a.I) * rowb + size_t(i0) * rowb;
+    const char* xs = reinterpret_cast<const char*>(a.x);
+    const int cpr = int(rowb / 16);
+    float accg[R], accu[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) accg[r] = accu[r] = 0.f;
+    auto compute = [&](const uint4 (&qg)[R], const uint4 (&qu)[R], const uint4& qx) {
+        Chunk<BF> cx;
+        cx.unpack(qx);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            Chunk<BF> cg, cu;
+            cg.unpack(qg[r]);
+            cu.unpack(qu[r]);
+            accg[r] = dotc<BF>(cg, cx, accg[r]);
+            accu[r] = dotc<BF>(cu, cx, accu[r]);
+        }
+    };
+    int c = g;
+    for (; c + (U - 1) * G < cpr; c += U * G) {
+        uint4 qg[U][R], qu[U][R], qx[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                qg[u][r] = ld_stream(wg + r * rowb + size_t(c + u * G) * 16);
+                qu[u][r] = ld_stream(wu + r * rowb + size_t(c + u * G) * 16);
+            }
+            qx[u] = ld_cached(xs + size_t(c + u * G) * 16);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) compute(qg[u], qu[u], qx[u]);
+    }
+    if (c < cpr) {
+        uint4 qg[U][R], qu[U][R], qx[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c + u * G < cpr) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    qg[u][r] = ld_stream(wg + r * rowb + size_t(c + u * G) * 16);
+                    qu[u][r] = ld_stream(wu + r * rowb + size_t(c + u * G) * 16);
+                }
+                qx[u] = ld_cached(xs + size_t(c + u * G) * 16);
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c + u * G < cpr) compute(qg[u], qu[u], qx[u]);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float gs = seg_sum<G>(accg[r]);
+        const float us = seg_sum<G>(accu[r]);
+        if (g == 0) store_act(a.act, act16, size_t(j) * a.I + i0 + r, wj * silu(gs) * us);
     }
 }
 
@@ -1330,6 +1520,14 @@ int launch_gate_up_r(const FfnArgs& a, const Shape& s, hipStream_t st) {
     const int bps = (a.I + rows - 1) / rows;
     const size_t xbytes = size_t(a.B) * a.H * (BF ? 2 : 4);
     const int act16 = act_bf16<BF>(s, a.B);
+    if constexpr (kUpB1 && NB == 1) {
+        if (a.B == 1 && (!a.logits || a.E <= kUpB1RouteMaxE)) {
+            hipLaunchKernelGGL((ffn_gate_up_b1<BF, G, R>), dim3(unsigned(bps * s.slots)), dim3(kThreads), 0, st, a,
+                               bps, act16);
+            STMOE_LAUNCHED();
+            return STMOE_OK;
+        }
+    }
     if (kStageX && xbytes <= size_t(kXStageMax))
         hipLaunchKernelGGL((ffn_gate_up<BF, G, R, NB, true>), dim3(unsigned(bps * s.slots)), dim3(kThreads),
                            unsigned(xbytes), st, a, bps, act16);

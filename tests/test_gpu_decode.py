@@ -208,12 +208,19 @@ def test_decode_resident_matches_oracle(name, over):
 
 @pytest.mark.parametrize("over,renorm", [(dict(E=7, K=3, B=2, T=6, P=3), False),
                                          (dict(E=64, K=4, B=4, T=4, P=2, C=16), False),
-                                         (dict(B=3, T=6, P=3), True)])
+                                         (dict(B=3, T=6, P=3), True),
+                                         (dict(E=7, K=3, B=1, T=6, P=3), False),
+                                         (dict(E=64, K=6, B=1, n_shared=2, T=5, P=2, C=12), True),
+                                         (dict(E=64, K=16, B=1, T=4, P=2, C=20), False),
+                                         (dict(E=65, K=4, B=1, T=4, P=2, C=10), False),
+                                         (dict(E=32, K=4, B=1, T=4, P=2, C=10, dtype="bf16"), True)])
 def test_decode_resident_edge_shapes(over, renorm):
     """The FFN's in-kernel gating at its edges: E not a multiple of 4 (padded
-    keys), B*E = 256 (the largest routed in-kernel), renormalised weights.
+    keys), B*E = 256 (the largest routed in-kernel), renormalised weights; at
+    batch 1 the gating in registers of the batch-1 gate/up kernel (E up to 64,
+    K up to 16, shared experts, bf16) and above 64 experts the LDS prologue.
     Selections, outputs and hit counts as in the oracle; the capped run (router
-    tail kernel) gives bit-identical outputs."""
+    tail kernel, selection passed to the FFN) gives bit-identical outputs."""
     from gpuhelp import rel_l2
     from oracle.stmoe_oracle import MODE_STMOE
     from paper_2606_15453_amd import workload as W

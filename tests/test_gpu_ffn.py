@@ -8,13 +8,13 @@ pytestmark = pytest.mark.gpu
 TOL = 1e-2
 
 
-def _run_ffn(cfg, layer, idx, w, x_store, n_shared=0):
+def _gpu_ffn(cfg, layer, idx, w, x_store, n_shared=0):
+    """moe_expert_ffn on seeded blobs of the row's valid experts."""
     import torch
-    from gpuhelp import DEV, blob_dev, expert_f64, i32, ptr_array, rel_l2, storage_dtype, to_dev
-    from oracle.stmoe_oracle import decode_storage, moe_ffn
+    from gpuhelp import DEV, blob_dev, i32, ptr_array, storage_dtype, to_dev
     from paper_2606_15453_amd import stmoe as S
     B, K = idx.shape
-    sel = sorted(set(idx.ravel().tolist()))
+    sel = sorted(e for e in set(idx.ravel().tolist()) if 0 <= e < cfg.E)
     blobs = {e: blob_dev(cfg, layer, e) for e in sel}
     ptrs = [blobs[e].data_ptr() if e in blobs else 0 for e in range(cfg.E)]
     shared = [blob_dev(cfg, layer, s, shared=True) for s in range(n_shared)]
@@ -26,7 +26,13 @@ def _run_ffn(cfg, layer, idx, w, x_store, n_shared=0):
                  shared_ptrs=ptr_array([s.data_ptr() for s in shared]) if n_shared else None,
                  n_shared=n_shared)
     torch.cuda.synchronize()
-    got = y.cpu().numpy()
+    return y.cpu().numpy()
+
+
+def _run_ffn(cfg, layer, idx, w, x_store, n_shared=0):
+    from gpuhelp import expert_f64, rel_l2
+    from oracle.stmoe_oracle import decode_storage, moe_ffn
+    got = _gpu_ffn(cfg, layer, idx, w, x_store, n_shared)
     ref = moe_ffn(decode_storage(x_store), idx, w, lambda e: expert_f64(cfg, layer, e),
                   shared=[expert_f64(cfg, layer, s, shared=True) for s in range(n_shared)])
     return got, ref, rel_l2(got, ref)
@@ -41,7 +47,7 @@ def _inputs(cfg, B, K, seed, distinct_rows=True):
     return idx, w, W.to_storage(cfg, x)
 
 
-@pytest.mark.parametrize("name,B", [("tiny", 1), ("qwen30b", 1), ("qwen30b", 3), ("qwen30b-b8", 8),
+@pytest.mark.parametrize("name,B", [("tiny", 1), ("qwen30b", 1), ("dsv2lite", 1), ("qwen30b", 3), ("qwen30b-b8", 8),
                                     ("qwen30b-b8", 12), ("dsv2lite", 4), ("dsv2lite", 9),
                                     ("qwen235b", 16), ("qwen235b", 9), ("qwen235b", 2), ("qwen235b", 4),
                                     ("mixtral", 4), ("mixtral", 8)])
@@ -142,3 +148,30 @@ def test_ffn_deterministic():
     a, _, _ = _run_ffn(cfg, 2, idx, w, x)
     b, _, _ = _run_ffn(cfg, 2, idx, w, x)
     assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("name,row", [("qwen30b", [5, 9, 5, -1, 17, 9, 3, 130]), ("tiny", [3, 3]),
+                                      ("dsv2lite", [7, 200, 7, 1, 63, -5])])
+def test_ffn_repeated_and_out_of_range_entries(name, row):
+    """A selection row that repeats an expert or holds an index outside
+    [0, E): out-of-range entries are ignored and a repeated expert counts once,
+    with the weight of its first entry (batch 1 takes the register slot
+    lookup; batch 2 repeats the row and takes the slot plan).  Checked against
+    the oracle on the row's distinct valid entries."""
+    from paper_2606_15453_amd import workload as W
+    base = W.CONFIGS[name]
+    K = len(row)
+    for B in (1, 2):
+        cfg = base.scaled(B=B, K=K, E=max(base.E, K))
+        rng = np.random.default_rng(K + B)
+        idx = np.array([row] * B, dtype=np.int32)
+        w = (rng.random((B, K)) + 0.1).astype(np.float32)
+        x = W.to_storage(cfg, rng.normal(0, 1, (B, cfg.H)))
+        keep = [k for k in range(K) if 0 <= row[k] < cfg.E and row[k] not in row[:k]]
+        got = _gpu_ffn(cfg, 1, idx, w, x, n_shared=cfg.n_shared)
+        _, ref, _ = _run_ffn(cfg, 1, idx[:, keep].copy(), w[:, keep].copy(), x, n_shared=cfg.n_shared)
+        from gpuhelp import rel_l2
+        err = rel_l2(got, ref)
+        print(f"{name} B={B} row {row}: rel L2 against the oracle on {len(keep)} entries {err:.3e}")
+        assert np.isfinite(got).all() and err <= TOL
+

@@ -54,7 +54,7 @@ constexpr int kDownWgTarget = 256;    // workgroups the MFMA down phase aims for
 constexpr int kMfmaMinB = 8;          // batch from which the MFMA kernels run
 constexpr int kUpInFlight = 2;        // 16-byte chunks per row in flight per lane (GEMV gate/up)
 constexpr bool kUpB1 = true;           // batch 1: the gate/up kernel that finds its slot in registers
-constexpr int kUpB1RouteMaxE = 64;     // ... and routes in registers up to this many experts
+constexpr int kUpB1RouteMaxE = 128;    // ... and routes up to this many experts (in registers up to 64)
 constexpr int kShortRowChunks = 4;    // down rows with at most this many chunks per lane are short: ...
 constexpr int kDownInFlightShort = 4; // ... the lane-group down kernel loads a slot's chunks in one step
 constexpr bool kStageX = true;        // GEMV gate/up: token activations staged in LDS ...
@@ -622,15 +622,39 @@ __device__ __forceinline__ int b1_routed(const FfnArgs& a, int j, float& wj, int
     return e;
 }
 
+// Router logits given, 64 < E <= 128: too many experts for every wave to
+// rank on its own, so the workgroup runs the lane-group kernel's gating
+// (route_into_plan: the router tail's steps, bit-identical) and only skips
+// the slot plan after it: slot j is the j-th smallest of the K winners,
+// found in registers.
+__device__ __forceinline__ int b1_routed_lds(const FfnArgs& a, int j, float& wj, int& n_routed, Plan& p) {
+    const int K = a.K, lane = threadIdx.x & 63;
+    route_into_plan(a, p);
+    __syncthreads();
+    const int ek = lane < K ? p.idx[lane] : 0;
+    const float wk = lane < K ? p.w[lane] : 0.f;
+    n_routed = K;
+    if (j >= K) return -1;
+    int place = 0;
+#pragma unroll
+    for (int r = 0; r < kMaxK; ++r) place += r < K && lane_i(ek, r) < ek;
+    const int src = __ffsll(__ballot(lane < K && place == j)) - 1;
+    wj = lane_f(wk, src);
+    return lane_i(ek, src);
+}
+
 template <bool BF, int G, int R>
 __global__ __launch_bounds__(kThreads) void ffn_gate_up_b1(FfnArgs a, int blocks_per_slot, int act16) {
     constexpr int esz = BF ? 2 : 4;
     constexpr int U = kUpInFlight;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = blockIdx.x / blocks_per_slot;
+    __shared__ Plan p;
     float wj = 1.f;
     int n_routed = 0;
-    const int e = a.logits ? b1_routed(a, j, wj, n_routed) : b1_given(a, j, wj, n_routed);
+    const int e = !a.logits      ? b1_given(a, j, wj, n_routed)
+                  : a.E <= 64    ? b1_routed(a, j, wj, n_routed)
+                                 : b1_routed_lds(a, j, wj, n_routed, p);
     const char* blob;
     if (e >= 0) {
         blob = routed_blob(a, e);

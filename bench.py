@@ -128,14 +128,41 @@ CALIB_BYTES = 1 << 30
 COUNTER_TOKENS = 20
 
 
+def strip_c_comments(text):
+    """C/C++ source without its comments (// to the end of the line and
+    /* ... */), string and character literals kept as they are."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return "".join(out)
+
+
 def ffn_source_sha():
-    """Hash of the sources the gate/up kernel is built from (the FFN kernels,
-    the gating steps of their routing prologue, the shared helpers)."""
+    """Hash of the code the gate/up kernel is built from (the FFN kernels,
+    the gating steps of their routing prologue, the shared helpers), comments
+    removed: an edit of a comment leaves the kernel and its counters as
+    they were."""
     import hashlib
     h = hashlib.sha256()
     for path in FFN_SOURCES:
-        with open(path, "rb") as f:
-            h.update(f.read())
+        with open(path, encoding="utf-8") as f:
+            h.update(strip_c_comments(f.read()).encode())
     return h.hexdigest()[:16]
 
 

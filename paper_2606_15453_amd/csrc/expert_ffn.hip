@@ -517,10 +517,11 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_wg(FfnArgs a, int blocks
 // ---------------------------------------------------------------- batch 1
 // One token: every routed slot serves it, so the slot plan reduces to the
 // selection ordered by expert index.  The batch-1 gate/up kernel finds its
-// slot in registers, each wave on its own (no LDS plan, no barrier), and
-// loads the token's activation chunks beside the weight chunks; chunks are
-// summed in the lane-group kernel's order, so the activations are
-// bit-identical to that kernel's.
+// slot in registers, each wave on its own (no LDS plan; with the selection
+// given or up to 64 experts to route, no barrier either), and loads the
+// token's activation chunks beside the weight chunks; chunks are summed in
+// the lane-group kernel's order, so the activations are bit-identical to
+// that kernel's.
 
 // Value of lane `src` (uniform) of v: a scalar read, no LDS traffic.
 __device__ __forceinline__ int lane_i(int v, int src) { return __builtin_amdgcn_readlane(v, src); }
@@ -561,8 +562,9 @@ __device__ __forceinline__ int b1_given(const FfnArgs& a, int j, float& wj, int&
     return lane_i(v, src);
 }
 
-// Router logits given (E <= 128): the router tail's softmax / top-K in
-// registers, lanes f and f + 64 holding expert f and f + 64.  The same order
+// Router logits given (used up to 64 experts, correct up to 128): the router
+// tail's softmax / top-K in registers, lanes f and f + 64 holding expert f
+// and f + 64.  The same order
 // keys and the same count of the keys that beat each expert (larger key, or
 // equal key at a lower index) give the same winners; the softmax sum takes
 // each lane's terms in the tail's order into the same wave sum, and lane k

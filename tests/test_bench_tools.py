@@ -83,3 +83,17 @@ def test_summarize_floor_interpolates_the_read_floor(tmp_path):
         assert abs(float(l.split("|")[6]) - 5000) <= 0.01 * 5000, l
     for l in dn:
         assert abs(float(l.split("|")[6]) - 4000) <= 0.01 * 4000, l
+
+
+def test_strip_c_comments_keeps_code_and_literals():
+    """The FFN source hash ignores comments: line and block comments go,
+    string and character literals (which may hold comment markers) stay."""
+    import bench
+    src = ('int a = 1; // line\n/* block\n over lines */ const char* s = "x // y /* z */";\n'
+           "char q = '\"'; char e = '\\\\'; int b; /**/ int c;\n")
+    out = bench.strip_c_comments(src)
+    assert "line" not in out and "block" not in out and "over lines" not in out
+    assert '"x // y /* z */"' in out and "'\"'" in out and "'\\\\'" in out
+    assert "int a = 1;" in out and "int b;" in out and "int c;" in out
+    # a comment-only edit leaves the stripped text unchanged
+    assert bench.strip_c_comments(src.replace("// line", "// another note")) == out

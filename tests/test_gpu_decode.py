@@ -213,7 +213,9 @@ def test_decode_resident_matches_oracle(name, over):
                                          (dict(E=64, K=6, B=1, n_shared=2, T=5, P=2, C=12), True),
                                          (dict(E=64, K=16, B=1, T=4, P=2, C=20), False),
                                          (dict(E=65, K=4, B=1, T=4, P=2, C=10), False),
-                                         (dict(E=32, K=4, B=1, T=4, P=2, C=10, dtype="bf16"), True)])
+                                         (dict(E=32, K=4, B=1, T=4, P=2, C=10, dtype="bf16"), True),
+                                         (dict(E=16, K=16, B=1, T=3, P=2, C=16), True),
+                                         (dict(E=2, K=1, B=1, T=4, P=2, C=1), False)])
 def test_decode_resident_edge_shapes(over, renorm):
     """The FFN's in-kernel gating at its edges: E not a multiple of 4 (padded
     keys), B*E = 256 (the largest routed in-kernel), renormalised weights; at

@@ -883,6 +883,15 @@ def run_tokens(ctx, wl, first, n, y, mode):
         ctx.token(t, wl.x[t % T], y, mode=mode)
 
 
+def repeat_summary(tokens, seconds):
+    """tokens/s of back-to-back timed runs of the same length (the first is
+    `value`), their median and their spread (max - min over the median)."""
+    rates = sorted(tokens / t for t in seconds)
+    med = rates[len(rates) // 2]
+    return {"runs": len(seconds), "tokens_per_s": [round(tokens / t, 3) for t in seconds],
+            "median": round(med, 3), "spread": round((rates[-1] - rates[0]) / med, 4)}
+
+
 def hbm_resident(wl, steps, warmup):
     import torch
     from paper_2606_15453_amd import stmoe as S
@@ -913,13 +922,22 @@ def hbm_resident(wl, steps, warmup):
     up_ms, down_ms, n_calls, n_exp = ctx.timing()
     route_ms, _, ffn_ms, pred_ms, n_timed = ctx.stage_timing()
     stats = pred.stats()
+    # the same timed run twice more (next tokens of the trace): the spread of
+    # the rate; the statistics above cover the first run only
+    repeats = []
+    for k in range(2):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run_tokens(ctx, wl, warmup + (k + 1) * steps, steps, y, S.MODE_STMOE)
+        torch.cuda.synchronize()
+        repeats.append(time.perf_counter() - t0)
     ctx.close()
     pred.close()
     per = 1e3 / max(n_timed, 1)
     stages = {"route_logits": round(route_ms * per, 2), "ffn_with_routing": round(ffn_ms * per, 2),
               "predict_side_stream": round(pred_ms * per, 2)}
     return dict(seconds=dt, up_ms=up_ms, down_ms=down_ms, n_calls=n_calls, n_experts=n_exp, stats=stats,
-                host_issue_us_per_layer=host_us, stages_us=stages)
+                host_issue_us_per_layer=host_us, stages_us=stages, repeat_seconds=repeats)
 
 
 #: host-to-HBM copy rate (GB/s): the latest on-demand run's copied bytes over its time
@@ -1879,6 +1897,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "repeats": repeat_summary(cfg.B * args.steps, [r["seconds"]] + r["repeat_seconds"]),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -97,3 +97,12 @@ def test_strip_c_comments_keeps_code_and_literals():
     assert "int a = 1;" in out and "int b;" in out and "int c;" in out
     # a comment-only edit leaves the stripped text unchanged
     assert bench.strip_c_comments(src.replace("// line", "// another note")) == out
+
+
+def test_repeat_summary():
+    """Rates of repeated timed runs: the first is the reported value, the
+    median and the spread summarise all of them."""
+    import bench
+    r = bench.repeat_summary(200, [0.8, 0.5, 1.0])
+    assert r["runs"] == 3 and r["tokens_per_s"] == [250.0, 400.0, 200.0]
+    assert r["median"] == 250.0 and r["spread"] == round((400 - 200) / 250, 4)

@@ -802,8 +802,16 @@ __device__ __forceinline__ void down_slot(const char* wd, size_t rowb, int cpr, 
 }
 
 // down_slot for bf16 activations (16 bytes per chunk and token, the same
-// chunk layout as a W_down row; weights unpacked as they are used).
-template <bool BF, int R, int NB, int U, bool CARRY>
+// chunk layout as a W_down row; weights unpacked as they are used).  With
+// TOKENS (and no CARRY) the step's weight chunks are loaded first and then,
+// token by token, all of that token's activation chunks of the step
+// together: one wait per token instead of one per chunk (an activation load
+// waits for every load issued before it).  Every accumulator still adds its
+// chunks in ascending order, so the order of the token loop does not change a
+// sum.  Lane-group kernel, DeepSeek-V2-Lite shapes at batch 4: 30.6 -> 29.2 us
+// per launch; the whole-workgroup kernel (Mixtral shapes) keeps the per-chunk
+// loads, about 1% faster there.
+template <bool BF, int R, int NB, int U, bool CARRY, bool TOKENS = false>
 __device__ __forceinline__ void down_slot16(const char* wd, size_t rowb, int cpr, int c0, int S,
                                             const char* act, unsigned tm, float (&acc)[R][NB]) {
     static_assert(BF, "bf16 activations go with bf16 weights");
@@ -827,6 +835,25 @@ __device__ __forceinline__ void down_slot16(const char* wd, size_t rowb, int cpr
             for (int r = 0; r < R; ++r) acc[r][b] = dotq<BF>(w[r], cx, acc[r][b]);
         }
     };
+    // TOKENS: token-outer over a step whose weights are in registers
+    auto tokens = [&](int c, const uint4 (&q)[U][R], bool guarded) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            if (!((tm >> b) & 1u)) continue;
+            uint4 xv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (!guarded || c + u * S < cpr) xv[u] = ld_cached(act + size_t(b) * rowb + size_t(c + u * S) * 16);
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (!guarded || c + u * S < cpr) {
+                    Chunk<BF> cx;
+                    cx.unpack(xv[u]);
+#pragma unroll
+                    for (int r = 0; r < R; ++r) acc[r][b] = dotq<BF>(q[u][r], cx, acc[r][b]);
+                }
+        }
+    };
     int c = c0;
     for (; c + (U - 1) * S < cpr; c += U * S) {
         uint4 q[U][R];
@@ -835,10 +862,14 @@ __device__ __forceinline__ void down_slot16(const char* wd, size_t rowb, int cpr
         for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int r = 0; r < R; ++r) q[u][r] = ld_stream(wd + r * rowb + size_t(c + u * S) * 16);
+        if constexpr (TOKENS && !CARRY) {
+            tokens(c, q, false);
+        } else {
 #pragma unroll
-        for (int u = 0; u < U; ++u) load_x(c + u * S, xv[u]);
+            for (int u = 0; u < U; ++u) load_x(c + u * S, xv[u]);
 #pragma unroll
-        for (int u = 0; u < U; ++u) compute(c + u * S, q[u], xv[u]);
+            for (int u = 0; u < U; ++u) compute(c + u * S, q[u], xv[u]);
+        }
     }
     if (c < cpr) {      // fewer than U steps left: one guarded step
         uint4 q[U][R];
@@ -848,12 +879,16 @@ __device__ __forceinline__ void down_slot16(const char* wd, size_t rowb, int cpr
             if (c + u * S < cpr)
 #pragma unroll
                 for (int r = 0; r < R; ++r) q[u][r] = ld_stream(wd + r * rowb + size_t(c + u * S) * 16);
+        if constexpr (TOKENS && !CARRY) {
+            tokens(c, q, true);
+        } else {
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (c + u * S < cpr) load_x(c + u * S, xv[u]);
+            for (int u = 0; u < U; ++u)
+                if (c + u * S < cpr) load_x(c + u * S, xv[u]);
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (c + u * S < cpr) compute(c + u * S, q[u], xv[u]);
+            for (int u = 0; u < U; ++u)
+                if (c + u * S < cpr) compute(c + u * S, q[u], xv[u]);
+        }
     }
 }
 
@@ -888,7 +923,7 @@ __global__ __launch_bounds__(kThreads) void ffn_down_rows(FfnArgs a) {
 
     for (int j = wave; live && j < p.n_slots; j += kWaves) {
         if constexpr (BF && R < 4)
-            down_slot16<BF, R, NB, U, (R == 1 && NB <= kDownCarryMaxNB)>(
+            down_slot16<BF, R, NB, U, (R == 1 && NB <= kDownCarryMaxNB), true>(
                 slot_blob(a, p, j) + 2 * size_t(a.I) * a.H * esz + size_t(h0) * rowb, rowb, cpr, g, G,
                 reinterpret_cast<const char*>(a.act) + size_t(j) * a.B * rowb, p.tok[j], acc);
         else

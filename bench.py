@@ -35,7 +35,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
 #: the FFN launches of every TIMING_EVERY-th token of the timed region carry HIP events
-TIMING_EVERY = 8
+TIMING_EVERY = 25
 
 
 def timing_cadence(steps):
@@ -1932,7 +1932,7 @@ def main():
         "step_hbm_gbps": round((up_bytes + dn_bytes) / max(r["n_calls"] / cfg.L, 1e-9) * args.steps
                                / r["seconds"] / 1e9, 1),
         "layer_us": round(1e6 * r["seconds"] / args.steps / cfg.L, 2),
-        # event-timed stages per layer (every 8th token); the side-stream
+        # event-timed stages per layer (every TIMING_EVERY-th token); the side-stream
         # predictor overlaps the FFN and the next router
         "stages_us_per_layer": r["stages_us"],
         "routing_near_tie_rows": near_tie_rows(wl, warmup=args.warmup, steps=args.steps),

@@ -39,9 +39,10 @@ TIMING_EVERY = 25
 
 
 def timing_cadence(steps):
-    """Tokens between event-timed tokens: TIMING_EVERY, or 1 when the timed
-    region is too short to hold a multiple of it."""
-    return TIMING_EVERY if steps >= TIMING_EVERY else 1
+    """Tokens between event-timed tokens: TIMING_EVERY, or half the timed
+    region when that is shorter (at least two timed tokens), 1 for a region
+    of one to three tokens."""
+    return max(1, min(TIMING_EVERY, steps // 2))
 
 
 def log(msg):

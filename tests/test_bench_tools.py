@@ -106,3 +106,17 @@ def test_repeat_summary():
     r = bench.repeat_summary(200, [0.8, 0.5, 1.0])
     assert r["runs"] == 3 and r["tokens_per_s"] == [250.0, 400.0, 200.0]
     assert r["median"] == 250.0 and r["spread"] == round((400 - 200) / 250, 4)
+
+
+def test_timing_cadence():
+    """Event-timed tokens: every TIMING_EVERY-th of a long run, at least two
+    of a short one, every token of a run of one to three."""
+    import bench
+    assert bench.timing_cadence(200) == bench.TIMING_EVERY
+    assert bench.timing_cadence(100) == bench.TIMING_EVERY
+    assert bench.timing_cadence(10) == 5
+    assert bench.timing_cadence(3) == 1 and bench.timing_cadence(1) == 1
+    for steps in range(1, 300):
+        c = bench.timing_cadence(steps)
+        timed = len(range(0, steps, c))
+        assert 1 <= c <= bench.TIMING_EVERY and (timed >= 2 or steps == 1)

@@ -73,6 +73,8 @@ def parse():
                          "(expert (l, e) reads blob (l*E + e) mod their number)")
     ap.add_argument("--attention-sweep", default=None, metavar="CTX1,CTX2,...",
                     help="capped cache with a decode-attention stand-in of these context lengths (markdown)")
+    ap.add_argument("--handoff-probe", action="store_true",
+                    help="producer -> consumer handoff as two launches or inside one launch (markdown) and exit")
     ap.add_argument("--copy-sweep", default=None, metavar="W1,W2,...",
                     help="capped cache with device decisions at these copy-kernel workgroup counts: the expert "
                          "tier's bandwidth as a measured sweep (markdown table; with --pool hbm up to TB/s)")
@@ -1267,6 +1269,63 @@ def offload_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, budgets):
     return head + rows
 
 
+def handoff_probe(iters=60, n_chunks=40, reps=2):
+    """Markdown: the handoff a single gate/up + down launch would need, at the
+    shape of a Qwen3-30B layer at batch 1 (1536 producer workgroups streaming
+    32 KiB each, 1024 consumer workgroups streaming 24 KiB each into registers
+    and then reading all 1536 published words), as two launches and as one
+    launch with write-through stores or release/acquire.  Every iteration uses
+    another of n_chunks copies of the data (3 GB in all: no cache holds it);
+    each mode's last output is checked against the two-launch result."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    P, Q, C1, C2 = 1536, 1024, 32 << 10, 24 << 10
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(2606)
+    w1 = torch.randint(-2 ** 31, 2 ** 31 - 1, (n_chunks * P * C1 // 4,), dtype=torch.int32, device=dev, generator=g)
+    w2 = torch.randint(-2 ** 31, 2 ** 31 - 1, (n_chunks * Q * C2 // 4,), dtype=torch.int32, device=dev, generator=g)
+    act = torch.zeros(P, dtype=torch.int32, device=dev)
+    out = torch.zeros(Q, dtype=torch.int32, device=dev)
+    ref = torch.zeros(Q, dtype=torch.int32, device=dev)
+    sync = torch.zeros(2, dtype=torch.int32, device=dev)
+    n1, n2 = P * C1 // 4, Q * C2 // 4
+    target = 0
+    names = {0: "two launches", 1: "one launch, write-through stores + relaxed counter",
+             2: "one launch, release/acquire counter"}
+    times = {m: [] for m in names}
+    checks = {}
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        for mode in names:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for it in range(iters):
+                k = it % n_chunks
+                if mode:
+                    target += P
+                S.calib_handoff(w1[k * n1:(k + 1) * n1], C1, P, w2[k * n2:(k + 1) * n2], C2, Q, mode, act, out,
+                                sync, target)
+            e1.record()
+            torch.cuda.synchronize()
+            times[mode].append(1e3 * e0.elapsed_time(e1) / iters)
+            k = (iters - 1) % n_chunks
+            S.calib_handoff(w1[k * n1:(k + 1) * n1], C1, P, w2[k * n2:(k + 1) * n2], C2, Q, 0, act, ref, sync,
+                            target)
+            torch.cuda.synchronize()
+            checks[mode] = (bool(torch.equal(out, ref)), int(sync[1].item()))
+    mb = (P * C1 + Q * C2) / 1e6
+    lines = ["Producer -> consumer handoff (`stmoe_calib_handoff`), Qwen3-30B batch-1 FFN shape: "
+             f"{P} x {C1 >> 10} KiB producers, {Q} x {C2 >> 10} KiB consumers, {mb:.1f} MB per iteration, "
+             f"{iters} iterations per run over {n_chunks} copies of the data:", "",
+             "| mode | us per iteration (runs) | GB/s | output equal to two launches | wait error word |",
+             "|---|---|---|---|---|"]
+    for m, name in names.items():
+        best = min(times[m])
+        lines.append(f"| {name} | {' / '.join(f'{t:.2f}' for t in times[m])} | {mb * 1e3 / best:.0f} | "
+                     f"{'yes' if checks[m][0] else 'NO'} | {checks[m][1]} |")
+    return lines
+
+
 def copy_sweep(wl, n_tokens, resident_ms_per_token, pinned_gb, workgroups):
     """The expert tier's bandwidth as a measured sweep: with device decisions
     the copy kernels' workgroup count sets the copy rate (from the pinned host
@@ -1836,6 +1895,9 @@ def main():
         return
     if args.read_floor:
         read_floor()
+        return
+    if args.handoff_probe:
+        print("\n".join(handoff_probe()), flush=True)
         return
     if args.predictor_sweep:
         predictor_sweep()

@@ -539,6 +539,26 @@ int stmoe_calib_copy(const void* src, void* dst, size_t bytes, void* stream);
 int stmoe_calib_copy_grid(const void* src, void* dst, size_t bytes, int workgroups, void* stream);
 size_t stmoe_calib_read_out_words(size_t bytes, int pattern);
 int stmoe_calib_read(const void* src, size_t bytes, int pattern, unsigned* out, void* stream);
+/* Handoff between workgroups, the step a single gate/up + down launch would
+ * need (Section 2's FFN: the down projection reads every activation the
+ * gate/up projection writes).  `producers` workgroups each read their chunk1
+ * bytes of w1 (device, producers x chunk1, 16-byte aligned) and write one
+ * word, the wrapping sum of the 32-bit words read, to act[p] (device
+ * [producers]); `consumers` workgroups each read their chunk2 bytes of w2
+ * (device, consumers x chunk2; chunk2 of 4, 8, 16, 24 or 32 KiB) into
+ * registers and then write out[c] (device [consumers]) = the sum of those
+ * words plus every act word.  mode 0: two launches (the kernel boundary
+ * orders them).  mode 1 and 2: one launch of producers + consumers
+ * workgroups whose consumers wait until the counter sync[0] reaches
+ * `target` (the caller zeroes sync[0..1] once and adds `producers` to the
+ * target at every launch): 1 publishes with a write-through store and a
+ * relaxed increment, 2 with a release increment and acquire polls.  A
+ * consumer that polls 32768 times in vain sets sync[1] (its output is then
+ * not meaningful) instead of waiting on; producers take the lower workgroup
+ * indices.  All three modes give the same out.  Errors: STMOE_EINVAL. */
+int stmoe_calib_handoff(const void* w1, size_t chunk1, int producers, const void* w2, size_t chunk2,
+                        int consumers, int mode, unsigned* act, unsigned* out, unsigned* sync,
+                        unsigned target, void* stream);
 
 #ifdef __cplusplus
 }

@@ -135,6 +135,7 @@ _SIGS = {
     "stmoe_calib_copy_grid": (i32, [vp, vp, sz, i32, vp]),
     "expert_cache_set_copy_workgroups": (i32, [vp, i32, i32]),
     "stmoe_calib_read": (i32, [vp, sz, i32, vp, vp]),
+    "stmoe_calib_handoff": (i32, [vp, sz, i32, vp, sz, i32, i32, vp, vp, vp, C.c_uint, vp]),
 }
 
 for _name, (_res, _args) in _SIGS.items():
@@ -572,3 +573,10 @@ def calib_copy_grid(src_ptr, dst_ptr, nbytes, workgroups, stream=None):
 
 def calib_read_out_words(nbytes, pattern=0):
     return _lib.stmoe_calib_read_out_words(nbytes, int(pattern))
+
+
+def calib_handoff(w1, chunk1, producers, w2, chunk2, consumers, mode, act, out, sync, target, stream=None):
+    """stmoe_calib_handoff: producers publish one word each, consumers read them
+    all (mode 0 two launches, 1 and 2 one launch with an in-kernel wait)."""
+    _call("stmoe_calib_handoff", _p(w1), chunk1, int(producers), _p(w2), chunk2, int(consumers), int(mode),
+          _p(act), _p(out), _p(sync), int(target) & 0xFFFFFFFF, _s(stream))

@@ -43,3 +43,31 @@ def test_calib_copy_grid_copies_every_byte(workgroups, nbytes):
     torch.cuda.synchronize()
     assert torch.equal(dst[:nbytes], src)
     assert int(dst[nbytes:].sum()) == 0          # nothing written past the end
+
+
+@pytest.mark.parametrize("producers,consumers,chunk1,chunk2", [(64, 32, 4096, 8192), (7, 300, 16 << 10, 24 << 10),
+                                                               (260, 5, 48, 32 << 10)])
+def test_calib_handoff_modes_agree(producers, consumers, chunk1, chunk2):
+    """Every mode gives each consumer the wrapping sum of its own chunk's
+    words plus every producer's published word; the in-launch waits end
+    without the error word, and the counter advances by the producers of
+    every one-launch call."""
+    rng = np.random.default_rng(producers + consumers)
+    w1h = rng.integers(0, 2 ** 32, producers * chunk1 // 4, dtype=np.uint64).astype(np.uint32)
+    w2h = rng.integers(0, 2 ** 32, consumers * chunk2 // 4, dtype=np.uint64).astype(np.uint32)
+    w1 = torch.from_numpy(w1h.view(np.int32)).to(DEV)
+    w2 = torch.from_numpy(w2h.view(np.int32)).to(DEV)
+    act = torch.zeros(producers, dtype=torch.int32, device=DEV)
+    sync = torch.zeros(2, dtype=torch.int32, device=DEV)
+    total = int(w1h.astype(np.uint64).sum() % 2 ** 32)
+    want = (w2h.reshape(consumers, -1).astype(np.uint64).sum(axis=1) + total) % 2 ** 32
+    target = 0
+    for mode in (0, 1, 2, 1, 2):
+        out = torch.full((consumers,), -1, dtype=torch.int32, device=DEV)
+        if mode:
+            target += producers
+        S.calib_handoff(w1, chunk1, producers, w2, chunk2, consumers, mode, act, out, sync, target)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy().view(np.uint32), want.astype(np.uint32)), mode
+        assert int(sync[1].item()) == 0
+        assert int(sync[0].item()) == target

@@ -96,6 +96,9 @@ def parse():
                          "stdout) and exit")
     ap.add_argument("--read-floor", action="store_true",
                     help="time one streaming-read launch per size, bytes in no cache (markdown table) and exit")
+    ap.add_argument("--reread-probe", action="store_true",
+                    help="streaming reads of bytes in no cache against bytes the Infinity Cache may hold (phase "
+                         "order as markdown; durations from a kernel trace) and exit")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("KERNEL_TRACE_CSV", "TITLE", "COMMAND"),
                     help="median kernel durations per kernel and grid size of a rocprofv3 kernel trace")
     ap.add_argument("--summarize-mfma", nargs=2, metavar=("COUNTER_CSV", "COMMAND"),
@@ -690,6 +693,60 @@ def read_floor(sizes_mib=READ_FLOOR_MIB, reps=40, buf_bytes=4 << 30):
             print(f"| {mib} | {region >> 10} KiB | {S.calib_read_out_words(n, pattern)} | {us:.2f} | "
                   f"{n / us / 1e3:.0f} |", flush=True)
     del src
+
+
+def reread_probe(sizes_mib=(24, 48, 96), reps=20, buf_bytes=4 << 30, other_mib=72):
+    """One stmoe_calib_read launch (32 KiB per workgroup) on bytes in no
+    cache, against the same bytes once the Infinity Cache may hold them: read
+    again by the same kernel, first read by a plain-load kernel (torch's sum),
+    and first read that way with `other_mib` MiB of other data streamed in
+    between (what a prefetch one layer ahead would leave for the next
+    layer).  Phases are separated by idle time so that a kernel trace of this
+    run splits them (--summarize-trace); the order is printed."""
+    import torch
+    from paper_2606_15453_amd import stmoe as S
+    dev = "cuda:0"
+    src = torch.empty(buf_bytes, dtype=torch.uint8, device=dev)
+    src.zero_()
+    other = torch.empty(buf_bytes // 2, dtype=torch.uint8, device=dev)
+    other.zero_()
+    on = other_mib << 20
+    top = max(max(sizes_mib) << 20, on)
+    out = torch.empty(S.calib_read_out_words(top, 2), dtype=torch.int32, device=dev)
+    acc = torch.zeros((), dtype=torch.int64, device=dev)
+    run = 0
+
+    def pause(label):
+        nonlocal run
+        torch.cuda.synchronize()
+        time.sleep(0.01)
+        print(f"| {run} | {label} |", flush=True)
+        run += 1
+
+    print("| trace run | phase |")
+    print("|---|---|")
+    for mib in sizes_mib:
+        n = mib << 20
+        offs = [((k * n) % (buf_bytes - n)) & ~((256 << 10) - 1) for k in range(reps)]
+        assert all(o + n <= buf_bytes for o in offs)
+        for o in offs:
+            S.calib_read(src[o:], n, out, pattern=2)
+        pause(f"{mib} MiB, bytes in no cache")
+        for _ in range(reps):
+            S.calib_read(src[offs[-1]:], n, out, pattern=2)
+        pause(f"{mib} MiB, the same bytes read again")
+        for o in offs:
+            acc += src[o:o + n].view(torch.int32).sum()
+            S.calib_read(src[o:], n, out, pattern=2)
+        pause(f"{mib} MiB, first read by torch's sum")
+        for k, o in enumerate(offs):
+            acc += src[o:o + n].view(torch.int32).sum()
+            oo = ((k * (on + (8 << 20))) % (buf_bytes // 2 - on)) & ~((256 << 10) - 1)
+            assert oo + on <= buf_bytes // 2
+            S.calib_read(other[oo:], on, out, pattern=2)
+            S.calib_read(src[o:], n, out, pattern=2)
+        pause(f"{mib} MiB, first read by torch's sum, then {other_mib} MiB of other data streamed")
+    del src, other
 
 
 def trace_groups(path, pause_ns=1_000_000):
@@ -1895,6 +1952,9 @@ def main():
         return
     if args.read_floor:
         read_floor()
+        return
+    if args.reread_probe:
+        reread_probe()
         return
     if args.handoff_probe:
         print("\n".join(handoff_probe()), flush=True)

@@ -81,11 +81,6 @@ struct FfnArgs {
     float* y;                        // [B][H]
     unsigned long long* n_experts;   // optional: += distinct routed experts (block 0)
     int ng, spg;                     // expert-slot groups of the down phase, slots per group
-    // ng > 1 with the fold: per row block of the MFMA down phase, how many of
-    // its ng workgroups have stored their partial sums (the MFMA gate/up
-    // launch zeroes the n_rb words)
-    unsigned* cnt;
-    int n_rb;
     // optional routing prologue of the gate/up kernels: softmax + top-K of
     // these router logits [B][E] (B*E <= kRouteInFfnMax); block 0 writes the
     // selection to idx/w for the down kernel and the caller
@@ -1012,65 +1007,12 @@ __global__ __launch_bounds__(kThreads) void ffn_down_wg(FfnArgs a) {
 // MFMA path (batch >= 8, bf16, H and I multiples of 64)
 // ============================================================================
 
-// The down phase's slot groups, folded: every down workgroup stores its
-// partial sums with agent-scope (write-through) stores, waits until they are
-// complete and counts itself in its row block's word of a.cnt; the one that
-// counts last adds the ng partials of the block in group order (the additions
-// a separate reduce launch would make, so y is the same bit for bit) and
-// writes y.  No workgroup waits for another.  The gate/up launch before it
-// zeroes the counts.
-__device__ __forceinline__ void clear_group_counts(const FfnArgs& a) {
-    if (blockIdx.x == 0 && a.cnt)
-        for (int i = threadIdx.x; i < a.n_rb; i += kThreads) a.cnt[i] = 0u;
-}
-
-__device__ __forceinline__ void store_partial(const FfnArgs& a, float* out, float v) {
-    if (a.cnt) __hip_atomic_store(out, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else *out = v;
-}
-
-template <int NT>
-__device__ void fold_row_block(const FfnArgs& a, int rb) {
-    __shared__ int last;
-    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's partial stores are complete
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const unsigned before = __hip_atomic_fetch_add(a.cnt + rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        last = before == unsigned(a.ng - 1);
-    }
-    __syncthreads();
-    if (!last) return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // no stale partials in this XCD's caches
-    constexpr int R = kWaves * NT * 16;   // rows of a block
-    const int n = a.B * R / 4;            // four outputs per item
-    const size_t gstride = size_t(a.B) * a.H;
-    for (int i = threadIdx.x; i < n; i += kThreads) {
-        const int b = i / (R / 4), c = i % (R / 4);
-        const size_t o = size_t(b) * a.H + size_t(rb) * R + 4 * c;
-        float s[4] = {0.f, 0.f, 0.f, 0.f};
-        int g = 0;
-        for (; g + 16 <= a.ng; g += 16) {
-            float4 v[16];
-#pragma unroll
-            for (int u = 0; u < 16; ++u) v[u] = *reinterpret_cast<const float4*>(a.part + size_t(g + u) * gstride + o);
-#pragma unroll
-            for (int u = 0; u < 16; ++u) { s[0] += v[u].x; s[1] += v[u].y; s[2] += v[u].z; s[3] += v[u].w; }
-        }
-        for (; g < a.ng; ++g) {
-            const float4 v = *reinterpret_cast<const float4*>(a.part + size_t(g) * gstride + o);
-            s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
-        }
-        *reinterpret_cast<float4*>(a.y + o) = make_float4(s[0], s[1], s[2], s[3]);
-    }
-}
-
 // gate/up: each wave computes NT tiles of 16 rows x 16 tokens for W_gate and
 // W_up over the whole hidden dimension, then writes the bf16 activation
 // (zero for tokens not routed to the slot).
 template <int NT>
 __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma(FfnArgs a, int blocks_per_slot) {
     __shared__ Plan p;
-    clear_group_counts(a);
     build_plan(a, p, true);
     const int j = blockIdx.x / blocks_per_slot;
     if (j >= p.n_slots) return;
@@ -1176,7 +1118,6 @@ __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma_lds(FfnArgs a, int 
     __shared__ Plan p;
     __shared__ float red[SK ? kWaves : 1][2][64][4];
     extern __shared__ uint4 stage[];
-    clear_group_counts(a);
     build_plan(a, p, true);
     const int j = blockIdx.x / blocks_per_slot;
     if (j >= p.n_slots) return;
@@ -1366,9 +1307,8 @@ __global__ __launch_bounds__(kThreads) void ffn_down_mfma_lds(FfnArgs a) {
         const int b = 4 * q + r;
         if (!live || b >= a.B) continue;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) store_partial(a, out + size_t(b) * a.H + h0 + t * 16 + n, d[t][r]);
+        for (int t = 0; t < NT; ++t) out[size_t(b) * a.H + h0 + t * 16 + n] = d[t][r];
     }
-    if (a.ng > 1 && a.cnt) fold_row_block<NT>(a, rb);
 }
 
 // gate/up, split-K: one workgroup = 16 rows of one slot; wave w covers the
@@ -1377,7 +1317,6 @@ __global__ __launch_bounds__(kThreads) void ffn_down_mfma_lds(FfnArgs a) {
 __global__ __launch_bounds__(kThreads) void ffn_gate_up_mfma_sk(FfnArgs a, int blocks_per_slot) {
     __shared__ Plan p;
     __shared__ float red[kWaves][2][64][4];
-    clear_group_counts(a);
     build_plan(a, p, true);
     const int j = blockIdx.x / blocks_per_slot;
     if (j >= p.n_slots) return;
@@ -1511,9 +1450,8 @@ __global__ __launch_bounds__(kThreads) void ffn_down_mfma(FfnArgs a) {
         const int b = 4 * q + r;
         if (!live || b >= a.B) continue;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) store_partial(a, out + size_t(b) * a.H + h0 + t * 16 + n, d[t][r]);
+        for (int t = 0; t < NT; ++t) out[size_t(b) * a.H + h0 + t * 16 + n] = d[t][r];
     }
-    if (a.ng > 1 && a.cnt) fold_row_block<NT>(a, rb);
 }
 
 // y = sum over slot groups of the MFMA down phase's partial sums, in group
@@ -1573,7 +1511,6 @@ constexpr int kMfmaSplitKBelow = 2048;  // split-K MFMA gate/up when the tiled g
 constexpr bool kMfmaUpLds = true;       // MFMA gate/up stages weight rows through LDS (H % 128 == 0;
                                         // split-K: H % 512 == 0)
 constexpr bool kMfmaDownLds = true;     // MFMA down stages W_down rows through LDS (I % 128 == 0)
-constexpr bool kDownFoldGroups = true;  // MFMA down adds its slot groups' partials itself (no reduce launch)
 constexpr int kUpWgMinChunks = 512;   // ... used when a row has at least this many chunks
 
 Shape plan_shape(int B, int K, int H, int I, int E, int n_shared, int dtype) {
@@ -1619,7 +1556,7 @@ Shape plan_shape(int B, int K, int H, int I, int E, int n_shared, int dtype) {
 }
 
 struct WsLayout {
-    size_t act, part, cnt, total;
+    size_t act, part, total;
 };
 
 WsLayout ws_layout(int B, int H, int I, const Shape& s) {
@@ -1627,8 +1564,7 @@ WsLayout ws_layout(int B, int H, int I, const Shape& s) {
     WsLayout w{};
     w.act = 0;
     w.part = up(size_t(s.slots) * B * I * sizeof(float));
-    w.cnt = w.part + (s.ng > 1 ? up(size_t(s.ng) * B * H * sizeof(float)) : 0);
-    w.total = w.cnt + (s.ng > 1 && kDownFoldGroups ? up(size_t(s.n_rb) * sizeof(unsigned)) : 0);
+    w.total = w.part + (s.ng > 1 ? up(size_t(s.ng) * B * H * sizeof(float)) : 0);
     return w;
 }
 
@@ -1789,7 +1725,7 @@ int launch_mfma(const FfnArgs& a, const Shape& s, hipStream_t st, hipEvent_t ev_
         else hipLaunchKernelGGL((ffn_down_mfma<1>), dgrid, dim3(kThreads), 0, st, a);
     }
     STMOE_LAUNCHED();
-    if (s.ng > 1 && !a.cnt) {
+    if (s.ng > 1) {
         const int n4 = a.B * a.H / 4;   // H is a multiple of 64
         hipLaunchKernelGGL(ffn_reduce, dim3(unsigned((n4 + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
                            a.part, s.ng, n4, a.y);
@@ -1839,8 +1775,6 @@ int ffn_launch(const void* x, const int32_t* idx, const float* w, int B, int K, 
     a.n_experts = n_experts;
     a.ng = s.ng;
     a.spg = s.spg;
-    a.cnt = s.mfma && s.ng > 1 && kDownFoldGroups ? reinterpret_cast<unsigned*>(base + L.cnt) : nullptr;
-    a.n_rb = s.n_rb;
     a.logits = logits;
     a.renorm = renorm;
     if (s.mfma) return launch_mfma(a, s, st, ev_mid);

@@ -1331,7 +1331,9 @@ def handoff_probe(iters=60, n_chunks=40, reps=2):
     shape of a Qwen3-30B layer at batch 1 (1536 producer workgroups streaming
     32 KiB each, 1024 consumer workgroups streaming 24 KiB each into registers
     and then reading all 1536 published words), as two launches and as one
-    launch with write-through stores or release/acquire.  Every iteration uses
+    launch with write-through stores or release/acquire, every consumer polling
+    the count, or with the count's last producer (mode 4: counted in 64 group
+    words first) setting flag copies that the consumers poll.  Every iteration uses
     another of n_chunks copies of the data (3 GB in all: no cache holds it);
     each mode's last output is checked against the two-launch result."""
     import torch
@@ -1344,11 +1346,13 @@ def handoff_probe(iters=60, n_chunks=40, reps=2):
     act = torch.zeros(P, dtype=torch.int32, device=dev)
     out = torch.zeros(Q, dtype=torch.int32, device=dev)
     ref = torch.zeros(Q, dtype=torch.int32, device=dev)
-    sync = torch.zeros(2, dtype=torch.int32, device=dev)
+    sync = torch.zeros(S.HANDOFF_SYNC_WORDS, dtype=torch.int32, device=dev)
     n1, n2 = P * C1 // 4, Q * C2 // 4
     target = 0
     names = {0: "two launches", 1: "one launch, write-through stores + relaxed counter",
-             2: "one launch, release/acquire counter"}
+             2: "one launch, release/acquire counter",
+             3: "one launch, relaxed counter, the last producer sets 64 flag copies",
+             4: "one launch, 64 group counters, the last group sets 64 flag copies"}
     times = {m: [] for m in names}
     checks = {}
     torch.cuda.synchronize()

@@ -548,14 +548,22 @@ int stmoe_calib_read(const void* src, size_t bytes, int pattern, unsigned* out, 
  * (device, consumers x chunk2; chunk2 of 4, 8, 16, 24 or 32 KiB) into
  * registers and then write out[c] (device [consumers]) = the sum of those
  * words plus every act word.  mode 0: two launches (the kernel boundary
- * orders them).  mode 1 and 2: one launch of producers + consumers
- * workgroups whose consumers wait until the counter sync[0] reaches
- * `target` (the caller zeroes sync[0..1] once and adds `producers` to the
+ * orders them).  modes 1-4: one launch of producers + consumers workgroups
+ * whose consumers wait until the count of published producers, sync[0],
+ * reaches `target` (the caller zeroes sync once and adds `producers` to the
  * target at every launch): 1 publishes with a write-through store and a
- * relaxed increment, 2 with a release increment and acquire polls.  A
+ * relaxed increment and every consumer polls sync[0]; 2 the same with a
+ * release increment and acquire polls; 3 as 1, and the producer whose
+ * increment reaches the target writes it to 64 flag words (sync[64 + 1024 r],
+ * r < 64, on different memory channels), consumer c polling copy c mod 64;
+ * 4 as 3, but producer p counts itself in group word sync[576 + 1024 (p mod
+ * 64)], the last of each group in sync[2], and the last group (which sets
+ * those words back to 0 and adds `producers` to sync[0]) writes the flags.
+ * Modes 3 and 4 need at least STMOE_HANDOFF_SYNC_WORDS words of sync.  A
  * consumer that polls 32768 times in vain sets sync[1] (its output is then
  * not meaningful) instead of waiting on; producers take the lower workgroup
- * indices.  All three modes give the same out.  Errors: STMOE_EINVAL. */
+ * indices.  Every mode gives the same out.  Errors: STMOE_EINVAL. */
+#define STMOE_HANDOFF_SYNC_WORDS (64 + 64 * 1024)
 int stmoe_calib_handoff(const void* w1, size_t chunk1, int producers, const void* w2, size_t chunk2,
                         int consumers, int mode, unsigned* act, unsigned* out, unsigned* sync,
                         unsigned target, void* stream);

@@ -95,6 +95,12 @@ __global__ __launch_bounds__(kThreads) void calib_read_blocked_kernel(const char
 
 // ------------------------------------------------------------- handoff
 constexpr unsigned kHandoffSpin = 1u << 15;   // polls before a consumer gives up (each one memory round trip)
+// modes 3 and 4: the target is published to kFlagCopies words kFlagStride
+// words apart (on different memory channels), from word kFlagBase of sync
+// on; mode 4 counts producer p first in group counter p mod kFlagCopies
+// (kGroupOffset words after flag copy p mod kFlagCopies), then once per
+// complete group in sync[2]
+constexpr int kFlagBase = 64, kFlagCopies = 64, kFlagStride = 1024, kGroupOffset = 512;
 
 __device__ unsigned block_sum_u32(unsigned v) {
     __shared__ unsigned red[kThreads / 64];
@@ -172,10 +178,34 @@ __global__ __launch_bounds__(kThreads) void handoff_fused_kernel(const char* w1,
     if (int(blockIdx.x) < producers) {
         const unsigned s = produce_sum(reinterpret_cast<const u32x4*>(w1) + size_t(blockIdx.x) * n1, n1);
         if (threadIdx.x == 0) {
-            if (MODE == 1) {
+            if (MODE == 1 || MODE == 3) {
                 __hip_atomic_store(act + blockIdx.x, s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
-                __hip_atomic_fetch_add(sync, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const unsigned before = __hip_atomic_fetch_add(sync, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                // mode 3: the producer that completes the count tells every flag copy
+                if (MODE == 3 && before + 1u == target)
+                    for (int r = 0; r < kFlagCopies; ++r)
+                        __hip_atomic_store(sync + kFlagBase + r * kFlagStride, target, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+            } else if (MODE == 4) {
+                __hip_atomic_store(act + blockIdx.x, s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                const int g = int(blockIdx.x) % kFlagCopies;
+                const unsigned in_group = unsigned((producers - 1 - g) / kFlagCopies + 1);
+                const unsigned groups = unsigned(producers < kFlagCopies ? producers : kFlagCopies);
+                unsigned* gc = sync + kFlagBase + g * kFlagStride + kGroupOffset;
+                if (__hip_atomic_fetch_add(gc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u == in_group) {
+                    // every producer of the group has counted: ready for the next launch
+                    __hip_atomic_store(gc, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (__hip_atomic_fetch_add(sync + 2, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u ==
+                        groups) {
+                        __hip_atomic_store(sync + 2, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_fetch_add(sync, unsigned(producers), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        for (int r = 0; r < kFlagCopies; ++r)
+                            __hip_atomic_store(sync + kFlagBase + r * kFlagStride, target, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                }
             } else {
                 act[blockIdx.x] = s;
                 __hip_atomic_fetch_add(sync, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
@@ -187,17 +217,19 @@ __global__ __launch_bounds__(kThreads) void handoff_fused_kernel(const char* w1,
     u32x4 q[NX];
     consume_load<NX>(w2, c, q);
     if (threadIdx.x == 0) {
+        // mode 3 polls this consumer's flag copy; modes 1 and 2 the count itself
+        const unsigned* w = MODE >= 3 ? sync + kFlagBase + (c % kFlagCopies) * kFlagStride : sync;
         unsigned it = 0;
         for (; it < kHandoffSpin; ++it) {
-            const unsigned v = MODE == 1 ? __hip_atomic_load(sync, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                                         : __hip_atomic_load(sync, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+            const unsigned v = MODE == 2 ? __hip_atomic_load(w, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT)
+                                         : __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (int(v - target) >= 0) break;
             __builtin_amdgcn_s_sleep(1);
         }
         if (it == kHandoffSpin) atomicOr(sync + 1, 1u);
     }
     __syncthreads();
-    consume_finish<NX, MODE == 1>(act, producers, q, out, c);
+    consume_finish<NX, MODE != 2>(act, producers, q, out, c);
 }
 
 template <int NX>
@@ -210,8 +242,14 @@ void launch_handoff(const char* w1, size_t n1, int producers, const char* w2, in
     } else if (mode == 1) {
         hipLaunchKernelGGL((handoff_fused_kernel<NX, 1>), dim3(unsigned(producers + consumers)), dim3(kThreads), 0,
                            s, w1, n1, w2, producers, act, out, sync, target);
-    } else {
+    } else if (mode == 2) {
         hipLaunchKernelGGL((handoff_fused_kernel<NX, 2>), dim3(unsigned(producers + consumers)), dim3(kThreads), 0,
+                           s, w1, n1, w2, producers, act, out, sync, target);
+    } else if (mode == 3) {
+        hipLaunchKernelGGL((handoff_fused_kernel<NX, 3>), dim3(unsigned(producers + consumers)), dim3(kThreads), 0,
+                           s, w1, n1, w2, producers, act, out, sync, target);
+    } else {
+        hipLaunchKernelGGL((handoff_fused_kernel<NX, 4>), dim3(unsigned(producers + consumers)), dim3(kThreads), 0,
                            s, w1, n1, w2, producers, act, out, sync, target);
     }
 }
@@ -294,7 +332,8 @@ extern "C" int stmoe_calib_handoff(const void* w1, size_t chunk1, int producers,
     STMOE_CHECK(w1 && w2 && act && out && (mode == 0 || sync), "null pointer");
     STMOE_CHECK((reinterpret_cast<uintptr_t>(w1) & 15) == 0 && (reinterpret_cast<uintptr_t>(w2) & 15) == 0,
                 "w1 and w2 must be 16-byte aligned");
-    STMOE_CHECK(mode >= 0 && mode <= 2, "mode must be 0 (two launches), 1 (write-through) or 2 (release/acquire)");
+    STMOE_CHECK(mode >= 0 && mode <= 4, "mode must be 0 (two launches), 1 (write-through), 2 (release/acquire), "
+                                        "3 (flag copies) or 4 (group counters and flag copies)");
     STMOE_CHECK(producers >= 1 && consumers >= 1 && producers + consumers <= (1 << 20), "workgroup counts out of range");
     STMOE_CHECK(chunk1 >= 16 && chunk1 % 16 == 0, "chunk1 must be a positive multiple of 16");
     const size_t nx = chunk2 / (16 * kThreads);

@@ -575,8 +575,14 @@ def calib_read_out_words(nbytes, pattern=0):
     return _lib.stmoe_calib_read_out_words(nbytes, int(pattern))
 
 
+HANDOFF_SYNC_WORDS = 64 + 64 * 1024   # sync words modes 3 and 4 of stmoe_calib_handoff use
+
+
 def calib_handoff(w1, chunk1, producers, w2, chunk2, consumers, mode, act, out, sync, target, stream=None):
     """stmoe_calib_handoff: producers publish one word each, consumers read them
-    all (mode 0 two launches, 1 and 2 one launch with an in-kernel wait)."""
+    all (mode 0 two launches, 1-4 one launch with an in-kernel wait; modes 3
+    and 4 need HANDOFF_SYNC_WORDS words of sync)."""
+    if mode >= 3 and sync.numel() * sync.element_size() < 4 * HANDOFF_SYNC_WORDS:
+        raise ValueError("modes 3 and 4 need HANDOFF_SYNC_WORDS words of sync")
     _call("stmoe_calib_handoff", _p(w1), chunk1, int(producers), _p(w2), chunk2, int(consumers), int(mode),
           _p(act), _p(out), _p(sync), int(target) & 0xFFFFFFFF, _s(stream))

@@ -54,9 +54,9 @@ def test_invalid_arguments_rejected_without_device_work():
     assert S._lib.stmoe_calib_read(256 + 8, 1 << 20, 2, 256, None) == S.EINVAL      # misaligned
     assert S._lib.stmoe_calib_copy_grid(256, 512, 1 << 20, 0, None) == S.EINVAL     # workgroups in [1, 1024]
     assert S._lib.stmoe_calib_copy_grid(256, 512, 1 << 20, 1025, None) == S.EINVAL
-    # the handoff probe: modes 0..2, chunk2 of 4/8/16/24/32 KiB, aligned buffers
+    # the handoff probe: modes 0..4, chunk2 of 4/8/16/24/32 KiB, aligned buffers
     h = S._lib.stmoe_calib_handoff
-    assert h(256, 4096, 4, 512, 4096, 4, 3, 768, 1024, 1280, 4, None) == S.EINVAL      # mode
+    assert h(256, 4096, 4, 512, 4096, 4, 5, 768, 1024, 1280, 4, None) == S.EINVAL      # mode
     assert h(256, 4096, 4, 512, 12288, 4, 1, 768, 1024, 1280, 4, None) == S.EINVAL     # 12 KiB chunk2
     assert h(256, 4096, 4, 512, 4096, 4, 1, 768, 1024, None, 4, None) == S.EINVAL      # no sync words
     assert h(264, 4096, 4, 512, 4096, 4, 0, 768, 1024, 1280, 0, None) == S.EINVAL      # misaligned w1

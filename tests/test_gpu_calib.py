@@ -58,11 +58,11 @@ def test_calib_handoff_modes_agree(producers, consumers, chunk1, chunk2):
     w1 = torch.from_numpy(w1h.view(np.int32)).to(DEV)
     w2 = torch.from_numpy(w2h.view(np.int32)).to(DEV)
     act = torch.zeros(producers, dtype=torch.int32, device=DEV)
-    sync = torch.zeros(2, dtype=torch.int32, device=DEV)
+    sync = torch.zeros(S.HANDOFF_SYNC_WORDS, dtype=torch.int32, device=DEV)
     total = int(w1h.astype(np.uint64).sum() % 2 ** 32)
     want = (w2h.reshape(consumers, -1).astype(np.uint64).sum(axis=1) + total) % 2 ** 32
     target = 0
-    for mode in (0, 1, 2, 1, 2):
+    for mode in (0, 1, 2, 3, 4, 1, 2, 3, 4, 4):
         out = torch.full((consumers,), -1, dtype=torch.int32, device=DEV)
         if mode:
             target += producers

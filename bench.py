@@ -94,6 +94,10 @@ def parse():
     ap.add_argument("--ffn-sweep", action="store_true",
                     help="time moe_expert_ffn on every config shape, weights in no cache (markdown table on "
                          "stdout) and exit")
+    ap.add_argument("--largest-tokens", type=int, default=10,
+                    help="with the default workload, also decode the Qwen3-235B shapes (batch 16, HBM-resident "
+                         "stand-in) for this many tokens after 2 warm-up tokens and report them in the JSON "
+                         "line's 'largest_config' (0 skips)")
     ap.add_argument("--read-floor", action="store_true",
                     help="time one streaming-read launch per size, bytes in no cache (markdown table) and exit")
     ap.add_argument("--reread-probe", action="store_true",
@@ -998,6 +1002,48 @@ def hbm_resident(wl, steps, warmup):
               "predict_side_stream": round(pred_ms * per, 2)}
     return dict(seconds=dt, up_ms=up_ms, down_ms=down_ms, n_calls=n_calls, n_experts=n_exp, stats=stats,
                 host_issue_us_per_layer=host_us, stages_us=stages, repeat_seconds=repeats)
+
+
+def largest_config(steps, warmup, hbm_pool_gb):
+    """The largest workload, Qwen3-235B-A22B shapes at batch 16, decoded with
+    its experts in HBM.  Its stack does not fit, so a pool of distinct blobs
+    stands in (expert (l, e) reads blob (l*E + e) mod the pool's size): the
+    timing of the real stack, not its values.  tokens/s with two repeats, the
+    gate/up kernel's event-timed rate and the predictor's hit rates."""
+    import torch
+    from paper_2606_15453_amd import workload as W
+    cfg = W.CONFIGS["qwen235b"]
+    wl = Workload(cfg, hbm_blobs=int(hbm_pool_gb * 1e9) // cfg.blob_bytes, x_tokens=warmup + steps)
+    r = hbm_resident(wl, steps, warmup)
+    esz = cfg.wbytes
+    up_bytes = r["n_experts"] * 2 * cfg.H * cfg.I * esz + r["n_calls"] * cfg.n_shared * 2 * cfg.H * cfg.I * esz
+    dn_bytes = r["n_experts"] * cfg.H * cfg.I * esz + r["n_calls"] * cfg.n_shared * cfg.H * cfg.I * esz
+    up_gbps = up_bytes / (r["up_ms"] * 1e-3) / 1e9
+    dn_gbps = dn_bytes / (r["down_ms"] * 1e-3) / 1e9
+    stats = r["stats"]
+    out = {
+        "workload": cfg.name,
+        "mode": (f"HBM-resident stand-in: {wl.n_blobs} distinct expert blobs in HBM, expert (l, e) reads blob "
+                 f"(l*E + e) mod {wl.n_blobs}; ST-MoE predictor on"),
+        "steps": steps, "warmup": warmup,
+        "tokens_per_s": round(cfg.B * steps / r["seconds"], 3),
+        "ms_per_step": round(1e3 * r["seconds"] / steps, 3),
+        "repeats": repeat_summary(cfg.B * steps, [r["seconds"]] + r["repeat_seconds"]),
+        "ffn_gate_up": {"achieved_gbps": round(up_gbps, 1), "frac": round(up_gbps / PEAK_HBM_GBPS, 4),
+                        "avg_launch_us": round(1e3 * r["up_ms"] / max(r["n_calls"], 1), 3),
+                        "launches": r["n_calls"]},
+        "ffn_down": {"achieved_gbps": round(dn_gbps, 1), "frac": round(dn_gbps / PEAK_HBM_GBPS, 4),
+                     "avg_launch_us": round(1e3 * r["down_ms"] / max(r["n_calls"], 1), 3)},
+        "layer_us": round(1e6 * r["seconds"] / steps / cfg.L, 2),
+        "prediction": {
+            "recall_layers_ge1": round(float(stats[1:, 0].sum() / max(stats[1:, 1].sum(), 1)), 4),
+            "recall_layer0": round(float(stats[0, 0] / max(stats[0, 1], 1)), 4),
+            "precision": round(float(stats[:, 0].sum() / max(stats[:, 2].sum(), 1)), 4),
+        },
+    }
+    del wl
+    torch.cuda.empty_cache()
+    return out
 
 
 #: host-to-HBM copy rate (GB/s): the latest on-demand run's copied bytes over its time
@@ -2084,6 +2130,13 @@ def main():
         t0 = time.time()
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens, args.cpu_seconds)
         log(f"cpu baseline {out['cpu_baseline']['value']} tok/s in {time.time() - t0:.1f}s wall")
+    if args.largest_tokens > 0 and args.config == "mixtral":
+        del wl
+        torch.cuda.empty_cache()
+        t0 = time.time()
+        out["largest_config"] = largest_config(args.largest_tokens, 2, args.hbm_pool_gb)
+        log(f"largest config {out['largest_config']['workload']}: {out['largest_config']['tokens_per_s']} tok/s "
+            f"({time.time() - t0:.1f}s wall)")
     print(json.dumps(out), flush=True)
 
 

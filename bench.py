@@ -98,6 +98,8 @@ def parse():
                     help="with the default workload, also decode the Qwen3-235B shapes (batch 16, HBM-resident "
                          "stand-in) for this many tokens after 2 warm-up tokens and report them in the JSON "
                          "line's 'largest_config' (0 skips)")
+    ap.add_argument("--largest-capped-tokens", type=int, default=3,
+                    help="tokens of the largest workload's capped-cache runs in 'largest_config' (0 skips)")
     ap.add_argument("--read-floor", action="store_true",
                     help="time one streaming-read launch per size, bytes in no cache (markdown table) and exit")
     ap.add_argument("--reread-probe", action="store_true",
@@ -1004,12 +1006,16 @@ def hbm_resident(wl, steps, warmup):
                 host_issue_us_per_layer=host_us, stages_us=stages, repeat_seconds=repeats)
 
 
-def largest_config(steps, warmup, hbm_pool_gb):
+def largest_config(steps, warmup, hbm_pool_gb, capped_tokens, pinned_gb):
     """The largest workload, Qwen3-235B-A22B shapes at batch 16, decoded with
     its experts in HBM.  Its stack does not fit, so a pool of distinct blobs
     stands in (expert (l, e) reads blob (l*E + e) mod the pool's size): the
     timing of the real stack, not its values.  tokens/s with two repeats, the
-    gate/up kernel's event-timed rate and the predictor's hit rates."""
+    gate/up kernel's event-timed rate and the predictor's hit rates; with
+    capped_tokens > 0 also the config's capped cache (45 of 128 experts per
+    layer in HBM, the rest in pinned host memory) for that many tokens:
+    on-demand loading and ST-MoE prefetch (into slots and staged), decisions
+    on the device."""
     import torch
     from paper_2606_15453_amd import workload as W
     cfg = W.CONFIGS["qwen235b"]
@@ -1041,6 +1047,9 @@ def largest_config(steps, warmup, hbm_pool_gb):
             "precision": round(float(stats[:, 0].sum() / max(stats[:, 2].sum(), 1)), 4),
         },
     }
+    if capped_tokens > 0:
+        out["capped"] = offload(wl, capped_tokens, out["ms_per_step"], pinned_gb,
+                                "on_demand_device,st_moe_device,st_moe_staged_device")
     del wl
     torch.cuda.empty_cache()
     return out
@@ -2134,7 +2143,8 @@ def main():
         del wl
         torch.cuda.empty_cache()
         t0 = time.time()
-        out["largest_config"] = largest_config(args.largest_tokens, 2, args.hbm_pool_gb)
+        out["largest_config"] = largest_config(args.largest_tokens, 2, args.hbm_pool_gb, args.largest_capped_tokens,
+                                               args.pinned_gb)
         log(f"largest config {out['largest_config']['workload']}: {out['largest_config']['tokens_per_s']} tok/s "
             f"({time.time() - t0:.1f}s wall)")
     print(json.dumps(out), flush=True)

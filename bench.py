@@ -475,6 +475,8 @@ def counters_workload(config="mixtral", meta_path=None):
     from paper_2606_15453_amd import stmoe as S
     from paper_2606_15453_amd import workload as W
     cfg = W.CONFIGS[config]
+    if cfg.L * cfg.E * cfg.blob_bytes > 0.8 * torch.cuda.get_device_properties(0).total_memory:
+        raise SystemExit(f"--counters: the {cfg.name} stack does not fit in HBM; only resident stacks are profiled")
     wl = Workload(cfg)
     pred = S.Predictor(cfg.L, cfg.E, cfg.K, cfg.B)
     pred.profile(wl.prof)
